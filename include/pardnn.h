@@ -1,0 +1,253 @@
+/*
+ * pardnn.h -- C ABI of the MI355X (gfx950) placement-aware critical-path
+ * evaluator: the data-parallel hot path of ParDNN's partitioner
+ * (arXiv 2008.08636).
+ *
+ * The problem (paper Sec. 2 and 3): a computational DAG G = (V, E) whose node
+ * n costs comp(n) time and holds mem(n) bytes (Table 2), whose edge e costs
+ * comm(e) to transfer its tensor (Table 2) -- zero when both ends sit on the
+ * same device label (Fig. 2 caption; Sec. 3.1.2, cluster criticality) -- and a
+ * placement of every node on a label. The evaluator computes the quantities
+ * the partitioner recomputes again and again (Alg. 1 compute_weighted_levels
+ * and find_heaviest_path; Alg. 2; Memory Heuristic II of Sec. 3.2):
+ *   - topological levels,
+ *   - t-level tl(n) (costliest source-to-n path, excluding n) and b-level
+ *     bl(n) (costliest n-to-sink path, including n), Table 2,
+ *   - makespan M = max over n of tl(n) + bl(n), the critical nodes
+ *     (tl + bl == M) and one canonical critical path (Table 2, CP),
+ *   - memory per label and its overflow against a capacity (Sec. 3.2, Sec. 4).
+ *
+ * Conventions shared by every entry point
+ *   - Array arguments are DEVICE pointers on the handle's device (e.g. the
+ *     data_ptr() of a torch tensor), owned by the caller. Outputs are
+ *     allocated by the caller. Work is enqueued on the handle's stream; the
+ *     caller synchronises that stream before reading outputs on the host.
+ *     Only arguments documented as "host" are host pointers.
+ *   - Node ids are 0..n_nodes-1 in the caller's numbering; every per-node
+ *     output is in that numbering.
+ *   - Weights (comp, edge_cost, mem) are int64 and must be >= 0. All
+ *     arithmetic is exact int64: results are bit-exact.
+ *   - The artificial source and sink of Sec. 3 are implicit: a node without
+ *     predecessors has tl = 0, a node without successors has bl = comp.
+ *   - Multi-edges are allowed; each edge is relaxed on its own.
+ *   - Every call returns PARDNN_OK or a negative status, never aborts and never
+ *     throws. pardnn_last_error() gives a detail string for the calling thread.
+ *   - A handle is used by one host thread at a time. Calls that report an
+ *     error found on the device (marked "syncs") wait for the stream.
+ *
+ * Batched layout: arrays of several placements are PLACEMENT-MINOR, i.e.
+ * element (node v, placement p) of a [V][n_place] array sits at
+ * v * n_place + p.
+ */
+#ifndef PARDNN_H
+#define PARDNN_H
+
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+typedef struct pardnn_graph pardnn_graph;
+
+enum pardnn_status {
+    PARDNN_OK = 0,
+    PARDNN_E_INVAL = -1,    /* bad argument: NULL pointer, id or label out of range, negative weight */
+    PARDNN_E_CYCLE = -2,    /* the graph has a cycle or a self-loop */
+    PARDNN_E_OVERFLOW = -3, /* sum(comp) + sum(edge_cost) or sum(mem) exceeds INT64_MAX */
+    PARDNN_E_NOMEM = -4,    /* a device allocation failed */
+    PARDNN_E_DEVICE = -5    /* no usable GPU, or a HIP runtime call failed */
+};
+
+typedef struct pardnn_info {
+    int32_t n_nodes;
+    int64_t n_edges;
+    int32_t n_levels;      /* valid once levelized, else -1 */
+    int32_t max_width;     /* widest level, valid once levelized, else -1 */
+    int32_t device;        /* HIP device ordinal the handle lives on */
+} pardnn_info;
+
+/*
+ * Create a handle for G = (V, E) (Sec. 2; Table 2 comp, comm, mem).
+ *   n_nodes        V >= 0.
+ *   n_edges        |E|, 0 <= n_edges < 2^31.
+ *   src, dst       int32[n_edges], edge e runs src[e] -> dst[e].
+ *   comp           int64[n_nodes], node cost (comp(n)), >= 0.
+ *   edge_cost      int64[n_edges], transfer cost of edge e when its ends carry
+ *                  different labels (comm(e)), >= 0.
+ *   mem            int64[n_nodes], output memory of node n (mem(n)), >= 0.
+ *   stream         hipStream_t for all later work on the handle (NULL: the
+ *                  default stream of the current device).
+ *   out            host pointer receiving the new handle.
+ * The handle copies what it needs; the caller may free the inputs afterwards.
+ * Errors: E_INVAL (NULL pointer, id out of range, negative weight),
+ * E_OVERFLOW, E_NOMEM, E_DEVICE. Syncs once (validation result).
+ */
+int pardnn_graph_create(int32_t n_nodes, int64_t n_edges, const int32_t *src,
+                        const int32_t *dst, const int64_t *comp,
+                        const int64_t *edge_cost, const int64_t *mem,
+                        void *stream, pardnn_graph **out);
+
+/* Release a handle and its device memory (waits for its stream). NULL is a no-op. */
+int pardnn_graph_destroy(pardnn_graph *g);
+
+/* Rebind the handle to another stream of the same device. */
+int pardnn_set_stream(pardnn_graph *g, void *stream);
+
+/* Host query of sizes; levels are reported once pardnn_levelize has run. */
+int pardnn_get_info(const pardnn_graph *g, pardnn_info *info);
+
+/*
+ * Topological levels by Kahn's algorithm (Sec. 3.1.1: computing weighted
+ * levels is a variant of topological sorting, O(|V| + |E|); the per-level work
+ * tables of Sec. 3.1.2 are indexed by level). level(v) = 0 without
+ * predecessors, else 1 + the largest level of its predecessors.
+ *   level          int32[n_nodes] or NULL: level of each node.
+ *   order          int32[n_nodes] or NULL: node ids sorted by (level, id).
+ *   level_ptr      int32[n_nodes + 1] or NULL: order[level_ptr[l] ..
+ *                  level_ptr[l+1]) is level l; entries past n_levels are
+ *                  left untouched.
+ *   n_levels_host  host int32* or NULL: number of levels.
+ * The result depends on the structure only and is cached: later calls only
+ * copy it out. Errors: E_CYCLE. Syncs (once per handle).
+ */
+int pardnn_levelize(pardnn_graph *g, int32_t *level, int32_t *order,
+                    int32_t *level_ptr, int32_t *n_levels_host);
+
+/*
+ * t-levels, b-levels and makespan under one placement (Table 2: tl, bl,
+ * w_lvl; Alg. 1 compute_weighted_levels).
+ *   tl(v) = max over edges (u,v) of tl(u) + comp(u) + c(u,v), 0 if none;
+ *   bl(v) = comp(v) + max over edges (v,s) of c(v,s) + bl(s), or comp(v);
+ *   c(u,v) = 0 if placement[u] == placement[v] else edge_cost(u,v);
+ *   M = max over v of tl(v) + bl(v) (0 for an empty graph).
+ *   placement      int32[n_nodes], any int32 values: only equality matters,
+ *                  so cluster ids work as labels (Sec. 3.1.2 criticality).
+ *   tl, bl         int64[n_nodes] outputs.
+ *   makespan       int64[1] output.
+ * Levelizes first if needed (E_CYCLE). No sync.
+ */
+int pardnn_tb_levels(pardnn_graph *g, const int32_t *placement, int64_t *tl,
+                     int64_t *bl, int64_t *makespan);
+
+/*
+ * Critical nodes and the canonical critical path (Table 2 CP; Alg. 1
+ * find_heaviest_path on freshly computed weighted levels).
+ *   is_critical[v] = (tl[v] + bl[v] == *makespan).
+ *   path           int32[n_nodes] output: starts at the smallest-id node
+ *                  without predecessors that is critical, then repeatedly
+ *                  steps to the smallest-id successor s of the current node u
+ *                  with tl[u] + comp[u] + c(u,s) + bl[s] == *makespan, and
+ *                  stops at a node without such a successor. For tl/bl/M from
+ *                  pardnn_tb_levels this is the lexicographically smallest
+ *                  node sequence among the maximum-length paths.
+ *   path_len       int32[1] output, <= number of levels.
+ *   placement, tl, bl, makespan  inputs as produced by pardnn_tb_levels.
+ * No sync.
+ */
+int pardnn_critical_path(pardnn_graph *g, const int32_t *placement,
+                         const int64_t *tl, const int64_t *bl,
+                         const int64_t *makespan, uint8_t *is_critical,
+                         int32_t *path, int32_t *path_len);
+
+/*
+ * Memory per label (Sec. 3.2, Memory Heuristic II per-partition totals,
+ * without the residual/normal split; Sec. 4 capacity):
+ *   label_mem[k] = sum of mem[v] over v with placement[v] == k;
+ *   overflow[k]  = max(0, label_mem[k] - capacity[k]).
+ *   placement      int32[n_nodes], every value in [0, n_labels).
+ *   n_labels       K >= 1.
+ *   capacity       int64[K] >= 0, or NULL (no limit: overflow = 0). The caller
+ *                  applies the paper's 10 % reserve (Sec. 4) itself.
+ *   label_mem      int64[K] output.
+ *   overflow       int64[K] output or NULL.
+ * Errors: E_INVAL if a label is outside [0, K) or a capacity is negative.
+ * Syncs.
+ */
+int pardnn_label_memory(pardnn_graph *g, const int32_t *placement,
+                        int32_t n_labels, const int64_t *capacity,
+                        int64_t *label_mem, int64_t *overflow);
+
+/*
+ * Apply moves to a placement in place: placement[node[i]] = label[i] for
+ * i = 0..n_moves-1 in order (a later move of the same node wins). This is the
+ * node movement of Sec. 3.2 (overflow handling, Heuristic II) as the
+ * refinement loop issues it.
+ *   placement      int32[n_nodes], updated in place.
+ *   node, label    int32[n_moves].
+ * Errors: E_INVAL if a node id is out of range (no move is applied then).
+ * Syncs.
+ */
+int pardnn_apply_moves(pardnn_graph *g, int32_t *placement, int32_t n_moves,
+                       const int32_t *node, const int32_t *label);
+
+/*
+ * Materialise n_place successive placements of a refinement loop: placement
+ * p is `base` with the moves of steps 0..p applied in order, where step p's
+ * moves are node[step_ptr[p] .. step_ptr[p+1]) -> label[same range] (a later
+ * move of a node wins, within and across steps).
+ *   base           int32[n_nodes].
+ *   step_ptr       int64[n_place + 1], non-decreasing, step_ptr[0] = 0.
+ *   node, label    int32[step_ptr[n_place]].
+ *   placements     int32[n_nodes][n_place] output (placement-minor).
+ * Errors: E_INVAL if a node id is out of range. Syncs.
+ */
+int pardnn_build_placements(pardnn_graph *g, const int32_t *base,
+                            int32_t n_place, const int64_t *step_ptr,
+                            const int32_t *node, const int32_t *label,
+                            int32_t *placements);
+
+/*
+ * Evaluate n_place placements at once: for every placement p the results of
+ * pardnn_tb_levels, pardnn_critical_path and pardnn_label_memory. All arrays
+ * are placement-minor.
+ *   placements     int32[n_nodes][n_place].
+ *   n_labels, capacity  as for pardnn_label_memory (n_labels is ignored when
+ *                  label_mem is NULL).
+ *   tl, bl         int64[n_nodes][n_place] outputs.
+ *   makespan       int64[n_place] output.
+ *   is_critical    uint8[n_nodes][n_place] output or NULL.
+ *   path           int32[n_place][path_stride] output or NULL: row p holds
+ *                  placement p's canonical critical path.
+ *   path_stride    >= number of levels when path != NULL.
+ *   path_len       int32[n_place] output (NULL iff path is NULL).
+ *   label_mem      int64[n_place][n_labels] output or NULL.
+ *   overflow       int64[n_place][n_labels] output or NULL.
+ * Errors: E_INVAL (bad label when label_mem != NULL, short path_stride).
+ * Syncs when label_mem != NULL.
+ */
+int pardnn_evaluate_batch(pardnn_graph *g, int32_t n_place,
+                          const int32_t *placements, int32_t n_labels,
+                          const int64_t *capacity, int64_t *tl, int64_t *bl,
+                          int64_t *makespan, uint8_t *is_critical,
+                          int32_t *path, int32_t path_stride,
+                          int32_t *path_len, int64_t *label_mem,
+                          int64_t *overflow);
+
+/* pardnn_evaluate_batch restricted to tl, bl and makespan. No sync. */
+int pardnn_tb_levels_batch(pardnn_graph *g, int32_t n_place,
+                           const int32_t *placements, int64_t *tl, int64_t *bl,
+                           int64_t *makespan);
+
+/*
+ * Instrumentation (not part of the method): when enabled, the handle records
+ * a pair of HIP events on its stream around the main kernel of each
+ * pardnn_tb_levels, pardnn_evaluate_batch / pardnn_tb_levels_batch and
+ * pardnn_levelize call. pardnn_get_timing waits for the last recorded pair and
+ * returns its elapsed time in milliseconds and the kernel's name (a static
+ * string). Errors: E_INVAL if nothing was recorded yet.
+ */
+int pardnn_set_timing(pardnn_graph *g, int enable);
+int pardnn_get_timing(pardnn_graph *g, const char **kernel, float *ms);
+
+/* Static text for a status code. */
+const char *pardnn_status_string(int status);
+
+/* Detail of the last failing call on this host thread ("" if none). */
+const char *pardnn_last_error(void);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* PARDNN_H */

@@ -1,0 +1,585 @@
+// api.hip -- the C ABI declared in include/pardnn.h: argument checks, handle
+// and memory management, launch sequencing. Every step of the evaluation runs
+// in the kernels of structure.hip, levelize.hip, sweep.hip, critpath.hip and
+// labelmem.hip; this file only checks, allocates and enqueues.
+#include <cstring>
+#include <new>
+#include <string>
+
+#include "internal.h"
+
+using namespace pardnn;
+
+namespace {
+
+thread_local std::string g_last_error;
+
+int hip_status(hipError_t e) {
+    return e == hipErrorOutOfMemory || e == hipErrorMemoryAllocation ? PARDNN_E_NOMEM
+                                                                     : PARDNN_E_DEVICE;
+}
+
+#define HIP_TRY(expr)                                                                      \
+    do {                                                                                   \
+        hipError_t e_ = (expr);                                                            \
+        if (e_ != hipSuccess)                                                              \
+            return fail(hip_status(e_), std::string(#expr) + ": " + hipGetErrorString(e_)); \
+    } while (0)
+
+// Makes the handle's device current for the duration of a call and restores
+// the caller's device afterwards.
+struct DeviceScope {
+    int prev = -1;
+    bool ok = true;
+    explicit DeviceScope(int dev) {
+        if (hipGetDevice(&prev) != hipSuccess) {
+            ok = false;
+            return;
+        }
+        if (prev != dev && hipSetDevice(dev) != hipSuccess) ok = false;
+    }
+    ~DeviceScope() {
+        int cur = -1;
+        if (prev >= 0 && hipGetDevice(&cur) == hipSuccess && cur != prev) (void)hipSetDevice(prev);
+    }
+};
+
+template <class T>
+hipError_t dalloc(Graph &g, T **p, size_t n) {
+    if (n == 0) n = 1;
+    hipError_t e = hipMalloc((void **)p, n * sizeof(T));
+    if (e == hipSuccess) g.allocs.push_back((void *)*p);
+    return e;
+}
+
+void release(Graph *g) {
+    (void)hipStreamSynchronize(g->stream);
+    for (void *p : g->allocs) (void)hipFree(p);
+    g->allocs.clear();
+    if (g->batch_ws) (void)hipFree(g->batch_ws);
+    if (g->h_err) (void)hipHostFree(g->h_err);
+    if (g->ev0) (void)hipEventDestroy(g->ev0);
+    if (g->ev1) (void)hipEventDestroy(g->ev1);
+    delete g;
+}
+
+// Copy the device error words to the host after the enqueued work finished.
+int read_errors(Graph *g) {
+    HIP_TRY(hipMemcpyAsync(g->h_err, g->err, 4 * sizeof(int32_t), hipMemcpyDeviceToHost,
+                           g->stream));
+    HIP_TRY(hipStreamSynchronize(g->stream));
+    return PARDNN_OK;
+}
+
+// Event pair around the main kernel of a call (instrumentation only).
+struct TimedLaunch {
+    Graph *g;
+    TimedLaunch(Graph *g_, const char *name) : g(g_) {
+        if (g->timing) {
+            g->timed_kernel = name;
+            (void)hipEventRecord(g->ev0, g->stream);
+        }
+    }
+    ~TimedLaunch() {
+        if (g->timing) {
+            (void)hipEventRecord(g->ev1, g->stream);
+            g->timed = true;
+        }
+    }
+};
+
+int ensure_levelized(Graph *g) {
+    if (g->levelized) return PARDNN_OK;
+    const int32_t V = g->V;
+    if (!g->level) {
+        HIP_TRY(dalloc(*g, &g->level, V));
+        HIP_TRY(dalloc(*g, &g->order, V));
+        HIP_TRY(dalloc(*g, &g->rank, V));
+        HIP_TRY(dalloc(*g, &g->level_ptr, (size_t)V + 2));
+    }
+    int32_t *indeg_work = nullptr, *sort_scratch = nullptr, *result = nullptr;
+    int32_t pow2 = 1;
+    while (pow2 < V) pow2 <<= 1;
+    auto cleanup = [&]() {
+        (void)hipStreamSynchronize(g->stream);
+        if (indeg_work) (void)hipFree(indeg_work);
+        if (sort_scratch) (void)hipFree(sort_scratch);
+        if (result) (void)hipFree(result);
+    };
+    hipError_t e = hipMalloc((void **)&indeg_work, sizeof(int32_t) * ((size_t)V + 1));
+    if (e == hipSuccess) e = hipMalloc((void **)&sort_scratch, sizeof(int32_t) * (size_t)pow2);
+    if (e == hipSuccess) e = hipMalloc((void **)&result, sizeof(int32_t) * 2);
+    if (e == hipSuccess && V > 0)
+        e = hipMemcpyAsync(indeg_work, g->indeg, sizeof(int32_t) * (size_t)V,
+                           hipMemcpyDeviceToDevice, g->stream);
+    if (e == hipSuccess) {
+        TimedLaunch t(g, "k_kahn");
+        e = launch_kahn(*g, indeg_work, sort_scratch, result);
+    }
+    int32_t h_result[2] = {0, 0};
+    if (e == hipSuccess)
+        e = hipMemcpyAsync(h_result, result, sizeof(h_result), hipMemcpyDeviceToHost, g->stream);
+    if (e == hipSuccess) e = hipStreamSynchronize(g->stream);
+    cleanup();
+    if (e != hipSuccess) return fail(hip_status(e), std::string("levelize: ") + hipGetErrorString(e));
+    if (h_result[1] != V)
+        return fail(PARDNN_E_CYCLE, "levelize: " + std::to_string(V - h_result[1]) +
+                                        " node(s) lie on or behind a cycle");
+    const int32_t L = h_result[0];
+    g->L = L;
+    g->h_level_ptr.assign((size_t)L + 1, 0);
+    HIP_TRY(hipMemcpyAsync(g->h_level_ptr.data(), g->level_ptr, sizeof(int32_t) * ((size_t)L + 1),
+                           hipMemcpyDeviceToHost, g->stream));
+    HIP_TRY(hipStreamSynchronize(g->stream));
+    int32_t mw = 0;
+    for (int32_t k = 0; k < L; k++) mw = std::max(mw, g->h_level_ptr[k + 1] - g->h_level_ptr[k]);
+    g->max_width = mw;
+
+    const size_t E = (size_t)g->E;
+    HIP_TRY(dalloc(*g, &g->linfo, (size_t)L + 1));
+    HIP_TRY(dalloc(*g, &g->in_off, (size_t)V + 1));
+    HIP_TRY(dalloc(*g, &g->in_src, E));
+    HIP_TRY(dalloc(*g, &g->in_dst, E));
+    HIP_TRY(dalloc(*g, &g->in_cost, E));
+    HIP_TRY(dalloc(*g, &g->out_off, (size_t)V + 1));
+    HIP_TRY(dalloc(*g, &g->out_src, E));
+    HIP_TRY(dalloc(*g, &g->out_dst, E));
+    HIP_TRY(dalloc(*g, &g->out_dst_orig, E));
+    HIP_TRY(dalloc(*g, &g->out_cost, E));
+    HIP_TRY(dalloc(*g, &g->comp_lm, V));
+    HIP_TRY(dalloc(*g, &g->mem_lm, V));
+    HIP_TRY(dalloc(*g, &g->lab_lm, V));
+    HIP_TRY(dalloc(*g, &g->next_lm, V));
+    HIP_TRY(dalloc(*g, &g->crit_lm, V));
+    HIP_TRY(dalloc(*g, &g->ft_lm, V));
+    HIP_TRY(dalloc(*g, &g->bl_lm, V));
+    if (!g->move_stamp) {
+        HIP_TRY(dalloc(*g, &g->move_stamp, V));
+        HIP_TRY(launch_fill_i32(g->move_stamp, V, -1, g->stream));
+    }
+
+    int32_t *tmp = nullptr;
+    const size_t scan_n = scan_workspace_elems(V);
+    e = hipMalloc((void **)&tmp, sizeof(int32_t) * (4 * (size_t)V + scan_n + 4));
+    if (e == hipSuccess)
+        e = launch_build_lm(*g, tmp, tmp + 2 * (size_t)V, tmp + 3 * (size_t)V,
+                            tmp + 4 * (size_t)V);
+    if (e == hipSuccess) e = hipStreamSynchronize(g->stream);
+    if (tmp) {
+        (void)hipStreamSynchronize(g->stream);
+        (void)hipFree(tmp);
+    }
+    if (e != hipSuccess) return fail(hip_status(e), std::string("levelize: ") + hipGetErrorString(e));
+    g->levelized = true;
+    return PARDNN_OK;
+}
+
+#define CHECK_HANDLE(g)                                            \
+    do {                                                           \
+        if ((g) == nullptr) return fail(PARDNN_E_INVAL, "null handle"); \
+    } while (0)
+
+#define DEVICE_SCOPE(g)                                                         \
+    DeviceScope scope_((g)->device);                                            \
+    if (!scope_.ok) return fail(PARDNN_E_DEVICE, "cannot select the handle's device")
+
+}  // namespace
+
+int pardnn::fail(int status, const std::string &msg) {
+    g_last_error = msg;
+    return status;
+}
+
+extern "C" {
+
+const char *pardnn_status_string(int status) {
+    switch (status) {
+        case PARDNN_OK: return "ok";
+        case PARDNN_E_INVAL: return "invalid argument";
+        case PARDNN_E_CYCLE: return "graph has a cycle";
+        case PARDNN_E_OVERFLOW: return "weights overflow int64";
+        case PARDNN_E_NOMEM: return "device out of memory";
+        case PARDNN_E_DEVICE: return "device or HIP runtime error";
+        default: return "unknown status";
+    }
+}
+
+const char *pardnn_last_error(void) { return g_last_error.c_str(); }
+
+int pardnn_graph_create(int32_t n_nodes, int64_t n_edges, const int32_t *src, const int32_t *dst,
+                        const int64_t *comp, const int64_t *edge_cost, const int64_t *mem,
+                        void *stream, pardnn_graph **out) {
+    g_last_error.clear();
+    if (out == nullptr) return fail(PARDNN_E_INVAL, "out is null");
+    *out = nullptr;
+    if (n_nodes < 0 || n_edges < 0 || n_edges >= (int64_t)INT32_MAX)
+        return fail(PARDNN_E_INVAL, "n_nodes must be >= 0 and 0 <= n_edges < 2^31 - 1");
+    if (n_edges > 0 && (src == nullptr || dst == nullptr || edge_cost == nullptr))
+        return fail(PARDNN_E_INVAL, "src, dst and edge_cost must be non-null when n_edges > 0");
+    if (n_nodes > 0 && (comp == nullptr || mem == nullptr))
+        return fail(PARDNN_E_INVAL, "comp and mem must be non-null when n_nodes > 0");
+    int ndev = 0;
+    if (hipGetDeviceCount(&ndev) != hipSuccess || ndev <= 0)
+        return fail(PARDNN_E_DEVICE, "no HIP device available");
+    Graph *g = new (std::nothrow) Graph();
+    if (g == nullptr) return fail(PARDNN_E_NOMEM, "host allocation failed");
+    if (hipGetDevice(&g->device) != hipSuccess) {
+        delete g;
+        return fail(PARDNN_E_DEVICE, "hipGetDevice failed");
+    }
+    g->stream = (hipStream_t)stream;
+    g->V = n_nodes;
+    g->E = n_edges;
+    int st = [&]() -> int {
+        const size_t V = (size_t)n_nodes, E = (size_t)n_edges;
+        HIP_TRY(dalloc(*g, &g->e_src, E));
+        HIP_TRY(dalloc(*g, &g->e_dst, E));
+        HIP_TRY(dalloc(*g, &g->e_cost, E));
+        HIP_TRY(dalloc(*g, &g->comp, V));
+        HIP_TRY(dalloc(*g, &g->mem, V));
+        HIP_TRY(dalloc(*g, &g->indeg, V));
+        HIP_TRY(dalloc(*g, &g->outdeg, V));
+        HIP_TRY(dalloc(*g, &g->o_off, V + 1));
+        HIP_TRY(dalloc(*g, &g->o_nbr, E));
+        HIP_TRY(dalloc(*g, &g->err, 4));
+        HIP_TRY(hipHostMalloc((void **)&g->h_err, 4 * sizeof(int32_t), hipHostMallocDefault));
+        ValidateAcc *acc = nullptr;
+        HIP_TRY(dalloc(*g, &acc, 1));
+        HIP_TRY(hipMemsetAsync(acc, 0, sizeof(ValidateAcc), g->stream));
+        HIP_TRY(launch_validate(*g, src, dst, comp, edge_cost, mem, acc));
+        ValidateAcc h{};
+        HIP_TRY(hipMemcpyAsync(&h, acc, sizeof(h), hipMemcpyDeviceToHost, g->stream));
+        HIP_TRY(hipStreamSynchronize(g->stream));
+        if (h.flags & 1ull) return fail(PARDNN_E_INVAL, "an edge endpoint is outside [0, n_nodes)");
+        if (h.flags & 2ull) return fail(PARDNN_E_INVAL, "a weight (comp, edge_cost or mem) is negative");
+        const unsigned __int128 w = ((unsigned __int128)h.w_hi << 32) + h.w_lo;
+        const unsigned __int128 m = ((unsigned __int128)h.m_hi << 32) + h.m_lo;
+        if (w > (unsigned __int128)INT64_MAX)
+            return fail(PARDNN_E_OVERFLOW, "sum(comp) + sum(edge_cost) exceeds INT64_MAX");
+        if (m > (unsigned __int128)INT64_MAX)
+            return fail(PARDNN_E_OVERFLOW, "sum(mem) exceeds INT64_MAX");
+        if (E > 0) {
+            HIP_TRY(hipMemcpyAsync(g->e_src, src, E * sizeof(int32_t), hipMemcpyDeviceToDevice, g->stream));
+            HIP_TRY(hipMemcpyAsync(g->e_dst, dst, E * sizeof(int32_t), hipMemcpyDeviceToDevice, g->stream));
+            HIP_TRY(hipMemcpyAsync(g->e_cost, edge_cost, E * sizeof(int64_t), hipMemcpyDeviceToDevice, g->stream));
+        }
+        if (V > 0) {
+            HIP_TRY(hipMemcpyAsync(g->comp, comp, V * sizeof(int64_t), hipMemcpyDeviceToDevice, g->stream));
+            HIP_TRY(hipMemcpyAsync(g->mem, mem, V * sizeof(int64_t), hipMemcpyDeviceToDevice, g->stream));
+        }
+        HIP_TRY(launch_fill_i32(g->indeg, (int64_t)V, 0, g->stream));
+        HIP_TRY(launch_fill_i32(g->outdeg, (int64_t)V, 0, g->stream));
+        HIP_TRY(launch_count_degrees(*g));
+        int32_t *ws = nullptr;
+        HIP_TRY(hipMalloc((void **)&ws, sizeof(int32_t) * (scan_workspace_elems(n_nodes) + V + 1)));
+        hipError_t e = launch_exclusive_scan(g->outdeg, g->o_off, n_nodes, ws, g->stream);
+        if (e == hipSuccess) e = launch_build_orig_csr(*g, ws + scan_workspace_elems(n_nodes));
+        if (e == hipSuccess) e = hipStreamSynchronize(g->stream);
+        (void)hipStreamSynchronize(g->stream);
+        (void)hipFree(ws);
+        HIP_TRY(e);
+        return PARDNN_OK;
+    }();
+    if (st != PARDNN_OK) {
+        std::string msg = g_last_error;
+        release(g);
+        g_last_error = msg;
+        return st;
+    }
+    *out = reinterpret_cast<pardnn_graph *>(g);
+    return PARDNN_OK;
+}
+
+int pardnn_graph_destroy(pardnn_graph *h) {
+    if (h == nullptr) return PARDNN_OK;
+    Graph *g = reinterpret_cast<Graph *>(h);
+    DeviceScope scope(g->device);
+    release(g);
+    return PARDNN_OK;
+}
+
+int pardnn_set_stream(pardnn_graph *h, void *stream) {
+    CHECK_HANDLE(h);
+    reinterpret_cast<Graph *>(h)->stream = (hipStream_t)stream;
+    return PARDNN_OK;
+}
+
+int pardnn_get_info(const pardnn_graph *h, pardnn_info *info) {
+    CHECK_HANDLE(h);
+    if (info == nullptr) return fail(PARDNN_E_INVAL, "info is null");
+    const Graph *g = reinterpret_cast<const Graph *>(h);
+    info->n_nodes = g->V;
+    info->n_edges = g->E;
+    info->n_levels = g->levelized ? g->L : -1;
+    info->max_width = g->levelized ? g->max_width : -1;
+    info->device = g->device;
+    return PARDNN_OK;
+}
+
+int pardnn_levelize(pardnn_graph *h, int32_t *level, int32_t *order, int32_t *level_ptr,
+                    int32_t *n_levels_host) {
+    CHECK_HANDLE(h);
+    Graph *g = reinterpret_cast<Graph *>(h);
+    DEVICE_SCOPE(g);
+    g_last_error.clear();
+    int st = ensure_levelized(g);
+    if (st != PARDNN_OK) return st;
+    const size_t V = (size_t)g->V;
+    if (level && V)
+        HIP_TRY(hipMemcpyAsync(level, g->level, V * sizeof(int32_t), hipMemcpyDeviceToDevice, g->stream));
+    if (order && V)
+        HIP_TRY(hipMemcpyAsync(order, g->order, V * sizeof(int32_t), hipMemcpyDeviceToDevice, g->stream));
+    if (level_ptr)
+        HIP_TRY(hipMemcpyAsync(level_ptr, g->level_ptr, ((size_t)g->L + 1) * sizeof(int32_t),
+                               hipMemcpyDeviceToDevice, g->stream));
+    if (n_levels_host) *n_levels_host = g->L;
+    return PARDNN_OK;
+}
+
+int pardnn_tb_levels(pardnn_graph *h, const int32_t *placement, int64_t *tl, int64_t *bl,
+                     int64_t *makespan) {
+    CHECK_HANDLE(h);
+    Graph *g = reinterpret_cast<Graph *>(h);
+    if (makespan == nullptr || (g->V > 0 && (placement == nullptr || tl == nullptr || bl == nullptr)))
+        return fail(PARDNN_E_INVAL, "placement, tl, bl and makespan must be non-null");
+    DEVICE_SCOPE(g);
+    int st = ensure_levelized(g);
+    if (st != PARDNN_OK) return st;
+    HIP_TRY(launch_permute_labels(*g, placement, g->lab_lm));
+    WalkArgs a{};
+    a.V = g->V;
+    a.L = g->L;
+    a.linfo = g->linfo;
+    a.in_off = g->in_off;
+    a.in_src = g->in_src;
+    a.in_dst = g->in_dst;
+    a.in_cost = g->in_cost;
+    a.out_off = g->out_off;
+    a.out_src = g->out_src;
+    a.out_dst = g->out_dst;
+    a.out_cost = g->out_cost;
+    a.comp_lm = g->comp_lm;
+    a.order = g->order;
+    a.lab = g->lab_lm;
+    a.ft = g->ft_lm;
+    a.blw = g->bl_lm;
+    a.tl_out = tl;
+    a.bl_out = bl;
+    a.makespan = makespan;
+    {
+        TimedLaunch t(g, "k_tb_single");
+        HIP_TRY(launch_tb_single(a, g->stream));
+    }
+    return PARDNN_OK;
+}
+
+int pardnn_critical_path(pardnn_graph *h, const int32_t *placement, const int64_t *tl,
+                         const int64_t *bl, const int64_t *makespan, uint8_t *is_critical,
+                         int32_t *path, int32_t *path_len) {
+    CHECK_HANDLE(h);
+    Graph *g = reinterpret_cast<Graph *>(h);
+    if (makespan == nullptr || path_len == nullptr ||
+        (g->V > 0 && (placement == nullptr || tl == nullptr || bl == nullptr ||
+                      is_critical == nullptr || path == nullptr)))
+        return fail(PARDNN_E_INVAL, "all arguments of pardnn_critical_path must be non-null");
+    DEVICE_SCOPE(g);
+    int st = ensure_levelized(g);
+    if (st != PARDNN_OK) return st;
+    HIP_TRY(launch_critical_path(*g, placement, tl, bl, makespan, is_critical, path, path_len));
+    return PARDNN_OK;
+}
+
+int pardnn_label_memory(pardnn_graph *h, const int32_t *placement, int32_t n_labels,
+                        const int64_t *capacity, int64_t *label_mem, int64_t *overflow) {
+    CHECK_HANDLE(h);
+    Graph *g = reinterpret_cast<Graph *>(h);
+    if (n_labels < 1) return fail(PARDNN_E_INVAL, "n_labels must be >= 1");
+    if (label_mem == nullptr || (g->V > 0 && placement == nullptr))
+        return fail(PARDNN_E_INVAL, "placement and label_mem must be non-null");
+    DEVICE_SCOPE(g);
+    HIP_TRY(launch_fill_i32(g->err, 4, 0, g->stream));
+    HIP_TRY(launch_label_memory(*g, placement, n_labels, capacity, label_mem, overflow, g->err));
+    int st = read_errors(g);
+    if (st != PARDNN_OK) return st;
+    if (g->h_err[0] & 1) return fail(PARDNN_E_INVAL, "a label lies outside [0, n_labels)");
+    if (g->h_err[0] & 2) return fail(PARDNN_E_INVAL, "a capacity is negative");
+    return PARDNN_OK;
+}
+
+int pardnn_apply_moves(pardnn_graph *h, int32_t *placement, int32_t n_moves, const int32_t *node,
+                       const int32_t *label) {
+    CHECK_HANDLE(h);
+    Graph *g = reinterpret_cast<Graph *>(h);
+    if (n_moves < 0) return fail(PARDNN_E_INVAL, "n_moves must be >= 0");
+    if (n_moves == 0) return PARDNN_OK;
+    if (placement == nullptr || node == nullptr || label == nullptr)
+        return fail(PARDNN_E_INVAL, "placement, node and label must be non-null");
+    DEVICE_SCOPE(g);
+    if (!g->move_stamp) {
+        HIP_TRY(dalloc(*g, &g->move_stamp, g->V));
+        HIP_TRY(launch_fill_i32(g->move_stamp, g->V, -1, g->stream));
+    }
+    HIP_TRY(launch_fill_i32(g->err, 4, 0, g->stream));
+    HIP_TRY(launch_apply_moves(*g, placement, n_moves, node, label, g->err));
+    int st = read_errors(g);
+    if (st != PARDNN_OK) return st;
+    if (g->h_err[0] & 1) return fail(PARDNN_E_INVAL, "a moved node id is outside [0, n_nodes)");
+    return PARDNN_OK;
+}
+
+int pardnn_build_placements(pardnn_graph *h, const int32_t *base, int32_t n_place,
+                            const int64_t *step_ptr, const int32_t *node, const int32_t *label,
+                            int32_t *placements) {
+    CHECK_HANDLE(h);
+    Graph *g = reinterpret_cast<Graph *>(h);
+    if (n_place < 0) return fail(PARDNN_E_INVAL, "n_place must be >= 0");
+    if (n_place == 0) return PARDNN_OK;
+    if (step_ptr == nullptr || (g->V > 0 && (base == nullptr || placements == nullptr)))
+        return fail(PARDNN_E_INVAL, "base, step_ptr and placements must be non-null");
+    DEVICE_SCOPE(g);
+    int64_t ends[2] = {0, 0};
+    HIP_TRY(hipMemcpyAsync(&ends[0], step_ptr, sizeof(int64_t), hipMemcpyDeviceToHost, g->stream));
+    HIP_TRY(hipMemcpyAsync(&ends[1], step_ptr + n_place, sizeof(int64_t), hipMemcpyDeviceToHost,
+                           g->stream));
+    HIP_TRY(hipStreamSynchronize(g->stream));
+    const int64_t M = ends[1];
+    if (ends[0] != 0 || M < 0 || M >= (int64_t)INT32_MAX)
+        return fail(PARDNN_E_INVAL, "step_ptr must start at 0 and hold fewer than 2^31 moves");
+    if (M > 0 && (node == nullptr || label == nullptr))
+        return fail(PARDNN_E_INVAL, "node and label must be non-null");
+    HIP_TRY(launch_fill_i32(g->err, 4, 0, g->stream));
+    HIP_TRY(launch_build_placements(*g, base, n_place, step_ptr, M, node, label, placements,
+                                    g->err));
+    int st = read_errors(g);
+    if (st != PARDNN_OK) return st;
+    if (g->h_err[0] & 1) return fail(PARDNN_E_INVAL, "a moved node id is outside [0, n_nodes)");
+    return PARDNN_OK;
+}
+
+int pardnn_evaluate_batch(pardnn_graph *h, int32_t n_place, const int32_t *placements,
+                          int32_t n_labels, const int64_t *capacity, int64_t *tl, int64_t *bl,
+                          int64_t *makespan, uint8_t *is_critical, int32_t *path,
+                          int32_t path_stride, int32_t *path_len, int64_t *label_mem,
+                          int64_t *overflow) {
+    CHECK_HANDLE(h);
+    Graph *g = reinterpret_cast<Graph *>(h);
+    if (n_place < 0) return fail(PARDNN_E_INVAL, "n_place must be >= 0");
+    if (n_place == 0) return PARDNN_OK;
+    if (makespan == nullptr || (g->V > 0 && (placements == nullptr || tl == nullptr || bl == nullptr)))
+        return fail(PARDNN_E_INVAL, "placements, tl, bl and makespan must be non-null");
+    if ((path == nullptr) != (path_len == nullptr))
+        return fail(PARDNN_E_INVAL, "path and path_len must both be given or both be null");
+    if (label_mem == nullptr && overflow != nullptr)
+        return fail(PARDNN_E_INVAL, "overflow needs label_mem");
+    if (label_mem != nullptr && n_labels < 1) return fail(PARDNN_E_INVAL, "n_labels must be >= 1");
+    DEVICE_SCOPE(g);
+    int st = ensure_levelized(g);
+    if (st != PARDNN_OK) return st;
+    if (path != nullptr && path_stride < std::max(g->L, 1))
+        return fail(PARDNN_E_INVAL, "path_stride must be at least the number of levels");
+
+    const int32_t S = batch_slots();
+    const int64_t n_slices = (n_place + S - 1) / S;
+    const size_t per = (size_t)n_slices * (size_t)g->V * (size_t)S;
+    const size_t need = per * (sizeof(int32_t) + 2 * sizeof(int64_t) + sizeof(int32_t)) + 256;
+    if (g->batch_ws_bytes < need) {
+        if (g->batch_ws) {
+            HIP_TRY(hipStreamSynchronize(g->stream));
+            HIP_TRY(hipFree(g->batch_ws));
+            g->batch_ws = nullptr;
+            g->batch_ws_bytes = 0;
+        }
+        HIP_TRY(hipMalloc(&g->batch_ws, need));
+        g->batch_ws_bytes = need;
+    }
+    char *ws = (char *)g->batch_ws;
+    int64_t *ft_w = (int64_t *)ws;
+    int64_t *bl_w = ft_w + per;
+    int32_t *lab_w = (int32_t *)(bl_w + per);
+    int32_t *nx_w = lab_w + per;
+
+    HIP_TRY(launch_permute_labels_batch(*g, placements, n_place, S, lab_w));
+    const int32_t K = label_mem != nullptr ? n_labels : 0;
+    if (K > 0) {
+        HIP_TRY(launch_fill_i32(g->err, 4, 0, g->stream));
+        HIP_TRY(launch_fill_i64(label_mem, (int64_t)n_place * K, 0, g->stream));
+    }
+    BatchArgs a{};
+    a.V = g->V;
+    a.L = g->L;
+    a.P = n_place;
+    a.K = K;
+    a.linfo = g->linfo;
+    a.in_off = g->in_off;
+    a.in_src = g->in_src;
+    a.in_dst = g->in_dst;
+    a.in_cost = g->in_cost;
+    a.out_off = g->out_off;
+    a.out_src = g->out_src;
+    a.out_dst = g->out_dst;
+    a.out_dst_orig = g->out_dst_orig;
+    a.out_cost = g->out_cost;
+    a.comp_lm = g->comp_lm;
+    a.mem_lm = g->mem_lm;
+    a.order = g->order;
+    a.lab_w = lab_w;
+    a.ft_w = ft_w;
+    a.bl_w = bl_w;
+    a.nx_w = nx_w;
+    a.tl_out = tl;
+    a.bl_out = bl;
+    a.makespan = makespan;
+    a.crit_out = is_critical;
+    a.path = path;
+    a.path_stride = path_stride;
+    a.path_len = path_len;
+    a.label_mem = label_mem;
+    a.err = g->err;
+    {
+        TimedLaunch t(g, "k_eval_batch");
+        HIP_TRY(launch_eval_batch(a, S, g->stream));
+    }
+    if (K > 0) {
+        if (overflow != nullptr || capacity != nullptr)
+            HIP_TRY(launch_overflow((int64_t)n_place * K, K, capacity, label_mem, overflow, g->err,
+                                    g->stream));
+        st = read_errors(g);
+        if (st != PARDNN_OK) return st;
+        if (g->h_err[0] & 1) return fail(PARDNN_E_INVAL, "a label lies outside [0, n_labels)");
+        if (g->h_err[0] & 2) return fail(PARDNN_E_INVAL, "a capacity is negative");
+    }
+    return PARDNN_OK;
+}
+
+int pardnn_set_timing(pardnn_graph *h, int enable) {
+    CHECK_HANDLE(h);
+    Graph *g = reinterpret_cast<Graph *>(h);
+    DEVICE_SCOPE(g);
+    if (enable && !g->ev0) {
+        HIP_TRY(hipEventCreate(&g->ev0));
+        HIP_TRY(hipEventCreate(&g->ev1));
+    }
+    g->timing = enable != 0;
+    g->timed = false;
+    return PARDNN_OK;
+}
+
+int pardnn_get_timing(pardnn_graph *h, const char **kernel, float *ms) {
+    CHECK_HANDLE(h);
+    Graph *g = reinterpret_cast<Graph *>(h);
+    if (ms == nullptr) return fail(PARDNN_E_INVAL, "ms is null");
+    if (!g->timed) return fail(PARDNN_E_INVAL, "no timed launch recorded");
+    DEVICE_SCOPE(g);
+    HIP_TRY(hipEventSynchronize(g->ev1));
+    HIP_TRY(hipEventElapsedTime(ms, g->ev0, g->ev1));
+    if (kernel) *kernel = g->timed_kernel;
+    return PARDNN_OK;
+}
+
+int pardnn_tb_levels_batch(pardnn_graph *h, int32_t n_place, const int32_t *placements,
+                           int64_t *tl, int64_t *bl, int64_t *makespan) {
+    return pardnn_evaluate_batch(h, n_place, placements, 0, nullptr, tl, bl, makespan, nullptr,
+                                 nullptr, 0, nullptr, nullptr, nullptr);
+}
+
+}  // extern "C"

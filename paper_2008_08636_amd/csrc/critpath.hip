@@ -1,0 +1,128 @@
+// critpath.hip -- critical nodes and the canonical critical path for one
+// placement (paper Table 2, CP; Alg. 1 find_heaviest_path walking by weighted
+// level on fresh values).
+//
+//   is_critical(v) = (tl(v) + bl(v) == M)
+//   next(u)        = smallest-id successor s with tl(u)+comp(u)+c(u,s)+bl(s) == M
+//   path           = smallest-id critical node without predecessors, then next()
+//                    until a node without a tight successor.
+//
+// Design for gfx950: next() of every node is one data-parallel pass over the
+// out-edges (level-major CSR). The remaining walk is a pointer chase, and its
+// links only point to strictly later levels, i.e. to larger level-major ids.
+// One workgroup therefore stages a window of next() in LDS with a coalesced
+// load, chases inside the window at LDS latency, and reloads the window only
+// when the chase leaves it -- the window only ever moves forward.
+#include "device_utils.h"
+#include "internal.h"
+
+namespace pardnn {
+
+namespace {
+
+constexpr int kBlock = 256;
+constexpr int kChaseThreads = 1024;
+constexpr int kWindow = 8192;
+
+inline unsigned grid_for(int64_t n, int block, int cap = 65536) {
+    int64_t g = (n + block - 1) / block;
+    if (g < 1) g = 1;
+    if (g > cap) g = cap;
+    return (unsigned)g;
+}
+
+// Additions wrap instead of overflowing for inputs not produced by the sweep;
+// for consistent inputs every sum stays below the ingest bound.
+__device__ __forceinline__ int64_t wadd(int64_t a, int64_t b) {
+    return (int64_t)((uint64_t)a + (uint64_t)b);
+}
+
+__global__ void k_crit_next(int32_t V, const int32_t *order, const int32_t *out_off,
+                            const int32_t *out_dst, const int32_t *out_dst_orig,
+                            const int64_t *out_cost, const int64_t *comp_lm,
+                            const int32_t *placement, const int64_t *tl, const int64_t *bl,
+                            const int64_t *makespan, uint8_t *is_critical, int32_t *next_lm,
+                            uint8_t *crit_lm) {
+    const int64_t M = *makespan;
+    for (int32_t v = blockIdx.x * blockDim.x + threadIdx.x; v < V; v += gridDim.x * blockDim.x) {
+        const int32_t ov = order[v];
+        const int64_t t = tl[ov];
+        const uint8_t crit = wadd(t, bl[ov]) == M;
+        is_critical[ov] = crit;
+        crit_lm[v] = crit;
+        const int32_t lu = placement[ov];
+        const int64_t base = wadd(t, comp_lm[v]);
+        int32_t best_o = INT32_MAX, best = -1;
+        for (int32_t j = out_off[v]; j < out_off[v + 1]; j++) {
+            const int32_t so = out_dst_orig[j];
+            const int64_t c = lu != placement[so] ? out_cost[j] : 0;
+            if (wadd(wadd(base, c), bl[so]) == M && so < best_o) {
+                best_o = so;
+                best = out_dst[j];
+            }
+        }
+        next_lm[v] = best;
+    }
+}
+
+__global__ __launch_bounds__(kChaseThreads) void k_chase(int32_t V, int32_t n0,
+                                                         const int32_t *order,
+                                                         const int32_t *next_lm,
+                                                         const uint8_t *crit_lm, int32_t *path,
+                                                         int32_t *path_len) {
+    __shared__ int32_t win[kWindow];
+    __shared__ int s_start, s_cur, s_len;
+    const int tid = threadIdx.x;
+    if (tid == 0) {
+        s_start = INT32_MAX;
+        s_len = 0;
+    }
+    __syncthreads();
+    // level 0 is sorted by original id: the smallest critical lm index there
+    // is the smallest-id critical node without predecessors
+    for (int32_t v = tid; v < n0; v += kChaseThreads)
+        if (crit_lm[v]) lds_min_i32(&s_start, v);
+    __syncthreads();
+    if (tid == 0) s_cur = s_start == INT32_MAX ? -1 : s_start;
+    __syncthreads();
+    while (true) {
+        const int32_t base = s_cur;
+        if (base < 0) break;
+        for (int i = tid; i < kWindow; i += kChaseThreads)
+            win[i] = base + i < V ? next_lm[base + i] : -1;
+        __syncthreads();
+        if (tid == 0) {
+            int32_t c = base, len = s_len;
+            while (c >= base && c < base + kWindow) {
+                path[len++] = order[c];
+                int32_t n = win[c - base];
+                // links go to strictly later levels; anything else ends the walk
+                c = n > c ? n : -1;
+            }
+            s_cur = c;
+            s_len = len;
+        }
+        __syncthreads();
+    }
+    if (tid == 0) *path_len = s_len;
+}
+
+}  // namespace
+
+hipError_t launch_critical_path(const Graph &g, const int32_t *placement, const int64_t *tl,
+                                const int64_t *bl, const int64_t *makespan,
+                                uint8_t *is_critical, int32_t *path, int32_t *path_len) {
+    if (g.V > 0) {
+        k_crit_next<<<grid_for(g.V, kBlock), kBlock, 0, g.stream>>>(
+            g.V, g.order, g.out_off, g.out_dst, g.out_dst_orig, g.out_cost, g.comp_lm, placement,
+            tl, bl, makespan, is_critical, g.next_lm, g.crit_lm);
+        hipError_t e = hipGetLastError();
+        if (e != hipSuccess) return e;
+    }
+    const int32_t n0 = g.L > 0 ? g.h_level_ptr[1] : 0;
+    k_chase<<<1, kChaseThreads, 0, g.stream>>>(g.V, n0, g.order, g.next_lm, g.crit_lm, path,
+                                               path_len);
+    return hipGetLastError();
+}
+
+}  // namespace pardnn

@@ -1,0 +1,173 @@
+// internal.h -- private declarations of the gfx950 evaluator library.
+//
+// Device data layout (all owned by the handle):
+//   original numbering (caller's ids):
+//     e_src, e_dst int32[E], e_cost int64[E]        edge list copy
+//     comp, mem int64[V], indeg, outdeg int32[V]
+//     o_off int32[V+1], o_nbr int32[E]              out-adjacency (Kahn)
+//   level-major numbering ("lm": nodes sorted by (level, id)):
+//     order int32[V] lm -> original id, rank int32[V] original -> lm
+//     level int32[V] (original ids), level_ptr int32[L+1]
+//     linfo LevelInfo[L+1]: first node, first in-edge, first out-edge of
+//       each level (entry L holds the totals)
+//     CSC (in-edges, grouped by destination):  in_off[V+1], in_src, in_dst,
+//       in_cost -- the in-edges of one level are one contiguous range
+//     CSR (out-edges, grouped by source):      out_off[V+1], out_src,
+//       out_dst, out_dst_orig (original id of the destination), out_cost
+//     comp_lm, mem_lm int64[V]
+#pragma once
+
+#include <hip/hip_runtime.h>
+
+#include <cstdint>
+#include <string>
+#include <vector>
+
+#include "pardnn.h"
+
+namespace pardnn {
+
+struct LevelInfo {
+    int32_t node_lo;   // first lm node of the level
+    int32_t in_e_lo;   // first CSC edge of the level
+    int32_t out_e_lo;  // first CSR edge of the level
+    int32_t pad;
+};
+
+struct ValidateAcc {
+    unsigned long long flags;    // bit 0: id out of range, bit 1: negative weight
+    unsigned long long w_lo, w_hi;  // sum(comp) + sum(edge_cost), split at bit 32
+    unsigned long long m_lo, m_hi;  // sum(mem), split at bit 32
+};
+
+// Scratch for the fixed-size walker kernels.
+constexpr int kWalkThreads = 1024;   // threads of a single-placement walker block
+constexpr int kAccNodes = 2048;      // LDS accumulators of a single-placement walker
+
+struct WalkArgs {
+    int32_t V, L;
+    const LevelInfo *linfo;
+    const int32_t *in_off, *in_src, *in_dst;
+    const int64_t *in_cost;
+    const int32_t *out_off, *out_src, *out_dst;
+    const int64_t *out_cost;
+    const int64_t *comp_lm;
+    const int32_t *order;
+    const int32_t *lab;     // lm labels
+    int64_t *ft;            // lm: tl + comp
+    int64_t *blw;           // lm: bl
+    int64_t *tl_out, *bl_out, *makespan;
+};
+
+struct BatchArgs {
+    int32_t V, L, P, K;     // nodes, levels, placements, labels (K = 0: no label sums)
+    const LevelInfo *linfo;
+    const int32_t *in_off, *in_src, *in_dst;
+    const int64_t *in_cost;
+    const int32_t *out_off, *out_src, *out_dst, *out_dst_orig;
+    const int64_t *out_cost;
+    const int64_t *comp_lm, *mem_lm;
+    const int32_t *order;
+    const int32_t *lab_w;   // [slice][V][S]
+    int64_t *ft_w, *bl_w;   // [slice][V][S]
+    int32_t *nx_w;          // [slice][V][S]
+    int64_t *tl_out, *bl_out, *makespan;  // [V][P], [V][P], [P]
+    uint8_t *crit_out;      // [V][P] or null
+    int32_t *path;          // [P][stride] or null
+    int32_t path_stride;
+    int32_t *path_len;      // [P]
+    int64_t *label_mem;     // [P][K] or null (must be zeroed when bins overflow LDS)
+    int32_t *err;           // device error word
+};
+
+struct Graph {
+    int device = 0;
+    hipStream_t stream = nullptr;
+    int32_t V = 0;
+    int64_t E = 0;
+
+    int32_t *e_src = nullptr, *e_dst = nullptr;
+    int64_t *e_cost = nullptr;
+    int64_t *comp = nullptr, *mem = nullptr;
+    int32_t *indeg = nullptr, *outdeg = nullptr;
+    int32_t *o_off = nullptr, *o_nbr = nullptr;
+
+    bool levelized = false;
+    int32_t L = -1, max_width = -1;
+    int32_t *level = nullptr, *order = nullptr, *rank = nullptr, *level_ptr = nullptr;
+    LevelInfo *linfo = nullptr;
+    std::vector<int32_t> h_level_ptr;
+    int32_t *in_off = nullptr, *in_src = nullptr, *in_dst = nullptr;
+    int64_t *in_cost = nullptr;
+    int32_t *out_off = nullptr, *out_src = nullptr, *out_dst = nullptr, *out_dst_orig = nullptr;
+    int64_t *out_cost = nullptr;
+    int64_t *comp_lm = nullptr, *mem_lm = nullptr;
+
+    // single-placement scratch
+    int32_t *lab_lm = nullptr, *next_lm = nullptr, *move_stamp = nullptr;
+    uint8_t *crit_lm = nullptr;
+    int64_t *ft_lm = nullptr, *bl_lm = nullptr;
+    int32_t *err = nullptr;          // device error words [4]
+    int32_t *h_err = nullptr;        // pinned host mirror [4]
+
+    // batch workspace, grown on demand
+    void *batch_ws = nullptr;
+    size_t batch_ws_bytes = 0;
+
+    // instrumentation: events around the main kernel of a call
+    bool timing = false;
+    bool timed = false;
+    hipEvent_t ev0 = nullptr, ev1 = nullptr;
+    const char *timed_kernel = "";
+
+    std::vector<void *> allocs;
+};
+
+// ---- status helpers (api.hip) ----
+int fail(int status, const std::string &msg);
+
+// ---- structure.hip ----
+hipError_t launch_fill_i32(int32_t *p, int64_t n, int32_t value, hipStream_t s);
+hipError_t launch_fill_i64(int64_t *p, int64_t n, int64_t value, hipStream_t s);
+hipError_t launch_validate(const Graph &g, const int32_t *src, const int32_t *dst,
+                           const int64_t *comp, const int64_t *cost, const int64_t *mem,
+                           ValidateAcc *acc);
+hipError_t launch_count_degrees(const Graph &g);
+hipError_t launch_exclusive_scan(const int32_t *in, int32_t *out, int32_t n, int32_t *ws,
+                                 hipStream_t s);
+size_t scan_workspace_elems(int32_t n);
+hipError_t launch_build_orig_csr(const Graph &g, int32_t *cursor);
+hipError_t launch_build_lm(Graph &g, int32_t *deg_ws, int32_t *cursor_in, int32_t *cursor_out,
+                           int32_t *scan_ws);
+
+// ---- levelize.hip ----
+hipError_t launch_kahn(const Graph &g, int32_t *indeg_work, int32_t *sort_scratch,
+                       int32_t *result);
+
+// ---- sweep.hip ----
+hipError_t launch_permute_labels(const Graph &g, const int32_t *placement, int32_t *lab_lm);
+hipError_t launch_tb_single(const WalkArgs &a, hipStream_t s);
+hipError_t launch_permute_labels_batch(const Graph &g, const int32_t *placements, int32_t P,
+                                       int32_t S, int32_t *lab_w);
+hipError_t launch_eval_batch(const BatchArgs &a, int32_t S, hipStream_t s);
+int batch_slots();  // placements per walker block of the batched evaluation
+
+// ---- critpath.hip ----
+hipError_t launch_critical_path(const Graph &g, const int32_t *placement, const int64_t *tl,
+                                const int64_t *bl, const int64_t *makespan,
+                                uint8_t *is_critical, int32_t *path, int32_t *path_len);
+
+// ---- labelmem.hip ----
+hipError_t launch_label_memory(const Graph &g, const int32_t *placement, int32_t K,
+                               const int64_t *capacity, int64_t *label_mem, int64_t *overflow,
+                               int32_t *err);
+hipError_t launch_overflow(int64_t n, int32_t K, const int64_t *capacity,
+                           const int64_t *label_mem, int64_t *overflow, int32_t *err,
+                           hipStream_t s);
+hipError_t launch_apply_moves(const Graph &g, int32_t *placement, int32_t n, const int32_t *node,
+                              const int32_t *label, int32_t *err);
+hipError_t launch_build_placements(const Graph &g, const int32_t *base, int32_t P,
+                                   const int64_t *step_ptr, int64_t M, const int32_t *node,
+                                   const int32_t *label, int32_t *placements, int32_t *err);
+
+}  // namespace pardnn

@@ -1,0 +1,350 @@
+"""GPU parity: the HIP library (through its C ABI) against the CPU oracle.
+
+All values are int64/int32/uint8, so every comparison is bit-exact. Inputs
+come from the seeded generators in ``workloads``; expected values come only
+from ``oracle``. Each case prints its name before touching the GPU.
+"""
+import functools
+import sys
+
+import numpy as np
+import pytest
+import torch
+
+import oracle
+import workloads as W
+
+pytestmark = pytest.mark.gpu
+
+
+def say(msg):
+    print(f"[gpu-case] {msg}", flush=True)
+    sys.stdout.flush()
+
+
+@pytest.fixture(scope="module")
+def P():
+    import paper_2008_08636_amd as P
+    if not torch.cuda.is_available():
+        pytest.fail("GPU tests need a visible GPU")
+    P.load_library()
+    return P
+
+
+@functools.lru_cache(maxsize=None)
+def cfg(i):
+    return W.make_config(i)
+
+
+def dev(x, dt):
+    return torch.as_tensor(np.ascontiguousarray(x), dtype=dt).cuda()
+
+
+def gpu_single(P, g, placement=None):
+    lab_np = g.placement if placement is None else placement
+    G = P.Graph(g.n_nodes, g.src, g.dst, g.comp, g.edge_cost, g.mem)
+    level, order, lptr, n = G.levelize()
+    lab = dev(lab_np, torch.int32)
+    tl, bl, m = G.tb_levels(lab)
+    crit, path, plen = G.critical_path(lab, tl, bl, m)
+    sums, over = G.label_memory(lab, g.n_labels, dev(g.capacity, torch.int64))
+    torch.cuda.synchronize()
+    out = {
+        "level": level.cpu().numpy(), "order": order.cpu().numpy(),
+        "level_ptr": lptr.cpu().numpy(), "n_levels": n,
+        "tl": tl.cpu().numpy(), "bl": bl.cpu().numpy(), "makespan": int(m.item()),
+        "is_critical": crit.cpu().numpy(), "path": path[: int(plen.item())].cpu().numpy(),
+        "label_mem": sums.cpu().numpy(), "overflow": over.cpu().numpy(),
+    }
+    G.close()
+    return out
+
+
+def oracle_single(g, placement=None):
+    lab = g.placement if placement is None else placement
+    level, order, lptr, n = oracle.levelize(g.n_nodes, g.src, g.dst)
+    r = oracle.evaluate(g.n_nodes, g.src, g.dst, g.comp, g.edge_cost, g.mem, lab,
+                        g.n_labels, g.capacity)
+    r.update(level=level, order=order, level_ptr=lptr, n_levels=n)
+    return r
+
+
+def assert_same(got, exp, keys=None):
+    keys = keys or ["level", "order", "level_ptr", "n_levels", "tl", "bl", "makespan",
+                    "is_critical", "path", "label_mem", "overflow"]
+    for k in keys:
+        a, b = got[k], exp[k]
+        if isinstance(b, np.ndarray):
+            assert a.shape == b.shape, (k, a.shape, b.shape)
+            bad = np.nonzero(a != b)[0]
+            assert bad.size == 0, f"{k}: {bad.size} mismatches, first at {bad[:5]}: {a[bad[:5]]} vs {b[bad[:5]]}"
+        else:
+            assert a == b, (k, a, b)
+
+
+# ------------------------------------------------------------ single placement --
+
+@pytest.mark.parametrize("i", [0, 1, 2, 3])
+def test_config_single(P, i):
+    g = cfg(i)
+    say(f"config{i} single V={g.n_nodes} E={g.n_edges}")
+    got = gpu_single(P, g)
+    exp = oracle_single(g)
+    assert_same(got, exp)
+
+
+def test_random_small_graphs(P):
+    say("random small DAGs")
+    rng = np.random.default_rng(20080863)
+    for t in range(150):
+        n = int(rng.integers(0, 40)) if t > 2 else t  # includes V = 0, 1, 2
+        g = W.random_dag(rng, n, p_edge=float(rng.uniform(0.0, 0.5)),
+                         max_weight=int(rng.integers(0, 5)), n_labels=int(rng.integers(1, 4)))
+        got = gpu_single(P, g)
+        exp = oracle_single(g)
+        assert_same(got, exp)
+
+
+def test_all_zero_weights_ties(P):
+    # every path has length 0: every node critical, path = lexicographic minimum
+    say("all-zero weights")
+    rng = np.random.default_rng(5)
+    g = W.random_dag(rng, 300, p_edge=0.02, max_weight=0, n_labels=2)
+    assert_same(gpu_single(P, g), oracle_single(g))
+
+
+def test_unit_weights_give_levels(P):
+    say("unit weights")
+    g = cfg(1)
+    g1 = W.SynthGraph("unit", g.n_nodes, g.src, g.dst, np.ones(g.n_nodes, np.int64),
+                      np.zeros(g.n_edges, np.int64), g.mem, g.placement, g.n_labels,
+                      g.capacity, {})
+    got = gpu_single(P, g1)
+    assert (got["tl"] == got["level"]).all()
+
+
+def test_critical_path_arbitrary_inputs(P):
+    # the path definition holds for any tl/bl/M, not only consistent ones
+    say("critical_path on perturbed inputs")
+    g = cfg(0)
+    rng = np.random.default_rng(3)
+    tl, bl, m = oracle.tb_levels(g.n_nodes, g.src, g.dst, g.comp, g.edge_cost, g.placement)
+    tl2 = tl.copy()
+    bl2 = bl.copy()
+    idx = rng.choice(g.n_nodes, 200, replace=False)
+    tl2[idx] += rng.integers(-5, 6, 200)
+    bl2[idx[::2]] -= 3
+    exp_crit, exp_path = oracle.critical_path(g.n_nodes, g.src, g.dst, g.comp, g.edge_cost,
+                                              g.placement, tl2, bl2, m)
+    G = P.Graph(g.n_nodes, g.src, g.dst, g.comp, g.edge_cost, g.mem)
+    lab = dev(g.placement, torch.int32)
+    crit, path, plen = G.critical_path(lab, dev(tl2, torch.int64), dev(bl2, torch.int64),
+                                       dev([m], torch.int64))
+    torch.cuda.synchronize()
+    assert (crit.cpu().numpy() == exp_crit).all()
+    assert (path[: int(plen.item())].cpu().numpy() == exp_path).all()
+    G.close()
+
+
+def test_determinism_and_stream(P):
+    say("determinism on a side stream")
+    g = cfg(2)
+    G = P.Graph(g.n_nodes, g.src, g.dst, g.comp, g.edge_cost, g.mem)
+    lab = dev(g.placement, torch.int32)
+    s = torch.cuda.Stream()
+    outs = []
+    for _ in range(2):
+        with torch.cuda.stream(s):
+            P.pardnn_set_stream(G.handle, s)
+            tl, bl, m = G.tb_levels(lab)
+        s.synchronize()
+        outs.append((tl.cpu().numpy(), bl.cpu().numpy(), int(m.item())))
+    assert (outs[0][0] == outs[1][0]).all() and (outs[0][1] == outs[1][1]).all()
+    assert outs[0][2] == outs[1][2]
+    G.close()
+
+
+# --------------------------------------------------------------------- errors --
+
+def test_error_paths(P):
+    say("error paths")
+    def mk(n, src, dst, comp=None, cost=None, mem=None):
+        comp = np.ones(n, np.int64) if comp is None else np.asarray(comp, np.int64)
+        cost = np.ones(len(src), np.int64) if cost is None else np.asarray(cost, np.int64)
+        mem = np.ones(n, np.int64) if mem is None else np.asarray(mem, np.int64)
+        return P.Graph(n, np.asarray(src, np.int32), np.asarray(dst, np.int32), comp, cost, mem)
+
+    with pytest.raises(P.PardnnError) as e:
+        mk(3, [0, 5], [1, 2])
+    assert e.value.status == P.E_INVAL
+    with pytest.raises(P.PardnnError) as e:
+        mk(3, [0], [-1])
+    assert e.value.status == P.E_INVAL
+    with pytest.raises(P.PardnnError) as e:
+        mk(2, [0], [1], comp=[1, -1])
+    assert e.value.status == P.E_INVAL
+    with pytest.raises(P.PardnnError) as e:
+        mk(2, [0], [1], cost=[-7])
+    assert e.value.status == P.E_INVAL
+    big = np.iinfo(np.int64).max
+    with pytest.raises(P.PardnnError) as e:
+        mk(2, [0], [1], comp=[big - 5, 0], cost=[10])
+    assert e.value.status == P.E_OVERFLOW
+    with pytest.raises(P.PardnnError) as e:
+        mk(2, [0], [1], mem=[big, 1])
+    assert e.value.status == P.E_OVERFLOW
+    ok = mk(2, [0], [1], comp=[big - 11, 0], cost=[10])  # exactly at the bound minus one
+    ok.close()
+    # cycles and self-loops
+    for src, dst in [([0, 1, 2], [1, 2, 0]), ([1], [1]), ([0, 1, 1], [1, 2, 1])]:
+        G = mk(3, src, dst)
+        with pytest.raises(P.PardnnError) as e:
+            G.levelize()
+        assert e.value.status == P.E_CYCLE
+        lab = dev([0, 0, 0], torch.int32)
+        with pytest.raises(P.PardnnError) as e:
+            G.tb_levels(lab)
+        assert e.value.status == P.E_CYCLE
+        G.close()
+    # labels out of range, negative capacity, bad move ids
+    G = mk(3, [0, 1], [1, 2])
+    with pytest.raises(P.PardnnError) as e:
+        G.label_memory(dev([0, 3, 1], torch.int32), 3)
+    assert e.value.status == P.E_INVAL
+    with pytest.raises(P.PardnnError) as e:
+        G.label_memory(dev([0, 1, 1], torch.int32), 2, dev([5, -1], torch.int64))
+    assert e.value.status == P.E_INVAL
+    place = dev([0, 0, 0], torch.int32)
+    with pytest.raises(P.PardnnError) as e:
+        G.apply_moves(place, dev([1, 7], torch.int32), dev([2, 2], torch.int32))
+    assert e.value.status == P.E_INVAL
+    assert place.cpu().tolist() == [0, 0, 0]  # nothing applied
+    G.close()
+
+
+# ---------------------------------------------------------------- moves --
+
+def test_apply_moves(P):
+    say("apply_moves")
+    rng = np.random.default_rng(11)
+    g = cfg(0)
+    G = P.Graph(g.n_nodes, g.src, g.dst, g.comp, g.edge_cost, g.mem)
+    place = g.placement.copy()
+    node = rng.integers(0, g.n_nodes, 500).astype(np.int32)  # with repeats
+    label = rng.integers(-3, 9, 500).astype(np.int32)
+    d = dev(place, torch.int32)
+    G.apply_moves(d, dev(node, torch.int32), dev(label, torch.int32))
+    for a, b in zip(node, label):  # in order, later wins
+        place[a] = b
+    assert (d.cpu().numpy() == place).all()
+    G.close()
+
+
+def test_build_placements(P):
+    say("build_placements")
+    g = cfg(0)
+    sched = W.config4_moves(g, n_place=70, frac=0.05, seed=77)
+    # add a repeated node inside one step and an empty step
+    node = sched.node.copy()
+    node[sched.ptr[3] + 1] = node[sched.ptr[3]]
+    ptr = sched.ptr.copy()
+    ptr[5] = ptr[4]  # step 4 now empty, step 5 gets its moves
+    sched2 = W.MoveSchedule(sched.base, ptr, node, sched.label, sched.n_labels)
+    exp = W.materialize_placements(sched2).T.copy()  # [V][P]
+    G = P.Graph(g.n_nodes, g.src, g.dst, g.comp, g.edge_cost, g.mem)
+    got = G.build_placements(dev(sched2.base, torch.int32), dev(ptr, torch.int64),
+                             dev(node, torch.int32), dev(sched2.label, torch.int32))
+    torch.cuda.synchronize()
+    assert (got.cpu().numpy() == exp).all()
+    G.close()
+
+
+# ---------------------------------------------------------------- batches --
+
+def check_batch(g, placements_vp, out, cols):
+    for p in cols:
+        lab = placements_vp[:, p].copy()
+        exp = oracle.evaluate(g.n_nodes, g.src, g.dst, g.comp, g.edge_cost, g.mem, lab,
+                              g.n_labels, g.capacity)
+        assert (out["tl"][:, p] == exp["tl"]).all(), p
+        assert (out["bl"][:, p] == exp["bl"]).all(), p
+        assert out["makespan"][p] == exp["makespan"], p
+        assert (out["is_critical"][:, p] == exp["is_critical"]).all(), p
+        plen = out["path_len"][p]
+        assert (out["path"][p, :plen] == exp["path"]).all(), p
+        assert (out["label_mem"][p] == exp["label_mem"]).all(), p
+        assert (out["overflow"][p] == exp["overflow"]).all(), p
+
+
+def run_batch(P, G, placements_vp, g):
+    out = G.evaluate_batch(dev(placements_vp, torch.int32), g.n_labels,
+                           dev(g.capacity, torch.int64))
+    torch.cuda.synchronize()
+    return {k: v.cpu().numpy() for k, v in out.items()}
+
+
+@pytest.mark.parametrize("i,n_place", [(0, 37), (1, 5), (2, 9)])
+def test_batch_random_placements(P, i, n_place):
+    g = cfg(i)
+    say(f"batch config{i} P={n_place}")
+    rng = np.random.default_rng(100 + i)
+    pl = rng.integers(0, g.n_labels, (g.n_nodes, n_place)).astype(np.int32)
+    pl[:, 0] = g.placement
+    pl[:, -1] = 0  # a single label: no communication at all
+    G = P.Graph(g.n_nodes, g.src, g.dst, g.comp, g.edge_cost, g.mem)
+    out = run_batch(P, G, pl, g)
+    check_batch(g, pl, out, range(n_place))
+    # the batched tl/bl/M agree with the single-placement entry point
+    lab = dev(pl[:, 1].copy(), torch.int32)
+    tl, bl, m = G.tb_levels(lab)
+    torch.cuda.synchronize()
+    assert (tl.cpu().numpy() == out["tl"][:, 1]).all() and int(m.item()) == out["makespan"][1]
+    G.close()
+
+
+def test_batch_small_graphs(P):
+    say("batch on small random DAGs")
+    rng = np.random.default_rng(4242)
+    for t in range(40):
+        n = int(rng.integers(0, 30)) if t > 1 else t
+        g = W.random_dag(rng, n, p_edge=0.3, max_weight=3, n_labels=3)
+        n_place = int(rng.integers(1, 6))
+        pl = rng.integers(0, 3, (n, n_place)).astype(np.int32)
+        G = P.Graph(g.n_nodes, g.src, g.dst, g.comp, g.edge_cost, g.mem)
+        out = run_batch(P, G, pl, g)
+        check_batch(g, pl, out, range(n_place))
+        G.close()
+
+
+def test_c4_refinement_loop_full_size(P):
+    """The 1000-placement refinement loop on the transformer graph, in the
+    launch configuration the benchmark times; sampled placements against the
+    oracle, properties on all of them."""
+    g = cfg(2)
+    say(f"config4 full size V={g.n_nodes} P=1000")
+    sched = W.config4_moves(g, n_place=1000)
+    G = P.Graph(g.n_nodes, g.src, g.dst, g.comp, g.edge_cost, g.mem)
+    pl = G.build_placements(dev(sched.base, torch.int32), dev(sched.ptr, torch.int64),
+                            dev(sched.node, torch.int32), dev(sched.label, torch.int32))
+    out = G.evaluate_batch(pl, g.n_labels, dev(g.capacity, torch.int64))
+    torch.cuda.synchronize()
+    cols = [0, 1, 2, 499, 998, 999] + list(range(50, 1000, 97))
+    exp_pl = W.materialize_placements(sched)  # [P][V]
+    for p in cols:
+        assert (pl[:, p].cpu().numpy() == exp_pl[p]).all(), p
+    sub = {k: (v[:, cols] if v.dim() == 2 and v.shape[0] == g.n_nodes else
+               v[cols]).cpu().numpy() for k, v in out.items()}
+    check_batch(g, exp_pl[cols].T.copy(), sub, range(len(cols)))
+    # properties on every placement, evaluated on the GPU in chunks
+    M = out["makespan"]
+    for c0 in range(0, 1000, 100):
+        tl = out["tl"][:, c0:c0 + 100]
+        bl = out["bl"][:, c0:c0 + 100]
+        w = tl + bl
+        assert bool((w <= M[c0:c0 + 100]).all())
+        crit = out["is_critical"][:, c0:c0 + 100].bool()
+        assert bool((crit == (w == M[c0:c0 + 100])).all())
+    assert bool((out["path_len"] >= 1).all())
+    total_mem = int(g.mem.sum())
+    assert bool((out["label_mem"].sum(dim=1) == total_mem).all())
+    G.close()
