@@ -151,8 +151,8 @@ int ensure_levelized(Graph *g) {
     HIP_TRY(dalloc(*g, &g->lab_lm, V));
     HIP_TRY(dalloc(*g, &g->next_lm, V));
     HIP_TRY(dalloc(*g, &g->crit_lm, V));
-    HIP_TRY(dalloc(*g, &g->ft_lm, V));
-    HIP_TRY(dalloc(*g, &g->bl_lm, V));
+    HIP_TRY(dalloc(*g, &g->ft_lm, 2 * (size_t)V));
+    HIP_TRY(dalloc(*g, &g->bl_lm, 2 * (size_t)V));
     if (!g->move_stamp) {
         HIP_TRY(dalloc(*g, &g->move_stamp, V));
         HIP_TRY(launch_fill_i32(g->move_stamp, V, -1, g->stream));
@@ -172,6 +172,28 @@ int ensure_levelized(Graph *g) {
     if (e != hipSuccess) return fail(hip_status(e), std::string("levelize: ") + hipGetErrorString(e));
     g->levelized = true;
     return PARDNN_OK;
+}
+
+SweepArgs sweep_args(const Graph *g) {
+    SweepArgs a{};
+    a.V = g->V;
+    a.E = g->E;
+    a.L = g->L;
+    a.linfo = g->linfo;
+    a.in_off = g->in_off;
+    a.in_src = g->in_src;
+    a.in_dst = g->in_dst;
+    a.in_cost = g->in_cost;
+    a.out_off = g->out_off;
+    a.out_src = g->out_src;
+    a.out_dst = g->out_dst;
+    a.out_dst_orig = g->out_dst_orig;
+    a.out_cost = g->out_cost;
+    a.comp_lm = g->comp_lm;
+    a.mem_lm = g->mem_lm;
+    a.order = g->order;
+    a.err = g->err;
+    return a;
 }
 
 #define CHECK_HANDLE(g)                                            \
@@ -258,6 +280,7 @@ int pardnn_graph_create(int32_t n_nodes, int64_t n_edges, const int32_t *src, co
             return fail(PARDNN_E_OVERFLOW, "sum(comp) + sum(edge_cost) exceeds INT64_MAX");
         if (m > (unsigned __int128)INT64_MAX)
             return fail(PARDNN_E_OVERFLOW, "sum(mem) exceeds INT64_MAX");
+        g->weight_bound = (int64_t)w;
         if (E > 0) {
             HIP_TRY(hipMemcpyAsync(g->e_src, src, E * sizeof(int32_t), hipMemcpyDeviceToDevice, g->stream));
             HIP_TRY(hipMemcpyAsync(g->e_dst, dst, E * sizeof(int32_t), hipMemcpyDeviceToDevice, g->stream));
@@ -346,29 +369,19 @@ int pardnn_tb_levels(pardnn_graph *h, const int32_t *placement, int64_t *tl, int
     int st = ensure_levelized(g);
     if (st != PARDNN_OK) return st;
     HIP_TRY(launch_permute_labels(*g, placement, g->lab_lm));
-    WalkArgs a{};
-    a.V = g->V;
-    a.L = g->L;
-    a.linfo = g->linfo;
-    a.in_off = g->in_off;
-    a.in_src = g->in_src;
-    a.in_dst = g->in_dst;
-    a.in_cost = g->in_cost;
-    a.out_off = g->out_off;
-    a.out_src = g->out_src;
-    a.out_dst = g->out_dst;
-    a.out_cost = g->out_cost;
-    a.comp_lm = g->comp_lm;
-    a.order = g->order;
-    a.lab = g->lab_lm;
-    a.ft = g->ft_lm;
-    a.blw = g->bl_lm;
+    SweepArgs a = sweep_args(g);
+    a.P = 1;
+    a.K = 0;
+    a.lab_w = g->lab_lm;
+    a.ftl = g->ft_lm;
+    a.bll = g->bl_lm;
     a.tl_out = tl;
     a.bl_out = bl;
     a.makespan = makespan;
+    a.direct = 1;
     {
-        TimedLaunch t(g, "k_tb_single");
-        HIP_TRY(launch_tb_single(a, g->stream));
+        TimedLaunch t(g, "k_sweep<1>");
+        HIP_TRY(launch_sweep(a, 1, g->stream));
     }
     return PARDNN_OK;
 }
@@ -481,7 +494,9 @@ int pardnn_evaluate_batch(pardnn_graph *h, int32_t n_place, const int32_t *place
     const int32_t S = batch_slots();
     const int64_t n_slices = (n_place + S - 1) / S;
     const size_t per = (size_t)n_slices * (size_t)g->V * (size_t)S;
-    const size_t need = per * (sizeof(int32_t) + 2 * sizeof(int64_t) + sizeof(int32_t)) + 256;
+    // lab_w, nx_w: int32 per (node, slot); ftl, bll: 16-byte pairs; start: [P]
+    const size_t need = per * (2 * sizeof(int32_t) + 4 * sizeof(int64_t)) +
+                        (size_t)n_place * sizeof(int32_t) + 1024;
     if (g->batch_ws_bytes < need) {
         if (g->batch_ws) {
             HIP_TRY(hipStreamSynchronize(g->stream));
@@ -492,11 +507,19 @@ int pardnn_evaluate_batch(pardnn_graph *h, int32_t n_place, const int32_t *place
         HIP_TRY(hipMalloc(&g->batch_ws, need));
         g->batch_ws_bytes = need;
     }
-    char *ws = (char *)g->batch_ws;
-    int64_t *ft_w = (int64_t *)ws;
-    int64_t *bl_w = ft_w + per;
-    int32_t *lab_w = (int32_t *)(bl_w + per);
+    // Pack {value, label} into one int64 when labels are known to lie in
+    // [0, n_labels) (they are checked) and values leave room for their bits.
+    int32_t lb = 0;
+    if (label_mem != nullptr) {
+        int32_t bits = 1;
+        while ((1ll << bits) < (int64_t)n_labels) bits++;
+        if (bits <= 16 && g->weight_bound < (1ll << (62 - bits))) lb = bits;
+    }
+    int64_t *ftl = (int64_t *)g->batch_ws;
+    int64_t *bll = ftl + 2 * per;
+    int32_t *lab_w = (int32_t *)(bll + 2 * per);
     int32_t *nx_w = lab_w + per;
+    int32_t *start = nx_w + per;
 
     HIP_TRY(launch_permute_labels_batch(*g, placements, n_place, S, lab_w));
     const int32_t K = label_mem != nullptr ? n_labels : 0;
@@ -504,41 +527,27 @@ int pardnn_evaluate_batch(pardnn_graph *h, int32_t n_place, const int32_t *place
         HIP_TRY(launch_fill_i32(g->err, 4, 0, g->stream));
         HIP_TRY(launch_fill_i64(label_mem, (int64_t)n_place * K, 0, g->stream));
     }
-    BatchArgs a{};
-    a.V = g->V;
-    a.L = g->L;
+    SweepArgs a = sweep_args(g);
     a.P = n_place;
     a.K = K;
-    a.linfo = g->linfo;
-    a.in_off = g->in_off;
-    a.in_src = g->in_src;
-    a.in_dst = g->in_dst;
-    a.in_cost = g->in_cost;
-    a.out_off = g->out_off;
-    a.out_src = g->out_src;
-    a.out_dst = g->out_dst;
-    a.out_dst_orig = g->out_dst_orig;
-    a.out_cost = g->out_cost;
-    a.comp_lm = g->comp_lm;
-    a.mem_lm = g->mem_lm;
-    a.order = g->order;
     a.lab_w = lab_w;
-    a.ft_w = ft_w;
-    a.bl_w = bl_w;
-    a.nx_w = nx_w;
+    a.ftl = ftl;
+    a.bll = bll;
+    a.nx_w = path != nullptr ? nx_w : nullptr;
     a.tl_out = tl;
     a.bl_out = bl;
     a.makespan = makespan;
-    a.crit_out = is_critical;
-    a.path = path;
-    a.path_stride = path_stride;
-    a.path_len = path_len;
+    a.start = path != nullptr ? start : nullptr;
     a.label_mem = label_mem;
-    a.err = g->err;
+    a.lb = lb;
+    a.direct = 0;
     {
-        TimedLaunch t(g, "k_eval_batch");
-        HIP_TRY(launch_eval_batch(a, S, g->stream));
+        TimedLaunch t(g, "k_sweep<2>");
+        HIP_TRY(launch_sweep(a, S, g->stream));
     }
+    HIP_TRY(launch_emit(a, S, is_critical, g->stream));
+    if (path != nullptr)
+        HIP_TRY(launch_chase_batch(a, S, g->order, path, path_stride, path_len, g->stream));
     if (K > 0) {
         if (overflow != nullptr || capacity != nullptr)
             HIP_TRY(launch_overflow((int64_t)n_place * K, K, capacity, label_mem, overflow, g->err,

@@ -40,27 +40,17 @@ struct ValidateAcc {
     unsigned long long m_lo, m_hi;  // sum(mem), split at bit 32
 };
 
-// Scratch for the fixed-size walker kernels.
-constexpr int kWalkThreads = 1024;   // threads of a single-placement walker block
-constexpr int kAccNodes = 2048;      // LDS accumulators of a single-placement walker
+// Sweep kernels: LDS accumulators cover this many nodes of a level per chunk;
+// per-label memory bins live in LDS while labels x slots fit kBinsCap.
+constexpr int kSweepAccNodes = 512;
+constexpr int kBinsCap = 1024;
+constexpr int kLevelWindow = 256;   // level boundaries staged in LDS at a time
 
-struct WalkArgs {
-    int32_t V, L;
-    const LevelInfo *linfo;
-    const int32_t *in_off, *in_src, *in_dst;
-    const int64_t *in_cost;
-    const int32_t *out_off, *out_src, *out_dst;
-    const int64_t *out_cost;
-    const int64_t *comp_lm;
-    const int32_t *order;
-    const int32_t *lab;     // lm labels
-    int64_t *ft;            // lm: tl + comp
-    int64_t *blw;           // lm: bl
-    int64_t *tl_out, *bl_out, *makespan;
-};
-
-struct BatchArgs {
+struct SweepArgs {
     int32_t V, L, P, K;     // nodes, levels, placements, labels (K = 0: no label sums)
+    int64_t E;
+    int32_t lb;             // > 0: {value, label} packed as (value << lb) | label
+    int32_t direct;         // node phase writes tl_out / bl_out itself (one placement)
     const LevelInfo *linfo;
     const int32_t *in_off, *in_src, *in_dst;
     const int64_t *in_cost;
@@ -68,15 +58,12 @@ struct BatchArgs {
     const int64_t *out_cost;
     const int64_t *comp_lm, *mem_lm;
     const int32_t *order;
-    const int32_t *lab_w;   // [slice][V][S]
-    int64_t *ft_w, *bl_w;   // [slice][V][S]
-    int32_t *nx_w;          // [slice][V][S]
-    int64_t *tl_out, *bl_out, *makespan;  // [V][P], [V][P], [P]
-    uint8_t *crit_out;      // [V][P] or null
-    int32_t *path;          // [P][stride] or null
-    int32_t path_stride;
-    int32_t *path_len;      // [P]
-    int64_t *label_mem;     // [P][K] or null (must be zeroed when bins overflow LDS)
+    const int32_t *lab_w;   // [slice][V][S] labels in level-major order
+    int64_t *ftl, *bll;     // [slice][V][S] {value, label}: tl + comp, bl (packed or pairs)
+    int32_t *nx_w;          // [slice][V][S] level-major id of the chosen successor, or null
+    int64_t *tl_out, *bl_out, *makespan;  // [V][P], [V][P], [P], caller's numbering
+    int32_t *start;         // [P] level-major id where the critical path starts, or null
+    int64_t *label_mem;     // [P][K], zeroed by the caller, or null
     int32_t *err;           // device error word
 };
 
@@ -85,6 +72,7 @@ struct Graph {
     hipStream_t stream = nullptr;
     int32_t V = 0;
     int64_t E = 0;
+    int64_t weight_bound = 0;   // sum(comp) + sum(edge_cost): bounds every path length
 
     int32_t *e_src = nullptr, *e_dst = nullptr;
     int64_t *e_cost = nullptr;
@@ -106,7 +94,7 @@ struct Graph {
     // single-placement scratch
     int32_t *lab_lm = nullptr, *next_lm = nullptr, *move_stamp = nullptr;
     uint8_t *crit_lm = nullptr;
-    int64_t *ft_lm = nullptr, *bl_lm = nullptr;
+    int64_t *ft_lm = nullptr, *bl_lm = nullptr;   // {value, label} pairs, 2 * V each
     int32_t *err = nullptr;          // device error words [4]
     int32_t *h_err = nullptr;        // pinned host mirror [4]
 
@@ -146,11 +134,13 @@ hipError_t launch_kahn(const Graph &g, int32_t *indeg_work, int32_t *sort_scratc
 
 // ---- sweep.hip ----
 hipError_t launch_permute_labels(const Graph &g, const int32_t *placement, int32_t *lab_lm);
-hipError_t launch_tb_single(const WalkArgs &a, hipStream_t s);
 hipError_t launch_permute_labels_batch(const Graph &g, const int32_t *placements, int32_t P,
                                        int32_t S, int32_t *lab_w);
-hipError_t launch_eval_batch(const BatchArgs &a, int32_t S, hipStream_t s);
-int batch_slots();  // placements per walker block of the batched evaluation
+hipError_t launch_sweep(const SweepArgs &a, int32_t S, hipStream_t s);
+hipError_t launch_emit(const SweepArgs &a, int32_t S, uint8_t *crit, hipStream_t s);
+hipError_t launch_chase_batch(const SweepArgs &a, int32_t S, const int32_t *order, int32_t *path,
+                              int32_t stride, int32_t *path_len, hipStream_t s);
+int batch_slots();  // placements per workgroup of the batched evaluation
 
 // ---- critpath.hip ----
 hipError_t launch_critical_path(const Graph &g, const int32_t *placement, const int64_t *tl,
