@@ -4,11 +4,11 @@
 Default workload (one "step" = one pass of the whole hot path over one batch):
 the refinement loop of 1,000 successive placements of the transformer-shaped
 training DAG (48 blocks, ~307k ops, ~867k edges, 16 labels), each placement
-moving 1 % of the ops. A step materialises the 1,000 placements from the
-per-step moves (pardnn_build_placements) and evaluates every one of them in
-full -- t-levels, b-levels, makespan, critical nodes, canonical critical path,
-per-label memory and overflow (pardnn_evaluate_batch). Graph structure
-(create + levelize) is built once before the timed region and reported apart.
+moving 1 % of the ops. A step applies the per-step moves and evaluates every
+placement in full -- t-levels, b-levels, makespan, critical nodes, canonical
+critical path, per-label memory and overflow -- in one call
+(pardnn_evaluate_moves). Graph structure (create + levelize) is built once
+before the timed region and reported apart.
 
 Printed: ONE JSON line with GTEPS (2E relaxations per placement per t+b sweep)
 as `value`, placement evaluations/s, the roofline of the dominant kernel
@@ -156,7 +156,6 @@ def main() -> int:
     lab = dev(sched.label, torch.int32)
     cap = dev(g.capacity, torch.int64)
     Pn = sched.n_place
-    placements = torch.empty((V, Pn), dtype=torch.int32, device="cuda")
     out = {
         "tl": torch.empty((V, Pn), dtype=torch.int64, device="cuda"),
         "bl": torch.empty((V, Pn), dtype=torch.int64, device="cuda"),
@@ -170,8 +169,7 @@ def main() -> int:
     P.pardnn_set_timing(G.handle, True)
 
     def step():
-        P.pardnn_build_placements(G.handle, base, Pn, ptr, node, lab, placements)
-        P.pardnn_evaluate_batch(G.handle, Pn, placements, K, cap, out["tl"], out["bl"],
+        P.pardnn_evaluate_moves(G.handle, base, Pn, ptr, node, lab, K, cap, out["tl"], out["bl"],
                                 out["makespan"], out["crit"], out["path"], L,
                                 out["path_len"], out["label_mem"], out["overflow"])
 
@@ -179,10 +177,12 @@ def main() -> int:
         step()
     torch.cuda.synchronize()
     kernel_ms = []
+    kernel_name = ""
     t0 = time.perf_counter()
     for _ in range(args.steps):
         step()
-        kernel_ms.append(P.pardnn_get_timing(G.handle)[1])
+        kernel_name, ms = P.pardnn_get_timing(G.handle)
+        kernel_ms.append(ms)
     torch.cuda.synchronize()
     dt = time.perf_counter() - t0
     ms_per_step = dt * 1e3 / args.steps
@@ -195,10 +195,10 @@ def main() -> int:
     alg = algorithmic_bytes_batch(V, E, Pn)
     achieved = alg / (k_ms / 1e3) / 1e9
     workload_key = f"c4_transformer_V{V}_E{E}_P{Pn}"
-    traffic = load_traffic("k_eval_batch", workload_key)
+    traffic = load_traffic(kernel_name, workload_key)
     roofline = {"bound": "hbm", "achieved": round(achieved, 2), "peak": HBM_PEAK_GBS,
                 "unit": "GB/s", "frac": round(achieved / HBM_PEAK_GBS, 4), "traffic": traffic,
-                "kernel": "k_eval_batch", "kernel_ms": round(k_ms, 4),
+                "kernel": kernel_name, "kernel_ms": round(k_ms, 4),
                 "algorithmic_bytes_per_launch": alg}
 
     single = None
@@ -215,7 +215,8 @@ def main() -> int:
         torch.cuda.synchronize()
         tb_ms = float(np.median(ts))
         single = {"workload": "one placement of the same graph (pardnn_tb_levels)",
-                  "kernel": "k_tb_single", "tb_levels_ms": round(tb_ms, 4), "levels": L,
+                  "kernel": P.pardnn_get_timing(G.handle)[0], "tb_levels_ms": round(tb_ms, 4),
+                  "levels": L,
                   "tau_us_per_level": round(tb_ms * 1e3 / max(L, 1), 4),
                   "gteps": round(2 * E / (tb_ms / 1e3) / 1e9, 4)}
         print(f"[bench] single placement t+b: {tb_ms:.3f} ms over {L} levels", file=sys.stderr,

@@ -224,6 +224,27 @@ int pardnn_evaluate_batch(pardnn_graph *g, int32_t n_place,
                           int32_t *path_len, int64_t *label_mem,
                           int64_t *overflow);
 
+/*
+ * The refinement loop's successive placements evaluated in one call (the
+ * partitioner re-evaluates after every batch of node moves: Sec. 3.2 memory
+ * heuristics, Alg. 2 mapping). Placement p is `base` with the moves of steps
+ * 0..p applied in order, exactly as pardnn_build_placements defines them;
+ * every output is exactly that of pardnn_evaluate_batch on those placements,
+ * but the [V][n_place] placement matrix is never materialised.
+ *   base, step_ptr, node, label   as for pardnn_build_placements.
+ *   other arguments               as for pardnn_evaluate_batch.
+ * Errors: E_INVAL (bad move node id, bad label when label_mem != NULL, short
+ * path_stride, malformed step_ptr). Syncs.
+ */
+int pardnn_evaluate_moves(pardnn_graph *g, const int32_t *base, int32_t n_place,
+                          const int64_t *step_ptr, const int32_t *node,
+                          const int32_t *label, int32_t n_labels,
+                          const int64_t *capacity, int64_t *tl, int64_t *bl,
+                          int64_t *makespan, uint8_t *is_critical,
+                          int32_t *path, int32_t path_stride,
+                          int32_t *path_len, int64_t *label_mem,
+                          int64_t *overflow);
+
 /* pardnn_evaluate_batch restricted to tl, bl and makespan. No sync. */
 int pardnn_tb_levels_batch(pardnn_graph *g, int32_t n_place,
                            const int32_t *placements, int64_t *tl, int64_t *bl,

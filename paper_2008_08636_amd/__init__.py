@@ -20,6 +20,7 @@ __all__ = [
     "pardnn_graph_create", "pardnn_graph_destroy", "pardnn_set_stream", "pardnn_get_info",
     "pardnn_levelize", "pardnn_tb_levels", "pardnn_critical_path", "pardnn_label_memory",
     "pardnn_apply_moves", "pardnn_build_placements", "pardnn_evaluate_batch",
+    "pardnn_evaluate_moves",
     "pardnn_tb_levels_batch", "pardnn_set_timing", "pardnn_get_timing",
     "pardnn_status_string", "pardnn_last_error",
 ]
@@ -65,6 +66,7 @@ def load_library(path: str = LIB_PATH):
         "pardnn_apply_moves": [P, P, i32, P, P],
         "pardnn_build_placements": [P, P, i32, P, P, P, P],
         "pardnn_evaluate_batch": [P, i32, P, i32, P, P, P, P, P, P, i32, P, P, P],
+        "pardnn_evaluate_moves": [P, P, i32, P, P, P, i32, P, P, P, P, P, P, i32, P, P, P],
         "pardnn_tb_levels_batch": [P, i32, P, P, P, P],
         "pardnn_set_timing": [P, ctypes.c_int],
         "pardnn_get_timing": [P, ctypes.POINTER(ctypes.c_char_p), ctypes.POINTER(ctypes.c_float)],
@@ -206,6 +208,21 @@ def pardnn_evaluate_batch(h, n_place, placements, n_labels, capacity, tl, bl, ma
         "pardnn_evaluate_batch")
 
 
+def pardnn_evaluate_moves(h, base, n_place, step_ptr, node, label, n_labels, capacity, tl, bl,
+                          makespan, is_critical=None, path=None, path_stride=0, path_len=None,
+                          label_mem=None, overflow=None):
+    _check(load_library().pardnn_evaluate_moves(
+        h, _ptr(base, torch.int32, name="base"), n_place,
+        _ptr(step_ptr, torch.int64, n_place + 1, "step_ptr"), _ptr(node, torch.int32, name="node"),
+        _ptr(label, torch.int32, name="label"), n_labels,
+        _ptr(capacity, torch.int64, name="capacity"), _ptr(tl, torch.int64, name="tl"),
+        _ptr(bl, torch.int64, name="bl"), _ptr(makespan, torch.int64, n_place, "makespan"),
+        _ptr(is_critical, torch.uint8, name="is_critical"), _ptr(path, torch.int32, name="path"),
+        path_stride, _ptr(path_len, torch.int32, name="path_len"),
+        _ptr(label_mem, torch.int64, name="label_mem"), _ptr(overflow, torch.int64, name="overflow")),
+        "pardnn_evaluate_moves")
+
+
 def pardnn_tb_levels_batch(h, n_place, placements, tl, bl, makespan):
     _check(load_library().pardnn_tb_levels_batch(
         h, n_place, _ptr(placements, torch.int32, name="placements"),
@@ -299,6 +316,38 @@ class Graph:
         n_place = step_ptr.numel() - 1
         out = torch.empty((self.n_nodes, n_place), dtype=torch.int32, device=self.device)
         pardnn_build_placements(self._h, base, n_place, step_ptr, node, label, out)
+        return out
+
+    def _outputs(self, P, n_labels, crit, path, labels):
+        V, dev = self.n_nodes, self.device
+        L = self.info()["n_levels"]
+        if L < 0:
+            L = pardnn_levelize(self._h)
+        out = {
+            "tl": torch.empty((V, P), dtype=torch.int64, device=dev),
+            "bl": torch.empty((V, P), dtype=torch.int64, device=dev),
+            "makespan": torch.empty(P, dtype=torch.int64, device=dev),
+        }
+        if crit:
+            out["is_critical"] = torch.empty((V, P), dtype=torch.uint8, device=dev)
+        if path:
+            out["path"] = torch.empty((P, max(L, 1)), dtype=torch.int32, device=dev)
+            out["path_len"] = torch.empty(P, dtype=torch.int32, device=dev)
+        if labels and n_labels > 0:
+            out["label_mem"] = torch.empty((P, n_labels), dtype=torch.int64, device=dev)
+            out["overflow"] = torch.empty((P, n_labels), dtype=torch.int64, device=dev)
+        return out, max(L, 1)
+
+    def evaluate_moves(self, base, step_ptr, node, label, n_labels=0, capacity=None, crit=True,
+                       path=True, labels=True):
+        """All outputs for the successive placements base + moves (see
+        pardnn_evaluate_moves); arrays are placement-minor [V][P]."""
+        P = step_ptr.numel() - 1
+        out, stride = self._outputs(P, n_labels, crit, path, labels)
+        pardnn_evaluate_moves(self._h, base, P, step_ptr, node, label,
+                              n_labels if labels else 0, capacity, out["tl"], out["bl"],
+                              out["makespan"], out.get("is_critical"), out.get("path"), stride,
+                              out.get("path_len"), out.get("label_mem"), out.get("overflow"))
         return out
 
     def evaluate_batch(self, placements, n_labels=0, capacity=None, crit=True, path=True,

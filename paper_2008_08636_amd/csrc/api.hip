@@ -148,6 +148,9 @@ int ensure_levelized(Graph *g) {
     HIP_TRY(dalloc(*g, &g->out_cost, E));
     HIP_TRY(dalloc(*g, &g->comp_lm, V));
     HIP_TRY(dalloc(*g, &g->mem_lm, V));
+    HIP_TRY(dalloc(*g, &g->in_rec, E));
+    HIP_TRY(dalloc(*g, &g->out_rec, E));
+    HIP_TRY(dalloc(*g, &g->node_rec, V));
     HIP_TRY(dalloc(*g, &g->lab_lm, V));
     HIP_TRY(dalloc(*g, &g->next_lm, V));
     HIP_TRY(dalloc(*g, &g->crit_lm, V));
@@ -191,6 +194,9 @@ SweepArgs sweep_args(const Graph *g) {
     a.out_cost = g->out_cost;
     a.comp_lm = g->comp_lm;
     a.mem_lm = g->mem_lm;
+    a.in_rec = g->in_rec;
+    a.out_rec = g->out_rec;
+    a.node_rec = g->node_rec;
     a.order = g->order;
     a.err = g->err;
     return a;
@@ -204,6 +210,132 @@ SweepArgs sweep_args(const Graph *g) {
 #define DEVICE_SCOPE(g)                                                         \
     DeviceScope scope_((g)->device);                                            \
     if (!scope_.ok) return fail(PARDNN_E_DEVICE, "cannot select the handle's device")
+
+// Placements come either as a [V][P] matrix or as base + per-step moves.
+struct MovesIn {
+    const int32_t *base;
+    const int64_t *step_ptr;
+    const int32_t *node, *label;
+};
+
+int evaluate_impl(Graph *g, int32_t n_place, const int32_t *placements, const MovesIn *mv,
+                  int32_t n_labels, const int64_t *capacity, int64_t *tl, int64_t *bl,
+                  int64_t *makespan, uint8_t *is_critical, int32_t *path, int32_t path_stride,
+                  int32_t *path_len, int64_t *label_mem, int64_t *overflow) {
+    if (n_place < 0) return fail(PARDNN_E_INVAL, "n_place must be >= 0");
+    if (n_place == 0) return PARDNN_OK;
+    if (makespan == nullptr ||
+        (g->V > 0 && ((placements == nullptr && mv == nullptr) || tl == nullptr || bl == nullptr)))
+        return fail(PARDNN_E_INVAL, "placements, tl, bl and makespan must be non-null");
+    if ((path == nullptr) != (path_len == nullptr))
+        return fail(PARDNN_E_INVAL, "path and path_len must both be given or both be null");
+    if (label_mem == nullptr && overflow != nullptr)
+        return fail(PARDNN_E_INVAL, "overflow needs label_mem");
+    if (label_mem != nullptr && n_labels < 1) return fail(PARDNN_E_INVAL, "n_labels must be >= 1");
+    DEVICE_SCOPE(g);
+    int st = ensure_levelized(g);
+    if (st != PARDNN_OK) return st;
+    if (path != nullptr && path_stride < std::max(g->L, 1))
+        return fail(PARDNN_E_INVAL, "path_stride must be at least the number of levels");
+
+    const int32_t S = batch_slots();
+    const int64_t n_slices = (n_place + S - 1) / S;
+    const size_t per = (size_t)n_slices * (size_t)g->V * (size_t)S;
+    // lab_w, nx_w: int32 per (node, slot); ftl, bll: 16-byte pairs; start: [P]
+    const size_t need = per * (2 * sizeof(int32_t) + 4 * sizeof(int64_t)) +
+                        (size_t)n_place * sizeof(int32_t) + 1024;
+    if (g->batch_ws_bytes < need) {
+        if (g->batch_ws) {
+            HIP_TRY(hipStreamSynchronize(g->stream));
+            HIP_TRY(hipFree(g->batch_ws));
+            g->batch_ws = nullptr;
+            g->batch_ws_bytes = 0;
+        }
+        HIP_TRY(hipMalloc(&g->batch_ws, need));
+        g->batch_ws_bytes = need;
+    }
+    // Pack {value, label} into one int64 when labels are known to lie in
+    // [0, n_labels) (they are checked) and values leave room for their bits.
+    // The b keys then also carry the successor id: (value << ob) | (2^ob - 1 - id)
+    // with 2^ob > V, which needs values below 2^(62 - ob) as well.
+    int32_t lb = 0, ob = 0;
+    if (label_mem != nullptr) {
+        int32_t bits = 1;
+        while ((1ll << bits) < (int64_t)n_labels) bits++;
+        int32_t obits = 1;
+        while ((1ll << obits) <= (int64_t)g->V) obits++;
+        const int32_t wide = std::max(bits, obits);
+        if (bits <= 16 && wide < 62 && g->weight_bound < (1ll << (62 - wide))) {
+            lb = bits;
+            ob = obits;
+        }
+    }
+    int64_t *ftl = (int64_t *)g->batch_ws;
+    int64_t *bll = ftl + 2 * per;
+    int32_t *lab_w = (int32_t *)(bll + 2 * per);
+    int32_t *nx_w = lab_w + per;
+    int32_t *start = nx_w + per;
+
+    const int32_t K = label_mem != nullptr ? n_labels : 0;
+    HIP_TRY(launch_fill_i32(g->err, 4, 0, g->stream));
+    if (mv != nullptr) {
+        int64_t ends[2] = {0, 0};
+        HIP_TRY(hipMemcpyAsync(&ends[0], mv->step_ptr, sizeof(int64_t), hipMemcpyDeviceToHost,
+                               g->stream));
+        HIP_TRY(hipMemcpyAsync(&ends[1], mv->step_ptr + n_place, sizeof(int64_t),
+                               hipMemcpyDeviceToHost, g->stream));
+        HIP_TRY(hipStreamSynchronize(g->stream));
+        if (ends[0] != 0 || ends[1] < 0 || ends[1] >= (int64_t)INT32_MAX)
+            return fail(PARDNN_E_INVAL, "step_ptr must start at 0 and hold fewer than 2^31 moves");
+        if (ends[1] > 0 && (mv->node == nullptr || mv->label == nullptr))
+            return fail(PARDNN_E_INVAL, "node and label must be non-null");
+        if (g->V > 0 && mv->base == nullptr) return fail(PARDNN_E_INVAL, "base must be non-null");
+        // the move marks live in the t workspace, which the sweep overwrites later
+        HIP_TRY(launch_moves_to_slices(*g, mv->base, n_place, mv->step_ptr, ends[1], mv->node,
+                                       mv->label, S, reinterpret_cast<int32_t *>(ftl), lab_w,
+                                       g->err));
+    } else {
+        HIP_TRY(launch_permute_labels_batch(*g, placements, n_place, S, lab_w));
+    }
+    if (K > 0) {
+        HIP_TRY(launch_fill_i64(label_mem, (int64_t)n_place * K, 0, g->stream));
+    }
+    SweepArgs a = sweep_args(g);
+    a.P = n_place;
+    a.K = K;
+    a.lab_w = lab_w;
+    a.ftl = ftl;
+    a.bll = bll;
+    a.nx_w = path != nullptr ? nx_w : nullptr;
+    a.tl_out = tl;
+    a.bl_out = bl;
+    a.makespan = makespan;
+    a.start = path != nullptr ? start : nullptr;
+    a.label_mem = label_mem;
+    a.lb = lb;
+    a.ob = ob;
+    {
+        TimedLaunch t(g, "k_sweep<2>");
+        HIP_TRY(launch_sweep(a, S, g->stream));
+    }
+    HIP_TRY(launch_finish(a, S, is_critical, path, path_stride, path_len, g->stream));
+    if (K > 0) {
+        if (overflow != nullptr || capacity != nullptr)
+            HIP_TRY(launch_overflow((int64_t)n_place * K, K, capacity, label_mem, overflow, g->err,
+                                    g->stream));
+    }
+    if (K > 0 || mv != nullptr) {
+        st = read_errors(g);
+        if (st != PARDNN_OK) return st;
+        if (g->h_err[0] & 1)
+            return fail(PARDNN_E_INVAL, mv != nullptr && K == 0
+                                            ? "a moved node id is outside [0, n_nodes)"
+                                            : "a label or a moved node id is out of range");
+        if (g->h_err[0] & 2) return fail(PARDNN_E_INVAL, "a capacity is negative");
+    }
+    return PARDNN_OK;
+}
+
 
 }  // namespace
 
@@ -378,7 +510,6 @@ int pardnn_tb_levels(pardnn_graph *h, const int32_t *placement, int64_t *tl, int
     a.tl_out = tl;
     a.bl_out = bl;
     a.makespan = makespan;
-    a.direct = 1;
     {
         TimedLaunch t(g, "k_sweep<1>");
         HIP_TRY(launch_sweep(a, 1, g->stream));
@@ -476,88 +607,24 @@ int pardnn_evaluate_batch(pardnn_graph *h, int32_t n_place, const int32_t *place
                           int64_t *overflow) {
     CHECK_HANDLE(h);
     Graph *g = reinterpret_cast<Graph *>(h);
-    if (n_place < 0) return fail(PARDNN_E_INVAL, "n_place must be >= 0");
-    if (n_place == 0) return PARDNN_OK;
-    if (makespan == nullptr || (g->V > 0 && (placements == nullptr || tl == nullptr || bl == nullptr)))
-        return fail(PARDNN_E_INVAL, "placements, tl, bl and makespan must be non-null");
-    if ((path == nullptr) != (path_len == nullptr))
-        return fail(PARDNN_E_INVAL, "path and path_len must both be given or both be null");
-    if (label_mem == nullptr && overflow != nullptr)
-        return fail(PARDNN_E_INVAL, "overflow needs label_mem");
-    if (label_mem != nullptr && n_labels < 1) return fail(PARDNN_E_INVAL, "n_labels must be >= 1");
-    DEVICE_SCOPE(g);
-    int st = ensure_levelized(g);
-    if (st != PARDNN_OK) return st;
-    if (path != nullptr && path_stride < std::max(g->L, 1))
-        return fail(PARDNN_E_INVAL, "path_stride must be at least the number of levels");
+    if (g->V > 0 && n_place > 0 && placements == nullptr)
+        return fail(PARDNN_E_INVAL, "placements must be non-null");
+    return evaluate_impl(g, n_place, placements, nullptr, n_labels, capacity, tl, bl, makespan,
+                         is_critical, path, path_stride, path_len, label_mem, overflow);
+}
 
-    const int32_t S = batch_slots();
-    const int64_t n_slices = (n_place + S - 1) / S;
-    const size_t per = (size_t)n_slices * (size_t)g->V * (size_t)S;
-    // lab_w, nx_w: int32 per (node, slot); ftl, bll: 16-byte pairs; start: [P]
-    const size_t need = per * (2 * sizeof(int32_t) + 4 * sizeof(int64_t)) +
-                        (size_t)n_place * sizeof(int32_t) + 1024;
-    if (g->batch_ws_bytes < need) {
-        if (g->batch_ws) {
-            HIP_TRY(hipStreamSynchronize(g->stream));
-            HIP_TRY(hipFree(g->batch_ws));
-            g->batch_ws = nullptr;
-            g->batch_ws_bytes = 0;
-        }
-        HIP_TRY(hipMalloc(&g->batch_ws, need));
-        g->batch_ws_bytes = need;
-    }
-    // Pack {value, label} into one int64 when labels are known to lie in
-    // [0, n_labels) (they are checked) and values leave room for their bits.
-    int32_t lb = 0;
-    if (label_mem != nullptr) {
-        int32_t bits = 1;
-        while ((1ll << bits) < (int64_t)n_labels) bits++;
-        if (bits <= 16 && g->weight_bound < (1ll << (62 - bits))) lb = bits;
-    }
-    int64_t *ftl = (int64_t *)g->batch_ws;
-    int64_t *bll = ftl + 2 * per;
-    int32_t *lab_w = (int32_t *)(bll + 2 * per);
-    int32_t *nx_w = lab_w + per;
-    int32_t *start = nx_w + per;
-
-    HIP_TRY(launch_permute_labels_batch(*g, placements, n_place, S, lab_w));
-    const int32_t K = label_mem != nullptr ? n_labels : 0;
-    if (K > 0) {
-        HIP_TRY(launch_fill_i32(g->err, 4, 0, g->stream));
-        HIP_TRY(launch_fill_i64(label_mem, (int64_t)n_place * K, 0, g->stream));
-    }
-    SweepArgs a = sweep_args(g);
-    a.P = n_place;
-    a.K = K;
-    a.lab_w = lab_w;
-    a.ftl = ftl;
-    a.bll = bll;
-    a.nx_w = path != nullptr ? nx_w : nullptr;
-    a.tl_out = tl;
-    a.bl_out = bl;
-    a.makespan = makespan;
-    a.start = path != nullptr ? start : nullptr;
-    a.label_mem = label_mem;
-    a.lb = lb;
-    a.direct = 0;
-    {
-        TimedLaunch t(g, "k_sweep<2>");
-        HIP_TRY(launch_sweep(a, S, g->stream));
-    }
-    HIP_TRY(launch_emit(a, S, is_critical, g->stream));
-    if (path != nullptr)
-        HIP_TRY(launch_chase_batch(a, S, g->order, path, path_stride, path_len, g->stream));
-    if (K > 0) {
-        if (overflow != nullptr || capacity != nullptr)
-            HIP_TRY(launch_overflow((int64_t)n_place * K, K, capacity, label_mem, overflow, g->err,
-                                    g->stream));
-        st = read_errors(g);
-        if (st != PARDNN_OK) return st;
-        if (g->h_err[0] & 1) return fail(PARDNN_E_INVAL, "a label lies outside [0, n_labels)");
-        if (g->h_err[0] & 2) return fail(PARDNN_E_INVAL, "a capacity is negative");
-    }
-    return PARDNN_OK;
+int pardnn_evaluate_moves(pardnn_graph *h, const int32_t *base, int32_t n_place,
+                          const int64_t *step_ptr, const int32_t *node, const int32_t *label,
+                          int32_t n_labels, const int64_t *capacity, int64_t *tl, int64_t *bl,
+                          int64_t *makespan, uint8_t *is_critical, int32_t *path,
+                          int32_t path_stride, int32_t *path_len, int64_t *label_mem,
+                          int64_t *overflow) {
+    CHECK_HANDLE(h);
+    Graph *g = reinterpret_cast<Graph *>(h);
+    if (n_place > 0 && step_ptr == nullptr) return fail(PARDNN_E_INVAL, "step_ptr must be non-null");
+    MovesIn mv{base, step_ptr, node, label};
+    return evaluate_impl(g, n_place, nullptr, &mv, n_labels, capacity, tl, bl, makespan,
+                         is_critical, path, path_stride, path_len, label_mem, overflow);
 }
 
 int pardnn_set_timing(pardnn_graph *h, int enable) {

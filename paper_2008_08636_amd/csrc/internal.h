@@ -15,6 +15,8 @@
 //     CSR (out-edges, grouped by source):      out_off[V+1], out_src,
 //       out_dst, out_dst_orig (original id of the destination), out_cost
 //     comp_lm, mem_lm int64[V]
+//     in_rec, out_rec EdgeRec16[E] and node_rec NodeRec16[V]: the same data
+//       as 16-byte records, so a sweep task loads its edge with one load
 #pragma once
 
 #include <hip/hip_runtime.h>
@@ -34,29 +36,44 @@ struct LevelInfo {
     int32_t pad;
 };
 
+// Level-major edge record of one sweep direction: the neighbour whose value
+// is gathered, the node the candidate is folded into, and the edge cost.
+struct alignas(16) EdgeRec16 {
+    int32_t nb;
+    int32_t own;
+    int64_t cost;
+};
+
+// Per-node constants of the sweeps, level-major.
+struct alignas(16) NodeRec16 {
+    int64_t comp;
+    int64_t mem;
+};
+
 struct ValidateAcc {
     unsigned long long flags;    // bit 0: id out of range, bit 1: negative weight
     unsigned long long w_lo, w_hi;  // sum(comp) + sum(edge_cost), split at bit 32
     unsigned long long m_lo, m_hi;  // sum(mem), split at bit 32
 };
 
-// Sweep kernels: LDS accumulators cover this many nodes of a level per chunk;
-// per-label memory bins live in LDS while labels x slots fit kBinsCap.
-constexpr int kSweepAccNodes = 512;
-constexpr int kBinsCap = 1024;
-constexpr int kLevelWindow = 256;   // level boundaries staged in LDS at a time
+// Sweep kernels: per-label memory bins live in LDS while labels x slots fit
+// kBinsCap; level boundaries are staged in LDS kLevelWindow levels at a time.
+constexpr int kBinsCap = 512;
+constexpr int kLevelWindow = 128;
 
 struct SweepArgs {
     int32_t V, L, P, K;     // nodes, levels, placements, labels (K = 0: no label sums)
     int64_t E;
     int32_t lb;             // > 0: {value, label} packed as (value << lb) | label
-    int32_t direct;         // node phase writes tl_out / bl_out itself (one placement)
+    int32_t ob;             // with lb > 0: b keys are (value << ob) | (2^ob - 1 - successor id)
     const LevelInfo *linfo;
     const int32_t *in_off, *in_src, *in_dst;
     const int64_t *in_cost;
     const int32_t *out_off, *out_src, *out_dst, *out_dst_orig;
     const int64_t *out_cost;
     const int64_t *comp_lm, *mem_lm;
+    const EdgeRec16 *in_rec, *out_rec;   // t: {src, dst, cost} by dst; b: {dst, src, cost} by src
+    const NodeRec16 *node_rec;
     const int32_t *order;
     const int32_t *lab_w;   // [slice][V][S] labels in level-major order
     int64_t *ftl, *bll;     // [slice][V][S] {value, label}: tl + comp, bl (packed or pairs)
@@ -90,6 +107,8 @@ struct Graph {
     int32_t *out_off = nullptr, *out_src = nullptr, *out_dst = nullptr, *out_dst_orig = nullptr;
     int64_t *out_cost = nullptr;
     int64_t *comp_lm = nullptr, *mem_lm = nullptr;
+    EdgeRec16 *in_rec = nullptr, *out_rec = nullptr;
+    NodeRec16 *node_rec = nullptr;
 
     // single-placement scratch
     int32_t *lab_lm = nullptr, *next_lm = nullptr, *move_stamp = nullptr;
@@ -137,9 +156,8 @@ hipError_t launch_permute_labels(const Graph &g, const int32_t *placement, int32
 hipError_t launch_permute_labels_batch(const Graph &g, const int32_t *placements, int32_t P,
                                        int32_t S, int32_t *lab_w);
 hipError_t launch_sweep(const SweepArgs &a, int32_t S, hipStream_t s);
-hipError_t launch_emit(const SweepArgs &a, int32_t S, uint8_t *crit, hipStream_t s);
-hipError_t launch_chase_batch(const SweepArgs &a, int32_t S, const int32_t *order, int32_t *path,
-                              int32_t stride, int32_t *path_len, hipStream_t s);
+hipError_t launch_finish(const SweepArgs &a, int32_t S, uint8_t *crit, int32_t *path,
+                         int32_t stride, int32_t *path_len, hipStream_t s);
 int batch_slots();  // placements per workgroup of the batched evaluation
 
 // ---- critpath.hip ----
@@ -159,5 +177,9 @@ hipError_t launch_apply_moves(const Graph &g, int32_t *placement, int32_t n, con
 hipError_t launch_build_placements(const Graph &g, const int32_t *base, int32_t P,
                                    const int64_t *step_ptr, int64_t M, const int32_t *node,
                                    const int32_t *label, int32_t *placements, int32_t *err);
+hipError_t launch_moves_to_slices(const Graph &g, const int32_t *base, int32_t P,
+                                  const int64_t *step_ptr, int64_t M, const int32_t *node,
+                                  const int32_t *label, int32_t S, int32_t *mat, int32_t *lab_w,
+                                  int32_t *err);
 
 }  // namespace pardnn

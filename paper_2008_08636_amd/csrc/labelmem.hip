@@ -159,7 +159,85 @@ __global__ void k_bp_fill(int32_t V, int32_t P, const int32_t *base, const int32
     }
 }
 
+// Labels of successive placements straight into the sweep's slice-major
+// workspace lab_w[slice][v][s] (v level-major, placement p = slice * S + s).
+// `mat` holds, per original node row, the index of the last move at each step
+// (k_bp_mark) or -1. A workgroup owns 64 consecutive level-major nodes and
+// walks the placements in chunks of 64: one wave scans one node row chunk
+// (coalesced), carrying the running label across chunks, into an LDS tile
+// that is then written out slice by slice as contiguous runs.
+template <int S>
+__global__ __launch_bounds__(256) void k_moves_to_slices(int32_t V, int32_t P,
+                                                         const int32_t *order,
+                                                         const int32_t *base,
+                                                         const int32_t *label,
+                                                         const int32_t *mat, int32_t *lab_w) {
+    constexpr int TV = 64, TP = 64;
+    __shared__ int32_t tile[TV][TP + 1];
+    __shared__ int32_t carry[TV];
+    __shared__ int32_t rows[TV];
+    const int lane = lane_id(), w = wave_id();
+    const int32_t v0 = blockIdx.x * TV;
+    const int32_t n_slices = (P + S - 1) / S;
+    for (int r = threadIdx.x; r < TV; r += 256) {
+        const int32_t v = v0 + r;
+        rows[r] = v < V ? order[v] : -1;
+        carry[r] = v < V ? base[order[v]] : 0;
+    }
+    __syncthreads();
+    for (int32_t c0 = 0; c0 < n_slices * S; c0 += TP) {
+        for (int r = w; r < TV; r += 256 / kWave) {
+            const int32_t o = rows[r];
+            const int32_t p = c0 + lane;
+            const int32_t m = (o >= 0 && p < P) ? mat[(int64_t)o * P + p] : -1;
+            int32_t last = m >= 0 ? lane : -1;
+#pragma unroll
+            for (int off = 1; off < kWave; off <<= 1) {
+                int32_t y = __shfl_up(last, off, kWave);
+                if (lane >= off) last = max(last, y);
+            }
+            const int32_t mm = __shfl(m, last < 0 ? 0 : last, kWave);
+            const int32_t val = last >= 0 ? label[mm] : carry[r];
+            tile[r][lane] = val;
+            const int32_t tail = __shfl(val, kWave - 1, kWave);
+            if (lane == 0) carry[r] = tail;
+        }
+        __syncthreads();
+        const int32_t sl0 = c0 / S;
+        const int n_sl = min(TP / S, n_slices - sl0);
+        for (int i = threadIdx.x; i < n_sl * TV * S; i += 256) {
+            const int sl = i / (TV * S), j = i % (TV * S);
+            const int r = j / S, s2 = j % S;
+            const int32_t v = v0 + r;
+            if (v < V) lab_w[((int64_t)(sl0 + sl) * V + v) * S + s2] = tile[r][sl * S + s2];
+        }
+        __syncthreads();
+    }
+}
+
 }  // namespace
+
+hipError_t launch_moves_to_slices(const Graph &g, const int32_t *base, int32_t P,
+                                  const int64_t *step_ptr, int64_t M, const int32_t *node,
+                                  const int32_t *label, int32_t S, int32_t *mat, int32_t *lab_w,
+                                  int32_t *err) {
+    if (g.V == 0 || P == 0) return hipSuccess;
+    hipError_t e = launch_fill_i32(mat, (int64_t)g.V * P, -1, g.stream);
+    if (e != hipSuccess) return e;
+    if (M > 0) {
+        k_bp_mark<<<grid_for(M, kBlock), kBlock, 0, g.stream>>>(M, P, step_ptr, node, g.V, mat,
+                                                                 err);
+        if ((e = hipGetLastError()) != hipSuccess) return e;
+    }
+    const unsigned grid = (unsigned)((g.V + 63) / 64);
+    if (S == 2)
+        k_moves_to_slices<2><<<grid, 256, 0, g.stream>>>(g.V, P, g.order, base, label, mat, lab_w);
+    else if (S == 4)
+        k_moves_to_slices<4><<<grid, 256, 0, g.stream>>>(g.V, P, g.order, base, label, mat, lab_w);
+    else
+        return hipErrorInvalidValue;
+    return hipGetLastError();
+}
 
 hipError_t launch_label_memory(const Graph &g, const int32_t *placement, int32_t K,
                                const int64_t *capacity, int64_t *label_mem, int64_t *overflow,

@@ -190,6 +190,23 @@ __global__ void k_scatter_lm(int64_t E, const int32_t *src, const int32_t *dst,
     }
 }
 
+__global__ void k_pack_records(int64_t E, int32_t V, const int32_t *in_src,
+                               const int32_t *in_dst, const int64_t *in_cost,
+                               const int32_t *out_src, const int32_t *out_dst,
+                               const int64_t *out_cost, const int64_t *comp_lm,
+                               const int64_t *mem_lm, EdgeRec16 *in_rec, EdgeRec16 *out_rec,
+                               NodeRec16 *node_rec) {
+    const int64_t n = E > V ? E : (int64_t)V;
+    for (int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; i < n;
+         i += (int64_t)gridDim.x * blockDim.x) {
+        if (i < E) {
+            in_rec[i] = EdgeRec16{in_src[i], in_dst[i], in_cost[i]};
+            out_rec[i] = EdgeRec16{out_dst[i], out_src[i], out_cost[i]};
+        }
+        if (i < V) node_rec[i] = NodeRec16{comp_lm[i], mem_lm[i]};
+    }
+}
+
 __global__ void k_level_info(int32_t L, const int32_t *level_ptr, const int32_t *in_off,
                              const int32_t *out_off, LevelInfo *linfo) {
     for (int32_t k = blockIdx.x * blockDim.x + threadIdx.x; k <= L; k += gridDim.x * blockDim.x) {
@@ -282,6 +299,13 @@ hipError_t launch_build_lm(Graph &g, int32_t *deg_ws, int32_t *cursor_in, int32_
         k_scatter_lm<<<grid_for(g.E, kBlock), kBlock, 0, g.stream>>>(
             g.E, g.e_src, g.e_dst, g.e_cost, g.rank, cursor_in, cursor_out, g.in_src, g.in_dst,
             g.in_cost, g.out_src, g.out_dst, g.out_dst_orig, g.out_cost);
+        if ((err = hipGetLastError()) != hipSuccess) return err;
+    }
+    const int64_t nrec = g.E > g.V ? g.E : (int64_t)g.V;
+    if (nrec > 0) {
+        k_pack_records<<<grid_for(nrec, kBlock), kBlock, 0, g.stream>>>(
+            g.E, g.V, g.in_src, g.in_dst, g.in_cost, g.out_src, g.out_dst, g.out_cost, g.comp_lm,
+            g.mem_lm, g.in_rec, g.out_rec, g.node_rec);
         if ((err = hipGetLastError()) != hipSuccess) return err;
     }
     k_level_info<<<grid_for(g.L + 1, kBlock), kBlock, 0, g.stream>>>(g.L, g.level_ptr, g.in_off,

@@ -37,6 +37,9 @@ namespace pardnn {
 namespace {
 
 constexpr int kBlock = 256;
+constexpr int kChaseWindow = 2048;  // links staged per wave
+constexpr int kFinishLds = 4 * kChaseWindow * 4 > 2 * 32 * 65 * 8 ? 4 * kChaseWindow * 4
+                                                                  : 2 * 32 * 65 * 8;
 
 inline unsigned grid_for(int64_t n, int block, int cap = 65536) {
     int64_t g = (n + block - 1) / block;
@@ -110,46 +113,78 @@ struct Elem<false> {
     }
 };
 
+// LDS bytes of one sweep workgroup.
+template <int S, int ACC, bool PACKED>
+constexpr size_t sweep_lds_bytes() {
+    using ET = typename Elem<PACKED>::T;
+    return (size_t)2 * ACC * S * 8          // acc (double-buffered by step parity)
+           + (size_t)ACC * S * 8            // nacc
+           + (size_t)2 * ACC * S * 4        // slab
+           + (size_t)2 * ACC * S * sizeof(ET)  // nbuf
+           + (size_t)kBinsCap * 8 + (size_t)kLevelWindow * sizeof(LevelInfo);
+}
+
 // One direction of the sweep for slice `slice`. FWD: t levels; else b levels.
-template <int S, int T, bool FWD, bool PACKED>
+//
+// Per narrow level k (at most ACC nodes) a step is:
+//   edge phase: every (edge, slot) task folds its candidate into acc[k & 1]
+//     with an LDS max. The neighbour value comes from nbuf (LDS) when the
+//     neighbour lies on the level computed in the previous step, or from a
+//     register loaded one step earlier when it lies further back. So no global
+//     load sits on the critical path of a narrow level.
+//   barrier
+//   node phase: each (node, slot) reads its accumulator, writes its value to
+//     the workspace (global) and to nbuf (for the next level), and clears the
+//     accumulators of the previous level.
+//   barrier
+// While a step runs, the records of level k+2 and the far neighbour values
+// of level k+1 are loaded into registers. Two edge tasks per thread are
+// pipelined this way; further ones (levels with more than 2T tasks) load
+// inline. Levels wider than ACC nodes go through a chunked path without
+// pipelining.
+//
+// The b direction must also pick, among the successors reaching the max, the
+// one with the smallest original id (the next node of the critical path).
+// PACKED folds that into the max itself: key = (value << ob) | (omax - orig),
+// and the thread holding the winning key writes the successor link. Otherwise
+// a second LDS phase takes the min over the tied successors.
+template <int S, int T, int ACC, bool FWD, bool PACKED>
 __device__ void sweep_dir(const SweepArgs &a, int32_t slice, char *smem) {
+    constexpr bool DIRECT = S == 1;  // one placement: write tl/bl straight to the caller
     using EL = Elem<PACKED>;
     using ET = typename EL::T;
-    constexpr int ACC = kSweepAccNodes;  // nodes per accumulator chunk
-    constexpr int CH = kLevelWindow;     // level boundaries staged in LDS
-    long long *acc = reinterpret_cast<long long *>(smem);                              // [ACC*S]
-    unsigned long long *nacc = reinterpret_cast<unsigned long long *>(acc + ACC * S);  // [ACC*S]
-    int32_t *slab = reinterpret_cast<int32_t *>(nacc + ACC * S);                       // [2][ACC*S]
-    long long *bins = reinterpret_cast<long long *>(slab + 2 * ACC * S);               // [kBinsCap]
-    LevelInfo *s_li = reinterpret_cast<LevelInfo *>(bins + kBinsCap);                  // [CH]
+    constexpr int CH = kLevelWindow;
+    long long *acc = reinterpret_cast<long long *>(smem);                                  // [2][ACC*S]
+    unsigned long long *nacc = reinterpret_cast<unsigned long long *>(acc + 2 * ACC * S);  // [ACC*S]
+    int32_t *slab = reinterpret_cast<int32_t *>(nacc + ACC * S);                           // [2][ACC*S]
+    ET *nbuf = reinterpret_cast<ET *>(slab + 2 * ACC * S);                                 // [2][ACC*S]
+    long long *bins = reinterpret_cast<long long *>(nbuf + 2 * ACC * S);                   // [kBinsCap]
+    LevelInfo *s_li = reinterpret_cast<LevelInfo *>(bins + kBinsCap);                      // [CH]
     __shared__ long long s_m[S];
     __shared__ int s_start[S];
 
     const int tid = threadIdx.x;
     const int s0 = tid % S;
     const int lb = a.lb;
+    const int ob = PACKED && !FWD ? a.ob : 0;
+    const long long omax = (1ll << ob) - 1;
     const int32_t V = a.V, L = a.L, P = a.P;
     const int64_t wbase = (int64_t)slice * V * S;
     const int32_t *lab = a.lab_w + wbase;
     ET *vals = reinterpret_cast<ET *>(FWD ? a.ftl : a.bll) + wbase;
-    const int32_t *e_nb = FWD ? a.in_src : a.out_dst;
-    const int32_t *e_own = FWD ? a.in_dst : a.out_src;
-    const int64_t *e_cost = FWD ? a.in_cost : a.out_cost;
+    const EdgeRec16 *erec = FWD ? a.in_rec : a.out_rec;
     const int32_t *off = FWD ? a.in_off : a.out_off;
     const bool want_nx = !FWD && a.nx_w != nullptr;
+    const bool tie_phase = want_nx && !PACKED;
     const bool want_bins = FWD && a.K > 0;
     const bool lds_bins = want_bins && a.K * S <= kBinsCap;
     const int32_t p0 = slice * S;
 
-    for (int i = tid; i < ACC * S; i += T) {
-        acc[i] = 0;
-        nacc[i] = ~0ull;
-    }
+    for (int i = tid; i < 2 * ACC * S; i += T) acc[i] = 0;
+    for (int i = tid; i < ACC * S; i += T) nacc[i] = ~0ull;
     if (lds_bins)
         for (int i = tid; i < a.K * S; i += T) bins[i] = 0;
 
-    // Records prefetched for pass 0 of a level: one edge task and one node task
-    // per thread. Indices are clamped into range so the loads never branch.
     struct EdgeRec {
         int32_t nb, own, nbo;
         int64_t c;
@@ -158,25 +193,32 @@ __device__ void sweep_dir(const SweepArgs &a, int32_t slice, char *smem) {
         int32_t ord, lab;
         int64_t comp, mem;
     };
-    EdgeRec ce{0, 0, 0, 0}, ne{0, 0, 0, 0};
-    NodeRec cn{0, 0, 0, 0}, nn{0, 0, 0, 0};
+    struct Recs {        // prefetched records of one level: two edge tasks, one node task
+        EdgeRec e0, e1;
+        NodeRec n;
+    };
 
     auto level_at = [&](int32_t step) { return FWD ? step : L - 1 - step; };
     auto e_lo = [&](const LevelInfo &li) { return FWD ? li.in_e_lo : li.out_e_lo; };
 
+    // one 16-byte load per edge record (plus the successor's id for b)
     auto load_edge = [&](int32_t e) {
+        const EdgeRec16 x = erec[e];
         EdgeRec r;
-        r.nb = e_nb[e];
-        r.own = e_own[e];
-        r.c = e_cost[e];
+        r.nb = x.nb;
+        r.own = x.own;
+        r.c = x.cost;
         r.nbo = FWD ? 0 : a.out_dst_orig[e];
         return r;
     };
+    // one 16-byte load of the node constants, the label, and (single
+    // placement only) the node's original id for the direct outputs
     auto load_node = [&](int32_t v, int s) {
+        const NodeRec16 x = a.node_rec[v];
         NodeRec r;
-        r.ord = a.order[v];
-        r.comp = a.comp_lm[v];
-        r.mem = FWD ? a.mem_lm[v] : 0;
+        r.ord = DIRECT ? a.order[v] : 0;
+        r.comp = x.comp;
+        r.mem = x.mem;
         r.lab = lab[(int64_t)v * S + s];
         return r;
     };
@@ -191,36 +233,44 @@ __device__ void sweep_dir(const SweepArgs &a, int32_t slice, char *smem) {
             if (c0 + i <= L) s_li[i] = a.linfo[c0 + i];
         __syncthreads();
     };
-    auto LI = [&](int32_t k) -> const LevelInfo & { return s_li[k - c0]; };
+    auto LI = [&](int32_t k) -> LevelInfo { return s_li[k - c0]; };
 
-    // pass-0 loads of level k (boundaries li, ln), addresses clamped
-    auto prefetch = [&](const LevelInfo &li, const LevelInfo &ln, EdgeRec &e, NodeRec &n) {
+    // records of a level (boundaries li, ln), addresses clamped into range
+    auto prefetch = [&](const LevelInfo &li, const LevelInfo &ln, Recs &r) {
         const int32_t ea = e_lo(li), eb = e_lo(ln);
-        const int32_t ei = tid < (eb - ea) * S ? ea + tid / S : (eb > ea ? ea : 0);
-        const int32_t vi = tid < (ln.node_lo - li.node_lo) * S ? li.node_lo + tid / S : li.node_lo;
-        e = load_edge(a.E > 0 ? ei : 0);
-        n = load_node(min(vi, V - 1), s0);
+        const int32_t nt = (eb - ea) * S;
+        const int32_t e0 = tid < nt ? ea + tid / S : 0;
+        const int32_t e1 = tid + T < nt ? ea + (tid + T) / S : 0;
+        const int32_t vi = tid < (ln.node_lo - li.node_lo) * S ? li.node_lo + tid / S : 0;
+        r.e0 = load_edge(a.E > 0 ? e0 : 0);
+        r.e1 = load_edge(a.E > 0 ? e1 : 0);
+        r.n = load_node(min(vi, V - 1), s0);
     };
-    // own labels of a narrow level into slab[buf]; pass 0 comes from registers
     auto fill_labels = [&](const LevelInfo &li, const LevelInfo &ln, int buf, const NodeRec &n) {
         const int32_t lo = li.node_lo, w = ln.node_lo - lo;
         int32_t *sl = slab + buf * ACC * S;
         if (tid < w * S) sl[tid] = n.lab;
         for (int32_t i = tid + T; i < w * S; i += T) sl[i] = lab[(int64_t)lo * S + i];
     };
-
     auto cand = [&](const ET &g, int32_t own_lab, int64_t c) {
         return EL::val(g, lb) + (EL::lab(g, lb) != own_lab ? c : 0);
     };
+    // accumulator key of a candidate (b, PACKED: with the successor's id)
+    auto akey = [&](int64_t cv, int32_t nbo) -> long long {
+        return PACKED && !FWD ? (cv << ob) | (omax - nbo) : cv;
+    };
+    auto akey_val = [&](long long key) -> int64_t { return PACKED && !FWD ? key >> ob : key; };
 
-    auto finish_node = [&](int32_t v, int s, int32_t slot, const NodeRec &n) {
-        const int64_t t = acc[slot];
-        acc[slot] = 0;
+    auto finish_node = [&](int32_t v, int s, int32_t slot, long long key, const NodeRec &n,
+                           ET *nb_out) {
+        const int64_t t = akey_val(key);
         const int32_t p = p0 + s;
         if (FWD) {
-            vals[(int64_t)v * S + s] = EL::make(t + n.comp, n.lab, lb);
+            const ET out = EL::make(t + n.comp, n.lab, lb);
+            vals[(int64_t)v * S + s] = out;
+            if (nb_out) nb_out[slot] = out;
             if (p < P) {
-                if (a.direct) a.tl_out[(int64_t)n.ord * P + p] = t;
+                if (DIRECT) a.tl_out[(int64_t)n.ord * P + p] = t;
                 if (want_bins) {
                     const int32_t l = n.lab;
                     if (l < 0 || l >= a.K)
@@ -234,130 +284,214 @@ __device__ void sweep_dir(const SweepArgs &a, int32_t slice, char *smem) {
             }
         } else {
             const int64_t b = n.comp + t;
-            vals[(int64_t)v * S + s] = EL::make(b, n.lab, lb);
-            if (a.direct && p < P) a.bl_out[(int64_t)n.ord * P + p] = b;
+            const ET out = EL::make(b, n.lab, lb);
+            vals[(int64_t)v * S + s] = out;
+            if (nb_out) nb_out[slot] = out;
+            if (DIRECT && p < P) a.bl_out[(int64_t)n.ord * P + p] = b;
             if (want_nx) {
-                const unsigned long long key = nacc[slot];
-                nacc[slot] = ~0ull;
-                a.nx_w[wbase + (int64_t)v * S + s] =
-                    key == ~0ull ? -1 : (int32_t)(key & 0xffffffffull);
+                if (PACKED) {
+                    if (key == 0) a.nx_w[wbase + (int64_t)v * S + s] = -1;
+                } else {
+                    const unsigned long long k2 = nacc[slot];
+                    nacc[slot] = ~0ull;
+                    a.nx_w[wbase + (int64_t)v * S + s] =
+                        k2 == ~0ull ? -1 : (int32_t)(k2 & 0xffffffffull);
+                }
             }
         }
     };
 
+    // ---- prologue: records of the first two levels, labels of the first ----
+    Recs r0{}, r1{}, r2{};
+    ET fv0{}, fv1{}, fn0{}, fn1{};  // far neighbour values: current level / next level
+    bool h0 = false, h1 = false, hn0 = false, hn1 = false;
+    LevelInfo li{}, ln{}, lin{}, lnn{};
     if (L > 0) {
-        const int32_t k0 = level_at(0);
-        stage(k0, k0 + 1);
-        const LevelInfo li = LI(k0), ln = LI(k0 + 1);
-        if (ln.node_lo - li.node_lo <= ACC) {
-            prefetch(li, ln, ce, cn);
-            fill_labels(li, ln, 0, cn);
-        }
+        const int32_t k0 = level_at(0), k1 = L > 1 ? level_at(1) : k0;
+        stage(min(k0, k1), max(k0, k1) + 1);
+        li = LI(k0);
+        ln = LI(k0 + 1);
+        lin = LI(k1);
+        lnn = LI(k1 + 1);
+        prefetch(li, ln, r0);
+        prefetch(lin, lnn, r1);
+        if (ln.node_lo - li.node_lo <= ACC) fill_labels(li, ln, 0, r0.n);
     }
     __syncthreads();
+    int32_t plo = 0, phi = 0;     // previous level's node range
+    bool prev_in_lds = false;     // previous level's values sit in nbuf[(step - 1) & 1]
 
     for (int32_t step = 0; step < L; step++) {
-        const int32_t k = level_at(step);
         const bool has_next = step + 1 < L;
-        const int32_t kn = has_next ? level_at(step + 1) : k;
-        stage(min(k, kn), max(k, kn) + 1);
+        const int32_t k = level_at(step);
+        const int32_t knn = step + 2 < L ? level_at(step + 2) : (has_next ? level_at(step + 1) : k);
+        stage(min(k, knn), max(k, knn) + 1);
+        const LevelInfo l3 = LI(knn), l4 = LI(knn + 1);
         const int buf = step & 1;
-        const LevelInfo li = LI(k), ln = LI(k + 1);
-        const LevelInfo lin = LI(kn), lnn = LI(kn + 1);
         const int32_t lo = li.node_lo, hi = ln.node_lo;
         const int32_t ea = e_lo(li), eb = e_lo(ln);
+        const int32_t nt = (eb - ea) * S;
+        const int32_t nt_next = (e_lo(lnn) - e_lo(lin)) * S;
         const bool next_narrow = has_next && lnn.node_lo - lin.node_lo <= ACC;
+        long long *accb = acc + buf * ACC * S;
+        long long *accp = acc + (buf ^ 1) * ACC * S;
+        const ET *nprev = nbuf + (buf ^ 1) * ACC * S;
+
+        // neighbour value of a task: far (prefetched), near in LDS, or global
+        auto nval = [&](const EdgeRec &r, int s, bool has_far, const ET &far) -> ET {
+            if (has_far) return far;
+            if (prev_in_lds && r.nb >= plo && r.nb < phi) return nprev[(r.nb - plo) * S + s];
+            return vals[(int64_t)r.nb * S + s];
+        };
 
         if (hi - lo <= ACC) {
-            // ---- narrow level: one chunk, pass 0 prefetched ----
+            // ---- narrow level ----
             const int32_t *sl = slab + buf * ACC * S;
-            const int32_t nt = (eb - ea) * S;
-            const bool ev = tid < nt;
-            const ET g0 = vals[ev ? (int64_t)ce.nb * S + s0 : 0];  // gather, always in range
-            // issued on every path, so the wait for g0 leaves these loads in flight
-            prefetch(lin, lnn, ne, nn);
-            const int32_t slot0 = (ce.own - lo) * S + s0;
-            int64_t c0v = 0;
-            if (ev) {
-                c0v = cand(g0, sl[slot0], ce.c);
-                lds_max_i64(&acc[slot0], c0v);
+            const bool ev0 = tid < nt, ev1 = tid + T < nt;
+            const int sA = s0, sB = (tid + T) % S;
+            long long k0v = 0, k1v = 0;
+            // pass 0/1 neighbours: prefetched register (far, or everything after a
+            // wide level) or the previous level's values in LDS -- no global load
+            const ET l0 = nprev[ev0 && !h0 ? (r0.e0.nb - plo) * S + sA : 0];
+            const ET l1 = nprev[ev1 && !h1 ? (r0.e1.nb - plo) * S + sB : 0];
+            if (ev0) {
+                const ET g = h0 ? fv0 : l0;
+                k0v = akey(cand(g, sl[(r0.e0.own - lo) * S + sA], r0.e0.c), r0.e0.nbo);
+                lds_max_i64(&accb[(r0.e0.own - lo) * S + sA], k0v);
             }
-            for (int32_t i = tid + T; i < nt; i += T) {
+            if (ev1) {
+                const ET g = h1 ? fv1 : l1;
+                k1v = akey(cand(g, sl[(r0.e1.own - lo) * S + sB], r0.e1.c), r0.e1.nbo);
+                lds_max_i64(&accb[(r0.e1.own - lo) * S + sB], k1v);
+            }
+            // next level's far neighbours (final already) and level k+2's records
+            hn0 = has_next && tid < nt_next && (FWD ? r1.e0.nb < lo : r1.e0.nb >= hi);
+            hn1 = has_next && tid + T < nt_next && (FWD ? r1.e1.nb < lo : r1.e1.nb >= hi);
+            fn0 = vals[hn0 ? (int64_t)r1.e0.nb * S + s0 : 0];
+            fn1 = vals[hn1 ? (int64_t)r1.e1.nb * S + sB : 0];
+            prefetch(l3, l4, r2);
+            for (int32_t i = tid + 2 * T; i < nt; i += T) {
                 const EdgeRec r = load_edge(ea + i / S);
                 const int s = i % S;
-                const ET g = vals[(int64_t)r.nb * S + s];
-                lds_max_i64(&acc[(r.own - lo) * S + s], cand(g, sl[(r.own - lo) * S + s], r.c));
+                const ET g = nval(r, s, false, fn0);
+                lds_max_i64(&accb[(r.own - lo) * S + s],
+                            akey(cand(g, sl[(r.own - lo) * S + s], r.c), r.nbo));
             }
             __syncthreads();
-            if (want_nx) {
-                if (ev && c0v == acc[slot0])
-                    lds_min_u64(&nacc[slot0],
-                                ((unsigned long long)(uint32_t)ce.nbo << 32) | (uint32_t)ce.nb);
-                for (int32_t i = tid + T; i < nt; i += T) {
+            if (tie_phase) {
+                if (ev0 && k0v == accb[(r0.e0.own - lo) * S + sA])
+                    lds_min_u64(&nacc[(r0.e0.own - lo) * S + sA],
+                                ((unsigned long long)(uint32_t)r0.e0.nbo << 32) | (uint32_t)r0.e0.nb);
+                if (ev1 && k1v == accb[(r0.e1.own - lo) * S + sB])
+                    lds_min_u64(&nacc[(r0.e1.own - lo) * S + sB],
+                                ((unsigned long long)(uint32_t)r0.e1.nbo << 32) | (uint32_t)r0.e1.nb);
+                for (int32_t i = tid + 2 * T; i < nt; i += T) {
                     const EdgeRec r = load_edge(ea + i / S);
                     const int s = i % S;
-                    const ET g = vals[(int64_t)r.nb * S + s];
+                    const ET g = nval(r, s, false, fn0);
                     const int32_t slot = (r.own - lo) * S + s;
-                    if (cand(g, sl[slot], r.c) == acc[slot])
+                    if (akey(cand(g, sl[slot], r.c), r.nbo) == accb[slot])
                         lds_min_u64(&nacc[slot],
                                     ((unsigned long long)(uint32_t)r.nbo << 32) | (uint32_t)r.nb);
                 }
                 __syncthreads();
+            } else if (want_nx) {
+                // PACKED b: the task holding the winning key names the successor
+                if (ev0 && k0v == accb[(r0.e0.own - lo) * S + sA])
+                    a.nx_w[wbase + (int64_t)r0.e0.own * S + sA] = r0.e0.nb;
+                if (ev1 && k1v == accb[(r0.e1.own - lo) * S + sB])
+                    a.nx_w[wbase + (int64_t)r0.e1.own * S + sB] = r0.e1.nb;
+                for (int32_t i = tid + 2 * T; i < nt; i += T) {
+                    const EdgeRec r = load_edge(ea + i / S);
+                    const int s = i % S;
+                    const ET g = nval(r, s, false, fn0);
+                    const int32_t slot = (r.own - lo) * S + s;
+                    if (akey(cand(g, sl[slot], r.c), r.nbo) == accb[slot])
+                        a.nx_w[wbase + (int64_t)r.own * S + s] = r.nb;
+                }
             }
+            ET *nb_out = nbuf + buf * ACC * S;
             const int32_t nnt = (hi - lo) * S;
-            if (tid < nnt) finish_node(lo + tid / S, s0, tid, cn);
+            if (tid < nnt) finish_node(lo + tid / S, s0, tid, accb[tid], r0.n, nb_out);
             for (int32_t i = tid + T; i < nnt; i += T) {
                 const int s = i % S;
                 const int32_t v = lo + i / S;
                 NodeRec r = load_node(v, s);
                 r.lab = sl[i];
-                finish_node(v, s, i, r);
+                finish_node(v, s, i, accb[i], r, nb_out);
             }
-            if (next_narrow) fill_labels(lin, lnn, buf ^ 1, nn);
+            // clear the previous level's accumulators (used again at step + 1)
+            for (int32_t i = tid; i < (phi - plo) * S && phi - plo <= ACC; i += T) accp[i] = 0;
+            if (next_narrow) fill_labels(lin, lnn, buf ^ 1, r1.n);
             __syncthreads();
+            prev_in_lds = true;
         } else {
             // ---- wide level: chunks of ACC nodes, loads inline ----
+            if (phi - plo <= ACC)
+                for (int32_t i = tid; i < (phi - plo) * S; i += T) accp[i] = 0;
+            __syncthreads();
             for (int32_t cn0 = lo; cn0 < hi; cn0 += ACC) {
                 const int32_t cn1 = min(hi, cn0 + ACC);
                 const int32_t cea = cn0 == lo ? ea : off[cn0];
                 const int32_t ceb = cn1 == hi ? eb : off[cn1];
-                const int32_t nt = (ceb - cea) * S;
-                for (int32_t i = tid; i < nt; i += T) {
+                const int32_t cnt = (ceb - cea) * S;
+                for (int32_t i = tid; i < cnt; i += T) {
                     const EdgeRec r = load_edge(cea + i / S);
                     const int s = i % S;
-                    const ET g = vals[(int64_t)r.nb * S + s];
-                    lds_max_i64(&acc[(r.own - cn0) * S + s],
-                                cand(g, lab[(int64_t)r.own * S + s], r.c));
+                    const ET g = nval(r, s, false, fn0);
+                    lds_max_i64(&accb[(r.own - cn0) * S + s],
+                                akey(cand(g, lab[(int64_t)r.own * S + s], r.c), r.nbo));
                 }
                 __syncthreads();
                 if (want_nx) {
-                    for (int32_t i = tid; i < nt; i += T) {
+                    for (int32_t i = tid; i < cnt; i += T) {
                         const EdgeRec r = load_edge(cea + i / S);
                         const int s = i % S;
-                        const ET g = vals[(int64_t)r.nb * S + s];
+                        const ET g = nval(r, s, false, fn0);
                         const int32_t slot = (r.own - cn0) * S + s;
-                        if (cand(g, lab[(int64_t)r.own * S + s], r.c) == acc[slot])
-                            lds_min_u64(&nacc[slot], ((unsigned long long)(uint32_t)r.nbo << 32) |
-                                                         (uint32_t)r.nb);
+                        if (akey(cand(g, lab[(int64_t)r.own * S + s], r.c), r.nbo) == accb[slot]) {
+                            if (tie_phase)
+                                lds_min_u64(&nacc[slot],
+                                            ((unsigned long long)(uint32_t)r.nbo << 32) | (uint32_t)r.nb);
+                            else
+                                a.nx_w[wbase + (int64_t)r.own * S + s] = r.nb;
+                        }
                     }
-                    __syncthreads();
+                    if (tie_phase) __syncthreads();
                 }
-                const int32_t nnt = (cn1 - cn0) * S;
-                for (int32_t i = tid; i < nnt; i += T) {
+                const int32_t cnn = (cn1 - cn0) * S;
+                for (int32_t i = tid; i < cnn; i += T) {
                     const int s = i % S;
                     const int32_t v = cn0 + i / S;
-                    finish_node(v, s, i, load_node(v, s));
+                    finish_node(v, s, i, accb[i], load_node(v, s), nullptr);
                 }
                 __syncthreads();
-            }
-            if (next_narrow) {
-                prefetch(lin, lnn, ne, nn);
-                fill_labels(lin, lnn, buf ^ 1, nn);
+                for (int32_t i = tid; i < cnn; i += T) accb[i] = 0;
                 __syncthreads();
             }
+            // the wide level is final now: fetch every neighbour of the next
+            // level's pipelined tasks, near ones included
+            hn0 = has_next && tid < nt_next;
+            hn1 = has_next && tid + T < nt_next;
+            fn0 = vals[hn0 ? (int64_t)r1.e0.nb * S + s0 : 0];
+            fn1 = vals[hn1 ? (int64_t)r1.e1.nb * S + (tid + T) % S : 0];
+            prefetch(l3, l4, r2);
+            if (next_narrow) fill_labels(lin, lnn, buf ^ 1, r1.n);
+            __syncthreads();
+            prev_in_lds = false;
         }
-        ce = ne;
-        cn = nn;
+        plo = lo;
+        phi = hi;
+        r0 = r1;
+        r1 = r2;
+        fv0 = fn0;
+        fv1 = fn1;
+        h0 = hn0;
+        h1 = hn1;
+        li = lin;
+        ln = lnn;
+        lin = l3;
+        lnn = l4;
     }
 
     if (FWD) {
@@ -390,20 +524,14 @@ __device__ void sweep_dir(const SweepArgs &a, int32_t slice, char *smem) {
     }
 }
 
-template <int S, int T, bool PACKED>
+template <int S, int T, int ACC, bool PACKED>
 __global__ __launch_bounds__(T) void k_sweep(SweepArgs a) {
     extern __shared__ __align__(16) char smem[];
     const int32_t n_slices = (a.P + S - 1) / S;
     if ((int32_t)blockIdx.x < n_slices)
-        sweep_dir<S, T, false, PACKED>(a, blockIdx.x, smem);
+        sweep_dir<S, T, ACC, false, PACKED>(a, blockIdx.x, smem);
     else
-        sweep_dir<S, T, true, PACKED>(a, blockIdx.x - n_slices, smem);
-}
-
-template <int S>
-constexpr size_t sweep_lds_bytes() {
-    return (size_t)kSweepAccNodes * S * 8 * 2 + (size_t)kSweepAccNodes * S * 4 * 2 +
-           (size_t)kBinsCap * 8 + (size_t)kLevelWindow * sizeof(LevelInfo);
+        sweep_dir<S, T, ACC, true, PACKED>(a, blockIdx.x - n_slices, smem);
 }
 
 // Outputs in the caller's layout: tl, bl [V][P] in original ids and the
@@ -411,14 +539,15 @@ constexpr size_t sweep_lds_bytes() {
 // through LDS so that the slice-major workspace is read contiguously and each
 // output row order[v] is written as one contiguous 512-byte run.
 template <int S, bool PACKED>
-__global__ __launch_bounds__(256) void k_emit(SweepArgs a, uint8_t *crit) {
+__device__ void emit_tile(const SweepArgs &a, uint8_t *crit, int32_t bx, int32_t by,
+                          char *smem) {
     using EL = Elem<PACKED>;
     using ET = typename EL::T;
     constexpr int TV = 32, TP = 64;
-    __shared__ long long t_tl[TV][TP + 1];
-    __shared__ long long t_bl[TV][TP + 1];
+    long long(*t_tl)[TP + 1] = reinterpret_cast<long long(*)[TP + 1]>(smem);
+    long long(*t_bl)[TP + 1] = reinterpret_cast<long long(*)[TP + 1]>(smem + TV * (TP + 1) * 8);
     const int32_t V = a.V, P = a.P;
-    const int32_t v0 = blockIdx.x * TV, q0 = blockIdx.y * TP;
+    const int32_t v0 = bx * TV, q0 = by * TP;
     const int32_t sl0 = q0 / S;
     const int n_sl = min(TP / S, (P + S - 1) / S - sl0);
     const ET *ft = reinterpret_cast<const ET *>(a.ftl);
@@ -449,49 +578,66 @@ __global__ __launch_bounds__(256) void k_emit(SweepArgs a, uint8_t *crit) {
 
 // One wave per placement walks the chosen-successor links from the path
 // start. Links point to strictly later levels (larger level-major ids), so the
-// wave stages a window of its links in LDS with coalesced loads, lane 0
-// chases inside the window, and the window moves forward when the walk leaves
-// it.
+// wave stages a window of its links in LDS with coalesced loads and walks
+// inside the window (uniformly across the wave); the window moves forward when
+// the walk leaves it. Lane i keeps the (i mod 64)-th path node and the wave
+// writes 64 original ids at a time.
 template <int S>
-__global__ __launch_bounds__(256) void k_chase_batch(int32_t V, int32_t P, const int32_t *order,
-                                                     const int32_t *nx_w, const int32_t *start,
-                                                     int32_t *path, int32_t stride,
-                                                     int32_t *path_len) {
-    constexpr int kWin = 2048;
-    __shared__ int32_t win[256 / kWave][kWin];
-    const int lane = lane_id(), w = wave_id();
-    const int32_t p = blockIdx.x * (256 / kWave) + w;
-    if (p >= P) return;
+__device__ void chase_wave(const SweepArgs &a, int32_t p, int32_t *path, int32_t stride,
+                           int32_t *path_len, int32_t *win) {
+    constexpr int kWin = kChaseWindow;
+    const int lane = lane_id();
+    const int32_t V = a.V;
     const int32_t slice = p / S, s = p % S;
-    const int32_t *nx = nx_w + (int64_t)slice * V * S;
+    const int32_t *nx = a.nx_w + (int64_t)slice * V * S;
     int32_t *out = path + (int64_t)p * stride;
-    int32_t cur = start[p], len = 0, mine = -1;
-    // The walk is uniform across the wave; lane i keeps the (i mod 64)-th path
-    // node and the wave writes 64 original ids at a time.
+    int32_t cur = a.start[p], len = 0, mine = -1;
     while (cur >= 0) {
         const int32_t base = cur;
         for (int i = lane; i < kWin; i += kWave)
-            win[w][i] = base + i < V ? nx[(int64_t)(base + i) * S + s] : -1;
+            win[i] = base + i < V ? nx[(int64_t)(base + i) * S + s] : -1;
         __builtin_amdgcn_wave_barrier();
         int32_t c = base;
         while (c >= base && c < base + kWin) {
             if ((len & (kWave - 1)) == lane) mine = c;
             len++;
-            if ((len & (kWave - 1)) == 0) out[len - kWave + lane] = order[mine];
-            const int32_t n = win[w][c - base];
+            if ((len & (kWave - 1)) == 0) out[len - kWave + lane] = a.order[mine];
+            const int32_t n = win[c - base];
             c = n > c ? n : -1;  // links go to strictly later levels
         }
         cur = c;
         __builtin_amdgcn_wave_barrier();
     }
     const int32_t r = len & (kWave - 1);
-    if (lane < r) out[len - r + lane] = order[mine];
+    if (lane < r) out[len - r + lane] = a.order[mine];
     if (lane == 0) path_len[p] = len;
 }
 
+// After the sweeps: workgroups [0, n_chase) walk critical paths (one wave per
+// placement, latency-bound), the rest emit output tiles (bandwidth-bound), so
+// the two overlap in one launch.
+template <int S, bool PACKED>
+__global__ __launch_bounds__(256) void k_finish(SweepArgs a, uint8_t *crit, int32_t *path,
+                                                int32_t stride, int32_t *path_len,
+                                                int32_t n_chase, int32_t tiles_x) {
+    __shared__ __align__(16) char smem[kFinishLds];
+    if ((int32_t)blockIdx.x < n_chase) {
+        const int w = wave_id();
+        const int32_t p = blockIdx.x * (256 / kWave) + w;
+        if (p < a.P)
+            chase_wave<S>(a, p, path, stride, path_len,
+                          reinterpret_cast<int32_t *>(smem) + w * kChaseWindow);
+        return;
+    }
+    const int32_t t = blockIdx.x - n_chase;
+    emit_tile<S, PACKED>(a, crit, t % tiles_x, t / tiles_x, smem);
+}
+
 constexpr int kSingleThreads = 512;
+constexpr int kSingleAcc = 768;
 constexpr int kBatchSlots = 2;
 constexpr int kBatchThreads = 256;
+constexpr int kBatchAcc = 256;
 
 }  // namespace
 
@@ -520,44 +666,37 @@ hipError_t launch_sweep(const SweepArgs &a, int32_t S, hipStream_t s) {
     if (n_slices == 0) return hipSuccess;
     const bool packed = a.lb > 0;
     if (S == 1 && !packed) {
-        k_sweep<1, kSingleThreads, false>
-            <<<2 * n_slices, kSingleThreads, sweep_lds_bytes<1>(), s>>>(a);
+        constexpr size_t lds = sweep_lds_bytes<1, kSingleAcc, false>();
+        k_sweep<1, kSingleThreads, kSingleAcc, false><<<2 * n_slices, kSingleThreads, lds, s>>>(a);
     } else if (S == kBatchSlots && packed) {
-        k_sweep<kBatchSlots, kBatchThreads, true>
-            <<<2 * n_slices, kBatchThreads, sweep_lds_bytes<kBatchSlots>(), s>>>(a);
+        constexpr size_t lds = sweep_lds_bytes<kBatchSlots, kBatchAcc, true>();
+        k_sweep<kBatchSlots, kBatchThreads, kBatchAcc, true>
+            <<<2 * n_slices, kBatchThreads, lds, s>>>(a);
     } else if (S == kBatchSlots && !packed) {
-        k_sweep<kBatchSlots, kBatchThreads, false>
-            <<<2 * n_slices, kBatchThreads, sweep_lds_bytes<kBatchSlots>(), s>>>(a);
+        constexpr size_t lds = sweep_lds_bytes<kBatchSlots, kBatchAcc, false>();
+        k_sweep<kBatchSlots, kBatchThreads, kBatchAcc, false>
+            <<<2 * n_slices, kBatchThreads, lds, s>>>(a);
     } else {
         return hipErrorInvalidValue;
     }
     return hipGetLastError();
 }
 
-hipError_t launch_emit(const SweepArgs &a, int32_t S, uint8_t *crit, hipStream_t s) {
-    if ((int64_t)a.V * a.P == 0) return hipSuccess;
-    if (S != kBatchSlots) return hipErrorInvalidValue;
-    dim3 grid((a.V + 31) / 32, (a.P + 63) / 64);
-    if (a.lb > 0)
-        k_emit<kBatchSlots, true><<<grid, 256, 0, s>>>(a, crit);
-    else
-        k_emit<kBatchSlots, false><<<grid, 256, 0, s>>>(a, crit);
-    return hipGetLastError();
-}
-
-hipError_t launch_chase_batch(const SweepArgs &a, int32_t S, const int32_t *order, int32_t *path,
-                              int32_t stride, int32_t *path_len, hipStream_t s) {
+hipError_t launch_finish(const SweepArgs &a, int32_t S, uint8_t *crit, int32_t *path,
+                         int32_t stride, int32_t *path_len, hipStream_t s) {
     if (a.P == 0) return hipSuccess;
-    const int per_block = 256 / kWave;
-    const unsigned grid = (unsigned)((a.P + per_block - 1) / per_block);
-    if (S == 1)
-        k_chase_batch<1><<<grid, 256, 0, s>>>(a.V, a.P, order, a.nx_w, a.start, path, stride,
-                                              path_len);
-    else if (S == kBatchSlots)
-        k_chase_batch<kBatchSlots><<<grid, 256, 0, s>>>(a.V, a.P, order, a.nx_w, a.start, path,
-                                                        stride, path_len);
+    if (S != kBatchSlots) return hipErrorInvalidValue;
+    const int32_t n_chase = path != nullptr ? (a.P + 3) / 4 : 0;
+    const int32_t tiles_x = (a.V + 31) / 32, tiles_y = (a.P + 63) / 64;
+    const int64_t blocks = n_chase + (int64_t)tiles_x * tiles_y;
+    if (blocks == 0) return hipSuccess;
+    if (blocks > INT32_MAX) return hipErrorInvalidValue;
+    if (a.lb > 0)
+        k_finish<kBatchSlots, true><<<(unsigned)blocks, 256, 0, s>>>(a, crit, path, stride,
+                                                                     path_len, n_chase, tiles_x);
     else
-        return hipErrorInvalidValue;
+        k_finish<kBatchSlots, false><<<(unsigned)blocks, 256, 0, s>>>(a, crit, path, stride,
+                                                                      path_len, n_chase, tiles_x);
     return hipGetLastError();
 }
 

@@ -316,17 +316,48 @@ def test_batch_small_graphs(P):
         G.close()
 
 
+def test_evaluate_moves_small(P):
+    """The fused moves entry point equals build_placements + evaluate_batch
+    and the oracle, with repeated nodes, an empty step and an odd count."""
+    g = cfg(0)
+    say("evaluate_moves small")
+    sched = W.config4_moves(g, n_place=53, frac=0.05, seed=5)
+    node = sched.node.copy()
+    node[sched.ptr[7] + 2] = node[sched.ptr[7]]
+    ptr = sched.ptr.copy()
+    ptr[10] = ptr[9]
+    sched2 = W.MoveSchedule(sched.base, ptr, node, sched.label, sched.n_labels)
+    G = P.Graph(g.n_nodes, g.src, g.dst, g.comp, g.edge_cost, g.mem)
+    args = (dev(sched2.base, torch.int32), dev(ptr, torch.int64), dev(node, torch.int32),
+            dev(sched2.label, torch.int32))
+    out = G.evaluate_moves(*args, g.n_labels, dev(g.capacity, torch.int64))
+    torch.cuda.synchronize()
+    got = {k: v.cpu().numpy() for k, v in out.items()}
+    pl = W.materialize_placements(sched2).T.copy()
+    check_batch(g, pl, got, range(53))
+    ref = run_batch(P, G, pl, g)
+    for k in ref:
+        assert (ref[k] == got[k]).all(), k
+    with pytest.raises(P.PardnnError) as e:
+        bad = node.copy()
+        bad[3] = g.n_nodes + 7
+        G.evaluate_moves(args[0], args[1], dev(bad, torch.int32), args[3], g.n_labels)
+    assert e.value.status == P.E_INVAL
+    G.close()
+
+
 def test_c4_refinement_loop_full_size(P):
     """The 1000-placement refinement loop on the transformer graph, in the
-    launch configuration the benchmark times; sampled placements against the
-    oracle, properties on all of them."""
+    launch configuration the benchmark times (pardnn_evaluate_moves); sampled
+    placements against the oracle, properties on all of them."""
     g = cfg(2)
     say(f"config4 full size V={g.n_nodes} P=1000")
     sched = W.config4_moves(g, n_place=1000)
     G = P.Graph(g.n_nodes, g.src, g.dst, g.comp, g.edge_cost, g.mem)
-    pl = G.build_placements(dev(sched.base, torch.int32), dev(sched.ptr, torch.int64),
-                            dev(sched.node, torch.int32), dev(sched.label, torch.int32))
-    out = G.evaluate_batch(pl, g.n_labels, dev(g.capacity, torch.int64))
+    margs = (dev(sched.base, torch.int32), dev(sched.ptr, torch.int64),
+             dev(sched.node, torch.int32), dev(sched.label, torch.int32))
+    out = G.evaluate_moves(*margs, g.n_labels, dev(g.capacity, torch.int64))
+    pl = G.build_placements(*margs)
     torch.cuda.synchronize()
     cols = [0, 1, 2, 499, 998, 999] + list(range(50, 1000, 97))
     exp_pl = W.materialize_placements(sched)  # [P][V]
