@@ -32,11 +32,20 @@ HBM_PEAK_GBS = 8000.0
 
 
 def algorithmic_bytes_batch(V: int, E: int, P: int) -> int:
-    """Bytes one batched evaluation must move at minimum, by the accounting of
-    the design notes: per placement 24 B per edge (neighbour label + value, for
-    t and b) and 53 B per node; per batch the shared structure, 24 B per edge
-    and 32 B per node."""
+    """Bytes a full evaluation of P placements moves at minimum: per placement
+    24 B per edge (neighbour label 4 + value 8, for the t and the b sweep) and
+    53 B per node (t sweep: label 4, tl 8, tl + comp 8; b sweep: label 4, bl 8;
+    critical flags: tl 8, bl 8, flag 1; label sums: label 4); per batch the
+    shared structure, 24 B per edge (neighbour id 4 + cost 8, twice) and 32 B
+    per node (offsets 4 + comp 8, twice; mem 8)."""
     return P * (24 * E + 53 * V) + 24 * E + 32 * V
+
+
+def algorithmic_bytes_sweep(V: int, E: int, P: int) -> int:
+    """The share of the same accounting that the sweep kernel moves (t and b
+    sweeps plus the label sums; the critical flags are written afterwards): per
+    placement 24 B per edge and 36 B per node, plus the shared structure."""
+    return P * (24 * E + 36 * V) + 24 * E + 32 * V
 
 
 def algorithmic_bytes_single(V: int, E: int) -> int:
@@ -119,6 +128,9 @@ def main() -> int:
                     help="seconds of oracle work for the CPU baseline (0: skip)")
     ap.add_argument("--no-single", action="store_true",
                     help="skip the single-placement latency report")
+    ap.add_argument("--copy-calibration", action="store_true",
+                    help="only run a 1 GiB device copy three times (scale reference for the "
+                         "FETCH_SIZE / WRITE_SIZE counters) and exit")
     args = ap.parse_args()
     if args.gpus != 1:
         print(f"bench.py runs on one GPU only: the evaluator has no multi-GPU path "
@@ -134,6 +146,14 @@ def main() -> int:
     if not torch.cuda.is_available():
         print("bench.py needs a GPU", file=sys.stderr)
         return 1
+    if args.copy_calibration:
+        a = torch.ones(1 << 28, dtype=torch.int32, device="cuda")  # 1 GiB
+        b = torch.empty_like(a)
+        for _ in range(3):
+            b.copy_(a)
+        torch.cuda.synchronize()
+        print("copied 1 GiB three times", file=sys.stderr, flush=True)
+        return 0
     P.load_library()
     dev = lambda x, dt: torch.as_tensor(np.ascontiguousarray(x), dtype=dt).cuda()
 
@@ -192,14 +212,18 @@ def main() -> int:
           f"{gteps:.2f} GTEPS", file=sys.stderr, flush=True)
 
     k_ms = float(np.mean(kernel_ms))
-    alg = algorithmic_bytes_batch(V, E, Pn)
+    alg = algorithmic_bytes_sweep(V, E, Pn)
     achieved = alg / (k_ms / 1e3) / 1e9
+    step_alg = algorithmic_bytes_batch(V, E, Pn)
     workload_key = f"c4_transformer_V{V}_E{E}_P{Pn}"
     traffic = load_traffic(kernel_name, workload_key)
     roofline = {"bound": "hbm", "achieved": round(achieved, 2), "peak": HBM_PEAK_GBS,
                 "unit": "GB/s", "frac": round(achieved / HBM_PEAK_GBS, 4), "traffic": traffic,
                 "kernel": kernel_name, "kernel_ms": round(k_ms, 4),
-                "algorithmic_bytes_per_launch": alg}
+                "algorithmic_bytes_per_launch": alg,
+                "step": {"algorithmic_bytes": step_alg,
+                         "achieved": round(step_alg / (ms_per_step / 1e3) / 1e9, 2),
+                         "frac": round(step_alg / (ms_per_step / 1e3) / 1e9 / HBM_PEAK_GBS, 4)}}
 
     single = None
     if not args.no_single:

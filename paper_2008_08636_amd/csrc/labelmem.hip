@@ -185,19 +185,36 @@ __global__ __launch_bounds__(256) void k_moves_to_slices(int32_t V, int32_t P,
         carry[r] = v < V ? base[order[v]] : 0;
     }
     __syncthreads();
+    constexpr int RW = TV / (256 / kWave);  // node rows per wave
     for (int32_t c0 = 0; c0 < n_slices * S; c0 += TP) {
-        for (int r = w; r < TV; r += 256 / kWave) {
-            const int32_t o = rows[r];
-            const int32_t p = c0 + lane;
-            const int32_t m = (o >= 0 && p < P) ? mat[(int64_t)o * P + p] : -1;
-            int32_t last = m >= 0 ? lane : -1;
+        // all of this wave's row chunks in flight at once, then scan each
+        const int32_t p = c0 + lane;
+        int32_t m[RW];
+#pragma unroll
+        for (int j = 0; j < RW; j++) {
+            const int32_t o = rows[w + j * (256 / kWave)];
+            m[j] = mat[(int64_t)(o >= 0 ? o : 0) * P + min(p, P - 1)];
+            if (o < 0 || p >= P) m[j] = -1;
+        }
+        int32_t mm[RW], last[RW];
+#pragma unroll
+        for (int j = 0; j < RW; j++) {
+            int32_t l = m[j] >= 0 ? lane : -1;
 #pragma unroll
             for (int off = 1; off < kWave; off <<= 1) {
-                int32_t y = __shfl_up(last, off, kWave);
-                if (lane >= off) last = max(last, y);
+                int32_t y = __shfl_up(l, off, kWave);
+                if (lane >= off) l = max(l, y);
             }
-            const int32_t mm = __shfl(m, last < 0 ? 0 : last, kWave);
-            const int32_t val = last >= 0 ? label[mm] : carry[r];
+            last[j] = l;
+            mm[j] = __shfl(m[j], l < 0 ? 0 : l, kWave);
+        }
+        int32_t lv[RW];
+#pragma unroll
+        for (int j = 0; j < RW; j++) lv[j] = label[last[j] >= 0 ? mm[j] : 0];
+#pragma unroll
+        for (int j = 0; j < RW; j++) {
+            const int r = w + j * (256 / kWave);
+            const int32_t val = last[j] >= 0 ? lv[j] : carry[r];
             tile[r][lane] = val;
             const int32_t tail = __shfl(val, kWave - 1, kWave);
             if (lane == 0) carry[r] = tail;
@@ -230,10 +247,14 @@ hipError_t launch_moves_to_slices(const Graph &g, const int32_t *base, int32_t P
         if ((e = hipGetLastError()) != hipSuccess) return e;
     }
     const unsigned grid = (unsigned)((g.V + 63) / 64);
+    // the label gather is unconditional; without moves it reads a valid dummy
+    const int32_t *lab_src = M > 0 ? label : base;
     if (S == 2)
-        k_moves_to_slices<2><<<grid, 256, 0, g.stream>>>(g.V, P, g.order, base, label, mat, lab_w);
+        k_moves_to_slices<2><<<grid, 256, 0, g.stream>>>(g.V, P, g.order, base, lab_src, mat,
+                                                         lab_w);
     else if (S == 4)
-        k_moves_to_slices<4><<<grid, 256, 0, g.stream>>>(g.V, P, g.order, base, label, mat, lab_w);
+        k_moves_to_slices<4><<<grid, 256, 0, g.stream>>>(g.V, P, g.order, base, lab_src, mat,
+                                                         lab_w);
     else
         return hipErrorInvalidValue;
     return hipGetLastError();

@@ -37,9 +37,9 @@ namespace pardnn {
 namespace {
 
 constexpr int kBlock = 256;
-constexpr int kChaseWindow = 2048;  // links staged per wave
-constexpr int kFinishLds = 4 * kChaseWindow * 4 > 2 * 32 * 65 * 8 ? 4 * kChaseWindow * 4
-                                                                  : 2 * 32 * 65 * 8;
+constexpr int kChaseWindow = 1024;  // links staged per wave
+constexpr int kEmitLds = 2 * 32 * 65 * 8 + 32 * 4 + 64 * 8;
+constexpr int kFinishLds = 4 * kChaseWindow * 4 > kEmitLds ? 4 * kChaseWindow * 4 : kEmitLds;
 
 inline unsigned grid_for(int64_t n, int block, int cap = 65536) {
     int64_t g = (n + block - 1) / block;
@@ -537,55 +537,76 @@ __global__ __launch_bounds__(T) void k_sweep(SweepArgs a) {
 // Outputs in the caller's layout: tl, bl [V][P] in original ids and the
 // critical flags crit = (tl + bl == M_p). A 32-node x 64-placement tile goes
 // through LDS so that the slice-major workspace is read contiguously and each
-// output row order[v] is written as one contiguous 512-byte run.
+// output row order[v] is written as one contiguous 512-byte run. Every load of
+// a phase is issued before the first is consumed (unrolled, clamped
+// addresses), and the tile's node ids, costs and makespans are staged once.
 template <int S, bool PACKED>
 __device__ void emit_tile(const SweepArgs &a, uint8_t *crit, int32_t bx, int32_t by,
                           char *smem) {
     using EL = Elem<PACKED>;
     using ET = typename EL::T;
-    constexpr int TV = 32, TP = 64;
+    constexpr int TV = 32, TP = 64, NT = 256;
+    constexpr int PER = TV * TP / NT;  // elements per thread
     long long(*t_tl)[TP + 1] = reinterpret_cast<long long(*)[TP + 1]>(smem);
     long long(*t_bl)[TP + 1] = reinterpret_cast<long long(*)[TP + 1]>(smem + TV * (TP + 1) * 8);
+    int32_t *s_ord = reinterpret_cast<int32_t *>(smem + 2 * TV * (TP + 1) * 8);
+    long long *s_m = reinterpret_cast<long long *>(s_ord + TV);
+    const int tid = threadIdx.x;
     const int32_t V = a.V, P = a.P;
     const int32_t v0 = bx * TV, q0 = by * TP;
     const int32_t sl0 = q0 / S;
-    const int n_sl = min(TP / S, (P + S - 1) / S - sl0);
+    const int32_t n_slices = (P + S - 1) / S;
     const ET *ft = reinterpret_cast<const ET *>(a.ftl);
     const ET *bl = reinterpret_cast<const ET *>(a.bll);
-    for (int i = threadIdx.x; i < n_sl * TV * S; i += 256) {
-        const int sl = i / (TV * S), j = i % (TV * S);
-        const int r = j / S, s = j % S;
-        const int32_t v = v0 + r;
-        if (v < V) {
-            const int64_t idx = ((int64_t)(sl0 + sl) * V + v) * S + s;
-            t_tl[r][sl * S + s] = EL::val(ft[idx], a.lb) - a.comp_lm[v];
-            t_bl[r][sl * S + s] = EL::val(bl[idx], a.lb);
-        }
+    if (tid < TV) s_ord[tid] = a.order[min(v0 + tid, V - 1)];
+    if (tid < TP) s_m[tid] = a.makespan[min(q0 + tid, P - 1)];
+    // element i of the tile read: slice-local run of TV*S values per slice
+    ET fv[PER], bv[PER];
+    int64_t cv[PER];
+#pragma unroll
+    for (int j = 0; j < PER; j++) {
+        const int i = tid + j * NT;
+        const int sl = i / (TV * S), r = (i % (TV * S)) / S, s2 = i % S;
+        const int32_t v = min(v0 + r, V - 1);
+        const int64_t idx = ((int64_t)min(sl0 + sl, n_slices - 1) * V + v) * S + s2;
+        fv[j] = ft[idx];
+        bv[j] = bl[idx];
+        cv[j] = a.comp_lm[v];
+    }
+#pragma unroll
+    for (int j = 0; j < PER; j++) {
+        const int i = tid + j * NT;
+        const int sl = i / (TV * S), r = (i % (TV * S)) / S, s2 = i % S;
+        t_tl[r][sl * S + s2] = EL::val(fv[j], a.lb) - cv[j];
+        t_bl[r][sl * S + s2] = EL::val(bv[j], a.lb);
     }
     __syncthreads();
-    for (int i = threadIdx.x; i < TV * TP; i += 256) {
+#pragma unroll
+    for (int j = 0; j < PER; j++) {
+        const int i = tid + j * NT;
         const int r = i / TP, q = i % TP;
         const int32_t v = v0 + r, p = q0 + q;
         if (v < V && p < P) {
-            const int64_t o = (int64_t)a.order[v] * P + p;
+            const int64_t o = (int64_t)s_ord[r] * P + p;
             const int64_t t = t_tl[r][q], b = t_bl[r][q];
             a.tl_out[o] = t;
             a.bl_out[o] = b;
-            if (crit) crit[o] = (uint8_t)(t + b == a.makespan[p]);
+            if (crit) crit[o] = (uint8_t)(t + b == s_m[q]);
         }
     }
 }
 
 // One wave per placement walks the chosen-successor links from the path
 // start. Links point to strictly later levels (larger level-major ids), so the
-// wave stages a window of its links in LDS with coalesced loads and walks
-// inside the window (uniformly across the wave); the window moves forward when
-// the walk leaves it. Lane i keeps the (i mod 64)-th path node and the wave
-// writes 64 original ids at a time.
+// wave stages a window of its links in LDS (all loads in flight at once) and
+// walks inside the window (uniformly across the wave); the window moves
+// forward when the walk leaves it. Lane i keeps the (i mod 64)-th path node
+// and the wave writes 64 original ids at a time.
 template <int S>
 __device__ void chase_wave(const SweepArgs &a, int32_t p, int32_t *path, int32_t stride,
                            int32_t *path_len, int32_t *win) {
     constexpr int kWin = kChaseWindow;
+    constexpr int PER = kWin / kWave;
     const int lane = lane_id();
     const int32_t V = a.V;
     const int32_t slice = p / S, s = p % S;
@@ -594,8 +615,13 @@ __device__ void chase_wave(const SweepArgs &a, int32_t p, int32_t *path, int32_t
     int32_t cur = a.start[p], len = 0, mine = -1;
     while (cur >= 0) {
         const int32_t base = cur;
-        for (int i = lane; i < kWin; i += kWave)
-            win[i] = base + i < V ? nx[(int64_t)(base + i) * S + s] : -1;
+        int32_t tmp[PER];
+#pragma unroll
+        for (int j = 0; j < PER; j++)
+            tmp[j] = nx[(int64_t)min(base + lane + j * kWave, V - 1) * S + s];
+#pragma unroll
+        for (int j = 0; j < PER; j++)
+            win[lane + j * kWave] = base + lane + j * kWave < V ? tmp[j] : -1;
         __builtin_amdgcn_wave_barrier();
         int32_t c = base;
         while (c >= base && c < base + kWin) {

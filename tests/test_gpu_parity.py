@@ -338,6 +338,13 @@ def test_evaluate_moves_small(P):
     ref = run_batch(P, G, pl, g)
     for k in ref:
         assert (ref[k] == got[k]).all(), k
+    # no moves at all: every placement equals the base, label array may be empty
+    zero_ptr = dev(np.zeros(4, np.int64), torch.int64)
+    empty = torch.empty(0, dtype=torch.int32, device="cuda")
+    out0 = G.evaluate_moves(args[0], zero_ptr, empty, empty, g.n_labels)
+    torch.cuda.synchronize()
+    g0 = {k: v.cpu().numpy() for k, v in out0.items()}
+    check_batch(g, np.repeat(sched2.base[:, None], 3, axis=1), g0, range(3))
     with pytest.raises(P.PardnnError) as e:
         bad = node.copy()
         bad[3] = g.n_nodes + 7
