@@ -59,6 +59,11 @@ enum pardnn_status {
     PARDNN_E_DEVICE = -5    /* no usable GPU, or a HIP runtime call failed */
 };
 
+/* Largest graph a handle accepts: 2^26 nodes and 2^27 edges (the evaluation
+ * kernels address per-node and per-edge arrays with 32-bit byte offsets). */
+#define PARDNN_MAX_NODES (1 << 26)
+#define PARDNN_MAX_EDGES (1 << 27)
+
 typedef struct pardnn_info {
     int32_t n_nodes;
     int64_t n_edges;
@@ -69,8 +74,8 @@ typedef struct pardnn_info {
 
 /*
  * Create a handle for G = (V, E) (Sec. 2; Table 2 comp, comm, mem).
- *   n_nodes        V >= 0.
- *   n_edges        |E|, 0 <= n_edges < 2^31.
+ *   n_nodes        V, 0 <= V <= PARDNN_MAX_NODES.
+ *   n_edges        |E|, 0 <= |E| <= PARDNN_MAX_EDGES.
  *   src, dst       int32[n_edges], edge e runs src[e] -> dst[e].
  *   comp           int64[n_nodes], node cost (comp(n)), >= 0.
  *   edge_cost      int64[n_edges], transfer cost of edge e when its ends carry

@@ -366,8 +366,8 @@ int pardnn_graph_create(int32_t n_nodes, int64_t n_edges, const int32_t *src, co
     g_last_error.clear();
     if (out == nullptr) return fail(PARDNN_E_INVAL, "out is null");
     *out = nullptr;
-    if (n_nodes < 0 || n_edges < 0 || n_edges >= (int64_t)INT32_MAX)
-        return fail(PARDNN_E_INVAL, "n_nodes must be >= 0 and 0 <= n_edges < 2^31 - 1");
+    if (n_nodes < 0 || n_nodes > PARDNN_MAX_NODES || n_edges < 0 || n_edges > PARDNN_MAX_EDGES)
+        return fail(PARDNN_E_INVAL, "need 0 <= n_nodes <= 2^26 and 0 <= n_edges <= 2^27");
     if (n_edges > 0 && (src == nullptr || dst == nullptr || edge_cost == nullptr))
         return fail(PARDNN_E_INVAL, "src, dst and edge_cost must be non-null when n_edges > 0");
     if (n_nodes > 0 && (comp == nullptr || mem == nullptr))

@@ -29,6 +29,8 @@
 // Batch: a workgroup owns S placements ("slots") of one direction; the S
 // lanes of one edge read the same structure (a broadcast) and S adjacent
 // {value, label} pairs of the slice-major workspace.
+#include <type_traits>
+
 #include "device_utils.h"
 #include "internal.h"
 
@@ -79,6 +81,17 @@ __global__ __launch_bounds__(256) void k_permute_labels(int32_t V, int32_t P,
         const int32_t v = v0 + r;
         if (v < V) lab_w[((int64_t)(sl0 + sl) * V + v) * S + s] = tile[r][sl * S + s];
     }
+}
+
+// Element idx of an array whose base pointer is uniform over the workgroup,
+// addressed with a 32-bit byte offset, so that the access uses the scalar base
+// + 32-bit vector offset form: no 64-bit index arithmetic and no register pair
+// holding a sign-extended index. Graph creation bounds V and E so that every
+// such offset stays below 2^32.
+template <class T>
+__device__ __forceinline__ T &at(T *base, uint32_t idx) {
+    using B = typename std::conditional<std::is_const<T>::value, const char, char>::type;
+    return *reinterpret_cast<T *>(reinterpret_cast<B *>(base) + idx * (uint32_t)sizeof(T));
 }
 
 struct alignas(16) Pair {
@@ -175,6 +188,7 @@ __device__ void sweep_dir(const SweepArgs &a, int32_t slice, char *smem) {
     const EdgeRec16 *erec = FWD ? a.in_rec : a.out_rec;
     const int32_t *off = FWD ? a.in_off : a.out_off;
     const bool want_nx = !FWD && a.nx_w != nullptr;
+    int32_t *nxb = want_nx ? a.nx_w + wbase : nullptr;
     const bool tie_phase = want_nx && !PACKED;
     const bool want_bins = FWD && a.K > 0;
     const bool lds_bins = want_bins && a.K * S <= kBinsCap;
@@ -203,23 +217,23 @@ __device__ void sweep_dir(const SweepArgs &a, int32_t slice, char *smem) {
 
     // one 16-byte load per edge record (plus the successor's id for b)
     auto load_edge = [&](int32_t e) {
-        const EdgeRec16 x = erec[e];
+        const EdgeRec16 x = at(erec, (uint32_t)e);
         EdgeRec r;
         r.nb = x.nb;
         r.own = x.own;
         r.c = x.cost;
-        r.nbo = FWD ? 0 : a.out_dst_orig[e];
+        r.nbo = FWD ? 0 : at(a.out_dst_orig, (uint32_t)e);
         return r;
     };
     // one 16-byte load of the node constants, the label, and (single
     // placement only) the node's original id for the direct outputs
     auto load_node = [&](int32_t v, int s) {
-        const NodeRec16 x = a.node_rec[v];
+        const NodeRec16 x = at(a.node_rec, (uint32_t)v);
         NodeRec r;
-        r.ord = DIRECT ? a.order[v] : 0;
+        r.ord = DIRECT ? at(a.order, (uint32_t)v) : 0;
         r.comp = x.comp;
         r.mem = x.mem;
-        r.lab = lab[(int64_t)v * S + s];
+        r.lab = at(lab, (uint32_t)(v * S + s));
         return r;
     };
 
@@ -250,7 +264,7 @@ __device__ void sweep_dir(const SweepArgs &a, int32_t slice, char *smem) {
         const int32_t lo = li.node_lo, w = ln.node_lo - lo;
         int32_t *sl = slab + buf * ACC * S;
         if (tid < w * S) sl[tid] = n.lab;
-        for (int32_t i = tid + T; i < w * S; i += T) sl[i] = lab[(int64_t)lo * S + i];
+        for (int32_t i = tid + T; i < w * S; i += T) sl[i] = at(lab, (uint32_t)(lo * S + i));
     };
     auto cand = [&](const ET &g, int32_t own_lab, int64_t c) {
         return EL::val(g, lb) + (EL::lab(g, lb) != own_lab ? c : 0);
@@ -267,7 +281,7 @@ __device__ void sweep_dir(const SweepArgs &a, int32_t slice, char *smem) {
         const int32_t p = p0 + s;
         if (FWD) {
             const ET out = EL::make(t + n.comp, n.lab, lb);
-            vals[(int64_t)v * S + s] = out;
+            at(vals, (uint32_t)(v * S + s)) = out;
             if (nb_out) nb_out[slot] = out;
             if (p < P) {
                 if (DIRECT) a.tl_out[(int64_t)n.ord * P + p] = t;
@@ -285,110 +299,118 @@ __device__ void sweep_dir(const SweepArgs &a, int32_t slice, char *smem) {
         } else {
             const int64_t b = n.comp + t;
             const ET out = EL::make(b, n.lab, lb);
-            vals[(int64_t)v * S + s] = out;
+            at(vals, (uint32_t)(v * S + s)) = out;
             if (nb_out) nb_out[slot] = out;
             if (DIRECT && p < P) a.bl_out[(int64_t)n.ord * P + p] = b;
             if (want_nx) {
                 if (PACKED) {
-                    if (key == 0) a.nx_w[wbase + (int64_t)v * S + s] = -1;
+                    if (key == 0) at(nxb, (uint32_t)(v * S + s)) = -1;
                 } else {
                     const unsigned long long k2 = nacc[slot];
                     nacc[slot] = ~0ull;
-                    a.nx_w[wbase + (int64_t)v * S + s] =
+                    at(nxb, (uint32_t)(v * S + s)) =
                         k2 == ~0ull ? -1 : (int32_t)(k2 & 0xffffffffull);
                 }
             }
         }
     };
 
-    // ---- prologue: records of the first two levels, labels of the first ----
-    Recs r0{}, r1{}, r2{};
-    ET fv0{}, fv1{}, fn0{}, fn1{};  // far neighbour values: current level / next level
-    bool h0 = false, h1 = false, hn0 = false, hn1 = false;
-    LevelInfo li{}, ln{}, lin{}, lnn{};
+    // ---- pipeline state ----
+    // One set per level in flight: level k (consumed now), k+1 (its far values
+    // are being loaded) and k+2 (its records are being loaded). The step loop
+    // is unrolled three times and the sets rotate by name, so no register that
+    // a load is still filling is ever copied: such a copy would make the wave
+    // wait for every load in flight and drain the pipeline at each level.
+    struct Stage {
+        Recs r;            // records of the level, loaded two steps ahead
+        ET f0, f1;         // far neighbour values of the two pipelined tasks
+        bool h0, h1;       // the task's neighbour is far (value in f0 / f1)
+        LevelInfo li, ln;  // the level's boundaries and the next level's
+    };
+    Stage SA{}, SB{}, SC{};
     if (L > 0) {
         const int32_t k0 = level_at(0), k1 = L > 1 ? level_at(1) : k0;
         stage(min(k0, k1), max(k0, k1) + 1);
-        li = LI(k0);
-        ln = LI(k0 + 1);
-        lin = LI(k1);
-        lnn = LI(k1 + 1);
-        prefetch(li, ln, r0);
-        prefetch(lin, lnn, r1);
-        if (ln.node_lo - li.node_lo <= ACC) fill_labels(li, ln, 0, r0.n);
+        SA.li = LI(k0);
+        SA.ln = LI(k0 + 1);
+        SB.li = LI(k1);
+        SB.ln = LI(k1 + 1);
+        prefetch(SA.li, SA.ln, SA.r);
+        prefetch(SB.li, SB.ln, SB.r);
+        if (SA.ln.node_lo - SA.li.node_lo <= ACC) fill_labels(SA.li, SA.ln, 0, SA.r.n);
     }
     __syncthreads();
     int32_t plo = 0, phi = 0;     // previous level's node range
     bool prev_in_lds = false;     // previous level's values sit in nbuf[(step - 1) & 1]
 
-    for (int32_t step = 0; step < L; step++) {
+    auto body = [&](int32_t step, Stage &A, Stage &B, Stage &C) __attribute__((always_inline)) {
         const bool has_next = step + 1 < L;
         const int32_t k = level_at(step);
         const int32_t knn = step + 2 < L ? level_at(step + 2) : (has_next ? level_at(step + 1) : k);
         stage(min(k, knn), max(k, knn) + 1);
-        const LevelInfo l3 = LI(knn), l4 = LI(knn + 1);
+        C.li = LI(knn);
+        C.ln = LI(knn + 1);
         const int buf = step & 1;
-        const int32_t lo = li.node_lo, hi = ln.node_lo;
-        const int32_t ea = e_lo(li), eb = e_lo(ln);
+        const int32_t lo = A.li.node_lo, hi = A.ln.node_lo;
+        const int32_t ea = e_lo(A.li), eb = e_lo(A.ln);
         const int32_t nt = (eb - ea) * S;
-        const int32_t nt_next = (e_lo(lnn) - e_lo(lin)) * S;
-        const bool next_narrow = has_next && lnn.node_lo - lin.node_lo <= ACC;
+        const int32_t nt_next = (e_lo(B.ln) - e_lo(B.li)) * S;
+        const bool next_narrow = has_next && B.ln.node_lo - B.li.node_lo <= ACC;
         long long *accb = acc + buf * ACC * S;
         long long *accp = acc + (buf ^ 1) * ACC * S;
         const ET *nprev = nbuf + (buf ^ 1) * ACC * S;
+        const int sB = (tid + T) % S;
 
-        // neighbour value of a task: far (prefetched), near in LDS, or global
-        auto nval = [&](const EdgeRec &r, int s, bool has_far, const ET &far) -> ET {
-            if (has_far) return far;
+        // neighbour value of an inline task: near in LDS, else global
+        auto nval = [&](const EdgeRec &r, int s) -> ET {
             if (prev_in_lds && r.nb >= plo && r.nb < phi) return nprev[(r.nb - plo) * S + s];
-            return vals[(int64_t)r.nb * S + s];
+            return at(vals, (uint32_t)(r.nb * S + s));
         };
 
-        if (hi - lo <= ACC) {
+        if (__builtin_expect(hi - lo <= ACC, 1)) {
             // ---- narrow level ----
             const int32_t *sl = slab + buf * ACC * S;
             const bool ev0 = tid < nt, ev1 = tid + T < nt;
-            const int sA = s0, sB = (tid + T) % S;
             long long k0v = 0, k1v = 0;
             // pass 0/1 neighbours: prefetched register (far, or everything after a
             // wide level) or the previous level's values in LDS -- no global load
-            const ET l0 = nprev[ev0 && !h0 ? (r0.e0.nb - plo) * S + sA : 0];
-            const ET l1 = nprev[ev1 && !h1 ? (r0.e1.nb - plo) * S + sB : 0];
+            const ET l0 = nprev[ev0 && !A.h0 ? (A.r.e0.nb - plo) * S + s0 : 0];
+            const ET l1 = nprev[ev1 && !A.h1 ? (A.r.e1.nb - plo) * S + sB : 0];
             if (ev0) {
-                const ET g = h0 ? fv0 : l0;
-                k0v = akey(cand(g, sl[(r0.e0.own - lo) * S + sA], r0.e0.c), r0.e0.nbo);
-                lds_max_i64(&accb[(r0.e0.own - lo) * S + sA], k0v);
+                const ET g = A.h0 ? A.f0 : l0;
+                k0v = akey(cand(g, sl[(A.r.e0.own - lo) * S + s0], A.r.e0.c), A.r.e0.nbo);
+                lds_max_i64(&accb[(A.r.e0.own - lo) * S + s0], k0v);
             }
             if (ev1) {
-                const ET g = h1 ? fv1 : l1;
-                k1v = akey(cand(g, sl[(r0.e1.own - lo) * S + sB], r0.e1.c), r0.e1.nbo);
-                lds_max_i64(&accb[(r0.e1.own - lo) * S + sB], k1v);
+                const ET g = A.h1 ? A.f1 : l1;
+                k1v = akey(cand(g, sl[(A.r.e1.own - lo) * S + sB], A.r.e1.c), A.r.e1.nbo);
+                lds_max_i64(&accb[(A.r.e1.own - lo) * S + sB], k1v);
             }
             // next level's far neighbours (final already) and level k+2's records
-            hn0 = has_next && tid < nt_next && (FWD ? r1.e0.nb < lo : r1.e0.nb >= hi);
-            hn1 = has_next && tid + T < nt_next && (FWD ? r1.e1.nb < lo : r1.e1.nb >= hi);
-            fn0 = vals[hn0 ? (int64_t)r1.e0.nb * S + s0 : 0];
-            fn1 = vals[hn1 ? (int64_t)r1.e1.nb * S + sB : 0];
-            prefetch(l3, l4, r2);
+            B.h0 = has_next && tid < nt_next && (FWD ? B.r.e0.nb < lo : B.r.e0.nb >= hi);
+            B.h1 = has_next && tid + T < nt_next && (FWD ? B.r.e1.nb < lo : B.r.e1.nb >= hi);
+            B.f0 = at(vals, B.h0 ? (uint32_t)(B.r.e0.nb * S + s0) : 0u);
+            B.f1 = at(vals, B.h1 ? (uint32_t)(B.r.e1.nb * S + sB) : 0u);
+            prefetch(C.li, C.ln, C.r);
             for (int32_t i = tid + 2 * T; i < nt; i += T) {
                 const EdgeRec r = load_edge(ea + i / S);
                 const int s = i % S;
-                const ET g = nval(r, s, false, fn0);
+                const ET g = nval(r, s);
                 lds_max_i64(&accb[(r.own - lo) * S + s],
                             akey(cand(g, sl[(r.own - lo) * S + s], r.c), r.nbo));
             }
             __syncthreads();
             if (tie_phase) {
-                if (ev0 && k0v == accb[(r0.e0.own - lo) * S + sA])
-                    lds_min_u64(&nacc[(r0.e0.own - lo) * S + sA],
-                                ((unsigned long long)(uint32_t)r0.e0.nbo << 32) | (uint32_t)r0.e0.nb);
-                if (ev1 && k1v == accb[(r0.e1.own - lo) * S + sB])
-                    lds_min_u64(&nacc[(r0.e1.own - lo) * S + sB],
-                                ((unsigned long long)(uint32_t)r0.e1.nbo << 32) | (uint32_t)r0.e1.nb);
+                if (ev0 && k0v == accb[(A.r.e0.own - lo) * S + s0])
+                    lds_min_u64(&nacc[(A.r.e0.own - lo) * S + s0],
+                                ((unsigned long long)(uint32_t)A.r.e0.nbo << 32) | (uint32_t)A.r.e0.nb);
+                if (ev1 && k1v == accb[(A.r.e1.own - lo) * S + sB])
+                    lds_min_u64(&nacc[(A.r.e1.own - lo) * S + sB],
+                                ((unsigned long long)(uint32_t)A.r.e1.nbo << 32) | (uint32_t)A.r.e1.nb);
                 for (int32_t i = tid + 2 * T; i < nt; i += T) {
                     const EdgeRec r = load_edge(ea + i / S);
                     const int s = i % S;
-                    const ET g = nval(r, s, false, fn0);
+                    const ET g = nval(r, s);
                     const int32_t slot = (r.own - lo) * S + s;
                     if (akey(cand(g, sl[slot], r.c), r.nbo) == accb[slot])
                         lds_min_u64(&nacc[slot],
@@ -397,22 +419,22 @@ __device__ void sweep_dir(const SweepArgs &a, int32_t slice, char *smem) {
                 __syncthreads();
             } else if (want_nx) {
                 // PACKED b: the task holding the winning key names the successor
-                if (ev0 && k0v == accb[(r0.e0.own - lo) * S + sA])
-                    a.nx_w[wbase + (int64_t)r0.e0.own * S + sA] = r0.e0.nb;
-                if (ev1 && k1v == accb[(r0.e1.own - lo) * S + sB])
-                    a.nx_w[wbase + (int64_t)r0.e1.own * S + sB] = r0.e1.nb;
+                if (ev0 && k0v == accb[(A.r.e0.own - lo) * S + s0])
+                    at(nxb, (uint32_t)(A.r.e0.own * S + s0)) = A.r.e0.nb;
+                if (ev1 && k1v == accb[(A.r.e1.own - lo) * S + sB])
+                    at(nxb, (uint32_t)(A.r.e1.own * S + sB)) = A.r.e1.nb;
                 for (int32_t i = tid + 2 * T; i < nt; i += T) {
                     const EdgeRec r = load_edge(ea + i / S);
                     const int s = i % S;
-                    const ET g = nval(r, s, false, fn0);
+                    const ET g = nval(r, s);
                     const int32_t slot = (r.own - lo) * S + s;
                     if (akey(cand(g, sl[slot], r.c), r.nbo) == accb[slot])
-                        a.nx_w[wbase + (int64_t)r.own * S + s] = r.nb;
+                        at(nxb, (uint32_t)(r.own * S + s)) = r.nb;
                 }
             }
             ET *nb_out = nbuf + buf * ACC * S;
             const int32_t nnt = (hi - lo) * S;
-            if (tid < nnt) finish_node(lo + tid / S, s0, tid, accb[tid], r0.n, nb_out);
+            if (tid < nnt) finish_node(lo + tid / S, s0, tid, accb[tid], A.r.n, nb_out);
             for (int32_t i = tid + T; i < nnt; i += T) {
                 const int s = i % S;
                 const int32_t v = lo + i / S;
@@ -422,7 +444,7 @@ __device__ void sweep_dir(const SweepArgs &a, int32_t slice, char *smem) {
             }
             // clear the previous level's accumulators (used again at step + 1)
             for (int32_t i = tid; i < (phi - plo) * S && phi - plo <= ACC; i += T) accp[i] = 0;
-            if (next_narrow) fill_labels(lin, lnn, buf ^ 1, r1.n);
+            if (next_narrow) fill_labels(B.li, B.ln, buf ^ 1, B.r.n);
             __syncthreads();
             prev_in_lds = true;
         } else {
@@ -438,23 +460,23 @@ __device__ void sweep_dir(const SweepArgs &a, int32_t slice, char *smem) {
                 for (int32_t i = tid; i < cnt; i += T) {
                     const EdgeRec r = load_edge(cea + i / S);
                     const int s = i % S;
-                    const ET g = nval(r, s, false, fn0);
+                    const ET g = nval(r, s);
                     lds_max_i64(&accb[(r.own - cn0) * S + s],
-                                akey(cand(g, lab[(int64_t)r.own * S + s], r.c), r.nbo));
+                                akey(cand(g, at(lab, (uint32_t)(r.own * S + s)), r.c), r.nbo));
                 }
                 __syncthreads();
                 if (want_nx) {
                     for (int32_t i = tid; i < cnt; i += T) {
                         const EdgeRec r = load_edge(cea + i / S);
                         const int s = i % S;
-                        const ET g = nval(r, s, false, fn0);
+                        const ET g = nval(r, s);
                         const int32_t slot = (r.own - cn0) * S + s;
-                        if (akey(cand(g, lab[(int64_t)r.own * S + s], r.c), r.nbo) == accb[slot]) {
+                        if (akey(cand(g, at(lab, (uint32_t)(r.own * S + s)), r.c), r.nbo) == accb[slot]) {
                             if (tie_phase)
                                 lds_min_u64(&nacc[slot],
                                             ((unsigned long long)(uint32_t)r.nbo << 32) | (uint32_t)r.nb);
                             else
-                                a.nx_w[wbase + (int64_t)r.own * S + s] = r.nb;
+                                at(nxb, (uint32_t)(r.own * S + s)) = r.nb;
                         }
                     }
                     if (tie_phase) __syncthreads();
@@ -471,27 +493,30 @@ __device__ void sweep_dir(const SweepArgs &a, int32_t slice, char *smem) {
             }
             // the wide level is final now: fetch every neighbour of the next
             // level's pipelined tasks, near ones included
-            hn0 = has_next && tid < nt_next;
-            hn1 = has_next && tid + T < nt_next;
-            fn0 = vals[hn0 ? (int64_t)r1.e0.nb * S + s0 : 0];
-            fn1 = vals[hn1 ? (int64_t)r1.e1.nb * S + (tid + T) % S : 0];
-            prefetch(l3, l4, r2);
-            if (next_narrow) fill_labels(lin, lnn, buf ^ 1, r1.n);
+            B.h0 = has_next && tid < nt_next;
+            B.h1 = has_next && tid + T < nt_next;
+            B.f0 = at(vals, B.h0 ? (uint32_t)(B.r.e0.nb * S + s0) : 0u);
+            B.f1 = at(vals, B.h1 ? (uint32_t)(B.r.e1.nb * S + sB) : 0u);
+            prefetch(C.li, C.ln, C.r);
+            if (next_narrow) fill_labels(B.li, B.ln, buf ^ 1, B.r.n);
             __syncthreads();
             prev_in_lds = false;
         }
         plo = lo;
         phi = hi;
-        r0 = r1;
-        r1 = r2;
-        fv0 = fn0;
-        fv1 = fn1;
-        h0 = hn0;
-        h1 = hn1;
-        li = lin;
-        ln = lnn;
-        lin = l3;
-        lnn = l4;
+    };
+    int32_t step = 0;
+    for (; step + 3 <= L; step += 3) {
+        body(step, SA, SB, SC);
+        body(step + 1, SB, SC, SA);
+        body(step + 2, SC, SA, SB);
+    }
+    for (; step < L; step++) {  // the last L mod 3 levels: rotate by copying
+        body(step, SA, SB, SC);
+        const Stage t = SA;
+        SA = SB;
+        SB = SC;
+        SC = t;
     }
 
     if (FWD) {

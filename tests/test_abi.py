@@ -75,6 +75,12 @@ def test_null_arguments_rejected_on_host(lib):
     assert lib.pardnn_graph_create(3, 2, None, None, None, None, None, None, ctypes.byref(h)) == -1
     assert lib.pardnn_graph_create(-1, 0, None, None, None, None, None, None, ctypes.byref(h)) == -1
     assert lib.pardnn_graph_create(0, 0, None, None, None, None, None, None, None) == -1
+    # size limits: 2^26 nodes, 2^27 edges (checked before anything is read)
+    assert lib.pardnn_graph_create((1 << 26) + 1, 0, None, None, None, None, None, None,
+                                   ctypes.byref(h)) == -1
+    assert lib.pardnn_graph_create(4, (1 << 27) + 1, None, None, None, None, None, None,
+                                   ctypes.byref(h)) == -1
+    assert b"2^26" in lib.pardnn_last_error()
     assert lib.pardnn_tb_levels(None, None, None, None, None) == -1
     assert b"null" in lib.pardnn_last_error()
 
