@@ -136,7 +136,7 @@ int ensure_levelized(Graph *g) {
     g->max_width = mw;
 
     const size_t E = (size_t)g->E;
-    HIP_TRY(dalloc(*g, &g->linfo, (size_t)L + 1));
+    HIP_TRY(dalloc(*g, &g->linfo, (size_t)L + 2));
     HIP_TRY(dalloc(*g, &g->in_off, (size_t)V + 1));
     HIP_TRY(dalloc(*g, &g->in_src, E));
     HIP_TRY(dalloc(*g, &g->in_dst, E));
@@ -238,12 +238,16 @@ int evaluate_impl(Graph *g, int32_t n_place, const int32_t *placements, const Mo
     if (path != nullptr && path_stride < std::max(g->L, 1))
         return fail(PARDNN_E_INVAL, "path_stride must be at least the number of levels");
 
-    const int32_t S = batch_slots();
+    const int32_t S = kBatchSlots;
     const int64_t n_slices = (n_place + S - 1) / S;
-    const size_t per = (size_t)n_slices * (size_t)g->V * (size_t)S;
-    // lab_w, nx_w: int32 per (node, slot); ftl, bll: 16-byte pairs; start: [P]
-    const size_t need = per * (2 * sizeof(int32_t) + 4 * sizeof(int64_t)) +
-                        (size_t)n_place * sizeof(int32_t) + 1024;
+    // ftl, bll, nx_w: per slice (V + kSlicePad) x S elements (room for
+    // stores of idle lanes); lab_w: V x S per slice
+    const int64_t ws_stride = ((int64_t)g->V + kSlicePad) * S;
+    const size_t per = (size_t)n_slices * (size_t)ws_stride;
+    const size_t per_lab = (size_t)n_slices * (size_t)g->V * (size_t)S;
+    // ftl, bll: room for 16-byte pairs; lab_w, nx_w: int32; start: [P]
+    const size_t need = per * (4 * sizeof(int64_t) + sizeof(int32_t)) +
+                        per_lab * sizeof(int32_t) + (size_t)n_place * sizeof(int32_t) + 1024;
     if (g->batch_ws_bytes < need) {
         if (g->batch_ws) {
             HIP_TRY(hipStreamSynchronize(g->stream));
@@ -273,7 +277,7 @@ int evaluate_impl(Graph *g, int32_t n_place, const int32_t *placements, const Mo
     int64_t *ftl = (int64_t *)g->batch_ws;
     int64_t *bll = ftl + 2 * per;
     int32_t *lab_w = (int32_t *)(bll + 2 * per);
-    int32_t *nx_w = lab_w + per;
+    int32_t *nx_w = lab_w + per_lab;
     int32_t *start = nx_w + per;
 
     const int32_t K = label_mem != nullptr ? n_labels : 0;
@@ -293,9 +297,9 @@ int evaluate_impl(Graph *g, int32_t n_place, const int32_t *placements, const Mo
         // the move marks live in the t workspace, which the sweep overwrites later
         HIP_TRY(launch_moves_to_slices(*g, mv->base, n_place, mv->step_ptr, ends[1], mv->node,
                                        mv->label, S, reinterpret_cast<int32_t *>(ftl), lab_w,
-                                       g->err));
+                                       K, g->err));
     } else {
-        HIP_TRY(launch_permute_labels_batch(*g, placements, n_place, S, lab_w));
+        HIP_TRY(launch_permute_labels_batch(*g, placements, n_place, S, lab_w, K, g->err));
     }
     if (K > 0) {
         HIP_TRY(launch_fill_i64(label_mem, (int64_t)n_place * K, 0, g->stream));
@@ -314,6 +318,7 @@ int evaluate_impl(Graph *g, int32_t n_place, const int32_t *placements, const Mo
     a.label_mem = label_mem;
     a.lb = lb;
     a.ob = ob;
+    a.ws_stride = ws_stride;
     {
         TimedLaunch t(g, "k_sweep<2>");
         HIP_TRY(launch_sweep(a, S, g->stream));
@@ -507,6 +512,7 @@ int pardnn_tb_levels(pardnn_graph *h, const int32_t *placement, int64_t *tl, int
     a.lab_w = g->lab_lm;
     a.ftl = g->ft_lm;
     a.bll = g->bl_lm;
+    a.ws_stride = g->V;
     a.tl_out = tl;
     a.bl_out = bl;
     a.makespan = makespan;

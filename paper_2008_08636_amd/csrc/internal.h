@@ -17,6 +17,8 @@
 //     comp_lm, mem_lm int64[V]
 //     in_rec, out_rec EdgeRec16[E] and node_rec NodeRec16[V]: the same data
 //       as 16-byte records, so a sweep task loads its edge with one load
+//   linfo has L + 2 entries: entry L + 1 repeats entry L, so the pair
+//   (linfo[x], linfo[x + 1]) of an empty level can be read at x = L.
 #pragma once
 
 #include <hip/hip_runtime.h>
@@ -60,6 +62,10 @@ struct ValidateAcc {
 // kBinsCap; level boundaries are staged in LDS kLevelWindow levels at a time.
 constexpr int kBinsCap = 512;
 constexpr int kLevelWindow = 128;
+// Placements per chain of the batched evaluation (slice of the workspace),
+// and padding nodes per slice of ftl / bll / nx_w.
+constexpr int kBatchSlots = 2;
+constexpr int kSlicePad = 64;
 
 struct SweepArgs {
     int32_t V, L, P, K;     // nodes, levels, placements, labels (K = 0: no label sums)
@@ -78,6 +84,7 @@ struct SweepArgs {
     const int32_t *lab_w;   // [slice][V][S] labels in level-major order
     int64_t *ftl, *bll;     // [slice][V][S] {value, label}: tl + comp, bl (packed or pairs)
     int32_t *nx_w;          // [slice][V][S] level-major id of the chosen successor, or null
+    int64_t ws_stride;      // elements of ftl / bll / nx_w per slice (>= V * S)
     int64_t *tl_out, *bl_out, *makespan;  // [V][P], [V][P], [P], caller's numbering
     int32_t *start;         // [P] level-major id where the critical path starts, or null
     int64_t *label_mem;     // [P][K], zeroed by the caller, or null
@@ -153,12 +160,13 @@ hipError_t launch_kahn(const Graph &g, int32_t *indeg_work, int32_t *sort_scratc
 
 // ---- sweep.hip ----
 hipError_t launch_permute_labels(const Graph &g, const int32_t *placement, int32_t *lab_lm);
+// K > 0: labels outside [0, K) set bit 0 of err.
 hipError_t launch_permute_labels_batch(const Graph &g, const int32_t *placements, int32_t P,
-                                       int32_t S, int32_t *lab_w);
+                                       int32_t S, int32_t *lab_w, int32_t K = 0,
+                                       int32_t *err = nullptr);
 hipError_t launch_sweep(const SweepArgs &a, int32_t S, hipStream_t s);
 hipError_t launch_finish(const SweepArgs &a, int32_t S, uint8_t *crit, int32_t *path,
                          int32_t stride, int32_t *path_len, hipStream_t s);
-int batch_slots();  // placements per workgroup of the batched evaluation
 
 // ---- critpath.hip ----
 hipError_t launch_critical_path(const Graph &g, const int32_t *placement, const int64_t *tl,
@@ -180,6 +188,6 @@ hipError_t launch_build_placements(const Graph &g, const int32_t *base, int32_t 
 hipError_t launch_moves_to_slices(const Graph &g, const int32_t *base, int32_t P,
                                   const int64_t *step_ptr, int64_t M, const int32_t *node,
                                   const int32_t *label, int32_t S, int32_t *mat, int32_t *lab_w,
-                                  int32_t *err);
+                                  int32_t K, int32_t *err);
 
 }  // namespace pardnn

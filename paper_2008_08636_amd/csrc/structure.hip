@@ -209,8 +209,9 @@ __global__ void k_pack_records(int64_t E, int32_t V, const int32_t *in_src,
 
 __global__ void k_level_info(int32_t L, const int32_t *level_ptr, const int32_t *in_off,
                              const int32_t *out_off, LevelInfo *linfo) {
-    for (int32_t k = blockIdx.x * blockDim.x + threadIdx.x; k <= L; k += gridDim.x * blockDim.x) {
-        int32_t lo = level_ptr[k];
+    // entries 0..L, and L + 1 repeating L (the empty level past either end)
+    for (int32_t k = blockIdx.x * blockDim.x + threadIdx.x; k <= L + 1; k += gridDim.x * blockDim.x) {
+        int32_t lo = level_ptr[min(k, L)];
         LevelInfo li;
         li.node_lo = lo;
         li.in_e_lo = in_off[lo];
@@ -308,7 +309,7 @@ hipError_t launch_build_lm(Graph &g, int32_t *deg_ws, int32_t *cursor_in, int32_
             g.mem_lm, g.in_rec, g.out_rec, g.node_rec);
         if ((err = hipGetLastError()) != hipSuccess) return err;
     }
-    k_level_info<<<grid_for(g.L + 1, kBlock), kBlock, 0, g.stream>>>(g.L, g.level_ptr, g.in_off,
+    k_level_info<<<grid_for(g.L + 2, kBlock), kBlock, 0, g.stream>>>(g.L, g.level_ptr, g.in_off,
                                                                       g.out_off, g.linfo);
     return hipGetLastError();
 }

@@ -29,10 +29,9 @@
 // Batch: a workgroup owns S placements ("slots") of one direction; the S
 // lanes of one edge read the same structure (a broadcast) and S adjacent
 // {value, label} pairs of the slice-major workspace.
-#include <type_traits>
-
 #include "device_utils.h"
 #include "internal.h"
+#include "sweep_common.h"
 
 namespace pardnn {
 
@@ -57,7 +56,7 @@ template <int S>
 __global__ __launch_bounds__(256) void k_permute_labels(int32_t V, int32_t P,
                                                         const int32_t *order,
                                                         const int32_t *placements,
-                                                        int32_t *lab_w) {
+                                                        int32_t *lab_w, int32_t K, int32_t *err) {
     constexpr int TV = 64, TP = 64;  // tile: 64 nodes x 64 placements
     __shared__ int32_t tile[TV][TP + 1];
     const int32_t n_slices = (P + S - 1) / S;
@@ -67,7 +66,10 @@ __global__ __launch_bounds__(256) void k_permute_labels(int32_t V, int32_t P,
     for (int r = ty; r < TV; r += 256 / TP) {
         const int32_t v = v0 + r, p = q0 + tx;
         int32_t x = 0;
-        if (v < V && p < P) x = placements[(int64_t)order[v] * P + p];
+        if (v < V && p < P) {
+            x = placements[(int64_t)order[v] * P + p];
+            if (K > 0 && (x < 0 || x >= K)) atomicOr(err, 1);
+        }
         tile[r][tx] = x;
     }
     __syncthreads();
@@ -82,49 +84,6 @@ __global__ __launch_bounds__(256) void k_permute_labels(int32_t V, int32_t P,
         if (v < V) lab_w[((int64_t)(sl0 + sl) * V + v) * S + s] = tile[r][sl * S + s];
     }
 }
-
-// Element idx of an array whose base pointer is uniform over the workgroup,
-// addressed with a 32-bit byte offset, so that the access uses the scalar base
-// + 32-bit vector offset form: no 64-bit index arithmetic and no register pair
-// holding a sign-extended index. Graph creation bounds V and E so that every
-// such offset stays below 2^32.
-template <class T>
-__device__ __forceinline__ T &at(T *base, uint32_t idx) {
-    using B = typename std::conditional<std::is_const<T>::value, const char, char>::type;
-    return *reinterpret_cast<T *>(reinterpret_cast<B *>(base) + idx * (uint32_t)sizeof(T));
-}
-
-struct alignas(16) Pair {
-    int64_t val;
-    int64_t lab;
-};
-
-// Storage of one node's {value, label} in the sweep workspace. Packed: one
-// int64 key (value << lb) | label, valid when every label fits in lb bits and
-// every value in 63 - lb bits (checked by the host); otherwise a 16-byte pair.
-template <bool PACKED>
-struct Elem;
-template <>
-struct Elem<true> {
-    using T = int64_t;
-    __device__ static int64_t val(T e, int lb) { return e >> lb; }
-    __device__ static int32_t lab(T e, int lb) { return (int32_t)(e & ((1ll << lb) - 1)); }
-    __device__ static T make(int64_t v, int32_t l, int lb) {
-        return (v << lb) | ((int64_t)(uint32_t)l & ((1ll << lb) - 1));
-    }
-};
-template <>
-struct Elem<false> {
-    using T = Pair;
-    __device__ static int64_t val(const T &e, int) { return e.val; }
-    __device__ static int32_t lab(const T &e, int) { return (int32_t)e.lab; }
-    __device__ static T make(int64_t v, int32_t l, int) {
-        T e;
-        e.val = v;
-        e.lab = l;
-        return e;
-    }
-};
 
 // LDS bytes of one sweep workgroup.
 template <int S, int ACC, bool PACKED>
@@ -182,8 +141,8 @@ __device__ void sweep_dir(const SweepArgs &a, int32_t slice, char *smem) {
     const int ob = PACKED && !FWD ? a.ob : 0;
     const long long omax = (1ll << ob) - 1;
     const int32_t V = a.V, L = a.L, P = a.P;
-    const int64_t wbase = (int64_t)slice * V * S;
-    const int32_t *lab = a.lab_w + wbase;
+    const int64_t wbase = (int64_t)slice * a.ws_stride;
+    const int32_t *lab = a.lab_w + (int64_t)slice * V * S;
     ET *vals = reinterpret_cast<ET *>(FWD ? a.ftl : a.bll) + wbase;
     const EdgeRec16 *erec = FWD ? a.in_rec : a.out_rec;
     const int32_t *off = FWD ? a.in_off : a.out_off;
@@ -593,7 +552,7 @@ __device__ void emit_tile(const SweepArgs &a, uint8_t *crit, int32_t bx, int32_t
         const int i = tid + j * NT;
         const int sl = i / (TV * S), r = (i % (TV * S)) / S, s2 = i % S;
         const int32_t v = min(v0 + r, V - 1);
-        const int64_t idx = ((int64_t)min(sl0 + sl, n_slices - 1) * V + v) * S + s2;
+        const int64_t idx = (int64_t)min(sl0 + sl, n_slices - 1) * a.ws_stride + (int64_t)v * S + s2;
         fv[j] = ft[idx];
         bv[j] = bl[idx];
         cv[j] = a.comp_lm[v];
@@ -635,7 +594,7 @@ __device__ void chase_wave(const SweepArgs &a, int32_t p, int32_t *path, int32_t
     const int lane = lane_id();
     const int32_t V = a.V;
     const int32_t slice = p / S, s = p % S;
-    const int32_t *nx = a.nx_w + (int64_t)slice * V * S;
+    const int32_t *nx = a.nx_w + (int64_t)slice * a.ws_stride;
     int32_t *out = path + (int64_t)p * stride;
     int32_t cur = a.start[p], len = 0, mine = -1;
     while (cur >= 0) {
@@ -686,7 +645,6 @@ __global__ __launch_bounds__(256) void k_finish(SweepArgs a, uint8_t *crit, int3
 
 constexpr int kSingleThreads = 512;
 constexpr int kSingleAcc = 768;
-constexpr int kBatchSlots = 2;
 constexpr int kBatchThreads = 256;
 constexpr int kBatchAcc = 256;
 
@@ -697,20 +655,19 @@ hipError_t launch_permute_labels(const Graph &g, const int32_t *placement, int32
 }
 
 hipError_t launch_permute_labels_batch(const Graph &g, const int32_t *placements, int32_t P,
-                                       int32_t S, int32_t *lab_w) {
+                                       int32_t S, int32_t *lab_w, int32_t K, int32_t *err) {
     if (g.V == 0 || P == 0) return hipSuccess;
     dim3 grid((g.V + 63) / 64, (P + 63) / 64);
     if (S == 1)
-        k_permute_labels<1><<<grid, 256, 0, g.stream>>>(g.V, P, g.order, placements, lab_w);
+        k_permute_labels<1><<<grid, 256, 0, g.stream>>>(g.V, P, g.order, placements, lab_w, K,
+                                                        err);
     else if (S == kBatchSlots)
         k_permute_labels<kBatchSlots><<<grid, 256, 0, g.stream>>>(g.V, P, g.order, placements,
-                                                                  lab_w);
+                                                                  lab_w, K, err);
     else
         return hipErrorInvalidValue;
     return hipGetLastError();
 }
-
-int batch_slots() { return kBatchSlots; }
 
 hipError_t launch_sweep(const SweepArgs &a, int32_t S, hipStream_t s) {
     const int32_t n_slices = (a.P + S - 1) / S;

@@ -316,6 +316,63 @@ def test_batch_small_graphs(P):
         G.close()
 
 
+def level_shapes(seed):
+    """A level schedule that drives every path of the batched sweep: a chain,
+    a 100-wide level read back at spans 1..3, levels of exactly 64 and 65
+    nodes, a 36-node level with about 300 in-edges, a 10-node level with about
+    300 out-edges, a node with up to 64 predecessors, and a chain tail."""
+    sched = [(1, 1)] + [(1, 2)] * 5
+    sched += [(100, 3)]
+    sched += [(3, 6), (64, 4), (65, 3)]
+    sched += [(36, 16)]
+    sched += [(10, 2), (300, 1)]
+    sched += [(2, 4), (1, 3), (50, 5), (1, 64), (20, 3)]
+    sched += [(1, 2)] * 7
+    widths, fan = zip(*sched)
+    return W.layered_dag(np.random.default_rng(seed), widths, fan, max_span=4, n_labels=4)
+
+
+@pytest.mark.parametrize("seed", [11, 12, 13])
+def test_batch_level_shapes(P, seed):
+    g = level_shapes(seed)
+    say(f"batch level shapes seed={seed} V={g.n_nodes} E={g.n_edges}")
+    rng = np.random.default_rng(seed)
+    n_place = 7
+    pl = rng.integers(0, g.n_labels, (g.n_nodes, n_place)).astype(np.int32)
+    pl[:, 0] = 0
+    G = P.Graph(g.n_nodes, g.src, g.dst, g.comp, g.edge_cost, g.mem)
+    out = run_batch(P, G, pl, g)
+    check_batch(g, pl, out, range(n_place))
+    G.close()
+
+
+@pytest.mark.parametrize("seed", [21, 22])
+def test_batch_any_int32_labels(P, seed):
+    """Without label sums the batch takes any int32 labels (only equality
+    matters), so values are kept as full {value, label} pairs."""
+    g = level_shapes(seed)
+    say(f"batch int32 labels seed={seed}")
+    rng = np.random.default_rng(seed)
+    n_place = 5
+    pool = np.array([-2**31, -7, 0, 3, 2**20 + 1, 2**31 - 1], np.int64)
+    pl = pool[rng.integers(0, pool.size, (g.n_nodes, n_place))].astype(np.int32)
+    G = P.Graph(g.n_nodes, g.src, g.dst, g.comp, g.edge_cost, g.mem)
+    out = G.evaluate_batch(dev(pl, torch.int32), 0, labels=False)
+    torch.cuda.synchronize()
+    out = {k: v.cpu().numpy() for k, v in out.items()}
+    for p in range(n_place):
+        lab = pl[:, p].copy()
+        tl, bl, m = oracle.tb_levels(g.n_nodes, g.src, g.dst, g.comp, g.edge_cost, lab)
+        crit, path = oracle.critical_path(g.n_nodes, g.src, g.dst, g.comp, g.edge_cost, lab,
+                                          tl, bl, m)
+        assert (out["tl"][:, p] == tl).all(), p
+        assert (out["bl"][:, p] == bl).all(), p
+        assert out["makespan"][p] == m, p
+        assert (out["is_critical"][:, p] == crit).all(), p
+        assert (out["path"][p, : out["path_len"][p]] == path).all(), p
+    G.close()
+
+
 def test_evaluate_moves_small(P):
     """The fused moves entry point equals build_placements + evaluate_batch
     and the oracle, with repeated nodes, an empty step and an odd count."""

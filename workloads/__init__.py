@@ -16,4 +16,5 @@ from .graphs import (  # noqa: F401
     materialize_placements,
     random_dag,
     chain_graph,
+    layered_dag,
 )

@@ -528,3 +528,42 @@ def chain_graph(rng: np.random.Generator, n: int, n_labels: int = 2) -> SynthGra
     label = rng.integers(0, n_labels, n).astype(np.int32)
     return SynthGraph("chain", n, src, dst, comp, cost, mem, label, n_labels,
                       np.full(n_labels, 10_000, np.int64), {})
+
+
+def layered_dag(rng: np.random.Generator, widths, fan_in, max_span: int = 4,
+                max_weight: int = 50, n_labels: int = 4) -> SynthGraph:
+    """DAG built level by level: level k has widths[k] nodes; each node of a
+    level k >= 1 draws 1..fan_in[k] distinct predecessors, the first from
+    level k - 1 (so its level is exactly k) and the others from levels
+    k - 1 - U{0..max_span-1} (clamped at 0). Shapes the test cases need --
+    levels of exactly 64 / 65 nodes, wide levels read back at short spans,
+    levels with hundreds of edges on few nodes -- are set by the schedule.
+    Ids are permuted and edges shuffled."""
+    widths = [int(w) for w in widths]
+    lptr = np.concatenate([[0], np.cumsum(widths)]).astype(np.int64)
+    n = int(lptr[-1])
+    src, dst = [], []
+    for k in range(1, len(widths)):
+        for v in range(int(lptr[k]), int(lptr[k + 1])):
+            want = int(rng.integers(1, int(fan_in[k]) + 1))
+            preds = {int(rng.integers(lptr[k - 1], lptr[k]))}
+            tries = 0
+            while len(preds) < want and tries < 4 * want:
+                kk = max(0, k - 1 - int(rng.integers(0, max_span)))
+                preds.add(int(rng.integers(lptr[kk], lptr[kk + 1])))
+                tries += 1
+            for u in preds:
+                src.append(u)
+                dst.append(v)
+    perm = rng.permutation(n).astype(np.int64)
+    src = perm[np.asarray(src, np.int64)].astype(np.int32)
+    dst = perm[np.asarray(dst, np.int64)].astype(np.int32)
+    order = rng.permutation(src.shape[0])
+    src, dst = src[order], dst[order]
+    ne = src.shape[0]
+    comp = rng.integers(0, max_weight + 1, n).astype(np.int64)
+    cost = rng.integers(0, max_weight + 1, ne).astype(np.int64)
+    mem = rng.integers(0, 1000, n).astype(np.int64)
+    label = rng.integers(0, n_labels, n).astype(np.int32)
+    return SynthGraph("layered", n, src, dst, comp, cost, mem, label, n_labels,
+                      np.full(n_labels, 50_000, np.int64), {"levels": len(widths)})
