@@ -198,6 +198,7 @@ SweepArgs sweep_args(const Graph *g) {
     a.out_rec = g->out_rec;
     a.node_rec = g->node_rec;
     a.order = g->order;
+    a.rank = g->rank;
     a.err = g->err;
     return a;
 }

@@ -80,10 +80,11 @@ struct SweepArgs {
     const int64_t *comp_lm, *mem_lm;
     const EdgeRec16 *in_rec, *out_rec;   // t: {src, dst, cost} by dst; b: {dst, src, cost} by src
     const NodeRec16 *node_rec;
-    const int32_t *order;
+    const int32_t *order;   // level-major -> original id
+    const int32_t *rank;    // original id -> level-major
     const int32_t *lab_w;   // [slice][V][S] labels in level-major order
     int64_t *ftl, *bll;     // [slice][V][S] {value, label}: tl + comp, bl (packed or pairs)
-    int32_t *nx_w;          // [slice][V][S] level-major id of the chosen successor, or null
+    int32_t *nx_w;          // [slice][V][S] original id of the chosen successor (-1: none), or null
     int64_t ws_stride;      // elements of ftl / bll / nx_w per slice (>= V * S)
     int64_t *tl_out, *bl_out, *makespan;  // [V][P], [V][P], [P], caller's numbering
     int32_t *start;         // [P] level-major id where the critical path starts, or null

@@ -118,8 +118,9 @@ constexpr size_t sweep_lds_bytes() {
 // The b direction must also pick, among the successors reaching the max, the
 // one with the smallest original id (the next node of the critical path).
 // PACKED folds that into the max itself: key = (value << ob) | (omax - orig),
-// and the thread holding the winning key writes the successor link. Otherwise
-// a second LDS phase takes the min over the tied successors.
+// and the node phase reads the successor's original id back from the low
+// bits of the maximum. Otherwise a second LDS phase takes the min over the
+// tied successors.
 template <int S, int T, int ACC, bool FWD, bool PACKED>
 __device__ void sweep_dir(const SweepArgs &a, int32_t slice, char *smem) {
     constexpr bool DIRECT = S == 1;  // one placement: write tl/bl straight to the caller
@@ -261,14 +262,15 @@ __device__ void sweep_dir(const SweepArgs &a, int32_t slice, char *smem) {
             at(vals, (uint32_t)(v * S + s)) = out;
             if (nb_out) nb_out[slot] = out;
             if (DIRECT && p < P) a.bl_out[(int64_t)n.ord * P + p] = b;
+            // successor on the canonical path, as an original id: PACKED keys
+            // carry it in their low bits, else the tie phase left it in nacc
             if (want_nx) {
                 if (PACKED) {
-                    if (key == 0) at(nxb, (uint32_t)(v * S + s)) = -1;
+                    at(nxb, (uint32_t)(v * S + s)) = key == 0 ? -1 : (int32_t)(omax - (key & omax));
                 } else {
                     const unsigned long long k2 = nacc[slot];
                     nacc[slot] = ~0ull;
-                    at(nxb, (uint32_t)(v * S + s)) =
-                        k2 == ~0ull ? -1 : (int32_t)(k2 & 0xffffffffull);
+                    at(nxb, (uint32_t)(v * S + s)) = k2 == ~0ull ? -1 : (int32_t)(k2 >> 32);
                 }
             }
         }
@@ -376,20 +378,6 @@ __device__ void sweep_dir(const SweepArgs &a, int32_t slice, char *smem) {
                                     ((unsigned long long)(uint32_t)r.nbo << 32) | (uint32_t)r.nb);
                 }
                 __syncthreads();
-            } else if (want_nx) {
-                // PACKED b: the task holding the winning key names the successor
-                if (ev0 && k0v == accb[(A.r.e0.own - lo) * S + s0])
-                    at(nxb, (uint32_t)(A.r.e0.own * S + s0)) = A.r.e0.nb;
-                if (ev1 && k1v == accb[(A.r.e1.own - lo) * S + sB])
-                    at(nxb, (uint32_t)(A.r.e1.own * S + sB)) = A.r.e1.nb;
-                for (int32_t i = tid + 2 * T; i < nt; i += T) {
-                    const EdgeRec r = load_edge(ea + i / S);
-                    const int s = i % S;
-                    const ET g = nval(r, s);
-                    const int32_t slot = (r.own - lo) * S + s;
-                    if (akey(cand(g, sl[slot], r.c), r.nbo) == accb[slot])
-                        at(nxb, (uint32_t)(r.own * S + s)) = r.nb;
-                }
             }
             ET *nb_out = nbuf + buf * ACC * S;
             const int32_t nnt = (hi - lo) * S;
@@ -424,21 +412,17 @@ __device__ void sweep_dir(const SweepArgs &a, int32_t slice, char *smem) {
                                 akey(cand(g, at(lab, (uint32_t)(r.own * S + s)), r.c), r.nbo));
                 }
                 __syncthreads();
-                if (want_nx) {
+                if (tie_phase) {
                     for (int32_t i = tid; i < cnt; i += T) {
                         const EdgeRec r = load_edge(cea + i / S);
                         const int s = i % S;
                         const ET g = nval(r, s);
                         const int32_t slot = (r.own - cn0) * S + s;
-                        if (akey(cand(g, at(lab, (uint32_t)(r.own * S + s)), r.c), r.nbo) == accb[slot]) {
-                            if (tie_phase)
-                                lds_min_u64(&nacc[slot],
-                                            ((unsigned long long)(uint32_t)r.nbo << 32) | (uint32_t)r.nb);
-                            else
-                                at(nxb, (uint32_t)(r.own * S + s)) = r.nb;
-                        }
+                        if (akey(cand(g, at(lab, (uint32_t)(r.own * S + s)), r.c), r.nbo) == accb[slot])
+                            lds_min_u64(&nacc[slot],
+                                        ((unsigned long long)(uint32_t)r.nbo << 32) | (uint32_t)r.nb);
                     }
-                    if (tie_phase) __syncthreads();
+                    __syncthreads();
                 }
                 const int32_t cnn = (cn1 - cn0) * S;
                 for (int32_t i = tid; i < cnn; i += T) {
@@ -603,6 +587,9 @@ __device__ void chase_wave(const SweepArgs &a, int32_t p, int32_t *path, int32_t
 #pragma unroll
         for (int j = 0; j < PER; j++)
             tmp[j] = nx[(int64_t)min(base + lane + j * kWave, V - 1) * S + s];
+        // links hold original ids: their level-major positions come from rank
+#pragma unroll
+        for (int j = 0; j < PER; j++) tmp[j] = a.rank[tmp[j] < 0 ? 0 : tmp[j]] | (tmp[j] >> 31);
 #pragma unroll
         for (int j = 0; j < PER; j++)
             win[lane + j * kWave] = base + lane + j * kWave < V ? tmp[j] : -1;
