@@ -177,6 +177,71 @@ int ensure_levelized(Graph *g) {
     return PARDNN_OK;
 }
 
+// Near / far edge split of the batched sweeps, built once per graph.
+int ensure_pair(Graph *g) {
+    if (g->pl_t != nullptr) return PARDNN_OK;
+    const size_t E = (size_t)g->E;
+    int32_t *flag = nullptr, *rank = nullptr, *ws = nullptr;
+    auto cleanup = [&]() {
+        (void)hipStreamSynchronize(g->stream);
+        if (flag) (void)hipFree(flag);
+        if (rank) (void)hipFree(rank);
+        if (ws) (void)hipFree(ws);
+    };
+    hipError_t e = hipMalloc((void **)&flag, sizeof(int32_t) * (E + 1));
+    if (e == hipSuccess) e = hipMalloc((void **)&rank, sizeof(int32_t) * (E + 1));
+    if (e == hipSuccess)
+        e = hipMalloc((void **)&ws, sizeof(int32_t) * scan_workspace_elems((int32_t)E));
+    PairLevel *pl[2] = {nullptr, nullptr};
+    NearRec16 *nr[2] = {nullptr, nullptr};
+    FarRec16 *fr[2] = {nullptr, nullptr};
+    for (int d = 0; d < 2 && e == hipSuccess; d++) {
+        const bool fwd = d == 0;
+        e = launch_fill_i32(rank, (int64_t)E + 1, 0, g->stream);
+        if (e == hipSuccess && E > 0) e = launch_pair_flags(*g, fwd, flag);
+        if (e == hipSuccess && E > 0)
+            e = launch_exclusive_scan(flag, rank, (int32_t)E, ws, g->stream);
+        int32_t n_near = 0;
+        if (e == hipSuccess)
+            e = hipMemcpyAsync(&n_near, rank + E, sizeof(int32_t), hipMemcpyDeviceToHost,
+                               g->stream);
+        if (e == hipSuccess) e = hipStreamSynchronize(g->stream);
+        if (e == hipSuccess) e = dalloc(*g, &pl[d], (size_t)g->L + 2);
+        if (e == hipSuccess) e = dalloc(*g, &nr[d], (size_t)n_near);
+        if (e == hipSuccess) e = dalloc(*g, &fr[d], E - (size_t)n_near);
+        if (e == hipSuccess && !fwd) e = dalloc(*g, &g->ftie_b, E - (size_t)n_near);
+        if (e == hipSuccess)
+            e = launch_pair_split(*g, fwd, rank, pl[d], nr[d], fr[d], fwd ? nullptr : g->ftie_b);
+        // edges that wide levels fold early
+        if (e == hipSuccess) e = hipStreamSynchronize(g->stream);
+        if (e == hipSuccess) e = launch_fill_i32(rank, (int64_t)E + 1, 0, g->stream);
+        if (e == hipSuccess && E > 0) e = launch_pre_flags(*g, fwd, flag);
+        if (e == hipSuccess && E > 0)
+            e = launch_exclusive_scan(flag, rank, (int32_t)E, ws, g->stream);
+        int32_t n_pre = 0;
+        if (e == hipSuccess)
+            e = hipMemcpyAsync(&n_pre, rank + E, sizeof(int32_t), hipMemcpyDeviceToHost,
+                               g->stream);
+        if (e == hipSuccess) e = hipStreamSynchronize(g->stream);
+        int32_t *&preoff = fwd ? g->preoff_t : g->preoff_b;
+        PreRec16 *&pre = fwd ? g->pre_t : g->pre_b;
+        if (e == hipSuccess) e = dalloc(*g, &preoff, (size_t)g->L + 1);
+        if (e == hipSuccess) e = dalloc(*g, &pre, (size_t)n_pre);
+        if (e == hipSuccess && !fwd) e = dalloc(*g, &g->pretie_b, (size_t)n_pre);
+        if (e == hipSuccess)
+            e = launch_pre_split(*g, fwd, rank, preoff, pre, fwd ? nullptr : g->pretie_b);
+    }
+    cleanup();
+    if (e != hipSuccess) return fail(hip_status(e), std::string("batch structure: ") + hipGetErrorString(e));
+    g->pl_t = pl[0];
+    g->pl_b = pl[1];
+    g->nr_t = nr[0];
+    g->nr_b = nr[1];
+    g->fr_t = fr[0];
+    g->fr_b = fr[1];
+    return PARDNN_OK;
+}
+
 SweepArgs sweep_args(const Graph *g) {
     SweepArgs a{};
     a.V = g->V;
@@ -198,6 +263,8 @@ SweepArgs sweep_args(const Graph *g) {
     a.out_rec = g->out_rec;
     a.node_rec = g->node_rec;
     a.order = g->order;
+    a.level = g->level;
+    a.level_ptr = g->level_ptr;
     a.rank = g->rank;
     a.err = g->err;
     return a;
@@ -320,7 +387,24 @@ int evaluate_impl(Graph *g, int32_t n_place, const int32_t *placements, const Mo
     a.lb = lb;
     a.ob = ob;
     a.ws_stride = ws_stride;
-    {
+    if (lb > 0 && g->V > 0) {
+        st = ensure_pair(g);
+        if (st != PARDNN_OK) return st;
+        a.pl_t = g->pl_t;
+        a.pl_b = g->pl_b;
+        a.nr_t = g->nr_t;
+        a.nr_b = g->nr_b;
+        a.fr_t = g->fr_t;
+        a.fr_b = g->fr_b;
+        a.ftie_b = g->ftie_b;
+        a.preoff_t = g->preoff_t;
+        a.preoff_b = g->preoff_b;
+        a.pre_t = g->pre_t;
+        a.pre_b = g->pre_b;
+        a.pretie_b = g->pretie_b;
+        TimedLaunch t(g, "k_sweep_pair<2>");
+        HIP_TRY(launch_sweep_pair(a, g->stream));
+    } else {
         TimedLaunch t(g, "k_sweep<2>");
         HIP_TRY(launch_sweep(a, S, g->stream));
     }

@@ -17,6 +17,10 @@
 //     comp_lm, mem_lm int64[V]
 //     in_rec, out_rec EdgeRec16[E] and node_rec NodeRec16[V]: the same data
 //       as 16-byte records, so a sweep task loads its edge with one load
+//     pl_t / pl_b PairLevel[L+2], nr_t / nr_b NearRec16[], fr_t / fr_b
+//       FarRec16[], ftie_b int32[]: the edges of each level split into span-1
+//       ("near") and longer ("far") edges for the batched sweeps, per
+//       direction; built on first use
 //   linfo has L + 2 entries: entry L + 1 repeats entry L, so the pair
 //   (linfo[x], linfo[x + 1]) of an empty level can be read at x = L.
 #pragma once
@@ -45,6 +49,47 @@ struct alignas(16) EdgeRec16 {
     int32_t own;
     int64_t cost;
 };
+
+// Batched sweeps: per level and direction, the first node and the first
+// near / far edge record (entries L and L + 1 hold the totals).
+struct alignas(16) PairLevel {
+    int32_t node_lo, near_lo, far_lo, pad;
+};
+// A span-1 edge: owner's and neighbour's index inside their levels
+// (own | nb << 16), the successor tie-break key 2^ob - 1 - successor's
+// original id (b direction; 0 for t) and the cost.
+struct alignas(16) NearRec16 {
+    uint32_t ol;
+    int32_t tie;
+    int64_t cost;
+};
+// A longer edge: the neighbour (level-major id), the owner's index inside its
+// level and the neighbour's entry in the LDS ring of recent levels
+// (own | ring << 16; kNoRing: read the workspace; kPreFolded: folded by the
+// general path of the neighbour's level, which is too wide for the ring) and
+// the cost.
+struct alignas(16) FarRec16 {
+    int32_t nb;
+    uint32_t ol;
+    int64_t cost;
+};
+constexpr uint32_t kNoRing = 0xffffu;
+constexpr uint32_t kPreFolded = 0xfffeu;
+// An edge folded early by the general path of its neighbour's (wide) level:
+// the neighbour, the owner's index in its level and the span (own | span << 16)
+// and the cost; grouped by the neighbour's level (pre_off).
+struct alignas(16) PreRec16 {
+    int32_t nb;
+    uint32_t os;
+    int64_t cost;
+};
+
+// Bits that hold a node id in the b-direction keys: 2^bits > V.
+inline int32_t succ_bits(int32_t V) {
+    int32_t b = 1;
+    while ((1ll << b) <= (int64_t)V) b++;
+    return b;
+}
 
 // Per-node constants of the sweeps, level-major.
 struct alignas(16) NodeRec16 {
@@ -81,11 +126,20 @@ struct SweepArgs {
     const EdgeRec16 *in_rec, *out_rec;   // t: {src, dst, cost} by dst; b: {dst, src, cost} by src
     const NodeRec16 *node_rec;
     const int32_t *order;   // level-major -> original id
+    const int32_t *level;   // original id -> level
+    const int32_t *level_ptr;  // first level-major node of each level
     const int32_t *rank;    // original id -> level-major
     const int32_t *lab_w;   // [slice][V][S] labels in level-major order
     int64_t *ftl, *bll;     // [slice][V][S] {value, label}: tl + comp, bl (packed or pairs)
     int32_t *nx_w;          // [slice][V][S] original id of the chosen successor (-1: none), or null
     int64_t ws_stride;      // elements of ftl / bll / nx_w per slice (>= V * S)
+    const PairLevel *pl_t, *pl_b;         // batched sweeps: near / far split per level
+    const NearRec16 *nr_t, *nr_b;
+    const FarRec16 *fr_t, *fr_b;
+    const int32_t *ftie_b;
+    const int32_t *preoff_t, *preoff_b;   // [L + 1] per neighbour level
+    const PreRec16 *pre_t, *pre_b;
+    const int32_t *pretie_b;
     int64_t *tl_out, *bl_out, *makespan;  // [V][P], [V][P], [P], caller's numbering
     int32_t *start;         // [P] level-major id where the critical path starts, or null
     int64_t *label_mem;     // [P][K], zeroed by the caller, or null
@@ -117,6 +171,13 @@ struct Graph {
     int64_t *comp_lm = nullptr, *mem_lm = nullptr;
     EdgeRec16 *in_rec = nullptr, *out_rec = nullptr;
     NodeRec16 *node_rec = nullptr;
+    PairLevel *pl_t = nullptr, *pl_b = nullptr;   // built on first batched evaluation
+    NearRec16 *nr_t = nullptr, *nr_b = nullptr;
+    FarRec16 *fr_t = nullptr, *fr_b = nullptr;
+    int32_t *ftie_b = nullptr;
+    int32_t *preoff_t = nullptr, *preoff_b = nullptr;
+    PreRec16 *pre_t = nullptr, *pre_b = nullptr;
+    int32_t *pretie_b = nullptr;
 
     // single-placement scratch
     int32_t *lab_lm = nullptr, *next_lm = nullptr, *move_stamp = nullptr;
@@ -168,6 +229,20 @@ hipError_t launch_permute_labels_batch(const Graph &g, const int32_t *placements
 hipError_t launch_sweep(const SweepArgs &a, int32_t S, hipStream_t s);
 hipError_t launch_finish(const SweepArgs &a, int32_t S, uint8_t *crit, int32_t *path,
                          int32_t stride, int32_t *path_len, hipStream_t s);
+
+// ---- sweep_pair.hip ----
+// flag[e] = 1 for the span-1 edges of the direction's level-major edge order
+hipError_t launch_pair_flags(const Graph &g, bool fwd, int32_t *flag);
+// near_rank = exclusive scan of flag (E + 1 entries); fills pl, nr, fr, ftie
+hipError_t launch_pair_split(const Graph &g, bool fwd, const int32_t *near_rank, PairLevel *pl,
+                             NearRec16 *nr, FarRec16 *fr, int32_t *ftie);
+// flag[e] = 1 for the edges a wide level folds early (neighbour-grouped order)
+hipError_t launch_pre_flags(const Graph &g, bool fwd, int32_t *flag);
+// rank = exclusive scan of those flags; fills preoff [L + 1], pre, pretie
+hipError_t launch_pre_split(const Graph &g, bool fwd, const int32_t *rank, int32_t *preoff,
+                            PreRec16 *pre, int32_t *pretie);
+// Packed {value, label} only (a.lb > 0).
+hipError_t launch_sweep_pair(const SweepArgs &a, hipStream_t s);
 
 // ---- critpath.hip ----
 hipError_t launch_critical_path(const Graph &g, const int32_t *placement, const int64_t *tl,

@@ -1,0 +1,740 @@
+// sweep_pair.hip -- batched t-level / b-level sweeps (paper Table 2; Alg. 1
+// compute_weighted_levels) over many placements of one graph.
+//
+//   tl(v) = max over in-edges (u,v) of tl(u) + comp(u) + c(u,v)     (0 if none)
+//   bl(v) = comp(v) + max over out-edges (v,s) of c(v,s) + bl(s)     (comp(v) if none)
+//   c(u,v) = 0 when both ends carry the same label, else edge_cost  (Fig. 2
+//            caption: communication inside a cluster counts as zero)
+//
+// Design for gfx950. A sweep is a chain of L dependent level steps. One
+// workgroup of TWO waves walks one chain for S placements, with ONE barrier
+// per level:
+//   wave 0 ("near"): finalises level i from its LDS accumulators (value, label
+//     sums, successor), writes the values to an LDS ring and the workspace,
+//     then folds the span-1 edges of level i + 1 -- whose neighbours it has
+//     just finalised -- into the accumulators of level i + 1;
+//   wave 1 ("far"):  meanwhile folds the longer edges of level i + 1, whose
+//     neighbours were final one or more barriers ago: from the LDS ring when
+//     they finished in the last D levels, else from registers loaded D levels
+//     ahead.
+// So the dependent path of a level is one LDS round trip for the
+// accumulators, one for the ring, the arithmetic and one barrier; the global
+// loads all run ahead:
+//   near wave: node constants, labels and span-1 edge records LN levels ahead;
+//   far wave:  edge records D + RF levels ahead, neighbour values D ahead.
+// The register state of the levels in flight rotates by name through an
+// NS-times unrolled loop, and every global load and store of a fast level is
+// unconditional (clamped addresses; idle lanes store into the slice's
+// padding), so the in-order wait counters never drain the pipeline.
+//
+// The b keys carry the successor tie-break in their low bits,
+// (value << ob) | (2^ob - 1 - successor's original id), so the maximum names
+// the canonical successor. Levels outside the fast shape (more than 64
+// nodes, 64 * kNEn span-1 edges or 64 * kNEf longer edges) take a general
+// path that drains the workgroup, processes the level in chunks from the
+// workspace, and refills the pipeline.
+#include "device_utils.h"
+#include "internal.h"
+#include "sweep_common.h"
+
+namespace pardnn {
+
+namespace {
+
+constexpr int kLanes = 64;
+constexpr int kPNodes = 64;          // nodes of a fast level, one per lane of wave 0
+constexpr int kNEn = 2;              // span-1 edge tasks per lane of wave 0
+constexpr int kNEf = 3;              // longer-edge tasks per lane of wave 1
+constexpr int kD = 3;                // far values loaded D levels ahead
+constexpr int kRF = 2;               // far records loaded RF levels before their values
+constexpr int kNS = kD + kRF + 2;    // register sets in flight (loop unrolling)
+constexpr int kLN = kNS - 2;         // wave 0 loads LN levels ahead
+constexpr int kRS = kD + 1;          // LDS ring slots (levels)
+constexpr int kNB = kD + 2;          // accumulator buffers (levels)
+constexpr int kPBinsCap = 2048;      // labels x slots of the LDS label bins
+// label sums of the t sweep: none, in LDS bins (K S <= kPBinsCap), or by
+// global atomics; a template parameter, so that a chain carries one of them
+constexpr int kBinsNone = 0, kBinsLds = 1, kBinsGlobal = 2;
+
+typedef const __attribute__((address_space(4))) PairLevel *ConstPairLevel;
+typedef const __attribute__((address_space(4))) SweepArgs KArgs;
+
+// The kernel's argument block (its only argument, at offset 0 of the kernarg
+// segment) through a pointer the compiler cannot see through, so that loads
+// from it stay where they are written: the general level path re-reads its
+// pointers inside its branch instead of keeping them live across the loop.
+__device__ __forceinline__ KArgs *kargs_here() {
+    KArgs *p = (KArgs *)__builtin_amdgcn_kernarg_segment_ptr();
+    asm volatile("" : "+s"(p));
+    return p;
+}
+
+template <int I>
+struct IC {
+    static constexpr int value = I;
+};
+
+// S values / labels of one node (its S placements), adjacent in memory.
+template <int S>
+struct alignas(S * 8 >= 16 ? 16 : S * 8) VecS {
+    int64_t v[S];
+};
+template <int S>
+struct alignas(4 * S >= 16 ? 16 : 4 * S) LabS {
+    int32_t v[S];
+};
+
+// Level bounds of one step as staged in the LDS window: first node, first
+// near and far record, and the three counts saturated at 255 (enough to tell
+// a fast level; the general path reads exact bounds).
+struct alignas(16) WinEnt {
+    int32_t nlo, nrlo, frlo;
+    uint32_t cnt;   // min(w,255) | min(near,255) << 8 | min(far,255) << 16
+};
+constexpr int kWin = 128;            // window entries (steps); refilled every kWin / 2
+
+__device__ __forceinline__ int32_t cnt_w(uint32_t c) { return (int32_t)(c & 255u); }
+__device__ __forceinline__ int32_t cnt_near(uint32_t c) { return (int32_t)((c >> 8) & 255u); }
+__device__ __forceinline__ int32_t cnt_far(uint32_t c) { return (int32_t)((c >> 16) & 255u); }
+__device__ __forceinline__ bool cnt_fast(uint32_t c) {
+    return cnt_w(c) <= kPNodes && cnt_near(c) <= kNEn * kLanes && cnt_far(c) <= kNEf * kLanes;
+}
+
+template <int S>
+struct NearSet {   // wave 0, one level
+    uint32_t ol[kNEn];
+    int32_t tie[kNEn];
+    int64_t c[kNEn];
+    int64_t comp, mem;
+    LabS<S> lab;
+};
+
+template <int S>
+struct FarSet {    // wave 1, one level
+    int32_t nb[kNEf];
+    uint32_t ol[kNEf];
+    int64_t c[kNEf];
+    int32_t tie[kNEf];
+    VecS<S> f[kNEf];
+};
+
+template <int S>
+constexpr size_t pair_lds_fixed() {
+    return (size_t)kWin * sizeof(WinEnt)        // bounds window
+           + (size_t)kNB * kPNodes * S * 8       // acc[kNB]
+           + (size_t)kRS * kPNodes * S * 8       // ring
+           + (size_t)2 * kPNodes * S * 4;        // slab[2]
+}
+
+// Everything a chain derives from the arguments: the slice's workspace, the
+// LDS layout and the value encoding.
+template <int S, bool FWD, int BM>
+struct PairCtx {
+    static constexpr bool want_bins = FWD && BM != kBinsNone;
+    static constexpr bool lds_bins = FWD && BM == kBinsLds;
+    using EL = Elem<true>;
+    using VS = VecS<S>;
+    using LS = LabS<S>;
+    int lane, tid;
+    int32_t V, L, P, K, p0;
+    int lb, ob;
+    long long omax;
+    VS *vals;
+    const LS *labs;
+    LS *nxs;
+    bool want_nx;
+    ConstPairLevel pls;
+    WinEnt *win;
+    long long *acc;
+    VS *ring;
+    LS *slab;
+    long long *bins;
+
+    template <class AP>
+    __device__ __forceinline__ PairCtx(AP a, int32_t slice, char *smem) {
+        lane = lane_id();
+        tid = threadIdx.x;   // 0 .. 127 over both waves
+        V = a->V;
+        L = a->L;
+        P = a->P;
+        K = a->K;
+        p0 = slice * S;
+        lb = a->lb;
+        ob = FWD ? 0 : a->ob;
+        omax = (1ll << ob) - 1;
+        vals = reinterpret_cast<VS *>((FWD ? a->ftl : a->bll) + (int64_t)slice * a->ws_stride);
+        labs = reinterpret_cast<const LS *>(a->lab_w + (int64_t)slice * V * S);
+        want_nx = !FWD && a->nx_w != nullptr;
+        nxs = reinterpret_cast<LS *>(a->nx_w + (want_nx ? (int64_t)slice * a->ws_stride : 0));
+        pls = (ConstPairLevel)(FWD ? a->pl_t : a->pl_b);
+        win = reinterpret_cast<WinEnt *>(smem);                       // [kWin]
+        acc = reinterpret_cast<long long *>(win + kWin);              // [kNB][64 S]
+        ring = reinterpret_cast<VS *>(acc + kNB * kPNodes * S);       // [kRS][64]
+        slab = reinterpret_cast<LS *>(ring + kRS * kPNodes);           // [2][64]
+        bins = reinterpret_cast<long long *>(slab + 2 * kPNodes);     // [K S]
+    }
+    __device__ __forceinline__ int64_t cand(int64_t g, int32_t own_lab, int64_t c) const {
+        return EL::val(g, lb) + (EL::lab(g, lb) != own_lab ? c : 0);
+    }
+    __device__ __forceinline__ long long akey(int64_t cv, int32_t tie) const {
+        return FWD ? cv : (cv << ob) | tie;
+    }
+    __device__ __forceinline__ int32_t level_of(int32_t step) const {   // L: empty level
+        if (FWD) return step < L ? step : L;
+        return step < L ? L - 1 - step : L;
+    }
+    __device__ __forceinline__ WinEnt W(int32_t step) const { return win[step & (kWin - 1)]; }
+    __device__ __forceinline__ long long *accb(int32_t step) const {
+        return acc + (step % kNB) * kPNodes * S;
+    }
+
+    // finalise node v (slot = its index in the level) from the level's
+    // accumulators: value, successor, ring entry, label sums, workspace
+    __device__ __forceinline__ void finish(int64_t *label_mem, int32_t step, int32_t v, bool act,
+                                           bool to_ring, int slot, int64_t comp, int64_t mem,
+                                           const LS &lab) const {
+        long long *ab = accb(step);
+        VS out;
+        LS nxv;
+#pragma unroll
+        for (int s = 0; s < S; s++) {
+            const long long k = ab[slot * S + s];
+            const int64_t t = FWD ? k : k >> ob;
+            out.v[s] = EL::make(FWD ? t + comp : comp + t, lab.v[s], lb);
+            nxv.v[s] = k == 0 ? -1 : (int32_t)(omax - (k & omax));
+        }
+#pragma unroll
+        for (int s = 0; s < S; s++) ab[slot * S + s] = 0;
+        if (act) {
+            if (to_ring) ring[(step % kRS) * kPNodes + slot] = out;
+            if constexpr (want_bins) {
+#pragma unroll
+                for (int s = 0; s < S; s++) {
+                    const int32_t l = lab.v[s];
+                    if ((uint32_t)l < (uint32_t)K && p0 + s < P) {
+                        if constexpr (lds_bins)
+                            lds_add_i64(&bins[l * S + s], mem);
+                        else
+                            atomicAdd((unsigned long long *)&label_mem[(int64_t)(p0 + s) * K + l],
+                                      (unsigned long long)mem);
+                    }
+                }
+            }
+        }
+        const uint32_t sv = act ? (uint32_t)v : (uint32_t)V;   // idle lanes: one padding slot
+        at(vals, sv) = out;
+        if (want_nx) at(nxs, sv) = nxv;
+    }
+};
+
+// The general level step, for both waves: the level in chunks of 64 nodes
+// from the workspace, the early folds of a level too wide for the ring, and
+// the next level's edges. Everything it reads from the arguments is read
+// afresh through kargs_here(), so that the pipelined loop around it does not
+// carry its pointers in registers.
+template <int S, bool FWD, bool NEAR, int BM>
+__device__ __forceinline__ void pair_slow(int32_t slice, int32_t step, char *smem) {
+    KArgs *a = kargs_here();
+    const PairCtx<S, FWD, BM> c(a, slice, smem);
+    using VS = VecS<S>;
+    using LS = LabS<S>;
+    __builtin_amdgcn_s_waitcnt(0);
+    __syncthreads();
+    const int32_t *offs = FWD ? a->in_off : a->out_off;
+    const int32_t *srcs = FWD ? a->in_src : a->out_dst;
+    const int32_t *owns = FWD ? a->in_dst : a->out_src;
+    const int64_t *costs = FWD ? a->in_cost : a->out_cost;
+    const int32_t x = c.level_of(step), xn = c.level_of(step + 1);
+    const int32_t lo = c.pls[x].node_lo, hi = c.pls[x + 1].node_lo;
+    const bool to_ring = hi - lo <= kPNodes;
+    const uint32_t vmax = (uint32_t)(c.V - 1);
+    auto fold = [&](int32_t cn0, int32_t cea, int32_t ceb, long long *ab) {
+        for (int32_t e = cea + c.tid; e < ceb; e += 2 * kLanes) {
+            const int32_t nb = srcs[e], own = owns[e] - cn0;
+            const int64_t cost = costs[e];
+            const int32_t tie = FWD ? 0 : (int32_t)(c.omax - a->out_dst_orig[e]);
+            const VS g = c.vals[nb];
+            const LS ol = c.labs[cn0 + own];
+#pragma unroll
+            for (int s = 0; s < S; s++)
+                lds_max_i64(&ab[own * S + s], c.akey(c.cand(g.v[s], ol.v[s], cost), tie));
+        }
+    };
+    for (int32_t cn0 = lo; cn0 < hi; cn0 += kPNodes) {
+        const int32_t cn1 = min(hi, cn0 + kPNodes);
+        fold(cn0, offs[cn0], offs[cn1], c.accb(step));
+        __syncthreads();
+        if (NEAR) {
+            const int32_t v = cn0 + c.lane;
+            const uint32_t vc = min((uint32_t)v, vmax);
+            const NodeRec16 nr = at(a->node_rec, vc);
+            c.finish(a->label_mem, step, v, v < cn1, to_ring, c.lane, nr.comp, nr.mem, at(c.labs, vc));
+        }
+        __syncthreads();
+    }
+    // a level too wide for the ring: fold its edges of span 2 .. D + 1 now
+    // into the accumulators of their (narrow) owners' levels; the far records
+    // mark them kPreFolded
+    if (!to_ring) {
+        const int32_t *poff = FWD ? a->preoff_t : a->preoff_b;
+        const PreRec16 *pre = FWD ? a->pre_t : a->pre_b;
+        for (int32_t e = poff[x] + c.tid; e < poff[x + 1]; e += 2 * kLanes) {
+            const PreRec16 r = pre[e];
+            const int32_t own = (int32_t)(r.os & 0xffffu), span = (int32_t)(r.os >> 16);
+            const int32_t tie = FWD ? 0 : a->pretie_b[e];
+            const VS g = c.vals[r.nb];
+            const LS ol = c.labs[c.W(step + span).nlo + own];
+            long long *ab = c.accb(step + span);
+#pragma unroll
+            for (int s = 0; s < S; s++)
+                lds_max_i64(&ab[own * S + s], c.akey(c.cand(g.v[s], ol.v[s], r.cost), tie));
+        }
+    }
+    // the next level's edges, all from the workspace (everything before it is
+    // final now), unless that level takes this path itself
+    if (cnt_fast(c.W(step + 1).cnt)) {
+        const int32_t nlo = c.pls[xn].node_lo, nhi = c.pls[xn + 1].node_lo;
+        fold(nlo, offs[nlo], offs[nhi], c.accb(step + 1));
+    }
+}
+
+template <int S, bool FWD, bool NEAR, int BM>
+__device__ __forceinline__ void pair_chain(const SweepArgs &a, int32_t slice, char *smem) {
+    using EL = Elem<true>;
+    using VS = VecS<S>;
+    using LS = LabS<S>;
+    const PairCtx<S, FWD, BM> c(&a, slice, smem);
+    const int lane = c.lane;
+    const int32_t L = c.L;
+    const uint32_t vmax = c.V > 0 ? (uint32_t)(c.V - 1) : 0u;
+    const PairLevel *plv = FWD ? a.pl_t : a.pl_b;   // per-lane reads
+
+    // window entries for steps s0 + lane + 64 k, k < n (wave 0, synchronous)
+    auto fill = [&](int32_t s0, int n) {
+        for (int k = 0; k < n; k++) {
+            const int32_t sx = s0 + lane + k * kLanes;
+            const int32_t x = c.level_of(sx);
+            const PairLevel l0 = plv[x], l1 = plv[x + 1];
+            WinEnt e;
+            e.nlo = l0.node_lo;
+            e.nrlo = l0.near_lo;
+            e.frlo = l0.far_lo;
+            e.cnt = (uint32_t)min(l1.node_lo - l0.node_lo, 255) |
+                    (uint32_t)min(l1.near_lo - l0.near_lo, 255) << 8 |
+                    (uint32_t)min(l1.far_lo - l0.far_lo, 255) << 16;
+            c.win[sx & (kWin - 1)] = e;
+        }
+    };
+
+    if (NEAR) {
+        // ================= wave 0: finalise + span-1 edges =================
+        const NearRec16 *nrec = FWD ? a.nr_t : a.nr_b;
+        NearSet<S> st[kNS];
+        // unconditional loads (idle lanes read element 0), so that the
+        // compiler's in-order wait counts are the same on every path
+        auto loads = [&](NearSet<S> &X, const WinEnt &b) {
+            const int32_t nn = cnt_near(b.cnt), w = cnt_w(b.cnt);
+#pragma unroll
+            for (int j = 0; j < kNEn; j++) {
+                const uint32_t e = lane + j * kLanes < nn ? (uint32_t)(b.nrlo + lane + j * kLanes) : 0u;
+                const NearRec16 r = at(nrec, e);
+                X.ol[j] = r.ol;
+                X.tie[j] = r.tie;
+                X.c[j] = r.cost;
+            }
+            const uint32_t v = lane < w ? (uint32_t)(b.nlo + lane) : 0u;
+            const NodeRec16 n = at(a.node_rec, v);
+            X.comp = n.comp;
+            X.mem = n.mem;
+            X.lab = at(c.labs, v);
+        };
+        // after level `step`: labels of step + 2, loads of step + LN, window refill
+        auto tail = [&](int32_t step, const NearSet<S> &B2, NearSet<S> &LD, const WinEnt &b2,
+                        const WinEnt &bl) {
+            if (lane < cnt_w(b2.cnt)) c.slab[(step & 1) * kPNodes + lane] = B2.lab;
+            loads(LD, bl);
+            if ((step & (kWin / 2 - 1)) == 0 && step > 0) fill(step + kWin / 2, 1);
+            __syncthreads();
+        };
+        auto body = [&](int32_t step, const WinEnt &b0, const WinEnt &b1, NearSet<S> &A,
+                        const NearSet<S> &B1) {
+            c.finish(a.label_mem, step, b0.nlo + lane, lane < cnt_w(b0.cnt), true, lane, A.comp, A.mem,
+                     A.lab);
+            // span-1 edges of the next level, from the ring slot just written
+            if (cnt_fast(b1.cnt)) {
+                const int32_t nt = cnt_near(b1.cnt);
+                long long *ab = c.accb(step + 1);
+                const LS *sl = c.slab + ((step + 1) & 1) * kPNodes;
+                const VS *rs = c.ring + (step % kRS) * kPNodes;
+#pragma unroll
+                for (int j = 0; j < kNEn; j++) {
+                    if (lane + j * kLanes < nt) {
+                        const uint32_t own = B1.ol[j] & 0xffffu, nbl = B1.ol[j] >> 16;
+                        const VS g = rs[nbl];
+                        const LS ol = sl[own];
+#pragma unroll
+                        for (int s = 0; s < S; s++)
+                            lds_max_i64(&ab[own * S + s],
+                                        c.akey(c.cand(g.v[s], ol.v[s], B1.c[j]), B1.tie[j]));
+                    }
+                }
+            }
+        };
+        if (L > 0) {
+            fill(0, kWin / kLanes);
+            __builtin_amdgcn_s_waitcnt(0);
+#pragma unroll
+            for (int j = 0; j < kLN; j++) loads(st[j], c.W(j));
+            for (int i = lane; i < kNB * kPNodes * S; i += kLanes) c.acc[i] = 0;
+            if (c.lds_bins)
+                for (int i = lane; i < c.K * S; i += kLanes) c.bins[i] = 0;
+            __builtin_amdgcn_s_waitcnt(0);
+            if (lane < cnt_w(c.W(1).cnt)) c.slab[kPNodes + lane] = st[1].lab;
+        }
+        __syncthreads();
+        int32_t step = 0;
+        auto one = [&](auto RC) {
+            constexpr int r = decltype(RC)::value;
+            if constexpr (r < kNS) {
+                const WinEnt b0 = c.W(step), b1 = c.W(step + 1), b2 = c.W(step + 2),
+                             bl = c.W(step + kLN);
+                if (cnt_fast(b0.cnt))
+                    body(step, b0, b1, st[r], st[(r + 1) % kNS]);
+                else
+                    pair_slow<S, FWD, true, BM>(c.p0 / S, step, reinterpret_cast<char *>(c.win));
+                tail(step, st[(r + 2) % kNS], st[(r + kLN) % kNS], b2, bl);
+                step++;
+            }
+        };
+        // whole groups of kNS levels only: an exit inside the unrolled group
+        // would merge every body's loads in flight into the loop header
+        while (step + kNS <= L) {
+            one(IC<0>{});
+            one(IC<1>{});
+            one(IC<2>{});
+            one(IC<3>{});
+            one(IC<4>{});
+            one(IC<5>{});
+            one(IC<6>{});
+            one(IC<7>{});
+        }
+        // the last levels (fewer than kNS) on the general path; folding an
+        // edge a second time into a maximum changes nothing
+        for (; step < L; step++) {
+            pair_slow<S, FWD, true, BM>(c.p0 / S, step, reinterpret_cast<char *>(c.win));
+            __syncthreads();
+        }
+    } else {
+        // ================= wave 1: longer edges =================
+        const FarRec16 *frec = FWD ? a.fr_t : a.fr_b;
+        FarSet<S> st[kNS];
+        auto records = [&](FarSet<S> &X, const WinEnt &b) {
+            const int32_t nf = cnt_far(b.cnt);
+#pragma unroll
+            for (int j = 0; j < kNEf; j++) {
+                const uint32_t e = lane + j * kLanes < nf ? (uint32_t)(b.frlo + lane + j * kLanes) : 0u;
+                const FarRec16 r = at(frec, e);
+                X.nb[j] = r.nb;
+                X.ol[j] = r.ol;
+                X.c[j] = r.cost;
+                X.tie[j] = FWD ? 0 : at(a.ftie_b, e);
+            }
+        };
+        auto far_loads = [&](FarSet<S> &X, const WinEnt &b) {
+            const int32_t nt = cnt_far(b.cnt);
+#pragma unroll
+            for (int j = 0; j < kNEf; j++) {
+                const bool far = lane + j * kLanes < nt && (X.ol[j] >> 16) == kNoRing;
+                X.f[j] = at(c.vals, far ? (uint32_t)X.nb[j] : 0u);
+            }
+        };
+        auto fold_far = [&](int32_t step, const FarSet<S> &B1, const WinEnt &b1) {
+            const int32_t nt = cnt_far(b1.cnt);
+            long long *ab = c.accb(step + 1);
+            const LS *sl = c.slab + ((step + 1) & 1) * kPNodes;
+#pragma unroll
+            for (int j = 0; j < kNEf; j++) {
+                if (lane + j * kLanes < nt && (B1.ol[j] >> 16) != kPreFolded) {
+                    const uint32_t own = B1.ol[j] & 0xffffu, rg = B1.ol[j] >> 16;
+                    const VS g = rg != kNoRing ? c.ring[rg] : B1.f[j];
+                    const LS ol = sl[own];
+#pragma unroll
+                    for (int s = 0; s < S; s++)
+                        lds_max_i64(&ab[own * S + s],
+                                    c.akey(c.cand(g.v[s], ol.v[s], B1.c[j]), B1.tie[j]));
+                }
+            }
+        };
+        __syncthreads();   // the window is filled by wave 0
+        if (L > 0) {
+#pragma unroll
+            for (int j = 1; j <= kD + kRF; j++) records(st[j], c.W(j));
+#pragma unroll
+            for (int j = 1; j <= kD; j++)
+#pragma unroll
+                for (int t = 0; t < kNEf; t++) st[j].f[t] = VS{};
+            // nothing may be pending at the loop entry: a load in flight into a
+            // register the loop reuses would make the loop header wait for it
+            __builtin_amdgcn_s_waitcnt(0);
+        }
+        int32_t step = 0;
+        auto one = [&](auto RC) {
+            constexpr int r = decltype(RC)::value;
+            if constexpr (r < kNS) {
+                const WinEnt b0 = c.W(step), b1 = c.W(step + 1), bd = c.W(step + 1 + kD),
+                             brf = c.W(step + 1 + kD + kRF);
+                FarSet<S> &B1 = st[(r + 1) % kNS];
+                if (cnt_fast(b0.cnt)) {
+                    if (cnt_fast(b1.cnt)) fold_far(step, B1, b1);
+                } else {
+                    pair_slow<S, FWD, false, BM>(c.p0 / S, step, reinterpret_cast<char *>(c.win));
+                }
+                // far values in flight stay valid across a general-path level:
+                // a far edge either spans more than D + 1 levels or was folded
+                // early by its wide level
+                far_loads(st[(r + 1 + kD) % kNS], bd);
+                records(st[(r + 1 + kD + kRF) % kNS], brf);
+                __syncthreads();
+                step++;
+            }
+        };
+        while (step + kNS <= L) {
+            one(IC<0>{});
+            one(IC<1>{});
+            one(IC<2>{});
+            one(IC<3>{});
+            one(IC<4>{});
+            one(IC<5>{});
+            one(IC<6>{});
+            one(IC<7>{});
+        }
+        for (; step < L; step++) {
+            pair_slow<S, FWD, false, BM>(c.p0 / S, step, reinterpret_cast<char *>(c.win));
+            __syncthreads();
+        }
+    }
+
+    __builtin_amdgcn_s_waitcnt(0);
+    __syncthreads();
+    if (FWD) {
+        if (c.lds_bins && NEAR)
+            for (int i = lane; i < c.K * S; i += kLanes) {
+                const int l = i / S, s = i % S;
+                if (c.p0 + s < c.P) a.label_mem[(int64_t)(c.p0 + s) * c.K + l] = c.bins[i];
+            }
+        return;
+    }
+    if (!NEAR) return;
+    // b: makespan M = max over v of tl + bl is reached at a node without
+    // predecessors (tl = 0 there), i.e. at level 0; the path starts at the
+    // smallest-id such node with bl == M (level 0 is sorted by id).
+    const int32_t n0 = L > 0 ? c.pls[1].node_lo : 0;
+#pragma unroll
+    for (int s = 0; s < S; s++) {
+        long long m = 0;
+        for (int32_t i = lane; i < n0; i += kLanes) {
+            const long long x = EL::val(c.vals[i].v[s], c.lb);
+            m = x > m ? x : m;
+        }
+        m = wave_max_i64(m);
+        int32_t first = INT32_MAX;
+        for (int32_t i = lane; i < n0; i += kLanes)
+            if (EL::val(c.vals[i].v[s], c.lb) == m) first = min(first, i);
+#pragma unroll
+        for (int off = kLanes / 2; off > 0; off >>= 1) first = min(first, __shfl_xor(first, off, kLanes));
+        if (lane == 0 && c.p0 + s < c.P) {
+            a.makespan[c.p0 + s] = m;
+            if (a.start) a.start[c.p0 + s] = first == INT32_MAX ? -1 : first;
+        }
+    }
+    (void)vmax;
+}
+
+template <int S, int BM>
+__global__ __launch_bounds__(2 * kLanes) void k_sweep_pair(SweepArgs a) {
+    extern __shared__ __align__(16) char smem[];
+    const int32_t n_slices = (a.P + S - 1) / S;
+    const bool fwd = (int32_t)blockIdx.x >= n_slices;
+    const int32_t slice = fwd ? blockIdx.x - n_slices : blockIdx.x;
+    if (wave_id() == 0) {
+        if (fwd)
+            pair_chain<S, true, true, BM>(a, slice, smem);
+        else
+            pair_chain<S, false, true, kBinsNone>(a, slice, smem);
+    } else {
+        if (fwd)
+            pair_chain<S, true, false, BM>(a, slice, smem);
+        else
+            pair_chain<S, false, false, kBinsNone>(a, slice, smem);
+    }
+}
+
+// ---- structure: split each level's edges into span-1 and longer edges ----
+__global__ void k_pair_flags(int64_t E, bool fwd, const int32_t *level, const int32_t *order,
+                             const int32_t *nbr, const int32_t *own, int32_t *flag) {
+    for (int64_t e = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; e < E;
+         e += (int64_t)gridDim.x * blockDim.x) {
+        const int32_t lv_nb = level[order[nbr[e]]], lv_ow = level[order[own[e]]];
+        flag[e] = (fwd ? lv_ow - lv_nb : lv_nb - lv_ow) == 1 ? 1 : 0;
+    }
+}
+
+__global__ void k_pair_levels(int32_t L, const int32_t *level_ptr, const int32_t *off,
+                              const int32_t *near_rank, PairLevel *pl) {
+    for (int32_t k = blockIdx.x * blockDim.x + threadIdx.x; k <= L + 1;
+         k += gridDim.x * blockDim.x) {
+        const int32_t lo = level_ptr[min(k, L)];
+        const int32_t e = off[lo];
+        PairLevel x;
+        x.node_lo = lo;
+        x.near_lo = near_rank[e];
+        x.far_lo = e - near_rank[e];
+        x.pad = 0;
+        pl[k] = x;
+    }
+}
+
+__global__ void k_pair_records(int64_t E, int32_t L, bool fwd, int32_t ob, const int32_t *level,
+                               const int32_t *order, const int32_t *level_ptr, const int32_t *nbr,
+                               const int32_t *own, const int64_t *cost, const int32_t *nb_orig,
+                               const int32_t *near_rank, NearRec16 *nr, FarRec16 *fr,
+                               int32_t *ftie) {
+    const long long omax = (1ll << ob) - 1;
+    for (int64_t e = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; e < E;
+         e += (int64_t)gridDim.x * blockDim.x) {
+        const int32_t nb = nbr[e], ow = own[e];
+        const int32_t lv_nb = level[order[nb]], lv_ow = level[order[ow]];
+        const int32_t span = fwd ? lv_ow - lv_nb : lv_nb - lv_ow;
+        const int32_t nb_lo = level_ptr[lv_nb];
+        const uint32_t own_local = (uint32_t)(ow - level_ptr[lv_ow]) & 0xffffu;
+        const uint32_t nb_local = (uint32_t)(nb - nb_lo);
+        const int32_t tie = fwd ? 0 : (int32_t)(omax - nb_orig[e]);
+        if (span == 1) {
+            NearRec16 r;
+            r.ol = own_local | ((nb_local & 0xffffu) << 16);
+            r.tie = tie;
+            r.cost = cost[e];
+            nr[near_rank[e]] = r;
+        } else {
+            const int32_t w_nb = level_ptr[lv_nb + 1] - nb_lo;
+            const int32_t step_nb = fwd ? lv_nb : L - 1 - lv_nb;
+            const uint32_t rg = span > kD + 1 ? kNoRing
+                                : w_nb <= kPNodes ? (uint32_t)((step_nb % kRS) * kPNodes) + nb_local
+                                                  : kPreFolded;
+            FarRec16 r;
+            r.nb = nb;
+            r.ol = own_local | (rg << 16);
+            r.cost = cost[e];
+            const int64_t f = e - near_rank[e];
+            fr[f] = r;
+            if (!fwd) ftie[f] = tie;
+        }
+    }
+}
+
+// Edges a wide level folds early, in neighbour-grouped order (t: the CSR by
+// source, b: the CSC by destination): span 2 .. D + 1, neighbour's level wider
+// than the ring, owner's level narrow enough for the accumulators.
+__global__ void k_pre_flags(int64_t E, bool fwd, const int32_t *level, const int32_t *order,
+                            const int32_t *level_ptr, const int32_t *nbr, const int32_t *own,
+                            int32_t *flag) {
+    for (int64_t e = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; e < E;
+         e += (int64_t)gridDim.x * blockDim.x) {
+        const int32_t lv_nb = level[order[nbr[e]]], lv_ow = level[order[own[e]]];
+        const int32_t span = fwd ? lv_ow - lv_nb : lv_nb - lv_ow;
+        const int32_t w_nb = level_ptr[lv_nb + 1] - level_ptr[lv_nb];
+        const int32_t w_ow = level_ptr[lv_ow + 1] - level_ptr[lv_ow];
+        flag[e] = span >= 2 && span <= kD + 1 && w_nb > kPNodes && w_ow <= kPNodes ? 1 : 0;
+    }
+}
+
+__global__ void k_pre_off(int32_t L, const int32_t *level_ptr, const int32_t *off,
+                          const int32_t *rank, int32_t *preoff) {
+    for (int32_t k = blockIdx.x * blockDim.x + threadIdx.x; k <= L; k += gridDim.x * blockDim.x)
+        preoff[k] = rank[off[level_ptr[k]]];
+}
+
+__global__ void k_pre_records(int64_t E, bool fwd, int32_t ob, const int32_t *level,
+                              const int32_t *order, const int32_t *level_ptr, const int32_t *nbr,
+                              const int32_t *own, const int64_t *cost, const int32_t *rank,
+                              PreRec16 *pre, int32_t *pretie) {
+    const long long omax = (1ll << ob) - 1;
+    for (int64_t e = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; e < E;
+         e += (int64_t)gridDim.x * blockDim.x) {
+        if (rank[e + 1] == rank[e]) continue;   // not flagged (rank: exclusive scan)
+        const int32_t nb = nbr[e], ow = own[e];
+        const int32_t lv_nb = level[order[nb]], lv_ow = level[order[ow]];
+        const int32_t span = fwd ? lv_ow - lv_nb : lv_nb - lv_ow;
+        PreRec16 r;
+        r.nb = nb;
+        r.os = (uint32_t)(ow - level_ptr[lv_ow]) | ((uint32_t)span << 16);
+        r.cost = cost[e];
+        pre[rank[e]] = r;
+        if (!fwd) pretie[rank[e]] = (int32_t)(omax - order[nb]);
+    }
+}
+
+}  // namespace
+
+hipError_t launch_pre_flags(const Graph &g, bool fwd, int32_t *flag) {
+    if (g.E == 0) return hipSuccess;
+    const unsigned grid = (unsigned)std::min<int64_t>((g.E + 255) / 256, 65536);
+    k_pre_flags<<<grid, 256, 0, g.stream>>>(g.E, fwd, g.level, g.order, g.level_ptr,
+                                            fwd ? g.out_src : g.in_dst,
+                                            fwd ? g.out_dst : g.in_src, flag);
+    return hipGetLastError();
+}
+
+hipError_t launch_pre_split(const Graph &g, bool fwd, const int32_t *rank, int32_t *preoff,
+                            PreRec16 *pre, int32_t *pretie) {
+    k_pre_off<<<(unsigned)((g.L + 1 + 255) / 256), 256, 0, g.stream>>>(
+        g.L, g.level_ptr, fwd ? g.out_off : g.in_off, rank, preoff);
+    hipError_t e = hipGetLastError();
+    if (e != hipSuccess || g.E == 0) return e;
+    const unsigned grid = (unsigned)std::min<int64_t>((g.E + 255) / 256, 65536);
+    k_pre_records<<<grid, 256, 0, g.stream>>>(
+        g.E, fwd, succ_bits(g.V), g.level, g.order, g.level_ptr, fwd ? g.out_src : g.in_dst,
+        fwd ? g.out_dst : g.in_src, fwd ? g.out_cost : g.in_cost, rank, pre, pretie);
+    return hipGetLastError();
+}
+
+hipError_t launch_pair_flags(const Graph &g, bool fwd, int32_t *flag) {
+    if (g.E == 0) return hipSuccess;
+    const unsigned grid = (unsigned)std::min<int64_t>((g.E + 255) / 256, 65536);
+    k_pair_flags<<<grid, 256, 0, g.stream>>>(g.E, fwd, g.level, g.order,
+                                             fwd ? g.in_src : g.out_dst,
+                                             fwd ? g.in_dst : g.out_src, flag);
+    return hipGetLastError();
+}
+
+hipError_t launch_pair_split(const Graph &g, bool fwd, const int32_t *near_rank, PairLevel *pl,
+                             NearRec16 *nr, FarRec16 *fr, int32_t *ftie) {
+    k_pair_levels<<<(unsigned)((g.L + 2 + 255) / 256), 256, 0, g.stream>>>(
+        g.L, g.level_ptr, fwd ? g.in_off : g.out_off, near_rank, pl);
+    hipError_t e = hipGetLastError();
+    if (e != hipSuccess || g.E == 0) return e;
+    const unsigned grid = (unsigned)std::min<int64_t>((g.E + 255) / 256, 65536);
+    k_pair_records<<<grid, 256, 0, g.stream>>>(
+        g.E, g.L, fwd, succ_bits(g.V), g.level, g.order, g.level_ptr,
+        fwd ? g.in_src : g.out_dst, fwd ? g.in_dst : g.out_src, fwd ? g.in_cost : g.out_cost,
+        g.out_dst_orig, near_rank, nr, fr, ftie);
+    return hipGetLastError();
+}
+
+hipError_t launch_sweep_pair(const SweepArgs &a, hipStream_t s) {
+    constexpr int S = kBatchSlots;
+    const int32_t n_slices = (a.P + S - 1) / S;
+    if (n_slices == 0) return hipSuccess;
+    if (a.lb <= 0) return hipErrorInvalidValue;
+    const size_t bins = a.K > 0 && a.K * S <= kPBinsCap ? (size_t)a.K * S * 8 : 0;
+    const size_t lds = pair_lds_fixed<S>() + bins;
+    if (a.K <= 0)
+        k_sweep_pair<S, kBinsNone><<<2 * n_slices, 2 * kLanes, lds, s>>>(a);
+    else if (bins > 0)
+        k_sweep_pair<S, kBinsLds><<<2 * n_slices, 2 * kLanes, lds, s>>>(a);
+    else
+        k_sweep_pair<S, kBinsGlobal><<<2 * n_slices, 2 * kLanes, lds, s>>>(a);
+    return hipGetLastError();
+}
+
+}  // namespace pardnn
