@@ -263,6 +263,7 @@ SweepArgs sweep_args(const Graph *g) {
     a.out_rec = g->out_rec;
     a.node_rec = g->node_rec;
     a.order = g->order;
+    a.lab_stride = g->V;
     a.level = g->level;
     a.level_ptr = g->level_ptr;
     a.rank = g->rank;
@@ -309,10 +310,13 @@ int evaluate_impl(Graph *g, int32_t n_place, const int32_t *placements, const Mo
     const int32_t S = kBatchSlots;
     const int64_t n_slices = (n_place + S - 1) / S;
     // ftl, bll, nx_w: per slice (V + kSlicePad) x S elements (room for
-    // stores of idle lanes); lab_w: V x S per slice
-    const int64_t ws_stride = ((int64_t)g->V + kSlicePad) * S;
+    // stores of idle lanes); lab_w: V x S per slice. Both strides are rounded
+    // up to 256 bytes, so that every slice starts on a cache line and a run
+    // of nodes touches no more lines than its size needs.
+    const int64_t ws_stride = (((int64_t)g->V + kSlicePad) * S + 31) / 32 * 32;
+    const int64_t lab_stride = ((int64_t)g->V * S + 63) / 64 * 64;
     const size_t per = (size_t)n_slices * (size_t)ws_stride;
-    const size_t per_lab = (size_t)n_slices * (size_t)g->V * (size_t)S;
+    const size_t per_lab = (size_t)n_slices * (size_t)lab_stride;
     // ftl, bll: room for 16-byte pairs; lab_w, nx_w: int32; start: [P]
     const size_t need = per * (4 * sizeof(int64_t) + sizeof(int32_t)) +
                         per_lab * sizeof(int32_t) + (size_t)n_place * sizeof(int32_t) + 1024;
@@ -365,9 +369,10 @@ int evaluate_impl(Graph *g, int32_t n_place, const int32_t *placements, const Mo
         // the move marks live in the t workspace, which the sweep overwrites later
         HIP_TRY(launch_moves_to_slices(*g, mv->base, n_place, mv->step_ptr, ends[1], mv->node,
                                        mv->label, S, reinterpret_cast<int32_t *>(ftl), lab_w,
-                                       K, g->err));
+                                       lab_stride, K, g->err));
     } else {
-        HIP_TRY(launch_permute_labels_batch(*g, placements, n_place, S, lab_w, K, g->err));
+        HIP_TRY(launch_permute_labels_batch(*g, placements, n_place, S, lab_w, lab_stride, K,
+                                            g->err));
     }
     if (K > 0) {
         HIP_TRY(launch_fill_i64(label_mem, (int64_t)n_place * K, 0, g->stream));
@@ -376,6 +381,7 @@ int evaluate_impl(Graph *g, int32_t n_place, const int32_t *placements, const Mo
     a.P = n_place;
     a.K = K;
     a.lab_w = lab_w;
+    a.lab_stride = lab_stride;
     a.ftl = ftl;
     a.bll = bll;
     a.nx_w = path != nullptr ? nx_w : nullptr;
@@ -595,6 +601,7 @@ int pardnn_tb_levels(pardnn_graph *h, const int32_t *placement, int64_t *tl, int
     a.P = 1;
     a.K = 0;
     a.lab_w = g->lab_lm;
+    a.lab_stride = g->V;
     a.ftl = g->ft_lm;
     a.bll = g->bl_lm;
     a.ws_stride = g->V;

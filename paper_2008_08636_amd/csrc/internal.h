@@ -130,6 +130,7 @@ struct SweepArgs {
     const int32_t *level_ptr;  // first level-major node of each level
     const int32_t *rank;    // original id -> level-major
     const int32_t *lab_w;   // [slice][V][S] labels in level-major order
+    int64_t lab_stride;     // elements of lab_w per slice (>= V * S)
     int64_t *ftl, *bll;     // [slice][V][S] {value, label}: tl + comp, bl (packed or pairs)
     int32_t *nx_w;          // [slice][V][S] original id of the chosen successor (-1: none), or null
     int64_t ws_stride;      // elements of ftl / bll / nx_w per slice (>= V * S)
@@ -224,8 +225,8 @@ hipError_t launch_kahn(const Graph &g, int32_t *indeg_work, int32_t *sort_scratc
 hipError_t launch_permute_labels(const Graph &g, const int32_t *placement, int32_t *lab_lm);
 // K > 0: labels outside [0, K) set bit 0 of err.
 hipError_t launch_permute_labels_batch(const Graph &g, const int32_t *placements, int32_t P,
-                                       int32_t S, int32_t *lab_w, int32_t K = 0,
-                                       int32_t *err = nullptr);
+                                       int32_t S, int32_t *lab_w, int64_t lab_stride,
+                                       int32_t K = 0, int32_t *err = nullptr);
 hipError_t launch_sweep(const SweepArgs &a, int32_t S, hipStream_t s);
 hipError_t launch_finish(const SweepArgs &a, int32_t S, uint8_t *crit, int32_t *path,
                          int32_t stride, int32_t *path_len, hipStream_t s);
@@ -264,6 +265,6 @@ hipError_t launch_build_placements(const Graph &g, const int32_t *base, int32_t 
 hipError_t launch_moves_to_slices(const Graph &g, const int32_t *base, int32_t P,
                                   const int64_t *step_ptr, int64_t M, const int32_t *node,
                                   const int32_t *label, int32_t S, int32_t *mat, int32_t *lab_w,
-                                  int32_t K, int32_t *err);
+                                  int64_t lab_stride, int32_t K, int32_t *err);
 
 }  // namespace pardnn

@@ -172,7 +172,8 @@ __global__ __launch_bounds__(256) void k_moves_to_slices(int32_t V, int32_t P,
                                                          const int32_t *base,
                                                          const int32_t *label,
                                                          const int32_t *mat, int32_t *lab_w,
-                                                         int32_t K, int32_t *err) {
+                                                         int64_t lab_stride, int32_t K,
+                                                         int32_t *err) {
     constexpr int TV = 64, TP = 64;
     __shared__ int32_t tile[TV][TP + 1];
     __shared__ int32_t carry[TV];
@@ -229,7 +230,7 @@ __global__ __launch_bounds__(256) void k_moves_to_slices(int32_t V, int32_t P,
             const int32_t v = v0 + r;
             if (v < V) {
                 const int32_t x = tile[r][sl * S + s2];
-                lab_w[((int64_t)(sl0 + sl) * V + v) * S + s2] = x;
+                lab_w[(int64_t)(sl0 + sl) * lab_stride + (int64_t)v * S + s2] = x;
                 if (K > 0 && (x < 0 || x >= K) && c0 + sl * S + s2 < P) atomicOr(err, 1);
             }
         }
@@ -242,7 +243,7 @@ __global__ __launch_bounds__(256) void k_moves_to_slices(int32_t V, int32_t P,
 hipError_t launch_moves_to_slices(const Graph &g, const int32_t *base, int32_t P,
                                   const int64_t *step_ptr, int64_t M, const int32_t *node,
                                   const int32_t *label, int32_t S, int32_t *mat, int32_t *lab_w,
-                                  int32_t K, int32_t *err) {
+                                  int64_t lab_stride, int32_t K, int32_t *err) {
     if (g.V == 0 || P == 0) return hipSuccess;
     hipError_t e = launch_fill_i32(mat, (int64_t)g.V * P, -1, g.stream);
     if (e != hipSuccess) return e;
@@ -256,13 +257,13 @@ hipError_t launch_moves_to_slices(const Graph &g, const int32_t *base, int32_t P
     const int32_t *lab_src = M > 0 ? label : base;
     if (S == 1)
         k_moves_to_slices<1><<<grid, 256, 0, g.stream>>>(g.V, P, g.order, base, lab_src, mat,
-                                                         lab_w, K, err);
+                                                         lab_w, lab_stride, K, err);
     else if (S == 2)
         k_moves_to_slices<2><<<grid, 256, 0, g.stream>>>(g.V, P, g.order, base, lab_src, mat,
-                                                         lab_w, K, err);
+                                                         lab_w, lab_stride, K, err);
     else if (S == 4)
         k_moves_to_slices<4><<<grid, 256, 0, g.stream>>>(g.V, P, g.order, base, lab_src, mat,
-                                                         lab_w, K, err);
+                                                         lab_w, lab_stride, K, err);
     else
         return hipErrorInvalidValue;
     return hipGetLastError();

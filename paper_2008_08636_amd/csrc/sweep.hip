@@ -56,7 +56,8 @@ template <int S>
 __global__ __launch_bounds__(256) void k_permute_labels(int32_t V, int32_t P,
                                                         const int32_t *order,
                                                         const int32_t *placements,
-                                                        int32_t *lab_w, int32_t K, int32_t *err) {
+                                                        int32_t *lab_w, int64_t lab_stride,
+                                                        int32_t K, int32_t *err) {
     constexpr int TV = 64, TP = 64;  // tile: 64 nodes x 64 placements
     __shared__ int32_t tile[TV][TP + 1];
     const int32_t n_slices = (P + S - 1) / S;
@@ -81,7 +82,7 @@ __global__ __launch_bounds__(256) void k_permute_labels(int32_t V, int32_t P,
         const int rem = i % (TV * S);
         const int r = rem / S, s = rem % S;
         const int32_t v = v0 + r;
-        if (v < V) lab_w[((int64_t)(sl0 + sl) * V + v) * S + s] = tile[r][sl * S + s];
+        if (v < V) lab_w[(int64_t)(sl0 + sl) * lab_stride + (int64_t)v * S + s] = tile[r][sl * S + s];
     }
 }
 
@@ -143,7 +144,7 @@ __device__ void sweep_dir(const SweepArgs &a, int32_t slice, char *smem) {
     const long long omax = (1ll << ob) - 1;
     const int32_t V = a.V, L = a.L, P = a.P;
     const int64_t wbase = (int64_t)slice * a.ws_stride;
-    const int32_t *lab = a.lab_w + (int64_t)slice * V * S;
+    const int32_t *lab = a.lab_w + (int64_t)slice * a.lab_stride;
     ET *vals = reinterpret_cast<ET *>(FWD ? a.ftl : a.bll) + wbase;
     const EdgeRec16 *erec = FWD ? a.in_rec : a.out_rec;
     const int32_t *off = FWD ? a.in_off : a.out_off;
@@ -638,19 +639,20 @@ constexpr int kBatchAcc = 256;
 }  // namespace
 
 hipError_t launch_permute_labels(const Graph &g, const int32_t *placement, int32_t *lab_lm) {
-    return launch_permute_labels_batch(g, placement, 1, 1, lab_lm);
+    return launch_permute_labels_batch(g, placement, 1, 1, lab_lm, g.V);
 }
 
 hipError_t launch_permute_labels_batch(const Graph &g, const int32_t *placements, int32_t P,
-                                       int32_t S, int32_t *lab_w, int32_t K, int32_t *err) {
+                                       int32_t S, int32_t *lab_w, int64_t lab_stride, int32_t K,
+                                       int32_t *err) {
     if (g.V == 0 || P == 0) return hipSuccess;
     dim3 grid((g.V + 63) / 64, (P + 63) / 64);
     if (S == 1)
-        k_permute_labels<1><<<grid, 256, 0, g.stream>>>(g.V, P, g.order, placements, lab_w, K,
-                                                        err);
+        k_permute_labels<1><<<grid, 256, 0, g.stream>>>(g.V, P, g.order, placements, lab_w,
+                                                        lab_stride, K, err);
     else if (S == kBatchSlots)
         k_permute_labels<kBatchSlots><<<grid, 256, 0, g.stream>>>(g.V, P, g.order, placements,
-                                                                  lab_w, K, err);
+                                                                  lab_w, lab_stride, K, err);
     else
         return hipErrorInvalidValue;
     return hipGetLastError();

@@ -163,7 +163,7 @@ struct PairCtx {
         ob = FWD ? 0 : a->ob;
         omax = (1ll << ob) - 1;
         vals = reinterpret_cast<VS *>((FWD ? a->ftl : a->bll) + (int64_t)slice * a->ws_stride);
-        labs = reinterpret_cast<const LS *>(a->lab_w + (int64_t)slice * V * S);
+        labs = reinterpret_cast<const LS *>(a->lab_w + (int64_t)slice * a->lab_stride);
         want_nx = !FWD && a->nx_w != nullptr;
         nxs = reinterpret_cast<LS *>(a->nx_w + (want_nx ? (int64_t)slice * a->ws_stride : 0));
         pls = (ConstPairLevel)(FWD ? a->pl_t : a->pl_b);
