@@ -317,9 +317,31 @@ int evaluate_impl(Graph *g, int32_t n_place, const int32_t *placements, const Mo
     const int64_t lab_stride = ((int64_t)g->V * S + 63) / 64 * 64;
     const size_t per = (size_t)n_slices * (size_t)ws_stride;
     const size_t per_lab = (size_t)n_slices * (size_t)lab_stride;
-    // ftl, bll: room for 16-byte pairs; lab_w, nx_w: int32; start: [P]
+    // successive placements from moves: the number of moves sizes the scratch
+    // that groups them by node
+    int64_t n_moves = 0;
+    if (mv != nullptr) {
+        int64_t ends[2] = {0, 0};
+        HIP_TRY(hipMemcpyAsync(&ends[0], mv->step_ptr, sizeof(int64_t), hipMemcpyDeviceToHost,
+                               g->stream));
+        HIP_TRY(hipMemcpyAsync(&ends[1], mv->step_ptr + n_place, sizeof(int64_t),
+                               hipMemcpyDeviceToHost, g->stream));
+        HIP_TRY(hipStreamSynchronize(g->stream));
+        if (ends[0] != 0 || ends[1] < 0 || ends[1] >= (int64_t)INT32_MAX)
+            return fail(PARDNN_E_INVAL, "step_ptr must start at 0 and hold fewer than 2^31 moves");
+        if (ends[1] > 0 && (mv->node == nullptr || mv->label == nullptr))
+            return fail(PARDNN_E_INVAL, "node and label must be non-null");
+        if (g->V > 0 && mv->base == nullptr) return fail(PARDNN_E_INVAL, "base must be non-null");
+        n_moves = ends[1];
+    }
+    const size_t moves_bytes =
+        mv != nullptr ? (moves_scratch_elems(g->V, n_moves) * sizeof(int32_t) + 255) / 256 * 256
+                      : 0;
+    // ftl, bll: room for 16-byte pairs; lab_w, nx_w: int32; start: [P]; then
+    // the moves scratch
     const size_t need = per * (4 * sizeof(int64_t) + sizeof(int32_t)) +
-                        per_lab * sizeof(int32_t) + (size_t)n_place * sizeof(int32_t) + 1024;
+                        per_lab * sizeof(int32_t) + (size_t)n_place * sizeof(int32_t) + 1024 +
+                        moves_bytes;
     if (g->batch_ws_bytes < need) {
         if (g->batch_ws) {
             HIP_TRY(hipStreamSynchronize(g->stream));
@@ -351,25 +373,15 @@ int evaluate_impl(Graph *g, int32_t n_place, const int32_t *placements, const Mo
     int32_t *lab_w = (int32_t *)(bll + 2 * per);
     int32_t *nx_w = lab_w + per_lab;
     int32_t *start = nx_w + per;
+    int32_t *moves_scratch = reinterpret_cast<int32_t *>(
+        (char *)g->batch_ws + (need - moves_bytes) / 256 * 256);
 
     const int32_t K = label_mem != nullptr ? n_labels : 0;
     HIP_TRY(launch_fill_i32(g->err, 4, 0, g->stream));
     if (mv != nullptr) {
-        int64_t ends[2] = {0, 0};
-        HIP_TRY(hipMemcpyAsync(&ends[0], mv->step_ptr, sizeof(int64_t), hipMemcpyDeviceToHost,
-                               g->stream));
-        HIP_TRY(hipMemcpyAsync(&ends[1], mv->step_ptr + n_place, sizeof(int64_t),
-                               hipMemcpyDeviceToHost, g->stream));
-        HIP_TRY(hipStreamSynchronize(g->stream));
-        if (ends[0] != 0 || ends[1] < 0 || ends[1] >= (int64_t)INT32_MAX)
-            return fail(PARDNN_E_INVAL, "step_ptr must start at 0 and hold fewer than 2^31 moves");
-        if (ends[1] > 0 && (mv->node == nullptr || mv->label == nullptr))
-            return fail(PARDNN_E_INVAL, "node and label must be non-null");
-        if (g->V > 0 && mv->base == nullptr) return fail(PARDNN_E_INVAL, "base must be non-null");
-        // the move marks live in the t workspace, which the sweep overwrites later
-        HIP_TRY(launch_moves_to_slices(*g, mv->base, n_place, mv->step_ptr, ends[1], mv->node,
-                                       mv->label, S, reinterpret_cast<int32_t *>(ftl), lab_w,
-                                       lab_stride, K, g->err));
+        HIP_TRY(launch_moves_to_slices(*g, mv->base, n_place, mv->step_ptr, n_moves, mv->node,
+                                       mv->label, S, moves_scratch, lab_w, lab_stride, K,
+                                       g->err));
     } else {
         HIP_TRY(launch_permute_labels_batch(*g, placements, n_place, S, lab_w, lab_stride, K,
                                             g->err));

@@ -262,9 +262,11 @@ hipError_t launch_apply_moves(const Graph &g, int32_t *placement, int32_t n, con
 hipError_t launch_build_placements(const Graph &g, const int32_t *base, int32_t P,
                                    const int64_t *step_ptr, int64_t M, const int32_t *node,
                                    const int32_t *label, int32_t *placements, int32_t *err);
+// int32 elements of the scratch launch_moves_to_slices needs for M moves
+size_t moves_scratch_elems(int32_t V, int64_t M);
 hipError_t launch_moves_to_slices(const Graph &g, const int32_t *base, int32_t P,
                                   const int64_t *step_ptr, int64_t M, const int32_t *node,
-                                  const int32_t *label, int32_t S, int32_t *mat, int32_t *lab_w,
-                                  int64_t lab_stride, int32_t K, int32_t *err);
+                                  const int32_t *label, int32_t S, int32_t *scratch,
+                                  int32_t *lab_w, int64_t lab_stride, int32_t K, int32_t *err);
 
 }  // namespace pardnn

@@ -23,6 +23,12 @@ namespace {
 constexpr int kBlock = 256;
 constexpr int kLdsBins = 4096;
 
+// S labels of one node in a slice, stored with one access
+template <int S>
+struct alignas(4 * S) LabPack {
+    int32_t v[S];
+};
+
 inline unsigned grid_for(int64_t n, int block, int cap = 65536) {
     int64_t g = (n + block - 1) / block;
     if (g < 1) g = 1;
@@ -159,79 +165,131 @@ __global__ void k_bp_fill(int32_t V, int32_t P, const int32_t *base, const int32
     }
 }
 
+// Moves grouped by node (a counting sort): count per node, exclusive scan,
+// then scatter {step, move index, label} into the node's range. The order
+// inside a range is arbitrary; the consumer takes the latest move.
+__global__ void k_mv_count(int64_t M, const int32_t *node, int32_t V, int32_t *cnt,
+                           int32_t *err) {
+    for (int64_t m = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; m < M;
+         m += (int64_t)gridDim.x * blockDim.x) {
+        const int32_t v = node[m];
+        if (v < 0 || v >= V)
+            atomicOr(err, 1);
+        else
+            atomicAdd(&cnt[v], 1);
+    }
+}
+
+__global__ void k_mv_scatter(int64_t M, int32_t P, const int64_t *step_ptr, const int32_t *node,
+                             const int32_t *label, int32_t V, const int32_t *off, int32_t *cur,
+                             int4 *ent) {
+    for (int64_t m = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; m < M;
+         m += (int64_t)gridDim.x * blockDim.x) {
+        const int32_t v = node[m];
+        if (v < 0 || v >= V) continue;
+        // step of move m: largest p with step_ptr[p] <= m
+        int32_t lo = 0, hi = P;
+        while (hi - lo > 1) {
+            const int32_t mid = (lo + hi) >> 1;
+            if (step_ptr[mid] <= m)
+                lo = mid;
+            else
+                hi = mid;
+        }
+        ent[off[v] + atomicAdd(&cur[v], 1)] = make_int4(lo, (int32_t)m, label[m], 0);
+    }
+}
+
 // Labels of successive placements straight into the sweep's slice-major
 // workspace lab_w[slice][v][s] (v level-major, placement p = slice * S + s).
-// `mat` holds, per original node row, the index of the last move at each step
-// (k_bp_mark) or -1. A workgroup owns 64 consecutive level-major nodes and
-// walks the placements in chunks of 64: one wave scans one node row chunk
-// (coalesced), carrying the running label across chunks, into an LDS tile
-// that is then written out slice by slice as contiguous runs.
+// A workgroup owns 64 consecutive level-major nodes; each wave keeps the move
+// lists of its 16 node rows in registers (entry `lane` of a list of at most
+// 64 moves; longer lists are re-read per chunk). For a chunk of 64 placements
+// a row's value at lane p is the label of its latest move with a step in
+// [c0, c0 + p], else the row's label before the chunk: the moves that fall in
+// the chunk (a ballot, usually none or one) are broadcast one at a time. The
+// rows go through an LDS tile that is written out slice by slice as
+// contiguous runs.
 template <int S>
 __global__ __launch_bounds__(256) void k_moves_to_slices(int32_t V, int32_t P,
                                                          const int32_t *order,
                                                          const int32_t *base,
-                                                         const int32_t *label,
-                                                         const int32_t *mat, int32_t *lab_w,
+                                                         const int32_t *mv_off,
+                                                         const int4 *mv_ent, int32_t *lab_w,
                                                          int64_t lab_stride, int32_t K,
                                                          int32_t *err) {
-    constexpr int TV = 64, TP = 64;
+    constexpr int TV = 64, TP = 64, NW = 256 / kWave, RW = TV / NW;
     __shared__ int32_t tile[TV][TP + 1];
-    __shared__ int32_t carry[TV];
-    __shared__ int32_t rows[TV];
     const int lane = lane_id(), w = wave_id();
     const int32_t v0 = blockIdx.x * TV;
     const int32_t n_slices = (P + S - 1) / S;
-    for (int r = threadIdx.x; r < TV; r += 256) {
-        const int32_t v = v0 + r;
-        rows[r] = v < V ? order[v] : -1;
-        carry[r] = v < V ? base[order[v]] : 0;
+    int32_t lo[RW], cnt[RW], carry[RW];
+    int4 ent[RW];
+#pragma unroll
+    for (int j = 0; j < RW; j++) {
+        const int32_t v = v0 + w + j * NW;
+        const int32_t o = v < V ? order[v] : -1;
+        lo[j] = o >= 0 ? mv_off[o] : 0;
+        cnt[j] = o >= 0 ? mv_off[o + 1] - lo[j] : 0;
+        carry[j] = o >= 0 ? base[o] : 0;
     }
-    __syncthreads();
-    constexpr int RW = TV / (256 / kWave);  // node rows per wave
+#pragma unroll
+    for (int j = 0; j < RW; j++)
+        ent[j] = lane < cnt[j] ? mv_ent[lo[j] + lane] : make_int4(-1, -1, 0, 0);
+    // fold move x (uniform) into lane's value if it applies at lane's placement
+    auto apply = [&](int32_t c0, int32_t st, int32_t m, int32_t lab, int32_t &best,
+                     int32_t &val) {
+        if (st - c0 <= lane && m > best) {
+            best = m;
+            val = lab;
+        }
+    };
     for (int32_t c0 = 0; c0 < n_slices * S; c0 += TP) {
-        // all of this wave's row chunks in flight at once, then scan each
-        const int32_t p = c0 + lane;
-        int32_t m[RW];
 #pragma unroll
         for (int j = 0; j < RW; j++) {
-            const int32_t o = rows[w + j * (256 / kWave)];
-            m[j] = mat[(int64_t)(o >= 0 ? o : 0) * P + min(p, P - 1)];
-            if (o < 0 || p >= P) m[j] = -1;
-        }
-        int32_t mm[RW], last[RW];
-#pragma unroll
-        for (int j = 0; j < RW; j++) {
-            int32_t l = m[j] >= 0 ? lane : -1;
-#pragma unroll
-            for (int off = 1; off < kWave; off <<= 1) {
-                int32_t y = __shfl_up(l, off, kWave);
-                if (lane >= off) l = max(l, y);
+            int32_t val = carry[j], best = -1;
+            if (cnt[j] <= kWave) {
+                unsigned long long mask = __ballot(ent[j].x >= c0 && ent[j].x < c0 + TP);
+                while (mask) {
+                    const int e = __builtin_ctzll(mask);
+                    mask &= mask - 1;
+                    apply(c0, __builtin_amdgcn_readlane(ent[j].x, e),
+                          __builtin_amdgcn_readlane(ent[j].y, e),
+                          __builtin_amdgcn_readlane(ent[j].z, e), best, val);
+                }
+            } else {
+                for (int32_t g = 0; g < cnt[j]; g += kWave) {
+                    const int4 x = g + lane < cnt[j] ? mv_ent[lo[j] + g + lane]
+                                                     : make_int4(-1, -1, 0, 0);
+                    unsigned long long mask = __ballot(x.x >= c0 && x.x < c0 + TP);
+                    while (mask) {
+                        const int e = __builtin_ctzll(mask);
+                        mask &= mask - 1;
+                        apply(c0, __builtin_amdgcn_readlane(x.x, e),
+                              __builtin_amdgcn_readlane(x.y, e),
+                              __builtin_amdgcn_readlane(x.z, e), best, val);
+                    }
+                }
             }
-            last[j] = l;
-            mm[j] = __shfl(m[j], l < 0 ? 0 : l, kWave);
-        }
-        int32_t lv[RW];
-#pragma unroll
-        for (int j = 0; j < RW; j++) lv[j] = label[last[j] >= 0 ? mm[j] : 0];
-#pragma unroll
-        for (int j = 0; j < RW; j++) {
-            const int r = w + j * (256 / kWave);
-            const int32_t val = last[j] >= 0 ? lv[j] : carry[r];
-            tile[r][lane] = val;
-            const int32_t tail = __shfl(val, kWave - 1, kWave);
-            if (lane == 0) carry[r] = tail;
+            tile[w + j * NW][lane] = val;
+            carry[j] = __builtin_amdgcn_readlane(val, kWave - 1);
         }
         __syncthreads();
         const int32_t sl0 = c0 / S;
         const int n_sl = min(TP / S, n_slices - sl0);
-        for (int i = threadIdx.x; i < n_sl * TV * S; i += 256) {
-            const int sl = i / (TV * S), j = i % (TV * S);
-            const int r = j / S, s2 = j % S;
+        for (int i = threadIdx.x; i < n_sl * TV; i += 256) {
+            const int sl = i / TV, r = i % TV;
             const int32_t v = v0 + r;
             if (v < V) {
-                const int32_t x = tile[r][sl * S + s2];
-                lab_w[(int64_t)(sl0 + sl) * lab_stride + (int64_t)v * S + s2] = x;
-                if (K > 0 && (x < 0 || x >= K) && c0 + sl * S + s2 < P) atomicOr(err, 1);
+                LabPack<S> x;
+#pragma unroll
+                for (int s2 = 0; s2 < S; s2++) {
+                    x.v[s2] = tile[r][sl * S + s2];
+                    if (K > 0 && (x.v[s2] < 0 || x.v[s2] >= K) && c0 + sl * S + s2 < P)
+                        atomicOr(err, 1);
+                }
+                *reinterpret_cast<LabPack<S> *>(lab_w + (int64_t)(sl0 + sl) * lab_stride +
+                                                (int64_t)v * S) = x;
             }
         }
         __syncthreads();
@@ -240,30 +298,44 @@ __global__ __launch_bounds__(256) void k_moves_to_slices(int32_t V, int32_t P,
 
 }  // namespace
 
+size_t moves_scratch_elems(int32_t V, int64_t M) {
+    // cnt [V + 1], off [V + 1], scan workspace, then 16-byte aligned int4 entries
+    const size_t head = 2 * ((size_t)V + 1) + scan_workspace_elems(V);
+    return (head + 3) / 4 * 4 + 4 * (size_t)M;
+}
+
 hipError_t launch_moves_to_slices(const Graph &g, const int32_t *base, int32_t P,
                                   const int64_t *step_ptr, int64_t M, const int32_t *node,
-                                  const int32_t *label, int32_t S, int32_t *mat, int32_t *lab_w,
-                                  int64_t lab_stride, int32_t K, int32_t *err) {
+                                  const int32_t *label, int32_t S, int32_t *scratch,
+                                  int32_t *lab_w, int64_t lab_stride, int32_t K, int32_t *err) {
     if (g.V == 0 || P == 0) return hipSuccess;
-    hipError_t e = launch_fill_i32(mat, (int64_t)g.V * P, -1, g.stream);
-    if (e != hipSuccess) return e;
-    if (M > 0) {
-        k_bp_mark<<<grid_for(M, kBlock), kBlock, 0, g.stream>>>(M, P, step_ptr, node, g.V, mat,
-                                                                 err);
-        if ((e = hipGetLastError()) != hipSuccess) return e;
+    const int32_t V = g.V;
+    int32_t *cnt = scratch, *off = scratch + (V + 1), *ws = off + (V + 1);
+    const size_t head = 2 * ((size_t)V + 1) + scan_workspace_elems(V);
+    int4 *ent = reinterpret_cast<int4 *>(scratch + (head + 3) / 4 * 4);
+    hipError_t e = launch_fill_i32(cnt, (int64_t)V + 1, 0, g.stream);
+    if (e == hipSuccess && M > 0) {
+        k_mv_count<<<grid_for(M, kBlock), kBlock, 0, g.stream>>>(M, node, V, cnt, err);
+        e = hipGetLastError();
     }
-    const unsigned grid = (unsigned)((g.V + 63) / 64);
-    // the label gather is unconditional; without moves it reads a valid dummy
-    const int32_t *lab_src = M > 0 ? label : base;
+    if (e == hipSuccess) e = launch_exclusive_scan(cnt, off, V, ws, g.stream);
+    if (e == hipSuccess && M > 0) e = launch_fill_i32(cnt, (int64_t)V + 1, 0, g.stream);
+    if (e == hipSuccess && M > 0) {
+        k_mv_scatter<<<grid_for(M, kBlock), kBlock, 0, g.stream>>>(M, P, step_ptr, node, label,
+                                                                    V, off, cnt, ent);
+        e = hipGetLastError();
+    }
+    if (e != hipSuccess) return e;
+    const unsigned grid = (unsigned)((V + 63) / 64);
     if (S == 1)
-        k_moves_to_slices<1><<<grid, 256, 0, g.stream>>>(g.V, P, g.order, base, lab_src, mat,
-                                                         lab_w, lab_stride, K, err);
+        k_moves_to_slices<1><<<grid, 256, 0, g.stream>>>(V, P, g.order, base, off, ent, lab_w,
+                                                         lab_stride, K, err);
     else if (S == 2)
-        k_moves_to_slices<2><<<grid, 256, 0, g.stream>>>(g.V, P, g.order, base, lab_src, mat,
-                                                         lab_w, lab_stride, K, err);
+        k_moves_to_slices<2><<<grid, 256, 0, g.stream>>>(V, P, g.order, base, off, ent, lab_w,
+                                                         lab_stride, K, err);
     else if (S == 4)
-        k_moves_to_slices<4><<<grid, 256, 0, g.stream>>>(g.V, P, g.order, base, lab_src, mat,
-                                                         lab_w, lab_stride, K, err);
+        k_moves_to_slices<4><<<grid, 256, 0, g.stream>>>(V, P, g.order, base, off, ent, lab_w,
+                                                         lab_stride, K, err);
     else
         return hipErrorInvalidValue;
     return hipGetLastError();

@@ -37,6 +37,8 @@
 #include "internal.h"
 #include "sweep_common.h"
 
+#include <utility>
+
 namespace pardnn {
 
 namespace {
@@ -73,6 +75,13 @@ template <int I>
 struct IC {
     static constexpr int value = I;
 };
+
+// f(IC<0>), ..., f(IC<kNS - 1>): one group of levels, each with its register
+// sets named at compile time
+template <class F, int... I>
+__device__ __forceinline__ void unroll_seq(F &f, std::integer_sequence<int, I...>) {
+    (f(IC<I>{}), ...);
+}
 
 // S values / labels of one node (its S placements), adjacent in memory.
 template <int S>
@@ -408,16 +417,7 @@ __device__ __forceinline__ void pair_chain(const SweepArgs &a, int32_t slice, ch
         };
         // whole groups of kNS levels only: an exit inside the unrolled group
         // would merge every body's loads in flight into the loop header
-        while (step + kNS <= L) {
-            one(IC<0>{});
-            one(IC<1>{});
-            one(IC<2>{});
-            one(IC<3>{});
-            one(IC<4>{});
-            one(IC<5>{});
-            one(IC<6>{});
-            one(IC<7>{});
-        }
+        while (step + kNS <= L) unroll_seq(one, std::make_integer_sequence<int, kNS>{});
         // the last levels (fewer than kNS) on the general path; folding an
         // edge a second time into a maximum changes nothing
         for (; step < L; step++) {
@@ -498,16 +498,7 @@ __device__ __forceinline__ void pair_chain(const SweepArgs &a, int32_t slice, ch
                 step++;
             }
         };
-        while (step + kNS <= L) {
-            one(IC<0>{});
-            one(IC<1>{});
-            one(IC<2>{});
-            one(IC<3>{});
-            one(IC<4>{});
-            one(IC<5>{});
-            one(IC<6>{});
-            one(IC<7>{});
-        }
+        while (step + kNS <= L) unroll_seq(one, std::make_integer_sequence<int, kNS>{});
         for (; step < L; step++) {
             pair_slow<S, FWD, false, BM>(c.p0 / S, step, reinterpret_cast<char *>(c.win));
             __syncthreads();
