@@ -213,7 +213,9 @@ int pardnn_build_placements(pardnn_graph *g, const int32_t *base,
  *   makespan       int64[n_place] output.
  *   is_critical    uint8[n_nodes][n_place] output or NULL.
  *   path           int32[n_place][path_stride] output or NULL: row p holds
- *                  placement p's canonical critical path.
+ *                  placement p's canonical critical path in its first
+ *                  path_len[p] entries; the rest of the row is scratch
+ *                  (unspecified on return).
  *   path_stride    >= number of levels when path != NULL.
  *   path_len       int32[n_place] output (NULL iff path is NULL).
  *   label_mem      int64[n_place][n_labels] output or NULL.

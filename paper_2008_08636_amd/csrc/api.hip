@@ -94,7 +94,7 @@ int ensure_levelized(Graph *g) {
     if (!g->level) {
         HIP_TRY(dalloc(*g, &g->level, V));
         HIP_TRY(dalloc(*g, &g->order, V));
-        HIP_TRY(dalloc(*g, &g->rank, V));
+        HIP_TRY(dalloc(*g, &g->rank, (size_t)V + 1));   // rank[V] = -1: "no node"
         HIP_TRY(dalloc(*g, &g->level_ptr, (size_t)V + 2));
     }
     int32_t *indeg_work = nullptr, *sort_scratch = nullptr, *result = nullptr;
@@ -337,11 +337,14 @@ int evaluate_impl(Graph *g, int32_t n_place, const int32_t *placements, const Mo
     const size_t moves_bytes =
         mv != nullptr ? (moves_scratch_elems(g->V, n_moves) * sizeof(int32_t) + 255) / 256 * 256
                       : 0;
+    // critical bit words for the path walk: [P][ceil(V / 32)]
+    const size_t cbits_bytes =
+        path != nullptr ? (((size_t)g->V + 31) / 32 * (size_t)n_place * 4 + 255) / 256 * 256 : 0;
     // ftl, bll: room for 16-byte pairs; lab_w, nx_w: int32; start: [P]; then
-    // the moves scratch
+    // the critical bit words and the moves scratch
     const size_t need = per * (4 * sizeof(int64_t) + sizeof(int32_t)) +
                         per_lab * sizeof(int32_t) + (size_t)n_place * sizeof(int32_t) + 1024 +
-                        moves_bytes;
+                        cbits_bytes + moves_bytes;
     if (g->batch_ws_bytes < need) {
         if (g->batch_ws) {
             HIP_TRY(hipStreamSynchronize(g->stream));
@@ -373,6 +376,8 @@ int evaluate_impl(Graph *g, int32_t n_place, const int32_t *placements, const Mo
     int32_t *lab_w = (int32_t *)(bll + 2 * per);
     int32_t *nx_w = lab_w + per_lab;
     int32_t *start = nx_w + per;
+    uint32_t *cbits = reinterpret_cast<uint32_t *>(
+        (char *)g->batch_ws + (need - moves_bytes - cbits_bytes) / 256 * 256);
     int32_t *moves_scratch = reinterpret_cast<int32_t *>(
         (char *)g->batch_ws + (need - moves_bytes) / 256 * 256);
 
@@ -426,7 +431,7 @@ int evaluate_impl(Graph *g, int32_t n_place, const int32_t *placements, const Mo
         TimedLaunch t(g, "k_sweep<2>");
         HIP_TRY(launch_sweep(a, S, g->stream));
     }
-    HIP_TRY(launch_finish(a, S, is_critical, path, path_stride, path_len, g->stream));
+    HIP_TRY(launch_finish(a, S, is_critical, cbits, path, path_stride, path_len, g->stream));
     if (K > 0) {
         if (overflow != nullptr || capacity != nullptr)
             HIP_TRY(launch_overflow((int64_t)n_place * K, K, capacity, label_mem, overflow, g->err,

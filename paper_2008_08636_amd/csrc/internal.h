@@ -6,7 +6,7 @@
 //     comp, mem int64[V], indeg, outdeg int32[V]
 //     o_off int32[V+1], o_nbr int32[E]              out-adjacency (Kahn)
 //   level-major numbering ("lm": nodes sorted by (level, id)):
-//     order int32[V] lm -> original id, rank int32[V] original -> lm
+//     order int32[V] lm -> original id, rank int32[V + 1] original -> lm (rank[V] = -1)
 //     level int32[V] (original ids), level_ptr int32[L+1]
 //     linfo LevelInfo[L+1]: first node, first in-edge, first out-edge of
 //       each level (entry L holds the totals)
@@ -128,7 +128,7 @@ struct SweepArgs {
     const int32_t *order;   // level-major -> original id
     const int32_t *level;   // original id -> level
     const int32_t *level_ptr;  // first level-major node of each level
-    const int32_t *rank;    // original id -> level-major
+    const int32_t *rank;    // original id -> level-major, [V + 1] with rank[V] = -1
     const int32_t *lab_w;   // [slice][V][S] labels in level-major order
     int64_t lab_stride;     // elements of lab_w per slice (>= V * S)
     int64_t *ftl, *bll;     // [slice][V][S] {value, label}: tl + comp, bl (packed or pairs)
@@ -228,8 +228,10 @@ hipError_t launch_permute_labels_batch(const Graph &g, const int32_t *placements
                                        int32_t S, int32_t *lab_w, int64_t lab_stride,
                                        int32_t K = 0, int32_t *err = nullptr);
 hipError_t launch_sweep(const SweepArgs &a, int32_t S, hipStream_t s);
-hipError_t launch_finish(const SweepArgs &a, int32_t S, uint8_t *crit, int32_t *path,
-                         int32_t stride, int32_t *path_len, hipStream_t s);
+// cbits: [P][ceil(V / 32)] bit words of the critical flags, scratch for the
+// path walk (needed when path is given)
+hipError_t launch_finish(const SweepArgs &a, int32_t S, uint8_t *crit, uint32_t *cbits,
+                         int32_t *path, int32_t stride, int32_t *path_len, hipStream_t s);
 
 // ---- sweep_pair.hip ----
 // flag[e] = 1 for the span-1 edges of the direction's level-major edge order

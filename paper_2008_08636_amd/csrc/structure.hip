@@ -286,6 +286,7 @@ hipError_t launch_build_lm(Graph &g, int32_t *deg_ws, int32_t *cursor_in, int32_
         g.mem_lm);
     hipError_t err = hipGetLastError();
     if (err != hipSuccess) return err;
+    if ((err = launch_fill_i32(g.rank + V, 1, -1, g.stream)) != hipSuccess) return err;
     if ((err = launch_exclusive_scan(indeg_lm, g.in_off, V, scan_ws, g.stream)) != hipSuccess)
         return err;
     if ((err = launch_exclusive_scan(outdeg_lm, g.out_off, V, scan_ws, g.stream)) != hipSuccess)

@@ -38,9 +38,8 @@ namespace pardnn {
 namespace {
 
 constexpr int kBlock = 256;
-constexpr int kChaseWindow = 1024;  // links staged per wave
-constexpr int kEmitLds = 2 * 32 * 65 * 8 + 32 * 4 + 64 * 8;
-constexpr int kFinishLds = 4 * kChaseWindow * 4 > kEmitLds ? 4 * kChaseWindow * 4 : kEmitLds;
+constexpr int kChaseRegs = 16;      // registers per lane of a path-walk window
+constexpr int kEmitLds = 2 * 32 * 65 * 8 + 32 * 4 + 32 * 8 + 64 * 4;
 
 inline unsigned grid_for(int64_t n, int block, int cap = 65536) {
     int64_t g = (n + block - 1) / block;
@@ -504,131 +503,280 @@ __global__ __launch_bounds__(T) void k_sweep(SweepArgs a) {
 }
 
 // Outputs in the caller's layout: tl, bl [V][P] in original ids and the
-// critical flags crit = (tl + bl == M_p). A 32-node x 64-placement tile goes
-// through LDS so that the slice-major workspace is read contiguously and each
-// output row order[v] is written as one contiguous 512-byte run. Every load of
-// a phase is issued before the first is consumed (unrolled, clamped
-// addresses), and the tile's node ids, costs and makespans are staged once.
+// critical flags crit = (tl + bl == M_p). A workgroup owns TV = 32 level-major
+// nodes and walks the placements in chunks of TP = 64: a chunk goes through an
+// LDS tile so that the slice-major workspace is read contiguously and each
+// output row order[v] is written as one contiguous run. All of a row is
+// written by one workgroup, in order, so the partial lines of neighbouring
+// chunks (the byte-wide flags) meet in the same L2. The loads of the next
+// chunk are in flight while the current one is stored. When `cbits` is given,
+// the flags of the workgroup's 32 nodes also go out as one bit word per
+// placement, cbits[p][bx] (bit r: level-major node 32 bx + r), for the path
+// walk; node groups are assigned so that the workgroups of one XCD (every
+// 8th workgroup) take consecutive groups, so that the words of one placement
+// row meet in that XCD's L2.
 template <int S, bool PACKED>
-__device__ void emit_tile(const SweepArgs &a, uint8_t *crit, int32_t bx, int32_t by,
+__device__ void emit_rows(const SweepArgs &a, uint8_t *crit, uint32_t *cbits, int32_t bx,
                           char *smem) {
     using EL = Elem<PACKED>;
     using ET = typename EL::T;
     constexpr int TV = 32, TP = 64, NT = 256;
-    constexpr int PER = TV * TP / NT;  // elements per thread
+    constexpr int PER = TV * TP / NT;  // elements per thread and chunk
+    static_assert(NT % TP == 0, "a thread keeps one placement column");
+    static_assert(TV == 32, "one bit word per placement");
     long long(*t_tl)[TP + 1] = reinterpret_cast<long long(*)[TP + 1]>(smem);
     long long(*t_bl)[TP + 1] = reinterpret_cast<long long(*)[TP + 1]>(smem + TV * (TP + 1) * 8);
     int32_t *s_ord = reinterpret_cast<int32_t *>(smem + 2 * TV * (TP + 1) * 8);
-    long long *s_m = reinterpret_cast<long long *>(s_ord + TV);
-    const int tid = threadIdx.x;
+    long long *s_comp = reinterpret_cast<long long *>(s_ord + TV);
+    uint32_t *s_bits = reinterpret_cast<uint32_t *>(s_comp + TV);   // [TP]
+    const int tid = threadIdx.x, lane = lane_id();
     const int32_t V = a.V, P = a.P;
-    const int32_t v0 = bx * TV, q0 = by * TP;
-    const int32_t sl0 = q0 / S;
+    const int32_t v0 = bx * TV;
     const int32_t n_slices = (P + S - 1) / S;
+    const int32_t n_chunks = (P + TP - 1) / TP;
     const ET *ft = reinterpret_cast<const ET *>(a.ftl);
     const ET *bl = reinterpret_cast<const ET *>(a.bll);
-    if (tid < TV) s_ord[tid] = a.order[min(v0 + tid, V - 1)];
-    if (tid < TP) s_m[tid] = a.makespan[min(q0 + tid, P - 1)];
-    // element i of the tile read: slice-local run of TV*S values per slice
+    if (tid < TV) {
+        const int32_t v = min(v0 + tid, V - 1);
+        s_ord[tid] = a.order[v];
+        s_comp[tid] = a.comp_lm[v];
+    }
+    if (tid < TP) s_bits[tid] = 0;
+    // element i of a chunk read: slice i / (TV S), node (i % (TV S)) / S, slot i % S
     ET fv[PER], bv[PER];
-    int64_t cv[PER];
+    auto load = [&](int32_t ch) {
+        const int32_t sl0 = ch * (TP / S);
 #pragma unroll
-    for (int j = 0; j < PER; j++) {
-        const int i = tid + j * NT;
-        const int sl = i / (TV * S), r = (i % (TV * S)) / S, s2 = i % S;
-        const int32_t v = min(v0 + r, V - 1);
-        const int64_t idx = (int64_t)min(sl0 + sl, n_slices - 1) * a.ws_stride + (int64_t)v * S + s2;
-        fv[j] = ft[idx];
-        bv[j] = bl[idx];
-        cv[j] = a.comp_lm[v];
-    }
+        for (int j = 0; j < PER; j++) {
+            const int i = tid + j * NT;
+            const int sl = i / (TV * S), r = (i % (TV * S)) / S, s2 = i % S;
+            const int64_t idx = (int64_t)min(sl0 + sl, n_slices - 1) * a.ws_stride +
+                                (int64_t)min(v0 + r, V - 1) * S + s2;
+            fv[j] = ft[idx];
+            bv[j] = bl[idx];
+        }
+    };
+    load(0);
+    for (int32_t ch = 0; ch < n_chunks; ch++) {
+        __syncthreads();   // the tiles are free (and s_ord, s_comp, s_bits are set)
 #pragma unroll
-    for (int j = 0; j < PER; j++) {
-        const int i = tid + j * NT;
-        const int sl = i / (TV * S), r = (i % (TV * S)) / S, s2 = i % S;
-        t_tl[r][sl * S + s2] = EL::val(fv[j], a.lb) - cv[j];
-        t_bl[r][sl * S + s2] = EL::val(bv[j], a.lb);
-    }
-    __syncthreads();
+        for (int j = 0; j < PER; j++) {
+            const int i = tid + j * NT;
+            const int sl = i / (TV * S), r = (i % (TV * S)) / S, s2 = i % S;
+            t_tl[r][sl * S + s2] = EL::val(fv[j], a.lb) - s_comp[r];
+            t_bl[r][sl * S + s2] = EL::val(bv[j], a.lb);
+        }
+        if (ch + 1 < n_chunks) load(ch + 1);
+        const int32_t p = ch * TP + lane;   // this thread's placement column
+        const int64_t m = a.makespan[min(p, P - 1)];
+        __syncthreads();
+        uint32_t bits = 0;
+        if (p < P) {
 #pragma unroll
-    for (int j = 0; j < PER; j++) {
-        const int i = tid + j * NT;
-        const int r = i / TP, q = i % TP;
-        const int32_t v = v0 + r, p = q0 + q;
-        if (v < V && p < P) {
-            const int64_t o = (int64_t)s_ord[r] * P + p;
-            const int64_t t = t_tl[r][q], b = t_bl[r][q];
-            a.tl_out[o] = t;
-            a.bl_out[o] = b;
-            if (crit) crit[o] = (uint8_t)(t + b == s_m[q]);
+            for (int j = 0; j < PER; j++) {
+                const int r = (tid + j * NT) / TP;
+                if (v0 + r < V) {
+                    const int64_t o = (int64_t)s_ord[r] * P + p;
+                    const int64_t t = t_tl[r][lane], b = t_bl[r][lane];
+                    a.tl_out[o] = t;
+                    a.bl_out[o] = b;
+                    const bool c = t + b == m;
+                    if (crit) crit[o] = (uint8_t)c;
+                    bits |= (uint32_t)c << r;
+                }
+            }
+        }
+        if (cbits != nullptr) {
+            __hip_atomic_fetch_or(&s_bits[lane], bits, __ATOMIC_RELAXED,
+                                  __HIP_MEMORY_SCOPE_WORKGROUP);
+            __syncthreads();
+            if (tid < TP) {
+                if (p < P) cbits[(int64_t)p * ((V + TV - 1) / TV) + bx] = s_bits[tid];
+                s_bits[tid] = 0;
+            }
         }
     }
 }
 
-// One wave per placement walks the chosen-successor links from the path
-// start. Links point to strictly later levels (larger level-major ids), so the
-// wave stages a window of its links in LDS (all loads in flight at once) and
-// walks inside the window (uniformly across the wave); the window moves
-// forward when the walk leaves it. Lane i keeps the (i mod 64)-th path node
-// and the wave writes 64 original ids at a time.
+// One wave per placement extracts its canonical critical path. Every path
+// node is critical, so the wave (1) lists the placement's critical nodes in
+// level-major order from the bit words the emit pass wrote, and (2) maps the
+// successor link (an original id) of each listed node to a level-major id.
+// When each listed node links to the next one and the last has no successor
+// -- no other critical path crosses this one, the usual case -- the list is
+// the path, and (2) has already written it out. Otherwise (3) a walk from the
+// start follows the links, stepping forward through the sorted list; nodes
+// skipped on the way lie on other critical paths. Steps (1) and (2) have no
+// dependence between iterations, so many loads are in flight at once; the
+// walk reads the lists through registers, 64 x kChaseRegs entries at a time.
+// The list lives in the placement's half of its slice of the t workspace,
+// which holds nothing needed once the outputs have been emitted; the path is
+// written in original ids.
 template <int S>
-__device__ void chase_wave(const SweepArgs &a, int32_t p, int32_t *path, int32_t stride,
-                           int32_t *path_len, int32_t *win) {
-    constexpr int kWin = kChaseWindow;
-    constexpr int PER = kWin / kWave;
+__device__ void chase_wave(const SweepArgs &a, const uint32_t *cbits, int32_t p, int32_t *path,
+                           int32_t stride, int32_t *path_len) {
+    constexpr int RW = kChaseRegs;
+    constexpr int WIN = RW * kWave;
+    constexpr int U = 8;   // independent iterations in flight
     const int lane = lane_id();
     const int32_t V = a.V;
     const int32_t slice = p / S, s = p % S;
+    const int32_t n_words = (V + 31) / 32;
     const int32_t *nx = a.nx_w + (int64_t)slice * a.ws_stride;
+    const uint32_t *bits = cbits + (int64_t)p * n_words;
+    // scratch: pos[0, V) and link[V, 2V) in int32 units
+    int32_t *pos = reinterpret_cast<int32_t *>(a.ftl + (int64_t)slice * a.ws_stride) +
+                   (int64_t)s * a.ws_stride;
+    int32_t *link = pos + V;
     int32_t *out = path + (int64_t)p * stride;
-    int32_t cur = a.start[p], len = 0, mine = -1;
-    while (cur >= 0) {
-        const int32_t base = cur;
-        int32_t tmp[PER];
+    const int32_t start = __builtin_amdgcn_readfirstlane(a.start[p]);
+
+    // (1) critical nodes in level-major order
+    int32_t n = 0;
+    for (int32_t w0 = 0; w0 < n_words; w0 += U * kWave) {
+        uint32_t wd[U];
 #pragma unroll
-        for (int j = 0; j < PER; j++)
-            tmp[j] = nx[(int64_t)min(base + lane + j * kWave, V - 1) * S + s];
-        // links hold original ids: their level-major positions come from rank
-#pragma unroll
-        for (int j = 0; j < PER; j++) tmp[j] = a.rank[tmp[j] < 0 ? 0 : tmp[j]] | (tmp[j] >> 31);
-#pragma unroll
-        for (int j = 0; j < PER; j++)
-            win[lane + j * kWave] = base + lane + j * kWave < V ? tmp[j] : -1;
-        __builtin_amdgcn_wave_barrier();
-        int32_t c = base;
-        while (c >= base && c < base + kWin) {
-            if ((len & (kWave - 1)) == lane) mine = c;
-            len++;
-            if ((len & (kWave - 1)) == 0) out[len - kWave + lane] = a.order[mine];
-            const int32_t n = win[c - base];
-            c = n > c ? n : -1;  // links go to strictly later levels
+        for (int j = 0; j < U; j++) {
+            const int32_t w = w0 + j * kWave + lane;
+            wd[j] = w < n_words ? bits[w] : 0u;
         }
-        cur = c;
-        __builtin_amdgcn_wave_barrier();
+#pragma unroll
+        for (int j = 0; j < U; j++) {
+            const int32_t cnt = __popc(wd[j]);
+            const int32_t incl = wave_incl_scan_i32(cnt);
+            int32_t k = n + incl - cnt;
+            uint32_t x = wd[j];
+            while (x) {
+                const int b = __ffs(x) - 1;
+                x &= x - 1;
+                pos[k++] = 32 * (w0 + j * kWave + lane) + b;
+            }
+            n += __builtin_amdgcn_readlane(incl, kWave - 1);
+        }
+    }
+    __builtin_amdgcn_s_waitcnt(0);
+    // (2) links -> level-major ids (rank[V] = -1: none); the list as the path
+    bool chain = n > 0 && start >= 0;
+    for (int32_t i0 = 0; i0 < n; i0 += U * kWave) {
+        int32_t q[U], qn[U], l[U], o[U];
+#pragma unroll
+        for (int j = 0; j < U; j++) {
+            const int32_t i = min(i0 + j * kWave + lane, n - 1);
+            q[j] = pos[i];
+            qn[j] = i + 1 < n ? pos[i + 1] : -1;
+        }
+#pragma unroll
+        for (int j = 0; j < U; j++) l[j] = nx[(int64_t)q[j] * S + s];
+#pragma unroll
+        for (int j = 0; j < U; j++) {
+            l[j] = a.rank[l[j] < 0 ? V : l[j]];
+            o[j] = a.order[q[j]];
+        }
+#pragma unroll
+        for (int j = 0; j < U; j++) {
+            const int32_t i = i0 + j * kWave + lane;
+            if (i < n) {
+                link[i] = l[j];
+                // a chain is at most L <= stride long; a longer list is no chain
+                if (i < stride) out[i] = o[j];
+                chain = chain && l[j] == qn[j] && (i > 0 || q[j] == start);
+            }
+        }
+    }
+    chain = __ballot(!chain) == 0ull;
+    if (chain || n == 0 || start < 0) {
+        if (lane == 0) path_len[p] = start < 0 ? 0 : n;
+        return;
+    }
+    __builtin_amdgcn_s_waitcnt(0);
+    // (3) the walk, through register windows of the two lists
+    int32_t pa[RW], la[RW], pb[RW], lb[RW];
+    auto load = [&](int32_t base, int32_t(&pp)[RW], int32_t(&ll)[RW]) {
+#pragma unroll
+        for (int j = 0; j < RW; j++) {
+            const int32_t i = min(base + j * kWave + lane, n - 1);
+            pp[j] = pos[i];
+            ll[j] = link[i];
+        }
+    };
+    int32_t c = start;
+    int32_t len = 0, acc = -1, i = 0, wb = 0;
+    bool going = true;
+    load(0, pa, la);
+    load(WIN, pb, lb);
+    auto walk = [&](int32_t(&pp)[RW], int32_t(&ll)[RW]) {
+        if (!going) return;
+        // entries [wb, wb + WIN) are in pp / ll; the next window is in flight
+        while (i < wb + WIN && i < n) {
+            const int32_t x = i - wb;
+            const int32_t q = __builtin_amdgcn_readlane(pp[x / kWave], x & (kWave - 1));
+            i++;
+            if (q < c) continue;   // a critical node off this path
+            if (q != c) {          // cannot happen: every link names a listed node
+                going = false;
+                return;
+            }
+            acc = lane == (len & (kWave - 1)) ? c : acc;
+            len++;
+            if ((len & (kWave - 1)) == 0) out[len - kWave + lane] = acc;
+            c = __builtin_amdgcn_readlane(ll[x / kWave], x & (kWave - 1));
+            if (c < 0) {
+                going = false;
+                return;
+            }
+        }
+        if (i >= n) {
+            going = false;
+            return;
+        }
+        wb += WIN;
+        load(wb + WIN, pp, ll);   // the walked buffers take the window after next
+    };
+    while (going) {
+        walk(pa, la);
+        walk(pb, lb);
     }
     const int32_t r = len & (kWave - 1);
-    if (lane < r) out[len - r + lane] = a.order[mine];
+    if (lane < r) out[len - r + lane] = acc;
+    __builtin_amdgcn_s_waitcnt(0);
+    // level-major ids -> original ids, in place (each lane rewrites what it wrote)
+    for (int32_t i0 = 0; i0 < len; i0 += U * kWave) {
+        int32_t t[U];
+#pragma unroll
+        for (int j = 0; j < U; j++) t[j] = i0 + j * kWave + lane < len ? out[i0 + j * kWave + lane] : 0;
+#pragma unroll
+        for (int j = 0; j < U; j++) t[j] = a.order[t[j]];
+#pragma unroll
+        for (int j = 0; j < U; j++)
+            if (i0 + j * kWave + lane < len) out[i0 + j * kWave + lane] = t[j];
+    }
     if (lane == 0) path_len[p] = len;
 }
 
-// After the sweeps: workgroups [0, n_chase) walk critical paths (one wave per
-// placement, latency-bound), the rest emit output tiles (bandwidth-bound), so
-// the two overlap in one launch.
+// After the sweeps: the output rows and the critical bit words are emitted
+// (bandwidth-bound, many waves), then one wave per placement extracts its
+// critical path (latency-bound, few waves).
+template <int S>
+__global__ __launch_bounds__(256) void k_chase(SweepArgs a, const uint32_t *cbits, int32_t *path,
+                                               int32_t stride, int32_t *path_len) {
+    const int32_t p = __builtin_amdgcn_readfirstlane(blockIdx.x * (256 / kWave) + wave_id());
+    if (p < a.P) chase_wave<S>(a, cbits, p, path, stride, path_len);
+}
+
+// Workgroup b runs on XCD b % 8 (round-robin dispatch); give the workgroups of
+// one XCD consecutive node groups.
+__device__ __forceinline__ int32_t xcd_major(int32_t b, int32_t n) {
+    constexpr int kXcd = 8;
+    const int32_t x = b % kXcd;
+    int32_t start = 0;
+    for (int32_t y = 0; y < x; y++) start += (n - y + kXcd - 1) / kXcd;
+    return start + b / kXcd;
+}
+
 template <int S, bool PACKED>
-__global__ __launch_bounds__(256) void k_finish(SweepArgs a, uint8_t *crit, int32_t *path,
-                                                int32_t stride, int32_t *path_len,
-                                                int32_t n_chase, int32_t tiles_x) {
-    __shared__ __align__(16) char smem[kFinishLds];
-    if ((int32_t)blockIdx.x < n_chase) {
-        const int w = wave_id();
-        const int32_t p = blockIdx.x * (256 / kWave) + w;
-        if (p < a.P)
-            chase_wave<S>(a, p, path, stride, path_len,
-                          reinterpret_cast<int32_t *>(smem) + w * kChaseWindow);
-        return;
-    }
-    const int32_t t = blockIdx.x - n_chase;
-    emit_tile<S, PACKED>(a, crit, t % tiles_x, t / tiles_x, smem);
+__global__ __launch_bounds__(256) void k_emit(SweepArgs a, uint8_t *crit, uint32_t *cbits) {
+    __shared__ __align__(16) char smem[kEmitLds];
+    emit_rows<S, PACKED>(a, crit, cbits, xcd_major(blockIdx.x, gridDim.x), smem);
 }
 
 constexpr int kSingleThreads = 512;
@@ -679,22 +827,27 @@ hipError_t launch_sweep(const SweepArgs &a, int32_t S, hipStream_t s) {
     return hipGetLastError();
 }
 
-hipError_t launch_finish(const SweepArgs &a, int32_t S, uint8_t *crit, int32_t *path,
-                         int32_t stride, int32_t *path_len, hipStream_t s) {
+hipError_t launch_finish(const SweepArgs &a, int32_t S, uint8_t *crit, uint32_t *cbits,
+                         int32_t *path, int32_t stride, int32_t *path_len, hipStream_t s) {
     if (a.P == 0) return hipSuccess;
     if (S != kBatchSlots) return hipErrorInvalidValue;
-    const int32_t n_chase = path != nullptr ? (a.P + 3) / 4 : 0;
-    const int32_t tiles_x = (a.V + 31) / 32, tiles_y = (a.P + 63) / 64;
-    const int64_t blocks = n_chase + (int64_t)tiles_x * tiles_y;
-    if (blocks == 0) return hipSuccess;
-    if (blocks > INT32_MAX) return hipErrorInvalidValue;
-    if (a.lb > 0)
-        k_finish<kBatchSlots, true><<<(unsigned)blocks, 256, 0, s>>>(a, crit, path, stride,
-                                                                     path_len, n_chase, tiles_x);
-    else
-        k_finish<kBatchSlots, false><<<(unsigned)blocks, 256, 0, s>>>(a, crit, path, stride,
-                                                                      path_len, n_chase, tiles_x);
-    return hipGetLastError();
+    if (path != nullptr && cbits == nullptr) return hipErrorInvalidValue;
+    if (a.V > 0) {
+        const unsigned blocks = (unsigned)((a.V + 31) / 32);
+        uint32_t *bits = path != nullptr ? cbits : nullptr;
+        if (a.lb > 0)
+            k_emit<kBatchSlots, true><<<blocks, 256, 0, s>>>(a, crit, bits);
+        else
+            k_emit<kBatchSlots, false><<<blocks, 256, 0, s>>>(a, crit, bits);
+        const hipError_t e = hipGetLastError();
+        if (e != hipSuccess) return e;
+    }
+    if (path != nullptr) {
+        k_chase<kBatchSlots><<<(unsigned)((a.P + 3) / 4), 256, 0, s>>>(a, cbits, path, stride,
+                                                                      path_len);
+        return hipGetLastError();
+    }
+    return hipSuccess;
 }
 
 }  // namespace pardnn

@@ -346,6 +346,30 @@ def test_batch_level_shapes(P, seed):
     G.close()
 
 
+def test_batch_tie_rows_next_to_chains(P):
+    """Placements whose critical set is far larger than the number of levels
+    (zero node weights and one label: every node is critical) interleaved with
+    placements whose critical set is a single path. The path rows are exactly
+    as long as the number of levels, so a row that wrote past its end would
+    corrupt its neighbour's path."""
+    rng = np.random.default_rng(31)
+    base = W.layered_dag(rng, [1] + [24] * 20 + [1], [1] + [3] * 20 + [24], max_span=3,
+                         n_labels=4)
+    g = W.SynthGraph("ties", base.n_nodes, base.src, base.dst,
+                     np.zeros(base.n_nodes, np.int64), base.edge_cost + 1, base.mem,
+                     base.placement, 4, base.capacity, {})
+    say(f"batch tie rows V={g.n_nodes} E={g.n_edges}")
+    n_place = 12
+    pl = rng.integers(0, 4, (g.n_nodes, n_place)).astype(np.int32)
+    pl[:, 0::2] = 0
+    G = P.Graph(g.n_nodes, g.src, g.dst, g.comp, g.edge_cost, g.mem)
+    out = run_batch(P, G, pl, g)
+    assert (out["path_len"][0::2] <= 22).all()
+    assert out["is_critical"][:, 0::2].all()
+    check_batch(g, pl, out, range(n_place))
+    G.close()
+
+
 @pytest.mark.parametrize("seed", [21, 22])
 def test_batch_any_int32_labels(P, seed):
     """Without label sums the batch takes any int32 labels (only equality
