@@ -33,13 +33,16 @@
 #include "internal.h"
 #include "sweep_common.h"
 
+#include <type_traits>
+
 namespace pardnn {
 
 namespace {
 
 constexpr int kBlock = 256;
 constexpr int kChaseRegs = 16;      // registers per lane of a path-walk window
-constexpr int kEmitLds = 2 * 32 * 65 * 8 + 32 * 4 + 32 * 8 + 64 * 4;
+constexpr int kEmitNodes = 32;   // level-major nodes per emit workgroup
+constexpr int kEmitCols = 128;   // placements per emit chunk
 
 inline unsigned grid_for(int64_t n, int block, int cap = 65536) {
     int64_t g = (n + block - 1) / block;
@@ -503,35 +506,42 @@ __global__ __launch_bounds__(T) void k_sweep(SweepArgs a) {
 }
 
 // Outputs in the caller's layout: tl, bl [V][P] in original ids and the
-// critical flags crit = (tl + bl == M_p). A workgroup owns TV = 32 level-major
-// nodes and walks the placements in chunks of TP = 64: a chunk goes through an
-// LDS tile so that the slice-major workspace is read contiguously and each
-// output row order[v] is written as one contiguous run. All of a row is
-// written by one workgroup, in order, so the partial lines of neighbouring
-// chunks (the byte-wide flags) meet in the same L2. The loads of the next
-// chunk are in flight while the current one is stored. When `cbits` is given,
-// the flags of the workgroup's 32 nodes also go out as one bit word per
-// placement, cbits[p][bx] (bit r: level-major node 32 bx + r), for the path
-// walk; node groups are assigned so that the workgroups of one XCD (every
-// 8th workgroup) take consecutive groups, so that the words of one placement
-// row meet in that XCD's L2.
-template <int S, bool PACKED>
+// critical flags crit = (tl + bl == M_p). A workgroup owns TV level-major
+// nodes and walks the placements in chunks of TP: a chunk goes through an LDS
+// tile so that the slice-major workspace is read contiguously and each output
+// row order[v] is written as one contiguous run. All of a row is written by
+// one workgroup, in order, so the partial lines of neighbouring chunks (the
+// byte-wide flags) meet in the same L2. The loads of the next chunk are in
+// flight while the current one is stored. When `cbits` is given, the flags of
+// the workgroup's nodes also go out as TV / 32 bit words per placement,
+// cbits[p][w] (bit r of word w: level-major node 32 w + r), for the path
+// walk; node groups are assigned so that the workgroups of one XCD (every 8th
+// workgroup) take consecutive groups, so that the words of one placement row
+// meet in that XCD's L2.
+template <int TV, int TP>
+constexpr int emit_lds() {
+    return 2 * TV * (TP + 1) * 8 + TV * 4 + TV * 8 + TP * 8;
+}
+
+template <int S, bool PACKED, int TV, int TP>
 __device__ void emit_rows(const SweepArgs &a, uint8_t *crit, uint32_t *cbits, int32_t bx,
                           char *smem) {
     using EL = Elem<PACKED>;
     using ET = typename EL::T;
-    constexpr int TV = 32, TP = 64, NT = 256;
+    using BW = typename std::conditional<TV == 64, unsigned long long, uint32_t>::type;
+    constexpr int NT = 256;
     constexpr int PER = TV * TP / NT;  // elements per thread and chunk
     static_assert(NT % TP == 0, "a thread keeps one placement column");
-    static_assert(TV == 32, "one bit word per placement");
+    static_assert(TV == 32 || TV == 64, "one or two bit words per placement");
     long long(*t_tl)[TP + 1] = reinterpret_cast<long long(*)[TP + 1]>(smem);
     long long(*t_bl)[TP + 1] = reinterpret_cast<long long(*)[TP + 1]>(smem + TV * (TP + 1) * 8);
     int32_t *s_ord = reinterpret_cast<int32_t *>(smem + 2 * TV * (TP + 1) * 8);
     long long *s_comp = reinterpret_cast<long long *>(s_ord + TV);
-    uint32_t *s_bits = reinterpret_cast<uint32_t *>(s_comp + TV);   // [TP]
-    const int tid = threadIdx.x, lane = lane_id();
+    BW *s_bits = reinterpret_cast<BW *>(s_comp + TV);   // [TP]
+    const int tid = threadIdx.x, col = tid % TP;
     const int32_t V = a.V, P = a.P;
     const int32_t v0 = bx * TV;
+    const int32_t n_words = (V + 31) / 32;
     const int32_t n_slices = (P + S - 1) / S;
     const int32_t n_chunks = (P + TP - 1) / TP;
     const ET *ft = reinterpret_cast<const ET *>(a.ftl);
@@ -567,31 +577,36 @@ __device__ void emit_rows(const SweepArgs &a, uint8_t *crit, uint32_t *cbits, in
             t_bl[r][sl * S + s2] = EL::val(bv[j], a.lb);
         }
         if (ch + 1 < n_chunks) load(ch + 1);
-        const int32_t p = ch * TP + lane;   // this thread's placement column
+        const int32_t p = ch * TP + col;   // this thread's placement column
         const int64_t m = a.makespan[min(p, P - 1)];
         __syncthreads();
-        uint32_t bits = 0;
+        BW bits = 0;
         if (p < P) {
 #pragma unroll
             for (int j = 0; j < PER; j++) {
                 const int r = (tid + j * NT) / TP;
                 if (v0 + r < V) {
                     const int64_t o = (int64_t)s_ord[r] * P + p;
-                    const int64_t t = t_tl[r][lane], b = t_bl[r][lane];
+                    const int64_t t = t_tl[r][col], b = t_bl[r][col];
                     a.tl_out[o] = t;
                     a.bl_out[o] = b;
                     const bool c = t + b == m;
                     if (crit) crit[o] = (uint8_t)c;
-                    bits |= (uint32_t)c << r;
+                    bits |= (BW)c << r;
                 }
             }
         }
         if (cbits != nullptr) {
-            __hip_atomic_fetch_or(&s_bits[lane], bits, __ATOMIC_RELAXED,
+            __hip_atomic_fetch_or(&s_bits[col], bits, __ATOMIC_RELAXED,
                                   __HIP_MEMORY_SCOPE_WORKGROUP);
             __syncthreads();
             if (tid < TP) {
-                if (p < P) cbits[(int64_t)p * ((V + TV - 1) / TV) + bx] = s_bits[tid];
+                if (p < P) {
+                    const BW x = s_bits[tid];
+                    uint32_t *row = cbits + (int64_t)p * n_words + bx * (TV / 32);
+                    row[0] = (uint32_t)x;
+                    if (TV == 64 && bx * 2 + 1 < n_words) row[1] = (uint32_t)((uint64_t)x >> 32);
+                }
                 s_bits[tid] = 0;
             }
         }
@@ -775,8 +790,9 @@ __device__ __forceinline__ int32_t xcd_major(int32_t b, int32_t n) {
 
 template <int S, bool PACKED>
 __global__ __launch_bounds__(256) void k_emit(SweepArgs a, uint8_t *crit, uint32_t *cbits) {
-    __shared__ __align__(16) char smem[kEmitLds];
-    emit_rows<S, PACKED>(a, crit, cbits, xcd_major(blockIdx.x, gridDim.x), smem);
+    __shared__ __align__(16) char smem[emit_lds<kEmitNodes, kEmitCols>()];
+    emit_rows<S, PACKED, kEmitNodes, kEmitCols>(a, crit, cbits, xcd_major(blockIdx.x, gridDim.x),
+                                                smem);
 }
 
 constexpr int kSingleThreads = 512;
@@ -833,7 +849,7 @@ hipError_t launch_finish(const SweepArgs &a, int32_t S, uint8_t *crit, uint32_t 
     if (S != kBatchSlots) return hipErrorInvalidValue;
     if (path != nullptr && cbits == nullptr) return hipErrorInvalidValue;
     if (a.V > 0) {
-        const unsigned blocks = (unsigned)((a.V + 31) / 32);
+        const unsigned blocks = (unsigned)((a.V + kEmitNodes - 1) / kEmitNodes);
         uint32_t *bits = path != nullptr ? cbits : nullptr;
         if (a.lb > 0)
             k_emit<kBatchSlots, true><<<blocks, 256, 0, s>>>(a, crit, bits);

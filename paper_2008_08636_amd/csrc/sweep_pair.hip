@@ -52,7 +52,8 @@ constexpr int kRF = 2;               // far records loaded RF levels before thei
 constexpr int kNS = kD + kRF + 2;    // register sets in flight (loop unrolling)
 constexpr int kLN = kNS - 2;         // wave 0 loads LN levels ahead
 constexpr int kRS = kD + 1;          // LDS ring slots (levels)
-constexpr int kNB = kD + 2;          // accumulator buffers (levels)
+constexpr int kNB = 8;               // accumulator buffers (levels; >= kD + 2, a power of 2)
+static_assert(kNB >= kD + 2 && (kNB & (kNB - 1)) == 0, "accumulator buffers");
 constexpr int kPBinsCap = 2048;      // labels x slots of the LDS label bins
 // label sums of the t sweep: none, in LDS bins (K S <= kPBinsCap), or by
 // global atomics; a template parameter, so that a chain carries one of them
@@ -98,16 +99,16 @@ struct alignas(4 * S >= 16 ? 16 : 4 * S) LabS {
 // a fast level; the general path reads exact bounds).
 struct alignas(16) WinEnt {
     int32_t nlo, nrlo, frlo;
-    uint32_t cnt;   // min(w,255) | min(near,255) << 8 | min(far,255) << 16
+    uint32_t cnt;   // min(w,255) | min(near,255) << 8 | min(far,255) << 16 | fast << 31
 };
 constexpr int kWin = 128;            // window entries (steps); refilled every kWin / 2
 
 __device__ __forceinline__ int32_t cnt_w(uint32_t c) { return (int32_t)(c & 255u); }
 __device__ __forceinline__ int32_t cnt_near(uint32_t c) { return (int32_t)((c >> 8) & 255u); }
 __device__ __forceinline__ int32_t cnt_far(uint32_t c) { return (int32_t)((c >> 16) & 255u); }
-__device__ __forceinline__ bool cnt_fast(uint32_t c) {
-    return cnt_w(c) <= kPNodes && cnt_near(c) <= kNEn * kLanes && cnt_far(c) <= kNEf * kLanes;
-}
+// a level of the fast shape: at most 64 nodes, 64 kNEn span-1 and 64 kNEf
+// longer edges (decided when the window entry is staged)
+__device__ __forceinline__ bool cnt_fast(uint32_t c) { return (int32_t)c < 0; }
 
 template <int S>
 struct NearSet {   // wave 0, one level
@@ -328,9 +329,11 @@ __device__ __forceinline__ void pair_chain(const SweepArgs &a, int32_t slice, ch
             e.nlo = l0.node_lo;
             e.nrlo = l0.near_lo;
             e.frlo = l0.far_lo;
-            e.cnt = (uint32_t)min(l1.node_lo - l0.node_lo, 255) |
-                    (uint32_t)min(l1.near_lo - l0.near_lo, 255) << 8 |
-                    (uint32_t)min(l1.far_lo - l0.far_lo, 255) << 16;
+            const int32_t w = l1.node_lo - l0.node_lo, nn = l1.near_lo - l0.near_lo,
+                          nf = l1.far_lo - l0.far_lo;
+            const bool fast = w <= kPNodes && nn <= kNEn * kLanes && nf <= kNEf * kLanes;
+            e.cnt = (uint32_t)min(w, 255) | (uint32_t)min(nn, 255) << 8 |
+                    (uint32_t)min(nf, 255) << 16 | (fast ? 1u << 31 : 0u);
             c.win[sx & (kWin - 1)] = e;
         }
     };
