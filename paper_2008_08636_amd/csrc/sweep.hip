@@ -639,9 +639,9 @@ __device__ void chase_wave(const SweepArgs &a, const uint32_t *cbits, int32_t p,
     const int32_t n_words = (V + 31) / 32;
     const int32_t *nx = a.nx_w + (int64_t)slice * a.ws_stride;
     const uint32_t *bits = cbits + (int64_t)p * n_words;
-    // scratch: pos[0, V) and link[V, 2V) in int32 units
-    int32_t *pos = reinterpret_cast<int32_t *>(a.ftl + (int64_t)slice * a.ws_stride) +
-                   (int64_t)s * a.ws_stride;
+    // scratch: pos[0, V) and link[V, 2V) in int32 units, in the placement's
+    // share of the t workspace (4 ws_stride / S >= 4 (V + pad) int32 each)
+    int32_t *pos = reinterpret_cast<int32_t *>(a.ftl) + (int64_t)p * (4 * a.ws_stride / S);
     int32_t *link = pos + V;
     int32_t *out = path + (int64_t)p * stride;
     const int32_t start = __builtin_amdgcn_readfirstlane(a.start[p]);

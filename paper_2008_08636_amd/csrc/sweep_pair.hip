@@ -117,6 +117,8 @@ struct NearSet {   // wave 0, one level
     int64_t c[kNEn];
     int64_t comp, mem;
     LabS<S> lab;
+    int32_t wnlo;      // the level's first node and counts (its window entry),
+    uint32_t wcnt;     // carried with the set instead of re-read at every use
 };
 
 template <int S>
@@ -126,6 +128,7 @@ struct FarSet {    // wave 1, one level
     int64_t c[kNEf];
     int32_t tie[kNEf];
     VecS<S> f[kNEf];
+    uint32_t wcnt;     // the level's counts (its window entry)
 };
 
 template <int S>
@@ -359,6 +362,8 @@ __device__ __forceinline__ void pair_chain(const SweepArgs &a, int32_t slice, ch
             X.comp = n.comp;
             X.mem = n.mem;
             X.lab = at(c.labs, v);
+            X.wnlo = b.nlo;
+            X.wcnt = b.cnt;
         };
         // after level `step`: labels of step + 2, loads of step + LN, window refill
         auto tail = [&](int32_t step, const NearSet<S> &B2, NearSet<S> &LD, const WinEnt &b2,
@@ -408,8 +413,12 @@ __device__ __forceinline__ void pair_chain(const SweepArgs &a, int32_t slice, ch
         auto one = [&](auto RC) {
             constexpr int r = decltype(RC)::value;
             if constexpr (r < kNS) {
-                const WinEnt b0 = c.W(step), b1 = c.W(step + 1), b2 = c.W(step + 2),
-                             bl = c.W(step + kLN);
+                // the entries of levels step .. step + 2 came with their sets;
+                // only the one of the level loaded now is read from LDS
+                const WinEnt b0 = {st[r].wnlo, 0, 0, st[r].wcnt};
+                const WinEnt b1 = {0, 0, 0, st[(r + 1) % kNS].wcnt};
+                const WinEnt b2 = {0, 0, 0, st[(r + 2) % kNS].wcnt};
+                const WinEnt bl = c.W(step + kLN);
                 if (cnt_fast(b0.cnt))
                     body(step, b0, b1, st[r], st[(r + 1) % kNS]);
                 else
@@ -433,6 +442,7 @@ __device__ __forceinline__ void pair_chain(const SweepArgs &a, int32_t slice, ch
         FarSet<S> st[kNS];
         auto records = [&](FarSet<S> &X, const WinEnt &b) {
             const int32_t nf = cnt_far(b.cnt);
+            X.wcnt = b.cnt;
 #pragma unroll
             for (int j = 0; j < kNEf; j++) {
                 const uint32_t e = lane + j * kLanes < nf ? (uint32_t)(b.frlo + lane + j * kLanes) : 0u;
@@ -470,6 +480,7 @@ __device__ __forceinline__ void pair_chain(const SweepArgs &a, int32_t slice, ch
         };
         __syncthreads();   // the window is filled by wave 0
         if (L > 0) {
+            st[0].wcnt = c.W(0).cnt;
 #pragma unroll
             for (int j = 1; j <= kD + kRF; j++) records(st[j], c.W(j));
 #pragma unroll
@@ -484,8 +495,10 @@ __device__ __forceinline__ void pair_chain(const SweepArgs &a, int32_t slice, ch
         auto one = [&](auto RC) {
             constexpr int r = decltype(RC)::value;
             if constexpr (r < kNS) {
-                const WinEnt b0 = c.W(step), b1 = c.W(step + 1), bd = c.W(step + 1 + kD),
-                             brf = c.W(step + 1 + kD + kRF);
+                const WinEnt b0 = {0, 0, 0, st[r].wcnt};
+                const WinEnt b1 = {0, 0, 0, st[(r + 1) % kNS].wcnt};
+                const WinEnt bd = {0, 0, 0, st[(r + 1 + kD) % kNS].wcnt};
+                const WinEnt brf = c.W(step + 1 + kD + kRF);
                 FarSet<S> &B1 = st[(r + 1) % kNS];
                 if (cnt_fast(b0.cnt)) {
                     if (cnt_fast(b1.cnt)) fold_far(step, B1, b1);
