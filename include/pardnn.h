@@ -252,6 +252,32 @@ int pardnn_evaluate_moves(pardnn_graph *g, const int32_t *base, int32_t n_place,
                           int32_t *path_len, int64_t *label_mem,
                           int64_t *overflow);
 
+/*
+ * Memory Heuristic II (Sec. 3.2.2) evaluated for n_place placements: the
+ * per-partition memory of residual and of normal nodes, the balance predicate
+ * of Eq. 6 per partition, and the co-location of reference nodes with the
+ * residual node they mutate (node kinds of Sec. 3.2.1).
+ *   placements     int32[n_nodes][n_place], labels in [0, n_labels).
+ *   node_type      int32[n_nodes]: 0 normal, 1 residual, 2 reference.
+ *   ref_target     int32[n_nodes]: for a reference node the node it mutates,
+ *                  or -1; ignored for other kinds.
+ *   res_mem, nor_mem  int64[n_place][n_labels] outputs: sum of the graph's
+ *                  mem over the residual / normal nodes of each label
+ *                  (reference nodes reserve no memory).
+ *   balanced       uint8[n_place][n_labels] output: Eq. 6, n_labels / 2 *
+ *                  (res share + normal share) >= 1, decided exactly; a kind
+ *                  with no memory at all counts as the fair share 1 / n_labels.
+ *   ref_misplaced  int64[n_place] output: reference nodes whose target carries
+ *                  another label.
+ * Errors: E_INVAL (null pointers, n_labels < 1, a label, kind or target out of
+ * range). Syncs.
+ */
+int pardnn_memory_balance(pardnn_graph *g, int32_t n_place,
+                          const int32_t *placements, const int32_t *node_type,
+                          const int32_t *ref_target, int32_t n_labels,
+                          int64_t *res_mem, int64_t *nor_mem, uint8_t *balanced,
+                          int64_t *ref_misplaced);
+
 /* pardnn_evaluate_batch restricted to tl, bl and makespan. No sync. */
 int pardnn_tb_levels_batch(pardnn_graph *g, int32_t n_place,
                            const int32_t *placements, int64_t *tl, int64_t *bl,

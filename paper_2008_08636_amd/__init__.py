@@ -68,6 +68,7 @@ def load_library(path: str = LIB_PATH):
         "pardnn_evaluate_batch": [P, i32, P, i32, P, P, P, P, P, P, i32, P, P, P],
         "pardnn_evaluate_moves": [P, P, i32, P, P, P, i32, P, P, P, P, P, P, i32, P, P, P],
         "pardnn_tb_levels_batch": [P, i32, P, P, P, P],
+        "pardnn_memory_balance": [P, i32, P, P, P, i32, P, P, P, P],
         "pardnn_set_timing": [P, ctypes.c_int],
         "pardnn_get_timing": [P, ctypes.POINTER(ctypes.c_char_p), ctypes.POINTER(ctypes.c_float)],
     }
@@ -230,6 +231,15 @@ def pardnn_tb_levels_batch(h, n_place, placements, tl, bl, makespan):
         _ptr(makespan, torch.int64, n_place, "makespan")), "pardnn_tb_levels_batch")
 
 
+def pardnn_memory_balance(h, n_place, placements, node_type, ref_target, n_labels, res_mem,
+                          nor_mem, balanced, ref_misplaced):
+    _check(load_library().pardnn_memory_balance(
+        h, n_place, _ptr(placements, torch.int32), _ptr(node_type, torch.int32),
+        _ptr(ref_target, torch.int32), n_labels, _ptr(res_mem, torch.int64),
+        _ptr(nor_mem, torch.int64), _ptr(balanced, torch.uint8),
+        _ptr(ref_misplaced, torch.int64)), "pardnn_memory_balance")
+
+
 def pardnn_set_timing(h, enable: bool = True):
     _check(load_library().pardnn_set_timing(h, 1 if enable else 0), "pardnn_set_timing")
 
@@ -348,6 +358,22 @@ class Graph:
                               n_labels if labels else 0, capacity, out["tl"], out["bl"],
                               out["makespan"], out.get("is_critical"), out.get("path"), stride,
                               out.get("path_len"), out.get("label_mem"), out.get("overflow"))
+        return out
+
+    def memory_balance(self, placements, node_type, ref_target, n_labels):
+        """Memory Heuristic II per placement (see pardnn_memory_balance);
+        placements [V] or [V][P] (placement-minor)."""
+        P = 1 if placements.dim() == 1 else placements.shape[1]
+        dev = self.device
+        out = {
+            "res_mem": torch.empty((P, n_labels), dtype=torch.int64, device=dev),
+            "nor_mem": torch.empty((P, n_labels), dtype=torch.int64, device=dev),
+            "balanced": torch.empty((P, n_labels), dtype=torch.uint8, device=dev),
+            "ref_misplaced": torch.empty(P, dtype=torch.int64, device=dev),
+        }
+        pardnn_memory_balance(self._h, P, placements, node_type, ref_target, n_labels,
+                              out["res_mem"], out["nor_mem"], out["balanced"],
+                              out["ref_misplaced"])
         return out
 
     def evaluate_batch(self, placements, n_labels=0, capacity=None, crit=True, path=True,

@@ -665,6 +665,31 @@ int pardnn_label_memory(pardnn_graph *h, const int32_t *placement, int32_t n_lab
     return PARDNN_OK;
 }
 
+int pardnn_memory_balance(pardnn_graph *h, int32_t n_place, const int32_t *placements,
+                          const int32_t *node_type, const int32_t *ref_target, int32_t n_labels,
+                          int64_t *res_mem, int64_t *nor_mem, uint8_t *balanced,
+                          int64_t *ref_misplaced) {
+    CHECK_HANDLE(h);
+    Graph *g = reinterpret_cast<Graph *>(h);
+    if (n_place < 0) return fail(PARDNN_E_INVAL, "n_place must be >= 0");
+    if (n_labels < 1) return fail(PARDNN_E_INVAL, "n_labels must be >= 1");
+    if (n_place == 0) return PARDNN_OK;
+    if (res_mem == nullptr || nor_mem == nullptr || balanced == nullptr || ref_misplaced == nullptr)
+        return fail(PARDNN_E_INVAL, "res_mem, nor_mem, balanced and ref_misplaced must be non-null");
+    if (g->V > 0 && (placements == nullptr || node_type == nullptr || ref_target == nullptr))
+        return fail(PARDNN_E_INVAL, "placements, node_type and ref_target must be non-null");
+    DEVICE_SCOPE(g);
+    HIP_TRY(launch_fill_i32(g->err, 4, 0, g->stream));
+    HIP_TRY(launch_mem_balance(*g, n_place, placements, node_type, ref_target, n_labels, res_mem,
+                               nor_mem, balanced, ref_misplaced, g->err));
+    int st = read_errors(g);
+    if (st != PARDNN_OK) return st;
+    if (g->h_err[0] & 1) return fail(PARDNN_E_INVAL, "a label lies outside [0, n_labels)");
+    if (g->h_err[0] & 2) return fail(PARDNN_E_INVAL, "a node kind is not 0, 1 or 2");
+    if (g->h_err[0] & 4) return fail(PARDNN_E_INVAL, "a reference target lies outside [-1, n_nodes)");
+    return PARDNN_OK;
+}
+
 int pardnn_apply_moves(pardnn_graph *h, int32_t *placement, int32_t n_moves, const int32_t *node,
                        const int32_t *label) {
     CHECK_HANDLE(h);

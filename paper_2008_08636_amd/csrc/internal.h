@@ -264,6 +264,14 @@ hipError_t launch_apply_moves(const Graph &g, int32_t *placement, int32_t n, con
 hipError_t launch_build_placements(const Graph &g, const int32_t *base, int32_t P,
                                    const int64_t *step_ptr, int64_t M, const int32_t *node,
                                    const int32_t *label, int32_t *placements, int32_t *err);
+// ---- heuristics.hip ----
+// Memory Heuristic II sums, Eq. 6 and reference co-location for P placements
+// [V][P]; err bits: 1 label out of range, 2 bad node kind, 4 bad reference target
+hipError_t launch_mem_balance(const Graph &g, int32_t P, const int32_t *placements,
+                              const int32_t *node_type, const int32_t *ref_target, int32_t K,
+                              int64_t *res_mem, int64_t *nor_mem, uint8_t *balanced,
+                              int64_t *misplaced, int32_t *err);
+
 // int32 elements of the scratch launch_moves_to_slices needs for M moves
 size_t moves_scratch_elems(int32_t V, int64_t M);
 hipError_t launch_moves_to_slices(const Graph &g, const int32_t *base, int32_t P,

@@ -1,0 +1,159 @@
+"""GPU parity for the rows after the core path, through the C ABI, against the
+oracle: Memory Heuristic II evaluation (pardnn_memory_balance). All values are
+integers, so every comparison is exact. Each case prints its name first.
+"""
+import json
+import os
+import sys
+
+import numpy as np
+import pytest
+import torch
+
+import workloads as W
+from oracle.memory_balance import memory_balance
+
+pytestmark = pytest.mark.gpu
+GOLDEN = os.path.join(os.path.dirname(__file__), "golden", "next")
+
+
+def say(msg):
+    print(f"[gpu-case] {msg}", flush=True)
+    sys.stdout.flush()
+
+
+@pytest.fixture(scope="module")
+def P():
+    import paper_2008_08636_amd as P
+    if not torch.cuda.is_available():
+        pytest.fail("GPU tests need a visible GPU")
+    P.load_library()
+    return P
+
+
+def dev(x, dt):
+    return torch.as_tensor(np.ascontiguousarray(x), dtype=dt).cuda()
+
+
+def check_balance(g_nodes, mem, kind, tgt, pl_vp, K, out, cols):
+    for p in cols:
+        e = memory_balance(g_nodes, mem, kind, tgt, pl_vp[:, p], K)
+        assert (out["res_mem"][p] == e["res_mem"]).all(), p
+        assert (out["nor_mem"][p] == e["nor_mem"]).all(), p
+        assert (out["balanced"][p] == e["balanced"]).all(), p
+        assert int(out["ref_misplaced"][p]) == e["ref_misplaced"], p
+
+
+def run_balance(G, pl_vp, kind, tgt, K):
+    out = G.memory_balance(dev(pl_vp, torch.int32), dev(kind, torch.int32),
+                           dev(tgt, torch.int32), K)
+    torch.cuda.synchronize()
+    return {k: v.cpu().numpy() for k, v in out.items()}
+
+
+def test_memory_balance_paper_example(P):
+    say("heuristic II paper example")
+    d = json.load(open(os.path.join(GOLDEN, "heuristic2_paper_example.json")))
+    G = P.Graph(d["n_nodes"], np.array(d["src"], np.int32), np.array(d["dst"], np.int32),
+                np.array(d["comp"], np.int64), np.array(d["edge_cost"], np.int64),
+                np.array(d["mem"], np.int64))
+    pl = np.stack([d["placements"]["before"], d["placements"]["after"]], axis=1)
+    out = run_balance(G, pl, d["node_type"], d["ref_target"], d["n_labels"])
+    for p, name in enumerate(["before", "after"]):
+        exp = d["expect"][name]
+        assert out["res_mem"][p].tolist() == exp["res_mem"]
+        assert out["nor_mem"][p].tolist() == exp["nor_mem"]
+        assert out["balanced"][p].tolist() == exp["balanced"]
+        assert int(out["ref_misplaced"][p]) == exp["ref_misplaced"]
+    G.close()
+
+
+@pytest.mark.parametrize("K,n_place", [(1, 3), (2, 1), (16, 37), (33, 5), (100, 70)])
+def test_memory_balance_random(P, K, n_place):
+    """K = 33 and 100 take the global-atomic path (more labels than LDS bins);
+    70 placements span two placement tiles with a ragged tail."""
+    say(f"heuristic II random K={K} P={n_place}")
+    rng = np.random.default_rng(1000 + K)
+    g = W.random_dag(rng, 700, p_edge=0.01, max_weight=9, n_labels=min(K, 4))
+    kind, tgt = W.node_kinds(g, seed=K)
+    pl = rng.integers(0, K, (g.n_nodes, n_place)).astype(np.int32)
+    G = P.Graph(g.n_nodes, g.src, g.dst, g.comp, g.edge_cost, g.mem)
+    out = run_balance(G, pl, kind, tgt, K)
+    check_balance(g.n_nodes, g.mem, kind, tgt, pl, K, out, range(n_place))
+    G.close()
+
+
+def test_memory_balance_degenerate(P):
+    say("heuristic II degenerate kinds")
+    rng = np.random.default_rng(5)
+    g = W.random_dag(rng, 200, p_edge=0.02, max_weight=5, n_labels=3)
+    pl = rng.integers(0, 3, (g.n_nodes, 4)).astype(np.int32)
+    G = P.Graph(g.n_nodes, g.src, g.dst, g.comp, g.edge_cost, g.mem)
+    none = np.full(g.n_nodes, -1, np.int32)
+    for kind in (np.zeros(g.n_nodes, np.int32), np.ones(g.n_nodes, np.int32),
+                 np.full(g.n_nodes, 2, np.int32)):
+        out = run_balance(G, pl, kind, none, 3)
+        check_balance(g.n_nodes, g.mem, kind, none, pl, 3, out, range(4))
+    G.close()
+    # no memory at all
+    z = np.zeros(g.n_nodes, np.int64)
+    G = P.Graph(g.n_nodes, g.src, g.dst, g.comp, g.edge_cost, z)
+    kind, tgt = W.node_kinds(g)
+    out = run_balance(G, pl, kind, tgt, 3)
+    assert out["balanced"].all()
+    check_balance(g.n_nodes, z, kind, tgt, pl, 3, out, range(4))
+    G.close()
+
+
+def test_memory_balance_errors(P):
+    say("heuristic II errors")
+    rng = np.random.default_rng(6)
+    g = W.random_dag(rng, 50, p_edge=0.1, max_weight=5, n_labels=2)
+    kind, tgt = W.node_kinds(g)
+    G = P.Graph(g.n_nodes, g.src, g.dst, g.comp, g.edge_cost, g.mem)
+    pl = np.zeros((g.n_nodes, 2), np.int32)
+    bad = pl.copy()
+    bad[3, 1] = 2
+    with pytest.raises(P.PardnnError) as e:
+        run_balance(G, bad, kind, tgt, 2)
+    assert e.value.status == P.E_INVAL
+    k2 = kind.copy()
+    k2[7] = 3
+    with pytest.raises(P.PardnnError) as e:
+        run_balance(G, pl, k2, tgt, 2)
+    assert e.value.status == P.E_INVAL
+    k3, t3 = kind.copy(), tgt.copy()
+    k3[9], t3[9] = 2, g.n_nodes
+    with pytest.raises(P.PardnnError) as e:
+        run_balance(G, pl, k3, t3, 2)
+    assert e.value.status == P.E_INVAL
+    with pytest.raises(P.PardnnError) as e:
+        run_balance(G, pl, kind, tgt, 0)
+    assert e.value.status == P.E_INVAL
+    G.close()
+
+
+def test_memory_balance_refinement_loop_full_size(P):
+    """The 1000 placements of the refinement loop on the transformer graph, with
+    the graph's own memory kinds (variables residual, their optimiser updates
+    reference nodes): sampled placements against the oracle, totals on all."""
+    g = W.make_config(2)
+    say(f"heuristic II full size V={g.n_nodes} P=1000")
+    kind, tgt = W.node_kinds(g)
+    sched = W.config4_moves(g, n_place=1000)
+    G = P.Graph(g.n_nodes, g.src, g.dst, g.comp, g.edge_cost, g.mem)
+    pl = G.build_placements(dev(sched.base, torch.int32), dev(sched.ptr, torch.int64),
+                            dev(sched.node, torch.int32), dev(sched.label, torch.int32))
+    out = G.memory_balance(pl, dev(kind, torch.int32), dev(tgt, torch.int32), g.n_labels)
+    torch.cuda.synchronize()
+    res_total = int(g.mem[kind == 1].sum())
+    nor_total = int(g.mem[kind == 0].sum())
+    assert bool((out["res_mem"].sum(dim=1) == res_total).all())
+    assert bool((out["nor_mem"].sum(dim=1) == nor_total).all())
+    assert bool((out["balanced"].sum(dim=1) >= 1).all())
+    host = {k: v.cpu().numpy() for k, v in out.items()}
+    exp_pl = W.materialize_placements(sched)
+    cols = [0, 1, 500, 998, 999]
+    check_balance(g.n_nodes, g.mem, kind, tgt, exp_pl[cols].T.copy(), g.n_labels,
+                  {k: v[cols] for k, v in host.items()}, range(len(cols)))
+    G.close()

@@ -1,0 +1,123 @@
+"""Pins of the oracle functions for the rows after the core path: Memory
+Heuristic II evaluation (Sec. 3.2.2). CPU only.
+
+The paper's own worked example of Heuristic II (a fixture under tests/golden/)
+pins the Eq. 6 predicate and the memory kinds; a per-node loop written here
+pins the vectorised sums; invariants pin the rest.
+"""
+import json
+import os
+from fractions import Fraction
+
+import numpy as np
+import pytest
+
+from oracle.memory_balance import memory_balance
+import workloads as W
+
+GOLDEN = os.path.join(os.path.dirname(__file__), "golden", "next")
+
+
+def test_heuristic2_paper_example():
+    d = json.load(open(os.path.join(GOLDEN, "heuristic2_paper_example.json")))
+    for name, lab in d["placements"].items():
+        r = memory_balance(d["n_nodes"], d["mem"], d["node_type"], d["ref_target"], lab,
+                           d["n_labels"])
+        exp = d["expect"][name]
+        assert r["res_mem"].tolist() == exp["res_mem"], name
+        assert r["nor_mem"].tolist() == exp["nor_mem"], name
+        assert r["balanced"].tolist() == exp["balanced"], name
+        assert r["ref_misplaced"] == exp["ref_misplaced"], name
+
+
+def _per_node(n, mem, kind, target, label, K):
+    res, nor = [0] * K, [0] * K
+    mis = 0
+    for v in range(n):
+        if kind[v] == 1:
+            res[label[v]] += int(mem[v])
+        elif kind[v] == 0:
+            nor[label[v]] += int(mem[v])
+        elif target[v] >= 0 and label[target[v]] != label[v]:
+            mis += 1
+    return res, nor, mis
+
+
+@pytest.mark.parametrize("seed", range(6))
+def test_heuristic2_sums_against_a_node_loop(seed):
+    rng = np.random.default_rng(seed)
+    n = int(rng.integers(0, 300))
+    K = int(rng.integers(1, 9))
+    mem = rng.integers(0, 1000, n)
+    kind = rng.integers(0, 3, n)
+    res_nodes = np.nonzero(kind == 1)[0]
+    target = np.full(n, -1)
+    for v in np.nonzero(kind == 2)[0]:
+        if res_nodes.size and rng.random() < 0.9:
+            target[v] = res_nodes[rng.integers(res_nodes.size)]
+    label = rng.integers(0, K, n)
+    r = memory_balance(n, mem, kind, target, label, K)
+    res, nor, mis = _per_node(n, mem, kind, target, label, K)
+    assert r["res_mem"].tolist() == res and r["nor_mem"].tolist() == nor
+    assert r["ref_misplaced"] == mis
+    # the K shares of each kind sum to one, so their mean is 1 / K and some
+    # partition is at or above it: Eq. 6 holds somewhere
+    assert r["balanced"].any()
+
+
+def test_heuristic2_invariants():
+    rng = np.random.default_rng(7)
+    n, K = 500, 5
+    mem = rng.integers(1, 10 ** 6, n)
+    kind = rng.integers(0, 2, n)
+    label = rng.integers(0, K, n)
+    tgt = np.full(n, -1)
+    r = memory_balance(n, mem, kind, tgt, label, K)
+    assert r["res_mem"].sum() == mem[kind == 1].sum()
+    assert r["nor_mem"].sum() == mem[kind == 0].sum()
+    # relabelling the partitions permutes the outputs
+    perm = rng.permutation(K)
+    r2 = memory_balance(n, mem, kind, tgt, perm[label], K)
+    assert (r2["res_mem"][perm] == r["res_mem"]).all()
+    assert (r2["balanced"][perm] == r["balanced"]).all()
+    # one partition holds everything: balanced
+    assert memory_balance(n, mem, kind, tgt, np.zeros(n, int), 1)["balanced"].tolist() == [1]
+    # identical per-label content (node i on label i mod K, kind (i div K)
+    # mod 2, equal memory): every partition exactly at its share
+    i = np.arange(n)
+    r3 = memory_balance(n, np.full(n, 7), (i // K) % 2, tgt, i % K, K)
+    assert r3["balanced"].all()
+
+
+def test_heuristic2_one_kind_missing():
+    # no residual memory: the residual share counts as 1/K on every partition,
+    # so Eq. 6 reads K/2 (1/K + share) >= 1, i.e. share >= 1/K
+    n, K = 6, 3
+    mem = [30, 30, 20, 10, 5, 5]
+    kind = [0] * 6
+    label = [0, 0, 1, 1, 2, 2]
+    r = memory_balance(n, mem, kind, [-1] * 6, label, K)
+    shares = [Fraction(60, 100), Fraction(30, 100), Fraction(10, 100)]
+    assert r["balanced"].tolist() == [int(s >= Fraction(1, K)) for s in shares] == [1, 0, 0]
+    # no memory at all: balanced everywhere
+    r0 = memory_balance(n, [0] * 6, kind, [-1] * 6, label, K)
+    assert r0["balanced"].tolist() == [1, 1, 1]
+
+
+def test_heuristic2_rejects_bad_input():
+    with pytest.raises(ValueError):
+        memory_balance(2, [1, 1], [0, 0], [-1, -1], [0, 2], 2)
+    with pytest.raises(ValueError):
+        memory_balance(2, [1, 1], [0, 3], [-1, -1], [0, 1], 2)
+    with pytest.raises(ValueError):
+        memory_balance(2, [1, 1], [0, 2], [-1, 5], [0, 1], 2)
+
+
+def test_transformer_kinds_are_variables_and_their_updates():
+    g = W.make_config(2)
+    kind, tgt = W.node_kinds(g)
+    refs = np.nonzero(kind == 2)[0]
+    assert refs.size > 0 and (kind[tgt[refs]] == 1).all()
+    # an optimiser op is a direct successor of the variable it updates
+    pairs = set(zip(g.src.tolist(), g.dst.tolist()))
+    assert all((int(tgt[v]), int(v)) in pairs for v in refs[:500])

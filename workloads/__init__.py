@@ -17,4 +17,5 @@ from .graphs import (  # noqa: F401
     random_dag,
     chain_graph,
     layered_dag,
+    node_kinds,
 )

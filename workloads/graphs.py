@@ -90,8 +90,10 @@ class MoveSchedule:
 
 
 def _finish(name, rng, n, src, dst, comp, nbytes, mem, label, n_labels, meta,
-            permute=True):
-    """Convert to arrays, renumber nodes by a random permutation, shuffle edges."""
+            permute=True, kinds=None):
+    """Convert to arrays, renumber nodes by a random permutation, shuffle edges.
+    ``kinds`` (optional) is (node_type int[n], ref_target int[n]) in the
+    pre-permutation ids; it is renumbered with the nodes into meta."""
     src = np.asarray(src, np.int64)
     dst = np.asarray(dst, np.int64)
     comp = np.asarray(comp, np.int64)
@@ -107,6 +109,15 @@ def _finish(name, rng, n, src, dst, comp, nbytes, mem, label, n_labels, meta,
         comp, mem, label = inv_comp, inv_mem, inv_label
         eperm = rng.permutation(src.shape[0])
         src, dst, cost = src[eperm], dst[eperm], cost[eperm]
+        if kinds is not None:
+            kt, kr = np.asarray(kinds[0], np.int32), np.asarray(kinds[1], np.int64)
+            nt, nr = np.empty_like(kt), np.empty(n, np.int32)
+            nt[perm] = kt
+            nr[perm] = np.where(kr >= 0, perm[np.maximum(kr, 0)], -1)
+            meta = dict(meta, node_type=nt, ref_target=nr)
+    elif kinds is not None:
+        meta = dict(meta, node_type=np.asarray(kinds[0], np.int32),
+                    ref_target=np.asarray(kinds[1], np.int32))
     cap = np.full(n_labels, CAPACITY_32G_90, np.int64)
     return SynthGraph(name, int(n), src.astype(np.int32), dst.astype(np.int32), comp,
                       cost.astype(np.int64), mem, label, int(n_labels), cap, meta)
@@ -333,11 +344,21 @@ def config2(seed: int = SEED_BASE + 2) -> SynthGraph:
     D_loss = alloc(1, K - 1)
     S += [block_in, loss, D_loss]; D += [loss, D_loss, A_in]
     clip = alloc(1, K - 1)
+    opt_of = []   # (optimiser op, the variable it updates)
     for var, dd, lbl in param_pairs:
         opt = alloc(1, lbl)
         S += [dd, var, dd, clip]; D += [clip, opt, opt, opt]
+        opt_of.append((opt, var))
     del param_D
     n = len(labels)
+    # memory kinds (Sec. 3.2.1): variables are residual, the optimiser op that
+    # updates a variable in place is a reference node to it, the rest normal
+    node_type = np.zeros(n, np.int32)
+    ref_target = np.full(n, -1, np.int64)
+    for opt, var in opt_of:
+        node_type[var] = 1
+        node_type[opt] = 2
+        ref_target[opt] = var
     label = np.asarray(labels, np.int32)
     moved = rng.choice(n, int(round(0.02 * n)), replace=False)
     label[moved] = (label[moved] + rng.integers(1, K, moved.shape[0])) % K
@@ -347,7 +368,8 @@ def config2(seed: int = SEED_BASE + 2) -> SynthGraph:
     comp = _log_uniform(rng, 1, 10_000, n)
     mem = _log_uniform(rng, 4 * KIB, 64 * MIB, n)
     return _finish("transformer_48blk_300k", rng, n, S, D, comp, nbytes, mem, label, K,
-                   {"template_depth": depth, "template_ops": F})
+                   {"template_depth": depth, "template_ops": F},
+                   kinds=(node_type, ref_target))
 
 
 # --------------------------------------------------------------------------
@@ -480,6 +502,28 @@ def materialize_placements(sched: MoveSchedule, first: int = 0, count: int | Non
         if p >= first:
             out[p - first] = cur
     return out
+
+
+def node_kinds(g: SynthGraph, seed: int = SEED_BASE + 100, p_res: float = 0.10,
+               p_ref: float = 0.08):
+    """Memory kinds of the nodes (Sec. 3.2.1): the graph's own when its
+    generator records them, else a seeded draw -- a fraction p_res residual,
+    p_ref reference nodes each mutating a uniform residual node, the rest
+    normal. Returns (node_type int32[V], ref_target int32[V])."""
+    if "node_type" in g.meta:
+        return g.meta["node_type"], g.meta["ref_target"]
+    rng = _rng(seed)
+    n = g.n_nodes
+    u = rng.random(n)
+    node_type = np.where(u < p_res, 1, np.where(u < p_res + p_ref, 2, 0)).astype(np.int32)
+    res = np.nonzero(node_type == 1)[0]
+    ref_target = np.full(n, -1, np.int32)
+    refs = np.nonzero(node_type == 2)[0]
+    if res.size:
+        ref_target[refs] = res[rng.integers(0, res.size, refs.size)]
+    else:
+        node_type[refs] = 0
+    return node_type, ref_target
 
 
 def make_config(i: int, seed: int | None = None) -> SynthGraph:
