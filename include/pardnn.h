@@ -278,6 +278,27 @@ int pardnn_memory_balance(pardnn_graph *g, int32_t n_place,
                           int64_t *res_mem, int64_t *nor_mem, uint8_t *balanced,
                           int64_t *ref_misplaced);
 
+/*
+ * The primary clusters of graph slicing (Alg. 1, Sec. 3.1.1): K rounds, each
+ * computing the weighted levels of the remaining graph, taking its heaviest
+ * path -- a critical path, the canonical one of pardnn_critical_path -- as
+ * primary cluster j, and removing that path's nodes and their edges. Before
+ * any placement exists every edge carries its communication cost (every node
+ * is its own cluster). A path starts at a node without remaining predecessors.
+ *   primary        int32[n_nodes] output: the round that took each node, or -1.
+ *   paths          int32[K][path_stride] output: round j's path in its first
+ *                  path_len[j] entries (original ids, source to sink).
+ *   path_stride    >= number of levels.
+ *   path_len       int32[K] output (0 once no node remains).
+ *   makespan       int64[K] output: the critical-path length of the graph
+ *                  remaining before round j (0 when empty).
+ * Errors: E_INVAL (K < 0, null pointers, short path_stride), E_CYCLE.
+ * Syncs only when the graph is levelised first.
+ */
+int pardnn_slice_primaries(pardnn_graph *g, int32_t K, int32_t *primary,
+                           int32_t *paths, int32_t path_stride,
+                           int32_t *path_len, int64_t *makespan);
+
 /* pardnn_evaluate_batch restricted to tl, bl and makespan. No sync. */
 int pardnn_tb_levels_batch(pardnn_graph *g, int32_t n_place,
                            const int32_t *placements, int64_t *tl, int64_t *bl,

@@ -69,6 +69,7 @@ def load_library(path: str = LIB_PATH):
         "pardnn_evaluate_moves": [P, P, i32, P, P, P, i32, P, P, P, P, P, P, i32, P, P, P],
         "pardnn_tb_levels_batch": [P, i32, P, P, P, P],
         "pardnn_memory_balance": [P, i32, P, P, P, i32, P, P, P, P],
+        "pardnn_slice_primaries": [P, i32, P, P, i32, P, P],
         "pardnn_set_timing": [P, ctypes.c_int],
         "pardnn_get_timing": [P, ctypes.POINTER(ctypes.c_char_p), ctypes.POINTER(ctypes.c_float)],
     }
@@ -240,6 +241,12 @@ def pardnn_memory_balance(h, n_place, placements, node_type, ref_target, n_label
         _ptr(ref_misplaced, torch.int64)), "pardnn_memory_balance")
 
 
+def pardnn_slice_primaries(h, K, primary, paths, path_stride, path_len, makespan):
+    _check(load_library().pardnn_slice_primaries(
+        h, K, _ptr(primary, torch.int32), _ptr(paths, torch.int32), path_stride,
+        _ptr(path_len, torch.int32), _ptr(makespan, torch.int64)), "pardnn_slice_primaries")
+
+
 def pardnn_set_timing(h, enable: bool = True):
     _check(load_library().pardnn_set_timing(h, 1 if enable else 0), "pardnn_set_timing")
 
@@ -374,6 +381,22 @@ class Graph:
         pardnn_memory_balance(self._h, P, placements, node_type, ref_target, n_labels,
                               out["res_mem"], out["nor_mem"], out["balanced"],
                               out["ref_misplaced"])
+        return out
+
+    def slice_primaries(self, K):
+        """The K primary clusters of graph slicing (see pardnn_slice_primaries)."""
+        L = self.info()["n_levels"]
+        if L < 0:
+            L = pardnn_levelize(self._h)
+        dev, stride = self.device, max(L, 1)
+        out = {
+            "primary": torch.empty(self.n_nodes, dtype=torch.int32, device=dev),
+            "paths": torch.empty((K, stride), dtype=torch.int32, device=dev),
+            "path_len": torch.empty(K, dtype=torch.int32, device=dev),
+            "makespan": torch.empty(K, dtype=torch.int64, device=dev),
+        }
+        pardnn_slice_primaries(self._h, K, out["primary"], out["paths"], stride,
+                               out["path_len"], out["makespan"])
         return out
 
     def evaluate_batch(self, placements, n_labels=0, capacity=None, crit=True, path=True,

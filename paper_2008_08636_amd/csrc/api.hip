@@ -690,6 +690,69 @@ int pardnn_memory_balance(pardnn_graph *h, int32_t n_place, const int32_t *place
     return PARDNN_OK;
 }
 
+int pardnn_slice_primaries(pardnn_graph *h, int32_t K, int32_t *primary, int32_t *paths,
+                           int32_t path_stride, int32_t *path_len, int64_t *makespan) {
+    CHECK_HANDLE(h);
+    Graph *g = reinterpret_cast<Graph *>(h);
+    if (K < 0) return fail(PARDNN_E_INVAL, "K must be >= 0");
+    if (K > 0 && (path_len == nullptr || makespan == nullptr || paths == nullptr))
+        return fail(PARDNN_E_INVAL, "paths, path_len and makespan must be non-null");
+    if (g->V > 0 && primary == nullptr) return fail(PARDNN_E_INVAL, "primary must be non-null");
+    DEVICE_SCOPE(g);
+    int st = ensure_levelized(g);
+    if (st != PARDNN_OK) return st;
+    if (K > 0 && path_stride < std::max(g->L, 1))
+        return fail(PARDNN_E_INVAL, "path_stride must be at least the number of levels");
+    const int32_t V = g->V;
+    if (V == 0) {
+        if (K > 0) {
+            HIP_TRY(launch_fill_i32(path_len, K, 0, g->stream));
+            HIP_TRY(launch_fill_i64(makespan, K, 0, g->stream));
+        }
+        return PARDNN_OK;
+    }
+    if (!g->sl_node_rec) {
+        HIP_TRY(dalloc(*g, &g->sl_node_rec, V));
+        HIP_TRY(dalloc(*g, &g->sl_comp, V));
+        HIP_TRY(dalloc(*g, &g->sl_tl, V));
+        HIP_TRY(dalloc(*g, &g->sl_bl, V));
+        HIP_TRY(dalloc(*g, &g->sl_alive, V));
+        HIP_TRY(dalloc(*g, &g->sl_crit, V));
+        HIP_TRY(dalloc(*g, &g->sl_iota, V));
+        HIP_TRY(dalloc(*g, &g->sl_start, 1));
+        // every node its own label: before placement all communication counts
+        HIP_TRY(launch_iota_i32(g->sl_iota, V, g->stream));
+    }
+    // a removed node weighs -B with B above every path length
+    const int64_t big = g->weight_bound < INT64_MAX ? g->weight_bound + 1 : INT64_MAX;
+    HIP_TRY(launch_slice_init(*g, g->sl_node_rec, g->sl_comp, g->sl_alive, primary));
+    for (int32_t j = 0; j < K; j++) {
+        SweepArgs a = sweep_args(g);
+        a.P = 1;
+        a.K = 0;
+        a.lab_w = g->order;   // pairwise distinct labels in level-major order
+        a.lab_stride = V;
+        a.ftl = g->ft_lm;
+        a.bll = g->bl_lm;
+        a.ws_stride = V;
+        a.tl_out = g->sl_tl;
+        a.bl_out = g->sl_bl;
+        a.makespan = makespan + j;
+        a.node_rec = g->sl_node_rec;
+        a.comp_lm = g->sl_comp;
+        HIP_TRY(launch_sweep(a, 1, g->stream));
+        HIP_TRY(launch_slice_makespan(*g, g->sl_alive, g->sl_tl, g->sl_bl, makespan + j));
+        HIP_TRY(launch_crit_next(*g, g->sl_iota, g->sl_comp, g->sl_tl, g->sl_bl, makespan + j,
+                                 g->sl_crit));
+        HIP_TRY(launch_slice_start(*g, g->sl_alive, g->sl_start));
+        int32_t *pj = paths + (int64_t)j * path_stride;
+        HIP_TRY(launch_chase_from(*g, g->sl_start, pj, path_len + j));
+        HIP_TRY(launch_slice_remove(*g, j, pj, path_len + j, big, g->sl_node_rec, g->sl_comp,
+                                    g->sl_alive, primary));
+    }
+    return PARDNN_OK;
+}
+
 int pardnn_apply_moves(pardnn_graph *h, int32_t *placement, int32_t n_moves, const int32_t *node,
                        const int32_t *label) {
     CHECK_HANDLE(h);

@@ -65,8 +65,12 @@ __global__ void k_crit_next(int32_t V, const int32_t *order, const int32_t *out_
     }
 }
 
+// The walk starts at the smallest-id critical node without predecessors, or,
+// when start_orig is given, at that node (INT32_MAX: no path).
 __global__ __launch_bounds__(kChaseThreads) void k_chase(int32_t V, int32_t n0,
                                                          const int32_t *order,
+                                                         const int32_t *rank,
+                                                         const int32_t *start_orig,
                                                          const int32_t *next_lm,
                                                          const uint8_t *crit_lm, int32_t *path,
                                                          int32_t *path_len) {
@@ -80,8 +84,12 @@ __global__ __launch_bounds__(kChaseThreads) void k_chase(int32_t V, int32_t n0,
     __syncthreads();
     // level 0 is sorted by original id: the smallest critical lm index there
     // is the smallest-id critical node without predecessors
-    for (int32_t v = tid; v < n0; v += kChaseThreads)
-        if (crit_lm[v]) lds_min_i32(&s_start, v);
+    if (start_orig == nullptr) {
+        for (int32_t v = tid; v < n0; v += kChaseThreads)
+            if (crit_lm[v]) lds_min_i32(&s_start, v);
+    } else if (tid == 0 && *start_orig != INT32_MAX) {
+        s_start = rank[*start_orig];
+    }
     __syncthreads();
     if (tid == 0) s_cur = s_start == INT32_MAX ? -1 : s_start;
     __syncthreads();
@@ -109,20 +117,30 @@ __global__ __launch_bounds__(kChaseThreads) void k_chase(int32_t V, int32_t n0,
 
 }  // namespace
 
+hipError_t launch_crit_next(const Graph &g, const int32_t *placement, const int64_t *comp_lm,
+                            const int64_t *tl, const int64_t *bl, const int64_t *makespan,
+                            uint8_t *is_critical) {
+    if (g.V == 0) return hipSuccess;
+    k_crit_next<<<grid_for(g.V, kBlock), kBlock, 0, g.stream>>>(
+        g.V, g.order, g.out_off, g.out_dst, g.out_dst_orig, g.out_cost, comp_lm, placement, tl,
+        bl, makespan, is_critical, g.next_lm, g.crit_lm);
+    return hipGetLastError();
+}
+
+hipError_t launch_chase_from(const Graph &g, const int32_t *start_orig, int32_t *path,
+                             int32_t *path_len) {
+    const int32_t n0 = g.L > 0 ? g.h_level_ptr[1] : 0;
+    k_chase<<<1, kChaseThreads, 0, g.stream>>>(g.V, n0, g.order, g.rank, start_orig, g.next_lm,
+                                               g.crit_lm, path, path_len);
+    return hipGetLastError();
+}
+
 hipError_t launch_critical_path(const Graph &g, const int32_t *placement, const int64_t *tl,
                                 const int64_t *bl, const int64_t *makespan,
                                 uint8_t *is_critical, int32_t *path, int32_t *path_len) {
-    if (g.V > 0) {
-        k_crit_next<<<grid_for(g.V, kBlock), kBlock, 0, g.stream>>>(
-            g.V, g.order, g.out_off, g.out_dst, g.out_dst_orig, g.out_cost, g.comp_lm, placement,
-            tl, bl, makespan, is_critical, g.next_lm, g.crit_lm);
-        hipError_t e = hipGetLastError();
-        if (e != hipSuccess) return e;
-    }
-    const int32_t n0 = g.L > 0 ? g.h_level_ptr[1] : 0;
-    k_chase<<<1, kChaseThreads, 0, g.stream>>>(g.V, n0, g.order, g.next_lm, g.crit_lm, path,
-                                               path_len);
-    return hipGetLastError();
+    hipError_t e = launch_crit_next(g, placement, g.comp_lm, tl, bl, makespan, is_critical);
+    if (e != hipSuccess) return e;
+    return launch_chase_from(g, nullptr, path, path_len);
 }
 
 }  // namespace pardnn

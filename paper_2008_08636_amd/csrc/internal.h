@@ -184,6 +184,12 @@ struct Graph {
     int32_t *lab_lm = nullptr, *next_lm = nullptr, *move_stamp = nullptr;
     uint8_t *crit_lm = nullptr;
     int64_t *ft_lm = nullptr, *bl_lm = nullptr;   // {value, label} pairs, 2 * V each
+    // graph slicing scratch (allocated on first use): masked node weights,
+    // remaining-node flags, an identity placement, tl / bl / flags, the start
+    NodeRec16 *sl_node_rec = nullptr;
+    int64_t *sl_comp = nullptr, *sl_tl = nullptr, *sl_bl = nullptr;
+    uint8_t *sl_alive = nullptr, *sl_crit = nullptr;
+    int32_t *sl_iota = nullptr, *sl_start = nullptr;
     int32_t *err = nullptr;          // device error words [4]
     int32_t *h_err = nullptr;        // pinned host mirror [4]
 
@@ -206,6 +212,7 @@ int fail(int status, const std::string &msg);
 // ---- structure.hip ----
 hipError_t launch_fill_i32(int32_t *p, int64_t n, int32_t value, hipStream_t s);
 hipError_t launch_fill_i64(int64_t *p, int64_t n, int64_t value, hipStream_t s);
+hipError_t launch_iota_i32(int32_t *p, int32_t n, hipStream_t s);   // p[i] = i
 hipError_t launch_validate(const Graph &g, const int32_t *src, const int32_t *dst,
                            const int64_t *comp, const int64_t *cost, const int64_t *mem,
                            ValidateAcc *acc);
@@ -248,6 +255,23 @@ hipError_t launch_pre_split(const Graph &g, bool fwd, const int32_t *rank, int32
 hipError_t launch_sweep_pair(const SweepArgs &a, hipStream_t s);
 
 // ---- critpath.hip ----
+// tight successors and critical flags of one placement (comp_lm: the node
+// weights to use), then the walk from start_orig (device, INT32_MAX: none) or,
+// when null, from the smallest-id critical node without predecessors
+hipError_t launch_crit_next(const Graph &g, const int32_t *placement, const int64_t *comp_lm,
+                            const int64_t *tl, const int64_t *bl, const int64_t *makespan,
+                            uint8_t *is_critical);
+hipError_t launch_chase_from(const Graph &g, const int32_t *start_orig, int32_t *path,
+                             int32_t *path_len);
+// ---- slicing.hip ----
+hipError_t launch_slice_init(const Graph &g, NodeRec16 *node_rec_s, int64_t *comp_lm_s,
+                             uint8_t *alive_lm, int32_t *primary);
+hipError_t launch_slice_makespan(const Graph &g, const uint8_t *alive_lm, const int64_t *tl,
+                                const int64_t *bl, int64_t *makespan);
+hipError_t launch_slice_start(const Graph &g, const uint8_t *alive_lm, int32_t *start);
+hipError_t launch_slice_remove(const Graph &g, int32_t round, const int32_t *path,
+                               const int32_t *path_len, int64_t big, NodeRec16 *node_rec_s,
+                               int64_t *comp_lm_s, uint8_t *alive_lm, int32_t *primary);
 hipError_t launch_critical_path(const Graph &g, const int32_t *placement, const int64_t *tl,
                                 const int64_t *bl, const int64_t *makespan,
                                 uint8_t *is_critical, int32_t *path, int32_t *path_len);

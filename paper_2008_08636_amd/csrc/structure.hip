@@ -229,6 +229,17 @@ hipError_t launch_fill_i32(int32_t *p, int64_t n, int32_t value, hipStream_t s) 
     return hipGetLastError();
 }
 
+__global__ void k_iota_i32(int32_t *p, int32_t n) {
+    for (int32_t i = blockIdx.x * blockDim.x + threadIdx.x; i < n; i += gridDim.x * blockDim.x)
+        p[i] = i;
+}
+
+hipError_t launch_iota_i32(int32_t *p, int32_t n, hipStream_t s) {
+    if (n <= 0) return hipSuccess;
+    k_iota_i32<<<grid_for(n, kBlock), kBlock, 0, s>>>(p, n);
+    return hipGetLastError();
+}
+
 hipError_t launch_fill_i64(int64_t *p, int64_t n, int64_t value, hipStream_t s) {
     if (n <= 0) return hipSuccess;
     k_fill_i64<<<grid_for(n, kBlock), kBlock, 0, s>>>(p, n, value);

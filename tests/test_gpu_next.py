@@ -157,3 +157,46 @@ def test_memory_balance_refinement_loop_full_size(P):
     check_balance(g.n_nodes, g.mem, kind, tgt, exp_pl[cols].T.copy(), g.n_labels,
                   {k: v[cols] for k, v in host.items()}, range(len(cols)))
     G.close()
+
+
+# ---------------------------------------------------------------------------
+# Graph slicing primaries (Alg. 1): pardnn_slice_primaries
+# ---------------------------------------------------------------------------
+from oracle.slicing import slice_primaries  # noqa: E402
+
+
+def check_slicing(P, g, K):
+    G = P.Graph(g.n_nodes, g.src, g.dst, g.comp, g.edge_cost, g.mem)
+    out = G.slice_primaries(K)
+    torch.cuda.synchronize()
+    got = {k: v.cpu().numpy() for k, v in out.items()}
+    G.close()
+    primary, paths, ms = slice_primaries(g.n_nodes, g.src, g.dst, g.comp, g.edge_cost, K)
+    assert (got["primary"] == primary).all()
+    assert (got["makespan"] == ms).all(), (got["makespan"], ms)
+    for j in range(K):
+        n = int(got["path_len"][j])
+        assert n == len(paths[j]), j
+        assert (got["paths"][j, :n] == paths[j]).all(), j
+
+
+@pytest.mark.parametrize("i,K", [(0, 16), (1, 8), (2, 16)])
+def test_slicing_configs(P, i, K):
+    g = W.make_config(i)
+    say(f"slicing config{i} K={K} V={g.n_nodes}")
+    check_slicing(P, g, K)
+
+
+def test_slicing_small_and_exhausted(P):
+    """Random small DAGs (zero weights and ties included) with K up to past the
+    point where no node remains."""
+    say("slicing small random DAGs")
+    rng = np.random.default_rng(77)
+    for t in range(25):
+        n = int(rng.integers(1, 40))
+        g = W.random_dag(rng, n, p_edge=float(rng.uniform(0.05, 0.5)),
+                         max_weight=int(rng.integers(0, 6)), n_labels=1)
+        check_slicing(P, g, int(rng.integers(1, n + 3)))
+    rng = np.random.default_rng(78)
+    g = W.chain_graph(rng, 50)
+    check_slicing(P, g, 3)

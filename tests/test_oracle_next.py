@@ -121,3 +121,94 @@ def test_transformer_kinds_are_variables_and_their_updates():
     # an optimiser op is a direct successor of the variable it updates
     pairs = set(zip(g.src.tolist(), g.dst.tolist()))
     assert all((int(tgt[v]), int(v)) in pairs for v in refs[:500])
+
+
+# ---------------------------------------------------------------------------
+# Graph slicing primaries (Alg. 1)
+# ---------------------------------------------------------------------------
+from oracle.slicing import slice_primaries  # noqa: E402
+
+
+def _brute_rounds(n, src, dst, comp, cost, K):
+    """Every round by enumerating all source-to-sink paths of the remaining
+    graph: the longest (all edges pay), ties to the smallest node sequence."""
+    alive = set(range(n))
+    out = []
+    for _ in range(K):
+        succ = {v: [] for v in alive}
+        indeg = {v: 0 for v in alive}
+        for e, (a, b) in enumerate(zip(src, dst)):
+            if a in alive and b in alive:
+                succ[a].append((b, cost[e]))
+                indeg[b] += 1
+        best = None
+
+        def walk(v, seq, length):
+            nonlocal best
+            length += comp[v]
+            seq = seq + [v]
+            if not succ[v]:
+                key = (-length, seq)
+                if best is None or key < best:
+                    best = key
+                return
+            for b, c in succ[v]:
+                walk(b, seq, length + c)
+
+        for v in sorted(alive):
+            if indeg[v] == 0:
+                walk(v, [], 0)
+        if best is None:
+            out.append(([], 0))
+            continue
+        out.append((best[1], -best[0]))
+        alive -= set(best[1])
+    return out
+
+
+@pytest.mark.parametrize("seed", range(12))
+def test_slicing_against_path_enumeration(seed):
+    rng = np.random.default_rng(300 + seed)
+    n = int(rng.integers(1, 11))
+    g = W.random_dag(rng, n, p_edge=float(rng.uniform(0.1, 0.6)),
+                     max_weight=int(rng.integers(0, 4)), n_labels=1)
+    K = int(rng.integers(1, n + 2))
+    primary, paths, ms = slice_primaries(g.n_nodes, g.src, g.dst, g.comp, g.edge_cost, K)
+    brute = _brute_rounds(g.n_nodes, g.src.tolist(), g.dst.tolist(), g.comp.tolist(),
+                          g.edge_cost.tolist(), K)
+    for j, (seq, length) in enumerate(brute):
+        assert paths[j].tolist() == seq, (j, paths[j], seq)
+        assert ms[j] == length
+        assert all(primary[v] == j for v in seq)
+
+
+def test_slicing_invariants():
+    g = W.make_config(0)
+    K = 8
+    primary, paths, ms = slice_primaries(g.n_nodes, g.src, g.dst, g.comp, g.edge_cost, K)
+    edges = set(zip(g.src.tolist(), g.dst.tolist()))
+    seen = set()
+    for j, p in enumerate(paths):
+        assert len(p) > 0 and not (set(p.tolist()) & seen)   # disjoint clusters
+        seen |= set(p.tolist())
+        assert all((int(a), int(b)) in edges for a, b in zip(p[:-1], p[1:]))
+        # the path's own length (all edges pay; of parallel edges the
+        # costliest) is the round's makespan
+        cost = {}
+        for x, y, c in zip(g.src.tolist(), g.dst.tolist(), g.edge_cost.tolist()):
+            cost[(x, y)] = max(cost.get((x, y), 0), c)
+        length = int(g.comp[p].sum()) + sum(cost[(int(a), int(b))] for a, b in zip(p[:-1], p[1:]))
+        assert length == ms[j]
+    assert (np.diff(ms) <= 0).all()   # removing nodes never lengthens the longest path
+    assert (primary >= 0).sum() == len(seen)
+
+
+def test_slicing_chain_and_exhaustion():
+    rng = np.random.default_rng(9)
+    g = W.chain_graph(rng, 12)
+    primary, paths, ms = slice_primaries(g.n_nodes, g.src, g.dst, g.comp, g.edge_cost, 3)
+    # a chain is one path: its length is the sum of all weights, then nothing remains
+    assert sorted(paths[0].tolist()) == list(range(12))
+    assert ms[0] == int(g.comp.sum() + g.edge_cost.sum())
+    assert paths[1].size == 0 and paths[2].size == 0 and ms[1] == ms[2] == 0
+    assert (primary == 0).all()
