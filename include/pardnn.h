@@ -279,6 +279,23 @@ int pardnn_memory_balance(pardnn_graph *g, int32_t n_place,
                           int64_t *ref_misplaced);
 
 /*
+ * Cluster criticality of the mapping stage (Sec. 3.1.2): with communication
+ * inside every cluster set to zero (the cluster ids used as labels), the
+ * weighted levels w(n) = tl(n) + bl(n) are recomputed and each cluster gets
+ * the largest w of its nodes, the length of the longest path through it; the
+ * clusters are then ordered by non-increasing criticality.
+ *   cluster        int32[n_nodes], ids in [0, n_clusters).
+ *   criticality    int64[n_clusters] output (-1 for a cluster without nodes).
+ *   order          int32[n_clusters] output: cluster ids by criticality
+ *                  descending, equal criticality by id ascending.
+ * Errors: E_INVAL (null pointers, n_clusters < 1 on a non-empty graph, an id
+ * out of range), E_CYCLE. Syncs.
+ */
+int pardnn_cluster_criticality(pardnn_graph *g, const int32_t *cluster,
+                               int32_t n_clusters, int64_t *criticality,
+                               int32_t *order);
+
+/*
  * The primary clusters of graph slicing (Alg. 1, Sec. 3.1.1): K rounds, each
  * computing the weighted levels of the remaining graph, taking its heaviest
  * path -- a critical path, the canonical one of pardnn_critical_path -- as

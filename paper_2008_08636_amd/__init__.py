@@ -70,6 +70,7 @@ def load_library(path: str = LIB_PATH):
         "pardnn_tb_levels_batch": [P, i32, P, P, P, P],
         "pardnn_memory_balance": [P, i32, P, P, P, i32, P, P, P, P],
         "pardnn_slice_primaries": [P, i32, P, P, i32, P, P],
+        "pardnn_cluster_criticality": [P, P, i32, P, P],
         "pardnn_set_timing": [P, ctypes.c_int],
         "pardnn_get_timing": [P, ctypes.POINTER(ctypes.c_char_p), ctypes.POINTER(ctypes.c_float)],
     }
@@ -247,6 +248,12 @@ def pardnn_slice_primaries(h, K, primary, paths, path_stride, path_len, makespan
         _ptr(path_len, torch.int32), _ptr(makespan, torch.int64)), "pardnn_slice_primaries")
 
 
+def pardnn_cluster_criticality(h, cluster, n_clusters, criticality, order):
+    _check(load_library().pardnn_cluster_criticality(
+        h, _ptr(cluster, torch.int32), n_clusters, _ptr(criticality, torch.int64),
+        _ptr(order, torch.int32)), "pardnn_cluster_criticality")
+
+
 def pardnn_set_timing(h, enable: bool = True):
     _check(load_library().pardnn_set_timing(h, 1 if enable else 0), "pardnn_set_timing")
 
@@ -382,6 +389,14 @@ class Graph:
                               out["res_mem"], out["nor_mem"], out["balanced"],
                               out["ref_misplaced"])
         return out
+
+    def cluster_criticality(self, cluster, n_clusters):
+        """Criticality per cluster and the cluster order (see
+        pardnn_cluster_criticality)."""
+        crit = torch.empty(n_clusters, dtype=torch.int64, device=self.device)
+        order = torch.empty(n_clusters, dtype=torch.int32, device=self.device)
+        pardnn_cluster_criticality(self._h, cluster, n_clusters, crit, order)
+        return crit, order
 
     def slice_primaries(self, K):
         """The K primary clusters of graph slicing (see pardnn_slice_primaries)."""

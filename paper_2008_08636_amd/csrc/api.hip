@@ -57,6 +57,7 @@ void release(Graph *g) {
     for (void *p : g->allocs) (void)hipFree(p);
     g->allocs.clear();
     if (g->batch_ws) (void)hipFree(g->batch_ws);
+    if (g->cl_scratch) (void)hipFree(g->cl_scratch);
     if (g->h_err) (void)hipHostFree(g->h_err);
     if (g->ev0) (void)hipEventDestroy(g->ev0);
     if (g->ev1) (void)hipEventDestroy(g->ev1);
@@ -687,6 +688,61 @@ int pardnn_memory_balance(pardnn_graph *h, int32_t n_place, const int32_t *place
     if (g->h_err[0] & 1) return fail(PARDNN_E_INVAL, "a label lies outside [0, n_labels)");
     if (g->h_err[0] & 2) return fail(PARDNN_E_INVAL, "a node kind is not 0, 1 or 2");
     if (g->h_err[0] & 4) return fail(PARDNN_E_INVAL, "a reference target lies outside [-1, n_nodes)");
+    return PARDNN_OK;
+}
+
+int pardnn_cluster_criticality(pardnn_graph *h, const int32_t *cluster, int32_t n_clusters,
+                               int64_t *criticality, int32_t *order) {
+    CHECK_HANDLE(h);
+    Graph *g = reinterpret_cast<Graph *>(h);
+    if (n_clusters < 0 || (n_clusters == 0 && g->V > 0))
+        return fail(PARDNN_E_INVAL, "n_clusters must be >= 1 (>= 0 for an empty graph)");
+    if (n_clusters == 0) return PARDNN_OK;
+    if (criticality == nullptr || order == nullptr || (g->V > 0 && cluster == nullptr))
+        return fail(PARDNN_E_INVAL, "cluster, criticality and order must be non-null");
+    DEVICE_SCOPE(g);
+    int st = ensure_levelized(g);
+    if (st != PARDNN_OK) return st;
+    const int32_t V = g->V;
+    if (V > 0 && !g->cl_m) {
+        HIP_TRY(dalloc(*g, &g->cl_tl, V));
+        HIP_TRY(dalloc(*g, &g->cl_bl, V));
+        HIP_TRY(dalloc(*g, &g->cl_m, 1));
+    }
+    const size_t need = cluster_sort_bytes(n_clusters);
+    if (g->cl_scratch_bytes < need) {
+        if (g->cl_scratch) {
+            HIP_TRY(hipStreamSynchronize(g->stream));
+            HIP_TRY(hipFree(g->cl_scratch));
+            g->cl_scratch = nullptr;
+            g->cl_scratch_bytes = 0;
+        }
+        HIP_TRY(hipMalloc(&g->cl_scratch, need));
+        g->cl_scratch_bytes = need;
+    }
+    HIP_TRY(launch_fill_i32(g->err, 4, 0, g->stream));
+    if (V > 0) {
+        // weighted levels with the cluster ids as labels: communication inside
+        // a cluster is zero
+        HIP_TRY(launch_permute_labels(*g, cluster, g->lab_lm));
+        SweepArgs a = sweep_args(g);
+        a.P = 1;
+        a.K = 0;
+        a.lab_w = g->lab_lm;
+        a.lab_stride = V;
+        a.ftl = g->ft_lm;
+        a.bll = g->bl_lm;
+        a.ws_stride = V;
+        a.tl_out = g->cl_tl;
+        a.bl_out = g->cl_bl;
+        a.makespan = g->cl_m;
+        HIP_TRY(launch_sweep(a, 1, g->stream));
+    }
+    HIP_TRY(launch_cluster_criticality(*g, cluster, n_clusters, g->cl_tl, g->cl_bl, criticality,
+                                       order, g->cl_scratch, g->cl_scratch_bytes, g->err));
+    st = read_errors(g);
+    if (st != PARDNN_OK) return st;
+    if (g->h_err[0] & 1) return fail(PARDNN_E_INVAL, "a cluster id lies outside [0, n_clusters)");
     return PARDNN_OK;
 }
 

@@ -1,0 +1,79 @@
+// clusters.hip -- cluster criticality of the mapping stage (paper Sec. 3.1.2).
+//
+// After slicing, the criticality of a linear cluster is the length of the
+// longest source-to-sink path through it when communication inside every
+// cluster counts as zero; the clusters are then taken in non-increasing order
+// of criticality. With the cluster ids as labels, the weighted levels w(n) =
+// tl(n) + bl(n) of that evaluation give
+//   criticality(c) = max over the nodes n of cluster c of w(n)   (-1: no node)
+// and the order sorts clusters by (criticality descending, id ascending).
+//
+// Design for gfx950: the weighted levels come from the single-placement
+// sweep; the per-cluster maximum is one pass of 64-bit atomic maxima (cluster
+// ids are arbitrary, up to one per node); the order is a stable device radix
+// sort of (criticality, id) pairs, descending, over ids given ascending.
+#include <rocprim/device/device_radix_sort.hpp>
+
+#include "device_utils.h"
+#include "internal.h"
+
+namespace pardnn {
+
+namespace {
+
+constexpr int kBlock = 256;
+
+inline unsigned grid_for(int64_t n, int block, int cap = 65536) {
+    int64_t g = (n + block - 1) / block;
+    if (g < 1) g = 1;
+    if (g > cap) g = cap;
+    return (unsigned)g;
+}
+
+__global__ void k_cluster_max(int32_t V, int32_t n_clusters, const int32_t *cluster,
+                              const int64_t *tl, const int64_t *bl, long long *crit,
+                              int32_t *err) {
+    for (int32_t v = blockIdx.x * blockDim.x + threadIdx.x; v < V; v += gridDim.x * blockDim.x) {
+        const int32_t c = cluster[v];
+        if ((uint32_t)c >= (uint32_t)n_clusters) {
+            atomicOr(err, 1);
+            continue;
+        }
+        atomicMax(&crit[c], (long long)(tl[v] + bl[v]));
+    }
+}
+
+}  // namespace
+
+// Scratch of the sort: `keys_out` int64[n], `ids` int32[n], then the radix
+// sort's own temporary storage. Returns the bytes needed for n clusters.
+size_t cluster_sort_bytes(int32_t n) {
+    size_t temp = 0;
+    (void)rocprim::radix_sort_pairs_desc(nullptr, temp, (const int64_t *)nullptr,
+                                         (int64_t *)nullptr, (const int32_t *)nullptr,
+                                         (int32_t *)nullptr, n);
+    return (size_t)n * 8 + (size_t)n * 4 + 256 + temp;
+}
+
+hipError_t launch_cluster_criticality(const Graph &g, const int32_t *cluster, int32_t n_clusters,
+                                      const int64_t *tl, const int64_t *bl, int64_t *crit,
+                                      int32_t *order, void *scratch, size_t scratch_bytes,
+                                      int32_t *err) {
+    hipError_t e = launch_fill_i64(crit, n_clusters, -1, g.stream);
+    if (e != hipSuccess) return e;
+    if (g.V > 0) {
+        k_cluster_max<<<grid_for(g.V, kBlock), kBlock, 0, g.stream>>>(
+            g.V, n_clusters, cluster, tl, bl, reinterpret_cast<long long *>(crit), err);
+        if ((e = hipGetLastError()) != hipSuccess) return e;
+    }
+    int64_t *keys_out = reinterpret_cast<int64_t *>(scratch);
+    int32_t *ids = reinterpret_cast<int32_t *>(keys_out + n_clusters);
+    void *temp = reinterpret_cast<char *>(scratch) +
+                 (((size_t)n_clusters * 12 + 255) / 256) * 256;
+    size_t temp_bytes = scratch_bytes - (((size_t)n_clusters * 12 + 255) / 256) * 256;
+    if ((e = launch_iota_i32(ids, n_clusters, g.stream)) != hipSuccess) return e;
+    return rocprim::radix_sort_pairs_desc(temp, temp_bytes, crit, keys_out, ids, order,
+                                          n_clusters, 0u, 64u, g.stream);
+}
+
+}  // namespace pardnn

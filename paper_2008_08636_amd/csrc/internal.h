@@ -190,6 +190,10 @@ struct Graph {
     int64_t *sl_comp = nullptr, *sl_tl = nullptr, *sl_bl = nullptr;
     uint8_t *sl_alive = nullptr, *sl_crit = nullptr;
     int32_t *sl_iota = nullptr, *sl_start = nullptr;
+    // cluster criticality scratch: tl, bl, makespan; the sort (grown on demand)
+    int64_t *cl_tl = nullptr, *cl_bl = nullptr, *cl_m = nullptr;
+    void *cl_scratch = nullptr;
+    size_t cl_scratch_bytes = 0;
     int32_t *err = nullptr;          // device error words [4]
     int32_t *h_err = nullptr;        // pinned host mirror [4]
 
@@ -263,6 +267,14 @@ hipError_t launch_crit_next(const Graph &g, const int32_t *placement, const int6
                             uint8_t *is_critical);
 hipError_t launch_chase_from(const Graph &g, const int32_t *start_orig, int32_t *path,
                              int32_t *path_len);
+// ---- clusters.hip ----
+size_t cluster_sort_bytes(int32_t n);
+// criticality[c] = max over nodes of cluster c of tl + bl (-1: none); order:
+// cluster ids by (criticality desc, id asc); err bit 1: cluster id out of range
+hipError_t launch_cluster_criticality(const Graph &g, const int32_t *cluster, int32_t n_clusters,
+                                      const int64_t *tl, const int64_t *bl, int64_t *crit,
+                                      int32_t *order, void *scratch, size_t scratch_bytes,
+                                      int32_t *err);
 // ---- slicing.hip ----
 hipError_t launch_slice_init(const Graph &g, NodeRec16 *node_rec_s, int64_t *comp_lm_s,
                              uint8_t *alive_lm, int32_t *primary);

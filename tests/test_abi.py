@@ -57,8 +57,10 @@ def test_library_exports_every_declared_symbol(lib):
 def test_library_targets_gfx950_only():
     import paper_2008_08636_amd as P
     blob = open(P.LIB_PATH, "rb").read()
-    assert b"gfx950" in blob
-    assert b"gfx942" not in blob and b"gfx90a" not in blob
+    # the offload bundle names one target per code object; host code may
+    # still hold other architecture names (a library's arch dispatch tables)
+    targets = set(re.findall(rb"amdgcn-amd-amdhsa--(gfx[0-9a-f]+)", blob))
+    assert targets == {b"gfx950"}, targets
 
 
 def test_status_strings(lib):

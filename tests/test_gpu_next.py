@@ -200,3 +200,68 @@ def test_slicing_small_and_exhausted(P):
     rng = np.random.default_rng(78)
     g = W.chain_graph(rng, 50)
     check_slicing(P, g, 3)
+
+
+# ---------------------------------------------------------------------------
+# Cluster criticality (Sec. 3.1.2): pardnn_cluster_criticality
+# ---------------------------------------------------------------------------
+from oracle.clusters import cluster_criticality  # noqa: E402
+
+
+def check_clusters(P, g, cl, C):
+    G = P.Graph(g.n_nodes, g.src, g.dst, g.comp, g.edge_cost, g.mem)
+    crit, order = G.cluster_criticality(dev(cl, torch.int32), C)
+    torch.cuda.synchronize()
+    crit, order = crit.cpu().numpy(), order.cpu().numpy()
+    G.close()
+    ec, eo = cluster_criticality(g.n_nodes, g.src, g.dst, g.comp, g.edge_cost, cl, C)
+    assert (crit == ec).all()
+    assert (order == eo).all()
+
+
+def test_clusters_small_random(P):
+    say("cluster criticality small random DAGs")
+    rng = np.random.default_rng(91)
+    for t in range(20):
+        n = int(rng.integers(1, 60))
+        g = W.random_dag(rng, n, p_edge=float(rng.uniform(0.05, 0.4)),
+                         max_weight=int(rng.integers(0, 6)), n_labels=1)
+        C = int(rng.integers(1, n + 5))
+        check_clusters(P, g, rng.integers(0, C, n).astype(np.int32), C)
+
+
+@pytest.mark.parametrize("i", [0, 1, 2])
+def test_clusters_of_slicing(P, i):
+    """Clusters as the mapping stage sees them: the primaries of 16 slicing
+    rounds, every other node a cluster of its own (tens of thousands of
+    clusters on the transformer graph: several sort tiles)."""
+    g = W.make_config(i)
+    say(f"cluster criticality config{i} V={g.n_nodes}")
+    K = 16
+    G = P.Graph(g.n_nodes, g.src, g.dst, g.comp, g.edge_cost, g.mem)
+    primary = G.slice_primaries(K)["primary"].cpu().numpy()
+    G.close()
+    cl = np.where(primary >= 0, primary, K + np.arange(g.n_nodes)).astype(np.int32)
+    check_clusters(P, g, cl, K + g.n_nodes)
+
+
+def test_clusters_errors(P):
+    say("cluster criticality errors")
+    rng = np.random.default_rng(92)
+    g = W.random_dag(rng, 40, p_edge=0.1, max_weight=5, n_labels=1)
+    G = P.Graph(g.n_nodes, g.src, g.dst, g.comp, g.edge_cost, g.mem)
+    cl = np.zeros(g.n_nodes, np.int32)
+    cl[5] = 3
+    with pytest.raises(P.PardnnError) as e:
+        G.cluster_criticality(dev(cl, torch.int32), 3)
+    assert e.value.status == P.E_INVAL
+    cl[5] = -1
+    with pytest.raises(P.PardnnError) as e:
+        G.cluster_criticality(dev(cl, torch.int32), 3)
+    assert e.value.status == P.E_INVAL
+    with pytest.raises(P.PardnnError) as e:
+        G.cluster_criticality(dev(np.zeros(g.n_nodes, np.int32), torch.int32), 0)
+    assert e.value.status == P.E_INVAL
+    # still usable after an error
+    check_clusters(P, g, np.arange(g.n_nodes, dtype=np.int32) % 7, 7)
+    G.close()

@@ -212,3 +212,86 @@ def test_slicing_chain_and_exhaustion():
     assert ms[0] == int(g.comp.sum() + g.edge_cost.sum())
     assert paths[1].size == 0 and paths[2].size == 0 and ms[1] == ms[2] == 0
     assert (primary == 0).all()
+
+
+# ---------------------------------------------------------------------------
+# Cluster criticality (Sec. 3.1.2)
+# ---------------------------------------------------------------------------
+from oracle.clusters import cluster_criticality  # noqa: E402
+
+
+def _brute_criticality(n, src, dst, comp, cost, cluster, C):
+    """Enumerate every source-to-sink path; an edge inside one cluster is free.
+    Each cluster takes the longest path that visits one of its nodes."""
+    succ = [[] for _ in range(n)]
+    indeg = [0] * n
+    for a, b, c in zip(src, dst, cost):
+        succ[a].append((b, 0 if cluster[a] == cluster[b] else c))
+        indeg[b] += 1
+    crit = [-1] * C
+
+    def walk(v, seen, length):
+        length += comp[v]
+        seen = seen | {cluster[v]}
+        if not succ[v]:
+            for c in seen:
+                crit[c] = max(crit[c], length)
+            return
+        for b, c in succ[v]:
+            walk(b, seen, length + c)
+
+    for v in range(n):
+        if indeg[v] == 0:
+            walk(v, frozenset(), 0)
+    return crit
+
+
+@pytest.mark.parametrize("seed", range(12))
+def test_cluster_criticality_against_path_enumeration(seed):
+    rng = np.random.default_rng(500 + seed)
+    n = int(rng.integers(1, 12))
+    g = W.random_dag(rng, n, p_edge=float(rng.uniform(0.1, 0.6)),
+                     max_weight=int(rng.integers(0, 5)), n_labels=1)
+    C = int(rng.integers(1, n + 3))          # some clusters may stay empty
+    cl = rng.integers(0, C, n)
+    crit, order = cluster_criticality(n, g.src, g.dst, g.comp, g.edge_cost, cl, C)
+    brute = _brute_criticality(n, g.src.tolist(), g.dst.tolist(), g.comp.tolist(),
+                               g.edge_cost.tolist(), cl.tolist(), C)
+    assert crit.tolist() == brute
+    assert order.tolist() == sorted(range(C), key=lambda c: (-brute[c], c))
+
+
+def test_cluster_criticality_special_cases():
+    rng = np.random.default_rng(11)
+    g = W.chain_graph(rng, 10)
+    # one cluster holding a whole chain: all communication is internal, so the
+    # criticality is the sum of the computation weights
+    crit, order = cluster_criticality(10, g.src, g.dst, g.comp, g.edge_cost, np.zeros(10, int), 1)
+    assert crit.tolist() == [int(g.comp.sum())]
+    # every node its own cluster: every node of a chain lies on the one path,
+    # whose length counts every edge
+    crit, _ = cluster_criticality(10, g.src, g.dst, g.comp, g.edge_cost, np.arange(10), 10)
+    assert (crit == int(g.comp.sum() + g.edge_cost.sum())).all()
+    # two isolated nodes, one empty cluster: order by criticality, empty last
+    crit, order = cluster_criticality(2, [], [], [5, 9], [], [2, 0], 3)
+    assert crit.tolist() == [9, -1, 5] and order.tolist() == [0, 2, 1]
+    # ties keep ascending ids
+    crit, order = cluster_criticality(3, [], [], [4, 4, 4], [], [2, 1, 0], 3)
+    assert order.tolist() == [0, 1, 2]
+    with pytest.raises(ValueError):
+        cluster_criticality(2, [], [], [1, 1], [], [0, 2], 2)
+
+
+def test_cluster_criticality_of_slicing_clusters():
+    """The primary clusters of slicing (each a path): a cluster is at least as
+    critical as its own path with the path's edges now free (the sum of its
+    computation weights), and no cluster exceeds the makespan of the whole
+    graph, since making edges free never lengthens a path."""
+    g = W.make_config(0)
+    K = 8
+    primary, paths, ms = slice_primaries(g.n_nodes, g.src, g.dst, g.comp, g.edge_cost, K)
+    cl = np.where(primary >= 0, primary, K + np.arange(g.n_nodes))
+    C = K + g.n_nodes
+    crit, order = cluster_criticality(g.n_nodes, g.src, g.dst, g.comp, g.edge_cost, cl, C)
+    assert crit.max() <= ms[0]
+    assert all(crit[j] >= int(g.comp[paths[j]].sum()) for j in range(K))
