@@ -296,6 +296,35 @@ int pardnn_cluster_criticality(pardnn_graph *g, const int32_t *cluster,
                                int32_t *order);
 
 /*
+ * The terms of level-aware load balancing (Eq. 2, Sec. 3.1.2) for a batch of
+ * clusters against the K partitions of a partial placement, all answered
+ * against the same state (the sequential mapping loop that merges one cluster
+ * at a time stays with the caller).
+ *   label      int32[n_nodes]: partition of each mapped node, -1 unmapped.
+ *   cluster    int32[n_nodes]: cluster id in [0, n_clusters), -1 for none.
+ *   tl         int64[n_nodes]: the top levels the spans are measured in
+ *              (for instance pardnn_tb_levels with cluster ids as labels).
+ * With f the cluster's first node and l its last (smallest and largest
+ * (hop level, id)), span = [lo, hi] with lo = max over parents p of f of
+ * tl(p) + comp(p) (0 without parents) and hi = min over children c of l of
+ * tl(c) (max over all nodes of tl + comp without children) -- Table 2's span.
+ * Outputs (device, caller-allocated):
+ *   span_lo, span_hi int64[n_clusters]  (0 and -1 for a cluster without nodes)
+ *   work  int64[n_clusters][K]: sum of comp over nodes on partition k whose tl
+ *         lies in [lo, hi] (the first sum of Eq. 2)
+ *   comm  int64[n_clusters][K]: sum of edge costs between the cluster and
+ *         nodes on partition k, edges inside one cluster excluded
+ *   choice int32[n_clusters]: argmin over k of work + sum(comm) - comm[k]
+ *         (Eq. 2), ties to the largest comm[k], then the smallest k; -1 for a
+ *         cluster without nodes.
+ * Errors: E_INVAL (K < 1, n_clusters < 0, null pointers, an id out of
+ * range), E_CYCLE. Syncs.
+ */
+int pardnn_span_work(pardnn_graph *g, const int32_t *label, int32_t K, const int32_t *cluster,
+                     int32_t n_clusters, const int64_t *tl, int64_t *span_lo, int64_t *span_hi,
+                     int64_t *work, int64_t *comm, int32_t *choice);
+
+/*
  * The primary clusters of graph slicing (Alg. 1, Sec. 3.1.1): K rounds, each
  * computing the weighted levels of the remaining graph, taking its heaviest
  * path -- a critical path, the canonical one of pardnn_critical_path -- as

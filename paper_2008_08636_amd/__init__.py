@@ -71,6 +71,7 @@ def load_library(path: str = LIB_PATH):
         "pardnn_memory_balance": [P, i32, P, P, P, i32, P, P, P, P],
         "pardnn_slice_primaries": [P, i32, P, P, i32, P, P],
         "pardnn_cluster_criticality": [P, P, i32, P, P],
+        "pardnn_span_work": [P, P, i32, P, i32, P, P, P, P, P, P],
         "pardnn_set_timing": [P, ctypes.c_int],
         "pardnn_get_timing": [P, ctypes.POINTER(ctypes.c_char_p), ctypes.POINTER(ctypes.c_float)],
     }
@@ -254,6 +255,14 @@ def pardnn_cluster_criticality(h, cluster, n_clusters, criticality, order):
         _ptr(order, torch.int32)), "pardnn_cluster_criticality")
 
 
+def pardnn_span_work(h, label, K, cluster, n_clusters, tl, span_lo, span_hi, work, comm, choice):
+    _check(load_library().pardnn_span_work(
+        h, _ptr(label, torch.int32), K, _ptr(cluster, torch.int32), n_clusters,
+        _ptr(tl, torch.int64), _ptr(span_lo, torch.int64), _ptr(span_hi, torch.int64),
+        _ptr(work, torch.int64), _ptr(comm, torch.int64), _ptr(choice, torch.int32)),
+        "pardnn_span_work")
+
+
 def pardnn_set_timing(h, enable: bool = True):
     _check(load_library().pardnn_set_timing(h, 1 if enable else 0), "pardnn_set_timing")
 
@@ -397,6 +406,17 @@ class Graph:
         order = torch.empty(n_clusters, dtype=torch.int32, device=self.device)
         pardnn_cluster_criticality(self._h, cluster, n_clusters, crit, order)
         return crit, order
+
+    def span_work(self, label, K, cluster, n_clusters, tl):
+        """Eq. 2 terms and choices for every cluster (see pardnn_span_work)."""
+        C = n_clusters
+        i64 = dict(dtype=torch.int64, device=self.device)
+        out = {"span_lo": torch.empty(C, **i64), "span_hi": torch.empty(C, **i64),
+               "work": torch.empty((C, K), **i64), "comm": torch.empty((C, K), **i64),
+               "choice": torch.empty(C, dtype=torch.int32, device=self.device)}
+        pardnn_span_work(self._h, label, K, cluster, C, tl, out["span_lo"], out["span_hi"],
+                         out["work"], out["comm"], out["choice"])
+        return out
 
     def slice_primaries(self, K):
         """The K primary clusters of graph slicing (see pardnn_slice_primaries)."""

@@ -57,7 +57,7 @@ void release(Graph *g) {
     for (void *p : g->allocs) (void)hipFree(p);
     g->allocs.clear();
     if (g->batch_ws) (void)hipFree(g->batch_ws);
-    if (g->cl_scratch) (void)hipFree(g->cl_scratch);
+    if (g->aux_scratch) (void)hipFree(g->aux_scratch);
     if (g->h_err) (void)hipHostFree(g->h_err);
     if (g->ev0) (void)hipEventDestroy(g->ev0);
     if (g->ev1) (void)hipEventDestroy(g->ev1);
@@ -691,6 +691,52 @@ int pardnn_memory_balance(pardnn_graph *h, int32_t n_place, const int32_t *place
     return PARDNN_OK;
 }
 
+// Scratch of the cluster and span calls, grown on demand (calls on one handle
+// are ordered on its stream; the old block is freed only after a sync).
+hipError_t grow_aux(Graph *g, size_t need) {
+    if (g->aux_scratch_bytes >= need) return hipSuccess;
+    hipError_t e;
+    if (g->aux_scratch) {
+        if ((e = hipStreamSynchronize(g->stream)) != hipSuccess) return e;
+        if ((e = hipFree(g->aux_scratch)) != hipSuccess) return e;
+        g->aux_scratch = nullptr;
+        g->aux_scratch_bytes = 0;
+    }
+    if ((e = hipMalloc(&g->aux_scratch, need)) != hipSuccess) return e;
+    g->aux_scratch_bytes = need;
+    return hipSuccess;
+}
+
+int pardnn_span_work(pardnn_graph *h, const int32_t *label, int32_t K, const int32_t *cluster,
+                     int32_t n_clusters, const int64_t *tl, int64_t *span_lo, int64_t *span_hi,
+                     int64_t *work, int64_t *comm, int32_t *choice) {
+    CHECK_HANDLE(h);
+    Graph *g = reinterpret_cast<Graph *>(h);
+    if (K < 1) return fail(PARDNN_E_INVAL, "K must be >= 1");
+    if (n_clusters < 0) return fail(PARDNN_E_INVAL, "n_clusters must be >= 0");
+    if (g->V > 0 && (label == nullptr || cluster == nullptr || tl == nullptr))
+        return fail(PARDNN_E_INVAL, "label, cluster and tl must be non-null");
+    if (n_clusters > 0 && (span_lo == nullptr || span_hi == nullptr || work == nullptr ||
+                           comm == nullptr || choice == nullptr))
+        return fail(PARDNN_E_INVAL, "output pointers must be non-null");
+    if (n_clusters == 0 && g->V == 0) return PARDNN_OK;
+    DEVICE_SCOPE(g);
+    int st = ensure_levelized(g);
+    if (st != PARDNN_OK) return st;
+    HIP_TRY(grow_aux(g, span_work_scratch_bytes(g->V, n_clusters, K)));
+    HIP_TRY(launch_fill_i32(g->err, 4, 0, g->stream));
+    {
+        TimedLaunch t(g, "span_work");
+        HIP_TRY(launch_span_work(*g, label, K, cluster, n_clusters, tl, span_lo, span_hi, work,
+                                 comm, choice, g->aux_scratch, g->err));
+    }
+    st = read_errors(g);
+    if (st != PARDNN_OK) return st;
+    if (g->h_err[0] & 1) return fail(PARDNN_E_INVAL, "a cluster id lies outside [-1, n_clusters)");
+    if (g->h_err[0] & 2) return fail(PARDNN_E_INVAL, "a label lies outside [-1, K)");
+    return PARDNN_OK;
+}
+
 int pardnn_cluster_criticality(pardnn_graph *h, const int32_t *cluster, int32_t n_clusters,
                                int64_t *criticality, int32_t *order) {
     CHECK_HANDLE(h);
@@ -709,17 +755,7 @@ int pardnn_cluster_criticality(pardnn_graph *h, const int32_t *cluster, int32_t 
         HIP_TRY(dalloc(*g, &g->cl_bl, V));
         HIP_TRY(dalloc(*g, &g->cl_m, 1));
     }
-    const size_t need = cluster_sort_bytes(n_clusters);
-    if (g->cl_scratch_bytes < need) {
-        if (g->cl_scratch) {
-            HIP_TRY(hipStreamSynchronize(g->stream));
-            HIP_TRY(hipFree(g->cl_scratch));
-            g->cl_scratch = nullptr;
-            g->cl_scratch_bytes = 0;
-        }
-        HIP_TRY(hipMalloc(&g->cl_scratch, need));
-        g->cl_scratch_bytes = need;
-    }
+    HIP_TRY(grow_aux(g, cluster_sort_bytes(n_clusters)));
     HIP_TRY(launch_fill_i32(g->err, 4, 0, g->stream));
     if (V > 0) {
         // weighted levels with the cluster ids as labels: communication inside
@@ -739,7 +775,7 @@ int pardnn_cluster_criticality(pardnn_graph *h, const int32_t *cluster, int32_t 
         HIP_TRY(launch_sweep(a, 1, g->stream));
     }
     HIP_TRY(launch_cluster_criticality(*g, cluster, n_clusters, g->cl_tl, g->cl_bl, criticality,
-                                       order, g->cl_scratch, g->cl_scratch_bytes, g->err));
+                                       order, g->aux_scratch, g->aux_scratch_bytes, g->err));
     st = read_errors(g);
     if (st != PARDNN_OK) return st;
     if (g->h_err[0] & 1) return fail(PARDNN_E_INVAL, "a cluster id lies outside [0, n_clusters)");

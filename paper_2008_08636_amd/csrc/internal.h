@@ -190,10 +190,11 @@ struct Graph {
     int64_t *sl_comp = nullptr, *sl_tl = nullptr, *sl_bl = nullptr;
     uint8_t *sl_alive = nullptr, *sl_crit = nullptr;
     int32_t *sl_iota = nullptr, *sl_start = nullptr;
-    // cluster criticality scratch: tl, bl, makespan; the sort (grown on demand)
+    // cluster criticality scratch: tl, bl, makespan
     int64_t *cl_tl = nullptr, *cl_bl = nullptr, *cl_m = nullptr;
-    void *cl_scratch = nullptr;
-    size_t cl_scratch_bytes = 0;
+    // sort and table scratch of the cluster and span calls (grown on demand)
+    void *aux_scratch = nullptr;
+    size_t aux_scratch_bytes = 0;
     int32_t *err = nullptr;          // device error words [4]
     int32_t *h_err = nullptr;        // pinned host mirror [4]
 
@@ -267,10 +268,19 @@ hipError_t launch_crit_next(const Graph &g, const int32_t *placement, const int6
                             uint8_t *is_critical);
 hipError_t launch_chase_from(const Graph &g, const int32_t *start_orig, int32_t *path,
                              int32_t *path_len);
+// ---- spanwork.hip ----
+// Eq. 2 terms for C clusters against K partitions (see pardnn_span_work);
+// err bit 0: cluster id outside [-1, C), bit 1: label outside [-1, K).
+size_t span_work_scratch_bytes(int32_t V, int32_t C, int32_t K);
+hipError_t launch_span_work(const Graph &g, const int32_t *label, int32_t K,
+                            const int32_t *cluster, int32_t C, const int64_t *tl,
+                            int64_t *span_lo, int64_t *span_hi, int64_t *work, int64_t *comm,
+                            int32_t *choice, void *scratch, int32_t *err);
+
 // ---- clusters.hip ----
 size_t cluster_sort_bytes(int32_t n);
 // criticality[c] = max over nodes of cluster c of tl + bl (-1: none); order:
-// cluster ids by (criticality desc, id asc); err bit 1: cluster id out of range
+// cluster ids by (criticality desc, id asc); err bit 0: cluster id out of range
 hipError_t launch_cluster_criticality(const Graph &g, const int32_t *cluster, int32_t n_clusters,
                                       const int64_t *tl, const int64_t *bl, int64_t *crit,
                                       int32_t *order, void *scratch, size_t scratch_bytes,

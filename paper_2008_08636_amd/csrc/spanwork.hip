@@ -1,0 +1,332 @@
+// spanwork.hip -- the terms of level-aware load balancing (paper Eq. 2, Sec.
+// 3.1.2) for a batch of secondary clusters against the current partitions.
+//
+// For a cluster sc with topologically first node f and last node l, span(sc)
+// runs from the latest finish time tl(p) + comp(p) over the parents p of f
+// (0 without parents) to the earliest start time tl(c) over the children c of
+// l (the makespan max tl + comp without children) -- the span of Table 2.
+// Per cluster and partition k:
+//   work[sc][k] = sum of comp(n) over nodes n on k with lo <= tl(n) <= hi
+//   comm[sc][k] = sum of edge costs between sc and nodes on k (edges inside
+//                 one cluster excluded)
+//   Eq. 2 cost  = work[sc][k] + (sum over k' of comm[sc][k']) - comm[sc][k]
+// and the choice is the partition of least cost, ties to the largest comm,
+// then to the smallest k.
+//
+// Design for gfx950: the paper keeps per-level weights in Fenwick trees so the
+// sequential mapping loop can query one span at a time. Here all queries of a
+// batch run at once, so the table is static: the mapped nodes sorted by
+// (partition, tl) with a prefix sum of their weights, after which one span
+// query is two binary searches in its partition's segment. The sort is two
+// stable device radix sorts (by tl, then by partition); the communication
+// table is one pass of 64-bit atomic adds over the edge list; cluster ends are
+// 64-bit atomic min / max of (level, id) keys.
+#include <rocprim/device/device_radix_sort.hpp>
+#include <rocprim/device/device_scan.hpp>
+
+#include <climits>
+
+#include "device_utils.h"
+#include "internal.h"
+
+namespace pardnn {
+
+namespace {
+
+constexpr int kBlock = 256;
+
+inline unsigned grid_for(int64_t n, int block, int cap = 65536) {
+    int64_t g = (n + block - 1) / block;
+    if (g < 1) g = 1;
+    if (g > cap) g = cap;
+    return (unsigned)g;
+}
+
+inline size_t align256(size_t b) { return (b + 255) / 256 * 256; }
+
+// Scratch layout for V nodes, C clusters, K partitions.
+struct SwLayout {
+    size_t ids0, ids1, tl_tmp, lab_key, lab_sorted, s_tl, pre, seg, first, last, m, temp;
+    size_t temp_bytes, total;
+    SwLayout(int32_t V, int32_t C, int32_t K) {
+        size_t o = 0;
+        auto take = [&](size_t bytes) {
+            size_t at = o;
+            o += align256(bytes);
+            return at;
+        };
+        ids0 = take((size_t)V * 4);
+        ids1 = take((size_t)V * 4);
+        tl_tmp = take((size_t)V * 8);
+        lab_key = take((size_t)V * 4);
+        lab_sorted = take((size_t)V * 4);
+        s_tl = take((size_t)V * 8);
+        pre = take((size_t)(V + 1) * 8);
+        seg = take((size_t)(K + 1) * 4);
+        first = take((size_t)C * 8);
+        last = take((size_t)C * 8);
+        m = take(8);
+        size_t t1 = 0, t2 = 0, t3 = 0;
+        (void)rocprim::radix_sort_pairs(nullptr, t1, (const int64_t *)nullptr, (int64_t *)nullptr,
+                                        (const int32_t *)nullptr, (int32_t *)nullptr, V);
+        (void)rocprim::radix_sort_pairs(nullptr, t2, (const uint32_t *)nullptr,
+                                        (uint32_t *)nullptr, (const int32_t *)nullptr,
+                                        (int32_t *)nullptr, V);
+        (void)rocprim::inclusive_scan(nullptr, t3, (const int64_t *)nullptr, (int64_t *)nullptr,
+                                      (size_t)V, rocprim::plus<int64_t>());
+        temp_bytes = t1 > t2 ? t1 : t2;
+        temp_bytes = temp_bytes > t3 ? temp_bytes : t3;
+        temp = take(temp_bytes);
+        total = o;
+    }
+};
+
+template <class T>
+T *at(void *base, size_t off) {
+    return reinterpret_cast<T *>(reinterpret_cast<char *>(base) + off);
+}
+
+// Per node: validate ids, cluster ends as (level << 32 | id) keys, the makespan
+// max(tl + comp), identity values for the first sort.
+__global__ void k_sw_nodes(int32_t V, int32_t K, int32_t C, const int32_t *label,
+                           const int32_t *cluster, const int32_t *level, const int64_t *tl,
+                           const int64_t *comp, long long *first, long long *last, long long *m,
+                           int32_t *ids, int32_t *err) {
+    long long best = LLONG_MIN;
+    for (int32_t v = blockIdx.x * blockDim.x + threadIdx.x; v < V; v += gridDim.x * blockDim.x) {
+        const int32_t c = cluster[v], k = label[v];
+        if (c < -1 || c >= C) atomicOr(err, 1);
+        if (k < -1 || k >= K) atomicOr(err, 2);
+        if (c >= 0 && c < C) {
+            const long long key = ((long long)level[v] << 32) | (long long)v;
+            atomicMin(&first[c], key);
+            atomicMax(&last[c], key);
+        }
+        const long long f = tl[v] + comp[v];
+        best = f > best ? f : best;
+        ids[v] = v;
+    }
+    best = wave_max_i64(best);
+    if (lane_id() == 0 && best != LLONG_MIN) atomicMax(m, best);
+}
+
+// partition of the i-th node in tl order; unmapped (or invalid) nodes sort last
+__global__ void k_sw_lab_keys(int32_t V, int32_t K, const int32_t *label, const int32_t *ids,
+                              uint32_t *key) {
+    for (int32_t i = blockIdx.x * blockDim.x + threadIdx.x; i < V; i += gridDim.x * blockDim.x) {
+        const int32_t k = label[ids[i]];
+        key[i] = (k >= 0 && k < K) ? (uint32_t)k : (uint32_t)K;
+    }
+}
+
+// nodes in (partition, tl) order: their tl, and their weights into pre[1..V]
+__global__ void k_sw_gather(int32_t V, const int32_t *ids, const int64_t *tl,
+                            const int64_t *comp, int64_t *s_tl, int64_t *w) {
+    for (int32_t i = blockIdx.x * blockDim.x + threadIdx.x; i < V; i += gridDim.x * blockDim.x) {
+        const int32_t v = ids[i];
+        s_tl[i] = tl[v];
+        w[i] = comp[v];
+    }
+}
+
+// seg[k] = first position with partition >= k, k = 0..K
+__global__ void k_sw_seg(int32_t V, int32_t K, const uint32_t *lab_sorted, int32_t *seg) {
+    const int32_t k = blockIdx.x * blockDim.x + threadIdx.x;
+    if (k > K) return;
+    int32_t lo = 0, hi = V;
+    while (lo < hi) {
+        const int32_t mid = (lo + hi) >> 1;
+        if (lab_sorted[mid] < (uint32_t)k)
+            lo = mid + 1;
+        else
+            hi = mid;
+    }
+    seg[k] = lo;
+}
+
+// span(sc): latest parent finish of the first node (0 without parents),
+// earliest child start of the last node (the makespan without children);
+// level-major adjacency, original ids through order / rank
+__global__ void k_sw_bounds(int32_t C, const long long *first, const long long *last,
+                            const int32_t *rank, const int32_t *order, const int32_t *in_off,
+                            const int32_t *in_src, const int32_t *out_off,
+                            const int32_t *out_dst_orig, const int64_t *tl, const int64_t *comp,
+                            const long long *m, int64_t *lo, int64_t *hi) {
+    for (int32_t c = blockIdx.x * blockDim.x + threadIdx.x; c < C; c += gridDim.x * blockDim.x) {
+        const long long fk = first[c];
+        if (fk == LLONG_MAX) {   // no node
+            lo[c] = 0;
+            hi[c] = -1;
+            continue;
+        }
+        const int32_t f = (int32_t)(fk & 0xffffffffLL), l = (int32_t)(last[c] & 0xffffffffLL);
+        const int32_t fl = rank[f], ll = rank[l];
+        int64_t a = 0;
+        if (in_off[fl] < in_off[fl + 1]) {
+            a = LLONG_MIN;
+            for (int32_t j = in_off[fl]; j < in_off[fl + 1]; j++) {
+                const int32_t p = order[in_src[j]];
+                const int64_t t = tl[p] + comp[p];
+                a = t > a ? t : a;
+            }
+        }
+        int64_t b = *m;
+        if (out_off[ll] < out_off[ll + 1]) {
+            b = LLONG_MAX;
+            for (int32_t j = out_off[ll]; j < out_off[ll + 1]; j++) {
+                const int64_t t = tl[out_dst_orig[j]];
+                b = t < b ? t : b;
+            }
+        }
+        lo[c] = a;
+        hi[c] = b;
+    }
+}
+
+// Eq. 2 communication: edges between a cluster and a node on partition k
+__global__ void k_sw_comm(int64_t E, int32_t K, int32_t C, const int32_t *src,
+                          const int32_t *dst, const int64_t *cost, const int32_t *cluster,
+                          const int32_t *label, unsigned long long *comm) {
+    for (int64_t e = blockIdx.x * (int64_t)blockDim.x + threadIdx.x; e < E;
+         e += (int64_t)gridDim.x * blockDim.x) {
+        const int32_t a = src[e], b = dst[e];
+        const int32_t ca = cluster[a], cb = cluster[b];
+        if (ca == cb && ca >= 0) continue;   // inside one cluster
+        const unsigned long long w = (unsigned long long)cost[e];
+        if (w == 0) continue;
+        const int32_t la = label[a], lb = label[b];
+        if (ca >= 0 && ca < C && lb >= 0 && lb < K) atomicAdd(&comm[(int64_t)ca * K + lb], w);
+        if (cb >= 0 && cb < C && la >= 0 && la < K) atomicAdd(&comm[(int64_t)cb * K + la], w);
+    }
+}
+
+// first position in [b, e) with s[i] > x (strict) or >= x
+template <bool STRICT>
+__device__ __forceinline__ int32_t bound(const int64_t *s, int32_t b, int32_t e, int64_t x) {
+    while (b < e) {
+        const int32_t mid = (int32_t)(((uint32_t)b + (uint32_t)e) >> 1);
+        const bool left = STRICT ? (s[mid] <= x) : (s[mid] < x);
+        if (left)
+            b = mid + 1;
+        else
+            e = mid;
+    }
+    return b;
+}
+
+// work[c][k]: partition k's weight with tl inside span(c)
+__global__ void k_sw_work(int32_t C, int32_t K, const int64_t *lo, const int64_t *hi,
+                          const int32_t *seg, const int64_t *s_tl, const int64_t *pre,
+                          int64_t *work) {
+    const int64_t n = (int64_t)C * K;
+    for (int64_t i = blockIdx.x * (int64_t)blockDim.x + threadIdx.x; i < n;
+         i += (int64_t)gridDim.x * blockDim.x) {
+        const int32_t c = (int32_t)(i / K), k = (int32_t)(i - (int64_t)c * K);
+        const int64_t a = lo[c], b = hi[c];
+        int64_t w = 0;
+        if (a <= b) {
+            const int32_t s0 = seg[k], s1 = seg[k + 1];
+            const int32_t x = bound<false>(s_tl, s0, s1, a);
+            const int32_t y = bound<true>(s_tl, x, s1, b);
+            w = pre[y] - pre[x];
+        }
+        work[i] = w;
+    }
+}
+
+__global__ void k_sw_decide(int32_t C, int32_t K, const long long *first, const int64_t *work,
+                            const int64_t *comm, int32_t *choice) {
+    for (int32_t c = blockIdx.x * blockDim.x + threadIdx.x; c < C; c += gridDim.x * blockDim.x) {
+        if (first[c] == LLONG_MAX) {
+            choice[c] = -1;
+            continue;
+        }
+        const int64_t *wr = work + (int64_t)c * K, *cr = comm + (int64_t)c * K;
+        int64_t tot = 0;
+        for (int32_t k = 0; k < K; k++) tot += cr[k];
+        int32_t best = 0;
+        int64_t bc = wr[0] + tot - cr[0], bm = cr[0];
+        for (int32_t k = 1; k < K; k++) {
+            const int64_t cost = wr[k] + tot - cr[k];
+            if (cost < bc || (cost == bc && cr[k] > bm)) {
+                best = k;
+                bc = cost;
+                bm = cr[k];
+            }
+        }
+        choice[c] = best;
+    }
+}
+
+}  // namespace
+
+size_t span_work_scratch_bytes(int32_t V, int32_t C, int32_t K) {
+    return SwLayout(V, C, K).total;
+}
+
+hipError_t launch_span_work(const Graph &g, const int32_t *label, int32_t K,
+                            const int32_t *cluster, int32_t C, const int64_t *tl,
+                            int64_t *span_lo, int64_t *span_hi, int64_t *work, int64_t *comm,
+                            int32_t *choice, void *scratch, int32_t *err) {
+    const int32_t V = g.V;
+    const SwLayout L(V, C, K);
+    hipStream_t s = g.stream;
+    int32_t *ids0 = at<int32_t>(scratch, L.ids0), *ids1 = at<int32_t>(scratch, L.ids1);
+    int64_t *tl_tmp = at<int64_t>(scratch, L.tl_tmp);
+    uint32_t *lab_key = at<uint32_t>(scratch, L.lab_key);
+    uint32_t *lab_sorted = at<uint32_t>(scratch, L.lab_sorted);
+    int64_t *s_tl = at<int64_t>(scratch, L.s_tl), *pre = at<int64_t>(scratch, L.pre);
+    int32_t *seg = at<int32_t>(scratch, L.seg);
+    int64_t *first = at<int64_t>(scratch, L.first), *last = at<int64_t>(scratch, L.last);
+    int64_t *m = at<int64_t>(scratch, L.m);
+    void *temp = at<char>(scratch, L.temp);
+    size_t temp_bytes = L.temp_bytes;
+    hipError_t e;
+
+    if ((e = launch_fill_i64(first, C, LLONG_MAX, s)) != hipSuccess) return e;
+    if ((e = launch_fill_i64(last, C, -1, s)) != hipSuccess) return e;
+    if ((e = launch_fill_i64(m, 1, LLONG_MIN, s)) != hipSuccess) return e;
+    if ((e = launch_fill_i64(pre, 1, 0, s)) != hipSuccess) return e;
+    if ((e = launch_fill_i64(comm, (int64_t)C * K, 0, s)) != hipSuccess) return e;
+    if (V > 0) {
+        k_sw_nodes<<<grid_for(V, kBlock, 2048), kBlock, 0, s>>>(
+            V, K, C, label, cluster, g.level, tl, g.comp, reinterpret_cast<long long *>(first),
+            reinterpret_cast<long long *>(last), reinterpret_cast<long long *>(m), ids0, err);
+        if ((e = hipGetLastError()) != hipSuccess) return e;
+        // nodes by tl, then (stably) by partition
+        if ((e = rocprim::radix_sort_pairs(temp, temp_bytes, tl, tl_tmp, ids0, ids1, V, 0u, 64u,
+                                           s)) != hipSuccess)
+            return e;
+        k_sw_lab_keys<<<grid_for(V, kBlock), kBlock, 0, s>>>(V, K, label, ids1, lab_key);
+        if ((e = hipGetLastError()) != hipSuccess) return e;
+        unsigned bits = 1;
+        while (bits < 32 && ((uint64_t)K >> bits) != 0) bits++;
+        if ((e = rocprim::radix_sort_pairs(temp, temp_bytes, lab_key, lab_sorted, ids1, ids0, V,
+                                           0u, bits, s)) != hipSuccess)
+            return e;
+        k_sw_gather<<<grid_for(V, kBlock), kBlock, 0, s>>>(V, ids0, tl, g.comp, s_tl, tl_tmp);
+        if ((e = hipGetLastError()) != hipSuccess) return e;
+        if ((e = rocprim::inclusive_scan(temp, temp_bytes, (const int64_t *)tl_tmp, pre + 1, (size_t)V,
+                                         rocprim::plus<int64_t>(), s)) != hipSuccess)
+            return e;
+        k_sw_comm<<<grid_for(g.E, kBlock), kBlock, 0, s>>>(
+            g.E, K, C, g.e_src, g.e_dst, g.e_cost, cluster, label,
+            reinterpret_cast<unsigned long long *>(comm));
+        if ((e = hipGetLastError()) != hipSuccess) return e;
+    }
+    k_sw_seg<<<grid_for(K + 1, kBlock), kBlock, 0, s>>>(V, K, lab_sorted, seg);
+    if ((e = hipGetLastError()) != hipSuccess) return e;
+    k_sw_bounds<<<grid_for(C, kBlock), kBlock, 0, s>>>(
+        C, reinterpret_cast<const long long *>(first), reinterpret_cast<const long long *>(last),
+        g.rank, g.order, g.in_off, g.in_src, g.out_off, g.out_dst_orig, tl, g.comp,
+        reinterpret_cast<const long long *>(m), span_lo, span_hi);
+    if ((e = hipGetLastError()) != hipSuccess) return e;
+    k_sw_work<<<grid_for((int64_t)C * K, kBlock), kBlock, 0, s>>>(C, K, span_lo, span_hi, seg,
+                                                                  s_tl, pre, work);
+    if ((e = hipGetLastError()) != hipSuccess) return e;
+    k_sw_decide<<<grid_for(C, kBlock), kBlock, 0, s>>>(
+        C, K, reinterpret_cast<const long long *>(first), work, comm, choice);
+    return hipGetLastError();
+}
+
+}  // namespace pardnn

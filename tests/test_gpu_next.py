@@ -265,3 +265,121 @@ def test_clusters_errors(P):
     # still usable after an error
     check_clusters(P, g, np.arange(g.n_nodes, dtype=np.int32) % 7, 7)
     G.close()
+
+
+# ---------------------------------------------------------------------------
+# Eq. 2 span-work terms (Sec. 3.1.2): pardnn_span_work
+# ---------------------------------------------------------------------------
+from oracle.span_work import span_work  # noqa: E402
+from oracle import tb_levels  # noqa: E402
+
+
+def run_span(G, label, K, cluster, C, tl):
+    out = G.span_work(dev(label, torch.int32), K, dev(cluster, torch.int32), C,
+                      dev(tl, torch.int64))
+    torch.cuda.synchronize()
+    return {k: v.cpu().numpy() for k, v in out.items()}
+
+
+def check_span(got, exp, rows=None):
+    for key in ("span_lo", "span_hi", "work", "comm", "choice"):
+        g = got[key] if rows is None else got[key][rows]
+        assert (g == exp[key]).all(), key
+
+
+def test_span_work_hand_example(P):
+    say("eq2 hand example")
+    d = json.load(open(os.path.join(GOLDEN, "eq2_hand_example.json")))
+    G = P.Graph(d["n_nodes"], np.array(d["src"], np.int32), np.array(d["dst"], np.int32),
+                np.array(d["comp"], np.int64), np.array(d["edge_cost"], np.int64),
+                np.zeros(d["n_nodes"], np.int64))
+    got = run_span(G, d["label"], d["K"], d["cluster"], d["n_clusters"], d["tl"])
+    for key, exp in d["expect"].items():
+        assert got[key].tolist() == exp, key
+    G.close()
+
+
+def test_span_work_small_random(P):
+    """Random DAGs, partial placements and clusters; tl either the graph's top
+    levels or arbitrary values with many duplicates (negative ones included)."""
+    say("eq2 small random")
+    rng = np.random.default_rng(801)
+    for t in range(24):
+        n = int(rng.integers(1, 300))
+        g = W.random_dag(rng, n, p_edge=float(rng.uniform(0.005, 0.1)),
+                         max_weight=int(rng.integers(0, 9)), n_labels=1)
+        K = int(rng.integers(1, 9))
+        C = int(rng.integers(0, n + 4))
+        label = np.where(rng.random(n) < 0.5, rng.integers(0, K, n), -1).astype(np.int32)
+        cluster = (np.where(label < 0, rng.integers(-1, C, n), -1) if C else
+                   np.full(n, -1)).astype(np.int32)
+        if t % 3 == 2:
+            tl = rng.integers(-5, 12, n).astype(np.int64)
+        else:
+            tl = tb_levels(n, g.src, g.dst, g.comp, g.edge_cost, np.arange(n))[0]
+        G = P.Graph(g.n_nodes, g.src, g.dst, g.comp, g.edge_cost, g.mem)
+        got = run_span(G, label, K, cluster, C, tl)
+        G.close()
+        exp = span_work(n, g.src, g.dst, g.comp, g.edge_cost, label, K, cluster, C, tl)
+        check_span(got, exp)
+
+
+@pytest.mark.parametrize("i", [0, 1, 2])
+def test_span_work_mapping_state(P, i):
+    """The mapping stage's state on each graph: the primaries of 16 slicing
+    rounds mapped to 16 partitions, every other node a secondary cluster of
+    its own; tl with every edge paying. All clusters on C0-C1, sampled rows
+    (each computed by the oracle alone) on the transformer graph."""
+    g = W.make_config(i)
+    n = g.n_nodes
+    say(f"eq2 mapping state config{i} V={n}")
+    K = 16
+    G = P.Graph(n, g.src, g.dst, g.comp, g.edge_cost, g.mem)
+    primary = G.slice_primaries(K)["primary"].cpu().numpy()
+    label = primary.astype(np.int32)
+    free = np.nonzero(primary < 0)[0]
+    cluster = np.full(n, -1, np.int32)
+    cluster[free] = np.arange(free.size)
+    C = int(free.size)
+    tl = tb_levels(n, g.src, g.dst, g.comp, g.edge_cost, np.arange(n))[0]
+    got = run_span(G, label, K, cluster, C, tl)
+    G.close()
+    rows = None if n < 50000 else [0, 1, 2, C // 3, C // 2, C - 2, C - 1]
+    exp = span_work(n, g.src, g.dst, g.comp, g.edge_cost, label, K, cluster, C, tl,
+                    clusters=rows)
+    check_span(got, exp, rows)
+    if rows is not None:
+        # every row: the choice minimises Eq. 2 with the tie rules
+        tot = got["comm"].sum(axis=1, keepdims=True)
+        cost = got["work"] + tot - got["comm"]
+        best = cost.min(axis=1)
+        assert (cost[np.arange(C), got["choice"]] == best).all()
+
+
+def test_span_work_errors(P):
+    say("eq2 errors")
+    rng = np.random.default_rng(802)
+    g = W.random_dag(rng, 30, p_edge=0.1, max_weight=5, n_labels=1)
+    G = P.Graph(g.n_nodes, g.src, g.dst, g.comp, g.edge_cost, g.mem)
+    lab = np.zeros(30, np.int32)
+    cl = np.full(30, -1, np.int32)
+    tl = np.zeros(30, np.int64)
+    bad = lab.copy()
+    bad[4] = 2
+    with pytest.raises(P.PardnnError) as e:
+        run_span(G, bad, 2, cl, 3, tl)
+    assert e.value.status == P.E_INVAL
+    bad = cl.copy()
+    bad[4] = 3
+    with pytest.raises(P.PardnnError) as e:
+        run_span(G, lab, 2, bad, 3, tl)
+    assert e.value.status == P.E_INVAL
+    with pytest.raises(P.PardnnError) as e:
+        run_span(G, lab, 0, cl, 3, tl)
+    assert e.value.status == P.E_INVAL
+    # still usable after an error
+    cl2 = (np.arange(30) % 4 - 1).astype(np.int32)
+    lab2 = np.where(cl2 < 0, 1, -1).astype(np.int32)
+    got = run_span(G, lab2, 2, cl2, 3, tl)
+    check_span(got, span_work(30, g.src, g.dst, g.comp, g.edge_cost, lab2, 2, cl2, 3, tl))
+    G.close()

@@ -295,3 +295,120 @@ def test_cluster_criticality_of_slicing_clusters():
     crit, order = cluster_criticality(g.n_nodes, g.src, g.dst, g.comp, g.edge_cost, cl, C)
     assert crit.max() <= ms[0]
     assert all(crit[j] >= int(g.comp[paths[j]].sum()) for j in range(K))
+
+
+# ---------------------------------------------------------------------------
+# Eq. 2 span-work terms (Sec. 3.1.2)
+# ---------------------------------------------------------------------------
+from oracle.span_work import span_work  # noqa: E402
+from oracle import tb_levels  # noqa: E402
+
+
+def test_eq2_hand_example():
+    d = json.load(open(os.path.join(GOLDEN, "eq2_hand_example.json")))
+    n = d["n_nodes"]
+    # the fixture's tl is the top level with every edge paying
+    tl, _, m = tb_levels(n, d["src"], d["dst"], d["comp"], d["edge_cost"], list(range(n)))
+    assert tl.tolist() == d["tl"] and m == 17
+    r = span_work(n, d["src"], d["dst"], d["comp"], d["edge_cost"], d["label"], d["K"],
+                  d["cluster"], d["n_clusters"], d["tl"])
+    for key, exp in d["expect"].items():
+        assert r[key].tolist() == exp, key
+
+
+class Fenwick:
+    """The paper's range-sum structure over per-level weights (binary indexed
+    tree, 1-based), written here as an independent check of the work sums."""
+
+    def __init__(self, n):
+        self.t = [0] * (n + 1)
+
+    def add(self, i, w):
+        i += 1
+        while i < len(self.t):
+            self.t[i] += w
+            i += i & -i
+
+    def prefix(self, i):        # sum of positions [0, i)
+        s = 0
+        while i > 0:
+            s += self.t[i]
+            i -= i & -i
+        return s
+
+
+def _fenwick_work(levels, tl, comp, label, K, lo, hi):
+    import bisect
+    trees = [Fenwick(len(levels)) for _ in range(K)]
+    for v in range(len(tl)):
+        if label[v] >= 0:
+            trees[label[v]].add(levels.index(tl[v]), int(comp[v]))
+    out = []
+    for a, b in zip(lo, hi):
+        i, j = bisect.bisect_left(levels, a), bisect.bisect_right(levels, b)
+        out.append([trees[k].prefix(j) - trees[k].prefix(i) if a <= b else 0 for k in range(K)])
+    return trees, out
+
+
+@pytest.mark.parametrize("seed", range(6))
+def test_eq2_work_matches_fenwick_trees_through_a_mapping_loop(seed):
+    """Level-aware load balancing as the paper runs it: per-partition Fenwick
+    trees over the distinct top levels, one cluster merged at a time into its
+    Eq. 2 choice (the trees updated with its nodes). After every merge the
+    oracle, re-run on the new placement, gives the trees' span sums."""
+    rng = np.random.default_rng(700 + seed)
+    n = int(rng.integers(20, 80))
+    g = W.random_dag(rng, n, p_edge=0.08, max_weight=9, n_labels=1)
+    K = int(rng.integers(2, 5))
+    tl, _, _ = tb_levels(n, g.src, g.dst, g.comp, g.edge_cost, np.arange(n))
+    label = np.where(rng.random(n) < 0.4, rng.integers(0, K, n), -1)
+    C = int(rng.integers(1, 12))
+    cluster = np.where(label < 0, rng.integers(-1, C, n), -1)
+    levels = sorted(set(tl.tolist()))
+    for step in range(C):
+        r = span_work(n, g.src, g.dst, g.comp, g.edge_cost, label, K, cluster, C, tl)
+        _, fw = _fenwick_work(levels, tl.tolist(), g.comp, label, K, r["span_lo"], r["span_hi"])
+        assert r["work"].tolist() == fw, step
+        c = step
+        if r["choice"][c] >= 0:
+            label = np.where(cluster == c, r["choice"][c], label)
+            cluster = np.where(cluster == c, -1, cluster)
+
+
+def test_eq2_invariants():
+    rng = np.random.default_rng(17)
+    g = W.make_config(0)
+    n = g.n_nodes
+    K = 4
+    tl, _, m = tb_levels(n, g.src, g.dst, g.comp, g.edge_cost, np.arange(n))
+    label = np.where(rng.random(n) < 0.5, rng.integers(0, K, n), -1)
+    C = 300
+    cluster = np.where(label < 0, rng.integers(-1, C, n), -1)
+    rows = list(range(0, C, 7))
+    r = span_work(n, g.src, g.dst, g.comp, g.edge_cost, label, K, cluster, C, tl, clusters=rows)
+    total = np.array([g.comp[label == k].sum() for k in range(K)])
+    assert (r["work"] <= total).all() and (r["span_lo"] <= m).all()
+    # a cluster spanning the whole run sees all mapped work
+    whole = (r["span_lo"] == 0) & (r["span_hi"] == m)
+    assert (r["work"][whole] == total).all()
+    # renaming the partitions permutes the columns
+    perm = rng.permutation(K)
+    r2 = span_work(n, g.src, g.dst, g.comp, g.edge_cost, np.where(label >= 0, perm[label], -1), K,
+                   cluster, C, tl, clusters=rows)
+    assert (r2["work"][:, perm] == r["work"]).all() and (r2["comm"][:, perm] == r["comm"]).all()
+    # the choice minimises Eq. 2
+    tot = r["comm"].sum(axis=1, keepdims=True)
+    cost = r["work"] + tot - r["comm"]
+    ok = r["choice"] >= 0
+    assert (cost[ok, r["choice"][ok]] == cost[ok].min(axis=1)).all()
+    # a single partition takes every cluster that has nodes
+    r1 = span_work(n, g.src, g.dst, g.comp, g.edge_cost, np.where(label >= 0, 0, -1), 1,
+                   cluster, C, tl, clusters=rows)
+    assert set(r1["choice"].tolist()) <= {0, -1}
+
+
+def test_eq2_rejects_bad_ids():
+    with pytest.raises(ValueError):
+        span_work(2, [0], [1], [1, 1], [1], [0, 2], 2, [-1, 0], 1, [0, 2])
+    with pytest.raises(ValueError):
+        span_work(2, [0], [1], [1, 1], [1], [0, 1], 2, [-1, 1], 1, [0, 2])
