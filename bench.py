@@ -53,6 +53,30 @@ def algorithmic_bytes_single(V: int, E: int) -> int:
     return 48 * E + 85 * V
 
 
+def algorithmic_bytes_tb_single(V: int, E: int) -> int:
+    """One t+b sweep of one placement without the critical path: 48 B per edge
+    (per direction: neighbour id 4, cost 8, neighbour label 4, value 8) and
+    64 B per node (labels 4 + 4, offsets 4 + 4, comp 8 + 8, tl written 8,
+    tl + comp 8, bl 8, bl written 8)."""
+    return 48 * E + 64 * V
+
+
+def algorithmic_bytes_mem_balance(V: int, P: int, K: int, n_ref: int) -> int:
+    """Memory Heuristic II on P placements: the [V][P] placement matrix (4 B
+    per entry), the target label of each reference node (4 B per placement),
+    per node mem 8, kind 4, target 4; per placement and label 17 B written
+    (two sums, one flag) and 8 B of misplaced count."""
+    return 4 * V * P + 4 * n_ref * P + 16 * V + 17 * P * K + 8 * P
+
+
+def algorithmic_bytes_span_work(V: int, E: int, C: int, K: int) -> int:
+    """Eq. 2 terms for C clusters and K partitions: per node label 4, cluster 4,
+    level 4, tl 8, comp 8; per edge src 4, dst 4, cost 8; per cluster the span
+    (16 B) and choice (4 B) written; per (cluster, partition) work and comm
+    (16 B) written."""
+    return 28 * V + 16 * E + 20 * C + 16 * C * K
+
+
 def source_digest(*names) -> str:
     h = hashlib.sha256()
     for n in names:
@@ -118,6 +142,211 @@ def cpu_baseline(g, sched, budget_s: float):
     }
 
 
+ROWS = ("refinement", "memory_balance", "cluster_criticality", "slicing", "span_work")
+
+
+def time_calls(P, G, fn, steps: int, warmup: int):
+    """Wall time per call (ms) and the mean HIP-event time of the call's timed
+    kernel (ms) over `steps` calls after `warmup` untimed ones."""
+    import numpy as np
+    import torch
+
+    for _ in range(warmup):
+        fn()
+    torch.cuda.synchronize()
+    ks = []
+    t0 = time.perf_counter()
+    for _ in range(steps):
+        fn()
+        ks.append(P.pardnn_get_timing(G.handle)[1])
+    torch.cuda.synchronize()
+    wall = (time.perf_counter() - t0) * 1e3 / steps
+    return wall, float(np.mean(ks)), P.pardnn_get_timing(G.handle)[0]
+
+
+def hbm_roofline(kernel: str, kernel_ms: float, alg_bytes: int, note: str = ""):
+    achieved = alg_bytes / (kernel_ms / 1e3) / 1e9
+    r = {"bound": "hbm", "achieved": round(achieved, 3), "peak": HBM_PEAK_GBS, "unit": "GB/s",
+         "frac": round(achieved / HBM_PEAK_GBS, 5), "traffic": None, "kernel": kernel,
+         "kernel_ms": round(kernel_ms, 4), "algorithmic_bytes_per_launch": alg_bytes}
+    if note:
+        r["note"] = note
+    return r
+
+
+def bench_row(args, row: str) -> int:
+    """One JSON line for a row after the core path, on the transformer graph."""
+    import numpy as np
+    import torch
+
+    import paper_2008_08636_amd as P
+    import workloads as W
+
+    P.load_library()
+    dev = lambda x, dt: torch.as_tensor(np.ascontiguousarray(x), dtype=dt).cuda()
+    g = W.make_config(2)
+    V, E, K = g.n_nodes, g.n_edges, g.n_labels
+    G = P.Graph(V, g.src, g.dst, g.comp, g.edge_cost, g.mem)
+    L = P.pardnn_levelize(G.handle)
+    P.pardnn_set_timing(G.handle, True)
+    graph_desc = f"transformer-shaped training DAG, 48 blocks, V={V}, E={E}, {L} levels"
+    print(f"[bench] row {row}: {graph_desc}", file=sys.stderr, flush=True)
+    budget = args.cpu_budget
+    cpu = None
+    sweep_note = ("a single-placement sweep walks the level chain one level at a time, so "
+                  "its bound is per-level latency, not bandwidth")
+
+    if row == "memory_balance":
+        sched = W.config4_moves(g, n_place=args.n_place)
+        Pn = sched.n_place
+        pl = G.build_placements(dev(sched.base, torch.int32), dev(sched.ptr, torch.int64),
+                                dev(sched.node, torch.int32), dev(sched.label, torch.int32))
+        kind_h, tgt_h = W.node_kinds(g)
+        kind, tgt = dev(kind_h, torch.int32), dev(tgt_h, torch.int32)
+        i64 = dict(dtype=torch.int64, device="cuda")
+        res, nor = torch.empty((Pn, K), **i64), torch.empty((Pn, K), **i64)
+        bal = torch.empty((Pn, K), dtype=torch.uint8, device="cuda")
+        mis = torch.empty(Pn, **i64)
+        fn = lambda: P.pardnn_memory_balance(G.handle, Pn, pl, kind, tgt, K, res, nor, bal, mis)
+        wall, k_ms, kname = time_calls(P, G, fn, args.steps, args.warmup)
+        n_ref = int(((kind_h == 2) & (tgt_h >= 0)).sum())
+        roof = hbm_roofline(kname, k_ms, algorithmic_bytes_mem_balance(V, Pn, K, n_ref))
+        value, unit = Pn / (wall / 1e3), "placements/s"
+        metric = "Memory Heuristic II evaluations/sec (Eq. 6 per partition), 1 MI355X"
+        workload = (f"Eq. 6 balance of {Pn} placements of the refinement loop (1% of ops moved "
+                    f"per placement) on the {graph_desc}, {K} partitions, node kinds from the "
+                    f"graph (variables residual, their optimiser updates reference nodes)")
+        if budget > 0:
+            from oracle.memory_balance import memory_balance
+            pls = W.materialize_placements(sched, 0, min(Pn, 256))
+            t0, n = time.perf_counter(), 0
+            while n < pls.shape[0] and time.perf_counter() - t0 < budget:
+                memory_balance(V, g.mem, kind_h, tgt_h, pls[n], K)
+                n += 1
+            dt = time.perf_counter() - t0
+            cpu = {"value": round(n / dt, 3), "unit": unit, "cores": 1, "kind": "oracle",
+                   "sample": f"first {n} placements of the same loop, {dt:.1f} s on one core "
+                             f"of '{host_cpu_model()}'"}
+    elif row in ("cluster_criticality", "span_work"):
+        n_pri = 16
+        primary = G.slice_primaries(n_pri)["primary"]
+        prim_h = primary.cpu().numpy()
+        free = np.nonzero(prim_h < 0)[0]
+        if row == "cluster_criticality":
+            cl_h = np.where(prim_h >= 0, prim_h, n_pri + np.cumsum(prim_h < 0) - 1)
+            C = n_pri + free.size
+            cl = dev(cl_h, torch.int32)
+            crit = torch.empty(C, dtype=torch.int64, device="cuda")
+            order = torch.empty(C, dtype=torch.int32, device="cuda")
+            fn = lambda: P.pardnn_cluster_criticality(G.handle, cl, C, crit, order)
+            wall, k_ms, kname = time_calls(P, G, fn, args.steps, args.warmup)
+            roof = hbm_roofline(kname, k_ms, algorithmic_bytes_tb_single(V, E), sweep_note)
+            value, unit = C / (wall / 1e3), "clusters/s"
+            metric = "cluster criticality rankings/sec (clusters ranked), 1 MI355X"
+            workload = (f"criticality and order of {C} clusters (the {n_pri} primaries of "
+                        f"slicing, every other node on its own) on the {graph_desc}")
+            if budget > 0:
+                from oracle.clusters import cluster_criticality
+                t0 = time.perf_counter()
+                cluster_criticality(V, g.src, g.dst, g.comp, g.edge_cost, cl_h, C)
+                dt = time.perf_counter() - t0
+                cpu = {"value": round(C / dt, 1), "unit": unit, "cores": 1, "kind": "oracle",
+                       "sample": f"one full call ({C} clusters), {dt:.1f} s on one core of "
+                                 f"'{host_cpu_model()}'"}
+        else:
+            Kp = n_pri
+            cl_h = np.full(V, -1, np.int64)
+            cl_h[free] = np.arange(free.size)
+            C = int(free.size)
+            cl = dev(cl_h, torch.int32)
+            lab = primary
+            iota = torch.arange(V, dtype=torch.int32, device="cuda")
+            tl = torch.empty(V, dtype=torch.int64, device="cuda")
+            bl = torch.empty(V, dtype=torch.int64, device="cuda")
+            m = torch.empty(1, dtype=torch.int64, device="cuda")
+            P.pardnn_tb_levels(G.handle, iota, tl, bl, m)
+            i64 = dict(dtype=torch.int64, device="cuda")
+            lo, hi = torch.empty(C, **i64), torch.empty(C, **i64)
+            work, comm = torch.empty((C, Kp), **i64), torch.empty((C, Kp), **i64)
+            choice = torch.empty(C, dtype=torch.int32, device="cuda")
+            fn = lambda: P.pardnn_span_work(G.handle, lab, Kp, cl, C, tl, lo, hi, work, comm,
+                                            choice)
+            wall, k_ms, kname = time_calls(P, G, fn, args.steps, args.warmup)
+            roof = hbm_roofline(kname, k_ms, algorithmic_bytes_span_work(V, E, C, Kp),
+                                "whole call: node pass, two radix sorts, a scan, spans, "
+                                "communication table, queries, choice")
+            value, unit = C / (wall / 1e3), "clusters/s"
+            metric = "Eq. 2 span-work queries/sec (clusters answered), 1 MI355X"
+            workload = (f"Eq. 2 terms and choice of {C} secondary clusters (every node "
+                        f"outside the {Kp} slicing primaries on its own) against the {Kp} "
+                        f"primaries as partitions, tl with every edge paying, on the "
+                        f"{graph_desc}")
+            if budget > 0:
+                from oracle.span_work import span_work
+                import oracle
+                tl_h = oracle.tb_levels(V, g.src, g.dst, g.comp, g.edge_cost, np.arange(V))[0]
+                lab_h = prim_h
+                span_work(V, g.src, g.dst, g.comp, g.edge_cost, lab_h, Kp, cl_h, C, tl_h,
+                          clusters=[0])
+                t0 = time.perf_counter()
+                span_work(V, g.src, g.dst, g.comp, g.edge_cost, lab_h, Kp, cl_h, C, tl_h,
+                          clusters=[])
+                setup = time.perf_counter() - t0
+                t1 = time.perf_counter()
+                span_work(V, g.src, g.dst, g.comp, g.edge_cost, lab_h, Kp, cl_h, C, tl_h,
+                          clusters=range(0, C, max(1, C // 8))[:8])
+                per = (time.perf_counter() - t1 - setup) / 8
+                n = max(8, min(C, int(max(budget - 2 * setup, 1) / max(per, 1e-6))))
+                rows = np.linspace(0, C - 1, n).astype(np.int64)
+                t0 = time.perf_counter()
+                span_work(V, g.src, g.dst, g.comp, g.edge_cost, lab_h, Kp, cl_h, C, tl_h,
+                          clusters=rows)
+                dt = time.perf_counter() - t0
+                cpu = {"value": round(n / dt, 2), "unit": unit, "cores": 1, "kind": "oracle",
+                       "sample": f"{n} of the {C} clusters, evenly spaced, {dt:.1f} s on one "
+                                 f"core of '{host_cpu_model()}'"}
+    elif row == "slicing":
+        Ks = 16
+        stride = max(L, 1)
+        primary = torch.empty(V, dtype=torch.int32, device="cuda")
+        paths = torch.empty((Ks, stride), dtype=torch.int32, device="cuda")
+        plen = torch.empty(Ks, dtype=torch.int32, device="cuda")
+        ms = torch.empty(Ks, dtype=torch.int64, device="cuda")
+        fn = lambda: P.pardnn_slice_primaries(G.handle, Ks, primary, paths, stride, plen, ms)
+        wall, k_ms, kname = time_calls(P, G, fn, args.steps, args.warmup)
+        roof = hbm_roofline(kname, k_ms, algorithmic_bytes_tb_single(V, E),
+                            sweep_note + "; the timed launch is the last round's sweep")
+        value, unit = Ks / (wall / 1e3), "rounds/s"
+        metric = "graph slicing rounds/sec (Alg. 1 primaries), 1 MI355X"
+        workload = f"{Ks} slicing rounds (Alg. 1 primaries) on the {graph_desc}"
+        if budget > 0:
+            from oracle.slicing import slice_primaries
+            t0 = time.perf_counter()
+            slice_primaries(V, g.src, g.dst, g.comp, g.edge_cost, 1)
+            first = time.perf_counter() - t0
+            n = max(1, min(Ks, int(budget / max(first, 1e-6))))
+            t0 = time.perf_counter()
+            slice_primaries(V, g.src, g.dst, g.comp, g.edge_cost, n)
+            dt = time.perf_counter() - t0
+            cpu = {"value": round(n / dt, 3), "unit": unit, "cores": 1, "kind": "oracle",
+                   "sample": f"the first {n} rounds, {dt:.1f} s on one core of "
+                             f"'{host_cpu_model()}'"}
+    else:
+        raise ValueError(row)
+
+    print(f"[bench] {row}: {wall:.3f} ms/call, {value:.1f} {unit}", file=sys.stderr, flush=True)
+    line = {
+        "metric": metric, "value": round(value, 3), "unit": unit, "n_gpus": 1,
+        "steps": args.steps, "warmup": args.warmup, "ms_per_step": round(wall, 4),
+        "higher_is_better": True, "scaling": "weak", "vs_baseline": None, "dtype": "int64",
+        "data": "synthetic", "config": {"workload": workload, "V": V, "E": E, "levels": L},
+        "roofline": roof, "cpu_baseline": cpu,
+    }
+    print(json.dumps(line), flush=True)
+    G.close()
+    return 0
+
+
 def main() -> int:
     ap = argparse.ArgumentParser(description=__doc__.split("\n")[0])
     ap.add_argument("--gpus", type=int, default=1)
@@ -131,6 +360,9 @@ def main() -> int:
     ap.add_argument("--copy-calibration", action="store_true",
                     help="only run a 1 GiB device copy three times (scale reference for the "
                          "FETCH_SIZE / WRITE_SIZE counters) and exit")
+    ap.add_argument("--row", choices=ROWS, default="refinement",
+                    help="refinement (default): the evaluator's refinement loop; the others "
+                         "measure the rows after it on the same graph")
     args = ap.parse_args()
     if args.gpus != 1:
         print(f"bench.py runs on one GPU only: the evaluator has no multi-GPU path "
@@ -154,6 +386,8 @@ def main() -> int:
         torch.cuda.synchronize()
         print("copied 1 GiB three times", file=sys.stderr, flush=True)
         return 0
+    if args.row != "refinement":
+        return bench_row(args, args.row)
     P.load_library()
     dev = lambda x, dt: torch.as_tensor(np.ascontiguousarray(x), dtype=dt).cuda()
 

@@ -1,7 +1,9 @@
 // api.hip -- the C ABI declared in include/pardnn.h: argument checks, handle
-// and memory management, launch sequencing. Every step of the evaluation runs
-// in the kernels of structure.hip, levelize.hip, sweep.hip, critpath.hip and
-// labelmem.hip; this file only checks, allocates and enqueues.
+// and memory management, launch sequencing. Every step runs in the kernels of
+// structure.hip, levelize.hip, sweep.hip, sweep_pair.hip, critpath.hip,
+// labelmem.hip, heuristics.hip, slicing.hip, clusters.hip and spanwork.hip
+// (and the device sorts and scans they call); this file only checks,
+// allocates and enqueues.
 #include <cstring>
 #include <new>
 #include <string>
@@ -681,8 +683,11 @@ int pardnn_memory_balance(pardnn_graph *h, int32_t n_place, const int32_t *place
         return fail(PARDNN_E_INVAL, "placements, node_type and ref_target must be non-null");
     DEVICE_SCOPE(g);
     HIP_TRY(launch_fill_i32(g->err, 4, 0, g->stream));
-    HIP_TRY(launch_mem_balance(*g, n_place, placements, node_type, ref_target, n_labels, res_mem,
-                               nor_mem, balanced, ref_misplaced, g->err));
+    {
+        TimedLaunch t(g, "mem_balance");
+        HIP_TRY(launch_mem_balance(*g, n_place, placements, node_type, ref_target, n_labels,
+                                   res_mem, nor_mem, balanced, ref_misplaced, g->err));
+    }
     int st = read_errors(g);
     if (st != PARDNN_OK) return st;
     if (g->h_err[0] & 1) return fail(PARDNN_E_INVAL, "a label lies outside [0, n_labels)");
@@ -772,6 +777,7 @@ int pardnn_cluster_criticality(pardnn_graph *h, const int32_t *cluster, int32_t 
         a.tl_out = g->cl_tl;
         a.bl_out = g->cl_bl;
         a.makespan = g->cl_m;
+        TimedLaunch t(g, "k_sweep<1>");
         HIP_TRY(launch_sweep(a, 1, g->stream));
     }
     HIP_TRY(launch_cluster_criticality(*g, cluster, n_clusters, g->cl_tl, g->cl_bl, criticality,
@@ -832,7 +838,10 @@ int pardnn_slice_primaries(pardnn_graph *h, int32_t K, int32_t *primary, int32_t
         a.makespan = makespan + j;
         a.node_rec = g->sl_node_rec;
         a.comp_lm = g->sl_comp;
-        HIP_TRY(launch_sweep(a, 1, g->stream));
+        {
+            TimedLaunch t(g, "k_sweep<1>");
+            HIP_TRY(launch_sweep(a, 1, g->stream));
+        }
         HIP_TRY(launch_slice_makespan(*g, g->sl_alive, g->sl_tl, g->sl_bl, makespan + j));
         HIP_TRY(launch_crit_next(*g, g->sl_iota, g->sl_comp, g->sl_tl, g->sl_bl, makespan + j,
                                  g->sl_crit));

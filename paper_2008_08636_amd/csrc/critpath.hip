@@ -37,31 +37,44 @@ __device__ __forceinline__ int64_t wadd(int64_t a, int64_t b) {
     return (int64_t)((uint64_t)a + (uint64_t)b);
 }
 
-__global__ void k_crit_next(int32_t V, const int32_t *order, const int32_t *out_off,
-                            const int32_t *out_dst, const int32_t *out_dst_orig,
-                            const int64_t *out_cost, const int64_t *comp_lm,
-                            const int32_t *placement, const int64_t *tl, const int64_t *bl,
-                            const int64_t *makespan, uint8_t *is_critical, int32_t *next_lm,
-                            uint8_t *crit_lm) {
+// Critical flags per node; the next-hop slot starts empty.
+__global__ void k_crit_flags(int32_t V, const int32_t *order, const int64_t *tl,
+                             const int64_t *bl, const int64_t *makespan, uint8_t *is_critical,
+                             int32_t *next_lm, uint8_t *crit_lm) {
     const int64_t M = *makespan;
     for (int32_t v = blockIdx.x * blockDim.x + threadIdx.x; v < V; v += gridDim.x * blockDim.x) {
         const int32_t ov = order[v];
-        const int64_t t = tl[ov];
-        const uint8_t crit = wadd(t, bl[ov]) == M;
+        const uint8_t crit = wadd(tl[ov], bl[ov]) == M;
         is_critical[ov] = crit;
         crit_lm[v] = crit;
-        const int32_t lu = placement[ov];
-        const int64_t base = wadd(t, comp_lm[v]);
-        int32_t best_o = INT32_MAX, best = -1;
-        for (int32_t j = out_off[v]; j < out_off[v + 1]; j++) {
-            const int32_t so = out_dst_orig[j];
-            const int64_t c = lu != placement[so] ? out_cost[j] : 0;
-            if (wadd(wadd(base, c), bl[so]) == M && so < best_o) {
-                best_o = so;
-                best = out_dst[j];
-            }
-        }
-        next_lm[v] = best;
+        next_lm[v] = INT32_MAX;
+    }
+}
+
+// One thread per out-edge (level-major): a tight edge out of a critical node
+// offers its successor's original id; the smallest wins. Edge-parallel, so a
+// node with thousands of successors costs no more than as many edges.
+__global__ void k_crit_tight(int64_t E, const int32_t *order, const int32_t *out_src,
+                             const int32_t *out_dst_orig, const int64_t *out_cost,
+                             const int64_t *comp_lm, const int32_t *placement, const int64_t *tl,
+                             const int64_t *bl, const int64_t *makespan, const uint8_t *crit_lm,
+                             int32_t *next_lm) {
+    const int64_t M = *makespan;
+    for (int64_t j = blockIdx.x * (int64_t)blockDim.x + threadIdx.x; j < E;
+         j += (int64_t)gridDim.x * blockDim.x) {
+        const int32_t v = out_src[j];
+        if (!crit_lm[v]) continue;   // a tight edge leaves a critical node only
+        const int32_t ov = order[v], so = out_dst_orig[j];
+        const int64_t c = placement[ov] != placement[so] ? out_cost[j] : 0;
+        if (wadd(wadd(wadd(tl[ov], comp_lm[v]), c), bl[so]) == M) atomicMin(&next_lm[v], so);
+    }
+}
+
+// original id of the chosen successor -> its level-major index (-1: none)
+__global__ void k_crit_link(int32_t V, const int32_t *rank, int32_t *next_lm) {
+    for (int32_t v = blockIdx.x * blockDim.x + threadIdx.x; v < V; v += gridDim.x * blockDim.x) {
+        const int32_t o = next_lm[v];
+        next_lm[v] = o == INT32_MAX ? -1 : rank[o];
     }
 }
 
@@ -121,9 +134,17 @@ hipError_t launch_crit_next(const Graph &g, const int32_t *placement, const int6
                             const int64_t *tl, const int64_t *bl, const int64_t *makespan,
                             uint8_t *is_critical) {
     if (g.V == 0) return hipSuccess;
-    k_crit_next<<<grid_for(g.V, kBlock), kBlock, 0, g.stream>>>(
-        g.V, g.order, g.out_off, g.out_dst, g.out_dst_orig, g.out_cost, comp_lm, placement, tl,
-        bl, makespan, is_critical, g.next_lm, g.crit_lm);
+    k_crit_flags<<<grid_for(g.V, kBlock), kBlock, 0, g.stream>>>(
+        g.V, g.order, tl, bl, makespan, is_critical, g.next_lm, g.crit_lm);
+    hipError_t e = hipGetLastError();
+    if (e != hipSuccess) return e;
+    if (g.E > 0) {
+        k_crit_tight<<<grid_for(g.E, kBlock), kBlock, 0, g.stream>>>(
+            g.E, g.order, g.out_src, g.out_dst_orig, g.out_cost, comp_lm, placement, tl, bl,
+            makespan, g.crit_lm, g.next_lm);
+        if ((e = hipGetLastError()) != hipSuccess) return e;
+    }
+    k_crit_link<<<grid_for(g.V, kBlock), kBlock, 0, g.stream>>>(g.V, g.rank, g.next_lm);
     return hipGetLastError();
 }
 

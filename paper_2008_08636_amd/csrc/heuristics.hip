@@ -15,9 +15,11 @@
 //     another label.
 //
 // Design for gfx950: the placements arrive placement-minor, [V][P], so a
-// wave reads 64 placements of one node as one 256-byte run. A workgroup owns
-// 64 placements and a stripe of nodes, keeps its (placement, label, kind)
-// sums in LDS (ds_add_u64) and flushes them with one global atomic per bin;
+// wave reads 64 placements of one node as one 256-byte run, eight nodes' runs
+// in flight at once. A workgroup owns 64 placements and a stripe of nodes,
+// keeps its (label, kind, placement) sums in LDS (ds_add_u64 on 64
+// consecutive bins per wave, free of bank conflicts) and flushes them with one
+// global atomic per bin;
 // a reference node's wave also reads its target's row (again one run) and
 // counts mismatches per placement. A second pass decides Eq. 6 per
 // (placement, label) with 128-bit integer products.
@@ -31,51 +33,92 @@ namespace pardnn {
 namespace {
 
 constexpr int kCols = 64;          // placements per workgroup
-constexpr int kRows = 4;           // nodes in flight per workgroup step (one per wave)
+constexpr int kRows = 4;           // node rows in flight per workgroup step (one per wave)
+constexpr int kUnroll = 8;         // nodes per wave whose placement loads are issued together
 constexpr int kMbLdsLabels = 32;   // labels kept in LDS bins; more go to global atomics
 
+template <bool LDS>
 __global__ __launch_bounds__(kCols * kRows) void k_mem_balance_sums(
-    int32_t V, int32_t P, int32_t K, const int32_t *placements, const int64_t *mem,
-    const int32_t *node_type, const int32_t *ref_target, int64_t *res_mem, int64_t *nor_mem,
-    int64_t *misplaced, int32_t *err) {
-    __shared__ long long bins[kCols * kMbLdsLabels * 2];   // [col][label][kind]
+    int32_t V, int32_t P, int32_t K, const int32_t *__restrict__ placements,
+    const int64_t *__restrict__ mem, const int32_t *__restrict__ node_type,
+    const int32_t *__restrict__ ref_target, int64_t *__restrict__ res_mem,
+    int64_t *__restrict__ nor_mem, int64_t *__restrict__ misplaced, int32_t *__restrict__ err) {
+    // LDS bins [label][kind][col] plus one trash row for out-of-range labels:
+    // the 64 lanes of a wave (64 placements) add to 64 consecutive 8-byte
+    // bins, so an LDS atomic never conflicts on a bank (dynamic LDS,
+    // (2 K + 1) * kCols entries)
+    extern __shared__ long long bins[];
     __shared__ unsigned long long s_mis[kCols];
-    const int col = threadIdx.x % kCols, row = threadIdx.x / kCols;
+    const int col = threadIdx.x % kCols;
+    const int row = __builtin_amdgcn_readfirstlane(threadIdx.x / kCols);
     const int32_t p = blockIdx.x * kCols + col;
-    const bool lds = K <= kMbLdsLabels;
-    if (lds)
-        for (int i = threadIdx.x; i < kCols * K * 2; i += blockDim.x) bins[i] = 0;
+    if (LDS)
+        for (int i = threadIdx.x; i < (2 * K + 1) * kCols; i += blockDim.x) bins[i] = 0;
     for (int i = threadIdx.x; i < kCols; i += blockDim.x) s_mis[i] = 0;
     __syncthreads();
     int bad = 0;
     unsigned long long mis = 0;
     const int32_t stripe = (V + gridDim.y - 1) / gridDim.y;
     const int32_t v0 = blockIdx.y * stripe, v1 = min(V, v0 + stripe);
+    // one node's contribution to this lane's placement; t, m and tg are the
+    // node's kind, memory and target (wave-uniform), l its label here
+    auto account = [&](int32_t t, int64_t m, int32_t tg, int32_t l) {
+        const bool ok = (uint32_t)l < (uint32_t)K;
+        bad |= ok ? 0 : 1;
+        if (t == 0 || t == 1) {
+            if (LDS) {
+                lds_add_i64(&bins[(ok ? (l * 2 + t) : 2 * K) * kCols + col], m);
+            } else if (ok) {
+                atomicAdd((unsigned long long *)&(t == 1 ? res_mem : nor_mem)[(int64_t)p * K + l],
+                          (unsigned long long)m);
+            }
+        } else if (t == 2) {
+            if (tg >= V || tg < -1)
+                bad |= 4;
+            else if (tg >= 0)
+                mis += placements[(int64_t)tg * P + p] != l;
+        } else {
+            bad |= 2;
+        }
+    };
     if (p < P) {
-        for (int32_t v = v0 + row; v < v1; v += kRows) {
-            const int32_t t = node_type[v];
-            const int32_t l = placements[(int64_t)v * P + p];
-            if ((uint32_t)l >= (uint32_t)K) {
-                bad |= 1;
-                continue;
+        // Node indices are wave-uniform, so node records come through scalar
+        // loads. Software-pipelined: the kUnroll placement runs and records
+        // of the next group are issued before the current group is added up
+        // (indices clamped into the graph, so the look-ahead stays in bounds).
+        struct Group {
+            int32_t t[kUnroll], l[kUnroll], tg[kUnroll];
+            int64_t m[kUnroll];
+        };
+        auto fetch = [&](int32_t v, Group &G) {
+#pragma unroll
+            for (int u = 0; u < kUnroll; u++) {
+                const int32_t vs = __builtin_amdgcn_readfirstlane(min(v + u * kRows, V - 1));
+                G.l[u] = placements[(int64_t)vs * P + p];
+                G.t[u] = node_type[vs];
+                G.m[u] = mem[vs];
+                G.tg[u] = ref_target[vs];
             }
-            if (t == 0 || t == 1) {
-                const int64_t m = mem[v];
-                if (lds)
-                    lds_add_i64(&bins[(col * K + l) * 2 + t], m);
-                else
-                    atomicAdd((unsigned long long *)&(t == 1 ? res_mem : nor_mem)[(int64_t)p * K + l],
-                              (unsigned long long)m);
-            } else if (t == 2) {
-                const int32_t tg = ref_target[v];
-                if (tg >= V || tg < -1) {
-                    bad |= 4;
-                } else if (tg >= 0) {
-                    mis += placements[(int64_t)tg * P + p] != l;
-                }
-            } else {
-                bad |= 2;
+        };
+        int32_t v = v0 + row;
+        if (v + (kUnroll - 1) * kRows < v1) {
+            Group cur, nxt;
+            fetch(v, cur);
+            while (true) {
+                const int32_t vn = v + kUnroll * kRows;
+                fetch(vn, nxt);
+#pragma unroll
+                for (int u = 0; u < kUnroll; u++)
+                    account(__builtin_amdgcn_readfirstlane(cur.t[u]), cur.m[u],
+                            __builtin_amdgcn_readfirstlane(cur.tg[u]), cur.l[u]);
+                v = vn;
+                if (v + (kUnroll - 1) * kRows >= v1) break;
+                cur = nxt;
             }
+        }
+        for (; v < v1; v += kRows) {
+            const int32_t vs = __builtin_amdgcn_readfirstlane(v);
+            account(node_type[vs], mem[vs], ref_target[vs], placements[(int64_t)vs * P + p]);
         }
     }
     if (bad) atomicOr(err, bad);
@@ -83,9 +126,9 @@ __global__ __launch_bounds__(kCols * kRows) void k_mem_balance_sums(
     __syncthreads();
     if (threadIdx.x < kCols && p < P && s_mis[threadIdx.x])
         atomicAdd((unsigned long long *)&misplaced[p], s_mis[threadIdx.x]);
-    if (lds) {
+    if (LDS) {
         for (int i = threadIdx.x; i < kCols * K * 2; i += blockDim.x) {
-            const int c = i / (K * 2), l = (i / 2) % K, kind = i % 2;
+            const int c = i % kCols, kind = (i / kCols) % 2, l = i / (2 * kCols);
             const int32_t pc = blockIdx.x * kCols + c;
             if (pc < P && bins[i] != 0)
                 atomicAdd((unsigned long long *)&(kind == 1 ? res_mem : nor_mem)[(int64_t)pc * K + l],
@@ -166,11 +209,18 @@ hipError_t launch_mem_balance(const Graph &g, int32_t P, const int32_t *placemen
     if (g.V > 0) {
         // enough workgroups to fill the chip: placement tiles x node stripes
         const int32_t tiles = (P + kCols - 1) / kCols;
-        int32_t stripes = (1024 + tiles - 1) / tiles;
+        int32_t stripes = (2048 + tiles - 1) / tiles;
         stripes = std::max(1, std::min(stripes, (g.V + 255) / 256));
-        k_mem_balance_sums<<<dim3((unsigned)tiles, (unsigned)stripes), kCols * kRows, 0,
-                             g.stream>>>(g.V, P, K, placements, g.mem, node_type, ref_target,
-                                         res_mem, nor_mem, misplaced, err);
+        const dim3 grid((unsigned)tiles, (unsigned)stripes);
+        if (K <= kMbLdsLabels)
+            k_mem_balance_sums<true>
+                <<<grid, kCols * kRows, (size_t)(2 * K + 1) * kCols * sizeof(long long),
+                   g.stream>>>(g.V, P, K, placements, g.mem, node_type, ref_target, res_mem,
+                               nor_mem, misplaced, err);
+        else
+            k_mem_balance_sums<false><<<grid, kCols * kRows, 0, g.stream>>>(
+                g.V, P, K, placements, g.mem, node_type, ref_target, res_mem, nor_mem,
+                misplaced, err);
         if ((e = hipGetLastError()) != hipSuccess) return e;
     }
     k_mem_balance_decide<<<(unsigned)((P + 255) / 256), 256, 0, g.stream>>>(P, K, res_mem, nor_mem,

@@ -19,8 +19,9 @@
 // (partition, tl) with a prefix sum of their weights, after which one span
 // query is two binary searches in its partition's segment. The sort is two
 // stable device radix sorts (by tl, then by partition); the communication
-// table is one pass of 64-bit atomic adds over the edge list; cluster ends are
-// 64-bit atomic min / max of (level, id) keys.
+// table and the span ends are passes of 64-bit atomics over the edge list
+// (edge-parallel, so hub nodes with thousands of edges cost no serial loop);
+// cluster ends are 64-bit atomic min / max of (level, id) keys.
 #include <rocprim/device/device_radix_sort.hpp>
 #include <rocprim/device/device_scan.hpp>
 
@@ -145,41 +146,40 @@ __global__ void k_sw_seg(int32_t V, int32_t K, const uint32_t *lab_sorted, int32
 }
 
 // span(sc): latest parent finish of the first node (0 without parents),
-// earliest child start of the last node (the makespan without children);
-// level-major adjacency, original ids through order / rank
-__global__ void k_sw_bounds(int32_t C, const long long *first, const long long *last,
-                            const int32_t *rank, const int32_t *order, const int32_t *in_off,
-                            const int32_t *in_src, const int32_t *out_off,
-                            const int32_t *out_dst_orig, const int64_t *tl, const int64_t *comp,
-                            const long long *m, int64_t *lo, int64_t *hi) {
+// earliest child start of the last node (the makespan without children).
+// Edge-parallel, so a first or last node with thousands of neighbours costs no
+// more than as many edges: init, one pass over the edges, then the defaults.
+__global__ void k_sw_bounds_init(int32_t C, const long long *first, long long *lo,
+                                 long long *hi) {
     for (int32_t c = blockIdx.x * blockDim.x + threadIdx.x; c < C; c += gridDim.x * blockDim.x) {
-        const long long fk = first[c];
-        if (fk == LLONG_MAX) {   // no node
-            lo[c] = 0;
-            hi[c] = -1;
-            continue;
-        }
-        const int32_t f = (int32_t)(fk & 0xffffffffLL), l = (int32_t)(last[c] & 0xffffffffLL);
-        const int32_t fl = rank[f], ll = rank[l];
-        int64_t a = 0;
-        if (in_off[fl] < in_off[fl + 1]) {
-            a = LLONG_MIN;
-            for (int32_t j = in_off[fl]; j < in_off[fl + 1]; j++) {
-                const int32_t p = order[in_src[j]];
-                const int64_t t = tl[p] + comp[p];
-                a = t > a ? t : a;
-            }
-        }
-        int64_t b = *m;
-        if (out_off[ll] < out_off[ll + 1]) {
-            b = LLONG_MAX;
-            for (int32_t j = out_off[ll]; j < out_off[ll + 1]; j++) {
-                const int64_t t = tl[out_dst_orig[j]];
-                b = t < b ? t : b;
-            }
-        }
-        lo[c] = a;
-        hi[c] = b;
+        const bool empty = first[c] == LLONG_MAX;
+        lo[c] = empty ? 0 : LLONG_MIN;
+        hi[c] = empty ? -1 : LLONG_MAX;
+    }
+}
+
+__global__ void k_sw_bounds_edges(int64_t E, int32_t C, const int32_t *src, const int32_t *dst,
+                                  const int32_t *cluster, const int32_t *level,
+                                  const long long *first, const long long *last,
+                                  const int64_t *tl, const int64_t *comp, long long *lo,
+                                  long long *hi) {
+    for (int64_t e = blockIdx.x * (int64_t)blockDim.x + threadIdx.x; e < E;
+         e += (int64_t)gridDim.x * blockDim.x) {
+        const int32_t a = src[e], b = dst[e];
+        const int32_t ca = cluster[a], cb = cluster[b];
+        if (cb >= 0 && cb < C && first[cb] == (((long long)level[b] << 32) | (long long)b))
+            atomicMax(&lo[cb], (long long)(tl[a] + comp[a]));
+        if (ca >= 0 && ca < C && last[ca] == (((long long)level[a] << 32) | (long long)a))
+            atomicMin(&hi[ca], (long long)tl[b]);
+    }
+}
+
+__global__ void k_sw_bounds_fix(int32_t C, const long long *first, const long long *m,
+                                long long *lo, long long *hi) {
+    for (int32_t c = blockIdx.x * blockDim.x + threadIdx.x; c < C; c += gridDim.x * blockDim.x) {
+        if (first[c] == LLONG_MAX) continue;
+        if (lo[c] == LLONG_MIN) lo[c] = 0;
+        if (hi[c] == LLONG_MAX) hi[c] = *m;
     }
 }
 
@@ -316,11 +316,22 @@ hipError_t launch_span_work(const Graph &g, const int32_t *label, int32_t K,
     }
     k_sw_seg<<<grid_for(K + 1, kBlock), kBlock, 0, s>>>(V, K, lab_sorted, seg);
     if ((e = hipGetLastError()) != hipSuccess) return e;
-    k_sw_bounds<<<grid_for(C, kBlock), kBlock, 0, s>>>(
-        C, reinterpret_cast<const long long *>(first), reinterpret_cast<const long long *>(last),
-        g.rank, g.order, g.in_off, g.in_src, g.out_off, g.out_dst_orig, tl, g.comp,
-        reinterpret_cast<const long long *>(m), span_lo, span_hi);
-    if ((e = hipGetLastError()) != hipSuccess) return e;
+    {
+        const long long *fk = reinterpret_cast<const long long *>(first);
+        long long *lo = reinterpret_cast<long long *>(span_lo);
+        long long *hi = reinterpret_cast<long long *>(span_hi);
+        k_sw_bounds_init<<<grid_for(C, kBlock), kBlock, 0, s>>>(C, fk, lo, hi);
+        if ((e = hipGetLastError()) != hipSuccess) return e;
+        if (V > 0 && g.E > 0) {
+            k_sw_bounds_edges<<<grid_for(g.E, kBlock), kBlock, 0, s>>>(
+                g.E, C, g.e_src, g.e_dst, cluster, g.level, fk,
+                reinterpret_cast<const long long *>(last), tl, g.comp, lo, hi);
+            if ((e = hipGetLastError()) != hipSuccess) return e;
+        }
+        k_sw_bounds_fix<<<grid_for(C, kBlock), kBlock, 0, s>>>(
+            C, fk, reinterpret_cast<const long long *>(m), lo, hi);
+        if ((e = hipGetLastError()) != hipSuccess) return e;
+    }
     k_sw_work<<<grid_for((int64_t)C * K, kBlock), kBlock, 0, s>>>(C, K, span_lo, span_hi, seg,
                                                                   s_tl, pre, work);
     if ((e = hipGetLastError()) != hipSuccess) return e;
