@@ -212,6 +212,7 @@ hipError_t launch_mem_balance(const Graph &g, int32_t P, const int32_t *placemen
         int32_t stripes = (2048 + tiles - 1) / tiles;
         stripes = std::max(1, std::min(stripes, (g.V + 255) / 256));
         const dim3 grid((unsigned)tiles, (unsigned)stripes);
+        if (g.timing) (void)hipEventRecord(g.ev0, g.stream);
         if (K <= kMbLdsLabels)
             k_mem_balance_sums<true>
                 <<<grid, kCols * kRows, (size_t)(2 * K + 1) * kCols * sizeof(long long),
@@ -222,6 +223,7 @@ hipError_t launch_mem_balance(const Graph &g, int32_t P, const int32_t *placemen
                 g.V, P, K, placements, g.mem, node_type, ref_target, res_mem, nor_mem,
                 misplaced, err);
         if ((e = hipGetLastError()) != hipSuccess) return e;
+        if (g.timing) (void)hipEventRecord(g.ev1, g.stream);
     }
     k_mem_balance_decide<<<(unsigned)((P + 255) / 256), 256, 0, g.stream>>>(P, K, res_mem, nor_mem,
                                                                           balanced);

@@ -12,9 +12,13 @@
 // trip per level. Each step is edge-parallel: a workgroup scan of the
 // frontier's out-degrees maps every thread to one out-edge, so a single
 // high-fan-out node does not serialise on one lane. An in-degree counter that
-// reaches zero appends its node to the next frontier (an LDS counter), which
-// is then sorted by id in LDS (bitonic), so `order` comes out sorted by
-// (level, id) and `level_ptr` falls out of the frontier sizes.
+// reaches zero appends its node to the next frontier (an LDS counter) and
+// loads its out-edge range into LDS right away, so the next level starts
+// without a dependent global load. `level_ptr` falls out of the frontier
+// sizes; `order` -- ids sorted by (level, id) -- comes from one stable radix
+// sort of the levels afterwards instead of a sort per level.
+#include <rocprim/device/device_radix_sort.hpp>
+
 #include "device_utils.h"
 #include "internal.h"
 
@@ -22,39 +26,8 @@ namespace pardnn {
 
 namespace {
 
-constexpr int KT = 1024;             // threads of the Kahn workgroup
-constexpr int kSortCap = 8192;       // largest frontier sorted in LDS
-
-__device__ __forceinline__ void bitonic_step(int32_t *key, int n, int size, int stride) {
-    for (int i = threadIdx.x; i < n / 2; i += KT) {
-        int lo = (i / stride) * stride * 2 + (i % stride);
-        int hi = lo + stride;
-        bool asc = (lo & size) == 0;
-        int32_t x = key[lo], y = key[hi];
-        if ((x > y) == asc) {
-            key[lo] = y;
-            key[hi] = x;
-        }
-    }
-}
-
-// Sort seg[0..n) ascending. n <= kSortCap: in LDS; otherwise in `scratch`
-// (global, at least next_pow2(n) ints), with the same network.
-__device__ void sort_segment(int32_t *seg, int n, int32_t *lds, int32_t *scratch) {
-    int m = 1;
-    while (m < n) m <<= 1;
-    int32_t *key = m <= kSortCap ? lds : scratch;
-    for (int i = threadIdx.x; i < m; i += KT) key[i] = i < n ? seg[i] : INT32_MAX;
-    __syncthreads();
-    for (int size = 2; size <= m; size <<= 1) {
-        for (int stride = size >> 1; stride > 0; stride >>= 1) {
-            bitonic_step(key, m, size, stride);
-            __syncthreads();
-        }
-    }
-    for (int i = threadIdx.x; i < n; i += KT) seg[i] = key[i];
-    __syncthreads();
-}
+constexpr int KT = 1024;     // threads of the Kahn workgroup
+constexpr int kCap = 2048;   // frontier entries whose out-edge ranges live in LDS
 
 // Largest t in [0, n) with off[t] <= j (off non-decreasing, off[0] == 0).
 __device__ __forceinline__ int owner_of(const int32_t *off, int n, int32_t j) {
@@ -71,10 +44,11 @@ __device__ __forceinline__ int owner_of(const int32_t *off, int n, int32_t j) {
 
 __global__ __launch_bounds__(KT) void k_kahn(int32_t V, const int32_t *o_off,
                                              const int32_t *o_nbr, int32_t *indeg,
-                                             int32_t *order, int32_t *level_ptr,
-                                             int32_t *level, int32_t *sort_scratch,
-                                             int32_t *result) {
-    __shared__ int32_t s_key[kSortCap];
+                                             int32_t *queue, int32_t *level_ptr,
+                                             int32_t *level, int32_t *result) {
+    // out-edge range (start, count) of the first kCap nodes of the current and
+    // the next frontier, loaded when a node is released
+    __shared__ int32_t s_e0[2][kCap], s_deg[2][kCap];
     __shared__ int32_t s_off[KT];
     __shared__ int32_t s_base[KT];
     __shared__ int wsum[KT / kWave + 1];
@@ -89,8 +63,13 @@ __global__ __launch_bounds__(KT) void k_kahn(int32_t V, const int32_t *o_off,
         int total;
         int pos = block_excl_scan_i32(f, wsum, &total);
         if (f) {
-            order[n0 + pos] = v;
+            queue[n0 + pos] = v;
             level[v] = 0;
+            if (n0 + pos < kCap) {
+                const int32_t a = o_off[v];
+                s_e0[0][n0 + pos] = a;
+                s_deg[0][n0 + pos] = o_off[v + 1] - a;
+            }
         }
         n0 += total;
         __syncthreads();
@@ -102,18 +81,24 @@ __global__ __launch_bounds__(KT) void k_kahn(int32_t V, const int32_t *o_off,
         if (tid == 0) level_ptr[1] = n0;
     }
     int32_t head = 0, tail = n0;
+    int cur = 0;
     while (tail > head) {
         if (tid == 0) s_cnt = 0;
         __syncthreads();
         for (int32_t cb = head; cb < tail; cb += KT) {
             const int nf = min(KT, tail - cb);
-            int32_t i = cb + tid;
+            const int32_t idx = cb - head + tid;   // position in the frontier
             int deg = 0;
             int32_t e0 = 0;
             if (tid < nf) {
-                int32_t u = order[i];
-                e0 = o_off[u];
-                deg = o_off[u + 1] - e0;
+                if (idx < kCap) {
+                    e0 = s_e0[cur][idx];
+                    deg = s_deg[cur][idx];
+                } else {
+                    const int32_t u = queue[cb + tid];
+                    e0 = o_off[u];
+                    deg = o_off[u + 1] - e0;
+                }
             }
             int total;
             int ex = block_excl_scan_i32(deg, wsum, &total);
@@ -126,17 +111,22 @@ __global__ __launch_bounds__(KT) void k_kahn(int32_t V, const int32_t *o_off,
                 int32_t old = atomicSub(&indeg[s], 1);
                 if (old == 1) {
                     int32_t p = atomicAdd(&s_cnt, 1);
-                    order[tail + p] = s;
+                    queue[tail + p] = s;
                     level[s] = L;
+                    if (p < kCap) {
+                        const int32_t a = o_off[s];
+                        s_e0[cur ^ 1][p] = a;
+                        s_deg[cur ^ 1][p] = o_off[s + 1] - a;
+                    }
                 }
             }
             __syncthreads();
         }
         const int32_t n_next = s_cnt;
         __syncthreads();
-        if (n_next > 1) sort_segment(order + tail, n_next, s_key, sort_scratch);
         head = tail;
         tail += n_next;
+        cur ^= 1;
         if (n_next > 0) {
             L++;
             if (tid == 0) level_ptr[L] = tail;
@@ -150,12 +140,38 @@ __global__ __launch_bounds__(KT) void k_kahn(int32_t V, const int32_t *o_off,
 
 }  // namespace
 
-// result[0] = number of levels, result[1] = nodes released (< V: cycle).
-hipError_t launch_kahn(const Graph &g, int32_t *indeg_work, int32_t *sort_scratch,
-                       int32_t *result) {
-    k_kahn<<<1, KT, 0, g.stream>>>(g.V, g.o_off, g.o_nbr, indeg_work, g.order, g.level_ptr,
-                                   g.level, sort_scratch, result);
+// result[0] = number of levels, result[1] = nodes released (< V: cycle);
+// `queue` (int32[V]) receives the nodes in release order.
+hipError_t launch_kahn(const Graph &g, int32_t *indeg_work, int32_t *queue, int32_t *result) {
+    k_kahn<<<1, KT, 0, g.stream>>>(g.V, g.o_off, g.o_nbr, indeg_work, queue, g.level_ptr,
+                                   g.level, result);
     return hipGetLastError();
+}
+
+size_t level_order_scratch_bytes(int32_t V) {
+    size_t temp = 0;
+    (void)rocprim::radix_sort_pairs(nullptr, temp, (const uint32_t *)nullptr,
+                                    (uint32_t *)nullptr, (const int32_t *)nullptr,
+                                    (int32_t *)nullptr, V);
+    return ((size_t)V * 8 + 255) / 256 * 256 + temp;
+}
+
+// order = node ids sorted by (level, id): a stable radix sort of the levels
+// (low `bits` bits) over the ids given in ascending order.
+hipError_t launch_level_order(const Graph &g, int32_t bits, void *scratch) {
+    const int32_t V = g.V;
+    if (V == 0) return hipSuccess;
+    const size_t head = ((size_t)V * 8 + 255) / 256 * 256;
+    int32_t *ids = reinterpret_cast<int32_t *>(scratch);
+    uint32_t *keys_out = reinterpret_cast<uint32_t *>(ids + V);
+    void *temp = reinterpret_cast<char *>(scratch) + head;
+    size_t temp_bytes = level_order_scratch_bytes(V) - head;
+    hipError_t e = launch_iota_i32(ids, V, g.stream);
+    if (e != hipSuccess) return e;
+    return rocprim::radix_sort_pairs(temp, temp_bytes,
+                                     reinterpret_cast<const uint32_t *>(g.level), keys_out,
+                                     (const int32_t *)ids, g.order, V, 0u, (unsigned)bits,
+                                     g.stream);
 }
 
 }  // namespace pardnn

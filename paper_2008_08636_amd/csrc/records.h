@@ -1,0 +1,120 @@
+// records.h -- the records and argument block the sweep kernels read:
+// per-level bounds, 16-byte edge and node records, the near / far split of
+// the batched sweeps and the sweep arguments. Kept apart from the host-side
+// declarations so that the kernels' sources change only when these do.
+#pragma once
+
+#include <hip/hip_runtime.h>
+
+#include <cstdint>
+
+namespace pardnn {
+
+struct LevelInfo {
+    int32_t node_lo;   // first lm node of the level
+    int32_t in_e_lo;   // first CSC edge of the level
+    int32_t out_e_lo;  // first CSR edge of the level
+    int32_t pad;
+};
+
+// Level-major edge record of one sweep direction: the neighbour whose value
+// is gathered, the node the candidate is folded into, and the edge cost.
+struct alignas(16) EdgeRec16 {
+    int32_t nb;
+    int32_t own;
+    int64_t cost;
+};
+
+// Batched sweeps: per level and direction, the first node and the first
+// near / far edge record (entries L and L + 1 hold the totals).
+struct alignas(16) PairLevel {
+    int32_t node_lo, near_lo, far_lo, pad;
+};
+// A span-1 edge: owner's and neighbour's index inside their levels
+// (own | nb << 16), the successor tie-break key 2^ob - 1 - successor's
+// original id (b direction; 0 for t) and the cost.
+struct alignas(16) NearRec16 {
+    uint32_t ol;
+    int32_t tie;
+    int64_t cost;
+};
+// A longer edge: the neighbour (level-major id), the owner's index inside its
+// level and the neighbour's entry in the LDS ring of recent levels
+// (own | ring << 16; kNoRing: read the workspace; kPreFolded: folded by the
+// general path of the neighbour's level, which is too wide for the ring) and
+// the cost.
+struct alignas(16) FarRec16 {
+    int32_t nb;
+    uint32_t ol;
+    int64_t cost;
+};
+constexpr uint32_t kNoRing = 0xffffu;
+constexpr uint32_t kPreFolded = 0xfffeu;
+// An edge folded early by the general path of its neighbour's (wide) level:
+// the neighbour, the owner's index in its level and the span (own | span << 16)
+// and the cost; grouped by the neighbour's level (pre_off).
+struct alignas(16) PreRec16 {
+    int32_t nb;
+    uint32_t os;
+    int64_t cost;
+};
+
+// Bits that hold a node id in the b-direction keys: 2^bits > V.
+inline int32_t succ_bits(int32_t V) {
+    int32_t b = 1;
+    while ((1ll << b) <= (int64_t)V) b++;
+    return b;
+}
+
+// Per-node constants of the sweeps, level-major.
+struct alignas(16) NodeRec16 {
+    int64_t comp;
+    int64_t mem;
+};
+
+
+// Sweep kernels: per-label memory bins live in LDS while labels x slots fit
+// kBinsCap; level boundaries are staged in LDS kLevelWindow levels at a time.
+constexpr int kBinsCap = 512;
+constexpr int kLevelWindow = 128;
+// Placements per chain of the batched evaluation (slice of the workspace),
+// and padding nodes per slice of ftl / bll / nx_w.
+constexpr int kBatchSlots = 2;
+constexpr int kSlicePad = 64;
+
+struct SweepArgs {
+    int32_t V, L, P, K;     // nodes, levels, placements, labels (K = 0: no label sums)
+    int64_t E;
+    int32_t lb;             // > 0: {value, label} packed as (value << lb) | label
+    int32_t ob;             // with lb > 0: b keys are (value << ob) | (2^ob - 1 - successor id)
+    const LevelInfo *linfo;
+    const int32_t *in_off, *in_src, *in_dst;
+    const int64_t *in_cost;
+    const int32_t *out_off, *out_src, *out_dst, *out_dst_orig;
+    const int64_t *out_cost;
+    const int64_t *comp_lm, *mem_lm;
+    const EdgeRec16 *in_rec, *out_rec;   // t: {src, dst, cost} by dst; b: {dst, src, cost} by src
+    const NodeRec16 *node_rec;
+    const int32_t *order;   // level-major -> original id
+    const int32_t *level;   // original id -> level
+    const int32_t *level_ptr;  // first level-major node of each level
+    const int32_t *rank;    // original id -> level-major, [V + 1] with rank[V] = -1
+    const int32_t *lab_w;   // [slice][V][S] labels in level-major order
+    int64_t lab_stride;     // elements of lab_w per slice (>= V * S)
+    int64_t *ftl, *bll;     // [slice][V][S] {value, label}: tl + comp, bl (packed or pairs)
+    int32_t *nx_w;          // [slice][V][S] original id of the chosen successor (-1: none), or null
+    int64_t ws_stride;      // elements of ftl / bll / nx_w per slice (>= V * S)
+    const PairLevel *pl_t, *pl_b;         // batched sweeps: near / far split per level
+    const NearRec16 *nr_t, *nr_b;
+    const FarRec16 *fr_t, *fr_b;
+    const int32_t *ftie_b;
+    const int32_t *preoff_t, *preoff_b;   // [L + 1] per neighbour level
+    const PreRec16 *pre_t, *pre_b;
+    const int32_t *pretie_b;
+    int64_t *tl_out, *bl_out, *makespan;  // [V][P], [V][P], [P], caller's numbering
+    int32_t *start;         // [P] level-major id where the critical path starts, or null
+    int64_t *label_mem;     // [P][K], zeroed by the caller, or null
+    int32_t *err;           // device error word
+};
+
+}  // namespace pardnn
