@@ -704,6 +704,84 @@ int pardnn_memory_balance(pardnn_graph *h, int32_t n_place, const int32_t *place
     return PARDNN_OK;
 }
 
+// One placement through the batched pair sweep, for the single-placement
+// passes of slicing and cluster criticality: the pair kernel's per-level chain
+// is shorter than the single sweep's. Its packed keys hold labels below 2^lb
+// (lb <= 16) and values of magnitude up to `bound`; pair_single_bits says
+// whether they fit and sets lb / ob.
+bool pair_single_bits(const Graph *g, int64_t n_labels, int64_t bound, int32_t *lb,
+                      int32_t *ob) {
+    int32_t bits = 1;
+    while ((1ll << bits) < n_labels) bits++;
+    const int32_t obits = succ_bits(g->V);
+    const int32_t wide = std::max(bits, obits);
+    if (bits > 16 || wide >= 62 || bound >= (1ll << (62 - wide))) return false;
+    *lb = bits;
+    *ob = obits;
+    return true;
+}
+
+constexpr int64_t ps_ws_stride(int32_t V) {
+    return (((int64_t)V + kSlicePad) * kBatchSlots + 31) / 32 * 32;
+}
+
+// labels (original ids) into the pair layout, slot 1 idle
+int pair_single_labels(Graph *g, const int32_t *labels) {
+    const int32_t V = g->V;
+    if (!g->ps_ftl) {
+        HIP_TRY(dalloc(*g, &g->ps_ftl, (size_t)ps_ws_stride(V)));
+        HIP_TRY(dalloc(*g, &g->ps_bll, (size_t)ps_ws_stride(V)));
+        HIP_TRY(dalloc(*g, &g->ps_lab, ((size_t)V * kBatchSlots + 63) / 64 * 64));
+    }
+    HIP_TRY(launch_permute_labels_batch(*g, labels, 1, kBatchSlots, g->ps_lab,
+                                        ((int64_t)V * kBatchSlots + 63) / 64 * 64));
+    return PARDNN_OK;
+}
+
+// tl, bl (original order) and the level-0 makespan of the labels set by
+// pair_single_labels, with the given node weights
+int pair_single_sweep(Graph *g, int32_t lb, int32_t ob, NodeRec16 *node_rec, int64_t *comp_lm,
+                      int64_t *tl, int64_t *bl, int64_t *makespan) {
+    int st = ensure_pair(g);
+    if (st != PARDNN_OK) return st;
+    SweepArgs a = sweep_args(g);
+    a.P = 1;
+    a.K = 0;
+    a.lab_w = g->ps_lab;
+    a.lab_stride = ((int64_t)g->V * kBatchSlots + 63) / 64 * 64;
+    a.ftl = g->ps_ftl;
+    a.bll = g->ps_bll;
+    a.ws_stride = ps_ws_stride(g->V);
+    a.nx_w = nullptr;
+    a.start = nullptr;
+    a.label_mem = nullptr;
+    a.tl_out = tl;
+    a.bl_out = bl;
+    a.makespan = makespan;
+    a.node_rec = node_rec;
+    a.comp_lm = comp_lm;
+    a.lb = lb;
+    a.ob = ob;
+    a.pl_t = g->pl_t;
+    a.pl_b = g->pl_b;
+    a.nr_t = g->nr_t;
+    a.nr_b = g->nr_b;
+    a.fr_t = g->fr_t;
+    a.fr_b = g->fr_b;
+    a.ftie_b = g->ftie_b;
+    a.preoff_t = g->preoff_t;
+    a.preoff_b = g->preoff_b;
+    a.pre_t = g->pre_t;
+    a.pre_b = g->pre_b;
+    a.pretie_b = g->pretie_b;
+    {
+        TimedLaunch t(g, "k_sweep_pair<2>");
+        HIP_TRY(launch_sweep_pair(a, g->stream));
+    }
+    HIP_TRY(launch_finish(a, kBatchSlots, nullptr, nullptr, nullptr, 0, nullptr, g->stream));
+    return PARDNN_OK;
+}
+
 // Scratch of the cluster and span calls, grown on demand (calls on one handle
 // are ordered on its stream; the old block is freed only after a sync).
 hipError_t grow_aux(Graph *g, size_t need) {
@@ -770,7 +848,15 @@ int pardnn_cluster_criticality(pardnn_graph *h, const int32_t *cluster, int32_t 
     }
     HIP_TRY(grow_aux(g, cluster_sort_bytes(n_clusters)));
     HIP_TRY(launch_fill_i32(g->err, 4, 0, g->stream));
-    if (V > 0) {
+    int32_t lb = 0, ob = 0;
+    if (V > 0 && pair_single_bits(g, n_clusters, g->weight_bound, &lb, &ob)) {
+        // up to 2^16 clusters: the ids fit the pair sweep's packed keys
+        st = pair_single_labels(g, cluster);
+        if (st == PARDNN_OK)
+            st = pair_single_sweep(g, lb, ob, g->node_rec, g->comp_lm, g->cl_tl, g->cl_bl,
+                                   g->cl_m);
+        if (st != PARDNN_OK) return st;
+    } else if (V > 0) {
         // weighted levels with the cluster ids as labels: communication inside
         // a cluster is zero
         HIP_TRY(launch_permute_labels(*g, cluster, g->lab_lm));
@@ -832,21 +918,34 @@ int pardnn_slice_primaries(pardnn_graph *h, int32_t K, int32_t *primary, int32_t
     // a removed node weighs -B with B above every path length
     const int64_t big = g->weight_bound < INT64_MAX ? g->weight_bound + 1 : INT64_MAX;
     HIP_TRY(launch_slice_init(*g, g->sl_node_rec, g->sl_comp, g->sl_alive, primary));
+    // Every edge joins two levels, so the level as label makes every edge pay,
+    // as distinct labels do: with fewer than 2^16 levels the rounds can take
+    // the pair sweep (values lie in [-B, B]).
+    int32_t lb = 0, ob = 0;
+    const bool pair = K > 0 && big < INT64_MAX && pair_single_bits(g, g->L, big, &lb, &ob);
+    if (pair) {
+        st = pair_single_labels(g, g->level);
+        if (st != PARDNN_OK) return st;
+    }
     for (int32_t j = 0; j < K; j++) {
-        SweepArgs a = sweep_args(g);
-        a.P = 1;
-        a.K = 0;
-        a.lab_w = g->order;   // pairwise distinct labels in level-major order
-        a.lab_stride = V;
-        a.ftl = g->ft_lm;
-        a.bll = g->bl_lm;
-        a.ws_stride = V;
-        a.tl_out = g->sl_tl;
-        a.bl_out = g->sl_bl;
-        a.makespan = makespan + j;
-        a.node_rec = g->sl_node_rec;
-        a.comp_lm = g->sl_comp;
-        {
+        if (pair) {
+            st = pair_single_sweep(g, lb, ob, g->sl_node_rec, g->sl_comp, g->sl_tl, g->sl_bl,
+                                   makespan + j);
+            if (st != PARDNN_OK) return st;
+        } else {
+            SweepArgs a = sweep_args(g);
+            a.P = 1;
+            a.K = 0;
+            a.lab_w = g->order;   // pairwise distinct labels in level-major order
+            a.lab_stride = V;
+            a.ftl = g->ft_lm;
+            a.bll = g->bl_lm;
+            a.ws_stride = V;
+            a.tl_out = g->sl_tl;
+            a.bl_out = g->sl_bl;
+            a.makespan = makespan + j;
+            a.node_rec = g->sl_node_rec;
+            a.comp_lm = g->sl_comp;
             TimedLaunch t(g, "k_sweep<1>");
             HIP_TRY(launch_sweep(a, 1, g->stream));
         }

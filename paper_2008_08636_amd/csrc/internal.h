@@ -85,6 +85,10 @@ struct Graph {
     int64_t *sl_comp = nullptr, *sl_tl = nullptr, *sl_bl = nullptr;
     uint8_t *sl_alive = nullptr, *sl_crit = nullptr;
     int32_t *sl_iota = nullptr, *sl_start = nullptr;
+    // one placement through the batched pair sweep (two slots, one idle):
+    // ftl, bll [V + pad][2] packed, labels [V][2]; allocated on first use
+    int64_t *ps_ftl = nullptr, *ps_bll = nullptr;
+    int32_t *ps_lab = nullptr;
     // cluster criticality scratch: tl, bl, makespan
     int64_t *cl_tl = nullptr, *cl_bl = nullptr, *cl_m = nullptr;
     // sort and table scratch of the cluster and span calls (grown on demand)

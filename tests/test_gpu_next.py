@@ -383,3 +383,12 @@ def test_span_work_errors(P):
     got = run_span(G, lab2, 2, cl2, 3, tl)
     check_span(got, span_work(30, g.src, g.dst, g.comp, g.edge_cost, lab2, 2, cl2, 3, tl))
     G.close()
+
+
+def test_slicing_beyond_packed_levels(P):
+    """More than 2^16 levels: the rounds take the single-placement sweep
+    instead of the pair sweep (labels = levels no longer fit 16 bits)."""
+    rng = np.random.default_rng(79)
+    g = W.chain_graph(rng, 70000)
+    say(f"slicing deep chain V={g.n_nodes}")
+    check_slicing(P, g, 2)
