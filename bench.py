@@ -211,6 +211,7 @@ def bench_row(args, row: str) -> int:
         wall, k_ms, kname = time_calls(P, G, fn, args.steps, args.warmup)
         n_ref = int(((kind_h == 2) & (tgt_h >= 0)).sum())
         roof = hbm_roofline(kname, k_ms, algorithmic_bytes_mem_balance(V, Pn, K, n_ref))
+        roof["traffic"] = load_traffic("k_mem_balance_sums", f"heuristic2_transformer_V{V}_P{Pn}")
         value, unit = Pn / (wall / 1e3), "placements/s"
         metric = "Memory Heuristic II evaluations/sec (Eq. 6 per partition), 1 MI355X"
         workload = (f"Eq. 6 balance of {Pn} placements of the refinement loop (1% of ops moved "

@@ -71,4 +71,15 @@ __device__ __forceinline__ int block_excl_scan_i32(int x, int *wsum, int *total)
     return base + incl - x;
 }
 
+// Workgroup b of n runs on XCD b % 8 (round-robin dispatch); this maps b to a
+// logical index such that the workgroups of one XCD take consecutive logical
+// indices (a bijection on [0, n)), so neighbouring work shares one L2.
+__device__ __forceinline__ int32_t xcd_major(int32_t b, int32_t n) {
+    constexpr int kXcd = 8;
+    const int32_t x = b % kXcd;
+    int32_t start = 0;
+    for (int32_t y = 0; y < x; y++) start += (n - y + kXcd - 1) / kXcd;
+    return start + b / kXcd;
+}
+
 }  // namespace pardnn

@@ -49,17 +49,23 @@ __global__ __launch_bounds__(kCols * kRows) void k_mem_balance_sums(
     // (2 K + 1) * kCols entries)
     extern __shared__ long long bins[];
     __shared__ unsigned long long s_mis[kCols];
+    // logical (tile, stripe): the placement tiles of one node stripe run on
+    // one XCD, so the 128-byte lines that two neighbouring tiles share are
+    // fetched into one L2 only
+    const int32_t tiles = (P + kCols - 1) / kCols;
+    const int32_t lb = xcd_major(blockIdx.x, gridDim.x);
+    const int32_t tile = lb % tiles, stripe_id = lb / tiles, n_stripes = gridDim.x / tiles;
     const int col = threadIdx.x % kCols;
     const int row = __builtin_amdgcn_readfirstlane(threadIdx.x / kCols);
-    const int32_t p = blockIdx.x * kCols + col;
+    const int32_t p = tile * kCols + col;
     if (LDS)
         for (int i = threadIdx.x; i < (2 * K + 1) * kCols; i += blockDim.x) bins[i] = 0;
     for (int i = threadIdx.x; i < kCols; i += blockDim.x) s_mis[i] = 0;
     __syncthreads();
     int bad = 0;
     unsigned long long mis = 0;
-    const int32_t stripe = (V + gridDim.y - 1) / gridDim.y;
-    const int32_t v0 = blockIdx.y * stripe, v1 = min(V, v0 + stripe);
+    const int32_t stripe = (V + n_stripes - 1) / n_stripes;
+    const int32_t v0 = stripe_id * stripe, v1 = min(V, v0 + stripe);
     // one node's contribution to this lane's placement; t, m and tg are the
     // node's kind, memory and target (wave-uniform), l its label here
     auto account = [&](int32_t t, int64_t m, int32_t tg, int32_t l) {
@@ -129,7 +135,7 @@ __global__ __launch_bounds__(kCols * kRows) void k_mem_balance_sums(
     if (LDS) {
         for (int i = threadIdx.x; i < kCols * K * 2; i += blockDim.x) {
             const int c = i % kCols, kind = (i / kCols) % 2, l = i / (2 * kCols);
-            const int32_t pc = blockIdx.x * kCols + c;
+            const int32_t pc = tile * kCols + c;
             if (pc < P && bins[i] != 0)
                 atomicAdd((unsigned long long *)&(kind == 1 ? res_mem : nor_mem)[(int64_t)pc * K + l],
                           (unsigned long long)bins[i]);
@@ -211,7 +217,7 @@ hipError_t launch_mem_balance(const Graph &g, int32_t P, const int32_t *placemen
         const int32_t tiles = (P + kCols - 1) / kCols;
         int32_t stripes = (2048 + tiles - 1) / tiles;
         stripes = std::max(1, std::min(stripes, (g.V + 255) / 256));
-        const dim3 grid((unsigned)tiles, (unsigned)stripes);
+        const unsigned grid = (unsigned)tiles * (unsigned)stripes;   // tile-minor, see xcd_major
         if (g.timing) (void)hipEventRecord(g.ev0, g.stream);
         if (K <= kMbLdsLabels)
             k_mem_balance_sums<true>

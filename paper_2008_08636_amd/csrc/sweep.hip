@@ -778,16 +778,6 @@ __global__ __launch_bounds__(256) void k_chase(SweepArgs a, const uint32_t *cbit
     if (p < a.P) chase_wave<S>(a, cbits, p, path, stride, path_len);
 }
 
-// Workgroup b runs on XCD b % 8 (round-robin dispatch); give the workgroups of
-// one XCD consecutive node groups.
-__device__ __forceinline__ int32_t xcd_major(int32_t b, int32_t n) {
-    constexpr int kXcd = 8;
-    const int32_t x = b % kXcd;
-    int32_t start = 0;
-    for (int32_t y = 0; y < x; y++) start += (n - y + kXcd - 1) / kXcd;
-    return start + b / kXcd;
-}
-
 template <int S, bool PACKED>
 __global__ __launch_bounds__(256) void k_emit(SweepArgs a, uint8_t *crit, uint32_t *cbits) {
     __shared__ __align__(16) char smem[emit_lds<kEmitNodes, kEmitCols>()];
