@@ -130,7 +130,11 @@ int pardnn_levelize(pardnn_graph *g, int32_t *level, int32_t *order,
  *                  so cluster ids work as labels (Sec. 3.1.2 criticality).
  *   tl, bl         int64[n_nodes] outputs.
  *   makespan       int64[1] output.
- * Levelizes first if needed (E_CYCLE). No sync.
+ * Levelizes first if needed (E_CYCLE). The first single or batched
+ * evaluation on a handle also builds the per-graph edge split of the batched
+ * sweep and syncs once; later calls do not sync. Labels all in [0, 2^16) take
+ * the batched sweep with one placement (decided on the device), others the
+ * single-placement sweep; the results are the same.
  */
 int pardnn_tb_levels(pardnn_graph *g, const int32_t *placement, int64_t *tl,
                      int64_t *bl, int64_t *makespan);

@@ -459,6 +459,91 @@ int evaluate_impl(Graph *g, int32_t n_place, const int32_t *placements, const Mo
 }
 
 
+// One placement through the batched pair sweep, for the single-placement
+// passes of slicing and cluster criticality: the pair kernel's per-level chain
+// is shorter than the single sweep's. Its packed keys hold labels below 2^lb
+// (lb <= 16) and values of magnitude up to `bound`; pair_single_bits says
+// whether they fit and sets lb / ob.
+bool pair_single_bits(const Graph *g, int64_t n_labels, int64_t bound, int32_t *lb,
+                      int32_t *ob) {
+    int32_t bits = 1;
+    while ((1ll << bits) < n_labels) bits++;
+    const int32_t obits = succ_bits(g->V);
+    const int32_t wide = std::max(bits, obits);
+    if (bits > 16 || wide >= 62 || bound >= (1ll << (62 - wide))) return false;
+    *lb = bits;
+    *ob = obits;
+    return true;
+}
+
+constexpr int64_t ps_ws_stride(int32_t V) {
+    return (((int64_t)V + kSlicePad) * kBatchSlots + 31) / 32 * 32;
+}
+
+// labels (original ids) into the pair layout, slot 1 idle
+int pair_single_labels(Graph *g, const int32_t *labels) {
+    const int32_t V = g->V;
+    if (!g->ps_ftl) {
+        HIP_TRY(dalloc(*g, &g->ps_ftl, (size_t)ps_ws_stride(V)));
+        HIP_TRY(dalloc(*g, &g->ps_bll, (size_t)ps_ws_stride(V)));
+        HIP_TRY(dalloc(*g, &g->ps_lab, ((size_t)V * kBatchSlots + 63) / 64 * 64));
+        HIP_TRY(dalloc(*g, &g->ps_gate, 1));
+    }
+    HIP_TRY(launch_permute_labels_batch(*g, labels, 1, kBatchSlots, g->ps_lab,
+                                        ((int64_t)V * kBatchSlots + 63) / 64 * 64));
+    return PARDNN_OK;
+}
+
+// tl, bl (original order) and the level-0 makespan of the labels set by
+// pair_single_labels, with the given node weights; with `gate`, the launches
+// run only if *gate == 1
+int pair_single_sweep(Graph *g, int32_t lb, int32_t ob, NodeRec16 *node_rec, int64_t *comp_lm,
+                      int64_t *tl, int64_t *bl, int64_t *makespan, const int32_t *gate = nullptr,
+                      bool timed = true) {
+    int st = ensure_pair(g);
+    if (st != PARDNN_OK) return st;
+    SweepArgs a = sweep_args(g);
+    a.P = 1;
+    a.K = 0;
+    a.lab_w = g->ps_lab;
+    a.lab_stride = ((int64_t)g->V * kBatchSlots + 63) / 64 * 64;
+    a.ftl = g->ps_ftl;
+    a.bll = g->ps_bll;
+    a.ws_stride = ps_ws_stride(g->V);
+    a.nx_w = nullptr;
+    a.start = nullptr;
+    a.label_mem = nullptr;
+    a.tl_out = tl;
+    a.bl_out = bl;
+    a.makespan = makespan;
+    a.node_rec = node_rec;
+    a.comp_lm = comp_lm;
+    a.lb = lb;
+    a.ob = ob;
+    a.pl_t = g->pl_t;
+    a.pl_b = g->pl_b;
+    a.nr_t = g->nr_t;
+    a.nr_b = g->nr_b;
+    a.fr_t = g->fr_t;
+    a.fr_b = g->fr_b;
+    a.ftie_b = g->ftie_b;
+    a.preoff_t = g->preoff_t;
+    a.preoff_b = g->preoff_b;
+    a.pre_t = g->pre_t;
+    a.pre_b = g->pre_b;
+    a.pretie_b = g->pretie_b;
+    a.gate = gate;
+    a.gate_want = 1;
+    if (timed) {
+        TimedLaunch t(g, "k_sweep_pair<2>");
+        HIP_TRY(launch_sweep_pair(a, g->stream));
+    } else {
+        HIP_TRY(launch_sweep_pair(a, g->stream));
+    }
+    HIP_TRY(launch_finish(a, kBatchSlots, nullptr, nullptr, nullptr, 0, nullptr, g->stream));
+    return PARDNN_OK;
+}
+
 }  // namespace
 
 int pardnn::fail(int status, const std::string &msg) {
@@ -622,6 +707,16 @@ int pardnn_tb_levels(pardnn_graph *h, const int32_t *placement, int64_t *tl, int
     DEVICE_SCOPE(g);
     int st = ensure_levelized(g);
     if (st != PARDNN_OK) return st;
+    // Labels below 2^16 fit the pair sweep's packed keys. Whether they do is
+    // decided on the device: both paths are enqueued and the one that does
+    // not apply returns at once, so the call stays asynchronous.
+    int32_t lb = 0, ob = 0;
+    const bool pair = g->V > 0 && pair_single_bits(g, 1 << 16, g->weight_bound, &lb, &ob);
+    if (pair) {
+        st = ensure_pair(g);
+        if (st == PARDNN_OK) st = pair_single_labels(g, placement);
+        if (st != PARDNN_OK) return st;
+    }
     HIP_TRY(launch_permute_labels(*g, placement, g->lab_lm));
     SweepArgs a = sweep_args(g);
     a.P = 1;
@@ -634,10 +729,16 @@ int pardnn_tb_levels(pardnn_graph *h, const int32_t *placement, int64_t *tl, int
     a.tl_out = tl;
     a.bl_out = bl;
     a.makespan = makespan;
-    {
-        TimedLaunch t(g, "k_sweep<1>");
-        HIP_TRY(launch_sweep(a, 1, g->stream));
+    TimedLaunch t(g, pair ? "k_sweep_pair<2> or k_sweep<1>" : "k_sweep<1>");
+    if (pair) {
+        HIP_TRY(launch_label_fit(*g, placement, 1 << 16, g->ps_gate));
+        st = pair_single_sweep(g, lb, ob, g->node_rec, g->comp_lm, tl, bl, makespan, g->ps_gate,
+                               false);
+        if (st != PARDNN_OK) return st;
+        a.gate = g->ps_gate;
+        a.gate_want = 0;
     }
+    HIP_TRY(launch_sweep(a, 1, g->stream));
     return PARDNN_OK;
 }
 
@@ -701,84 +802,6 @@ int pardnn_memory_balance(pardnn_graph *h, int32_t n_place, const int32_t *place
     if (g->h_err[0] & 1) return fail(PARDNN_E_INVAL, "a label lies outside [0, n_labels)");
     if (g->h_err[0] & 2) return fail(PARDNN_E_INVAL, "a node kind is not 0, 1 or 2");
     if (g->h_err[0] & 4) return fail(PARDNN_E_INVAL, "a reference target lies outside [-1, n_nodes)");
-    return PARDNN_OK;
-}
-
-// One placement through the batched pair sweep, for the single-placement
-// passes of slicing and cluster criticality: the pair kernel's per-level chain
-// is shorter than the single sweep's. Its packed keys hold labels below 2^lb
-// (lb <= 16) and values of magnitude up to `bound`; pair_single_bits says
-// whether they fit and sets lb / ob.
-bool pair_single_bits(const Graph *g, int64_t n_labels, int64_t bound, int32_t *lb,
-                      int32_t *ob) {
-    int32_t bits = 1;
-    while ((1ll << bits) < n_labels) bits++;
-    const int32_t obits = succ_bits(g->V);
-    const int32_t wide = std::max(bits, obits);
-    if (bits > 16 || wide >= 62 || bound >= (1ll << (62 - wide))) return false;
-    *lb = bits;
-    *ob = obits;
-    return true;
-}
-
-constexpr int64_t ps_ws_stride(int32_t V) {
-    return (((int64_t)V + kSlicePad) * kBatchSlots + 31) / 32 * 32;
-}
-
-// labels (original ids) into the pair layout, slot 1 idle
-int pair_single_labels(Graph *g, const int32_t *labels) {
-    const int32_t V = g->V;
-    if (!g->ps_ftl) {
-        HIP_TRY(dalloc(*g, &g->ps_ftl, (size_t)ps_ws_stride(V)));
-        HIP_TRY(dalloc(*g, &g->ps_bll, (size_t)ps_ws_stride(V)));
-        HIP_TRY(dalloc(*g, &g->ps_lab, ((size_t)V * kBatchSlots + 63) / 64 * 64));
-    }
-    HIP_TRY(launch_permute_labels_batch(*g, labels, 1, kBatchSlots, g->ps_lab,
-                                        ((int64_t)V * kBatchSlots + 63) / 64 * 64));
-    return PARDNN_OK;
-}
-
-// tl, bl (original order) and the level-0 makespan of the labels set by
-// pair_single_labels, with the given node weights
-int pair_single_sweep(Graph *g, int32_t lb, int32_t ob, NodeRec16 *node_rec, int64_t *comp_lm,
-                      int64_t *tl, int64_t *bl, int64_t *makespan) {
-    int st = ensure_pair(g);
-    if (st != PARDNN_OK) return st;
-    SweepArgs a = sweep_args(g);
-    a.P = 1;
-    a.K = 0;
-    a.lab_w = g->ps_lab;
-    a.lab_stride = ((int64_t)g->V * kBatchSlots + 63) / 64 * 64;
-    a.ftl = g->ps_ftl;
-    a.bll = g->ps_bll;
-    a.ws_stride = ps_ws_stride(g->V);
-    a.nx_w = nullptr;
-    a.start = nullptr;
-    a.label_mem = nullptr;
-    a.tl_out = tl;
-    a.bl_out = bl;
-    a.makespan = makespan;
-    a.node_rec = node_rec;
-    a.comp_lm = comp_lm;
-    a.lb = lb;
-    a.ob = ob;
-    a.pl_t = g->pl_t;
-    a.pl_b = g->pl_b;
-    a.nr_t = g->nr_t;
-    a.nr_b = g->nr_b;
-    a.fr_t = g->fr_t;
-    a.fr_b = g->fr_b;
-    a.ftie_b = g->ftie_b;
-    a.preoff_t = g->preoff_t;
-    a.preoff_b = g->preoff_b;
-    a.pre_t = g->pre_t;
-    a.pre_b = g->pre_b;
-    a.pretie_b = g->pretie_b;
-    {
-        TimedLaunch t(g, "k_sweep_pair<2>");
-        HIP_TRY(launch_sweep_pair(a, g->stream));
-    }
-    HIP_TRY(launch_finish(a, kBatchSlots, nullptr, nullptr, nullptr, 0, nullptr, g->stream));
     return PARDNN_OK;
 }
 

@@ -88,7 +88,7 @@ struct Graph {
     // one placement through the batched pair sweep (two slots, one idle):
     // ftl, bll [V + pad][2] packed, labels [V][2]; allocated on first use
     int64_t *ps_ftl = nullptr, *ps_bll = nullptr;
-    int32_t *ps_lab = nullptr;
+    int32_t *ps_lab = nullptr, *ps_gate = nullptr;
     // cluster criticality scratch: tl, bl, makespan
     int64_t *cl_tl = nullptr, *cl_bl = nullptr, *cl_m = nullptr;
     // sort and table scratch of the cluster and span calls (grown on demand)
@@ -141,6 +141,8 @@ hipError_t launch_permute_labels(const Graph &g, const int32_t *placement, int32
 hipError_t launch_permute_labels_batch(const Graph &g, const int32_t *placements, int32_t P,
                                        int32_t S, int32_t *lab_w, int64_t lab_stride,
                                        int32_t K = 0, int32_t *err = nullptr);
+// flag = 1 if every label lies in [0, limit), else 0 (on the device)
+hipError_t launch_label_fit(const Graph &g, const int32_t *labels, int32_t limit, int32_t *flag);
 hipError_t launch_sweep(const SweepArgs &a, int32_t S, hipStream_t s);
 // cbits: [P][ceil(V / 32)] bit words of the critical flags, scratch for the
 // path walk (needed when path is given)

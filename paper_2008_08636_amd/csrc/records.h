@@ -115,6 +115,10 @@ struct SweepArgs {
     int32_t *start;         // [P] level-major id where the critical path starts, or null
     int64_t *label_mem;     // [P][K], zeroed by the caller, or null
     int32_t *err;           // device error word
+    // set: the launch runs only if *gate == gate_want (two alternative paths
+    // enqueued together, chosen on the device without a host round trip)
+    const int32_t *gate;
+    int32_t gate_want;
 };
 
 }  // namespace pardnn

@@ -498,6 +498,7 @@ __device__ void sweep_dir(const SweepArgs &a, int32_t slice, char *smem) {
 template <int S, int T, int ACC, bool PACKED>
 __global__ __launch_bounds__(T) void k_sweep(SweepArgs a) {
     extern __shared__ __align__(16) char smem[];
+    if (a.gate != nullptr && *a.gate != a.gate_want) return;
     const int32_t n_slices = (a.P + S - 1) / S;
     if ((int32_t)blockIdx.x < n_slices)
         sweep_dir<S, T, ACC, false, PACKED>(a, blockIdx.x, smem);
@@ -781,6 +782,7 @@ __global__ __launch_bounds__(256) void k_chase(SweepArgs a, const uint32_t *cbit
 template <int S, bool PACKED>
 __global__ __launch_bounds__(256) void k_emit(SweepArgs a, uint8_t *crit, uint32_t *cbits) {
     __shared__ __align__(16) char smem[emit_lds<kEmitNodes, kEmitCols>()];
+    if (a.gate != nullptr && *a.gate != a.gate_want) return;
     emit_rows<S, PACKED, kEmitNodes, kEmitCols>(a, crit, cbits, xcd_major(blockIdx.x, gridDim.x),
                                                 smem);
 }
@@ -809,6 +811,25 @@ hipError_t launch_permute_labels_batch(const Graph &g, const int32_t *placements
                                                                   lab_w, lab_stride, K, err);
     else
         return hipErrorInvalidValue;
+    return hipGetLastError();
+}
+
+namespace {
+
+// flag = 0 if some label lies outside [0, limit) (flag set to 1 beforehand)
+__global__ void k_label_fit(int32_t V, const int32_t *lab, int32_t limit, int32_t *flag) {
+    for (int32_t v = blockIdx.x * blockDim.x + threadIdx.x; v < V; v += gridDim.x * blockDim.x)
+        if ((uint32_t)lab[v] >= (uint32_t)limit) *flag = 0;
+}
+
+}  // namespace
+
+hipError_t launch_label_fit(const Graph &g, const int32_t *labels, int32_t limit, int32_t *flag) {
+    hipError_t e = launch_fill_i32(flag, 1, 1, g.stream);
+    if (e != hipSuccess || g.V == 0) return e;
+    int64_t blocks = (g.V + 255) / 256;
+    k_label_fit<<<(unsigned)(blocks < 4096 ? blocks : 4096), 256, 0, g.stream>>>(g.V, labels,
+                                                                               limit, flag);
     return hipGetLastError();
 }
 

@@ -560,6 +560,7 @@ __device__ __forceinline__ void pair_chain(const SweepArgs &a, int32_t slice, ch
 template <int S, int BM>
 __global__ __launch_bounds__(2 * kLanes) void k_sweep_pair(SweepArgs a) {
     extern __shared__ __align__(16) char smem[];
+    if (a.gate != nullptr && *a.gate != a.gate_want) return;
     const int32_t n_slices = (a.P + S - 1) / S;
     const bool fwd = (int32_t)blockIdx.x >= n_slices;
     const int32_t slice = fwd ? blockIdx.x - n_slices : blockIdx.x;

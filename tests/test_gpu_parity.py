@@ -105,6 +105,33 @@ def test_random_small_graphs(P):
         assert_same(got, exp)
 
 
+def test_single_labels_beyond_16_bits(P):
+    """Labels outside [0, 2^16) -- one stray label is enough -- send a single
+    evaluation to the single-placement sweep instead of the batched one; the
+    results must not depend on which ran."""
+    say("single placement, labels beyond 16 bits")
+    rng = np.random.default_rng(65536)
+    for t, g in enumerate([W.random_dag(rng, 600, p_edge=0.01, max_weight=9, n_labels=3),
+                           cfg(0)]):
+        pools = [np.array([-5, 65536, 70000, 2 ** 30, 123456789]), np.arange(4)]
+        for pool in pools:
+            lab = pool[rng.integers(0, pool.size, g.n_nodes)].astype(np.int32)
+            if pool.size == 4:
+                lab[g.n_nodes // 2] = 65536   # a single label out of range
+            G = P.Graph(g.n_nodes, g.src, g.dst, g.comp, g.edge_cost, g.mem)
+            tl, bl, m = G.tb_levels(dev(lab, torch.int32))
+            crit, path, plen = G.critical_path(dev(lab, torch.int32), tl, bl, m)
+            torch.cuda.synchronize()
+            etl, ebl, em = oracle.tb_levels(g.n_nodes, g.src, g.dst, g.comp, g.edge_cost, lab)
+            ecrit, epath = oracle.critical_path(g.n_nodes, g.src, g.dst, g.comp, g.edge_cost, lab,
+                                                etl, ebl, em)
+            assert (tl.cpu().numpy() == etl).all() and (bl.cpu().numpy() == ebl).all()
+            assert int(m.item()) == em
+            assert (crit.cpu().numpy() == ecrit).all()
+            assert (path[: int(plen.item())].cpu().numpy() == epath).all()
+            G.close()
+
+
 def test_all_zero_weights_ties(P):
     # every path has length 0: every node critical, path = lexicographic minimum
     say("all-zero weights")
