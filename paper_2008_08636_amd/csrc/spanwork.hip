@@ -47,7 +47,7 @@ inline size_t align256(size_t b) { return (b + 255) / 256 * 256; }
 
 // Scratch layout for V nodes, C clusters, K partitions.
 struct SwLayout {
-    size_t ids0, ids1, tl_tmp, lab_key, lab_sorted, s_tl, pre, seg, first, last, m, temp;
+    size_t ids0, ids1, tl_tmp, lab_key, lab_sorted, s_tl, pre, seg, first, last, m, range, temp;
     size_t temp_bytes, total;
     SwLayout(int32_t V, int32_t C, int32_t K) {
         size_t o = 0;
@@ -67,7 +67,8 @@ struct SwLayout {
         first = take((size_t)C * 8);
         last = take((size_t)C * 8);
         m = take(8);
-        size_t t1 = 0, t2 = 0, t3 = 0;
+        range = take(16);
+        size_t t1 = 0, t2 = 0, t3 = 0, t4 = 0;
         (void)rocprim::radix_sort_pairs(nullptr, t1, (const int64_t *)nullptr, (int64_t *)nullptr,
                                         (const int32_t *)nullptr, (int32_t *)nullptr, V);
         (void)rocprim::radix_sort_pairs(nullptr, t2, (const uint32_t *)nullptr,
@@ -75,8 +76,12 @@ struct SwLayout {
                                         (int32_t *)nullptr, V);
         (void)rocprim::inclusive_scan(nullptr, t3, (const int64_t *)nullptr, (int64_t *)nullptr,
                                       (size_t)V, rocprim::plus<int64_t>());
+        (void)rocprim::radix_sort_pairs(nullptr, t4, (const uint64_t *)nullptr,
+                                        (uint64_t *)nullptr, (const int32_t *)nullptr,
+                                        (int32_t *)nullptr, V);
         temp_bytes = t1 > t2 ? t1 : t2;
         temp_bytes = temp_bytes > t3 ? temp_bytes : t3;
+        temp_bytes = temp_bytes > t4 ? temp_bytes : t4;
         temp = take(temp_bytes);
         total = o;
     }
@@ -92,8 +97,8 @@ T *at(void *base, size_t off) {
 __global__ void k_sw_nodes(int32_t V, int32_t K, int32_t C, const int32_t *label,
                            const int32_t *cluster, const int32_t *level, const int64_t *tl,
                            const int64_t *comp, long long *first, long long *last, long long *m,
-                           int32_t *ids, int32_t *err) {
-    long long best = LLONG_MIN;
+                           long long *range, int32_t *ids, int32_t *err) {
+    long long best = LLONG_MIN, tmin = LLONG_MAX, tmax = LLONG_MIN;
     for (int32_t v = blockIdx.x * blockDim.x + threadIdx.x; v < V; v += gridDim.x * blockDim.x) {
         const int32_t c = cluster[v], k = label[v];
         if (c < -1 || c >= C) atomicOr(err, 1);
@@ -105,10 +110,48 @@ __global__ void k_sw_nodes(int32_t V, int32_t K, int32_t C, const int32_t *label
         }
         const long long f = tl[v] + comp[v];
         best = f > best ? f : best;
+        tmin = tl[v] < tmin ? tl[v] : tmin;
+        tmax = tl[v] > tmax ? tl[v] : tmax;
         ids[v] = v;
     }
     best = wave_max_i64(best);
-    if (lane_id() == 0 && best != LLONG_MIN) atomicMax(m, best);
+    tmax = wave_max_i64(tmax);
+#pragma unroll
+    for (int off = kWave / 2; off > 0; off >>= 1) {
+        const long long o = __shfl_xor(tmin, off, kWave);
+        tmin = o < tmin ? o : tmin;
+    }
+    if (lane_id() == 0 && best != LLONG_MIN) {
+        atomicMax(m, best);
+        atomicMin(&range[0], tmin);
+        atomicMax(&range[1], tmax);
+    }
+}
+
+// one sort key per node: (partition << tb) | (tl - tmin), unmapped nodes last
+__global__ void k_sw_keys(int32_t V, int32_t K, const int32_t *label, const int64_t *tl,
+                          int64_t tmin, int32_t tb, uint64_t *key) {
+    for (int32_t v = blockIdx.x * blockDim.x + threadIdx.x; v < V; v += gridDim.x * blockDim.x) {
+        const int32_t k = label[v];
+        const uint64_t part = (k >= 0 && k < K) ? (uint64_t)k : (uint64_t)K;
+        key[v] = (part << tb) | ((uint64_t)tl[v] - (uint64_t)tmin);
+    }
+}
+
+// seg[k] = first position whose key's partition is >= k (keys sorted)
+__global__ void k_sw_seg64(int32_t V, int32_t K, const uint64_t *key, int32_t tb, int32_t *seg) {
+    const int32_t k = blockIdx.x * blockDim.x + threadIdx.x;
+    if (k > K) return;
+    const uint64_t x = (uint64_t)k << tb;
+    int32_t lo = 0, hi = V;
+    while (lo < hi) {
+        const int32_t mid = (lo + hi) >> 1;
+        if (key[mid] < x)
+            lo = mid + 1;
+        else
+            hi = mid;
+    }
+    seg[k] = lo;
 }
 
 // partition of the i-th node in tl order; unmapped (or invalid) nodes sort last
@@ -234,6 +277,49 @@ __global__ void k_sw_work(int32_t C, int32_t K, const int64_t *lo, const int64_t
     }
 }
 
+// Work and choice together for K <= 64: a group of G lanes (G = the power of
+// two >= K) holds one cluster, lane k its partition k; the group sums the
+// communication and picks the Eq. 2 minimum with wave shuffles.
+template <int G>
+__global__ __launch_bounds__(256) void k_sw_work_decide(
+    int32_t C, int32_t K, const int64_t *lo, const int64_t *hi, const int32_t *seg,
+    const int64_t *s_tl, const int64_t *pre, const long long *first, const int64_t *comm,
+    int64_t *work, int32_t *choice) {
+    const int64_t i = blockIdx.x * (int64_t)blockDim.x + threadIdx.x;
+    const int32_t c = (int32_t)(i / G), k = (int32_t)(i % G);
+    const bool on = c < C && k < K;
+    int64_t w = 0, cm = 0;
+    if (on) {
+        const int64_t a = lo[c], b = hi[c];
+        if (a <= b) {
+            const int32_t s0 = seg[k], s1 = seg[k + 1];
+            const int32_t x = bound<false>(s_tl, s0, s1, a);
+            const int32_t y = bound<true>(s_tl, x, s1, b);
+            w = pre[y] - pre[x];
+        }
+        cm = comm[(int64_t)c * K + k];
+        work[(int64_t)c * K + k] = w;
+    }
+    long long tot = cm;
+#pragma unroll
+    for (int off = 1; off < G; off <<= 1) tot += __shfl_xor(tot, off, kWave);
+    // (cost, -comm, k) lexicographic minimum over the group
+    long long cost = on ? (long long)(w + tot - cm) : LLONG_MAX;
+    long long neg = on ? -(long long)cm : LLONG_MAX;
+    int32_t kk = on ? k : INT32_MAX;
+#pragma unroll
+    for (int off = 1; off < G; off <<= 1) {
+        const long long oc = __shfl_xor(cost, off, kWave), on2 = __shfl_xor(neg, off, kWave);
+        const int32_t ok = __shfl_xor(kk, off, kWave);
+        if (oc < cost || (oc == cost && (on2 < neg || (on2 == neg && ok < kk)))) {
+            cost = oc;
+            neg = on2;
+            kk = ok;
+        }
+    }
+    if (on && k == 0) choice[c] = first[c] == LLONG_MAX ? -1 : kk;
+}
+
 __global__ void k_sw_decide(int32_t C, int32_t K, const long long *first, const int64_t *work,
                             const int64_t *comm, int32_t *choice) {
     for (int32_t c = blockIdx.x * blockDim.x + threadIdx.x; c < C; c += gridDim.x * blockDim.x) {
@@ -279,6 +365,7 @@ hipError_t launch_span_work(const Graph &g, const int32_t *label, int32_t K,
     int32_t *seg = at<int32_t>(scratch, L.seg);
     int64_t *first = at<int64_t>(scratch, L.first), *last = at<int64_t>(scratch, L.last);
     int64_t *m = at<int64_t>(scratch, L.m);
+    int64_t *range = at<int64_t>(scratch, L.range);
     void *temp = at<char>(scratch, L.temp);
     size_t temp_bytes = L.temp_bytes;
     hipError_t e;
@@ -286,36 +373,72 @@ hipError_t launch_span_work(const Graph &g, const int32_t *label, int32_t K,
     if ((e = launch_fill_i64(first, C, LLONG_MAX, s)) != hipSuccess) return e;
     if ((e = launch_fill_i64(last, C, -1, s)) != hipSuccess) return e;
     if ((e = launch_fill_i64(m, 1, LLONG_MIN, s)) != hipSuccess) return e;
+    if ((e = launch_fill_i64(range, 1, LLONG_MAX, s)) != hipSuccess) return e;
+    if ((e = launch_fill_i64(range + 1, 1, LLONG_MIN, s)) != hipSuccess) return e;
     if ((e = launch_fill_i64(pre, 1, 0, s)) != hipSuccess) return e;
     if ((e = launch_fill_i64(comm, (int64_t)C * K, 0, s)) != hipSuccess) return e;
+    unsigned pbits = 1;   // partitions 0..K (K: unmapped) fit in pbits bits
+    while (pbits < 32 && ((uint64_t)K >> pbits) != 0) pbits++;
+    bool composite = false;
     if (V > 0) {
         k_sw_nodes<<<grid_for(V, kBlock, 2048), kBlock, 0, s>>>(
             V, K, C, label, cluster, g.level, tl, g.comp, reinterpret_cast<long long *>(first),
-            reinterpret_cast<long long *>(last), reinterpret_cast<long long *>(m), ids0, err);
+            reinterpret_cast<long long *>(last), reinterpret_cast<long long *>(m),
+            reinterpret_cast<long long *>(range), ids0, err);
         if ((e = hipGetLastError()) != hipSuccess) return e;
-        // nodes by tl, then (stably) by partition
-        if ((e = rocprim::radix_sort_pairs(temp, temp_bytes, tl, tl_tmp, ids0, ids1, V, 0u, 64u,
-                                           s)) != hipSuccess)
+        // The tl range sizes the sort: when (partition, tl - min) fits one
+        // 64-bit key, a single stable radix sort over its bits orders the
+        // nodes by (partition, tl, id); otherwise two sorts (tl, then partition).
+        int64_t h_range[2] = {0, 0};
+        if ((e = hipMemcpyAsync(h_range, range, sizeof(h_range), hipMemcpyDeviceToHost, s)) !=
+            hipSuccess)
             return e;
-        k_sw_lab_keys<<<grid_for(V, kBlock), kBlock, 0, s>>>(V, K, label, ids1, lab_key);
+        if ((e = hipStreamSynchronize(s)) != hipSuccess) return e;
+        const uint64_t span = (uint64_t)h_range[1] - (uint64_t)h_range[0];
+        unsigned tb = 1;
+        while (tb < 64 && (span >> tb) != 0) tb++;
+        const int32_t *sorted_ids;
+        if (tb + pbits <= 64) {
+            composite = true;
+            uint64_t *keys_in = reinterpret_cast<uint64_t *>(tl_tmp);
+            uint64_t *keys_out = reinterpret_cast<uint64_t *>(s_tl);
+            k_sw_keys<<<grid_for(V, kBlock), kBlock, 0, s>>>(V, K, label, tl, h_range[0],
+                                                             (int32_t)tb, keys_in);
+            if ((e = hipGetLastError()) != hipSuccess) return e;
+            if ((e = rocprim::radix_sort_pairs(temp, temp_bytes, (const uint64_t *)keys_in,
+                                               keys_out, (const int32_t *)ids0, ids1, V, 0u,
+                                               tb + pbits, s)) != hipSuccess)
+                return e;
+            k_sw_seg64<<<grid_for(K + 1, kBlock), kBlock, 0, s>>>(V, K, keys_out, (int32_t)tb,
+                                                                  seg);
+            if ((e = hipGetLastError()) != hipSuccess) return e;
+            sorted_ids = ids1;
+        } else {
+            if ((e = rocprim::radix_sort_pairs(temp, temp_bytes, tl, tl_tmp, ids0, ids1, V, 0u,
+                                               64u, s)) != hipSuccess)
+                return e;
+            k_sw_lab_keys<<<grid_for(V, kBlock), kBlock, 0, s>>>(V, K, label, ids1, lab_key);
+            if ((e = hipGetLastError()) != hipSuccess) return e;
+            if ((e = rocprim::radix_sort_pairs(temp, temp_bytes, lab_key, lab_sorted, ids1, ids0,
+                                               V, 0u, pbits, s)) != hipSuccess)
+                return e;
+            sorted_ids = ids0;
+        }
+        k_sw_gather<<<grid_for(V, kBlock), kBlock, 0, s>>>(V, sorted_ids, tl, g.comp, s_tl,
+                                                           tl_tmp);
         if ((e = hipGetLastError()) != hipSuccess) return e;
-        unsigned bits = 1;
-        while (bits < 32 && ((uint64_t)K >> bits) != 0) bits++;
-        if ((e = rocprim::radix_sort_pairs(temp, temp_bytes, lab_key, lab_sorted, ids1, ids0, V,
-                                           0u, bits, s)) != hipSuccess)
-            return e;
-        k_sw_gather<<<grid_for(V, kBlock), kBlock, 0, s>>>(V, ids0, tl, g.comp, s_tl, tl_tmp);
-        if ((e = hipGetLastError()) != hipSuccess) return e;
-        if ((e = rocprim::inclusive_scan(temp, temp_bytes, (const int64_t *)tl_tmp, pre + 1, (size_t)V,
-                                         rocprim::plus<int64_t>(), s)) != hipSuccess)
+        if ((e = rocprim::inclusive_scan(temp, temp_bytes, (const int64_t *)tl_tmp, pre + 1,
+                                         (size_t)V, rocprim::plus<int64_t>(), s)) != hipSuccess)
             return e;
         k_sw_comm<<<grid_for(g.E, kBlock), kBlock, 0, s>>>(
             g.E, K, C, g.e_src, g.e_dst, g.e_cost, cluster, label,
             reinterpret_cast<unsigned long long *>(comm));
         if ((e = hipGetLastError()) != hipSuccess) return e;
     }
-    k_sw_seg<<<grid_for(K + 1, kBlock), kBlock, 0, s>>>(V, K, lab_sorted, seg);
-    if ((e = hipGetLastError()) != hipSuccess) return e;
+    if (!composite) {
+        k_sw_seg<<<grid_for(K + 1, kBlock), kBlock, 0, s>>>(V, K, lab_sorted, seg);
+        if ((e = hipGetLastError()) != hipSuccess) return e;
+    }
     {
         const long long *fk = reinterpret_cast<const long long *>(first);
         long long *lo = reinterpret_cast<long long *>(span_lo);
@@ -332,11 +455,27 @@ hipError_t launch_span_work(const Graph &g, const int32_t *label, int32_t K,
             C, fk, reinterpret_cast<const long long *>(m), lo, hi);
         if ((e = hipGetLastError()) != hipSuccess) return e;
     }
+    if (C == 0) return hipSuccess;
+    const long long *fk = reinterpret_cast<const long long *>(first);
+    if (K <= 64) {
+        int G = 1;
+        while (G < K) G <<= 1;
+        const unsigned blocks = (unsigned)(((int64_t)C * G + 255) / 256);
+        switch (G) {
+#define SW_CASE(g_)                                                                              \
+    case g_:                                                                                     \
+        k_sw_work_decide<g_><<<blocks, 256, 0, s>>>(C, K, span_lo, span_hi, seg, s_tl, pre, fk, \
+                                                    comm, work, choice);                         \
+        break;
+            SW_CASE(1) SW_CASE(2) SW_CASE(4) SW_CASE(8) SW_CASE(16) SW_CASE(32) SW_CASE(64)
+#undef SW_CASE
+        }
+        return hipGetLastError();
+    }
     k_sw_work<<<grid_for((int64_t)C * K, kBlock), kBlock, 0, s>>>(C, K, span_lo, span_hi, seg,
                                                                   s_tl, pre, work);
     if ((e = hipGetLastError()) != hipSuccess) return e;
-    k_sw_decide<<<grid_for(C, kBlock), kBlock, 0, s>>>(
-        C, K, reinterpret_cast<const long long *>(first), work, comm, choice);
+    k_sw_decide<<<grid_for(C, kBlock), kBlock, 0, s>>>(C, K, fk, work, comm, choice);
     return hipGetLastError();
 }
 

@@ -324,6 +324,29 @@ def test_span_work_small_random(P):
         check_span(got, exp)
 
 
+def test_span_work_wide_cases(P):
+    """More than 64 partitions (the choice in its own pass) and a tl range too
+    wide for one (partition, tl) sort key (two sorts instead of one)."""
+    say("eq2 wide cases")
+    rng = np.random.default_rng(803)
+    for K, wide in [(100, False), (3, True), (70, True)]:
+        n = 400
+        g = W.random_dag(rng, n, p_edge=0.01, max_weight=9, n_labels=1)
+        label = np.where(rng.random(n) < 0.6, rng.integers(0, K, n), -1).astype(np.int32)
+        C = 90
+        cluster = np.where(label < 0, rng.integers(-1, C, n), -1).astype(np.int32)
+        if wide:
+            tl = rng.integers(-2 ** 62, 2 ** 62, n).astype(np.int64)
+            tl[:5] = [-2 ** 62, 2 ** 62 - 1, 0, 0, 7]
+        else:
+            tl = tb_levels(n, g.src, g.dst, g.comp, g.edge_cost, np.arange(n))[0]
+        # comp is small, so tl + comp stays inside int64
+        G = P.Graph(g.n_nodes, g.src, g.dst, g.comp, g.edge_cost, g.mem)
+        got = run_span(G, label, K, cluster, C, tl)
+        G.close()
+        check_span(got, span_work(n, g.src, g.dst, g.comp, g.edge_cost, label, K, cluster, C, tl))
+
+
 @pytest.mark.parametrize("i", [0, 1, 2])
 def test_span_work_mapping_state(P, i):
     """The mapping stage's state on each graph: the primaries of 16 slicing
