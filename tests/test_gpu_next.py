@@ -415,3 +415,40 @@ def test_slicing_beyond_packed_levels(P):
     g = W.chain_graph(rng, 70000)
     say(f"slicing deep chain V={g.n_nodes}")
     check_slicing(P, g, 2)
+
+
+def test_next_rows_on_empty_and_single_node_graphs(P):
+    """V = 0 and V = 1 through every entry point after the core path, against
+    the oracle."""
+    say("next rows: empty and single-node graphs")
+    e32, e64 = np.zeros(0, np.int32), np.zeros(0, np.int64)
+    for n in (0, 1):
+        comp = np.full(n, 5, np.int64)
+        mem = np.full(n, 7, np.int64)
+        G = P.Graph(n, e32, e32, comp, e64, mem)
+        # Heuristic II
+        pl = np.zeros((n, 3), np.int32)
+        kind = np.ones(n, np.int32)
+        tgt = np.full(n, -1, np.int32)
+        out = run_balance(G, pl, kind, tgt, 2)
+        check_balance(n, mem, kind, tgt, pl, 2, out, range(3))
+        # cluster criticality
+        crit, order = G.cluster_criticality(dev(np.zeros(n, np.int32), torch.int32), 3)
+        ec, eo = cluster_criticality(n, e32, e32, comp, e64, np.zeros(n, np.int64), 3)
+        assert crit.cpu().numpy().tolist() == ec.tolist() and order.cpu().numpy().tolist() == eo.tolist()
+        # span work
+        lab = np.full(n, -1, np.int32)
+        cl = np.zeros(n, np.int32)
+        tl = np.zeros(n, np.int64)
+        got = run_span(G, lab, 2, cl, 2, tl)
+        check_span(got, span_work(n, e32, e32, comp, e64, lab, 2, cl, 2, tl))
+        # slicing
+        out = G.slice_primaries(2)
+        torch.cuda.synchronize()
+        primary, paths, ms = slice_primaries(n, e32, e32, comp, e64, 2)
+        assert out["makespan"].cpu().numpy().tolist() == ms.tolist()
+        assert out["primary"].cpu().numpy().tolist() == primary.tolist()
+        for j in range(2):
+            k = int(out["path_len"][j])
+            assert out["paths"][j, :k].cpu().numpy().tolist() == paths[j].tolist()
+        G.close()
