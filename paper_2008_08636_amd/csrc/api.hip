@@ -869,12 +869,31 @@ int pardnn_cluster_criticality(pardnn_graph *h, const int32_t *cluster, int32_t 
         HIP_TRY(dalloc(*g, &g->cl_bl, V));
         HIP_TRY(dalloc(*g, &g->cl_m, 1));
     }
-    HIP_TRY(grow_aux(g, cluster_sort_bytes(n_clusters)));
+    const size_t sort_bytes = (cluster_sort_bytes(n_clusters) + 255) / 256 * 256;
+    HIP_TRY(grow_aux(g, sort_bytes + cluster_relabel_bytes(V, n_clusters)));
     HIP_TRY(launch_fill_i32(g->err, 4, 0, g->stream));
+    // The pair sweep packs labels below 2^16. The cluster ids fit when there
+    // are few clusters; otherwise labels with the same equality on every edge
+    // (levels for lone nodes, L + rank for the others) often do.
     int32_t lb = 0, ob = 0;
-    if (V > 0 && pair_single_bits(g, n_clusters, g->weight_bound, &lb, &ob)) {
-        // up to 2^16 clusters: the ids fit the pair sweep's packed keys
-        st = pair_single_labels(g, cluster);
+    const int32_t *pair_labels = nullptr;
+    if (V > 0) {
+        int32_t *lab = nullptr, *n_multi = nullptr;
+        HIP_TRY(launch_cluster_relabel(
+            *g, cluster, n_clusters,
+            reinterpret_cast<int32_t *>(reinterpret_cast<char *>(g->aux_scratch) + sort_bytes),
+            &lab, &n_multi));
+        int32_t h_multi = 0;
+        HIP_TRY(hipMemcpyAsync(&h_multi, n_multi, sizeof(int32_t), hipMemcpyDeviceToHost,
+                               g->stream));
+        HIP_TRY(hipStreamSynchronize(g->stream));
+        if (pair_single_bits(g, (int64_t)g->L + h_multi, g->weight_bound, &lb, &ob))
+            pair_labels = lab;
+        else if (pair_single_bits(g, n_clusters, g->weight_bound, &lb, &ob))
+            pair_labels = cluster;
+    }
+    if (pair_labels != nullptr) {
+        st = pair_single_labels(g, pair_labels);
         if (st == PARDNN_OK)
             st = pair_single_sweep(g, lb, ob, g->node_rec, g->comp_lm, g->cl_tl, g->cl_bl,
                                    g->cl_m);
@@ -898,7 +917,7 @@ int pardnn_cluster_criticality(pardnn_graph *h, const int32_t *cluster, int32_t 
         HIP_TRY(launch_sweep(a, 1, g->stream));
     }
     HIP_TRY(launch_cluster_criticality(*g, cluster, n_clusters, g->cl_tl, g->cl_bl, criticality,
-                                       order, g->aux_scratch, g->aux_scratch_bytes, g->err));
+                                       order, g->aux_scratch, sort_bytes, g->err));
     st = read_errors(g);
     if (st != PARDNN_OK) return st;
     if (g->h_err[0] & 1) return fail(PARDNN_E_INVAL, "a cluster id lies outside [0, n_clusters)");

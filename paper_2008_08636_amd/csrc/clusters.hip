@@ -43,7 +43,65 @@ __global__ void k_cluster_max(int32_t V, int32_t n_clusters, const int32_t *clus
     }
 }
 
+__global__ void k_cl_count(int32_t V, int32_t C, const int32_t *cluster, int32_t *count) {
+    for (int32_t v = blockIdx.x * blockDim.x + threadIdx.x; v < V; v += gridDim.x * blockDim.x) {
+        const int32_t c = cluster[v];
+        if ((uint32_t)c < (uint32_t)C) atomicAdd(&count[c], 1);
+    }
+}
+
+__global__ void k_cl_multi(int32_t C, const int32_t *count, int32_t *flag) {
+    for (int32_t c = blockIdx.x * blockDim.x + threadIdx.x; c < C; c += gridDim.x * blockDim.x)
+        flag[c] = count[c] >= 2 ? 1 : 0;
+}
+
+// a node of a cluster with two or more nodes takes L + the cluster's rank
+// among those; a node alone in its cluster takes its level
+__global__ void k_cl_labels(int32_t V, int32_t C, int32_t L, const int32_t *cluster,
+                            const int32_t *count, const int32_t *rank, const int32_t *level,
+                            int32_t *lab) {
+    for (int32_t v = blockIdx.x * blockDim.x + threadIdx.x; v < V; v += gridDim.x * blockDim.x) {
+        const int32_t c = cluster[v];
+        const bool multi = (uint32_t)c < (uint32_t)C && count[c] >= 2;
+        lab[v] = multi ? L + rank[c] : level[v];
+    }
+}
+
 }  // namespace
+
+// Labels with the same equality on every edge as the cluster ids, drawn from
+// few values: communication matters only across an edge, and an edge always
+// joins two levels, so a node alone in its cluster can carry its level; the
+// clusters with two or more nodes take the values L, L + 1, ... in id order.
+// Scratch: count, flag int32[C], rank int32[C + 1], the scan's space; lab is
+// int32[V]. rank[C] receives the number of clusters with two or more nodes.
+size_t cluster_relabel_bytes(int32_t V, int32_t C) {
+    const size_t n = 3 * (size_t)C + 1 + scan_workspace_elems(C) + (size_t)V;
+    return (n * 4 + 255) / 256 * 256;
+}
+
+hipError_t launch_cluster_relabel(const Graph &g, const int32_t *cluster, int32_t C,
+                                  int32_t *scratch, int32_t **lab, int32_t **n_multi) {
+    int32_t *count = scratch, *flag = count + C, *rank = flag + C;
+    int32_t *ws = rank + C + 1;
+    *lab = ws + scan_workspace_elems(C);
+    *n_multi = rank + C;
+    hipError_t e = launch_fill_i32(count, C, 0, g.stream);
+    if (e != hipSuccess) return e;
+    if (g.V > 0) {
+        k_cl_count<<<grid_for(g.V, kBlock), kBlock, 0, g.stream>>>(g.V, C, cluster, count);
+        if ((e = hipGetLastError()) != hipSuccess) return e;
+    }
+    k_cl_multi<<<grid_for(C, kBlock), kBlock, 0, g.stream>>>(C, count, flag);
+    if ((e = hipGetLastError()) != hipSuccess) return e;
+    if ((e = launch_exclusive_scan(flag, rank, C, ws, g.stream)) != hipSuccess) return e;
+    if (g.V > 0) {
+        k_cl_labels<<<grid_for(g.V, kBlock), kBlock, 0, g.stream>>>(g.V, C, g.L, cluster, count,
+                                                                    rank, g.level, *lab);
+        e = hipGetLastError();
+    }
+    return e;
+}
 
 // Scratch of the sort: `keys_out` int64[n], `ids` int32[n], then the radix
 // sort's own temporary storage. Returns the bytes needed for n clusters.

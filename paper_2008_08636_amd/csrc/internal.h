@@ -183,6 +183,11 @@ hipError_t launch_span_work(const Graph &g, const int32_t *label, int32_t K,
 
 // ---- clusters.hip ----
 size_t cluster_sort_bytes(int32_t n);
+// labels with the cluster ids' equality on every edge, in [0, L + n_multi):
+// *lab (int32[V], original ids) and *n_multi (device) point into scratch
+size_t cluster_relabel_bytes(int32_t V, int32_t C);
+hipError_t launch_cluster_relabel(const Graph &g, const int32_t *cluster, int32_t C,
+                                  int32_t *scratch, int32_t **lab, int32_t **n_multi);
 // criticality[c] = max over nodes of cluster c of tl + bl (-1: none); order:
 // cluster ids by (criticality desc, id asc); err bit 0: cluster id out of range
 hipError_t launch_cluster_criticality(const Graph &g, const int32_t *cluster, int32_t n_clusters,

@@ -245,6 +245,22 @@ def test_clusters_of_slicing(P, i):
     check_clusters(P, g, cl, K + g.n_nodes)
 
 
+def test_clusters_label_paths(P):
+    """The three ways the sweep gets its labels: levels and cluster ranks
+    (usual), the cluster ids themselves (more than 2^16 levels, few
+    clusters), the single-placement sweep (many levels and many clusters)."""
+    rng = np.random.default_rng(93)
+    g = W.chain_graph(rng, 70000)
+    n = g.n_nodes
+    say(f"cluster criticality label paths, chain V={n}")
+    two = (np.arange(n) >= n // 2).astype(np.int32)      # ids fit: 2 clusters
+    check_clusters(P, g, two, 2)
+    alone = np.arange(n, dtype=np.int32)                 # neither fits
+    check_clusters(P, g, alone, n)
+    mixed = np.where(np.arange(n) % 3 == 0, np.arange(n) // 3, n).astype(np.int32)
+    check_clusters(P, g, mixed, n + 1)                   # one large cluster + lone nodes
+
+
 def test_clusters_errors(P):
     say("cluster criticality errors")
     rng = np.random.default_rng(92)
