@@ -142,7 +142,7 @@ def cpu_baseline(g, sched, budget_s: float):
     }
 
 
-ROWS = ("refinement", "memory_balance", "cluster_criticality", "slicing", "span_work")
+ROWS = ("refinement", "single", "memory_balance", "cluster_criticality", "slicing", "span_work")
 
 
 def time_calls(P, G, fn, steps: int, warmup: int):
@@ -172,6 +172,101 @@ def hbm_roofline(kernel: str, kernel_ms: float, alg_bytes: int, note: str = ""):
     if note:
         r["note"] = note
     return r
+
+
+def bench_single(args) -> int:
+    """One full evaluation of one placement (t/b levels, critical path, label
+    memory: pardnn_tb_levels + pardnn_critical_path + pardnn_label_memory) on
+    each of the four single-graph workloads; one JSON line, `value` on the
+    transformer graph."""
+    import numpy as np
+    import torch
+
+    import paper_2008_08636_amd as P
+    import workloads as W
+
+    P.load_library()
+    names = {0: "tiny layered DAG", 1: "stacked-LSTM training DAG",
+             2: "transformer training DAG", 3: "Wide-ResNet-shaped DAG"}
+    per, cpu = {}, {}
+    for i in (0, 1, 2, 3):
+        g = W.make_config(i)
+        V, E, K = g.n_nodes, g.n_edges, g.n_labels
+        G = P.Graph(V, g.src, g.dst, g.comp, g.edge_cost, g.mem)
+        L = P.pardnn_levelize(G.handle)
+        P.pardnn_set_timing(G.handle, True)
+        lab = torch.as_tensor(g.placement, dtype=torch.int32).cuda()
+        cap = torch.as_tensor(g.capacity, dtype=torch.int64).cuda()
+        tl = torch.empty(V, dtype=torch.int64, device="cuda")
+        bl = torch.empty(V, dtype=torch.int64, device="cuda")
+        m = torch.empty(1, dtype=torch.int64, device="cuda")
+        crit = torch.empty(V, dtype=torch.uint8, device="cuda")
+        path = torch.empty(max(V, 1), dtype=torch.int32, device="cuda")
+        plen = torch.empty(1, dtype=torch.int32, device="cuda")
+        sums = torch.empty(K, dtype=torch.int64, device="cuda")
+        over = torch.empty(K, dtype=torch.int64, device="cuda")
+
+        def fn():
+            P.pardnn_tb_levels(G.handle, lab, tl, bl, m)
+            P.pardnn_critical_path(G.handle, lab, tl, bl, m, crit, path, plen)
+            P.pardnn_label_memory(G.handle, lab, K, cap, sums, over)
+
+        steps = args.steps if i != 3 else max(2, args.steps // 4)
+        for _ in range(args.warmup):
+            fn()
+        torch.cuda.synchronize()
+        ks = []
+        t0 = time.perf_counter()
+        for _ in range(steps):
+            P.pardnn_tb_levels(G.handle, lab, tl, bl, m)
+            ks.append(P.pardnn_get_timing(G.handle)[1])
+            P.pardnn_critical_path(G.handle, lab, tl, bl, m, crit, path, plen)
+            P.pardnn_label_memory(G.handle, lab, K, cap, sums, over)
+        torch.cuda.synchronize()
+        wall = (time.perf_counter() - t0) * 1e3 / steps
+        sweep_ms = float(np.mean(ks))
+        per[f"config{i}"] = {"workload": names[i], "V": V, "E": E, "levels": L,
+                             "ms": round(wall, 4), "sweep_ms": round(sweep_ms, 4),
+                             "us_per_level": round(sweep_ms * 1e3 / max(L, 1), 4),
+                             "gteps": round(2 * E / (wall / 1e3) / 1e9, 4)}
+        print(f"[bench] single config{i}: {wall:.3f} ms per evaluation, sweep {sweep_ms:.3f} ms",
+              file=sys.stderr, flush=True)
+        if args.cpu_budget > 0 and i in (0, 1, 2):
+            import oracle
+            oracle.build(force=False)
+            t0, reps = time.perf_counter(), 0
+            while reps < 1 or time.perf_counter() - t0 < args.cpu_budget / 3:
+                oracle.evaluate(V, g.src, g.dst, g.comp, g.edge_cost, g.mem, g.placement, K,
+                                g.capacity)
+                reps += 1
+            dt = (time.perf_counter() - t0) / reps
+            cpu[f"config{i}"] = {"ms": round(dt * 1e3, 3), "reps": reps}
+        if i == 2:
+            main = per["config2"]
+            roof = hbm_roofline(P.pardnn_get_timing(G.handle)[0], sweep_ms,
+                                algorithmic_bytes_tb_single(V, E),
+                                "one placement walks the level chain one level at a time: "
+                                "latency-bound")
+        G.close()
+    line = {
+        "metric": "single-placement full evaluations/sec (t/b levels, critical path, label "
+                  "memory), 1 MI355X",
+        "value": round(1e3 / main["ms"], 3), "unit": "evaluations/s", "n_gpus": 1,
+        "steps": args.steps, "warmup": args.warmup, "ms_per_step": main["ms"],
+        "higher_is_better": True, "scaling": "weak", "vs_baseline": None, "dtype": "int64",
+        "data": "synthetic",
+        "config": {"workload": "one placement of the transformer training DAG, evaluated in "
+                               "full; the other graphs alongside", "per_graph": per},
+        "roofline": roof,
+        "cpu_baseline": ({"value": round(1e3 / cpu["config2"]["ms"], 3), "unit": "evaluations/s",
+                          "cores": 1, "kind": "oracle",
+                          "sample": f"whole evaluations on one core of '{host_cpu_model()}': " +
+                                    ", ".join(f"{k} {v['ms']} ms x {v['reps']}"
+                                              for k, v in cpu.items())}
+                         if cpu else None),
+    }
+    print(json.dumps(line), flush=True)
+    return 0
 
 
 def bench_row(args, row: str) -> int:
@@ -391,6 +486,8 @@ def main() -> int:
         torch.cuda.synchronize()
         print("copied 1 GiB three times", file=sys.stderr, flush=True)
         return 0
+    if args.row == "single":
+        return bench_single(args)
     if args.row != "refinement":
         return bench_row(args, args.row)
     P.load_library()

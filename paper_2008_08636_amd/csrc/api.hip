@@ -162,6 +162,11 @@ int ensure_levelized(Graph *g) {
     HIP_TRY(dalloc(*g, &g->node_rec, V));
     HIP_TRY(dalloc(*g, &g->lab_lm, V));
     HIP_TRY(dalloc(*g, &g->next_lm, V));
+    HIP_TRY(dalloc(*g, &g->cp_flag, (size_t)V + 1));
+    HIP_TRY(dalloc(*g, &g->cp_pos, (size_t)V + 1));
+    HIP_TRY(dalloc(*g, &g->cp_ws, scan_workspace_elems(V)));
+    HIP_TRY(dalloc(*g, &g->cp_list, V));
+    HIP_TRY(dalloc(*g, &g->cp_ok, 1));
     HIP_TRY(dalloc(*g, &g->crit_lm, V));
     HIP_TRY(dalloc(*g, &g->ft_lm, 2 * (size_t)V));
     HIP_TRY(dalloc(*g, &g->bl_lm, 2 * (size_t)V));

@@ -8,7 +8,10 @@
 //                    until a node without a tight successor.
 //
 // Design for gfx950: next() of every node is one data-parallel pass over the
-// out-edges (level-major CSR). The remaining walk is a pointer chase, and its
+// out-edges (level-major CSR). When the critical nodes form one chain (one
+// critical path) the path is their list in level-major order, found by a
+// scan and checked link by link in parallel. Otherwise the walk is a pointer
+// chase, and its
 // links only point to strictly later levels, i.e. to larger level-major ids.
 // One workgroup therefore stages a window of next() in LDS with a coalesced
 // load, chases inside the window at LDS latency, and reloads the window only
@@ -86,7 +89,8 @@ __global__ __launch_bounds__(kChaseThreads) void k_chase(int32_t V, int32_t n0,
                                                          const int32_t *start_orig,
                                                          const int32_t *next_lm,
                                                          const uint8_t *crit_lm, int32_t *path,
-                                                         int32_t *path_len) {
+                                                         int32_t *path_len, const int32_t *done) {
+    if (done != nullptr && *done) return;   // the list pass already wrote the path
     __shared__ int32_t win[kWindow];
     __shared__ int s_start, s_cur, s_len;
     const int tid = threadIdx.x;
@@ -128,6 +132,52 @@ __global__ __launch_bounds__(kChaseThreads) void k_chase(int32_t V, int32_t n0,
     if (tid == 0) *path_len = s_len;
 }
 
+// The list pass: when the critical nodes, in level-major order, form one
+// chain -- each links to the next, the last to nothing, and the first is the
+// walk's start -- that list is the path (the usual case: one critical path).
+// Then the path is written in parallel and the walk returns at once.
+__global__ void k_path_flags(int32_t V, const uint8_t *crit_lm, int32_t *f) {
+    for (int32_t v = blockIdx.x * blockDim.x + threadIdx.x; v < V; v += gridDim.x * blockDim.x)
+        f[v] = crit_lm[v] ? 1 : 0;
+}
+
+__global__ void k_path_list(int32_t V, const uint8_t *crit_lm, const int32_t *pos,
+                            int32_t *list) {
+    for (int32_t v = blockIdx.x * blockDim.x + threadIdx.x; v < V; v += gridDim.x * blockDim.x)
+        if (crit_lm[v]) list[pos[v]] = v;
+}
+
+// ok = 1 beforehand; n = pos[V] critical nodes
+__global__ void k_path_check(int32_t V, int32_t n0, const int32_t *pos, const int32_t *list,
+                             const int32_t *next_lm, const int32_t *rank,
+                             const int32_t *start_orig, int32_t *ok) {
+    const int32_t n = pos[V];
+    for (int32_t i = blockIdx.x * blockDim.x + threadIdx.x; i < n; i += gridDim.x * blockDim.x) {
+        const int32_t want = i + 1 < n ? list[i + 1] : -1;
+        if (next_lm[list[i]] != want) *ok = 0;
+    }
+    if (blockIdx.x == 0 && threadIdx.x == 0 && n > 0) {
+        bool start_ok;
+        if (start_orig == nullptr) {
+            start_ok = list[0] < n0;   // level 0 is sorted by id
+        } else {
+            const int32_t s = *start_orig;
+            start_ok = s != INT32_MAX && rank[s] == list[0];
+        }
+        if (!start_ok) *ok = 0;
+    }
+}
+
+__global__ void k_path_write(int32_t V, const int32_t *pos, const int32_t *list,
+                             const int32_t *order, const int32_t *ok, int32_t *path,
+                             int32_t *path_len) {
+    if (!*ok) return;
+    const int32_t n = pos[V];
+    for (int32_t i = blockIdx.x * blockDim.x + threadIdx.x; i < n; i += gridDim.x * blockDim.x)
+        path[i] = order[list[i]];
+    if (blockIdx.x == 0 && threadIdx.x == 0) *path_len = n;
+}
+
 }  // namespace
 
 hipError_t launch_crit_next(const Graph &g, const int32_t *placement, const int64_t *comp_lm,
@@ -151,8 +201,27 @@ hipError_t launch_crit_next(const Graph &g, const int32_t *placement, const int6
 hipError_t launch_chase_from(const Graph &g, const int32_t *start_orig, int32_t *path,
                              int32_t *path_len) {
     const int32_t n0 = g.L > 0 ? g.h_level_ptr[1] : 0;
-    k_chase<<<1, kChaseThreads, 0, g.stream>>>(g.V, n0, g.order, g.rank, start_orig, g.next_lm,
-                                               g.crit_lm, path, path_len);
+    const int32_t V = g.V;
+    int32_t *ok = g.cp_ok;
+    hipError_t e = launch_fill_i32(ok, 1, 1, g.stream);
+    if (e != hipSuccess) return e;
+    if (V > 0) {
+        k_path_flags<<<grid_for(V, kBlock), kBlock, 0, g.stream>>>(V, g.crit_lm, g.cp_flag);
+        if ((e = hipGetLastError()) != hipSuccess) return e;
+        if ((e = launch_exclusive_scan(g.cp_flag, g.cp_pos, V, g.cp_ws, g.stream)) != hipSuccess)
+            return e;
+        k_path_list<<<grid_for(V, kBlock), kBlock, 0, g.stream>>>(V, g.crit_lm, g.cp_pos,
+                                                                 g.cp_list);
+        if ((e = hipGetLastError()) != hipSuccess) return e;
+        k_path_check<<<grid_for(V, kBlock), kBlock, 0, g.stream>>>(
+            V, n0, g.cp_pos, g.cp_list, g.next_lm, g.rank, start_orig, ok);
+        if ((e = hipGetLastError()) != hipSuccess) return e;
+        k_path_write<<<grid_for(V, kBlock), kBlock, 0, g.stream>>>(V, g.cp_pos, g.cp_list,
+                                                                  g.order, ok, path, path_len);
+        if ((e = hipGetLastError()) != hipSuccess) return e;
+    }
+    k_chase<<<1, kChaseThreads, 0, g.stream>>>(V, n0, g.order, g.rank, start_orig, g.next_lm,
+                                               g.crit_lm, path, path_len, V > 0 ? ok : nullptr);
     return hipGetLastError();
 }
 

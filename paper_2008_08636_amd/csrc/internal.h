@@ -77,6 +77,9 @@ struct Graph {
 
     // single-placement scratch
     int32_t *lab_lm = nullptr, *next_lm = nullptr, *move_stamp = nullptr;
+    // the path's list pass: flags, positions [V + 1], scan space, list [V], ok
+    int32_t *cp_flag = nullptr, *cp_pos = nullptr, *cp_ws = nullptr, *cp_list = nullptr;
+    int32_t *cp_ok = nullptr;
     uint8_t *crit_lm = nullptr;
     int64_t *ft_lm = nullptr, *bl_lm = nullptr;   // {value, label} pairs, 2 * V each
     // graph slicing scratch (allocated on first use): masked node weights,
