@@ -39,17 +39,9 @@ namespace pardnn {
 
 namespace {
 
-constexpr int kBlock = 256;
-constexpr int kChaseRegs = 16;      // registers per lane of a path-walk window
+constexpr int kChaseRegs = 16;   // registers per lane of a path-walk window
 constexpr int kEmitNodes = 32;   // level-major nodes per emit workgroup
 constexpr int kEmitCols = 128;   // placements per emit chunk
-
-inline unsigned grid_for(int64_t n, int block, int cap = 65536) {
-    int64_t g = (n + block - 1) / block;
-    if (g < 1) g = 1;
-    if (g > cap) g = cap;
-    return (unsigned)g;
-}
 
 // Lanes of one placement slice: labels gathered into the slice-major layout
 // [slice][V][S] through an LDS tile, so that both the reads of the caller's
