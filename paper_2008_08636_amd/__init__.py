@@ -160,25 +160,31 @@ def pardnn_levelize(h, level=None, order=None, level_ptr=None) -> int:
     return n.value
 
 
+def _n_nodes(h) -> int:
+    return pardnn_get_info(h)["n_nodes"]
+
+
 def pardnn_tb_levels(h, placement, tl, bl, makespan):
-    _check(load_library().pardnn_tb_levels(h, _ptr(placement, torch.int32, name="placement"),
-                                           _ptr(tl, torch.int64, name="tl"),
-                                           _ptr(bl, torch.int64, name="bl"),
+    V = _n_nodes(h)
+    _check(load_library().pardnn_tb_levels(h, _ptr(placement, torch.int32, V, "placement"),
+                                           _ptr(tl, torch.int64, V, "tl"),
+                                           _ptr(bl, torch.int64, V, "bl"),
                                            _ptr(makespan, torch.int64, 1, "makespan")),
            "pardnn_tb_levels")
 
 
 def pardnn_critical_path(h, placement, tl, bl, makespan, is_critical, path, path_len):
+    V = _n_nodes(h)
     _check(load_library().pardnn_critical_path(
-        h, _ptr(placement, torch.int32, name="placement"), _ptr(tl, torch.int64, name="tl"),
-        _ptr(bl, torch.int64, name="bl"), _ptr(makespan, torch.int64, 1, "makespan"),
-        _ptr(is_critical, torch.uint8, name="is_critical"), _ptr(path, torch.int32, name="path"),
+        h, _ptr(placement, torch.int32, V, "placement"), _ptr(tl, torch.int64, V, "tl"),
+        _ptr(bl, torch.int64, V, "bl"), _ptr(makespan, torch.int64, 1, "makespan"),
+        _ptr(is_critical, torch.uint8, V, "is_critical"), _ptr(path, torch.int32, V, "path"),
         _ptr(path_len, torch.int32, 1, "path_len")), "pardnn_critical_path")
 
 
 def pardnn_label_memory(h, placement, n_labels, capacity, label_mem, overflow=None):
     _check(load_library().pardnn_label_memory(
-        h, _ptr(placement, torch.int32, name="placement"), n_labels,
+        h, _ptr(placement, torch.int32, _n_nodes(h), "placement"), n_labels,
         _ptr(capacity, torch.int64, n_labels, "capacity"),
         _ptr(label_mem, torch.int64, n_labels, "label_mem"),
         _ptr(overflow, torch.int64, n_labels, "overflow")), "pardnn_label_memory")
@@ -236,30 +242,40 @@ def pardnn_tb_levels_batch(h, n_place, placements, tl, bl, makespan):
 
 def pardnn_memory_balance(h, n_place, placements, node_type, ref_target, n_labels, res_mem,
                           nor_mem, balanced, ref_misplaced):
+    V, PK = _n_nodes(h), max(n_place, 0) * max(n_labels, 0)
     _check(load_library().pardnn_memory_balance(
-        h, n_place, _ptr(placements, torch.int32), _ptr(node_type, torch.int32),
-        _ptr(ref_target, torch.int32), n_labels, _ptr(res_mem, torch.int64),
-        _ptr(nor_mem, torch.int64), _ptr(balanced, torch.uint8),
-        _ptr(ref_misplaced, torch.int64)), "pardnn_memory_balance")
+        h, n_place, _ptr(placements, torch.int32, V * max(n_place, 0), "placements"),
+        _ptr(node_type, torch.int32, V, "node_type"), _ptr(ref_target, torch.int32, V, "ref_target"),
+        n_labels, _ptr(res_mem, torch.int64, PK, "res_mem"), _ptr(nor_mem, torch.int64, PK, "nor_mem"),
+        _ptr(balanced, torch.uint8, PK, "balanced"),
+        _ptr(ref_misplaced, torch.int64, max(n_place, 0), "ref_misplaced")), "pardnn_memory_balance")
 
 
 def pardnn_slice_primaries(h, K, primary, paths, path_stride, path_len, makespan):
+    Kn = max(K, 0)
     _check(load_library().pardnn_slice_primaries(
-        h, K, _ptr(primary, torch.int32), _ptr(paths, torch.int32), path_stride,
-        _ptr(path_len, torch.int32), _ptr(makespan, torch.int64)), "pardnn_slice_primaries")
+        h, K, _ptr(primary, torch.int32, _n_nodes(h), "primary"),
+        _ptr(paths, torch.int32, Kn * max(path_stride, 0), "paths"), path_stride,
+        _ptr(path_len, torch.int32, Kn, "path_len"), _ptr(makespan, torch.int64, Kn, "makespan")),
+        "pardnn_slice_primaries")
 
 
 def pardnn_cluster_criticality(h, cluster, n_clusters, criticality, order):
+    C = max(n_clusters, 0)
     _check(load_library().pardnn_cluster_criticality(
-        h, _ptr(cluster, torch.int32), n_clusters, _ptr(criticality, torch.int64),
-        _ptr(order, torch.int32)), "pardnn_cluster_criticality")
+        h, _ptr(cluster, torch.int32, _n_nodes(h), "cluster"), n_clusters,
+        _ptr(criticality, torch.int64, C, "criticality"), _ptr(order, torch.int32, C, "order")),
+        "pardnn_cluster_criticality")
 
 
 def pardnn_span_work(h, label, K, cluster, n_clusters, tl, span_lo, span_hi, work, comm, choice):
+    V, C = _n_nodes(h), max(n_clusters, 0)
+    CK = C * max(K, 0)
     _check(load_library().pardnn_span_work(
-        h, _ptr(label, torch.int32), K, _ptr(cluster, torch.int32), n_clusters,
-        _ptr(tl, torch.int64), _ptr(span_lo, torch.int64), _ptr(span_hi, torch.int64),
-        _ptr(work, torch.int64), _ptr(comm, torch.int64), _ptr(choice, torch.int32)),
+        h, _ptr(label, torch.int32, V, "label"), K, _ptr(cluster, torch.int32, V, "cluster"),
+        n_clusters, _ptr(tl, torch.int64, V, "tl"), _ptr(span_lo, torch.int64, C, "span_lo"),
+        _ptr(span_hi, torch.int64, C, "span_hi"), _ptr(work, torch.int64, CK, "work"),
+        _ptr(comm, torch.int64, CK, "comm"), _ptr(choice, torch.int32, C, "choice")),
         "pardnn_span_work")
 
 

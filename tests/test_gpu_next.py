@@ -468,3 +468,29 @@ def test_next_rows_on_empty_and_single_node_graphs(P):
             k = int(out["path_len"][j])
             assert out["paths"][j, :k].cpu().numpy().tolist() == paths[j].tolist()
         G.close()
+
+
+def test_binding_rejects_short_buffers(P):
+    """The binding checks buffer sizes before the C call, so a short output
+    never reaches a kernel."""
+    say("binding: short buffers")
+    rng = np.random.default_rng(804)
+    g = W.random_dag(rng, 50, p_edge=0.1, max_weight=5, n_labels=2)
+    G = P.Graph(g.n_nodes, g.src, g.dst, g.comp, g.edge_cost, g.mem)
+    lab = dev(np.zeros(g.n_nodes, np.int32), torch.int32)
+    short64 = torch.empty(g.n_nodes - 1, dtype=torch.int64, device="cuda")
+    ok64 = torch.empty(g.n_nodes, dtype=torch.int64, device="cuda")
+    m = torch.empty(1, dtype=torch.int64, device="cuda")
+    with pytest.raises(ValueError):
+        P.pardnn_tb_levels(G.handle, lab, short64, ok64, m)
+    with pytest.raises(ValueError):
+        P.pardnn_span_work(G.handle, lab, 2, lab, 3, ok64, torch.empty(3, dtype=torch.int64,
+                           device="cuda"), torch.empty(3, dtype=torch.int64, device="cuda"),
+                           torch.empty(5, dtype=torch.int64, device="cuda"),
+                           torch.empty(6, dtype=torch.int64, device="cuda"),
+                           torch.empty(3, dtype=torch.int32, device="cuda"))
+    with pytest.raises(ValueError):
+        P.pardnn_cluster_criticality(G.handle, lab, 4, torch.empty(3, dtype=torch.int64,
+                                     device="cuda"), torch.empty(4, dtype=torch.int32,
+                                                                 device="cuda"))
+    G.close()
