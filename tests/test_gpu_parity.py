@@ -424,6 +424,35 @@ def test_batch_any_int32_labels(P, seed):
     G.close()
 
 
+@pytest.mark.parametrize("K", [3000, 70000])
+def test_batch_many_labels(P, K):
+    """Label sums with many labels: 3,000 labels keep packed keys but sum by
+    global atomics (more than the LDS bins hold); 70,000 labels no longer pack
+    into 16 bits, so the batch keeps {value, label} pairs."""
+    say(f"batch with K={K} labels")
+    rng = np.random.default_rng(K)
+    g = W.random_dag(rng, 900, p_edge=0.01, max_weight=9, n_labels=1)
+    n_place = 5
+    pl = rng.integers(0, K, (g.n_nodes, n_place)).astype(np.int32)
+    pl[:, 1] = rng.integers(0, 3, g.n_nodes)      # a few labels in use, many idle
+    cap = rng.integers(0, 2000, K).astype(np.int64)
+    G = P.Graph(g.n_nodes, g.src, g.dst, g.comp, g.edge_cost, g.mem)
+    out = G.evaluate_batch(dev(pl, torch.int32), K, dev(cap, torch.int64))
+    torch.cuda.synchronize()
+    out = {k: v.cpu().numpy() for k, v in out.items()}
+    G.close()
+    for p in range(n_place):
+        exp = oracle.evaluate(g.n_nodes, g.src, g.dst, g.comp, g.edge_cost, g.mem,
+                              pl[:, p].copy(), K, cap)
+        assert (out["tl"][:, p] == exp["tl"]).all(), p
+        assert (out["bl"][:, p] == exp["bl"]).all(), p
+        assert out["makespan"][p] == exp["makespan"], p
+        assert (out["is_critical"][:, p] == exp["is_critical"]).all(), p
+        assert (out["path"][p, : out["path_len"][p]] == exp["path"]).all(), p
+        assert (out["label_mem"][p] == exp["label_mem"]).all(), p
+        assert (out["overflow"][p] == exp["overflow"]).all(), p
+
+
 def test_evaluate_moves_small(P):
     """The fused moves entry point equals build_placements + evaluate_batch
     and the oracle, with repeated nodes, an empty step and an odd count."""
