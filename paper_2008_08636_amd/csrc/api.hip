@@ -481,21 +481,20 @@ bool pair_single_bits(const Graph *g, int64_t n_labels, int64_t bound, int32_t *
     return true;
 }
 
-constexpr int64_t ps_ws_stride(int32_t V) {
-    return (((int64_t)V + kSlicePad) * kBatchSlots + 31) / 32 * 32;
-}
+// one placement per chain: workspace V + pad values, labels V
+constexpr int64_t ps_ws_stride(int32_t V) { return ((int64_t)V + kSlicePad + 31) / 32 * 32; }
+constexpr int64_t ps_lab_stride(int32_t V) { return ((int64_t)V + 63) / 64 * 64; }
 
-// labels (original ids) into the pair layout, slot 1 idle
+// labels (original ids) into the pair sweep's level-major layout
 int pair_single_labels(Graph *g, const int32_t *labels) {
     const int32_t V = g->V;
     if (!g->ps_ftl) {
         HIP_TRY(dalloc(*g, &g->ps_ftl, (size_t)ps_ws_stride(V)));
         HIP_TRY(dalloc(*g, &g->ps_bll, (size_t)ps_ws_stride(V)));
-        HIP_TRY(dalloc(*g, &g->ps_lab, ((size_t)V * kBatchSlots + 63) / 64 * 64));
+        HIP_TRY(dalloc(*g, &g->ps_lab, (size_t)ps_lab_stride(V)));
         HIP_TRY(dalloc(*g, &g->ps_gate, 1));
     }
-    HIP_TRY(launch_permute_labels_batch(*g, labels, 1, kBatchSlots, g->ps_lab,
-                                        ((int64_t)V * kBatchSlots + 63) / 64 * 64));
+    HIP_TRY(launch_permute_labels_batch(*g, labels, 1, 1, g->ps_lab, ps_lab_stride(V)));
     return PARDNN_OK;
 }
 
@@ -511,7 +510,7 @@ int pair_single_sweep(Graph *g, int32_t lb, int32_t ob, NodeRec16 *node_rec, int
     a.P = 1;
     a.K = 0;
     a.lab_w = g->ps_lab;
-    a.lab_stride = ((int64_t)g->V * kBatchSlots + 63) / 64 * 64;
+    a.lab_stride = ps_lab_stride(g->V);
     a.ftl = g->ps_ftl;
     a.bll = g->ps_bll;
     a.ws_stride = ps_ws_stride(g->V);
@@ -540,12 +539,12 @@ int pair_single_sweep(Graph *g, int32_t lb, int32_t ob, NodeRec16 *node_rec, int
     a.gate = gate;
     a.gate_want = 1;
     if (timed) {
-        TimedLaunch t(g, "k_sweep_pair<2>");
-        HIP_TRY(launch_sweep_pair(a, g->stream));
+        TimedLaunch t(g, "k_sweep_pair<1>");
+        HIP_TRY(launch_sweep_pair_one(a, g->stream));
     } else {
-        HIP_TRY(launch_sweep_pair(a, g->stream));
+        HIP_TRY(launch_sweep_pair_one(a, g->stream));
     }
-    HIP_TRY(launch_finish(a, kBatchSlots, nullptr, nullptr, nullptr, 0, nullptr, g->stream));
+    HIP_TRY(launch_finish(a, 1, nullptr, nullptr, nullptr, 0, nullptr, g->stream));
     return PARDNN_OK;
 }
 
@@ -734,7 +733,7 @@ int pardnn_tb_levels(pardnn_graph *h, const int32_t *placement, int64_t *tl, int
     a.tl_out = tl;
     a.bl_out = bl;
     a.makespan = makespan;
-    TimedLaunch t(g, pair ? "k_sweep_pair<2> or k_sweep<1>" : "k_sweep<1>");
+    TimedLaunch t(g, pair ? "k_sweep_pair<1> or k_sweep<1>" : "k_sweep<1>");
     if (pair) {
         HIP_TRY(launch_label_fit(*g, placement, 1 << 16, g->ps_gate));
         st = pair_single_sweep(g, lb, ob, g->node_rec, g->comp_lm, tl, bl, makespan, g->ps_gate,

@@ -165,6 +165,9 @@ hipError_t launch_pre_split(const Graph &g, bool fwd, const int32_t *rank, int32
                             PreRec16 *pre, int32_t *pretie);
 // Packed {value, label} only (a.lb > 0).
 hipError_t launch_sweep_pair(const SweepArgs &a, hipStream_t s);
+// The same with one placement per chain (workspace [P][V + pad], labels
+// [P][V]), no label sums.
+hipError_t launch_sweep_pair_one(const SweepArgs &a, hipStream_t s);
 
 // ---- critpath.hip ----
 // tight successors and critical flags of one placement (comp_lm: the node

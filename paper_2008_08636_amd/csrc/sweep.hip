@@ -849,12 +849,15 @@ hipError_t launch_sweep(const SweepArgs &a, int32_t S, hipStream_t s) {
 hipError_t launch_finish(const SweepArgs &a, int32_t S, uint8_t *crit, uint32_t *cbits,
                          int32_t *path, int32_t stride, int32_t *path_len, hipStream_t s) {
     if (a.P == 0) return hipSuccess;
-    if (S != kBatchSlots) return hipErrorInvalidValue;
+    // S = 1: outputs only (one placement from the pair sweep), no path
+    if (S != kBatchSlots && !(S == 1 && path == nullptr && a.lb > 0)) return hipErrorInvalidValue;
     if (path != nullptr && cbits == nullptr) return hipErrorInvalidValue;
     if (a.V > 0) {
         const unsigned blocks = (unsigned)((a.V + kEmitNodes - 1) / kEmitNodes);
         uint32_t *bits = path != nullptr ? cbits : nullptr;
-        if (a.lb > 0)
+        if (S == 1)
+            k_emit<1, true><<<blocks, 256, 0, s>>>(a, crit, bits);
+        else if (a.lb > 0)
             k_emit<kBatchSlots, true><<<blocks, 256, 0, s>>>(a, crit, bits);
         else
             k_emit<kBatchSlots, false><<<blocks, 256, 0, s>>>(a, crit, bits);

@@ -729,8 +729,8 @@ hipError_t launch_pair_split(const Graph &g, bool fwd, const int32_t *near_rank,
     return hipGetLastError();
 }
 
-hipError_t launch_sweep_pair(const SweepArgs &a, hipStream_t s) {
-    constexpr int S = kBatchSlots;
+template <int S>
+hipError_t launch_pair(const SweepArgs &a, hipStream_t s) {
     const int32_t n_slices = (a.P + S - 1) / S;
     if (n_slices == 0) return hipSuccess;
     if (a.lb <= 0) return hipErrorInvalidValue;
@@ -743,6 +743,17 @@ hipError_t launch_sweep_pair(const SweepArgs &a, hipStream_t s) {
     else
         k_sweep_pair<S, kBinsGlobal><<<2 * n_slices, 2 * kLanes, lds, s>>>(a);
     return hipGetLastError();
+}
+
+hipError_t launch_sweep_pair(const SweepArgs &a, hipStream_t s) {
+    return launch_pair<kBatchSlots>(a, s);
+}
+
+// One placement per chain: for a single placement (no label sums) the chain
+// carries one value per node, which shortens its per-level step.
+hipError_t launch_sweep_pair_one(const SweepArgs &a, hipStream_t s) {
+    if (a.K > 0) return hipErrorInvalidValue;
+    return launch_pair<1>(a, s);
 }
 
 }  // namespace pardnn
