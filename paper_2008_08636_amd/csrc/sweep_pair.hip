@@ -48,7 +48,7 @@ constexpr int kPNodes = 64;          // nodes of a fast level, one per lane of w
 constexpr int kNEn = 2;              // span-1 edge tasks per lane of wave 0
 constexpr int kNEf = 3;              // longer-edge tasks per lane of wave 1
 constexpr int kD = 3;                // far values loaded D levels ahead
-constexpr int kRF = 2;               // far records loaded RF levels before their values
+constexpr int kRF = 3;               // far records loaded RF levels before their values
 constexpr int kNS = kD + kRF + 2;    // register sets in flight (loop unrolling)
 constexpr int kLN = kNS - 2;         // wave 0 loads LN levels ahead
 constexpr int kRS = kD + 1;          // LDS ring slots (levels)
