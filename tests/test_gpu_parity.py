@@ -5,6 +5,7 @@ come from the seeded generators in ``workloads``; expected values come only
 from ``oracle``. Each case prints its name before touching the GPU.
 """
 import functools
+import os
 import sys
 
 import numpy as np
@@ -523,3 +524,50 @@ def test_c4_refinement_loop_full_size(P):
     total_mem = int(g.mem.sum())
     assert bool((out["label_mem"].sum(dim=1) == total_mem).all())
     G.close()
+
+
+# Every placement of the refinement loop against the oracle, through per-
+# placement checksums of tl, bl and the path (int64 sums, taken modulo 2^64 on
+# both sides, so the order of summation does not matter) and the exact
+# makespan, label sums and overflows. The oracle
+# (C, called through ctypes, which releases the GIL) runs on host threads.
+def _c4_oracle(g, sched, w, p):
+    lab = W.materialize_placements(sched, p, 1)[0]
+    e = oracle.evaluate(g.n_nodes, g.src, g.dst, g.comp, g.edge_cost, g.mem, lab, g.n_labels,
+                        g.capacity)
+    path = np.asarray(e["path"], np.int64)
+    return (p, int((e["tl"] * w).sum()), int((e["bl"] * w).sum()), int(e["makespan"]),
+            int(path.size), int((path * np.arange(1, path.size + 1)).sum()),
+            np.asarray(e["label_mem"]).tolist(), np.asarray(e["overflow"]).tolist())
+
+
+def test_c4_every_placement(P):
+    g = cfg(2)
+    say(f"config4 every placement V={g.n_nodes} P=1000")
+    sched = W.config4_moves(g, n_place=1000)
+    G = P.Graph(g.n_nodes, g.src, g.dst, g.comp, g.edge_cost, g.mem)
+    margs = (dev(sched.base, torch.int32), dev(sched.ptr, torch.int64),
+             dev(sched.node, torch.int32), dev(sched.label, torch.int32))
+    out = G.evaluate_moves(*margs, g.n_labels, dev(g.capacity, torch.int64))
+    torch.cuda.synchronize()
+    # node v weighs v + 1 in the checksums; tl, bl are [V][P] in original ids
+    w = torch.arange(1, g.n_nodes + 1, dtype=torch.int64, device="cuda").unsqueeze(1)
+    tl_sum = torch.cat([(out["tl"][:, c:c + 100] * w).sum(dim=0) for c in range(0, 1000, 100)])
+    bl_sum = torch.cat([(out["bl"][:, c:c + 100] * w).sum(dim=0) for c in range(0, 1000, 100)])
+    plen = out["path_len"].to(torch.int64)
+    stride = out["path"].shape[1]
+    pos = torch.arange(1, stride + 1, dtype=torch.int64, device="cuda")
+    mask = pos.unsqueeze(0) <= plen.unsqueeze(1)
+    path_sum = ((out["path"].to(torch.int64) * pos) * mask).sum(dim=1)
+    got = {k: v.cpu().numpy() for k, v in
+           dict(tl=tl_sum, bl=bl_sum, m=out["makespan"], plen=plen, path=path_sum,
+                lm=out["label_mem"], ov=out["overflow"]).items()}
+    G.close()
+    from concurrent.futures import ThreadPoolExecutor
+    wn = np.arange(1, g.n_nodes + 1, dtype=np.int64)
+    with ThreadPoolExecutor(max(1, min(16, os.cpu_count() or 1))) as ex:
+        res = list(ex.map(lambda p: _c4_oracle(g, sched, wn, p), range(1000)))
+    for p, t, b, m, n, ps, lm, ov in res:
+        assert got["tl"][p] == t and got["bl"][p] == b, p
+        assert got["m"][p] == m and got["plen"][p] == n and got["path"][p] == ps, p
+        assert got["lm"][p].tolist() == lm and got["ov"][p].tolist() == ov, p
