@@ -213,7 +213,10 @@ int pardnn_build_placements(pardnn_graph *g, const int32_t *base,
  *   placements     int32[n_nodes][n_place].
  *   n_labels, capacity  as for pardnn_label_memory (n_labels is ignored when
  *                  label_mem is NULL).
- *   tl, bl         int64[n_nodes][n_place] outputs.
+ *   tl, bl         int64[n_nodes][n_place] outputs, each or both NULL: the
+ *                  levels are still computed (they decide everything else)
+ *                  but not written out, for callers that keep only the
+ *                  per-placement results.
  *   makespan       int64[n_place] output.
  *   is_critical    uint8[n_nodes][n_place] output or NULL.
  *   path           int32[n_place][path_stride] output or NULL: row p holds

@@ -367,16 +367,15 @@ class Graph:
         pardnn_build_placements(self._h, base, n_place, step_ptr, node, label, out)
         return out
 
-    def _outputs(self, P, n_labels, crit, path, labels):
+    def _outputs(self, P, n_labels, crit, path, labels, values=True):
         V, dev = self.n_nodes, self.device
         L = self.info()["n_levels"]
         if L < 0:
             L = pardnn_levelize(self._h)
-        out = {
-            "tl": torch.empty((V, P), dtype=torch.int64, device=dev),
-            "bl": torch.empty((V, P), dtype=torch.int64, device=dev),
-            "makespan": torch.empty(P, dtype=torch.int64, device=dev),
-        }
+        out = {"makespan": torch.empty(P, dtype=torch.int64, device=dev)}
+        if values:
+            out["tl"] = torch.empty((V, P), dtype=torch.int64, device=dev)
+            out["bl"] = torch.empty((V, P), dtype=torch.int64, device=dev)
         if crit:
             out["is_critical"] = torch.empty((V, P), dtype=torch.uint8, device=dev)
         if path:
@@ -388,13 +387,14 @@ class Graph:
         return out, max(L, 1)
 
     def evaluate_moves(self, base, step_ptr, node, label, n_labels=0, capacity=None, crit=True,
-                       path=True, labels=True):
+                       path=True, labels=True, values=True):
         """All outputs for the successive placements base + moves (see
-        pardnn_evaluate_moves); arrays are placement-minor [V][P]."""
+        pardnn_evaluate_moves); arrays are placement-minor [V][P]. values=False
+        leaves out the per-node tl / bl."""
         P = step_ptr.numel() - 1
-        out, stride = self._outputs(P, n_labels, crit, path, labels)
+        out, stride = self._outputs(P, n_labels, crit, path, labels, values)
         pardnn_evaluate_moves(self._h, base, P, step_ptr, node, label,
-                              n_labels if labels else 0, capacity, out["tl"], out["bl"],
+                              n_labels if labels else 0, capacity, out.get("tl"), out.get("bl"),
                               out["makespan"], out.get("is_critical"), out.get("path"), stride,
                               out.get("path_len"), out.get("label_mem"), out.get("overflow"))
         return out

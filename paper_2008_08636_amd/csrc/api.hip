@@ -307,9 +307,8 @@ int evaluate_impl(Graph *g, int32_t n_place, const int32_t *placements, const Mo
                   int32_t *path_len, int64_t *label_mem, int64_t *overflow) {
     if (n_place < 0) return fail(PARDNN_E_INVAL, "n_place must be >= 0");
     if (n_place == 0) return PARDNN_OK;
-    if (makespan == nullptr ||
-        (g->V > 0 && ((placements == nullptr && mv == nullptr) || tl == nullptr || bl == nullptr)))
-        return fail(PARDNN_E_INVAL, "placements, tl, bl and makespan must be non-null");
+    if (makespan == nullptr || (g->V > 0 && placements == nullptr && mv == nullptr))
+        return fail(PARDNN_E_INVAL, "placements and makespan must be non-null");
     if ((path == nullptr) != (path_len == nullptr))
         return fail(PARDNN_E_INVAL, "path and path_len must both be given or both be null");
     if (label_mem == nullptr && overflow != nullptr)

@@ -581,8 +581,8 @@ __device__ void emit_rows(const SweepArgs &a, uint8_t *crit, uint32_t *cbits, in
                 if (v0 + r < V) {
                     const int64_t o = (int64_t)s_ord[r] * P + p;
                     const int64_t t = t_tl[r][col], b = t_bl[r][col];
-                    a.tl_out[o] = t;
-                    a.bl_out[o] = b;
+                    if (a.tl_out) a.tl_out[o] = t;   // optional outputs
+                    if (a.bl_out) a.bl_out[o] = b;
                     const bool c = t + b == m;
                     if (crit) crit[o] = (uint8_t)c;
                     bits |= (BW)c << r;

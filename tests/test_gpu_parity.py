@@ -454,6 +454,27 @@ def test_batch_many_labels(P, K):
         assert (out["overflow"][p] == exp["overflow"]).all(), p
 
 
+def test_evaluate_moves_without_values(P):
+    """tl / bl may be left out: every other output is unchanged."""
+    g = cfg(1)
+    say("evaluate_moves without tl / bl")
+    sched = W.config4_moves(g, n_place=37)
+    G = P.Graph(g.n_nodes, g.src, g.dst, g.comp, g.edge_cost, g.mem)
+    margs = (dev(sched.base, torch.int32), dev(sched.ptr, torch.int64),
+             dev(sched.node, torch.int32), dev(sched.label, torch.int32))
+    cap = dev(g.capacity, torch.int64)
+    full = G.evaluate_moves(*margs, g.n_labels, cap)
+    lean = G.evaluate_moves(*margs, g.n_labels, cap, values=False)
+    torch.cuda.synchronize()
+    assert "tl" not in lean and "bl" not in lean
+    for k in ("makespan", "is_critical", "path_len", "label_mem", "overflow"):
+        assert torch.equal(full[k], lean[k]), k
+    for p in range(37):
+        n = int(full["path_len"][p])
+        assert torch.equal(full["path"][p, :n], lean["path"][p, :n]), p
+    G.close()
+
+
 def test_evaluate_moves_small(P):
     """The fused moves entry point equals build_placements + evaluate_batch
     and the oracle, with repeated nodes, an empty step and an odd count."""
