@@ -555,8 +555,13 @@ __device__ void emit_rows(const SweepArgs &a, uint8_t *crit, uint32_t *cbits, in
             const int sl = i / (TV * S), r = (i % (TV * S)) / S, s2 = i % S;
             const int64_t idx = (int64_t)min(sl0 + sl, n_slices - 1) * a.ws_stride +
                                 (int64_t)min(v0 + r, V - 1) * S + s2;
-            fv[j] = ft[idx];
-            bv[j] = bl[idx];
+            if constexpr (PACKED) {   // read once: no need to keep the lines
+                fv[j] = __builtin_nontemporal_load(&ft[idx]);
+                bv[j] = __builtin_nontemporal_load(&bl[idx]);
+            } else {
+                fv[j] = ft[idx];
+                bv[j] = bl[idx];
+            }
         }
     };
     load(0);
@@ -581,8 +586,11 @@ __device__ void emit_rows(const SweepArgs &a, uint8_t *crit, uint32_t *cbits, in
                 if (v0 + r < V) {
                     const int64_t o = (int64_t)s_ord[r] * P + p;
                     const int64_t t = t_tl[r][col], b = t_bl[r][col];
-                    if (a.tl_out) a.tl_out[o] = t;   // optional outputs
-                    if (a.bl_out) a.bl_out[o] = b;
+                    // optional outputs, written once and streamed past the
+                    // caches; the byte flags stay ordinary stores so that
+                    // their partial lines merge in L2
+                    if (a.tl_out) __builtin_nontemporal_store(t, &a.tl_out[o]);
+                    if (a.bl_out) __builtin_nontemporal_store(b, &a.bl_out[o]);
                     const bool c = t + b == m;
                     if (crit) crit[o] = (uint8_t)c;
                     bits |= (BW)c << r;
