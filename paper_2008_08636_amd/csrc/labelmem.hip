@@ -13,6 +13,8 @@
 // placements marks each (node, step) with its last move index (atomicMax keeps
 // the latest move deterministic) and then forward-fills every placement-minor
 // row with one wave, a 64-lane max-scan per chunk of steps.
+#include <type_traits>
+
 #include "device_utils.h"
 #include "internal.h"
 
@@ -27,6 +29,12 @@ constexpr int kLdsBins = 4096;
 template <int S>
 struct alignas(4 * S) LabPack {
     int32_t v[S];
+    // the same bytes as one scalar or vector word, for non-temporal stores
+    using Word = typename std::conditional<
+        S == 1, int32_t,
+        typename std::conditional<S == 2, long long,
+                                  int __attribute__((ext_vector_type(4)))>::type>::type;
+    static_assert(S == 1 || S == 2 || S == 4, "one, two or four slots per slice");
 };
 
 inline unsigned grid_for(int64_t n, int block, int cap = 65536) {
@@ -288,8 +296,12 @@ __global__ __launch_bounds__(256) void k_moves_to_slices(int32_t V, int32_t P,
                     if (K > 0 && (x.v[s2] < 0 || x.v[s2] >= K) && c0 + sl * S + s2 < P)
                         atomicOr(err, 1);
                 }
-                *reinterpret_cast<LabPack<S> *>(lab_w + (int64_t)(sl0 + sl) * lab_stride +
-                                                (int64_t)v * S) = x;
+                // streamed: the sweep reads these long after, and dirty
+                // lines left in L2 would be written back during the sweep
+                using W = typename LabPack<S>::Word;
+                __builtin_nontemporal_store(
+                    *reinterpret_cast<const W *>(&x),
+                    reinterpret_cast<W *>(lab_w + (int64_t)(sl0 + sl) * lab_stride + (int64_t)v * S));
             }
         }
         __syncthreads();

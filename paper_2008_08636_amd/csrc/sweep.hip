@@ -76,7 +76,9 @@ __global__ __launch_bounds__(256) void k_permute_labels(int32_t V, int32_t P,
         const int rem = i % (TV * S);
         const int r = rem / S, s = rem % S;
         const int32_t v = v0 + r;
-        if (v < V) lab_w[(int64_t)(sl0 + sl) * lab_stride + (int64_t)v * S + s] = tile[r][sl * S + s];
+        if (v < V)   // streamed past L2, as the sweep reads it much later
+            __builtin_nontemporal_store(tile[r][sl * S + s],
+                                        &lab_w[(int64_t)(sl0 + sl) * lab_stride + (int64_t)v * S + s]);
     }
 }
 
