@@ -635,7 +635,7 @@ __device__ void chase_wave(const SweepArgs &a, const uint32_t *cbits, int32_t p,
                            int32_t stride, int32_t *path_len) {
     constexpr int RW = kChaseRegs;
     constexpr int WIN = RW * kWave;
-    constexpr int U = 8;   // independent iterations in flight
+    constexpr int U = 16;  // independent iterations in flight
     const int lane = lane_id();
     const int32_t V = a.V;
     const int32_t slice = p / S, s = p % S;
