@@ -15,6 +15,8 @@
 // row with one wave, a 64-lane max-scan per chunk of steps.
 #include <type_traits>
 
+#include <rocprim/device/device_radix_sort.hpp>
+
 #include "device_utils.h"
 #include "internal.h"
 
@@ -173,28 +175,46 @@ __global__ void k_bp_fill(int32_t V, int32_t P, const int32_t *base, const int32
     }
 }
 
-// Moves grouped by node (a counting sort): count per node, exclusive scan,
-// then scatter {step, move index, label} into the node's range. The order
-// inside a range is arbitrary; the consumer takes the latest move.
-__global__ void k_mv_count(int64_t M, const int32_t *node, int32_t V, int32_t *cnt,
-                           int32_t *err) {
+// Moves grouped by node: one stable radix sort of the node ids over the move
+// indices, so that each node's moves lie together in move order, with no
+// per-node atomics and no counting pass. An id outside [0, V) is flagged and sorted
+// past every node as V. Each node's range comes from a binary search of the
+// sorted ids; the entries {step, move index, label} are gathered in sorted
+// order.
+__global__ void k_mv_keys(int64_t M, const int32_t *node, int32_t V, uint32_t *key, int32_t *idx,
+                          int32_t *err) {
     for (int64_t m = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; m < M;
          m += (int64_t)gridDim.x * blockDim.x) {
         const int32_t v = node[m];
-        if (v < 0 || v >= V)
-            atomicOr(err, 1);
-        else
-            atomicAdd(&cnt[v], 1);
+        const bool bad = v < 0 || v >= V;
+        if (bad) atomicOr(err, 1);
+        key[m] = bad ? (uint32_t)V : (uint32_t)v;
+        idx[m] = (int32_t)m;
     }
 }
 
-__global__ void k_mv_scatter(int64_t M, int32_t P, const int64_t *step_ptr, const int32_t *node,
-                             const int32_t *label, int32_t V, const int32_t *off, int32_t *cur,
-                             int4 *ent) {
-    for (int64_t m = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; m < M;
-         m += (int64_t)gridDim.x * blockDim.x) {
-        const int32_t v = node[m];
-        if (v < 0 || v >= V) continue;
+// off[v] = first sorted position with id >= v, for v in [0, V]
+__global__ void k_mv_off(int32_t V, int64_t M, const uint32_t *key, int32_t *off) {
+    for (int64_t v = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; v <= V;
+         v += (int64_t)gridDim.x * blockDim.x) {
+        int64_t lo = 0, hi = M;   // answer in [lo, hi]
+        while (lo < hi) {
+            const int64_t mid = (lo + hi) >> 1;
+            if (key[mid] < (uint32_t)v)
+                lo = mid + 1;
+            else
+                hi = mid;
+        }
+        off[v] = (int32_t)lo;
+    }
+}
+
+__global__ void k_mv_gather(int64_t M, int32_t P, const int64_t *step_ptr, const uint32_t *key,
+                            const int32_t *idx, const int32_t *label, int32_t V, int4 *ent) {
+    for (int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; i < M;
+         i += (int64_t)gridDim.x * blockDim.x) {
+        if (key[i] >= (uint32_t)V) continue;
+        const int32_t m = idx[i];
         // step of move m: largest p with step_ptr[p] <= m
         int32_t lo = 0, hi = P;
         while (hi - lo > 1) {
@@ -204,7 +224,7 @@ __global__ void k_mv_scatter(int64_t M, int32_t P, const int64_t *step_ptr, cons
             else
                 hi = mid;
         }
-        ent[off[v] + atomicAdd(&cur[v], 1)] = make_int4(lo, (int32_t)m, label[m], 0);
+        ent[i] = make_int4(lo, m, label[m], 0);
     }
 }
 
@@ -310,10 +330,32 @@ __global__ __launch_bounds__(256) void k_moves_to_slices(int32_t V, int32_t P,
 
 }  // namespace
 
+namespace {
+
+// sorted id bits: ids run over [0, V] (V marks an invalid id)
+unsigned mv_key_bits(int32_t V) {
+    unsigned bits = 1;
+    while (bits < 32 && ((uint32_t)V >> bits) != 0) bits++;
+    return bits;
+}
+
+size_t mv_sort_temp_bytes(int32_t V, int64_t M) {
+    size_t temp = 0;
+    (void)rocprim::radix_sort_pairs(nullptr, temp, (const uint32_t *)nullptr, (uint32_t *)nullptr,
+                                    (const int32_t *)nullptr, (int32_t *)nullptr, (size_t)M, 0u,
+                                    mv_key_bits(V));
+    return temp;
+}
+
+constexpr size_t al64(size_t n) { return (n + 63) / 64 * 64; }   // int32 elements, 256 B
+
+}  // namespace
+
 size_t moves_scratch_elems(int32_t V, int64_t M) {
-    // cnt [V + 1], off [V + 1], scan workspace, then 16-byte aligned int4 entries
-    const size_t head = 2 * ((size_t)V + 1) + scan_workspace_elems(V);
-    return (head + 3) / 4 * 4 + 4 * (size_t)M;
+    // off [V + 1], ids and move indices before and after the sort [M] each,
+    // the entries (int4) [M], the sort's temporary storage; 256-byte aligned
+    return al64((size_t)V + 1) + 4 * al64((size_t)M) + 4 * al64((size_t)M) +
+           al64((mv_sort_temp_bytes(V, M) + 3) / 4);
 }
 
 hipError_t launch_moves_to_slices(const Graph &g, const int32_t *base, int32_t P,
@@ -322,19 +364,31 @@ hipError_t launch_moves_to_slices(const Graph &g, const int32_t *base, int32_t P
                                   int32_t *lab_w, int64_t lab_stride, int32_t K, int32_t *err) {
     if (g.V == 0 || P == 0) return hipSuccess;
     const int32_t V = g.V;
-    int32_t *cnt = scratch, *off = scratch + (V + 1), *ws = off + (V + 1);
-    const size_t head = 2 * ((size_t)V + 1) + scan_workspace_elems(V);
-    int4 *ent = reinterpret_cast<int4 *>(scratch + (head + 3) / 4 * 4);
-    hipError_t e = launch_fill_i32(cnt, (int64_t)V + 1, 0, g.stream);
-    if (e == hipSuccess && M > 0) {
-        k_mv_count<<<grid_for(M, kBlock), kBlock, 0, g.stream>>>(M, node, V, cnt, err);
+    const size_t m64 = al64((size_t)M);
+    int32_t *off = scratch;
+    uint32_t *key_in = reinterpret_cast<uint32_t *>(off + al64((size_t)V + 1));
+    uint32_t *key_out = key_in + m64;
+    int32_t *idx_in = reinterpret_cast<int32_t *>(key_out + m64);
+    int32_t *idx_out = idx_in + m64;
+    int4 *ent = reinterpret_cast<int4 *>(idx_out + m64);
+    void *temp = reinterpret_cast<int32_t *>(ent) + 4 * m64;
+    hipError_t e = hipSuccess;
+    if (M > 0) {
+        k_mv_keys<<<grid_for(M, kBlock), kBlock, 0, g.stream>>>(M, node, V, key_in, idx_in, err);
+        e = hipGetLastError();
+        size_t temp_bytes = mv_sort_temp_bytes(V, M);
+        if (e == hipSuccess)
+            e = rocprim::radix_sort_pairs(temp, temp_bytes, (const uint32_t *)key_in, key_out,
+                                          (const int32_t *)idx_in, idx_out, (size_t)M, 0u,
+                                          mv_key_bits(V), g.stream);
+    }
+    if (e == hipSuccess) {
+        k_mv_off<<<grid_for((int64_t)V + 1, kBlock), kBlock, 0, g.stream>>>(V, M, key_out, off);
         e = hipGetLastError();
     }
-    if (e == hipSuccess) e = launch_exclusive_scan(cnt, off, V, ws, g.stream);
-    if (e == hipSuccess && M > 0) e = launch_fill_i32(cnt, (int64_t)V + 1, 0, g.stream);
     if (e == hipSuccess && M > 0) {
-        k_mv_scatter<<<grid_for(M, kBlock), kBlock, 0, g.stream>>>(M, P, step_ptr, node, label,
-                                                                    V, off, cnt, ent);
+        k_mv_gather<<<grid_for(M, kBlock), kBlock, 0, g.stream>>>(M, P, step_ptr, key_out,
+                                                                   idx_out, label, V, ent);
         e = hipGetLastError();
     }
     if (e != hipSuccess) return e;

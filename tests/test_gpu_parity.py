@@ -509,6 +509,16 @@ def test_evaluate_moves_small(P):
         bad[3] = g.n_nodes + 7
         G.evaluate_moves(args[0], args[1], dev(bad, torch.int32), args[3], g.n_labels)
     assert e.value.status == P.E_INVAL
+    with pytest.raises(P.PardnnError) as e:
+        bad = node.copy()
+        bad[-1] = -2
+        G.evaluate_moves(args[0], args[1], dev(bad, torch.int32), args[3], g.n_labels)
+    assert e.value.status == P.E_INVAL
+    # still usable after the rejected calls
+    out2 = G.evaluate_moves(*args, g.n_labels, dev(g.capacity, torch.int64))
+    torch.cuda.synchronize()
+    for k in ref:
+        assert (ref[k] == out2[k].cpu().numpy()).all(), k
     G.close()
 
 
