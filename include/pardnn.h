@@ -103,8 +103,8 @@ int pardnn_set_stream(pardnn_graph *g, void *stream);
 int pardnn_get_info(const pardnn_graph *g, pardnn_info *info);
 
 /*
- * Topological levels by Kahn's algorithm (Sec. 3.1.1: computing weighted
- * levels is a variant of topological sorting, O(|V| + |E|); the per-level work
+ * Topological levels by Kahn's algorithm (Sec. 3.1.1: weighted levels come
+ * from one pass in topological order, O(|V| + |E|); the per-level work
  * tables of Sec. 3.1.2 are indexed by level). level(v) = 0 without
  * predecessors, else 1 + the largest level of its predecessors.
  *   level          int32[n_nodes] or NULL: level of each node.

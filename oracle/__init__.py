@@ -8,9 +8,9 @@ The arithmetic lives in ``pardnn_oracle.c`` (plain C, one thread); this module
 only marshals numpy arrays through ctypes. Each wrapper names the definition it
 follows in the paper (ParDNN, arXiv 2008.08636):
 
-* ``levelize``      -- hop levels by Kahn's algorithm (Sec. 3.1.1, the
-                        "variant of topological sorting"; levels index the
-                        per-level work tables of Sec. 3.1.2).
+* ``levelize``      -- hop levels by Kahn's algorithm (Sec. 3.1.1: weighted
+                        levels by a topological-order pass in O(V + E);
+                        levels index the per-level work tables of Sec. 3.1.2).
 * ``tb_levels``     -- tl, bl and the makespan (Table 2: tl, bl, w_lvl, CP).
 * ``critical_path`` -- critical nodes and the canonical critical path
                         (Table 2: CP; Alg. 1 find_heaviest_path on fresh

@@ -22,7 +22,7 @@
  *   - CP is the costliest path of the graph; its length is the makespan M.
  *   - Communication between two nodes on the same device label counts as
  *     zero (Fig. 2 caption; Sec. 3.1.2, cluster criticality).
- *   - compute_weighted_levels is a variant of topological sorting with cost
+ *   - compute_weighted_levels is one pass in topological order, costing
  *     O(|V| + |E|) (Sec. 3.1.1, complexity of Alg. 1).
  *
  * Readings where the paper is silent (each is also listed in the design

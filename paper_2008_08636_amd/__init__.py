@@ -21,8 +21,9 @@ __all__ = [
     "pardnn_levelize", "pardnn_tb_levels", "pardnn_critical_path", "pardnn_label_memory",
     "pardnn_apply_moves", "pardnn_build_placements", "pardnn_evaluate_batch",
     "pardnn_evaluate_moves",
-    "pardnn_tb_levels_batch", "pardnn_set_timing", "pardnn_get_timing",
-    "pardnn_status_string", "pardnn_last_error",
+    "pardnn_tb_levels_batch", "pardnn_memory_balance", "pardnn_slice_primaries",
+    "pardnn_cluster_criticality", "pardnn_span_work", "pardnn_set_timing",
+    "pardnn_get_timing", "pardnn_status_string", "pardnn_last_error",
 ]
 
 LIB_PATH = os.path.join(os.path.dirname(os.path.abspath(__file__)), "libpardnn.so")

@@ -54,19 +54,19 @@ __global__ void k_crit_flags(int32_t V, const int32_t *order, const int64_t *tl,
     }
 }
 
-// One thread per out-edge (level-major): a tight edge out of a critical node
-// offers its successor's original id; the smallest wins. Edge-parallel, so a
-// node with thousands of successors costs no more than as many edges.
+// One thread per out-edge (level-major): a tight edge offers its successor's
+// original id to its source; the smallest wins. Every node gets its next hop,
+// critical or not: the walk's definition steps along tight edges from any node
+// it reaches, which matters for tl / bl that no sweep produced. Edge-parallel,
+// so a node with thousands of successors costs no more than as many edges.
 __global__ void k_crit_tight(int64_t E, const int32_t *order, const int32_t *out_src,
                              const int32_t *out_dst_orig, const int64_t *out_cost,
                              const int64_t *comp_lm, const int32_t *placement, const int64_t *tl,
-                             const int64_t *bl, const int64_t *makespan, const uint8_t *crit_lm,
-                             int32_t *next_lm) {
+                             const int64_t *bl, const int64_t *makespan, int32_t *next_lm) {
     const int64_t M = *makespan;
     for (int64_t j = blockIdx.x * (int64_t)blockDim.x + threadIdx.x; j < E;
          j += (int64_t)gridDim.x * blockDim.x) {
         const int32_t v = out_src[j];
-        if (!crit_lm[v]) continue;   // a tight edge leaves a critical node only
         const int32_t ov = order[v], so = out_dst_orig[j];
         const int64_t c = placement[ov] != placement[so] ? out_cost[j] : 0;
         if (wadd(wadd(wadd(tl[ov], comp_lm[v]), c), bl[so]) == M) atomicMin(&next_lm[v], so);
@@ -191,7 +191,7 @@ hipError_t launch_crit_next(const Graph &g, const int32_t *placement, const int6
     if (g.E > 0) {
         k_crit_tight<<<grid_for(g.E, kBlock), kBlock, 0, g.stream>>>(
             g.E, g.order, g.out_src, g.out_dst_orig, g.out_cost, comp_lm, placement, tl, bl,
-            makespan, g.crit_lm, g.next_lm);
+            makespan, g.next_lm);
         if ((e = hipGetLastError()) != hipSuccess) return e;
     }
     k_crit_link<<<grid_for(g.V, kBlock), kBlock, 0, g.stream>>>(g.V, g.rank, g.next_lm);

@@ -1,8 +1,8 @@
 // levelize.hip -- topological levels by Kahn's algorithm in one persistent
 // workgroup.
 //
-// The paper computes weighted levels with "a variant of topological sorting"
-// in O(|V| + |E|) (Sec. 3.1.1, complexity of Alg. 1) and indexes per-level
+// The paper obtains weighted levels by a topological-order pass costing
+// O(|V| + |E|) (Sec. 3.1.1, complexity of Alg. 1) and indexes per-level
 // work by level (Sec. 3.1.2, Fenwick trees over levels). Here level(v) is the
 // Kahn frontier index: 0 without predecessors, else 1 + max over predecessors.
 //

@@ -174,6 +174,43 @@ def test_critical_path_arbitrary_inputs(P):
     G.close()
 
 
+def test_critical_path_walk_leaves_critical_set(P):
+    """Inconsistent tl / bl on which the walk passes a non-critical node: the
+    hand-derived 4-node case (path [0, 1, 3], node 1 not critical), then seeded
+    random DAGs with tl, bl drawn from a small range so that tight edges out of
+    non-critical nodes are common; expected values from the oracle."""
+    say("critical_path through non-critical nodes")
+    cases = [(4, [0, 1, 1], [1, 2, 3], [1] * 4, [0] * 3, [0] * 4, [0, 2, 2, 2], [3, 2, 1, 0], 3)]
+    rng = np.random.default_rng(77)
+    for t in range(120):
+        n = int(rng.integers(1, 48))
+        g = W.random_dag(rng, n, p_edge=float(rng.uniform(0.05, 0.4)),
+                         max_weight=int(rng.integers(0, 3)), n_labels=int(rng.integers(1, 3)))
+        tl = rng.integers(0, 5, n).astype(np.int64)
+        bl = rng.integers(0, 5, n).astype(np.int64)
+        m = int((tl + bl)[int(rng.integers(0, n))])
+        cases.append((n, g.src, g.dst, g.comp, g.edge_cost, g.placement, tl, bl, m))
+    walked_off = 0
+    for (n, src, dst, comp, cost, lab, tl, bl, m) in cases:
+        src = np.asarray(src, np.int32)
+        dst = np.asarray(dst, np.int32)
+        comp = np.asarray(comp, np.int64)
+        cost = np.asarray(cost, np.int64)
+        lab = np.asarray(lab, np.int32)
+        tl = np.asarray(tl, np.int64)
+        bl = np.asarray(bl, np.int64)
+        ecrit, epath = oracle.critical_path(n, src, dst, comp, cost, lab, tl, bl, m)
+        walked_off += int((ecrit[epath] == 0).any())
+        G = P.Graph(n, src, dst, comp, cost, np.zeros(n, np.int64))
+        crit, path, plen = G.critical_path(dev(lab, torch.int32), dev(tl, torch.int64),
+                                           dev(bl, torch.int64), dev([m], torch.int64))
+        torch.cuda.synchronize()
+        assert (crit.cpu().numpy() == ecrit).all()
+        assert path[: int(plen.item())].cpu().numpy().tolist() == epath.tolist()
+        G.close()
+    assert walked_off >= 10   # the cases do exercise the walk off the critical set
+
+
 def test_determinism_and_stream(P):
     say("determinism on a side stream")
     g = cfg(2)

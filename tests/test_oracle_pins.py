@@ -55,6 +55,24 @@ def test_golden(path, oracle_lib):
     assert sums.tolist() == x["label_mem"] and over.tolist() == x["overflow"]
 
 
+def test_walk_through_noncritical_node(oracle_lib):
+    """The path rule steps along tight edges from whatever node it reached,
+    critical or not (Table 2, CP; the walk of Sec. 3.1.1). Hand-derived:
+    edges 0->1, 1->2, 1->3, every comp 1, no cost. Consistent levels are
+    tl = [0, 1, 2, 2], bl = [3, 2, 1, 1], M = 3; raising tl(1) by one and
+    lowering bl(3) by one leaves node 1 off the critical set (w = 4) but keeps
+    0->1 (0 + 1 + 2 = 3) and 1->3 (2 + 1 + 0 = 3) tight, while 1->2 gives 4."""
+    src, dst = [0, 1, 1], [1, 2, 3]
+    comp, cost, lab = [1, 1, 1, 1], [0, 0, 0], [0, 0, 0, 0]
+    tl, bl, m = oracle.tb_levels(4, src, dst, comp, cost, lab)
+    assert tl.tolist() == [0, 1, 2, 2] and bl.tolist() == [3, 2, 1, 1] and m == 3
+    tl[1] += 1
+    bl[3] -= 1
+    crit, path = oracle.critical_path(4, src, dst, comp, cost, lab, tl, bl, m)
+    assert crit.tolist() == [1, 0, 1, 0]
+    assert path.tolist() == [0, 1, 3]
+
+
 # ----------------------------------------------------------- brute force --
 
 def _check_against_brute_force(g):
