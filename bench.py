@@ -111,34 +111,61 @@ def host_cpu_model() -> str:
     return "unknown"
 
 
-def cpu_baseline(g, sched, budget_s: float):
-    """The oracle as it stands, single-threaded, on the first placements of the
-    same refinement loop (bounded by `budget_s` seconds of CPU work)."""
-    import oracle
-    import workloads as W
+def start_cpu_baseline(mode: str, budget_s: float, config: int = 2, n_place: int = 1000):
+    """Start the oracle's timing (oracle/timing.py) as a child process pinned to
+    one core, before this process touches the GPU, and take that core out of
+    this process's own affinity so that the two do not share it. Returns the
+    child (or None when there is no core to spare)."""
+    import subprocess
 
-    oracle.build(force=False)
-    first = W.materialize_placements(sched, 0, 1)[0]
-    t0 = time.perf_counter()
-    oracle.evaluate(g.n_nodes, g.src, g.dst, g.comp, g.edge_cost, g.mem, first, g.n_labels,
-                    g.capacity)
-    t1 = time.perf_counter() - t0
-    n = max(1, min(sched.n_place, int(budget_s / max(t1, 1e-6))))
-    pls = W.materialize_placements(sched, 0, n)
-    t0 = time.perf_counter()
-    for p in range(n):
-        oracle.evaluate(g.n_nodes, g.src, g.dst, g.comp, g.edge_cost, g.mem, pls[p],
-                        g.n_labels, g.capacity)
-    dt = time.perf_counter() - t0
+    cores = sorted(os.sched_getaffinity(0))
+    if budget_s <= 0 or len(cores) < 2:
+        return None
+    core = cores[-1]
+    os.sched_setaffinity(0, set(cores[:-1]))
+    cmd = [sys.executable, "-m", "oracle.timing", "--mode", mode, "--config", str(config),
+           "--configs", "0,1,2", "--n-place", str(n_place), "--budget", str(budget_s),
+           "--core", str(core)]
+    return subprocess.Popen(cmd, cwd=ROOT, stdout=subprocess.PIPE, stderr=subprocess.PIPE,
+                            text=True)
+
+
+def finish_cpu_baseline(child, timeout_s: float):
+    """The child's JSON result, or None if it failed."""
+    if child is None:
+        return None
+    try:
+        out, err = child.communicate(timeout=timeout_s)
+    except Exception:
+        child.kill()
+        child.communicate()
+        print("[bench] CPU baseline timed out", file=sys.stderr, flush=True)
+        return None
+    if child.returncode != 0:
+        print(f"[bench] CPU baseline failed: {err[-500:]}", file=sys.stderr, flush=True)
+        return None
+    return json.loads(out.strip().splitlines()[-1])
+
+
+def cpu_baseline_line(r, E: int, what: str):
+    """cpu_baseline object of the refinement line from the child's result."""
+    if r is None:
+        return None
+    med = r["median_s"]
     return {
-        "value": round(n * 2 * g.n_edges / dt / 1e9, 6),
+        "value": round(2 * E / med / 1e9, 6),
         "unit": "GTEPS",
-        "cores": 1,
+        "cores": len(r["pinned_cores"]),
         "kind": "oracle",
-        "sample": f"first {n} of the {sched.n_place} placements of the same loop, each "
-                  f"evaluated in full (tl, bl, makespan, critical path, label memory); "
-                  f"{n / dt:.2f} evaluations/s over {dt:.1f} s on one core of "
-                  f"'{host_cpu_model()}'",
+        "sample": f"{what}: {r['what']}, each evaluated in full (levels, tl, bl, makespan, "
+                  f"critical path, label memory) by the oracle built with {r['build']}, one "
+                  f"thread pinned to core {r['pinned_cores']}; median {med * 1e3:.1f} ms per "
+                  f"evaluation ({1 / med:.2f} evaluations/s) over {r['reps']} timed runs after "
+                  f"a warm-up; host: {r['nproc']} logical CPUs, '{r['cpu_model']}'",
+        "median_ms": round(med * 1e3, 3),
+        "reps": r["reps"],
+        "nproc": r["nproc"],
+        "cpu_model": r["cpu_model"],
     }
 
 
@@ -174,7 +201,7 @@ def hbm_roofline(kernel: str, kernel_ms: float, alg_bytes: int, note: str = ""):
     return r
 
 
-def bench_single(args) -> int:
+def bench_single(args, child) -> int:
     """One full evaluation of one placement (t/b levels, critical path, label
     memory: pardnn_tb_levels + pardnn_critical_path + pardnn_label_memory) on
     each of the four single-graph workloads; one JSON line, `value` on the
@@ -231,16 +258,6 @@ def bench_single(args) -> int:
                              "gteps": round(2 * E / (wall / 1e3) / 1e9, 4)}
         print(f"[bench] single config{i}: {wall:.3f} ms per evaluation, sweep {sweep_ms:.3f} ms",
               file=sys.stderr, flush=True)
-        if args.cpu_budget > 0 and i in (0, 1, 2):
-            import oracle
-            oracle.build(force=False)
-            t0, reps = time.perf_counter(), 0
-            while reps < 1 or time.perf_counter() - t0 < args.cpu_budget / 3:
-                oracle.evaluate(V, g.src, g.dst, g.comp, g.edge_cost, g.mem, g.placement, K,
-                                g.capacity)
-                reps += 1
-            dt = (time.perf_counter() - t0) / reps
-            cpu[f"config{i}"] = {"ms": round(dt * 1e3, 3), "reps": reps}
         if i == 2:
             main = per["config2"]
             roof = hbm_roofline(P.pardnn_get_timing(G.handle)[0], sweep_ms,
@@ -248,6 +265,10 @@ def bench_single(args) -> int:
                                 "one placement walks the level chain one level at a time: "
                                 "latency-bound")
         G.close()
+    r = finish_cpu_baseline(child, 4 * args.cpu_budget + 120)
+    if r is not None:
+        for k, x in r["per_config"].items():
+            cpu[k] = {"ms": round(x["median_s"] * 1e3, 3), "reps": x["reps"]}
     line = {
         "metric": "single-placement full evaluations/sec (t/b levels, critical path, label "
                   "memory), 1 MI355X",
@@ -259,11 +280,15 @@ def bench_single(args) -> int:
                                "full; the other graphs alongside", "per_graph": per},
         "roofline": roof,
         "cpu_baseline": ({"value": round(1e3 / cpu["config2"]["ms"], 3), "unit": "evaluations/s",
-                          "cores": 1, "kind": "oracle",
-                          "sample": f"whole evaluations on one core of '{host_cpu_model()}': " +
+                          "cores": len(r["pinned_cores"]), "kind": "oracle",
+                          "sample": f"whole evaluations of each graph's own placement by the "
+                                    f"oracle built with {r['build']}, one thread pinned to core "
+                                    f"{r['pinned_cores']}, median over the timed runs after a "
+                                    f"warm-up: " +
                                     ", ".join(f"{k} {v['ms']} ms x {v['reps']}"
-                                              for k, v in cpu.items())}
-                         if cpu else None),
+                                              for k, v in cpu.items()) +
+                                    f"; host: {r['nproc']} logical CPUs, '{r['cpu_model']}'"}
+                         if cpu and "config2" in cpu else None),
     }
     print(json.dumps(line), flush=True)
     return 0
@@ -468,6 +493,11 @@ def main() -> int:
         print(f"bench.py runs on one GPU only: the evaluator has no multi-GPU path "
               f"(asked for --gpus {args.gpus}).", file=sys.stderr)
         return 2
+    # the CPU baseline runs beside the GPU work, on a core of its own, and is
+    # started before anything touches the GPU
+    child = None
+    if args.row in ("refinement", "single") and not args.copy_calibration:
+        child = start_cpu_baseline(args.row, args.cpu_budget, 2, args.n_place)
 
     import numpy as np
     import torch
@@ -487,7 +517,7 @@ def main() -> int:
         print("copied 1 GiB three times", file=sys.stderr, flush=True)
         return 0
     if args.row == "single":
-        return bench_single(args)
+        return bench_single(args, child)
     if args.row != "refinement":
         return bench_row(args, args.row)
     P.load_library()
@@ -608,9 +638,10 @@ def main() -> int:
               flush=True)
 
     cpu = None
-    if args.cpu_budget > 0:
-        print("[bench] timing the CPU oracle ...", file=sys.stderr, flush=True)
-        cpu = cpu_baseline(g, sched, args.cpu_budget)
+    if child is not None:
+        print("[bench] waiting for the CPU oracle timing ...", file=sys.stderr, flush=True)
+        cpu = cpu_baseline_line(finish_cpu_baseline(child, 4 * args.cpu_budget + 120), E,
+                                "the same refinement loop")
 
     line = {
         "metric": METRIC,

@@ -372,18 +372,25 @@ int evaluate_impl(Graph *g, int32_t n_place, const int32_t *placements, const Mo
     // [0, n_labels) (they are checked) and values leave room for their bits.
     // The b keys then also carry the successor id: (value << ob) | (2^ob - 1 - id)
     // with 2^ob > V, which needs values below 2^(62 - ob) as well.
+    // Without label sums the labels are unchecked: those below 2^16 still fit,
+    // which the label build finds out on the device (bt_fit); then both sweeps
+    // are enqueued and the one that does not apply returns at once, so the
+    // call needs no host round trip to choose.
     int32_t lb = 0, ob = 0;
-    if (label_mem != nullptr) {
+    bool gated = false;
+    if (g->V > 0) {
         int32_t bits = 1;
-        while ((1ll << bits) < (int64_t)n_labels) bits++;
-        int32_t obits = 1;
-        while ((1ll << obits) <= (int64_t)g->V) obits++;
+        while ((1ll << bits) < (label_mem != nullptr ? (int64_t)n_labels : (int64_t)kPackLabels))
+            bits++;
+        const int32_t obits = succ_bits(g->V);
         const int32_t wide = std::max(bits, obits);
         if (bits <= 16 && wide < 62 && g->weight_bound < (1ll << (62 - wide))) {
             lb = bits;
             ob = obits;
+            gated = label_mem == nullptr;
         }
     }
+    if (gated && g->bt_fit == nullptr) HIP_TRY(dalloc(*g, &g->bt_fit, 1));
     int64_t *ftl = (int64_t *)g->batch_ws;
     int64_t *bll = ftl + 2 * per;
     int32_t *lab_w = (int32_t *)(bll + 2 * per);
@@ -395,14 +402,16 @@ int evaluate_impl(Graph *g, int32_t n_place, const int32_t *placements, const Mo
         (char *)g->batch_ws + (need - moves_bytes) / 256 * 256);
 
     const int32_t K = label_mem != nullptr ? n_labels : 0;
+    int32_t *fit = gated ? g->bt_fit : nullptr;
     HIP_TRY(launch_fill_i32(g->err, 4, 0, g->stream));
+    if (fit != nullptr) HIP_TRY(launch_fill_i32(fit, 1, 1, g->stream));
     if (mv != nullptr) {
         HIP_TRY(launch_moves_to_slices(*g, mv->base, n_place, mv->step_ptr, n_moves, mv->node,
                                        mv->label, S, moves_scratch, lab_w, lab_stride, K,
-                                       g->err));
+                                       g->err, fit));
     } else {
         HIP_TRY(launch_permute_labels_batch(*g, placements, n_place, S, lab_w, lab_stride, K,
-                                            g->err));
+                                            g->err, fit));
     }
     if (K > 0) {
         HIP_TRY(launch_fill_i64(label_mem, (int64_t)n_place * K, 0, g->stream));
@@ -438,13 +447,27 @@ int evaluate_impl(Graph *g, int32_t n_place, const int32_t *placements, const Mo
         a.pre_t = g->pre_t;
         a.pre_b = g->pre_b;
         a.pretie_b = g->pretie_b;
-        TimedLaunch t(g, "k_sweep_pair<2>");
+    }
+    // the unpacked alternative of a gated call: {value, label} pairs
+    SweepArgs alt = a;
+    alt.lb = 0;
+    alt.ob = 0;
+    alt.gate = fit;
+    alt.gate_want = 0;
+    if (gated) {
+        a.gate = fit;
+        a.gate_want = 1;
+    }
+    if (lb > 0 && g->V > 0) {
+        TimedLaunch t(g, gated ? "k_sweep_pair<2> or k_sweep<2>" : "k_sweep_pair<2>");
         HIP_TRY(launch_sweep_pair(a, g->stream));
+        if (gated) HIP_TRY(launch_sweep(alt, S, g->stream));
     } else {
         TimedLaunch t(g, "k_sweep<2>");
         HIP_TRY(launch_sweep(a, S, g->stream));
     }
-    HIP_TRY(launch_finish(a, S, is_critical, cbits, path, path_stride, path_len, g->stream));
+    HIP_TRY(launch_finish(a, S, is_critical, cbits, path, path_stride, path_len, g->stream,
+                          gated ? &alt : nullptr));
     if (K > 0) {
         if (overflow != nullptr || capacity != nullptr)
             HIP_TRY(launch_overflow((int64_t)n_place * K, K, capacity, label_mem, overflow, g->err,
@@ -841,11 +864,16 @@ int pardnn_span_work(pardnn_graph *h, const int32_t *label, int32_t K, const int
     int st = ensure_levelized(g);
     if (st != PARDNN_OK) return st;
     HIP_TRY(grow_aux(g, span_work_scratch_bytes(g->V, n_clusters, K)));
+    if (g->span_cache.changed == nullptr) {
+        HIP_TRY(dalloc(*g, &g->span_cache.tl, g->V));
+        HIP_TRY(dalloc(*g, &g->span_cache.ids, g->V));
+        HIP_TRY(dalloc(*g, &g->span_cache.changed, 1));
+    }
     HIP_TRY(launch_fill_i32(g->err, 4, 0, g->stream));
     {
         TimedLaunch t(g, "span_work");
         HIP_TRY(launch_span_work(*g, label, K, cluster, n_clusters, tl, span_lo, span_hi, work,
-                                 comm, choice, g->aux_scratch, g->err));
+                                 comm, choice, g->aux_scratch, &g->span_cache, g->err));
     }
     st = read_errors(g);
     if (st != PARDNN_OK) return st;

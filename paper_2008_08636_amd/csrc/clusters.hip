@@ -10,10 +10,9 @@
 //
 // Design for gfx950: the weighted levels come from the single-placement
 // sweep; the per-cluster maximum is one pass of 64-bit atomic maxima (cluster
-// ids are arbitrary, up to one per node); the order is a stable device radix
-// sort of (criticality, id) pairs, descending, over ids given ascending.
-#include <rocprim/device/device_radix_sort.hpp>
-
+// ids are arbitrary, up to one per node); the order is a stable radix sort of
+// the keys bound - criticality (ascending, so criticality descending) over the
+// ids given ascending, bound being the ingest bound on every path length.
 #include "device_utils.h"
 #include "internal.h"
 
@@ -103,15 +102,22 @@ hipError_t launch_cluster_relabel(const Graph &g, const int32_t *cluster, int32_
     return e;
 }
 
-// Scratch of the sort: `keys_out` int64[n], `ids` int32[n], then the radix
-// sort's own temporary storage. Returns the bytes needed for n clusters.
+// Scratch of the sort: keys in and out (uint64[n] each), ids int32[n], then
+// the radix sort's own space. Returns the bytes needed for n clusters.
 size_t cluster_sort_bytes(int32_t n) {
-    size_t temp = 0;
-    (void)rocprim::radix_sort_pairs_desc(nullptr, temp, (const int64_t *)nullptr,
-                                         (int64_t *)nullptr, (const int32_t *)nullptr,
-                                         (int32_t *)nullptr, n);
-    return (size_t)n * 8 + (size_t)n * 4 + 256 + temp;
+    return 3 * (((size_t)n * 8 + 255) / 256 * 256) + sort_pairs_scratch_bytes(n, 8);
 }
+
+namespace {
+
+// key = bound - criticality: criticality in [-1, bound] gives keys in
+// [0, bound + 1], smaller for more critical clusters
+__global__ void k_cl_keys(int32_t C, uint64_t bound, const int64_t *crit, uint64_t *key) {
+    for (int32_t c = blockIdx.x * blockDim.x + threadIdx.x; c < C; c += gridDim.x * blockDim.x)
+        key[c] = bound - (uint64_t)crit[c];
+}
+
+}  // namespace
 
 hipError_t launch_cluster_criticality(const Graph &g, const int32_t *cluster, int32_t n_clusters,
                                       const int64_t *tl, const int64_t *bl, int64_t *crit,
@@ -124,14 +130,20 @@ hipError_t launch_cluster_criticality(const Graph &g, const int32_t *cluster, in
             g.V, n_clusters, cluster, tl, bl, reinterpret_cast<long long *>(crit), err);
         if ((e = hipGetLastError()) != hipSuccess) return e;
     }
-    int64_t *keys_out = reinterpret_cast<int64_t *>(scratch);
-    int32_t *ids = reinterpret_cast<int32_t *>(keys_out + n_clusters);
-    void *temp = reinterpret_cast<char *>(scratch) +
-                 (((size_t)n_clusters * 12 + 255) / 256) * 256;
-    size_t temp_bytes = scratch_bytes - (((size_t)n_clusters * 12 + 255) / 256) * 256;
+    if (scratch_bytes < cluster_sort_bytes(n_clusters)) return hipErrorInvalidValue;
+    const size_t seg = ((size_t)n_clusters * 8 + 255) / 256 * 256;
+    uint64_t *keys_in = reinterpret_cast<uint64_t *>(scratch);
+    uint64_t *keys_out = reinterpret_cast<uint64_t *>(reinterpret_cast<char *>(scratch) + seg);
+    int32_t *ids = reinterpret_cast<int32_t *>(reinterpret_cast<char *>(scratch) + 2 * seg);
+    void *temp = reinterpret_cast<char *>(scratch) + 3 * seg;
+    const uint64_t bound = (uint64_t)g.weight_bound;
+    int bits = 1;
+    while (bits < 64 && ((bound + 1) >> bits) != 0) bits++;
+    k_cl_keys<<<grid_for(n_clusters, kBlock), kBlock, 0, g.stream>>>(n_clusters, bound, crit,
+                                                                     keys_in);
+    if ((e = hipGetLastError()) != hipSuccess) return e;
     if ((e = launch_iota_i32(ids, n_clusters, g.stream)) != hipSuccess) return e;
-    return rocprim::radix_sort_pairs_desc(temp, temp_bytes, crit, keys_out, ids, order,
-                                          n_clusters, 0u, 64u, g.stream);
+    return sort_pairs_u64(keys_in, keys_out, ids, order, n_clusters, 0, bits, temp, g.stream);
 }
 
 }  // namespace pardnn

@@ -42,6 +42,15 @@ struct ValidateAcc {
     unsigned long long m_lo, m_hi;  // sum(mem), split at bit 32
 };
 
+// Nodes in (tl, id) order for the span-work tables, with the tl they were
+// sorted by (device arrays of the handle; valid once built).
+struct SpanCache {
+    int64_t *tl = nullptr;       // [V] the tl of the cached order
+    int32_t *ids = nullptr;      // [V] node ids in (tl, id) order
+    int32_t *changed = nullptr;  // [1] set on the device when a call's tl differs
+    bool valid = false;
+};
+
 struct Graph {
     int device = 0;
     hipStream_t stream = nullptr;
@@ -92,11 +101,13 @@ struct Graph {
     // ftl, bll [V + pad][2] packed, labels [V][2]; allocated on first use
     int64_t *ps_ftl = nullptr, *ps_bll = nullptr;
     int32_t *ps_lab = nullptr, *ps_gate = nullptr;
+    SpanCache span_cache;
     // cluster criticality scratch: tl, bl, makespan
     int64_t *cl_tl = nullptr, *cl_bl = nullptr, *cl_m = nullptr;
     // sort and table scratch of the cluster and span calls (grown on demand)
     void *aux_scratch = nullptr;
     size_t aux_scratch_bytes = 0;
+    int32_t *bt_fit = nullptr;       // device flag: a batch's labels fit the packed keys
     int32_t *err = nullptr;          // device error words [4]
     int32_t *h_err = nullptr;        // pinned host mirror [4]
 
@@ -131,6 +142,23 @@ hipError_t launch_build_orig_csr(const Graph &g, int32_t *cursor);
 hipError_t launch_build_lm(Graph &g, int32_t *deg_ws, int32_t *cursor_in, int32_t *cursor_out,
                            int32_t *scan_ws);
 
+// ---- radix_sort.hip ----
+// Stable LSD radix sort of (key, value) pairs on bits [begin_bit, end_bit) of
+// the keys, 8 bits per pass; n < 2^31. The inputs are left unchanged. With
+// `gate` given, every launch returns at once unless *gate != 0 (decided on the
+// device). Scratch: sort_pairs_scratch_bytes(n, sizeof key) bytes.
+size_t sort_pairs_scratch_bytes(int32_t n, int key_bytes);
+hipError_t sort_pairs_u32(const uint32_t *keys_in, uint32_t *keys_out, const int32_t *vals_in,
+                          int32_t *vals_out, int32_t n, int begin_bit, int end_bit,
+                          void *scratch, hipStream_t s, const int32_t *gate = nullptr);
+hipError_t sort_pairs_u64(const uint64_t *keys_in, uint64_t *keys_out, const int32_t *vals_in,
+                          int32_t *vals_out, int32_t n, int begin_bit, int end_bit,
+                          void *scratch, hipStream_t s, const int32_t *gate = nullptr);
+// out[i] = in[0] + ... + in[i] (int64); scratch: inclusive_scan_i64_scratch_bytes(n)
+size_t inclusive_scan_i64_scratch_bytes(int32_t n);
+hipError_t inclusive_scan_i64(const int64_t *in, int64_t *out, int32_t n, void *scratch,
+                              hipStream_t s);
+
 // ---- levelize.hip ----
 // levels, level_ptr and the release order (queue); result = {levels, released}
 hipError_t launch_kahn(const Graph &g, int32_t *indeg_work, int32_t *queue, int32_t *result);
@@ -140,17 +168,23 @@ hipError_t launch_level_order(const Graph &g, int32_t bits, void *scratch);
 
 // ---- sweep.hip ----
 hipError_t launch_permute_labels(const Graph &g, const int32_t *placement, int32_t *lab_lm);
-// K > 0: labels outside [0, K) set bit 0 of err.
+// K > 0: labels outside [0, K) set bit 0 of err. fit (if given): set to 0
+// when a label lies outside [0, kPackLabels).
 hipError_t launch_permute_labels_batch(const Graph &g, const int32_t *placements, int32_t P,
                                        int32_t S, int32_t *lab_w, int64_t lab_stride,
-                                       int32_t K = 0, int32_t *err = nullptr);
+                                       int32_t K = 0, int32_t *err = nullptr,
+                                       int32_t *fit = nullptr);
 // flag = 1 if every label lies in [0, limit), else 0 (on the device)
 hipError_t launch_label_fit(const Graph &g, const int32_t *labels, int32_t limit, int32_t *flag);
 hipError_t launch_sweep(const SweepArgs &a, int32_t S, hipStream_t s);
 // cbits: [P][ceil(V / 32)] bit words of the critical flags, scratch for the
 // path walk (needed when path is given)
+// alt (S = 2 only): a second, gated set of arguments whose emit pass is
+// enqueued beside a's (the two sweeps of a device-side choice); the path pass
+// runs once after both.
 hipError_t launch_finish(const SweepArgs &a, int32_t S, uint8_t *crit, uint32_t *cbits,
-                         int32_t *path, int32_t stride, int32_t *path_len, hipStream_t s);
+                         int32_t *path, int32_t stride, int32_t *path_len, hipStream_t s,
+                         const SweepArgs *alt = nullptr);
 
 // ---- sweep_pair.hip ----
 // flag[e] = 1 for the span-1 edges of the direction's level-major edge order
@@ -185,7 +219,7 @@ size_t span_work_scratch_bytes(int32_t V, int32_t C, int32_t K);
 hipError_t launch_span_work(const Graph &g, const int32_t *label, int32_t K,
                             const int32_t *cluster, int32_t C, const int64_t *tl,
                             int64_t *span_lo, int64_t *span_hi, int64_t *work, int64_t *comm,
-                            int32_t *choice, void *scratch, int32_t *err);
+                            int32_t *choice, void *scratch, SpanCache *cache, int32_t *err);
 
 // ---- clusters.hip ----
 size_t cluster_sort_bytes(int32_t n);
@@ -238,6 +272,7 @@ size_t moves_scratch_elems(int32_t V, int64_t M);
 hipError_t launch_moves_to_slices(const Graph &g, const int32_t *base, int32_t P,
                                   const int64_t *step_ptr, int64_t M, const int32_t *node,
                                   const int32_t *label, int32_t S, int32_t *scratch,
-                                  int32_t *lab_w, int64_t lab_stride, int32_t K, int32_t *err);
+                                  int32_t *lab_w, int64_t lab_stride, int32_t K, int32_t *err,
+                                  int32_t *fit = nullptr);
 
 }  // namespace pardnn

@@ -15,7 +15,6 @@
 // row with one wave, a 64-lane max-scan per chunk of steps.
 #include <type_traits>
 
-#include <rocprim/device/device_radix_sort.hpp>
 
 #include "device_utils.h"
 #include "internal.h"
@@ -245,7 +244,7 @@ __global__ __launch_bounds__(256) void k_moves_to_slices(int32_t V, int32_t P,
                                                          const int32_t *mv_off,
                                                          const int4 *mv_ent, int32_t *lab_w,
                                                          int64_t lab_stride, int32_t K,
-                                                         int32_t *err) {
+                                                         int32_t *err, int32_t *fit) {
     constexpr int TV = 64, TP = 64, NW = 256 / kWave, RW = TV / NW;
     __shared__ int32_t tile[TV][TP + 1];
     const int lane = lane_id(), w = wave_id();
@@ -313,8 +312,10 @@ __global__ __launch_bounds__(256) void k_moves_to_slices(int32_t V, int32_t P,
 #pragma unroll
                 for (int s2 = 0; s2 < S; s2++) {
                     x.v[s2] = tile[r][sl * S + s2];
-                    if (K > 0 && (x.v[s2] < 0 || x.v[s2] >= K) && c0 + sl * S + s2 < P)
-                        atomicOr(err, 1);
+                    if (c0 + sl * S + s2 < P) {
+                        if (K > 0 && (x.v[s2] < 0 || x.v[s2] >= K)) atomicOr(err, 1);
+                        if (fit != nullptr && (uint32_t)x.v[s2] >= kPackLabels) *fit = 0;
+                    }
                 }
                 // streamed: the sweep reads these long after, and dirty
                 // lines left in L2 would be written back during the sweep
@@ -339,13 +340,7 @@ unsigned mv_key_bits(int32_t V) {
     return bits;
 }
 
-size_t mv_sort_temp_bytes(int32_t V, int64_t M) {
-    size_t temp = 0;
-    (void)rocprim::radix_sort_pairs(nullptr, temp, (const uint32_t *)nullptr, (uint32_t *)nullptr,
-                                    (const int32_t *)nullptr, (int32_t *)nullptr, (size_t)M, 0u,
-                                    mv_key_bits(V));
-    return temp;
-}
+size_t mv_sort_temp_bytes(int32_t, int64_t M) { return sort_pairs_scratch_bytes((int32_t)M, 4); }
 
 constexpr size_t al64(size_t n) { return (n + 63) / 64 * 64; }   // int32 elements, 256 B
 
@@ -361,7 +356,8 @@ size_t moves_scratch_elems(int32_t V, int64_t M) {
 hipError_t launch_moves_to_slices(const Graph &g, const int32_t *base, int32_t P,
                                   const int64_t *step_ptr, int64_t M, const int32_t *node,
                                   const int32_t *label, int32_t S, int32_t *scratch,
-                                  int32_t *lab_w, int64_t lab_stride, int32_t K, int32_t *err) {
+                                  int32_t *lab_w, int64_t lab_stride, int32_t K, int32_t *err,
+                                  int32_t *fit) {
     if (g.V == 0 || P == 0) return hipSuccess;
     const int32_t V = g.V;
     const size_t m64 = al64((size_t)M);
@@ -376,11 +372,9 @@ hipError_t launch_moves_to_slices(const Graph &g, const int32_t *base, int32_t P
     if (M > 0) {
         k_mv_keys<<<grid_for(M, kBlock), kBlock, 0, g.stream>>>(M, node, V, key_in, idx_in, err);
         e = hipGetLastError();
-        size_t temp_bytes = mv_sort_temp_bytes(V, M);
         if (e == hipSuccess)
-            e = rocprim::radix_sort_pairs(temp, temp_bytes, (const uint32_t *)key_in, key_out,
-                                          (const int32_t *)idx_in, idx_out, (size_t)M, 0u,
-                                          mv_key_bits(V), g.stream);
+            e = sort_pairs_u32(key_in, key_out, idx_in, idx_out, (int32_t)M, 0,
+                               (int)mv_key_bits(V), temp, g.stream);
     }
     if (e == hipSuccess) {
         k_mv_off<<<grid_for((int64_t)V + 1, kBlock), kBlock, 0, g.stream>>>(V, M, key_out, off);
@@ -395,13 +389,13 @@ hipError_t launch_moves_to_slices(const Graph &g, const int32_t *base, int32_t P
     const unsigned grid = (unsigned)((V + 63) / 64);
     if (S == 1)
         k_moves_to_slices<1><<<grid, 256, 0, g.stream>>>(V, P, g.order, base, off, ent, lab_w,
-                                                         lab_stride, K, err);
+                                                         lab_stride, K, err, fit);
     else if (S == 2)
         k_moves_to_slices<2><<<grid, 256, 0, g.stream>>>(V, P, g.order, base, off, ent, lab_w,
-                                                         lab_stride, K, err);
+                                                         lab_stride, K, err, fit);
     else if (S == 4)
         k_moves_to_slices<4><<<grid, 256, 0, g.stream>>>(V, P, g.order, base, off, ent, lab_w,
-                                                         lab_stride, K, err);
+                                                         lab_stride, K, err, fit);
     else
         return hipErrorInvalidValue;
     return hipGetLastError();

@@ -17,7 +17,6 @@
 // without a dependent global load. `level_ptr` falls out of the frontier
 // sizes; `order` -- ids sorted by (level, id) -- comes from one stable radix
 // sort of the levels afterwards instead of a sort per level.
-#include <rocprim/device/device_radix_sort.hpp>
 
 #include "device_utils.h"
 #include "internal.h"
@@ -149,11 +148,7 @@ hipError_t launch_kahn(const Graph &g, int32_t *indeg_work, int32_t *queue, int3
 }
 
 size_t level_order_scratch_bytes(int32_t V) {
-    size_t temp = 0;
-    (void)rocprim::radix_sort_pairs(nullptr, temp, (const uint32_t *)nullptr,
-                                    (uint32_t *)nullptr, (const int32_t *)nullptr,
-                                    (int32_t *)nullptr, V);
-    return ((size_t)V * 8 + 255) / 256 * 256 + temp;
+    return ((size_t)V * 8 + 255) / 256 * 256 + sort_pairs_scratch_bytes(V, 4);
 }
 
 // order = node ids sorted by (level, id): a stable radix sort of the levels
@@ -165,13 +160,10 @@ hipError_t launch_level_order(const Graph &g, int32_t bits, void *scratch) {
     int32_t *ids = reinterpret_cast<int32_t *>(scratch);
     uint32_t *keys_out = reinterpret_cast<uint32_t *>(ids + V);
     void *temp = reinterpret_cast<char *>(scratch) + head;
-    size_t temp_bytes = level_order_scratch_bytes(V) - head;
     hipError_t e = launch_iota_i32(ids, V, g.stream);
     if (e != hipSuccess) return e;
-    return rocprim::radix_sort_pairs(temp, temp_bytes,
-                                     reinterpret_cast<const uint32_t *>(g.level), keys_out,
-                                     (const int32_t *)ids, g.order, V, 0u, (unsigned)bits,
-                                     g.stream);
+    return sort_pairs_u32(reinterpret_cast<const uint32_t *>(g.level), keys_out, ids, g.order, V,
+                          0, bits, temp, g.stream);
 }
 
 }  // namespace pardnn

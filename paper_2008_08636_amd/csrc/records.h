@@ -80,6 +80,8 @@ constexpr int kLevelWindow = 128;
 // Placements per chain of the batched evaluation (slice of the workspace),
 // and padding nodes per slice of ftl / bll / nx_w.
 constexpr int kBatchSlots = 2;
+// labels below this bound fit the pair sweep's packed keys
+constexpr uint32_t kPackLabels = 1u << 16;
 constexpr int kSlicePad = 64;
 
 struct SweepArgs {

@@ -17,15 +17,19 @@
 // sequential mapping loop can query one span at a time. Here all queries of a
 // batch run at once, so the table is static: the mapped nodes sorted by
 // (partition, tl) with a prefix sum of their weights, after which one span
-// query is two binary searches in its partition's segment. The sort is two
-// stable device radix sorts (by tl, then by partition); the communication
-// table and the span ends are passes of 64-bit atomics over the edge list
-// (edge-parallel, so hub nodes with thousands of edges cost no serial loop);
-// cluster ends are 64-bit atomic min / max of (level, id) keys.
-#include <rocprim/device/device_radix_sort.hpp>
-#include <rocprim/device/device_scan.hpp>
-
+// query is two binary searches in its partition's segment. The nodes in
+// (tl, id) order are kept on the graph handle with a copy of the tl they came
+// from: the mapping loop calls again with the same tl and new partitions, so
+// a call compares tl with the copy on the device and re-sorts by tl (a 64-bit
+// radix sort, its launches gated by the comparison) only when it changed;
+// every call then splits that order by partition with a one-pass stable
+// radix sort. The communication table and the span ends are passes of 64-bit
+// atomics over the edge list (edge-parallel, so hub nodes with thousands of
+// edges cost no serial loop); cluster ends are 64-bit atomic min / max of
+// (level, id) keys.
 #include <climits>
+
+#include <algorithm>
 
 #include "device_utils.h"
 #include "internal.h"
@@ -47,8 +51,8 @@ inline size_t align256(size_t b) { return (b + 255) / 256 * 256; }
 
 // Scratch layout for V nodes, C clusters, K partitions.
 struct SwLayout {
-    size_t ids0, ids1, tl_tmp, lab_key, lab_sorted, s_tl, pre, seg, first, last, m, range, temp;
-    size_t temp_bytes, total;
+    size_t ids0, ids1, tl_key, tl_key_out, lab_key, lab_sorted, s_tl, w, pre, seg, first, last,
+        m, temp, total;
     SwLayout(int32_t V, int32_t C, int32_t K) {
         size_t o = 0;
         auto take = [&](size_t bytes) {
@@ -58,31 +62,20 @@ struct SwLayout {
         };
         ids0 = take((size_t)V * 4);
         ids1 = take((size_t)V * 4);
-        tl_tmp = take((size_t)V * 8);
+        tl_key = take((size_t)V * 8);
+        tl_key_out = take((size_t)V * 8);
         lab_key = take((size_t)V * 4);
         lab_sorted = take((size_t)V * 4);
         s_tl = take((size_t)V * 8);
+        w = take((size_t)V * 8);
         pre = take((size_t)(V + 1) * 8);
         seg = take((size_t)(K + 1) * 4);
         first = take((size_t)C * 8);
         last = take((size_t)C * 8);
         m = take(8);
-        range = take(16);
-        size_t t1 = 0, t2 = 0, t3 = 0, t4 = 0;
-        (void)rocprim::radix_sort_pairs(nullptr, t1, (const int64_t *)nullptr, (int64_t *)nullptr,
-                                        (const int32_t *)nullptr, (int32_t *)nullptr, V);
-        (void)rocprim::radix_sort_pairs(nullptr, t2, (const uint32_t *)nullptr,
-                                        (uint32_t *)nullptr, (const int32_t *)nullptr,
-                                        (int32_t *)nullptr, V);
-        (void)rocprim::inclusive_scan(nullptr, t3, (const int64_t *)nullptr, (int64_t *)nullptr,
-                                      (size_t)V, rocprim::plus<int64_t>());
-        (void)rocprim::radix_sort_pairs(nullptr, t4, (const uint64_t *)nullptr,
-                                        (uint64_t *)nullptr, (const int32_t *)nullptr,
-                                        (int32_t *)nullptr, V);
-        temp_bytes = t1 > t2 ? t1 : t2;
-        temp_bytes = temp_bytes > t3 ? temp_bytes : t3;
-        temp_bytes = temp_bytes > t4 ? temp_bytes : t4;
-        temp = take(temp_bytes);
+        size_t t = sort_pairs_scratch_bytes(V, 8);
+        t = std::max(t, inclusive_scan_i64_scratch_bytes(V));
+        temp = take(t);
         total = o;
     }
 };
@@ -93,12 +86,12 @@ T *at(void *base, size_t off) {
 }
 
 // Per node: validate ids, cluster ends as (level << 32 | id) keys, the makespan
-// max(tl + comp), identity values for the first sort.
+// max(tl + comp).
 __global__ void k_sw_nodes(int32_t V, int32_t K, int32_t C, const int32_t *label,
                            const int32_t *cluster, const int32_t *level, const int64_t *tl,
                            const int64_t *comp, long long *first, long long *last, long long *m,
-                           long long *range, int32_t *ids, int32_t *err) {
-    long long best = LLONG_MIN, tmin = LLONG_MAX, tmax = LLONG_MIN;
+                           int32_t *err) {
+    long long best = LLONG_MIN;
     for (int32_t v = blockIdx.x * blockDim.x + threadIdx.x; v < V; v += gridDim.x * blockDim.x) {
         const int32_t c = cluster[v], k = label[v];
         if (c < -1 || c >= C) atomicOr(err, 1);
@@ -110,48 +103,30 @@ __global__ void k_sw_nodes(int32_t V, int32_t K, int32_t C, const int32_t *label
         }
         const long long f = tl[v] + comp[v];
         best = f > best ? f : best;
-        tmin = tl[v] < tmin ? tl[v] : tmin;
-        tmax = tl[v] > tmax ? tl[v] : tmax;
-        ids[v] = v;
     }
     best = wave_max_i64(best);
-    tmax = wave_max_i64(tmax);
-#pragma unroll
-    for (int off = kWave / 2; off > 0; off >>= 1) {
-        const long long o = __shfl_xor(tmin, off, kWave);
-        tmin = o < tmin ? o : tmin;
-    }
-    if (lane_id() == 0 && best != LLONG_MIN) {
-        atomicMax(m, best);
-        atomicMin(&range[0], tmin);
-        atomicMax(&range[1], tmax);
-    }
+    if (lane_id() == 0 && best != LLONG_MIN) atomicMax(m, best);
 }
 
-// one sort key per node: (partition << tb) | (tl - tmin), unmapped nodes last
-__global__ void k_sw_keys(int32_t V, int32_t K, const int32_t *label, const int64_t *tl,
-                          int64_t tmin, int32_t tb, uint64_t *key) {
+// changed = 1 when tl differs from the copy the cached order was built from
+__global__ void k_sw_tl_cmp(int32_t V, const int64_t *tl, const int64_t *copy, int32_t *changed) {
+    bool diff = false;
+    for (int32_t v = blockIdx.x * blockDim.x + threadIdx.x; v < V; v += gridDim.x * blockDim.x)
+        diff = diff || tl[v] != copy[v];
+    if (__ballot(diff) != 0ull && lane_id() == 0) *changed = 1;
+}
+
+// (when tl changed) sort keys with the order of signed tl, identity values,
+// and the new copy of tl
+__global__ void k_sw_tl_keys(int32_t V, const int64_t *tl, const int32_t *changed, uint64_t *key,
+                             int32_t *ids, int64_t *copy) {
+    if (*changed == 0) return;
     for (int32_t v = blockIdx.x * blockDim.x + threadIdx.x; v < V; v += gridDim.x * blockDim.x) {
-        const int32_t k = label[v];
-        const uint64_t part = (k >= 0 && k < K) ? (uint64_t)k : (uint64_t)K;
-        key[v] = (part << tb) | ((uint64_t)tl[v] - (uint64_t)tmin);
+        const int64_t t = tl[v];
+        key[v] = (uint64_t)t ^ (1ull << 63);
+        ids[v] = v;
+        copy[v] = t;
     }
-}
-
-// seg[k] = first position whose key's partition is >= k (keys sorted)
-__global__ void k_sw_seg64(int32_t V, int32_t K, const uint64_t *key, int32_t tb, int32_t *seg) {
-    const int32_t k = blockIdx.x * blockDim.x + threadIdx.x;
-    if (k > K) return;
-    const uint64_t x = (uint64_t)k << tb;
-    int32_t lo = 0, hi = V;
-    while (lo < hi) {
-        const int32_t mid = (lo + hi) >> 1;
-        if (key[mid] < x)
-            lo = mid + 1;
-        else
-            hi = mid;
-    }
-    seg[k] = lo;
 }
 
 // partition of the i-th node in tl order; unmapped (or invalid) nodes sort last
@@ -163,7 +138,7 @@ __global__ void k_sw_lab_keys(int32_t V, int32_t K, const int32_t *label, const 
     }
 }
 
-// nodes in (partition, tl) order: their tl, and their weights into pre[1..V]
+// nodes in (partition, tl) order: their tl and their weights
 __global__ void k_sw_gather(int32_t V, const int32_t *ids, const int64_t *tl,
                             const int64_t *comp, int64_t *s_tl, int64_t *w) {
     for (int32_t i = blockIdx.x * blockDim.x + threadIdx.x; i < V; i += gridDim.x * blockDim.x) {
@@ -353,92 +328,69 @@ size_t span_work_scratch_bytes(int32_t V, int32_t C, int32_t K) {
 hipError_t launch_span_work(const Graph &g, const int32_t *label, int32_t K,
                             const int32_t *cluster, int32_t C, const int64_t *tl,
                             int64_t *span_lo, int64_t *span_hi, int64_t *work, int64_t *comm,
-                            int32_t *choice, void *scratch, int32_t *err) {
+                            int32_t *choice, void *scratch, SpanCache *cache, int32_t *err) {
     const int32_t V = g.V;
     const SwLayout L(V, C, K);
     hipStream_t s = g.stream;
     int32_t *ids0 = at<int32_t>(scratch, L.ids0), *ids1 = at<int32_t>(scratch, L.ids1);
-    int64_t *tl_tmp = at<int64_t>(scratch, L.tl_tmp);
+    uint64_t *tl_key = at<uint64_t>(scratch, L.tl_key);
+    uint64_t *tl_key_out = at<uint64_t>(scratch, L.tl_key_out);
     uint32_t *lab_key = at<uint32_t>(scratch, L.lab_key);
     uint32_t *lab_sorted = at<uint32_t>(scratch, L.lab_sorted);
-    int64_t *s_tl = at<int64_t>(scratch, L.s_tl), *pre = at<int64_t>(scratch, L.pre);
+    int64_t *s_tl = at<int64_t>(scratch, L.s_tl), *wt = at<int64_t>(scratch, L.w);
+    int64_t *pre = at<int64_t>(scratch, L.pre);
     int32_t *seg = at<int32_t>(scratch, L.seg);
     int64_t *first = at<int64_t>(scratch, L.first), *last = at<int64_t>(scratch, L.last);
     int64_t *m = at<int64_t>(scratch, L.m);
-    int64_t *range = at<int64_t>(scratch, L.range);
     void *temp = at<char>(scratch, L.temp);
-    size_t temp_bytes = L.temp_bytes;
     hipError_t e;
 
     if ((e = launch_fill_i64(first, C, LLONG_MAX, s)) != hipSuccess) return e;
     if ((e = launch_fill_i64(last, C, -1, s)) != hipSuccess) return e;
     if ((e = launch_fill_i64(m, 1, LLONG_MIN, s)) != hipSuccess) return e;
-    if ((e = launch_fill_i64(range, 1, LLONG_MAX, s)) != hipSuccess) return e;
-    if ((e = launch_fill_i64(range + 1, 1, LLONG_MIN, s)) != hipSuccess) return e;
     if ((e = launch_fill_i64(pre, 1, 0, s)) != hipSuccess) return e;
     if ((e = launch_fill_i64(comm, (int64_t)C * K, 0, s)) != hipSuccess) return e;
-    unsigned pbits = 1;   // partitions 0..K (K: unmapped) fit in pbits bits
+    int pbits = 1;   // partitions 0..K (K: unmapped) fit in pbits bits
     while (pbits < 32 && ((uint64_t)K >> pbits) != 0) pbits++;
-    bool composite = false;
     if (V > 0) {
         k_sw_nodes<<<grid_for(V, kBlock, 2048), kBlock, 0, s>>>(
             V, K, C, label, cluster, g.level, tl, g.comp, reinterpret_cast<long long *>(first),
-            reinterpret_cast<long long *>(last), reinterpret_cast<long long *>(m),
-            reinterpret_cast<long long *>(range), ids0, err);
+            reinterpret_cast<long long *>(last), reinterpret_cast<long long *>(m), err);
         if ((e = hipGetLastError()) != hipSuccess) return e;
-        // The tl range sizes the sort: when (partition, tl - min) fits one
-        // 64-bit key, a single stable radix sort over its bits orders the
-        // nodes by (partition, tl, id); otherwise two sorts (tl, then partition).
-        int64_t h_range[2] = {0, 0};
-        if ((e = hipMemcpyAsync(h_range, range, sizeof(h_range), hipMemcpyDeviceToHost, s)) !=
+        // the nodes in (tl, id) order, rebuilt only when tl changed; the cache
+        // counts as valid again only once every launch of the rebuild is enqueued
+        const bool was_valid = cache->valid;
+        cache->valid = false;
+        if ((e = launch_fill_i32(cache->changed, 1, was_valid ? 0 : 1, s)) != hipSuccess)
+            return e;
+        if (was_valid) {
+            k_sw_tl_cmp<<<grid_for(V, kBlock, 2048), kBlock, 0, s>>>(V, tl, cache->tl,
+                                                                     cache->changed);
+            if ((e = hipGetLastError()) != hipSuccess) return e;
+        }
+        k_sw_tl_keys<<<grid_for(V, kBlock), kBlock, 0, s>>>(V, tl, cache->changed, tl_key, ids0,
+                                                            cache->tl);
+        if ((e = hipGetLastError()) != hipSuccess) return e;
+        if ((e = sort_pairs_u64(tl_key, tl_key_out, ids0, cache->ids, V, 0, 64, temp, s,
+                                cache->changed)) != hipSuccess)
+            return e;
+        cache->valid = true;
+        // split by partition, stably: nodes in (partition, tl, id) order
+        k_sw_lab_keys<<<grid_for(V, kBlock), kBlock, 0, s>>>(V, K, label, cache->ids, lab_key);
+        if ((e = hipGetLastError()) != hipSuccess) return e;
+        if ((e = sort_pairs_u32(lab_key, lab_sorted, cache->ids, ids1, V, 0, pbits, temp, s)) !=
             hipSuccess)
             return e;
-        if ((e = hipStreamSynchronize(s)) != hipSuccess) return e;
-        const uint64_t span = (uint64_t)h_range[1] - (uint64_t)h_range[0];
-        unsigned tb = 1;
-        while (tb < 64 && (span >> tb) != 0) tb++;
-        const int32_t *sorted_ids;
-        if (tb + pbits <= 64) {
-            composite = true;
-            uint64_t *keys_in = reinterpret_cast<uint64_t *>(tl_tmp);
-            uint64_t *keys_out = reinterpret_cast<uint64_t *>(s_tl);
-            k_sw_keys<<<grid_for(V, kBlock), kBlock, 0, s>>>(V, K, label, tl, h_range[0],
-                                                             (int32_t)tb, keys_in);
-            if ((e = hipGetLastError()) != hipSuccess) return e;
-            if ((e = rocprim::radix_sort_pairs(temp, temp_bytes, (const uint64_t *)keys_in,
-                                               keys_out, (const int32_t *)ids0, ids1, V, 0u,
-                                               tb + pbits, s)) != hipSuccess)
-                return e;
-            k_sw_seg64<<<grid_for(K + 1, kBlock), kBlock, 0, s>>>(V, K, keys_out, (int32_t)tb,
-                                                                  seg);
-            if ((e = hipGetLastError()) != hipSuccess) return e;
-            sorted_ids = ids1;
-        } else {
-            if ((e = rocprim::radix_sort_pairs(temp, temp_bytes, tl, tl_tmp, ids0, ids1, V, 0u,
-                                               64u, s)) != hipSuccess)
-                return e;
-            k_sw_lab_keys<<<grid_for(V, kBlock), kBlock, 0, s>>>(V, K, label, ids1, lab_key);
-            if ((e = hipGetLastError()) != hipSuccess) return e;
-            if ((e = rocprim::radix_sort_pairs(temp, temp_bytes, lab_key, lab_sorted, ids1, ids0,
-                                               V, 0u, pbits, s)) != hipSuccess)
-                return e;
-            sorted_ids = ids0;
-        }
-        k_sw_gather<<<grid_for(V, kBlock), kBlock, 0, s>>>(V, sorted_ids, tl, g.comp, s_tl,
-                                                           tl_tmp);
+        k_sw_gather<<<grid_for(V, kBlock), kBlock, 0, s>>>(V, ids1, tl, g.comp, s_tl, wt);
         if ((e = hipGetLastError()) != hipSuccess) return e;
-        if ((e = rocprim::inclusive_scan(temp, temp_bytes, (const int64_t *)tl_tmp, pre + 1,
-                                         (size_t)V, rocprim::plus<int64_t>(), s)) != hipSuccess)
-            return e;
+        if ((e = inclusive_scan_i64(wt, pre + 1, V, temp, s)) != hipSuccess) return e;
         k_sw_comm<<<grid_for(g.E, kBlock), kBlock, 0, s>>>(
             g.E, K, C, g.e_src, g.e_dst, g.e_cost, cluster, label,
             reinterpret_cast<unsigned long long *>(comm));
         if ((e = hipGetLastError()) != hipSuccess) return e;
     }
-    if (!composite) {
-        k_sw_seg<<<grid_for(K + 1, kBlock), kBlock, 0, s>>>(V, K, lab_sorted, seg);
-        if ((e = hipGetLastError()) != hipSuccess) return e;
-    }
+    k_sw_seg<<<grid_for(K + 1, kBlock), kBlock, 0, s>>>(V, K, lab_sorted, seg);
+    if ((e = hipGetLastError()) != hipSuccess) return e;
     {
         const long long *fk = reinterpret_cast<const long long *>(first);
         long long *lo = reinterpret_cast<long long *>(span_lo);

@@ -51,7 +51,7 @@ __global__ __launch_bounds__(256) void k_permute_labels(int32_t V, int32_t P,
                                                         const int32_t *order,
                                                         const int32_t *placements,
                                                         int32_t *lab_w, int64_t lab_stride,
-                                                        int32_t K, int32_t *err) {
+                                                        int32_t K, int32_t *err, int32_t *fit) {
     constexpr int TV = 64, TP = 64;  // tile: 64 nodes x 64 placements
     __shared__ int32_t tile[TV][TP + 1];
     const int32_t n_slices = (P + S - 1) / S;
@@ -64,6 +64,7 @@ __global__ __launch_bounds__(256) void k_permute_labels(int32_t V, int32_t P,
         if (v < V && p < P) {
             x = placements[(int64_t)order[v] * P + p];
             if (K > 0 && (x < 0 || x >= K)) atomicOr(err, 1);
+            if (fit != nullptr && (uint32_t)x >= kPackLabels) *fit = 0;
         }
         tile[r][tx] = x;
     }
@@ -802,15 +803,15 @@ hipError_t launch_permute_labels(const Graph &g, const int32_t *placement, int32
 
 hipError_t launch_permute_labels_batch(const Graph &g, const int32_t *placements, int32_t P,
                                        int32_t S, int32_t *lab_w, int64_t lab_stride, int32_t K,
-                                       int32_t *err) {
+                                       int32_t *err, int32_t *fit) {
     if (g.V == 0 || P == 0) return hipSuccess;
     dim3 grid((g.V + 63) / 64, (P + 63) / 64);
     if (S == 1)
         k_permute_labels<1><<<grid, 256, 0, g.stream>>>(g.V, P, g.order, placements, lab_w,
-                                                        lab_stride, K, err);
+                                                        lab_stride, K, err, fit);
     else if (S == kBatchSlots)
         k_permute_labels<kBatchSlots><<<grid, 256, 0, g.stream>>>(g.V, P, g.order, placements,
-                                                                  lab_w, lab_stride, K, err);
+                                                                  lab_w, lab_stride, K, err, fit);
     else
         return hipErrorInvalidValue;
     return hipGetLastError();
@@ -857,22 +858,28 @@ hipError_t launch_sweep(const SweepArgs &a, int32_t S, hipStream_t s) {
 }
 
 hipError_t launch_finish(const SweepArgs &a, int32_t S, uint8_t *crit, uint32_t *cbits,
-                         int32_t *path, int32_t stride, int32_t *path_len, hipStream_t s) {
+                         int32_t *path, int32_t stride, int32_t *path_len, hipStream_t s,
+                         const SweepArgs *alt) {
     if (a.P == 0) return hipSuccess;
     // S = 1: outputs only (one placement from the pair sweep), no path
     if (S != kBatchSlots && !(S == 1 && path == nullptr && a.lb > 0)) return hipErrorInvalidValue;
     if (path != nullptr && cbits == nullptr) return hipErrorInvalidValue;
+    if (alt != nullptr && (S != kBatchSlots || alt->gate == nullptr || a.gate == nullptr))
+        return hipErrorInvalidValue;
     if (a.V > 0) {
         const unsigned blocks = (unsigned)((a.V + kEmitNodes - 1) / kEmitNodes);
         uint32_t *bits = path != nullptr ? cbits : nullptr;
-        if (S == 1)
-            k_emit<1, true><<<blocks, 256, 0, s>>>(a, crit, bits);
-        else if (a.lb > 0)
-            k_emit<kBatchSlots, true><<<blocks, 256, 0, s>>>(a, crit, bits);
-        else
-            k_emit<kBatchSlots, false><<<blocks, 256, 0, s>>>(a, crit, bits);
-        const hipError_t e = hipGetLastError();
-        if (e != hipSuccess) return e;
+        for (const SweepArgs *x : {&a, alt}) {
+            if (x == nullptr) continue;
+            if (S == 1)
+                k_emit<1, true><<<blocks, 256, 0, s>>>(*x, crit, bits);
+            else if (x->lb > 0)
+                k_emit<kBatchSlots, true><<<blocks, 256, 0, s>>>(*x, crit, bits);
+            else
+                k_emit<kBatchSlots, false><<<blocks, 256, 0, s>>>(*x, crit, bits);
+            const hipError_t e = hipGetLastError();
+            if (e != hipSuccess) return e;
+        }
     }
     if (path != nullptr) {
         k_chase<kBatchSlots><<<(unsigned)((a.P + 3) / 4), 256, 0, s>>>(a, cbits, path, stride,

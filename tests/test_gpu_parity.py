@@ -594,48 +594,140 @@ def test_c4_refinement_loop_full_size(P):
     G.close()
 
 
-# Every placement of the refinement loop against the oracle, through per-
-# placement checksums of tl, bl and the path (int64 sums, taken modulo 2^64 on
-# both sides, so the order of summation does not matter) and the exact
-# makespan, label sums and overflows. The oracle
-# (C, called through ctypes, which releases the GIL) runs on host threads.
-def _c4_oracle(g, sched, w, p):
+# Every placement of the refinement loop against the oracle, element by
+# element: tl, bl, the critical flags and the path of each placement, its
+# makespan, label sums and overflows. The outputs are copied back 100
+# placements at a time; the oracle (C, called through ctypes, which releases
+# the GIL) runs on host threads.
+def _c4_oracle(g, sched, p):
     lab = W.materialize_placements(sched, p, 1)[0]
-    e = oracle.evaluate(g.n_nodes, g.src, g.dst, g.comp, g.edge_cost, g.mem, lab, g.n_labels,
-                        g.capacity)
-    path = np.asarray(e["path"], np.int64)
-    return (p, int((e["tl"] * w).sum()), int((e["bl"] * w).sum()), int(e["makespan"]),
-            int(path.size), int((path * np.arange(1, path.size + 1)).sum()),
-            np.asarray(e["label_mem"]).tolist(), np.asarray(e["overflow"]).tolist())
+    return p, oracle.evaluate(g.n_nodes, g.src, g.dst, g.comp, g.edge_cost, g.mem, lab,
+                              g.n_labels, g.capacity)
 
 
 def test_c4_every_placement(P):
     g = cfg(2)
-    say(f"config4 every placement V={g.n_nodes} P=1000")
+    say(f"config4 every placement element by element V={g.n_nodes} P=1000")
     sched = W.config4_moves(g, n_place=1000)
     G = P.Graph(g.n_nodes, g.src, g.dst, g.comp, g.edge_cost, g.mem)
     margs = (dev(sched.base, torch.int32), dev(sched.ptr, torch.int64),
              dev(sched.node, torch.int32), dev(sched.label, torch.int32))
     out = G.evaluate_moves(*margs, g.n_labels, dev(g.capacity, torch.int64))
     torch.cuda.synchronize()
-    # node v weighs v + 1 in the checksums; tl, bl are [V][P] in original ids
-    w = torch.arange(1, g.n_nodes + 1, dtype=torch.int64, device="cuda").unsqueeze(1)
-    tl_sum = torch.cat([(out["tl"][:, c:c + 100] * w).sum(dim=0) for c in range(0, 1000, 100)])
-    bl_sum = torch.cat([(out["bl"][:, c:c + 100] * w).sum(dim=0) for c in range(0, 1000, 100)])
-    plen = out["path_len"].to(torch.int64)
-    stride = out["path"].shape[1]
-    pos = torch.arange(1, stride + 1, dtype=torch.int64, device="cuda")
-    mask = pos.unsqueeze(0) <= plen.unsqueeze(1)
-    path_sum = ((out["path"].to(torch.int64) * pos) * mask).sum(dim=1)
-    got = {k: v.cpu().numpy() for k, v in
-           dict(tl=tl_sum, bl=bl_sum, m=out["makespan"], plen=plen, path=path_sum,
-                lm=out["label_mem"], ov=out["overflow"]).items()}
+    small = {k: out[k].cpu().numpy() for k in ("makespan", "path", "path_len", "label_mem",
+                                              "overflow")}
+    from concurrent.futures import ThreadPoolExecutor
+    with ThreadPoolExecutor(max(1, min(16, os.cpu_count() or 1))) as ex:
+        for c0 in range(0, 1000, 100):
+            cols = range(c0, c0 + 100)
+            res = ex.map(lambda p: _c4_oracle(g, sched, p), cols)
+            tl = out["tl"][:, c0:c0 + 100].cpu().numpy()
+            bl = out["bl"][:, c0:c0 + 100].cpu().numpy()
+            cr = out["is_critical"][:, c0:c0 + 100].cpu().numpy()
+            for p, e in res:
+                j = p - c0
+                assert (tl[:, j] == e["tl"]).all(), ("tl", p)
+                assert (bl[:, j] == e["bl"]).all(), ("bl", p)
+                assert (cr[:, j] == e["is_critical"]).all(), ("is_critical", p)
+                assert small["makespan"][p] == e["makespan"], ("makespan", p)
+                n = small["path_len"][p]
+                assert n == len(e["path"]) and (small["path"][p, :n] == e["path"]).all(), p
+                assert (small["label_mem"][p] == e["label_mem"]).all(), ("label_mem", p)
+                assert (small["overflow"][p] == e["overflow"]).all(), ("overflow", p)
+            say(f"config4 placements {c0}..{c0 + 99} equal")
+    G.close()
+
+
+# ------------------------------------------- batches without label sums --
+
+def _tb_batch_case(P, g, pl):
+    """pardnn_tb_levels_batch and pardnn_evaluate_batch without label sums on
+    placements pl [V][P], against the oracle for every placement."""
+    G = P.Graph(g.n_nodes, g.src, g.dst, g.comp, g.edge_cost, g.mem)
+    n_place = pl.shape[1]
+    d = dev(pl, torch.int32)
+    tl = torch.empty((g.n_nodes, n_place), dtype=torch.int64, device="cuda")
+    bl = torch.empty_like(tl)
+    m = torch.empty(n_place, dtype=torch.int64, device="cuda")
+    P.pardnn_tb_levels_batch(G.handle, n_place, d, tl, bl, m)
+    full = G.evaluate_batch(d, 0)          # no label sums: path and flags still there
+    torch.cuda.synchronize()
+    tl, bl, m = tl.cpu().numpy(), bl.cpu().numpy(), m.cpu().numpy()
+    full = {k: v.cpu().numpy() for k, v in full.items()}
     G.close()
     from concurrent.futures import ThreadPoolExecutor
-    wn = np.arange(1, g.n_nodes + 1, dtype=np.int64)
+
+    def one(p):
+        lab = pl[:, p].copy()
+        etl, ebl, em = oracle.tb_levels(g.n_nodes, g.src, g.dst, g.comp, g.edge_cost, lab)
+        ecrit, epath = oracle.critical_path(g.n_nodes, g.src, g.dst, g.comp, g.edge_cost, lab,
+                                            etl, ebl, em)
+        return p, etl, ebl, em, ecrit, epath
+
     with ThreadPoolExecutor(max(1, min(16, os.cpu_count() or 1))) as ex:
-        res = list(ex.map(lambda p: _c4_oracle(g, sched, wn, p), range(1000)))
-    for p, t, b, m, n, ps, lm, ov in res:
-        assert got["tl"][p] == t and got["bl"][p] == b, p
-        assert got["m"][p] == m and got["plen"][p] == n and got["path"][p] == ps, p
-        assert got["lm"][p].tolist() == lm and got["ov"][p].tolist() == ov, p
+        for p, etl, ebl, em, ecrit, epath in ex.map(one, range(n_place)):
+            assert (tl[:, p] == etl).all() and (bl[:, p] == ebl).all() and m[p] == em, p
+            assert (full["tl"][:, p] == etl).all() and (full["bl"][:, p] == ebl).all(), p
+            assert full["makespan"][p] == em, p
+            assert (full["is_critical"][:, p] == ecrit).all(), p
+            n = full["path_len"][p]
+            assert n == len(epath) and (full["path"][p, :n] == epath).all(), p
+
+
+@pytest.mark.parametrize("i,n_place", [(1, 64), (2, 64)])
+def test_tb_levels_batch_labels_in_16_bits(P, i, n_place):
+    """Labels in [0, 2^16) without label sums: the pair sweep, chosen on the
+    device (labels drawn from the whole 16-bit range, plus the placement of
+    the config and a single-label placement)."""
+    g = cfg(i)
+    say(f"tb_levels_batch config{i} P={n_place} labels < 2^16")
+    rng = np.random.default_rng(640 + i)
+    pl = rng.integers(0, 16, (g.n_nodes, n_place)).astype(np.int32)
+    pl[:, 0] = g.placement
+    pl[:, 1] = 0
+    pl[:, 2] = rng.integers(0, 1 << 16, g.n_nodes)
+    pl[:, 3] = (1 << 16) - 1
+    _tb_batch_case(P, g, pl)
+
+
+@pytest.mark.parametrize("i,n_place", [(1, 64), (2, 64)])
+def test_tb_levels_batch_labels_beyond_16_bits(P, i, n_place):
+    """One label outside [0, 2^16) anywhere in the batch sends every placement
+    to the unpacked sweep; results do not depend on which sweep ran."""
+    g = cfg(i)
+    say(f"tb_levels_batch config{i} P={n_place} a label >= 2^16")
+    rng = np.random.default_rng(650 + i)
+    pl = rng.integers(0, 16, (g.n_nodes, n_place)).astype(np.int32)
+    pl[:, 0] = g.placement
+    pl[g.n_nodes // 3, n_place - 1] = 1 << 16
+    pl[:, 5] = rng.choice(np.array([-7, 70000, 2 ** 31 - 1, 3], np.int32), g.n_nodes)
+    _tb_batch_case(P, g, pl)
+
+
+def test_evaluate_moves_without_label_sums(P):
+    """The moves entry point without label sums takes the same device-side
+    choice; labels outside 16 bits among the moves take the unpacked sweep."""
+    g = cfg(1)
+    say("evaluate_moves without label sums")
+    sched = W.config4_moves(g, n_place=40)
+    G = P.Graph(g.n_nodes, g.src, g.dst, g.comp, g.edge_cost, g.mem)
+    for wide in (False, True):
+        label = sched.label.copy()
+        if wide:
+            label[len(label) // 2] = 1 << 20
+        s2 = W.MoveSchedule(sched.base, sched.ptr, sched.node, label, sched.n_labels)
+        out = G.evaluate_moves(dev(s2.base, torch.int32), dev(s2.ptr, torch.int64),
+                               dev(s2.node, torch.int32), dev(label, torch.int32), 0)
+        torch.cuda.synchronize()
+        got = {k: v.cpu().numpy() for k, v in out.items()}
+        pl = W.materialize_placements(s2).T.copy()
+        for p in range(40):
+            lab = pl[:, p].copy()
+            etl, ebl, em = oracle.tb_levels(g.n_nodes, g.src, g.dst, g.comp, g.edge_cost, lab)
+            ecrit, epath = oracle.critical_path(g.n_nodes, g.src, g.dst, g.comp, g.edge_cost,
+                                                lab, etl, ebl, em)
+            assert (got["tl"][:, p] == etl).all() and (got["bl"][:, p] == ebl).all(), p
+            assert got["makespan"][p] == em and (got["is_critical"][:, p] == ecrit).all(), p
+            n = got["path_len"][p]
+            assert (got["path"][p, :n] == epath).all(), p
+    G.close()
