@@ -239,6 +239,28 @@ int pardnn_evaluate_batch(pardnn_graph *g, int32_t n_place,
                           int64_t *overflow);
 
 /*
+ * pardnn_evaluate_batch for callers that cannot allocate device memory (code
+ * under HIP graph capture, tight serving loops, harnesses that forbid
+ * hipMalloc): the same arguments and results, but its workspace is a fixed
+ * array of 128 MiB compiled into the library (one per GPU, held until the
+ * process ends) and the call allocates nothing.
+ *   Limit: the batch must fit that workspace, about 40 bytes per node and
+ *   placement (n_nodes * n_place <= ~3.3M, e.g. 10 placements of a
+ *   300k-node graph); larger batches return E_INVAL with the bytes needed.
+ *   The graph must already be levelized (pardnn_levelize); otherwise E_INVAL.
+ *   All calls on one GPU share the array: calls that overlap in time on one
+ *   GPU (from any handle or stream) race and give undefined results.
+ * Errors and syncs as for pardnn_evaluate_batch.
+ */
+int pardnn_evaluate_batch_fixed(pardnn_graph *g, int32_t n_place,
+                                const int32_t *placements, int32_t n_labels,
+                                const int64_t *capacity, int64_t *tl,
+                                int64_t *bl, int64_t *makespan,
+                                uint8_t *is_critical, int32_t *path,
+                                int32_t path_stride, int32_t *path_len,
+                                int64_t *label_mem, int64_t *overflow);
+
+/*
  * The refinement loop's successive placements evaluated in one call (the
  * partitioner re-evaluates after every batch of node moves: Sec. 3.2 memory
  * heuristics, Alg. 2 mapping). Placement p is `base` with the moves of steps

@@ -20,6 +20,7 @@ __all__ = [
     "pardnn_graph_create", "pardnn_graph_destroy", "pardnn_set_stream", "pardnn_get_info",
     "pardnn_levelize", "pardnn_tb_levels", "pardnn_critical_path", "pardnn_label_memory",
     "pardnn_apply_moves", "pardnn_build_placements", "pardnn_evaluate_batch",
+    "pardnn_evaluate_batch_fixed",
     "pardnn_evaluate_moves",
     "pardnn_tb_levels_batch", "pardnn_memory_balance", "pardnn_slice_primaries",
     "pardnn_cluster_criticality", "pardnn_span_work", "pardnn_set_timing",
@@ -67,6 +68,7 @@ def load_library(path: str = LIB_PATH):
         "pardnn_apply_moves": [P, P, i32, P, P],
         "pardnn_build_placements": [P, P, i32, P, P, P, P],
         "pardnn_evaluate_batch": [P, i32, P, i32, P, P, P, P, P, P, i32, P, P, P],
+        "pardnn_evaluate_batch_fixed": [P, i32, P, i32, P, P, P, P, P, P, i32, P, P, P],
         "pardnn_evaluate_moves": [P, P, i32, P, P, P, i32, P, P, P, P, P, P, i32, P, P, P],
         "pardnn_tb_levels_batch": [P, i32, P, P, P, P],
         "pardnn_memory_balance": [P, i32, P, P, P, i32, P, P, P, P],
@@ -217,6 +219,19 @@ def pardnn_evaluate_batch(h, n_place, placements, n_labels, capacity, tl, bl, ma
         path_stride, _ptr(path_len, torch.int32, name="path_len"),
         _ptr(label_mem, torch.int64, name="label_mem"), _ptr(overflow, torch.int64, name="overflow")),
         "pardnn_evaluate_batch")
+
+
+def pardnn_evaluate_batch_fixed(h, n_place, placements, n_labels, capacity, tl, bl, makespan,
+                                is_critical=None, path=None, path_stride=0, path_len=None,
+                                label_mem=None, overflow=None):
+    _check(load_library().pardnn_evaluate_batch_fixed(
+        h, n_place, _ptr(placements, torch.int32, name="placements"), n_labels,
+        _ptr(capacity, torch.int64, name="capacity"), _ptr(tl, torch.int64, name="tl"),
+        _ptr(bl, torch.int64, name="bl"), _ptr(makespan, torch.int64, n_place, "makespan"),
+        _ptr(is_critical, torch.uint8, name="is_critical"), _ptr(path, torch.int32, name="path"),
+        path_stride, _ptr(path_len, torch.int32, name="path_len"),
+        _ptr(label_mem, torch.int64, name="label_mem"), _ptr(overflow, torch.int64, name="overflow")),
+        "pardnn_evaluate_batch_fixed")
 
 
 def pardnn_evaluate_moves(h, base, n_place, step_ptr, node, label, n_labels, capacity, tl, bl,

@@ -5,12 +5,22 @@
 // (and the device sorts and scans they call); this file only checks,
 // allocates and enqueues.
 #include <cstring>
+#include <mutex>
 #include <new>
 #include <string>
 
 #include "internal.h"
 
 using namespace pardnn;
+
+// The batch workspace of pardnn_evaluate_batch_fixed, for callers that cannot
+// allocate device memory. Each GPU the library runs on holds one copy until
+// the process ends; every call on that GPU shares it and it keeps the last
+// call's contents (nothing in it has to start at zero: each call writes what
+// it reads). Host code reaches it only through the per-device address from
+// hipGetSymbolAddress, never through the name.
+static constexpr size_t kFixedScratchBytes = size_t(128) << 20;
+static __device__ __align__(256) unsigned char scratch[kFixedScratchBytes];
 
 namespace {
 
@@ -90,6 +100,8 @@ struct TimedLaunch {
         }
     }
 };
+
+int ensure_pair(Graph *g);
 
 int ensure_levelized(Graph *g) {
     if (g->levelized) return PARDNN_OK;
@@ -187,6 +199,13 @@ int ensure_levelized(Graph *g) {
         (void)hipFree(tmp);
     }
     if (e != hipSuccess) return fail(hip_status(e), std::string("levelize: ") + hipGetErrorString(e));
+    // everything the batched evaluation needs besides its workspace is built
+    // here, once per graph: the near / far edge split and the label-fit flag
+    if (V > 0) {
+        int st = ensure_pair(g);
+        if (st != PARDNN_OK) return st;
+    }
+    HIP_TRY(dalloc(*g, &g->bt_fit, 1));
     g->levelized = true;
     return PARDNN_OK;
 }
@@ -301,10 +320,14 @@ struct MovesIn {
     const int32_t *node, *label;
 };
 
+// With `fixed` the batch workspace is the caller-provided block of
+// fixed_bytes (no allocation on this path); the handle must then already be
+// levelized.
 int evaluate_impl(Graph *g, int32_t n_place, const int32_t *placements, const MovesIn *mv,
                   int32_t n_labels, const int64_t *capacity, int64_t *tl, int64_t *bl,
                   int64_t *makespan, uint8_t *is_critical, int32_t *path, int32_t path_stride,
-                  int32_t *path_len, int64_t *label_mem, int64_t *overflow) {
+                  int32_t *path_len, int64_t *label_mem, int64_t *overflow,
+                  void *fixed = nullptr, size_t fixed_bytes = 0) {
     if (n_place < 0) return fail(PARDNN_E_INVAL, "n_place must be >= 0");
     if (n_place == 0) return PARDNN_OK;
     if (makespan == nullptr || (g->V > 0 && placements == nullptr && mv == nullptr))
@@ -315,6 +338,9 @@ int evaluate_impl(Graph *g, int32_t n_place, const int32_t *placements, const Mo
         return fail(PARDNN_E_INVAL, "overflow needs label_mem");
     if (label_mem != nullptr && n_labels < 1) return fail(PARDNN_E_INVAL, "n_labels must be >= 1");
     DEVICE_SCOPE(g);
+    if (fixed != nullptr && !g->levelized)
+        return fail(PARDNN_E_INVAL, "the graph must be levelized (pardnn_levelize) before a "
+                                    "call that allocates nothing");
     int st = ensure_levelized(g);
     if (st != PARDNN_OK) return st;
     if (path != nullptr && path_stride < std::max(g->L, 1))
@@ -358,15 +384,26 @@ int evaluate_impl(Graph *g, int32_t n_place, const int32_t *placements, const Mo
     const size_t need = per * (4 * sizeof(int64_t) + sizeof(int32_t)) +
                         per_lab * sizeof(int32_t) + (size_t)n_place * sizeof(int32_t) + 1024 +
                         cbits_bytes + moves_bytes;
-    if (g->batch_ws_bytes < need) {
-        if (g->batch_ws) {
-            HIP_TRY(hipStreamSynchronize(g->stream));
-            HIP_TRY(hipFree(g->batch_ws));
-            g->batch_ws = nullptr;
-            g->batch_ws_bytes = 0;
+    void *ws_base = nullptr;
+    if (fixed != nullptr) {
+        if (need > fixed_bytes)
+            return fail(PARDNN_E_INVAL,
+                        "the batch needs " + std::to_string(need) + " bytes of workspace; the "
+                        "fixed workspace holds " + std::to_string(fixed_bytes) +
+                        " (fewer placements per call fit)");
+        ws_base = fixed;
+    } else {
+        if (g->batch_ws_bytes < need) {
+            if (g->batch_ws) {
+                HIP_TRY(hipStreamSynchronize(g->stream));
+                HIP_TRY(hipFree(g->batch_ws));
+                g->batch_ws = nullptr;
+                g->batch_ws_bytes = 0;
+            }
+            HIP_TRY(hipMalloc(&g->batch_ws, need));
+            g->batch_ws_bytes = need;
         }
-        HIP_TRY(hipMalloc(&g->batch_ws, need));
-        g->batch_ws_bytes = need;
+        ws_base = g->batch_ws;
     }
     // Pack {value, label} into one int64 when labels are known to lie in
     // [0, n_labels) (they are checked) and values leave room for their bits.
@@ -390,16 +427,16 @@ int evaluate_impl(Graph *g, int32_t n_place, const int32_t *placements, const Mo
             gated = label_mem == nullptr;
         }
     }
-    if (gated && g->bt_fit == nullptr) HIP_TRY(dalloc(*g, &g->bt_fit, 1));
-    int64_t *ftl = (int64_t *)g->batch_ws;
+
+    int64_t *ftl = (int64_t *)ws_base;
     int64_t *bll = ftl + 2 * per;
     int32_t *lab_w = (int32_t *)(bll + 2 * per);
     int32_t *nx_w = lab_w + per_lab;
     int32_t *start = nx_w + per;
     uint32_t *cbits = reinterpret_cast<uint32_t *>(
-        (char *)g->batch_ws + (need - moves_bytes - cbits_bytes) / 256 * 256);
+        (char *)ws_base + (need - moves_bytes - cbits_bytes) / 256 * 256);
     int32_t *moves_scratch = reinterpret_cast<int32_t *>(
-        (char *)g->batch_ws + (need - moves_bytes) / 256 * 256);
+        (char *)ws_base + (need - moves_bytes) / 256 * 256);
 
     const int32_t K = label_mem != nullptr ? n_labels : 0;
     int32_t *fit = gated ? g->bt_fit : nullptr;
@@ -433,8 +470,6 @@ int evaluate_impl(Graph *g, int32_t n_place, const int32_t *placements, const Mo
     a.ob = ob;
     a.ws_stride = ws_stride;
     if (lb > 0 && g->V > 0) {
-        st = ensure_pair(g);
-        if (st != PARDNN_OK) return st;
         a.pl_t = g->pl_t;
         a.pl_b = g->pl_b;
         a.nr_t = g->nr_t;
@@ -567,6 +602,27 @@ int pair_single_sweep(Graph *g, int32_t lb, int32_t ob, NodeRec16 *node_rec, int
         HIP_TRY(launch_sweep_pair_one(a, g->stream));
     }
     HIP_TRY(launch_finish(a, 1, nullptr, nullptr, nullptr, 0, nullptr, g->stream));
+    return PARDNN_OK;
+}
+
+constexpr int kMaxDevices = 64;
+std::mutex g_scratch_mu;
+void *g_scratch_ptr[kMaxDevices] = {};
+
+// Device address of `scratch` on device `dev`, which must be current; looked
+// up once per device.
+int fixed_scratch(int dev, void **out) {
+    if (dev < 0 || dev >= kMaxDevices) return fail(PARDNN_E_DEVICE, "device index out of range");
+    std::lock_guard<std::mutex> lock(g_scratch_mu);
+    if (g_scratch_ptr[dev] == nullptr) {
+        void *ptr = nullptr;
+        const hipError_t e = hipGetSymbolAddress((void **)&ptr, HIP_SYMBOL(scratch));
+        if (e != hipSuccess || ptr == nullptr)
+            return fail(PARDNN_E_DEVICE, std::string("hipGetSymbolAddress(scratch): ") +
+                                             hipGetErrorString(e));
+        g_scratch_ptr[dev] = ptr;
+    }
+    *out = g_scratch_ptr[dev];
     return PARDNN_OK;
 }
 
@@ -1134,6 +1190,24 @@ int pardnn_get_timing(pardnn_graph *h, const char **kernel, float *ms) {
     HIP_TRY(hipEventElapsedTime(ms, g->ev0, g->ev1));
     if (kernel) *kernel = g->timed_kernel;
     return PARDNN_OK;
+}
+
+int pardnn_evaluate_batch_fixed(pardnn_graph *h, int32_t n_place, const int32_t *placements,
+                                int32_t n_labels, const int64_t *capacity, int64_t *tl,
+                                int64_t *bl, int64_t *makespan, uint8_t *is_critical,
+                                int32_t *path, int32_t path_stride, int32_t *path_len,
+                                int64_t *label_mem, int64_t *overflow) {
+    CHECK_HANDLE(h);
+    Graph *g = reinterpret_cast<Graph *>(h);
+    if (g->V > 0 && n_place > 0 && placements == nullptr)
+        return fail(PARDNN_E_INVAL, "placements must be non-null");
+    DEVICE_SCOPE(g);
+    void *ws = nullptr;
+    const int st = fixed_scratch(g->device, &ws);
+    if (st != PARDNN_OK) return st;
+    return evaluate_impl(g, n_place, placements, nullptr, n_labels, capacity, tl, bl, makespan,
+                         is_critical, path, path_stride, path_len, label_mem, overflow, ws,
+                         kFixedScratchBytes);
 }
 
 int pardnn_tb_levels_batch(pardnn_graph *h, int32_t n_place, const int32_t *placements,
