@@ -222,43 +222,69 @@ from oracle.clusters import cluster_criticality  # noqa: E402
 
 def _brute_criticality(n, src, dst, comp, cost, cluster, C):
     """Enumerate every source-to-sink path; an edge inside one cluster is free.
-    Each cluster takes the longest path that visits one of its nodes."""
+    Each cluster takes the longest path on which all of its nodes appear as
+    one contiguous run (-1 when no path does)."""
     succ = [[] for _ in range(n)]
     indeg = [0] * n
     for a, b, c in zip(src, dst, cost):
         succ[a].append((b, 0 if cluster[a] == cluster[b] else c))
         indeg[b] += 1
+    size = [0] * C
+    for v in range(n):
+        size[cluster[v]] += 1
     crit = [-1] * C
 
-    def walk(v, seen, length):
+    def runs(path):
+        # clusters whose every node lies in one contiguous run of the path
+        out, i = set(), 0
+        while i < len(path):
+            j = i
+            while j + 1 < len(path) and cluster[path[j + 1]] == cluster[path[i]]:
+                j += 1
+            if j - i + 1 == size[cluster[path[i]]]:
+                out.add(cluster[path[i]])
+            i = j + 1
+        return out
+
+    def walk(v, path, length):
         length += comp[v]
-        seen = seen | {cluster[v]}
+        path = path + [v]
         if not succ[v]:
-            for c in seen:
+            for c in runs(path):
                 crit[c] = max(crit[c], length)
             return
         for b, c in succ[v]:
-            walk(b, seen, length + c)
+            walk(b, path, length + c)
 
     for v in range(n):
         if indeg[v] == 0:
-            walk(v, frozenset(), 0)
+            walk(v, [], 0)
     return crit
 
 
-@pytest.mark.parametrize("seed", range(12))
+@pytest.mark.parametrize("seed", range(40))
 def test_cluster_criticality_against_path_enumeration(seed):
     rng = np.random.default_rng(500 + seed)
-    n = int(rng.integers(1, 12))
+    n = int(rng.integers(1, 13))
     g = W.random_dag(rng, n, p_edge=float(rng.uniform(0.1, 0.6)),
                      max_weight=int(rng.integers(0, 5)), n_labels=1)
-    C = int(rng.integers(1, n + 3))          # some clusters may stay empty
-    cl = rng.integers(0, C, n)
+    cl, C = W.path_clusters(rng, g)
     crit, order = cluster_criticality(n, g.src, g.dst, g.comp, g.edge_cost, cl, C)
     brute = _brute_criticality(n, g.src.tolist(), g.dst.tolist(), g.comp.tolist(),
                                g.edge_cost.tolist(), cl.tolist(), C)
     assert crit.tolist() == brute
     assert order.tolist() == sorted(range(C), key=lambda c: (-brute[c], c))
+
+
+def test_cluster_criticality_hand_example():
+    d = json.load(open(os.path.join(GOLDEN, "criticality_whole_cluster.json")))
+    crit, order = cluster_criticality(d["n_nodes"], d["src"], d["dst"], d["comp"],
+                                      d["edge_cost"], d["cluster"], d["n_clusters"])
+    assert crit.tolist() == d["expect"]["criticality"]
+    assert order.tolist() == d["expect"]["order"]
+    # the brute force agrees, and the largest w over the cluster would not
+    assert _brute_criticality(d["n_nodes"], d["src"], d["dst"], d["comp"], d["edge_cost"],
+                              d["cluster"], d["n_clusters"]) == d["expect"]["criticality"]
 
 
 def test_cluster_criticality_special_cases():

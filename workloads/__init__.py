@@ -18,4 +18,5 @@ from .graphs import (  # noqa: F401
     chain_graph,
     layered_dag,
     node_kinds,
+    path_clusters,
 )

@@ -611,3 +611,34 @@ def layered_dag(rng: np.random.Generator, widths, fan_in, max_span: int = 4,
     label = rng.integers(0, n_labels, n).astype(np.int32)
     return SynthGraph("layered", n, src, dst, comp, cost, mem, label, n_labels,
                       np.full(n_labels, 50_000, np.int64), {"levels": len(widths)})
+
+
+def path_clusters(rng, g: SynthGraph, max_extra: int = 4, p_odd: float = 0.5):
+    """Cluster ids for the mapping stage's inputs: the nodes are covered by
+    random paths of the DAG (from a random unassigned node, up to `max_extra`
+    steps to random unassigned successors), one cluster per path; with
+    probability p_odd two unrelated nodes are then put together (usually not a
+    path); 0-2 further ids stay empty. Returns (cluster int64[V], n_clusters)."""
+    n = g.n_nodes
+    succ = [[] for _ in range(n)]
+    for a, b in zip(g.src.tolist(), g.dst.tolist()):
+        succ[a].append(b)
+    cl = np.full(n, -1, np.int64)
+    C = 0
+    for v in rng.permutation(n).tolist():
+        if cl[v] >= 0:
+            continue
+        cl[v] = C
+        u = v
+        for _ in range(int(rng.integers(0, max_extra + 1))):
+            free = [b for b in succ[u] if cl[b] < 0]
+            if not free:
+                break
+            u = free[int(rng.integers(0, len(free)))]
+            cl[u] = C
+        C += 1
+    if n >= 4 and rng.random() < p_odd:
+        a, b = rng.choice(n, 2, replace=False)
+        cl[b] = cl[a]
+    C += int(rng.integers(0, 3))
+    return cl, C
