@@ -203,6 +203,104 @@ def test_slicing_invariants():
     assert (primary >= 0).sum() == len(seen)
 
 
+from oracle.slicing import slice_all  # noqa: E402
+
+
+def _brute_secondaries(n, src, dst, comp, cost, alive):
+    """The secondary clusters of the remaining graph `alive` by enumeration:
+    w(v) is the longest source-to-sink path through v (all edges pay); then,
+    repeatedly, of all maximal paths (from a node without a remaining
+    predecessor to one without a remaining successor) the one whose sequence
+    of keys (w(v), -v) is lexicographically largest leaves the graph."""
+    alive = set(alive)
+
+    def adjacency(nodes):
+        succ = {v: [] for v in nodes}
+        indeg = {v: 0 for v in nodes}
+        for e, (a, b) in enumerate(zip(src, dst)):
+            if a in nodes and b in nodes:
+                succ[a].append((b, cost[e]))
+                indeg[b] += 1
+        return succ, indeg
+
+    succ, indeg = adjacency(alive)
+    w = {v: -1 for v in alive}
+
+    def through(v, seq, length):
+        length += comp[v]
+        seq = seq + [v]
+        if not succ[v]:
+            for x in seq:
+                w[x] = max(w[x], length)
+            return
+        for b, c in succ[v]:
+            through(b, seq, length + c)
+
+    for v in alive:
+        if indeg[v] == 0:
+            through(v, [], 0)
+    out = []
+    while alive:
+        succ, indeg = adjacency(alive)
+        best = None
+
+        def walk(v, seq):
+            nonlocal best
+            seq = seq + [v]
+            if not succ[v]:
+                key = [(w[x], -x) for x in seq]
+                if best is None or key > best[0]:
+                    best = (key, seq)
+                return
+            for b, _ in succ[v]:
+                walk(b, seq)
+
+        for v in alive:
+            if indeg[v] == 0:
+                walk(v, [])
+        out.append(best[1])
+        alive -= set(best[1])
+    return out
+
+
+@pytest.mark.parametrize("seed", range(100))
+def test_secondary_clusters_against_path_enumeration(seed):
+    rng = np.random.default_rng(700 + seed)
+    n = int(rng.integers(1, 11))
+    g = W.random_dag(rng, n, p_edge=float(rng.uniform(0.2, 0.7)),
+                     max_weight=int(rng.integers(0, 9)), n_labels=1)
+    K = int(rng.integers(0, 4))
+    cluster, paths = slice_all(g.n_nodes, g.src, g.dst, g.comp, g.edge_cost, K)
+    primary, _, _ = slice_primaries(g.n_nodes, g.src, g.dst, g.comp, g.edge_cost, K)
+    brute = _brute_secondaries(n, g.src.tolist(), g.dst.tolist(), g.comp.tolist(),
+                               g.edge_cost.tolist(), [v for v in range(n) if primary[v] < 0])
+    assert [p.tolist() for p in paths[K:]] == brute
+    for j, p in enumerate(paths):
+        assert (cluster[p] == j).all()
+    assert (cluster >= 0).all() and sum(len(p) for p in paths) == n
+
+
+def test_secondary_clusters_invariants():
+    """On the tiny layered DAG after 8 primaries: the clusters partition the
+    nodes; each secondary is a path of the graph; when it was taken its start
+    had no remaining predecessor and its end no remaining successor."""
+    g = W.make_config(0)
+    K = 8
+    cluster, paths = slice_all(g.n_nodes, g.src, g.dst, g.comp, g.edge_cost, K)
+    assert (cluster >= 0).all() and sum(len(p) for p in paths) == g.n_nodes
+    edges = set(zip(g.src.tolist(), g.dst.tolist()))
+    gone = np.zeros(g.n_nodes, bool)
+    for p in paths[:K]:
+        gone[p] = True
+    for p in paths[K:]:
+        assert all((int(a), int(b)) in edges for a, b in zip(p[:-1], p[1:]))
+        live = ~gone[g.src] & ~gone[g.dst]
+        assert not (live & (g.dst == p[0])).any()       # start: no remaining predecessor
+        assert not (live & (g.src == p[-1])).any()      # end: a dead end
+        gone[p] = True
+    assert len(paths) > K + 1
+
+
 def test_slicing_chain_and_exhaustion():
     rng = np.random.default_rng(9)
     g = W.chain_graph(rng, 12)
