@@ -374,6 +374,33 @@ int pardnn_slice_primaries(pardnn_graph *g, int32_t K, int32_t *primary,
                            int32_t *paths, int32_t path_stride,
                            int32_t *path_len, int64_t *makespan);
 
+/*
+ * Graph slicing in full (Alg. 1, Sec. 3.1.1): the K primary clusters exactly
+ * as pardnn_slice_primaries finds them, then the secondary clusters. Past K
+ * paths the weighted levels are no longer recomputed: with the priorities
+ * w = tl + bl of the graph left after the K-th primary (every edge paying its
+ * cost), each further path starts at the remaining node without a remaining
+ * predecessor of largest w, steps to the remaining successor of largest w and
+ * ends at a node without a remaining successor (a single node when the start
+ * has none); ties in w go to the smaller node id. The path and its edges
+ * leave the graph, and walks continue until no node remains.
+ * Outputs (device, caller-allocated):
+ *   cluster        int32[n_nodes]: cluster of each node; primaries 0..K-1,
+ *                  secondaries K, K+1, ... in the order found.
+ *   cluster_off    int32[n_nodes + K + 1]: cluster c holds
+ *                  cluster_nodes[cluster_off[c] .. cluster_off[c+1]) (a
+ *                  primary of an exhausted graph is empty).
+ *   cluster_nodes  int32[n_nodes]: every cluster's nodes in path order.
+ *   n_clusters     int32[1] (device): the number of clusters, K + secondaries.
+ *   makespan       int64[K] or NULL: as for pardnn_slice_primaries.
+ * The walk itself is sequential; it runs in one wave on the GPU (see the
+ * design notes). Environment: PARDNN_PEEL_GLOBAL_MAPS=1 keeps the walk's bit
+ * maps in device memory even when they fit in LDS (for testing).
+ * Errors: E_INVAL (K < 0, null pointers), E_CYCLE, E_DEVICE. Syncs.
+ */
+int pardnn_slice_graph(pardnn_graph *g, int32_t K, int32_t *cluster, int32_t *cluster_off,
+                       int32_t *cluster_nodes, int32_t *n_clusters, int64_t *makespan);
+
 /* pardnn_evaluate_batch restricted to tl, bl and makespan. No sync. */
 int pardnn_tb_levels_batch(pardnn_graph *g, int32_t n_place,
                            const int32_t *placements, int64_t *tl, int64_t *bl,

@@ -23,6 +23,7 @@ __all__ = [
     "pardnn_evaluate_batch_fixed",
     "pardnn_evaluate_moves",
     "pardnn_tb_levels_batch", "pardnn_memory_balance", "pardnn_slice_primaries",
+    "pardnn_slice_graph",
     "pardnn_cluster_criticality", "pardnn_span_work", "pardnn_set_timing",
     "pardnn_get_timing", "pardnn_status_string", "pardnn_last_error",
 ]
@@ -73,6 +74,7 @@ def load_library(path: str = LIB_PATH):
         "pardnn_tb_levels_batch": [P, i32, P, P, P, P],
         "pardnn_memory_balance": [P, i32, P, P, P, i32, P, P, P, P],
         "pardnn_slice_primaries": [P, i32, P, P, i32, P, P],
+        "pardnn_slice_graph": [P, i32, P, P, P, P, P],
         "pardnn_cluster_criticality": [P, P, i32, P, P],
         "pardnn_span_work": [P, P, i32, P, i32, P, P, P, P, P, P],
         "pardnn_set_timing": [P, ctypes.c_int],
@@ -276,6 +278,16 @@ def pardnn_slice_primaries(h, K, primary, paths, path_stride, path_len, makespan
         "pardnn_slice_primaries")
 
 
+def pardnn_slice_graph(h, K, cluster, cluster_off, cluster_nodes, n_clusters, makespan=None):
+    n = _n_nodes(h)
+    _check(load_library().pardnn_slice_graph(
+        h, K, _ptr(cluster, torch.int32, n, "cluster"),
+        _ptr(cluster_off, torch.int32, n + K + 1, "cluster_off"),
+        _ptr(cluster_nodes, torch.int32, n, "cluster_nodes"),
+        _ptr(n_clusters, torch.int32, 1, "n_clusters"),
+        _ptr(makespan, torch.int64, K, "makespan")), "pardnn_slice_graph")
+
+
 def pardnn_cluster_criticality(h, cluster, n_clusters, criticality, order):
     C = max(n_clusters, 0)
     _check(load_library().pardnn_cluster_criticality(
@@ -465,6 +477,22 @@ class Graph:
         pardnn_slice_primaries(self._h, K, out["primary"], out["paths"], stride,
                                out["path_len"], out["makespan"])
         return out
+
+    def slice_graph(self, K):
+        """Graph slicing in full: primaries and secondaries (see
+        pardnn_slice_graph). Returns cluster [V], the clusters as a list of
+        node-id tensors in path order, and the primaries' makespans."""
+        V, dev = self.n_nodes, self.device
+        cluster = torch.empty(V, dtype=torch.int32, device=dev)
+        off = torch.empty(V + K + 1, dtype=torch.int32, device=dev)
+        nodes = torch.empty(max(V, 1), dtype=torch.int32, device=dev)
+        n = torch.empty(1, dtype=torch.int32, device=dev)
+        ms = torch.empty(max(K, 1), dtype=torch.int64, device=dev)
+        pardnn_slice_graph(self._h, K, cluster, off, nodes, n, ms if K > 0 else None)
+        nc = int(n.item())
+        offs = off[: nc + 1].cpu().tolist()
+        return {"cluster": cluster, "cluster_off": off[: nc + 1], "cluster_nodes": nodes[:V],
+                "paths": [nodes[offs[c]:offs[c + 1]] for c in range(nc)], "makespan": ms[:K]}
 
     def evaluate_batch(self, placements, n_labels=0, capacity=None, crit=True, path=True,
                        labels=True):

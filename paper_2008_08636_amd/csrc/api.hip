@@ -4,6 +4,7 @@
 // labelmem.hip, heuristics.hip, slicing.hip, clusters.hip and spanwork.hip
 // (and the device sorts and scans they call); this file only checks,
 // allocates and enqueues.
+#include <cstdlib>
 #include <cstring>
 #include <mutex>
 #include <new>
@@ -670,6 +671,11 @@ int pardnn_graph_create(int32_t n_nodes, int64_t n_edges, const int32_t *src, co
         delete g;
         return fail(PARDNN_E_DEVICE, "hipGetDevice failed");
     }
+    int lds = 0;
+    if (hipDeviceGetAttribute(&lds, hipDeviceAttributeMaxSharedMemoryPerBlock, g->device) ==
+            hipSuccess &&
+        lds > 0)
+        g->lds_max = (size_t)lds;
     g->stream = (hipStream_t)stream;
     g->V = n_nodes;
     g->E = n_edges;
@@ -956,7 +962,7 @@ int pardnn_cluster_criticality(pardnn_graph *h, const int32_t *cluster, int32_t 
         HIP_TRY(dalloc(*g, &g->cl_bl, V));
         HIP_TRY(dalloc(*g, &g->cl_m, 1));
     }
-    const size_t sort_bytes = (cluster_sort_bytes(n_clusters) + 255) / 256 * 256;
+    const size_t sort_bytes = (cluster_sort_bytes(V, n_clusters) + 255) / 256 * 256;
     HIP_TRY(grow_aux(g, sort_bytes + cluster_relabel_bytes(V, n_clusters)));
     HIP_TRY(launch_fill_i32(g->err, 4, 0, g->stream));
     // The pair sweep packs labels below 2^16. The cluster ids fit when there
@@ -1011,6 +1017,82 @@ int pardnn_cluster_criticality(pardnn_graph *h, const int32_t *cluster, int32_t 
     return PARDNN_OK;
 }
 
+}  // extern "C"
+
+namespace {
+
+// The K rounds of Alg. 1 (slicing primaries) on a levelized graph with V > 0;
+// with `then_levels`, one more evaluation of the graph that remains (its tl /
+// bl in sl_tl / sl_bl), for the secondary clusters.
+int slice_rounds(Graph *g, int32_t K, int32_t *primary, int32_t *paths, int32_t path_stride,
+                 int32_t *path_len, int64_t *makespan, bool then_levels) {
+    const int32_t V = g->V;
+    if (!g->sl_node_rec) {
+        HIP_TRY(dalloc(*g, &g->sl_node_rec, V));
+        HIP_TRY(dalloc(*g, &g->sl_comp, V));
+        HIP_TRY(dalloc(*g, &g->sl_tl, V));
+        HIP_TRY(dalloc(*g, &g->sl_bl, V));
+        HIP_TRY(dalloc(*g, &g->sl_alive, V));
+        HIP_TRY(dalloc(*g, &g->sl_crit, V));
+        HIP_TRY(dalloc(*g, &g->sl_iota, V));
+        HIP_TRY(dalloc(*g, &g->sl_start, 1));
+        HIP_TRY(dalloc(*g, &g->sl_m, 1));
+        // every node its own label: before placement all communication counts
+        HIP_TRY(launch_iota_i32(g->sl_iota, V, g->stream));
+    }
+    // a removed node weighs -B with B above every path length
+    const int64_t big = g->weight_bound < INT64_MAX ? g->weight_bound + 1 : INT64_MAX;
+    HIP_TRY(launch_slice_init(*g, g->sl_node_rec, g->sl_comp, g->sl_alive, primary));
+    // Every edge joins two levels, so the level as label makes every edge pay,
+    // as distinct labels do: with fewer than 2^16 levels the rounds can take
+    // the pair sweep (values lie in [-B, B]).
+    int32_t lb = 0, ob = 0;
+    const bool pair = (K > 0 || then_levels) && big < INT64_MAX &&
+                      pair_single_bits(g, g->L, big, &lb, &ob);
+    if (pair) {
+        const int st = pair_single_labels(g, g->level);
+        if (st != PARDNN_OK) return st;
+    }
+    auto sweep = [&](int64_t *m) -> int {
+        if (pair)
+            return pair_single_sweep(g, lb, ob, g->sl_node_rec, g->sl_comp, g->sl_tl, g->sl_bl, m);
+        SweepArgs a = sweep_args(g);
+        a.P = 1;
+        a.K = 0;
+        a.lab_w = g->order;   // pairwise distinct labels in level-major order
+        a.lab_stride = V;
+        a.ftl = g->ft_lm;
+        a.bll = g->bl_lm;
+        a.ws_stride = V;
+        a.tl_out = g->sl_tl;
+        a.bl_out = g->sl_bl;
+        a.makespan = m;
+        a.node_rec = g->sl_node_rec;
+        a.comp_lm = g->sl_comp;
+        TimedLaunch t(g, "k_sweep<1>");
+        HIP_TRY(launch_sweep(a, 1, g->stream));
+        return PARDNN_OK;
+    };
+    for (int32_t j = 0; j < K; j++) {
+        int st = sweep(makespan + j);
+        if (st != PARDNN_OK) return st;
+        HIP_TRY(launch_slice_makespan(*g, g->sl_alive, g->sl_tl, g->sl_bl, makespan + j));
+        HIP_TRY(launch_crit_next(*g, g->sl_iota, g->sl_comp, g->sl_tl, g->sl_bl, makespan + j,
+                                 g->sl_crit));
+        HIP_TRY(launch_slice_start(*g, g->sl_alive, g->sl_start));
+        int32_t *pj = paths + (int64_t)j * path_stride;
+        HIP_TRY(launch_chase_from(*g, g->sl_start, pj, path_len + j));
+        HIP_TRY(launch_slice_remove(*g, j, pj, path_len + j, big, g->sl_node_rec, g->sl_comp,
+                                    g->sl_alive, primary));
+    }
+    if (then_levels) return sweep(g->sl_m);
+    return PARDNN_OK;
+}
+
+}  // namespace
+
+extern "C" {
+
 int pardnn_slice_primaries(pardnn_graph *h, int32_t K, int32_t *primary, int32_t *paths,
                            int32_t path_stride, int32_t *path_len, int64_t *makespan) {
     CHECK_HANDLE(h);
@@ -1024,69 +1106,62 @@ int pardnn_slice_primaries(pardnn_graph *h, int32_t K, int32_t *primary, int32_t
     if (st != PARDNN_OK) return st;
     if (K > 0 && path_stride < std::max(g->L, 1))
         return fail(PARDNN_E_INVAL, "path_stride must be at least the number of levels");
-    const int32_t V = g->V;
-    if (V == 0) {
+    if (g->V == 0) {
         if (K > 0) {
             HIP_TRY(launch_fill_i32(path_len, K, 0, g->stream));
             HIP_TRY(launch_fill_i64(makespan, K, 0, g->stream));
         }
         return PARDNN_OK;
     }
-    if (!g->sl_node_rec) {
-        HIP_TRY(dalloc(*g, &g->sl_node_rec, V));
-        HIP_TRY(dalloc(*g, &g->sl_comp, V));
-        HIP_TRY(dalloc(*g, &g->sl_tl, V));
-        HIP_TRY(dalloc(*g, &g->sl_bl, V));
-        HIP_TRY(dalloc(*g, &g->sl_alive, V));
-        HIP_TRY(dalloc(*g, &g->sl_crit, V));
-        HIP_TRY(dalloc(*g, &g->sl_iota, V));
-        HIP_TRY(dalloc(*g, &g->sl_start, 1));
-        // every node its own label: before placement all communication counts
-        HIP_TRY(launch_iota_i32(g->sl_iota, V, g->stream));
+    return slice_rounds(g, K, primary, paths, path_stride, path_len, makespan, false);
+}
+
+int pardnn_slice_graph(pardnn_graph *h, int32_t K, int32_t *cluster, int32_t *cluster_off,
+                       int32_t *cluster_nodes, int32_t *n_clusters, int64_t *makespan) {
+    CHECK_HANDLE(h);
+    Graph *g = reinterpret_cast<Graph *>(h);
+    if (K < 0) return fail(PARDNN_E_INVAL, "K must be >= 0");
+    if (cluster_off == nullptr || n_clusters == nullptr ||
+        (g->V > 0 && (cluster == nullptr || cluster_nodes == nullptr)))
+        return fail(PARDNN_E_INVAL, "cluster, cluster_off, cluster_nodes and n_clusters must "
+                                    "be non-null");
+    DEVICE_SCOPE(g);
+    int st = ensure_levelized(g);
+    if (st != PARDNN_OK) return st;
+    const int32_t V = g->V;
+    const int32_t stride = std::max(g->L, 1);
+    // scratch: primary paths [K][stride], their lengths and makespans, then
+    // the walk's own space
+    const size_t paths_bytes = ((size_t)K * stride * 4 + 255) / 256 * 256;
+    const size_t small_bytes = ((size_t)K * 12 + 255) / 256 * 256;
+    HIP_TRY(grow_aux(g, paths_bytes + small_bytes + peel_scratch_bytes(V, g->E)));
+    char *base = reinterpret_cast<char *>(g->aux_scratch);
+    int32_t *paths = reinterpret_cast<int32_t *>(base);
+    int64_t *ms = reinterpret_cast<int64_t *>(base + paths_bytes);
+    int32_t *plen = reinterpret_cast<int32_t *>(ms + K);
+    void *peel = base + paths_bytes + small_bytes;
+    HIP_TRY(launch_fill_i32(g->err, 4, 0, g->stream));
+    if (V == 0) {
+        HIP_TRY(launch_fill_i32(cluster_off, (int64_t)K + 1, 0, g->stream));
+        HIP_TRY(launch_fill_i32(n_clusters, 1, K, g->stream));
+        if (makespan != nullptr && K > 0) HIP_TRY(launch_fill_i64(makespan, K, 0, g->stream));
+        return PARDNN_OK;
     }
-    // a removed node weighs -B with B above every path length
-    const int64_t big = g->weight_bound < INT64_MAX ? g->weight_bound + 1 : INT64_MAX;
-    HIP_TRY(launch_slice_init(*g, g->sl_node_rec, g->sl_comp, g->sl_alive, primary));
-    // Every edge joins two levels, so the level as label makes every edge pay,
-    // as distinct labels do: with fewer than 2^16 levels the rounds can take
-    // the pair sweep (values lie in [-B, B]).
-    int32_t lb = 0, ob = 0;
-    const bool pair = K > 0 && big < INT64_MAX && pair_single_bits(g, g->L, big, &lb, &ob);
-    if (pair) {
-        st = pair_single_labels(g, g->level);
-        if (st != PARDNN_OK) return st;
+    st = slice_rounds(g, K, cluster, paths, stride, plen, makespan != nullptr ? makespan : ms,
+                      true);
+    if (st != PARDNN_OK) return st;
+    const char *env = std::getenv("PARDNN_PEEL_GLOBAL_MAPS");
+    const bool force_global = env != nullptr && env[0] == '1';
+    const bool lds = !force_global && peel_lds_bytes(V) <= g->lds_max;
+    {
+        TimedLaunch t(g, "secondary clusters");
+        HIP_TRY(launch_slice_secondaries(*g, K, paths, stride, plen, g->sl_tl, g->sl_bl,
+                                         g->sl_alive, cluster, cluster_off, cluster_nodes,
+                                         n_clusters, peel, lds, g->err));
     }
-    for (int32_t j = 0; j < K; j++) {
-        if (pair) {
-            st = pair_single_sweep(g, lb, ob, g->sl_node_rec, g->sl_comp, g->sl_tl, g->sl_bl,
-                                   makespan + j);
-            if (st != PARDNN_OK) return st;
-        } else {
-            SweepArgs a = sweep_args(g);
-            a.P = 1;
-            a.K = 0;
-            a.lab_w = g->order;   // pairwise distinct labels in level-major order
-            a.lab_stride = V;
-            a.ftl = g->ft_lm;
-            a.bll = g->bl_lm;
-            a.ws_stride = V;
-            a.tl_out = g->sl_tl;
-            a.bl_out = g->sl_bl;
-            a.makespan = makespan + j;
-            a.node_rec = g->sl_node_rec;
-            a.comp_lm = g->sl_comp;
-            TimedLaunch t(g, "k_sweep<1>");
-            HIP_TRY(launch_sweep(a, 1, g->stream));
-        }
-        HIP_TRY(launch_slice_makespan(*g, g->sl_alive, g->sl_tl, g->sl_bl, makespan + j));
-        HIP_TRY(launch_crit_next(*g, g->sl_iota, g->sl_comp, g->sl_tl, g->sl_bl, makespan + j,
-                                 g->sl_crit));
-        HIP_TRY(launch_slice_start(*g, g->sl_alive, g->sl_start));
-        int32_t *pj = paths + (int64_t)j * path_stride;
-        HIP_TRY(launch_chase_from(*g, g->sl_start, pj, path_len + j));
-        HIP_TRY(launch_slice_remove(*g, j, pj, path_len + j, big, g->sl_node_rec, g->sl_comp,
-                                    g->sl_alive, primary));
-    }
+    st = read_errors(g);
+    if (st != PARDNN_OK) return st;
+    if (g->h_err[0] & 1) return fail(PARDNN_E_DEVICE, "the secondary walk stopped early");
     return PARDNN_OK;
 }
 

@@ -53,6 +53,7 @@ struct SpanCache {
 
 struct Graph {
     int device = 0;
+    size_t lds_max = 65536;   // LDS bytes a workgroup may use on the device
     hipStream_t stream = nullptr;
     int32_t V = 0;
     int64_t E = 0;
@@ -97,6 +98,7 @@ struct Graph {
     int64_t *sl_comp = nullptr, *sl_tl = nullptr, *sl_bl = nullptr;
     uint8_t *sl_alive = nullptr, *sl_crit = nullptr;
     int32_t *sl_iota = nullptr, *sl_start = nullptr;
+    int64_t *sl_m = nullptr;   // makespan of the evaluation after the last round
     // one placement through the batched pair sweep (two slots, one idle):
     // ftl, bll [V + pad][2] packed, labels [V][2]; allocated on first use
     int64_t *ps_ftl = nullptr, *ps_bll = nullptr;
@@ -222,14 +224,17 @@ hipError_t launch_span_work(const Graph &g, const int32_t *label, int32_t K,
                             int32_t *choice, void *scratch, SpanCache *cache, int32_t *err);
 
 // ---- clusters.hip ----
-size_t cluster_sort_bytes(int32_t n);
+// scratch of launch_cluster_criticality for V nodes and n clusters
+size_t cluster_sort_bytes(int32_t V, int32_t n);
 // labels with the cluster ids' equality on every edge, in [0, L + n_multi):
 // *lab (int32[V], original ids) and *n_multi (device) point into scratch
 size_t cluster_relabel_bytes(int32_t V, int32_t C);
 hipError_t launch_cluster_relabel(const Graph &g, const int32_t *cluster, int32_t C,
                                   int32_t *scratch, int32_t **lab, int32_t **n_multi);
-// criticality[c] = max over nodes of cluster c of tl + bl (-1: none); order:
-// cluster ids by (criticality desc, id asc); err bit 0: cluster id out of range
+// criticality[c] = tl(first) + sum of comp + bl(last) - comp(last) for a
+// cluster whose nodes in (level, id) order form a path, else -1 (also when it
+// has no node); order: cluster ids by (criticality desc, id asc); err bit 0:
+// cluster id out of range
 hipError_t launch_cluster_criticality(const Graph &g, const int32_t *cluster, int32_t n_clusters,
                                       const int64_t *tl, const int64_t *bl, int64_t *crit,
                                       int32_t *order, void *scratch, size_t scratch_bytes,
@@ -243,6 +248,21 @@ hipError_t launch_slice_start(const Graph &g, const uint8_t *alive_lm, int32_t *
 hipError_t launch_slice_remove(const Graph &g, int32_t round, const int32_t *path,
                                const int32_t *path_len, int64_t big, NodeRec16 *node_rec_s,
                                int64_t *comp_lm_s, uint8_t *alive_lm, int32_t *primary);
+// ---- peel.hip ----
+size_t peel_scratch_bytes(int32_t V, int64_t E);
+size_t peel_lds_bytes(int32_t V);
+// The secondary clusters after K primaries (paths [K][stride], plen [K],
+// device): with tl / bl of the remaining graph (original ids) and its
+// remaining nodes alive_lm, fills cluster (secondaries K, K + 1, ...; the
+// primaries' entries are already set), cl_off [n_clusters + 1], cl_nodes [V]
+// (every cluster's nodes in path order) and n_clusters (device). lds_maps:
+// the walk's bit maps in LDS (peel_lds_bytes(V) of it), else in scratch.
+// err bit 0: the walk stopped early (inconsistent state; cannot happen).
+hipError_t launch_slice_secondaries(const Graph &g, int32_t K, const int32_t *paths,
+                                    int32_t stride, const int32_t *plen, const int64_t *tl,
+                                    const int64_t *bl, const uint8_t *alive_lm, int32_t *cluster,
+                                    int32_t *cl_off, int32_t *cl_nodes, int32_t *n_clusters,
+                                    void *scratch, bool lds_maps, int32_t *err);
 hipError_t launch_critical_path(const Graph &g, const int32_t *placement, const int64_t *tl,
                                 const int64_t *bl, const int64_t *makespan,
                                 uint8_t *is_critical, int32_t *path, int32_t *path_len);

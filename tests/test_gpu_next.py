@@ -218,14 +218,34 @@ def check_clusters(P, g, cl, C):
 
 
 def test_clusters_small_random(P):
+    """Random DAGs with clusters made of random paths (a few groupings that
+    are no path among them) and with arbitrary groupings (mostly no path)."""
     say("cluster criticality small random DAGs")
     rng = np.random.default_rng(91)
-    for t in range(20):
+    for t in range(40):
         n = int(rng.integers(1, 60))
         g = W.random_dag(rng, n, p_edge=float(rng.uniform(0.05, 0.4)),
                          max_weight=int(rng.integers(0, 6)), n_labels=1)
-        C = int(rng.integers(1, n + 5))
-        check_clusters(P, g, rng.integers(0, C, n).astype(np.int32), C)
+        if t % 4 == 3:
+            C = int(rng.integers(1, n + 5))
+            cl = rng.integers(0, C, n)
+        else:
+            cl, C = W.path_clusters(rng, g, max_extra=int(rng.integers(1, 12)))
+        check_clusters(P, g, cl.astype(np.int32), C)
+
+
+def test_clusters_hand_example(P):
+    say("cluster criticality hand example")
+    d = json.load(open(os.path.join(GOLDEN, "criticality_whole_cluster.json")))
+    n = d["n_nodes"]
+    G = P.Graph(n, np.array(d["src"], np.int32), np.array(d["dst"], np.int32),
+                np.array(d["comp"], np.int64), np.array(d["edge_cost"], np.int64),
+                np.zeros(n, np.int64))
+    crit, order = G.cluster_criticality(dev(d["cluster"], torch.int32), d["n_clusters"])
+    torch.cuda.synchronize()
+    assert crit.cpu().numpy().tolist() == d["expect"]["criticality"]
+    assert order.cpu().numpy().tolist() == d["expect"]["order"]
+    G.close()
 
 
 @pytest.mark.parametrize("i", [0, 1, 2])
@@ -257,6 +277,8 @@ def test_clusters_label_paths(P):
     check_clusters(P, g, alone, n)
     mixed = np.where(np.arange(n) % 3 == 0, np.arange(n) // 3, n).astype(np.int32)
     check_clusters(P, g, mixed, n + 1)                   # one large cluster + lone nodes
+    runs = (np.arange(n) // 7).astype(np.int32)          # paths of 7 chain nodes
+    check_clusters(P, g, runs, int(runs.max()) + 1)
 
 
 def test_clusters_errors(P):
@@ -525,3 +547,68 @@ def test_binding_rejects_short_buffers(P):
                                      device="cuda"), torch.empty(4, dtype=torch.int32,
                                                                  device="cuda"))
     G.close()
+
+
+# ---------------------------------------------------------------------------
+# Graph slicing in full (Alg. 1): primaries and secondaries, pardnn_slice_graph
+# ---------------------------------------------------------------------------
+from oracle.slicing import slice_all  # noqa: E402
+
+
+def check_slice_all(P, g, K):
+    G = P.Graph(g.n_nodes, g.src, g.dst, g.comp, g.edge_cost, g.mem)
+    out = G.slice_graph(K)
+    torch.cuda.synchronize()
+    cluster = out["cluster"].cpu().numpy()
+    paths = [p.cpu().numpy() for p in out["paths"]]
+    G.close()
+    ecl, epaths = slice_all(g.n_nodes, g.src, g.dst, g.comp, g.edge_cost, K)
+    assert len(paths) == len(epaths), (len(paths), len(epaths))
+    for j, (a, b) in enumerate(zip(paths, epaths)):
+        assert a.tolist() == b.tolist(), j
+    assert (cluster == ecl).all()
+
+
+def test_slice_graph_small_random(P):
+    say("slice_graph small random DAGs")
+    rng = np.random.default_rng(710)
+    for t in range(40):
+        n = int(rng.integers(0, 60)) if t > 1 else t
+        g = W.random_dag(rng, n, p_edge=float(rng.uniform(0.02, 0.5)),
+                         max_weight=int(rng.integers(0, 6)), n_labels=1)
+        check_slice_all(P, g, int(rng.integers(0, 6)))
+
+
+def test_slice_graph_hubs_and_long_lists(P):
+    """Nodes with more successors than a record holds inline, and with
+    hundreds of them (the walk's list path)."""
+    say("slice_graph hubs")
+    rng = np.random.default_rng(711)
+    g = level_hub_graph(rng)
+    for K in (0, 1, 3):
+        check_slice_all(P, g, K)
+
+
+def level_hub_graph(rng):
+    widths = [1, 300, 2, 40, 1, 200, 7]
+    fan = [1, 1, 300, 2, 40, 1, 150]
+    return W.layered_dag(rng, widths, fan, max_span=3, n_labels=1)
+
+
+@pytest.mark.parametrize("i,K", [(0, 8), (1, 8), (2, 16)])
+def test_slice_graph_configs(P, i, K):
+    g = W.make_config(i)
+    say(f"slice_graph config{i} K={K} V={g.n_nodes}")
+    check_slice_all(P, g, K)
+
+
+def test_slice_graph_maps_in_device_memory(P):
+    """The walk with its bit maps in device memory (as for graphs too large
+    for LDS) gives the same clusters."""
+    g = W.make_config(1)
+    say(f"slice_graph config1 maps in device memory V={g.n_nodes}")
+    os.environ["PARDNN_PEEL_GLOBAL_MAPS"] = "1"
+    try:
+        check_slice_all(P, g, 4)
+    finally:
+        del os.environ["PARDNN_PEEL_GLOBAL_MAPS"]
