@@ -220,8 +220,13 @@ def bench_single(args, child) -> int:
         g = W.make_config(i)
         V, E, K = g.n_nodes, g.n_edges, g.n_labels
         G = P.Graph(V, g.src, g.dst, g.comp, g.edge_cost, g.mem)
-        L = P.pardnn_levelize(G.handle)
         P.pardnn_set_timing(G.handle, True)
+        torch.cuda.synchronize()
+        t0 = time.perf_counter()
+        L = P.pardnn_levelize(G.handle)
+        torch.cuda.synchronize()
+        levelize_ms = (time.perf_counter() - t0) * 1e3
+        kahn_ms = P.pardnn_get_timing(G.handle)[1]
         lab = torch.as_tensor(g.placement, dtype=torch.int32).cuda()
         cap = torch.as_tensor(g.capacity, dtype=torch.int64).cuda()
         tl = torch.empty(V, dtype=torch.int64, device="cuda")
@@ -253,6 +258,7 @@ def bench_single(args, child) -> int:
         wall = (time.perf_counter() - t0) * 1e3 / steps
         sweep_ms = float(np.mean(ks))
         per[f"config{i}"] = {"workload": names[i], "V": V, "E": E, "levels": L,
+                             "levelize_ms": round(levelize_ms, 3), "k_kahn_ms": round(kahn_ms, 3),
                              "ms": round(wall, 4), "sweep_ms": round(sweep_ms, 4),
                              "us_per_level": round(sweep_ms * 1e3 / max(L, 1), 4),
                              "gteps": round(2 * E / (wall / 1e3) / 1e9, 4)}

@@ -115,7 +115,7 @@ int ensure_levelized(Graph *g) {
     }
     // scratch: in-degree counters, the release queue, the result words, then
     // the level sort's own space
-    const size_t sort_bytes = level_order_scratch_bytes(V);
+    const size_t sort_bytes = std::max(level_order_scratch_bytes(V), kahn_rec_bytes(V));
     const size_t head = (((size_t)V + 1) * 2 * sizeof(int32_t) + 8 + 255) / 256 * 256;
     char *work = nullptr;
     auto cleanup = [&]() {
@@ -131,7 +131,7 @@ int ensure_levelized(Graph *g) {
                            hipMemcpyDeviceToDevice, g->stream);
     if (e == hipSuccess) {
         TimedLaunch t(g, "k_kahn");
-        e = launch_kahn(*g, indeg_work, queue, result);
+        e = launch_kahn(*g, indeg_work, queue, result, work + head);
     }
     int32_t h_result[2] = {0, 0};
     if (e == hipSuccess)
@@ -556,6 +556,47 @@ int pair_single_labels(Graph *g, const int32_t *labels) {
     return PARDNN_OK;
 }
 
+// Levels wider than this many nodes are computed grid-wide between chain
+// segments in single-placement sweeps (environment PARDNN_WIDE_LEVEL; 0 or
+// less: never).
+int32_t wide_level_threshold() {
+    const char *e = std::getenv("PARDNN_WIDE_LEVEL");
+    if (e != nullptr && e[0] != 0) return (int32_t)std::strtol(e, nullptr, 10);
+    return 512;
+}
+
+// The plan of a segmented sweep for threshold `thr`: per direction, runs of
+// chain steps and the wide levels between them (cached on the handle).
+int seg_plan(Graph *g, int32_t thr) {
+    if (g->seg_thresh == thr) return PARDNN_OK;
+    if (g->h_linfo.empty()) {   // once per graph: the level bounds on the host
+        g->h_linfo.resize((size_t)g->L + 2);
+        HIP_TRY(hipMemcpyAsync(g->h_linfo.data(), g->linfo, sizeof(LevelInfo) * ((size_t)g->L + 2),
+                               hipMemcpyDeviceToHost, g->stream));
+        HIP_TRY(hipStreamSynchronize(g->stream));
+    }
+    g->seg_thresh = thr;
+    g->seg_t.clear();
+    g->seg_b.clear();
+    const int32_t L = g->L;
+    auto wide = [&](int32_t x) {
+        return thr > 0 && g->h_level_ptr[x + 1] - g->h_level_ptr[x] > thr;
+    };
+    for (int d = 0; d < 2; d++) {
+        std::vector<SegItem> &out = d == 0 ? g->seg_t : g->seg_b;
+        int32_t start = 0;
+        for (int32_t st = 0; st < L; st++) {
+            const int32_t x = d == 0 ? st : L - 1 - st;
+            if (!wide(x)) continue;
+            if (st > start) out.push_back({0, start, st});
+            out.push_back({1, x, 0});
+            start = st + 1;
+        }
+        if (start < L) out.push_back({0, start, L});
+    }
+    return PARDNN_OK;
+}
+
 // tl, bl (original order) and the level-0 makespan of the labels set by
 // pair_single_labels, with the given node weights; with `gate`, the launches
 // run only if *gate == 1
@@ -596,11 +637,66 @@ int pair_single_sweep(Graph *g, int32_t lb, int32_t ob, NodeRec16 *node_rec, int
     a.pretie_b = g->pretie_b;
     a.gate = gate;
     a.gate_want = 1;
-    if (timed) {
-        TimedLaunch t(g, "k_sweep_pair<1>");
-        HIP_TRY(launch_sweep_pair_one(a, g->stream));
+    const int32_t thr = wide_level_threshold();
+    const bool segmented = thr > 0 && g->max_width > thr;
+    if (!segmented) {
+        if (timed) {
+            TimedLaunch t(g, "k_sweep_pair<1>");
+            HIP_TRY(launch_sweep_pair_one(a, g->stream));
+        } else {
+            HIP_TRY(launch_sweep_pair_one(a, g->stream));
+        }
     } else {
-        HIP_TRY(launch_sweep_pair_one(a, g->stream));
+        // chain segments for the narrow runs, grid-wide passes for the wide
+        // levels; the t and b plans advance one item per round, paired in the
+        // same launches (the two directions are independent)
+        st = seg_plan(g, thr);
+        if (st != PARDNN_OK) return st;
+        if (!g->ps_acc) {
+            HIP_TRY(dalloc(*g, &g->ps_acc, 2 * (size_t)std::max(g->max_width, 1)));
+            HIP_TRY(launch_fill_i64(reinterpret_cast<int64_t *>(g->ps_acc),
+                                    2 * (int64_t)std::max(g->max_width, 1), 0, g->stream));
+        }
+        auto run = [&]() -> int {
+        const size_t nt = g->seg_t.size(), nb = g->seg_b.size();
+        for (size_t r = 0; r < std::max(nt, nb); r++) {
+            const SegItem *it = r < nt ? &g->seg_t[r] : nullptr;
+            const SegItem *ib = r < nb ? &g->seg_b[r] : nullptr;
+            SweepArgs x = a;
+            x.seg_on = 1;
+            x.seg_t0 = x.seg_t1 = x.seg_b0 = x.seg_b1 = 0;
+            if (it && it->kind == 0) {
+                x.seg_t0 = it->a;
+                x.seg_t1 = it->b;
+            }
+            if (ib && ib->kind == 0) {
+                x.seg_b0 = ib->a;
+                x.seg_b1 = ib->b;
+            }
+            if (x.seg_t1 > x.seg_t0 || x.seg_b1 > x.seg_b0)
+                HIP_TRY(launch_sweep_pair_one(x, g->stream));
+            const int32_t xt = it && it->kind == 1 ? it->a : -1;
+            const int32_t xb = ib && ib->kind == 1 ? ib->a : -1;
+            if (xt >= 0 || xb >= 0) {
+                const auto &li = g->h_linfo;
+                const int32_t wt = xt >= 0 ? li[xt + 1].node_lo - li[xt].node_lo : 0;
+                const int32_t wb = xb >= 0 ? li[xb + 1].node_lo - li[xb].node_lo : 0;
+                const int64_t et = xt >= 0 ? li[xt + 1].in_e_lo - li[xt].in_e_lo : 0;
+                const int64_t eb = xb >= 0 ? li[xb + 1].out_e_lo - li[xb].out_e_lo : 0;
+                HIP_TRY(launch_wide_level(a, xt, xb, et + eb, wt + wb, g->ps_acc,
+                                          g->ps_acc + std::max(g->max_width, 1), g->stream));
+            }
+        }
+        HIP_TRY(launch_level0_makespan(a, g->stream));
+        return PARDNN_OK;
+        };
+        if (timed) {
+            TimedLaunch t(g, "segmented k_sweep_pair<1> + k_wide_*");
+            st = run();
+        } else {
+            st = run();
+        }
+        if (st != PARDNN_OK) return st;
     }
     HIP_TRY(launch_finish(a, 1, nullptr, nullptr, nullptr, 0, nullptr, g->stream));
     return PARDNN_OK;

@@ -51,6 +51,12 @@ struct SpanCache {
     bool valid = false;
 };
 
+// One item of a segmented single-placement sweep, per direction: a run of
+// chain steps [a, b) or one wide level a computed grid-wide (kind 1).
+struct SegItem {
+    int32_t kind, a, b;
+};
+
 struct Graph {
     int device = 0;
     size_t lds_max = 65536;   // LDS bytes a workgroup may use on the device
@@ -103,6 +109,12 @@ struct Graph {
     // ftl, bll [V + pad][2] packed, labels [V][2]; allocated on first use
     int64_t *ps_ftl = nullptr, *ps_bll = nullptr;
     int32_t *ps_lab = nullptr, *ps_gate = nullptr;
+    // segmented single sweeps: levels wider than seg_thresh nodes are computed
+    // grid-wide; the plan per direction and the accumulators of one level
+    int32_t seg_thresh = -1;
+    std::vector<SegItem> seg_t, seg_b;
+    std::vector<LevelInfo> h_linfo;   // host copy of linfo, taken with the first plan
+    long long *ps_acc = nullptr;   // [2][max_width]
     SpanCache span_cache;
     // cluster criticality scratch: tl, bl, makespan
     int64_t *cl_tl = nullptr, *cl_bl = nullptr, *cl_m = nullptr;
@@ -163,7 +175,10 @@ hipError_t inclusive_scan_i64(const int64_t *in, int64_t *out, int32_t n, void *
 
 // ---- levelize.hip ----
 // levels, level_ptr and the release order (queue); result = {levels, released}
-hipError_t launch_kahn(const Graph &g, int32_t *indeg_work, int32_t *queue, int32_t *result);
+// rec_scratch: kahn_rec_bytes(V) bytes for the nodes' adjacency records
+size_t kahn_rec_bytes(int32_t V);
+hipError_t launch_kahn(const Graph &g, int32_t *indeg_work, int32_t *queue, int32_t *result,
+                       void *rec_scratch);
 // order = ids sorted by (level, id), levels below 2^bits
 size_t level_order_scratch_bytes(int32_t V);
 hipError_t launch_level_order(const Graph &g, int32_t bits, void *scratch);
@@ -204,6 +219,13 @@ hipError_t launch_sweep_pair(const SweepArgs &a, hipStream_t s);
 // The same with one placement per chain (workspace [P][V + pad], labels
 // [P][V]), no label sums.
 hipError_t launch_sweep_pair_one(const SweepArgs &a, hipStream_t s);
+// One placement, segmented: the t level xt and the b level xb (-1: none)
+// computed by grid-wide passes from the workspace (n_edges / n_nodes: their
+// edges and nodes together; acc_t / acc_b: int64 per node of the level, all
+// zero on entry, left zero); and the makespan over level 0 afterwards.
+hipError_t launch_wide_level(const SweepArgs &a, int32_t xt, int32_t xb, int64_t n_edges,
+                             int32_t n_nodes, long long *acc_t, long long *acc_b, hipStream_t s);
+hipError_t launch_level0_makespan(const SweepArgs &a, hipStream_t s);
 
 // ---- critpath.hip ----
 // tight successors and critical flags of one placement (comp_lm: the node

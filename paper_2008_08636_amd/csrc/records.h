@@ -121,6 +121,13 @@ struct SweepArgs {
     // enqueued together, chosen on the device without a host round trip)
     const int32_t *gate;
     int32_t gate_want;
+    // Segmented chains (one placement per chain, seg_on = 1): the t chain
+    // walks steps [seg_t0, seg_t1), the b chain [seg_b0, seg_b1); a segment
+    // that does not start at step 0 takes the general path for its first
+    // levels (its LDS state starts empty), and the makespan is left to a
+    // separate pass. seg_on = 0: both chains walk every step.
+    int32_t seg_on;
+    int32_t seg_t0, seg_t1, seg_b0, seg_b1;
 };
 
 }  // namespace pardnn

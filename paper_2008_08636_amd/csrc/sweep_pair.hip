@@ -37,6 +37,7 @@
 #include "internal.h"
 #include "sweep_common.h"
 
+#include <algorithm>
 #include <utility>
 
 namespace pardnn {
@@ -150,6 +151,7 @@ struct PairCtx {
     using LS = LabS<S>;
     int lane, tid;
     int32_t V, L, P, K, p0;
+    int32_t s0, s1, gen_end;   // steps of this chain; general path before gen_end
     int lb, ob;
     long long omax;
     VS *vals;
@@ -169,6 +171,9 @@ struct PairCtx {
         tid = threadIdx.x;   // 0 .. 127 over both waves
         V = a->V;
         L = a->L;
+        s0 = a->seg_on ? (FWD ? a->seg_t0 : a->seg_b0) : 0;
+        s1 = a->seg_on ? (FWD ? a->seg_t1 : a->seg_b1) : L;
+        gen_end = s0 > 0 ? s0 + kD + 1 : 0;
         P = a->P;
         K = a->K;
         p0 = slice * S;
@@ -198,7 +203,7 @@ struct PairCtx {
     }
     __device__ __forceinline__ WinEnt W(int32_t step) const { return win[step & (kWin - 1)]; }
     __device__ __forceinline__ long long *accb(int32_t step) const {
-        return acc + (step % kNB) * kPNodes * S;
+        return acc + ((uint32_t)step % kNB) * kPNodes * S;
     }
 
     // finalise node v (slot = its index in the level) from the level's
@@ -219,7 +224,7 @@ struct PairCtx {
 #pragma unroll
         for (int s = 0; s < S; s++) ab[slot * S + s] = 0;
         if (act) {
-            if (to_ring) ring[(step % kRS) * kPNodes + slot] = out;
+            if (to_ring) ring[((uint32_t)step % kRS) * kPNodes + slot] = out;
             if constexpr (want_bins) {
 #pragma unroll
                 for (int s = 0; s < S; s++) {
@@ -239,6 +244,16 @@ struct PairCtx {
         if (want_nx) at(nxs, sv) = nxv;
     }
 };
+
+// First step of the pipelined loop: a multiple of kNS, so that a step's
+// register set and LDS slots follow from its position in the unrolled group;
+// a segment that starts past step 0 walks its first levels (at least D + 1,
+// whose LDS state the walk has not built) on the general path up to it.
+template <class Ctx>
+__device__ __forceinline__ int32_t pipe_start(const Ctx &c) {
+    if (c.s0 == 0) return 0;
+    return min(c.s1, (c.gen_end + kNS - 1) & ~(kNS - 1));
+}
 
 // The general level step, for both waves: the level in chunks of 64 nodes
 // from the workspace, the early folds of a level too wide for the ring, and
@@ -334,7 +349,8 @@ __device__ __forceinline__ void pair_chain(const SweepArgs &a, int32_t slice, ch
             e.frlo = l0.far_lo;
             const int32_t w = l1.node_lo - l0.node_lo, nn = l1.near_lo - l0.near_lo,
                           nf = l1.far_lo - l0.far_lo;
-            const bool fast = w <= kPNodes && nn <= kNEn * kLanes && nf <= kNEf * kLanes;
+            const bool fast = w <= kPNodes && nn <= kNEn * kLanes && nf <= kNEf * kLanes &&
+                              sx >= c.gen_end;
             e.cnt = (uint32_t)min(w, 255) | (uint32_t)min(nn, 255) << 8 |
                     (uint32_t)min(nf, 255) << 16 | (fast ? 1u << 31 : 0u);
             c.win[sx & (kWin - 1)] = e;
@@ -382,7 +398,7 @@ __device__ __forceinline__ void pair_chain(const SweepArgs &a, int32_t slice, ch
                 const int32_t nt = cnt_near(b1.cnt);
                 long long *ab = c.accb(step + 1);
                 const LS *sl = c.slab + ((step + 1) & 1) * kPNodes;
-                const VS *rs = c.ring + (step % kRS) * kPNodes;
+                const VS *rs = c.ring + ((uint32_t)step % kRS) * kPNodes;
 #pragma unroll
                 for (int j = 0; j < kNEn; j++) {
                     if (lane + j * kLanes < nt) {
@@ -397,42 +413,55 @@ __device__ __forceinline__ void pair_chain(const SweepArgs &a, int32_t slice, ch
                 }
             }
         };
-        if (L > 0) {
-            fill(0, kWin / kLanes);
-            __builtin_amdgcn_s_waitcnt(0);
-#pragma unroll
-            for (int j = 0; j < kLN; j++) loads(st[j], c.W(j));
+        const int32_t s0 = c.s0, s1 = c.s1;
+        const int32_t a0 = pipe_start(c);
+        if (s1 > s0) {
+            fill(s0, kWin / kLanes);
             for (int i = lane; i < kNB * kPNodes * S; i += kLanes) c.acc[i] = 0;
             if (c.lds_bins)
                 for (int i = lane; i < c.K * S; i += kLanes) c.bins[i] = 0;
             __builtin_amdgcn_s_waitcnt(0);
-            if (lane < cnt_w(c.W(1).cnt)) c.slab[kPNodes + lane] = st[1].lab;
         }
         __syncthreads();
-        int32_t step = 0;
+        // a segment's first levels, on the general path
+        for (int32_t sx = s0; sx < a0; sx++) {
+            pair_slow<S, FWD, true, BM>(c.p0 / S, sx, reinterpret_cast<char *>(c.win));
+            __syncthreads();
+        }
+        if (a0 < s1) {
+#pragma unroll
+            for (int j = 0; j < kLN; j++) loads(st[j], c.W(a0 + j));
+            __builtin_amdgcn_s_waitcnt(0);
+            if (lane < cnt_w(c.W(a0 + 1).cnt)) c.slab[((a0 + 1) & 1) * kPNodes + lane] = st[1].lab;
+        }
+        __syncthreads();
+        int32_t step = a0;
         auto one = [&](auto RC) {
             constexpr int r = decltype(RC)::value;
             if constexpr (r < kNS) {
+                // step == r modulo kNS here; written so that the compiler sees
+                // it, and the LDS slots of the step become constants
+                const int32_t sa = (int32_t)(((uint32_t)step & ~(uint32_t)(kNS - 1)) | (uint32_t)r);
                 // the entries of levels step .. step + 2 came with their sets;
                 // only the one of the level loaded now is read from LDS
                 const WinEnt b0 = {st[r].wnlo, 0, 0, st[r].wcnt};
                 const WinEnt b1 = {0, 0, 0, st[(r + 1) % kNS].wcnt};
                 const WinEnt b2 = {0, 0, 0, st[(r + 2) % kNS].wcnt};
-                const WinEnt bl = c.W(step + kLN);
+                const WinEnt bl = c.W(sa + kLN);
                 if (cnt_fast(b0.cnt))
-                    body(step, b0, b1, st[r], st[(r + 1) % kNS]);
+                    body(sa, b0, b1, st[r], st[(r + 1) % kNS]);
                 else
-                    pair_slow<S, FWD, true, BM>(c.p0 / S, step, reinterpret_cast<char *>(c.win));
-                tail(step, st[(r + 2) % kNS], st[(r + kLN) % kNS], b2, bl);
+                    pair_slow<S, FWD, true, BM>(c.p0 / S, sa, reinterpret_cast<char *>(c.win));
+                tail(sa, st[(r + 2) % kNS], st[(r + kLN) % kNS], b2, bl);
                 step++;
             }
         };
         // whole groups of kNS levels only: an exit inside the unrolled group
         // would merge every body's loads in flight into the loop header
-        while (step + kNS <= L) unroll_seq(one, std::make_integer_sequence<int, kNS>{});
+        while (step + kNS <= s1) unroll_seq(one, std::make_integer_sequence<int, kNS>{});
         // the last levels (fewer than kNS) on the general path; folding an
         // edge a second time into a maximum changes nothing
-        for (; step < L; step++) {
+        for (; step < s1; step++) {
             pair_slow<S, FWD, true, BM>(c.p0 / S, step, reinterpret_cast<char *>(c.win));
             __syncthreads();
         }
@@ -479,31 +508,40 @@ __device__ __forceinline__ void pair_chain(const SweepArgs &a, int32_t slice, ch
             }
         };
         __syncthreads();   // the window is filled by wave 0
-        if (L > 0) {
-            st[0].wcnt = c.W(0).cnt;
+        const int32_t s0 = c.s0, s1 = c.s1;
+        const int32_t a0 = pipe_start(c);
+        for (int32_t sx = s0; sx < a0; sx++) {
+            pair_slow<S, FWD, false, BM>(c.p0 / S, sx, reinterpret_cast<char *>(c.win));
+            __syncthreads();
+        }
+        if (a0 < s1) {
+            st[0].wcnt = c.W(a0).cnt;
 #pragma unroll
-            for (int j = 1; j <= kD + kRF; j++) records(st[j], c.W(j));
+            for (int j = 1; j <= kD + kRF; j++) records(st[j], c.W(a0 + j));
+            __builtin_amdgcn_s_waitcnt(0);
+            // the values of the first levels' distant neighbours (none when
+            // the chain starts at level 0)
 #pragma unroll
-            for (int j = 1; j <= kD; j++)
-#pragma unroll
-                for (int t = 0; t < kNEf; t++) st[j].f[t] = VS{};
+            for (int j = 1; j <= kD; j++) far_loads(st[j], c.W(a0 + j));
             // nothing may be pending at the loop entry: a load in flight into a
             // register the loop reuses would make the loop header wait for it
             __builtin_amdgcn_s_waitcnt(0);
         }
-        int32_t step = 0;
+        __syncthreads();
+        int32_t step = a0;
         auto one = [&](auto RC) {
             constexpr int r = decltype(RC)::value;
             if constexpr (r < kNS) {
+                const int32_t sa = (int32_t)(((uint32_t)step & ~(uint32_t)(kNS - 1)) | (uint32_t)r);
                 const WinEnt b0 = {0, 0, 0, st[r].wcnt};
                 const WinEnt b1 = {0, 0, 0, st[(r + 1) % kNS].wcnt};
                 const WinEnt bd = {0, 0, 0, st[(r + 1 + kD) % kNS].wcnt};
-                const WinEnt brf = c.W(step + 1 + kD + kRF);
+                const WinEnt brf = c.W(sa + 1 + kD + kRF);
                 FarSet<S> &B1 = st[(r + 1) % kNS];
                 if (cnt_fast(b0.cnt)) {
-                    if (cnt_fast(b1.cnt)) fold_far(step, B1, b1);
+                    if (cnt_fast(b1.cnt)) fold_far(sa, B1, b1);
                 } else {
-                    pair_slow<S, FWD, false, BM>(c.p0 / S, step, reinterpret_cast<char *>(c.win));
+                    pair_slow<S, FWD, false, BM>(c.p0 / S, sa, reinterpret_cast<char *>(c.win));
                 }
                 // far values in flight stay valid across a general-path level:
                 // a far edge either spans more than D + 1 levels or was folded
@@ -514,8 +552,8 @@ __device__ __forceinline__ void pair_chain(const SweepArgs &a, int32_t slice, ch
                 step++;
             }
         };
-        while (step + kNS <= L) unroll_seq(one, std::make_integer_sequence<int, kNS>{});
-        for (; step < L; step++) {
+        while (step + kNS <= s1) unroll_seq(one, std::make_integer_sequence<int, kNS>{});
+        for (; step < s1; step++) {
             pair_slow<S, FWD, false, BM>(c.p0 / S, step, reinterpret_cast<char *>(c.win));
             __syncthreads();
         }
@@ -531,7 +569,7 @@ __device__ __forceinline__ void pair_chain(const SweepArgs &a, int32_t slice, ch
             }
         return;
     }
-    if (!NEAR) return;
+    if (!NEAR || a.seg_on) return;   // segmented: a separate pass takes the makespan
     // b: makespan M = max over v of tl + bl is reached at a node without
     // predecessors (tl = 0 there), i.e. at level 0; the path starts at the
     // smallest-id such node with bl == M (level 0 is sorted by id).
@@ -575,6 +613,84 @@ __global__ __launch_bounds__(2 * kLanes) void k_sweep_pair(SweepArgs a) {
         else
             pair_chain<S, false, false, kBinsNone>(a, slice, smem);
     }
+}
+
+// ---- wide levels of a single placement: grid-wide passes ----
+// A level wider than the segmented chain's threshold is computed by the whole
+// GPU between two chain launches: every in-edge (t) or out-edge (b) of the
+// level is one task that folds its candidate into the owner's accumulator
+// with a 64-bit atomic maximum (edge-parallel, so a hub costs no serial loop),
+// then one task per node finalises it. All neighbours are final in the
+// workspace. xt / xb: the t and b level (-1: none); acc_t / acc_b: one int64
+// per node of the level, 0 on entry and reset to 0 on exit (the empty maximum).
+__global__ void k_wide_edges(SweepArgs a, int32_t xt, int32_t xb, long long *acc_t,
+                             long long *acc_b) {
+    if (a.gate != nullptr && *a.gate != a.gate_want) return;
+    using EL = Elem<true>;
+    const int lb = a.lb, ob = a.ob;
+    const int64_t t0 = xt >= 0 ? a.linfo[xt].in_e_lo : 0;
+    const int64_t nt = xt >= 0 ? a.linfo[xt + 1].in_e_lo - t0 : 0;
+    const int64_t b0 = xb >= 0 ? a.linfo[xb].out_e_lo : 0;
+    const int64_t nb = xb >= 0 ? a.linfo[xb + 1].out_e_lo - b0 : 0;
+    const int32_t tlo = xt >= 0 ? a.linfo[xt].node_lo : 0;
+    const int32_t blo = xb >= 0 ? a.linfo[xb].node_lo : 0;
+    for (int64_t i = blockIdx.x * (int64_t)blockDim.x + threadIdx.x; i < nt + nb;
+         i += (int64_t)gridDim.x * blockDim.x) {
+        const bool fwd = i < nt;
+        const EdgeRec16 r = fwd ? a.in_rec[t0 + i] : a.out_rec[b0 + (i - nt)];
+        const int64_t g = fwd ? a.ftl[r.nb] : a.bll[r.nb];
+        const int32_t own_lab = a.lab_w[r.own];
+        const int64_t cand = EL::val(g, lb) + (EL::lab(g, lb) != own_lab ? r.cost : 0);
+        (void)ob;
+        if (fwd)
+            atomicMax(&acc_t[r.own - tlo], (long long)cand);
+        else
+            atomicMax(&acc_b[r.own - blo], (long long)cand);
+    }
+}
+
+__global__ void k_wide_nodes(SweepArgs a, int32_t xt, int32_t xb, long long *acc_t,
+                             long long *acc_b) {
+    if (a.gate != nullptr && *a.gate != a.gate_want) return;
+    using EL = Elem<true>;
+    const int lb = a.lb;
+    const int32_t tlo = xt >= 0 ? a.linfo[xt].node_lo : 0;
+    const int32_t nt = xt >= 0 ? a.linfo[xt + 1].node_lo - tlo : 0;
+    const int32_t blo = xb >= 0 ? a.linfo[xb].node_lo : 0;
+    const int32_t nb = xb >= 0 ? a.linfo[xb + 1].node_lo - blo : 0;
+    for (int32_t i = blockIdx.x * blockDim.x + threadIdx.x; i < nt + nb;
+         i += gridDim.x * blockDim.x) {
+        const bool fwd = i < nt;
+        const int32_t k = fwd ? i : i - nt;
+        const int32_t v = (fwd ? tlo : blo) + k;
+        long long *acc = fwd ? acc_t : acc_b;
+        const int64_t m = acc[k];
+        acc[k] = 0;
+        const int64_t comp = a.node_rec[v].comp;
+        const int64_t x = EL::make(m + comp, a.lab_w[v], lb);
+        if (fwd)
+            a.ftl[v] = x;
+        else
+            a.bll[v] = x;
+    }
+}
+
+// makespan of a segmented single sweep: the largest bl over level 0
+__global__ __launch_bounds__(256) void k_level0_makespan(SweepArgs a) {
+    if (a.gate != nullptr && *a.gate != a.gate_want) return;
+    using EL = Elem<true>;
+    __shared__ long long s_m;
+    if (threadIdx.x == 0) s_m = 0;
+    __syncthreads();
+    const int32_t n0 = a.L > 0 ? a.linfo[1].node_lo : 0;
+    long long m = 0;
+    for (int32_t v = threadIdx.x; v < n0; v += blockDim.x) {
+        const long long x = EL::val(a.bll[v], a.lb);
+        m = x > m ? x : m;
+    }
+    lds_max_i64(&s_m, m);
+    __syncthreads();
+    if (threadIdx.x == 0) *a.makespan = s_m;
 }
 
 // ---- structure: split each level's edges into span-1 and longer edges ----
@@ -747,6 +863,24 @@ hipError_t launch_pair(const SweepArgs &a, hipStream_t s) {
 
 hipError_t launch_sweep_pair(const SweepArgs &a, hipStream_t s) {
     return launch_pair<kBatchSlots>(a, s);
+}
+
+hipError_t launch_wide_level(const SweepArgs &a, int32_t xt, int32_t xb, int64_t n_edges,
+                             int32_t n_nodes, long long *acc_t, long long *acc_b, hipStream_t s) {
+    if (a.lb <= 0 || a.P != 1) return hipErrorInvalidValue;
+    const unsigned ge = (unsigned)std::max<int64_t>(1, std::min<int64_t>((n_edges + 255) / 256, 8192));
+    k_wide_edges<<<ge, 256, 0, s>>>(a, xt, xb, acc_t, acc_b);
+    hipError_t e = hipGetLastError();
+    if (e != hipSuccess) return e;
+    const unsigned gn = (unsigned)std::max<int64_t>(1, std::min<int64_t>((n_nodes + 255) / 256, 8192));
+    k_wide_nodes<<<gn, 256, 0, s>>>(a, xt, xb, acc_t, acc_b);
+    return hipGetLastError();
+}
+
+hipError_t launch_level0_makespan(const SweepArgs &a, hipStream_t s) {
+    if (a.lb <= 0 || a.P != 1) return hipErrorInvalidValue;
+    k_level0_makespan<<<1, 256, 0, s>>>(a);
+    return hipGetLastError();
 }
 
 // One placement per chain: for a single placement (no label sums) the chain

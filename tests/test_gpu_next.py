@@ -612,3 +612,15 @@ def test_slice_graph_maps_in_device_memory(P):
         check_slice_all(P, g, 4)
     finally:
         del os.environ["PARDNN_PEEL_GLOBAL_MAPS"]
+
+
+def test_slicing_and_criticality_with_grid_levels(P, monkeypatch):
+    """Slicing rounds and cluster criticality run single-placement sweeps;
+    with every level above 65 nodes computed grid-wide they are unchanged."""
+    monkeypatch.setenv("PARDNN_WIDE_LEVEL", "65")
+    g = W.make_config(1)
+    say(f"slicing and criticality, grid-wide levels, config1 V={g.n_nodes}")
+    check_slice_all(P, g, 6)
+    rng = np.random.default_rng(95)
+    cl, C = W.path_clusters(rng, g, max_extra=20)
+    check_clusters(P, g, cl.astype(np.int32), C)

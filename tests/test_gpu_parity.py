@@ -731,3 +731,51 @@ def test_evaluate_moves_without_label_sums(P):
             n = got["path_len"][p]
             assert (got["path"][p, :n] == epath).all(), p
     G.close()
+
+
+# ------------------------------------------- segmented single-placement sweeps --
+
+@pytest.fixture
+def wide_level(monkeypatch):
+    """Sets the width above which a single-placement sweep computes a level
+    grid-wide between chain segments (read by the library at every call)."""
+    def set_(n):
+        monkeypatch.setenv("PARDNN_WIDE_LEVEL", str(n))
+    return set_
+
+
+@pytest.mark.parametrize("thr", [1, 65, 300, 0])
+@pytest.mark.parametrize("i", [0, 1, 2])
+def test_single_wide_level_thresholds(P, wide_level, thr, i):
+    """Every level wider than thr nodes computed grid-wide between chain
+    segments (thr = 1: nearly every level; 0: none): results unchanged."""
+    wide_level(thr)
+    g = cfg(i)
+    say(f"config{i} single, wide levels above {thr} nodes grid-wide")
+    assert_same(gpu_single(P, g), oracle_single(g))
+
+
+def test_single_wide_levels_wide_resnet(P, wide_level):
+    """The Wide-ResNet-shaped graph (90 levels of about 10k nodes between long
+    one-wide chains) with the default threshold and with 65."""
+    g = cfg(3)
+    exp = oracle_single(g)
+    for thr in (512, 65):
+        wide_level(thr)
+        say(f"config3 single, wide levels above {thr} nodes grid-wide")
+        assert_same(gpu_single(P, g), exp)
+
+
+def test_single_wide_levels_random_shapes(P, wide_level):
+    """Level shapes that drive every path of the chain (level_shapes) and
+    random DAGs, with the grid-wide pass for every level above 2 nodes."""
+    wide_level(2)
+    say("segmented sweeps on level shapes and random DAGs")
+    for seed in (11, 12, 13):
+        g = level_shapes(seed)
+        assert_same(gpu_single(P, g), oracle_single(g))
+    rng = np.random.default_rng(2121)
+    for t in range(30):
+        g = W.random_dag(rng, int(rng.integers(1, 80)), p_edge=float(rng.uniform(0.02, 0.3)),
+                         max_weight=int(rng.integers(0, 6)), n_labels=int(rng.integers(1, 4)))
+        assert_same(gpu_single(P, g), oracle_single(g))
