@@ -10,6 +10,8 @@
 #include <new>
 #include <string>
 
+#include <rocprofiler-sdk-roctx/roctx.h>
+
 #include "internal.h"
 
 using namespace pardnn;
@@ -30,6 +32,40 @@ thread_local std::string g_last_error;
 int hip_status(hipError_t e) {
     return e == hipErrorOutOfMemory || e == hipErrorMemoryAllocation ? PARDNN_E_NOMEM
                                                                      : PARDNN_E_DEVICE;
+}
+
+// Allocation-failure injection, for tests of the out-of-memory paths: with
+// PARDNN_FAULT_ALLOC=n (n >= 1) in the environment, the n-th allocation the
+// library attempts -- host or device, counted from the first attempt that
+// sees this value of the variable -- fails as if memory were exhausted; later
+// attempts succeed again. Unset, empty or n <= 0: no failures.
+bool injected_alloc_failure() {
+    static std::mutex m;
+    static std::string seen;
+    static long long count = 0;
+    const char *e = std::getenv("PARDNN_FAULT_ALLOC");
+    std::lock_guard<std::mutex> lock(m);
+    if (e == nullptr || e[0] == 0) {
+        seen.clear();
+        count = 0;
+        return false;
+    }
+    if (seen != e) {
+        seen = e;
+        count = 0;
+    }
+    const long long n = std::strtoll(e, nullptr, 10);
+    return n > 0 && ++count == n;
+}
+
+// Every device allocation of the library goes through here (and the hook).
+// On failure *p is null.
+hipError_t dev_malloc(void **p, size_t bytes) {
+    *p = nullptr;
+    if (injected_alloc_failure()) return hipErrorOutOfMemory;
+    const hipError_t e = hipMalloc(p, bytes);
+    if (e != hipSuccess) *p = nullptr;
+    return e;
 }
 
 #define HIP_TRY(expr)                                                                      \
@@ -57,12 +93,20 @@ struct DeviceScope {
     }
 };
 
+// A per-graph array, freed with the handle. Each such array has one size for
+// the life of the handle, so one that an earlier, failed call already
+// allocated is kept: a call that fails half-way (out of memory) leaves the
+// handle fit for the next call, which allocates only what is missing.
 template <class T>
 hipError_t dalloc(Graph &g, T **p, size_t n) {
+    if (*p != nullptr) return hipSuccess;
     if (n == 0) n = 1;
-    hipError_t e = hipMalloc((void **)p, n * sizeof(T));
-    if (e == hipSuccess) g.allocs.push_back((void *)*p);
-    return e;
+    void *q = nullptr;
+    hipError_t e = dev_malloc(&q, n * sizeof(T));
+    if (e != hipSuccess) return e;
+    g.allocs.push_back(q);
+    *p = static_cast<T *>(q);
+    return hipSuccess;
 }
 
 void release(Graph *g) {
@@ -85,10 +129,13 @@ int read_errors(Graph *g) {
     return PARDNN_OK;
 }
 
-// Event pair around the main kernel of a call (instrumentation only).
+// Around the main kernels of a call (instrumentation only): a roctx range
+// named for them, which a profiler's marker trace shows with the dispatches
+// enqueued inside it, and, with timing on, an event pair on the stream.
 struct TimedLaunch {
     Graph *g;
     TimedLaunch(Graph *g_, const char *name) : g(g_) {
+        roctxRangePushA(name);
         if (g->timing) {
             g->timed_kernel = name;
             (void)hipEventRecord(g->ev0, g->stream);
@@ -99,6 +146,7 @@ struct TimedLaunch {
             (void)hipEventRecord(g->ev1, g->stream);
             g->timed = true;
         }
+        roctxRangePop();
     }
 };
 
@@ -107,12 +155,10 @@ int ensure_pair(Graph *g);
 int ensure_levelized(Graph *g) {
     if (g->levelized) return PARDNN_OK;
     const int32_t V = g->V;
-    if (!g->level) {
-        HIP_TRY(dalloc(*g, &g->level, V));
-        HIP_TRY(dalloc(*g, &g->order, V));
-        HIP_TRY(dalloc(*g, &g->rank, (size_t)V + 1));   // rank[V] = -1: "no node"
-        HIP_TRY(dalloc(*g, &g->level_ptr, (size_t)V + 2));
-    }
+    HIP_TRY(dalloc(*g, &g->level, V));
+    HIP_TRY(dalloc(*g, &g->order, V));
+    HIP_TRY(dalloc(*g, &g->rank, (size_t)V + 1));   // rank[V] = -1: "no node"
+    HIP_TRY(dalloc(*g, &g->level_ptr, (size_t)V + 2));
     // scratch: in-degree counters, the release queue, the result words, then
     // the level sort's own space
     const size_t sort_bytes = std::max(level_order_scratch_bytes(V), kahn_rec_bytes(V));
@@ -122,7 +168,7 @@ int ensure_levelized(Graph *g) {
         (void)hipStreamSynchronize(g->stream);
         if (work) (void)hipFree(work);
     };
-    hipError_t e = hipMalloc((void **)&work, head + sort_bytes);
+    hipError_t e = dev_malloc((void **)&work, head + sort_bytes);
     int32_t *indeg_work = reinterpret_cast<int32_t *>(work);
     int32_t *queue = indeg_work + (V + 1);
     int32_t *result = queue + (V + 1);
@@ -190,7 +236,7 @@ int ensure_levelized(Graph *g) {
 
     int32_t *tmp = nullptr;
     const size_t scan_n = scan_workspace_elems(V);
-    e = hipMalloc((void **)&tmp, sizeof(int32_t) * (4 * (size_t)V + scan_n + 4));
+    e = dev_malloc((void **)&tmp, sizeof(int32_t) * (4 * (size_t)V + scan_n + 4));
     if (e == hipSuccess)
         e = launch_build_lm(*g, tmp, tmp + 2 * (size_t)V, tmp + 3 * (size_t)V,
                             tmp + 4 * (size_t)V);
@@ -222,10 +268,10 @@ int ensure_pair(Graph *g) {
         if (rank) (void)hipFree(rank);
         if (ws) (void)hipFree(ws);
     };
-    hipError_t e = hipMalloc((void **)&flag, sizeof(int32_t) * (E + 1));
-    if (e == hipSuccess) e = hipMalloc((void **)&rank, sizeof(int32_t) * (E + 1));
+    hipError_t e = dev_malloc((void **)&flag, sizeof(int32_t) * (E + 1));
+    if (e == hipSuccess) e = dev_malloc((void **)&rank, sizeof(int32_t) * (E + 1));
     if (e == hipSuccess)
-        e = hipMalloc((void **)&ws, sizeof(int32_t) * scan_workspace_elems((int32_t)E));
+        e = dev_malloc((void **)&ws, sizeof(int32_t) * scan_workspace_elems((int32_t)E));
     PairLevel *pl[2] = {nullptr, nullptr};
     NearRec16 *nr[2] = {nullptr, nullptr};
     FarRec16 *fr[2] = {nullptr, nullptr};
@@ -243,9 +289,8 @@ int ensure_pair(Graph *g) {
         if (e == hipSuccess) e = dalloc(*g, &pl[d], (size_t)g->L + 2);
         if (e == hipSuccess) e = dalloc(*g, &nr[d], (size_t)n_near);
         if (e == hipSuccess) e = dalloc(*g, &fr[d], E - (size_t)n_near);
-        if (e == hipSuccess && !fwd) e = dalloc(*g, &g->ftie_b, E - (size_t)n_near);
         if (e == hipSuccess)
-            e = launch_pair_split(*g, fwd, rank, pl[d], nr[d], fr[d], fwd ? nullptr : g->ftie_b);
+            e = launch_pair_split(*g, fwd, rank, pl[d], nr[d], fr[d]);
         // edges that wide levels fold early
         if (e == hipSuccess) e = hipStreamSynchronize(g->stream);
         if (e == hipSuccess) e = launch_fill_i32(rank, (int64_t)E + 1, 0, g->stream);
@@ -401,7 +446,7 @@ int evaluate_impl(Graph *g, int32_t n_place, const int32_t *placements, const Mo
                 g->batch_ws = nullptr;
                 g->batch_ws_bytes = 0;
             }
-            HIP_TRY(hipMalloc(&g->batch_ws, need));
+            HIP_TRY(dev_malloc(&g->batch_ws, need));
             g->batch_ws_bytes = need;
         }
         ws_base = g->batch_ws;
@@ -477,17 +522,24 @@ int evaluate_impl(Graph *g, int32_t n_place, const int32_t *placements, const Mo
         a.nr_b = g->nr_b;
         a.fr_t = g->fr_t;
         a.fr_b = g->fr_b;
-        a.ftie_b = g->ftie_b;
         a.preoff_t = g->preoff_t;
         a.preoff_b = g->preoff_b;
         a.pre_t = g->pre_t;
         a.pre_b = g->pre_b;
         a.pretie_b = g->pretie_b;
     }
+    // The successor links ride in the packed b values when those have room
+    // for them (not in a gated call: its unpacked alternative writes nx_w,
+    // and the path walk reads one or the other)
+    a.nxf = path != nullptr && lb > 0 && !gated && lb + ob < 62 &&
+                    g->weight_bound < (1ll << (62 - lb - ob))
+                ? 1
+                : 0;
     // the unpacked alternative of a gated call: {value, label} pairs
     SweepArgs alt = a;
     alt.lb = 0;
     alt.ob = 0;
+    alt.nxf = 0;
     alt.gate = fit;
     alt.gate_want = 0;
     if (gated) {
@@ -546,12 +598,10 @@ constexpr int64_t ps_lab_stride(int32_t V) { return ((int64_t)V + 63) / 64 * 64;
 // labels (original ids) into the pair sweep's level-major layout
 int pair_single_labels(Graph *g, const int32_t *labels) {
     const int32_t V = g->V;
-    if (!g->ps_ftl) {
-        HIP_TRY(dalloc(*g, &g->ps_ftl, (size_t)ps_ws_stride(V)));
-        HIP_TRY(dalloc(*g, &g->ps_bll, (size_t)ps_ws_stride(V)));
-        HIP_TRY(dalloc(*g, &g->ps_lab, (size_t)ps_lab_stride(V)));
-        HIP_TRY(dalloc(*g, &g->ps_gate, 1));
-    }
+    HIP_TRY(dalloc(*g, &g->ps_ftl, (size_t)ps_ws_stride(V)));
+    HIP_TRY(dalloc(*g, &g->ps_bll, (size_t)ps_ws_stride(V)));
+    HIP_TRY(dalloc(*g, &g->ps_lab, (size_t)ps_lab_stride(V)));
+    HIP_TRY(dalloc(*g, &g->ps_gate, 1));
     HIP_TRY(launch_permute_labels_batch(*g, labels, 1, 1, g->ps_lab, ps_lab_stride(V)));
     return PARDNN_OK;
 }
@@ -629,7 +679,6 @@ int pair_single_sweep(Graph *g, int32_t lb, int32_t ob, NodeRec16 *node_rec, int
     a.nr_b = g->nr_b;
     a.fr_t = g->fr_t;
     a.fr_b = g->fr_b;
-    a.ftie_b = g->ftie_b;
     a.preoff_t = g->preoff_t;
     a.preoff_b = g->preoff_b;
     a.pre_t = g->pre_t;
@@ -758,11 +807,14 @@ int pardnn_graph_create(int32_t n_nodes, int64_t n_edges, const int32_t *src, co
         return fail(PARDNN_E_INVAL, "src, dst and edge_cost must be non-null when n_edges > 0");
     if (n_nodes > 0 && (comp == nullptr || mem == nullptr))
         return fail(PARDNN_E_INVAL, "comp and mem must be non-null when n_nodes > 0");
+    // the handle first: a host allocation, which needs no device
+    Graph *g = injected_alloc_failure() ? nullptr : new (std::nothrow) Graph();
+    if (g == nullptr) return fail(PARDNN_E_NOMEM, "host allocation of the handle failed");
     int ndev = 0;
-    if (hipGetDeviceCount(&ndev) != hipSuccess || ndev <= 0)
+    if (hipGetDeviceCount(&ndev) != hipSuccess || ndev <= 0) {
+        delete g;
         return fail(PARDNN_E_DEVICE, "no HIP device available");
-    Graph *g = new (std::nothrow) Graph();
-    if (g == nullptr) return fail(PARDNN_E_NOMEM, "host allocation failed");
+    }
     if (hipGetDevice(&g->device) != hipSuccess) {
         delete g;
         return fail(PARDNN_E_DEVICE, "hipGetDevice failed");
@@ -787,6 +839,8 @@ int pardnn_graph_create(int32_t n_nodes, int64_t n_edges, const int32_t *src, co
         HIP_TRY(dalloc(*g, &g->o_off, V + 1));
         HIP_TRY(dalloc(*g, &g->o_nbr, E));
         HIP_TRY(dalloc(*g, &g->err, 4));
+        if (injected_alloc_failure())
+            return fail(PARDNN_E_NOMEM, "host allocation of the error words failed");
         HIP_TRY(hipHostMalloc((void **)&g->h_err, 4 * sizeof(int32_t), hipHostMallocDefault));
         ValidateAcc *acc = nullptr;
         HIP_TRY(dalloc(*g, &acc, 1));
@@ -817,7 +871,7 @@ int pardnn_graph_create(int32_t n_nodes, int64_t n_edges, const int32_t *src, co
         HIP_TRY(launch_fill_i32(g->outdeg, (int64_t)V, 0, g->stream));
         HIP_TRY(launch_count_degrees(*g));
         int32_t *ws = nullptr;
-        HIP_TRY(hipMalloc((void **)&ws, sizeof(int32_t) * (scan_workspace_elems(n_nodes) + V + 1)));
+        HIP_TRY(dev_malloc((void **)&ws, sizeof(int32_t) * (scan_workspace_elems(n_nodes) + V + 1)));
         hipError_t e = launch_exclusive_scan(g->outdeg, g->o_off, n_nodes, ws, g->stream);
         if (e == hipSuccess) e = launch_build_orig_csr(*g, ws + scan_workspace_elems(n_nodes));
         if (e == hipSuccess) e = hipStreamSynchronize(g->stream);
@@ -1000,7 +1054,7 @@ hipError_t grow_aux(Graph *g, size_t need) {
         g->aux_scratch = nullptr;
         g->aux_scratch_bytes = 0;
     }
-    if ((e = hipMalloc(&g->aux_scratch, need)) != hipSuccess) return e;
+    if ((e = dev_malloc(&g->aux_scratch, need)) != hipSuccess) return e;
     g->aux_scratch_bytes = need;
     return hipSuccess;
 }
@@ -1123,7 +1177,7 @@ namespace {
 int slice_rounds(Graph *g, int32_t K, int32_t *primary, int32_t *paths, int32_t path_stride,
                  int32_t *path_len, int64_t *makespan, bool then_levels) {
     const int32_t V = g->V;
-    if (!g->sl_node_rec) {
+    if (!g->sl_m) {   // the last of the group (an earlier failed call may have made some)
         HIP_TRY(dalloc(*g, &g->sl_node_rec, V));
         HIP_TRY(dalloc(*g, &g->sl_comp, V));
         HIP_TRY(dalloc(*g, &g->sl_tl, V));

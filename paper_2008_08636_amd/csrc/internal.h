@@ -18,7 +18,7 @@
 //     in_rec, out_rec EdgeRec16[E] and node_rec NodeRec16[V]: the same data
 //       as 16-byte records, so a sweep task loads its edge with one load
 //     pl_t / pl_b PairLevel[L+2], nr_t / nr_b NearRec16[], fr_t / fr_b
-//       FarRec16[], ftie_b int32[]: the edges of each level split into span-1
+//       FarRec16[]: the edges of each level split into span-1
 //       ("near") and longer ("far") edges for the batched sweeps, per
 //       direction; built on first use
 //   linfo has L + 2 entries: entry L + 1 repeats entry L, so the pair
@@ -86,7 +86,6 @@ struct Graph {
     PairLevel *pl_t = nullptr, *pl_b = nullptr;   // built on first batched evaluation
     NearRec16 *nr_t = nullptr, *nr_b = nullptr;
     FarRec16 *fr_t = nullptr, *fr_b = nullptr;
-    int32_t *ftie_b = nullptr;
     int32_t *preoff_t = nullptr, *preoff_b = nullptr;
     PreRec16 *pre_t = nullptr, *pre_b = nullptr;
     int32_t *pretie_b = nullptr;
@@ -206,9 +205,9 @@ hipError_t launch_finish(const SweepArgs &a, int32_t S, uint8_t *crit, uint32_t 
 // ---- sweep_pair.hip ----
 // flag[e] = 1 for the span-1 edges of the direction's level-major edge order
 hipError_t launch_pair_flags(const Graph &g, bool fwd, int32_t *flag);
-// near_rank = exclusive scan of flag (E + 1 entries); fills pl, nr, fr, ftie
+// near_rank = exclusive scan of flag (E + 1 entries); fills pl, nr, fr
 hipError_t launch_pair_split(const Graph &g, bool fwd, const int32_t *near_rank, PairLevel *pl,
-                             NearRec16 *nr, FarRec16 *fr, int32_t *ftie);
+                             NearRec16 *nr, FarRec16 *fr);
 // flag[e] = 1 for the edges a wide level folds early (neighbour-grouped order)
 hipError_t launch_pre_flags(const Graph &g, bool fwd, int32_t *flag);
 // rank = exclusive scan of those flags; fills preoff [L + 1], pre, pretie

@@ -30,23 +30,28 @@ struct alignas(16) EdgeRec16 {
 struct alignas(16) PairLevel {
     int32_t node_lo, near_lo, far_lo, pad;
 };
+// The cost word of the batched sweeps' edge records: in the t direction the
+// edge cost; in the b direction the cost with the successor tie-break below
+// it, (cost << ob) | (2^ob - 1 - successor's original id), so that a b key
+// is (value << ob) plus this word (labels differ) or its low ob bits (same
+// label). It fits whenever the packed keys are used: their condition bounds
+// every cost by 2^(62 - ob).
 // A span-1 edge: owner's and neighbour's index inside their levels
-// (own | nb << 16), the successor tie-break key 2^ob - 1 - successor's
-// original id (b direction; 0 for t) and the cost.
+// (own | nb << 16) and the cost word.
 struct alignas(16) NearRec16 {
     uint32_t ol;
-    int32_t tie;
-    int64_t cost;
+    int32_t pad;
+    int64_t ck;
 };
 // A longer edge: the neighbour (level-major id), the owner's index inside its
 // level and the neighbour's entry in the LDS ring of recent levels
 // (own | ring << 16; kNoRing: read the workspace; kPreFolded: folded by the
 // general path of the neighbour's level, which is too wide for the ring) and
-// the cost.
+// the cost word.
 struct alignas(16) FarRec16 {
     int32_t nb;
     uint32_t ol;
-    int64_t cost;
+    int64_t ck;
 };
 constexpr uint32_t kNoRing = 0xffffu;
 constexpr uint32_t kPreFolded = 0xfffeu;
@@ -109,7 +114,6 @@ struct SweepArgs {
     const PairLevel *pl_t, *pl_b;         // batched sweeps: near / far split per level
     const NearRec16 *nr_t, *nr_b;
     const FarRec16 *fr_t, *fr_b;
-    const int32_t *ftie_b;
     const int32_t *preoff_t, *preoff_b;   // [L + 1] per neighbour level
     const PreRec16 *pre_t, *pre_b;
     const int32_t *pretie_b;
@@ -128,6 +132,11 @@ struct SweepArgs {
     // separate pass. seg_on = 0: both chains walk every step.
     int32_t seg_on;
     int32_t seg_t0, seg_t1, seg_b0, seg_b1;
+    // Batched pair sweep with successor links (nx_w given): 1 = the links
+    // ride in the b values instead of nx_w, each b value being
+    // (((bl << ob) | (2^ob - 1 - successor id, 0: none)) << lb) | label, which
+    // needs values below 2^(62 - ob - lb); 0 = plain packed b values.
+    int32_t nxf;
 };
 
 }  // namespace pardnn

@@ -542,6 +542,7 @@ __device__ void emit_rows(const SweepArgs &a, uint8_t *crit, uint32_t *cbits, in
     const int32_t n_chunks = (P + TP - 1) / TP;
     const ET *ft = reinterpret_cast<const ET *>(a.ftl);
     const ET *bl = reinterpret_cast<const ET *>(a.bll);
+    const int bfo = PACKED && a.nxf ? a.ob : 0;   // successor links below the label bits
     if (tid < TV) {
         const int32_t v = min(v0 + tid, V - 1);
         s_ord[tid] = a.order[v];
@@ -575,7 +576,7 @@ __device__ void emit_rows(const SweepArgs &a, uint8_t *crit, uint32_t *cbits, in
             const int i = tid + j * NT;
             const int sl = i / (TV * S), r = (i % (TV * S)) / S, s2 = i % S;
             t_tl[r][sl * S + s2] = EL::val(fv[j], a.lb) - s_comp[r];
-            t_bl[r][sl * S + s2] = EL::val(bv[j], a.lb);
+            t_bl[r][sl * S + s2] = EL::val(bv[j], a.lb) >> bfo;
         }
         if (ch + 1 < n_chunks) load(ch + 1);
         const int32_t p = ch * TP + col;   // this thread's placement column
@@ -641,7 +642,10 @@ __device__ void chase_wave(const SweepArgs &a, const uint32_t *cbits, int32_t p,
     const int32_t V = a.V;
     const int32_t slice = p / S, s = p % S;
     const int32_t n_words = (V + 31) / 32;
-    const int32_t *nx = a.nx_w + (int64_t)slice * a.ws_stride;
+    // successor links: nx_w, or the low bits of the packed b values
+    const int32_t *nx = a.nxf ? nullptr : a.nx_w + (int64_t)slice * a.ws_stride;
+    const int64_t *bvals = a.nxf ? a.bll + (int64_t)slice * a.ws_stride : nullptr;
+    const long long omax = (1ll << a.ob) - 1;
     const uint32_t *bits = cbits + (int64_t)p * n_words;
     // scratch: pos[0, V) and link[V, 2V) in int32 units, in the placement's
     // share of the t workspace (4 ws_stride / S >= 4 (V + pad) int32 each)
@@ -685,7 +689,14 @@ __device__ void chase_wave(const SweepArgs &a, const uint32_t *cbits, int32_t p,
             qn[j] = i + 1 < n ? pos[i + 1] : -1;
         }
 #pragma unroll
-        for (int j = 0; j < U; j++) l[j] = nx[(int64_t)q[j] * S + s];
+        for (int j = 0; j < U; j++) {
+            if (bvals != nullptr) {
+                const int64_t t = (bvals[(int64_t)q[j] * S + s] >> a.lb) & omax;
+                l[j] = t == 0 ? -1 : (int32_t)(omax - t);
+            } else {
+                l[j] = nx[(int64_t)q[j] * S + s];
+            }
+        }
 #pragma unroll
         for (int j = 0; j < U; j++) {
             l[j] = a.rank[l[j] < 0 ? V : l[j]];
@@ -839,6 +850,7 @@ hipError_t launch_label_fit(const Graph &g, const int32_t *labels, int32_t limit
 hipError_t launch_sweep(const SweepArgs &a, int32_t S, hipStream_t s) {
     const int32_t n_slices = (a.P + S - 1) / S;
     if (n_slices == 0) return hipSuccess;
+    if (a.nxf) return hipErrorInvalidValue;   // this sweep stores links in nx_w only
     const bool packed = a.lb > 0;
     if (S == 1 && !packed) {
         constexpr size_t lds = sweep_lds_bytes<1, kSingleAcc, false>();

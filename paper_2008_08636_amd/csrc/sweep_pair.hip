@@ -114,7 +114,6 @@ __device__ __forceinline__ bool cnt_fast(uint32_t c) { return (int32_t)c < 0; }
 template <int S>
 struct NearSet {   // wave 0, one level
     uint32_t ol[kNEn];
-    int32_t tie[kNEn];
     int64_t c[kNEn];
     int64_t comp, mem;
     LabS<S> lab;
@@ -127,7 +126,6 @@ struct FarSet {    // wave 1, one level
     int32_t nb[kNEf];
     uint32_t ol[kNEf];
     int64_t c[kNEf];
-    int32_t tie[kNEf];
     VecS<S> f[kNEf];
     uint32_t wcnt;     // the level's counts (its window entry)
 };
@@ -153,6 +151,7 @@ struct PairCtx {
     int32_t V, L, P, K, p0;
     int32_t s0, s1, gen_end;   // steps of this chain; general path before gen_end
     int lb, ob;
+    int fo;          // bits of successor link below a workspace value's label (b, folded)
     long long omax;
     VS *vals;
     const LS *labs;
@@ -179,10 +178,11 @@ struct PairCtx {
         p0 = slice * S;
         lb = a->lb;
         ob = FWD ? 0 : a->ob;
+        fo = !FWD && a->nxf ? ob : 0;
         omax = (1ll << ob) - 1;
         vals = reinterpret_cast<VS *>((FWD ? a->ftl : a->bll) + (int64_t)slice * a->ws_stride);
         labs = reinterpret_cast<const LS *>(a->lab_w + (int64_t)slice * a->lab_stride);
-        want_nx = !FWD && a->nx_w != nullptr;
+        want_nx = !FWD && a->nx_w != nullptr && !a->nxf;
         nxs = reinterpret_cast<LS *>(a->nx_w + (want_nx ? (int64_t)slice * a->ws_stride : 0));
         pls = (ConstPairLevel)(FWD ? a->pl_t : a->pl_b);
         win = reinterpret_cast<WinEnt *>(smem);                       // [kWin]
@@ -191,11 +191,17 @@ struct PairCtx {
         slab = reinterpret_cast<LS *>(ring + kRS * kPNodes);           // [2][64]
         bins = reinterpret_cast<long long *>(slab + 2 * kPNodes);     // [K S]
     }
+    // the tl + comp or bl of a workspace (or ring) value
+    __device__ __forceinline__ int64_t gval(int64_t g) const { return EL::val(g, lb) >> fo; }
     __device__ __forceinline__ int64_t cand(int64_t g, int32_t own_lab, int64_t c) const {
-        return EL::val(g, lb) + (EL::lab(g, lb) != own_lab ? c : 0);
+        return gval(g) + (EL::lab(g, lb) != own_lab ? c : 0);
     }
     __device__ __forceinline__ long long akey(int64_t cv, int32_t tie) const {
         return FWD ? cv : (cv << ob) | tie;
+    }
+    // the key of an edge record's candidate from its cost word ck (t: ob = 0)
+    __device__ __forceinline__ long long rkey(int64_t g, int32_t own_lab, int64_t ck) const {
+        return (gval(g) << ob) + (EL::lab(g, lb) != own_lab ? ck : (ck & omax));
     }
     __device__ __forceinline__ int32_t level_of(int32_t step) const {   // L: empty level
         if (FWD) return step < L ? step : L;
@@ -217,8 +223,10 @@ struct PairCtx {
 #pragma unroll
         for (int s = 0; s < S; s++) {
             const long long k = ab[slot * S + s];
-            const int64_t t = FWD ? k : k >> ob;
-            out.v[s] = EL::make(FWD ? t + comp : comp + t, lab.v[s], lb);
+            // b, folded: (comp << ob) + k = ((comp + max) << ob) | successor's tie
+            // key, with k = 0 (no successor) leaving the link bits 0
+            const int64_t x = FWD ? k + comp : fo != 0 ? (comp << ob) + k : comp + (k >> ob);
+            out.v[s] = EL::make(x, lab.v[s], lb);
             nxv.v[s] = k == 0 ? -1 : (int32_t)(omax - (k & omax));
         }
 #pragma unroll
@@ -370,8 +378,7 @@ __device__ __forceinline__ void pair_chain(const SweepArgs &a, int32_t slice, ch
                 const uint32_t e = lane + j * kLanes < nn ? (uint32_t)(b.nrlo + lane + j * kLanes) : 0u;
                 const NearRec16 r = at(nrec, e);
                 X.ol[j] = r.ol;
-                X.tie[j] = r.tie;
-                X.c[j] = r.cost;
+                X.c[j] = r.ck;
             }
             const uint32_t v = lane < w ? (uint32_t)(b.nlo + lane) : 0u;
             const NodeRec16 n = at(a.node_rec, v);
@@ -407,8 +414,7 @@ __device__ __forceinline__ void pair_chain(const SweepArgs &a, int32_t slice, ch
                         const LS ol = sl[own];
 #pragma unroll
                         for (int s = 0; s < S; s++)
-                            lds_max_i64(&ab[own * S + s],
-                                        c.akey(c.cand(g.v[s], ol.v[s], B1.c[j]), B1.tie[j]));
+                            lds_max_i64(&ab[own * S + s], c.rkey(g.v[s], ol.v[s], B1.c[j]));
                     }
                 }
             }
@@ -478,8 +484,7 @@ __device__ __forceinline__ void pair_chain(const SweepArgs &a, int32_t slice, ch
                 const FarRec16 r = at(frec, e);
                 X.nb[j] = r.nb;
                 X.ol[j] = r.ol;
-                X.c[j] = r.cost;
-                X.tie[j] = FWD ? 0 : at(a.ftie_b, e);
+                X.c[j] = r.ck;
             }
         };
         auto far_loads = [&](FarSet<S> &X, const WinEnt &b) {
@@ -502,8 +507,7 @@ __device__ __forceinline__ void pair_chain(const SweepArgs &a, int32_t slice, ch
                     const LS ol = sl[own];
 #pragma unroll
                     for (int s = 0; s < S; s++)
-                        lds_max_i64(&ab[own * S + s],
-                                    c.akey(c.cand(g.v[s], ol.v[s], B1.c[j]), B1.tie[j]));
+                        lds_max_i64(&ab[own * S + s], c.rkey(g.v[s], ol.v[s], B1.c[j]));
                 }
             }
         };
@@ -578,13 +582,13 @@ __device__ __forceinline__ void pair_chain(const SweepArgs &a, int32_t slice, ch
     for (int s = 0; s < S; s++) {
         long long m = 0;
         for (int32_t i = lane; i < n0; i += kLanes) {
-            const long long x = EL::val(c.vals[i].v[s], c.lb);
+            const long long x = c.gval(c.vals[i].v[s]);
             m = x > m ? x : m;
         }
         m = wave_max_i64(m);
         int32_t first = INT32_MAX;
         for (int32_t i = lane; i < n0; i += kLanes)
-            if (EL::val(c.vals[i].v[s], c.lb) == m) first = min(first, i);
+            if (c.gval(c.vals[i].v[s]) == m) first = min(first, i);
 #pragma unroll
         for (int off = kLanes / 2; off > 0; off >>= 1) first = min(first, __shfl_xor(first, off, kLanes));
         if (lane == 0 && c.p0 + s < c.P) {
@@ -721,8 +725,7 @@ __global__ void k_pair_levels(int32_t L, const int32_t *level_ptr, const int32_t
 __global__ void k_pair_records(int64_t E, int32_t L, bool fwd, int32_t ob, const int32_t *level,
                                const int32_t *order, const int32_t *level_ptr, const int32_t *nbr,
                                const int32_t *own, const int64_t *cost, const int32_t *nb_orig,
-                               const int32_t *near_rank, NearRec16 *nr, FarRec16 *fr,
-                               int32_t *ftie) {
+                               const int32_t *near_rank, NearRec16 *nr, FarRec16 *fr) {
     const long long omax = (1ll << ob) - 1;
     for (int64_t e = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; e < E;
          e += (int64_t)gridDim.x * blockDim.x) {
@@ -732,12 +735,15 @@ __global__ void k_pair_records(int64_t E, int32_t L, bool fwd, int32_t ob, const
         const int32_t nb_lo = level_ptr[lv_nb];
         const uint32_t own_local = (uint32_t)(ow - level_ptr[lv_ow]) & 0xffffu;
         const uint32_t nb_local = (uint32_t)(nb - nb_lo);
-        const int32_t tie = fwd ? 0 : (int32_t)(omax - nb_orig[e]);
+        // the cost word (unsigned: when costs are too large for it, the
+        // packed keys and these records go unused)
+        const int64_t ck = fwd ? cost[e]
+                               : (int64_t)(((uint64_t)cost[e] << ob) | (uint64_t)(omax - nb_orig[e]));
         if (span == 1) {
             NearRec16 r;
             r.ol = own_local | ((nb_local & 0xffffu) << 16);
-            r.tie = tie;
-            r.cost = cost[e];
+            r.pad = 0;
+            r.ck = ck;
             nr[near_rank[e]] = r;
         } else {
             const int32_t w_nb = level_ptr[lv_nb + 1] - nb_lo;
@@ -748,10 +754,8 @@ __global__ void k_pair_records(int64_t E, int32_t L, bool fwd, int32_t ob, const
             FarRec16 r;
             r.nb = nb;
             r.ol = own_local | (rg << 16);
-            r.cost = cost[e];
-            const int64_t f = e - near_rank[e];
-            fr[f] = r;
-            if (!fwd) ftie[f] = tie;
+            r.ck = ck;
+            fr[e - near_rank[e]] = r;
         }
     }
 }
@@ -832,7 +836,7 @@ hipError_t launch_pair_flags(const Graph &g, bool fwd, int32_t *flag) {
 }
 
 hipError_t launch_pair_split(const Graph &g, bool fwd, const int32_t *near_rank, PairLevel *pl,
-                             NearRec16 *nr, FarRec16 *fr, int32_t *ftie) {
+                             NearRec16 *nr, FarRec16 *fr) {
     k_pair_levels<<<(unsigned)((g.L + 2 + 255) / 256), 256, 0, g.stream>>>(
         g.L, g.level_ptr, fwd ? g.in_off : g.out_off, near_rank, pl);
     hipError_t e = hipGetLastError();
@@ -841,7 +845,7 @@ hipError_t launch_pair_split(const Graph &g, bool fwd, const int32_t *near_rank,
     k_pair_records<<<grid, 256, 0, g.stream>>>(
         g.E, g.L, fwd, succ_bits(g.V), g.level, g.order, g.level_ptr,
         fwd ? g.in_src : g.out_dst, fwd ? g.in_dst : g.out_src, fwd ? g.in_cost : g.out_cost,
-        g.out_dst_orig, near_rank, nr, fr, ftie);
+        g.out_dst_orig, near_rank, nr, fr);
     return hipGetLastError();
 }
 

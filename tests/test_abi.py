@@ -95,6 +95,37 @@ def test_no_device_reports_e_device(lib):
     assert st == -5 and not h.value
 
 
+def test_fault_alloc_hook_reports_e_nomem(lib, monkeypatch):
+    """PARDNN_FAULT_ALLOC=n fails the n-th allocation attempt as out of
+    memory; the handle is the first allocation of pardnn_graph_create and
+    needs no device, so n = 1 gives E_NOMEM here as on a GPU."""
+    import ctypes
+    h = ctypes.c_void_p()
+    monkeypatch.setenv("PARDNN_FAULT_ALLOC", "1")
+    assert lib.pardnn_graph_create(0, 0, None, None, None, None, None, None,
+                                   ctypes.byref(h)) == -4
+    assert not h.value and b"host allocation" in lib.pardnn_last_error()
+    # one failure per value of the variable: the next attempt goes through
+    st = lib.pardnn_graph_create(0, 0, None, None, None, None, None, None, ctypes.byref(h))
+    assert st in (0, -5)
+    if st == 0:
+        assert lib.pardnn_graph_destroy(h) == 0
+    # a new value restarts the count; 0 and empty never fail
+    monkeypatch.setenv("PARDNN_FAULT_ALLOC", "01")
+    assert lib.pardnn_graph_create(0, 0, None, None, None, None, None, None,
+                                   ctypes.byref(h)) == -4
+    for v in ("0", ""):
+        monkeypatch.setenv("PARDNN_FAULT_ALLOC", v)
+        st = lib.pardnn_graph_create(0, 0, None, None, None, None, None, None, ctypes.byref(h))
+        assert st in (0, -5)
+        if st == 0:
+            assert lib.pardnn_graph_destroy(h) == 0
+    # argument errors come before any allocation
+    monkeypatch.setenv("PARDNN_FAULT_ALLOC", "1")
+    assert lib.pardnn_graph_create(-1, 0, None, None, None, None, None, None,
+                                   ctypes.byref(h)) == -1
+
+
 def test_binding_has_no_fallback(monkeypatch, tmp_path):
     import paper_2008_08636_amd as P
     monkeypatch.setattr(P, "_lib", None)

@@ -231,6 +231,105 @@ def test_determinism_and_stream(P):
 
 # --------------------------------------------------------------------- errors --
 
+def test_alloc_failure_injection(P, monkeypatch):
+    """Each allocation of a create -> levelize -> tb_levels -> critical path ->
+    label memory -> batch sequence fails once in turn (PARDNN_FAULT_ALLOC=n,
+    n = 1, 2, ...): the call that meets the failure returns E_NOMEM, the same
+    handle then finishes the sequence (the retried call allocates only what is
+    missing), and every result equals the oracle's."""
+    g = cfg(0)
+    exp = oracle_single(g)
+    pls_np = np.stack([g.placement, (g.placement + 1) % g.n_labels], axis=1).astype(np.int32)
+    exp_b = [oracle.evaluate(g.n_nodes, g.src, g.dst, g.comp, g.edge_cost, g.mem,
+                             pls_np[:, p].copy(), g.n_labels, g.capacity) for p in range(2)]
+    lab = dev(g.placement, torch.int32)
+    pls = dev(pls_np, torch.int32)
+    cap = dev(g.capacity, torch.int64)
+    hits = []
+    for n in range(1, 400):
+        say(f"allocation failure at attempt {n}")
+        monkeypatch.setenv("PARDNN_FAULT_ALLOC", str(n))
+        hit = []
+
+        def attempt(name, fn):
+            try:
+                return fn()
+            except P.PardnnError as e:
+                assert e.status == P.E_NOMEM, (n, name, str(e))
+                assert not hit, (n, name, hit)   # one failure per value
+                hit.append(name)
+                return fn()
+
+        G = attempt("create", lambda: P.Graph(g.n_nodes, g.src, g.dst, g.comp, g.edge_cost,
+                                              g.mem))
+        level, order, lptr, nl = attempt("levelize", G.levelize)
+        tl, bl, m = attempt("tb_levels", lambda: G.tb_levels(lab))
+        crit, path, plen = attempt("critical_path", lambda: G.critical_path(lab, tl, bl, m))
+        sums, over = attempt("label_memory", lambda: G.label_memory(lab, g.n_labels, cap))
+        out = attempt("batch", lambda: G.evaluate_batch(pls, g.n_labels, cap))
+        torch.cuda.synchronize()
+        got = {"level": level.cpu().numpy(), "order": order.cpu().numpy(),
+               "level_ptr": lptr.cpu().numpy(), "n_levels": nl, "tl": tl.cpu().numpy(),
+               "bl": bl.cpu().numpy(), "makespan": int(m.item()),
+               "is_critical": crit.cpu().numpy(), "path": path[: int(plen.item())].cpu().numpy(),
+               "label_mem": sums.cpu().numpy(), "overflow": over.cpu().numpy()}
+        assert_same(got, exp)
+        for p in range(2):
+            e = exp_b[p]
+            assert (out["tl"][:, p].cpu().numpy() == e["tl"]).all(), (n, p)
+            assert (out["bl"][:, p].cpu().numpy() == e["bl"]).all(), (n, p)
+            assert int(out["makespan"][p]) == e["makespan"]
+            assert (out["is_critical"][:, p].cpu().numpy() == e["is_critical"]).all()
+            k = int(out["path_len"][p])
+            assert out["path"][p, :k].cpu().numpy().tolist() == e["path"].tolist()
+            assert (out["label_mem"][p].cpu().numpy() == e["label_mem"]).all()
+            assert (out["overflow"][p].cpu().numpy() == e["overflow"]).all()
+        G.close()
+        if not hit:
+            break
+        hits.append(hit[0])
+    assert not hit, "the sequence never ran without a failure"
+    # every call of the sequence met a failure at least once
+    assert {"create", "levelize", "tb_levels", "batch"} <= set(hits), hits
+
+
+def test_fixed_entry_point_attempts_no_allocation(P, monkeypatch):
+    """pardnn_evaluate_batch_fixed on a levelized handle makes no allocation
+    attempt: with PARDNN_FAULT_ALLOC=1 set just before it, it succeeds, and
+    the failure lands on the next call that allocates (the first batch
+    workspace of the allocating entry point)."""
+    say("fixed entry point under allocation-failure injection")
+    g = cfg(0)
+    G = P.Graph(g.n_nodes, g.src, g.dst, g.comp, g.edge_cost, g.mem)
+    L = P.pardnn_levelize(G.handle)
+    pls_np = np.stack([g.placement, (g.placement + 2) % g.n_labels], axis=1).astype(np.int32)
+    pls = dev(pls_np, torch.int32)
+    cap = dev(g.capacity, torch.int64)
+    V, K = g.n_nodes, g.n_labels
+    i64 = dict(dtype=torch.int64, device="cuda")
+    o = {"tl": torch.empty((V, 2), **i64), "bl": torch.empty((V, 2), **i64),
+         "m": torch.empty(2, **i64), "crit": torch.empty((V, 2), dtype=torch.uint8, device="cuda"),
+         "path": torch.empty((2, max(L, 1)), dtype=torch.int32, device="cuda"),
+         "plen": torch.empty(2, dtype=torch.int32, device="cuda"),
+         "lm": torch.empty((2, K), **i64), "ov": torch.empty((2, K), **i64)}
+    monkeypatch.setenv("PARDNN_FAULT_ALLOC", "1")
+    P.pardnn_evaluate_batch_fixed(G.handle, 2, pls, K, cap, o["tl"], o["bl"], o["m"], o["crit"],
+                                  o["path"], max(L, 1), o["plen"], o["lm"], o["ov"])
+    with pytest.raises(P.PardnnError) as ei:
+        G.evaluate_batch(pls, K, cap)
+    assert ei.value.status == P.E_NOMEM
+    monkeypatch.delenv("PARDNN_FAULT_ALLOC")
+    torch.cuda.synchronize()
+    for p in range(2):
+        e = oracle.evaluate(V, g.src, g.dst, g.comp, g.edge_cost, g.mem, pls_np[:, p].copy(), K,
+                            g.capacity)
+        assert (o["tl"][:, p].cpu().numpy() == e["tl"]).all()
+        assert (o["bl"][:, p].cpu().numpy() == e["bl"]).all()
+        assert int(o["m"][p]) == e["makespan"]
+        assert (o["lm"][p].cpu().numpy() == e["label_mem"]).all()
+    G.close()
+
+
 def test_error_paths(P):
     say("error paths")
     def mk(n, src, dst, comp=None, cost=None, mem=None):
@@ -364,6 +463,31 @@ def test_batch_random_placements(P, i, n_place):
     tl, bl, m = G.tb_levels(lab)
     torch.cuda.synchronize()
     assert (tl.cpu().numpy() == out["tl"][:, 1]).all() and int(m.item()) == out["makespan"][1]
+    G.close()
+
+
+@pytest.mark.parametrize("shift", [18, 20])
+def test_batch_large_weights_successor_links(P, shift):
+    """Weights scaled by 2^shift on config 0 (4 labels: 2 label bits; 2050
+    nodes: 12 successor bits). 2^18 keeps the weight bound below 2^48, where
+    the successor links ride in the packed b values; 2^20 puts it between 2^48
+    and 2^50, where the values are still packed but the links need their own
+    array. Both give the oracle's results, paths included."""
+    import types
+    g0 = cfg(0)
+    f = 1 << shift
+    g = types.SimpleNamespace(n_nodes=g0.n_nodes, src=g0.src, dst=g0.dst, comp=g0.comp * f,
+                              edge_cost=g0.edge_cost * f, mem=g0.mem, n_labels=g0.n_labels,
+                              capacity=g0.capacity, placement=g0.placement)
+    wb = int(g.comp.sum()) + int(g.edge_cost.sum())
+    assert (wb < 2 ** 48) == (shift == 18) and wb < 2 ** 50
+    say(f"batch config0 weights x 2^{shift}")
+    rng = np.random.default_rng(300 + shift)
+    pl = rng.integers(0, g.n_labels, (g.n_nodes, 11)).astype(np.int32)
+    pl[:, 0] = g.placement
+    G = P.Graph(g.n_nodes, g.src, g.dst, g.comp, g.edge_cost, g.mem)
+    out = run_batch(P, G, pl, g)
+    check_batch(g, pl, out, range(11))
     G.close()
 
 
