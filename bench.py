@@ -565,6 +565,9 @@ def main() -> int:
         "overflow": torch.empty((Pn, K), dtype=torch.int64, device="cuda"),
     }
     P.pardnn_set_timing(G.handle, True)
+    # argument errors found on the device are taken after the timed steps
+    # instead of after each call, so that the steps run back to back
+    P.pardnn_set_deferred_errors(G.handle, True)
 
     def step():
         P.pardnn_evaluate_moves(G.handle, base, Pn, ptr, node, lab, K, cap, out["tl"], out["bl"],
@@ -607,6 +610,8 @@ def main() -> int:
         lean_ms = (time.perf_counter() - t0) * 1e3 / args.steps
         print(f"[bench] per-placement results only: {lean_ms:.3f} ms/step", file=sys.stderr,
               flush=True)
+    P.pardnn_take_errors(G.handle)   # raises if any step found an argument error
+    P.pardnn_set_deferred_errors(G.handle, False)
 
     k_ms = float(np.mean(kernel_ms))
     alg = algorithmic_bytes_sweep(V, E, Pn)

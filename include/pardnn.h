@@ -33,7 +33,11 @@
  *   - Every call returns PARDNN_OK or a negative status, never aborts and never
  *     throws. pardnn_last_error() gives a detail string for the calling thread.
  *   - A handle is used by one host thread at a time. Calls that report an
- *     error found on the device (marked "syncs") wait for the stream.
+ *     error found on the device (marked "syncs") wait for the stream, unless
+ *     the handle defers such errors (pardnn_set_deferred_errors): then those
+ *     calls only enqueue, and pardnn_take_errors reports what they found.
+ *     Either way the kernels bound every access by the sizes passed, so bad
+ *     values give wrong results at worst, never an access out of bounds.
  *
  * Batched layout: arrays of several placements are PLACEMENT-MINOR, i.e.
  * element (node v, placement p) of a [V][n_place] array sits at
@@ -196,15 +200,19 @@ int pardnn_apply_moves(pardnn_graph *g, int32_t *placement, int32_t n_moves,
  * moves are node[step_ptr[p] .. step_ptr[p+1]) -> label[same range] (a later
  * move of a node wins, within and across steps).
  *   base           int32[n_nodes].
- *   step_ptr       int64[n_place + 1], non-decreasing, step_ptr[0] = 0.
- *   node, label    int32[step_ptr[n_place]].
+ *   step_ptr       int64[n_place + 1], non-decreasing, step_ptr[0] = 0,
+ *                  step_ptr[n_place] = n_moves (checked on the device).
+ *   n_moves        host value: the length of node and label, 0 <= n_moves
+ *                  < 2^31.
+ *   node, label    int32[n_moves].
  *   placements     int32[n_nodes][n_place] output (placement-minor).
- * Errors: E_INVAL if a node id is out of range. Syncs.
+ * Errors: E_INVAL if a node id is out of range or step_ptr does not match
+ * n_moves. Syncs (unless errors are deferred).
  */
 int pardnn_build_placements(pardnn_graph *g, const int32_t *base,
                             int32_t n_place, const int64_t *step_ptr,
-                            const int32_t *node, const int32_t *label,
-                            int32_t *placements);
+                            int64_t n_moves, const int32_t *node,
+                            const int32_t *label, int32_t *placements);
 
 /*
  * Evaluate n_place placements at once: for every placement p the results of
@@ -228,7 +236,7 @@ int pardnn_build_placements(pardnn_graph *g, const int32_t *base,
  *   label_mem      int64[n_place][n_labels] output or NULL.
  *   overflow       int64[n_place][n_labels] output or NULL.
  * Errors: E_INVAL (bad label when label_mem != NULL, short path_stride).
- * Syncs when label_mem != NULL.
+ * Syncs when label_mem != NULL (unless errors are deferred).
  */
 int pardnn_evaluate_batch(pardnn_graph *g, int32_t n_place,
                           const int32_t *placements, int32_t n_labels,
@@ -267,13 +275,14 @@ int pardnn_evaluate_batch_fixed(pardnn_graph *g, int32_t n_place,
  * 0..p applied in order, exactly as pardnn_build_placements defines them;
  * every output is exactly that of pardnn_evaluate_batch on those placements,
  * but the [V][n_place] placement matrix is never materialised.
- *   base, step_ptr, node, label   as for pardnn_build_placements.
+ *   base, step_ptr, n_moves, node, label   as for pardnn_build_placements.
  *   other arguments               as for pardnn_evaluate_batch.
  * Errors: E_INVAL (bad move node id, bad label when label_mem != NULL, short
- * path_stride, malformed step_ptr). Syncs.
+ * path_stride, step_ptr not matching n_moves). Syncs (unless errors are
+ * deferred); no other host round trip.
  */
 int pardnn_evaluate_moves(pardnn_graph *g, const int32_t *base, int32_t n_place,
-                          const int64_t *step_ptr, const int32_t *node,
+                          const int64_t *step_ptr, int64_t n_moves, const int32_t *node,
                           const int32_t *label, int32_t n_labels,
                           const int64_t *capacity, int64_t *tl, int64_t *bl,
                           int64_t *makespan, uint8_t *is_critical,
@@ -416,6 +425,21 @@ int pardnn_tb_levels_batch(pardnn_graph *g, int32_t n_place,
  */
 int pardnn_set_timing(pardnn_graph *g, int enable);
 int pardnn_get_timing(pardnn_graph *g, const char **kernel, float *ms);
+
+/*
+ * Deferred errors, for callers that keep the GPU busy with back-to-back calls
+ * (the refinement loop): with enable != 0, the calls that would wait for the
+ * stream to report an argument error found on the device (label or node id
+ * out of range, negative capacity, bad node kind or cluster id, step_ptr not
+ * matching n_moves; those marked "syncs") return PARDNN_OK once their work
+ * is enqueued, and the error flags accumulate on the device. Host-side checks
+ * still fail at once. pardnn_take_errors waits for the handle's stream,
+ * returns E_INVAL if a call made since the last take found such an error
+ * (detail: the flags; results of those calls are unspecified) and clears
+ * them; PARDNN_OK otherwise. Default: errors are not deferred.
+ */
+int pardnn_set_deferred_errors(pardnn_graph *g, int enable);
+int pardnn_take_errors(pardnn_graph *g);
 
 /* Static text for a status code. */
 const char *pardnn_status_string(int status);

@@ -25,7 +25,8 @@ __all__ = [
     "pardnn_tb_levels_batch", "pardnn_memory_balance", "pardnn_slice_primaries",
     "pardnn_slice_graph",
     "pardnn_cluster_criticality", "pardnn_span_work", "pardnn_set_timing",
-    "pardnn_get_timing", "pardnn_status_string", "pardnn_last_error",
+    "pardnn_get_timing", "pardnn_set_deferred_errors", "pardnn_take_errors",
+    "pardnn_status_string", "pardnn_last_error",
 ]
 
 LIB_PATH = os.path.join(os.path.dirname(os.path.abspath(__file__)), "libpardnn.so")
@@ -67,10 +68,10 @@ def load_library(path: str = LIB_PATH):
         "pardnn_critical_path": [P, P, P, P, P, P, P, P],
         "pardnn_label_memory": [P, P, i32, P, P, P],
         "pardnn_apply_moves": [P, P, i32, P, P],
-        "pardnn_build_placements": [P, P, i32, P, P, P, P],
+        "pardnn_build_placements": [P, P, i32, P, i64, P, P, P],
         "pardnn_evaluate_batch": [P, i32, P, i32, P, P, P, P, P, P, i32, P, P, P],
         "pardnn_evaluate_batch_fixed": [P, i32, P, i32, P, P, P, P, P, P, i32, P, P, P],
-        "pardnn_evaluate_moves": [P, P, i32, P, P, P, i32, P, P, P, P, P, P, i32, P, P, P],
+        "pardnn_evaluate_moves": [P, P, i32, P, i64, P, P, i32, P, P, P, P, P, P, i32, P, P, P],
         "pardnn_tb_levels_batch": [P, i32, P, P, P, P],
         "pardnn_memory_balance": [P, i32, P, P, P, i32, P, P, P, P],
         "pardnn_slice_primaries": [P, i32, P, P, i32, P, P],
@@ -79,6 +80,8 @@ def load_library(path: str = LIB_PATH):
         "pardnn_span_work": [P, P, i32, P, i32, P, P, P, P, P, P],
         "pardnn_set_timing": [P, ctypes.c_int],
         "pardnn_get_timing": [P, ctypes.POINTER(ctypes.c_char_p), ctypes.POINTER(ctypes.c_float)],
+        "pardnn_set_deferred_errors": [P, ctypes.c_int],
+        "pardnn_take_errors": [P],
     }
     for name, args in sig.items():
         f = getattr(lib, name)
@@ -202,11 +205,23 @@ def pardnn_apply_moves(h, placement, node, label):
         _ptr(label, torch.int32, n, "label")), "pardnn_apply_moves")
 
 
-def pardnn_build_placements(h, base, n_place, step_ptr, node, label, placements):
+def _n_moves(node, label, n_moves):
+    """The number of moves: the length of node (and label) unless given."""
+    if n_moves is None:
+        n_moves = 0 if node is None else node.numel()
+    for t, name in ((node, "node"), (label, "label")):
+        if n_moves > 0 and (t is None or t.numel() < n_moves):
+            raise ValueError(f"{name} must hold at least n_moves = {n_moves} elements")
+    return n_moves
+
+
+def pardnn_build_placements(h, base, n_place, step_ptr, node, label, placements, n_moves=None):
+    n_moves = _n_moves(node, label, n_moves)
     _check(load_library().pardnn_build_placements(
         h, _ptr(base, torch.int32, name="base"), n_place,
-        _ptr(step_ptr, torch.int64, n_place + 1, "step_ptr"), _ptr(node, torch.int32, name="node"),
-        _ptr(label, torch.int32, name="label"), _ptr(placements, torch.int32, name="placements")),
+        _ptr(step_ptr, torch.int64, n_place + 1, "step_ptr"), n_moves,
+        _ptr(node, torch.int32, name="node"), _ptr(label, torch.int32, name="label"),
+        _ptr(placements, torch.int32, name="placements")),
         "pardnn_build_placements")
 
 
@@ -238,10 +253,12 @@ def pardnn_evaluate_batch_fixed(h, n_place, placements, n_labels, capacity, tl, 
 
 def pardnn_evaluate_moves(h, base, n_place, step_ptr, node, label, n_labels, capacity, tl, bl,
                           makespan, is_critical=None, path=None, path_stride=0, path_len=None,
-                          label_mem=None, overflow=None):
+                          label_mem=None, overflow=None, n_moves=None):
+    n_moves = _n_moves(node, label, n_moves)
     _check(load_library().pardnn_evaluate_moves(
         h, _ptr(base, torch.int32, name="base"), n_place,
-        _ptr(step_ptr, torch.int64, n_place + 1, "step_ptr"), _ptr(node, torch.int32, name="node"),
+        _ptr(step_ptr, torch.int64, n_place + 1, "step_ptr"), n_moves,
+        _ptr(node, torch.int32, name="node"),
         _ptr(label, torch.int32, name="label"), n_labels,
         _ptr(capacity, torch.int64, name="capacity"), _ptr(tl, torch.int64, name="tl"),
         _ptr(bl, torch.int64, name="bl"), _ptr(makespan, torch.int64, n_place, "makespan"),
@@ -309,6 +326,15 @@ def pardnn_span_work(h, label, K, cluster, n_clusters, tl, span_lo, span_hi, wor
 
 def pardnn_set_timing(h, enable: bool = True):
     _check(load_library().pardnn_set_timing(h, 1 if enable else 0), "pardnn_set_timing")
+
+
+def pardnn_set_deferred_errors(h, enable: bool = True):
+    _check(load_library().pardnn_set_deferred_errors(h, 1 if enable else 0),
+           "pardnn_set_deferred_errors")
+
+
+def pardnn_take_errors(h):
+    _check(load_library().pardnn_take_errors(h), "pardnn_take_errors")
 
 
 def pardnn_get_timing(h):

@@ -121,8 +121,24 @@ void release(Graph *g) {
     delete g;
 }
 
-// Copy the device error words to the host after the enqueued work finished.
+// Error words on the device: err[0] holds the argument-error flags that
+// calls check on the device (bit meanings per call), err[1] the internal
+// check of the secondary slicing walk.
+//
+// Start of a call that checks arguments on the device: clear the flags,
+// unless errors are deferred (they then accumulate until taken).
+hipError_t clear_errors(Graph *g) {
+    if (g->defer_errors) return hipSuccess;
+    return launch_fill_i32(g->err, 1, 0, g->stream);
+}
+
+// End of such a call: wait for the stream and copy the error words to the
+// host. With errors deferred, no wait: the host copy reads as clear.
 int read_errors(Graph *g) {
+    if (g->defer_errors) {
+        for (int i = 0; i < 4; i++) g->h_err[i] = 0;
+        return PARDNN_OK;
+    }
     HIP_TRY(hipMemcpyAsync(g->h_err, g->err, 4 * sizeof(int32_t), hipMemcpyDeviceToHost,
                            g->stream));
     HIP_TRY(hipStreamSynchronize(g->stream));
@@ -363,6 +379,7 @@ SweepArgs sweep_args(const Graph *g) {
 struct MovesIn {
     const int32_t *base;
     const int64_t *step_ptr;
+    int64_t n_moves;   // host value: the length of node and label
     const int32_t *node, *label;
 };
 
@@ -406,18 +423,12 @@ int evaluate_impl(Graph *g, int32_t n_place, const int32_t *placements, const Mo
     // that groups them by node
     int64_t n_moves = 0;
     if (mv != nullptr) {
-        int64_t ends[2] = {0, 0};
-        HIP_TRY(hipMemcpyAsync(&ends[0], mv->step_ptr, sizeof(int64_t), hipMemcpyDeviceToHost,
-                               g->stream));
-        HIP_TRY(hipMemcpyAsync(&ends[1], mv->step_ptr + n_place, sizeof(int64_t),
-                               hipMemcpyDeviceToHost, g->stream));
-        HIP_TRY(hipStreamSynchronize(g->stream));
-        if (ends[0] != 0 || ends[1] < 0 || ends[1] >= (int64_t)INT32_MAX)
-            return fail(PARDNN_E_INVAL, "step_ptr must start at 0 and hold fewer than 2^31 moves");
-        if (ends[1] > 0 && (mv->node == nullptr || mv->label == nullptr))
+        if (mv->n_moves < 0 || mv->n_moves >= (int64_t)INT32_MAX)
+            return fail(PARDNN_E_INVAL, "n_moves must lie in [0, 2^31)");
+        if (mv->n_moves > 0 && (mv->node == nullptr || mv->label == nullptr))
             return fail(PARDNN_E_INVAL, "node and label must be non-null");
         if (g->V > 0 && mv->base == nullptr) return fail(PARDNN_E_INVAL, "base must be non-null");
-        n_moves = ends[1];
+        n_moves = mv->n_moves;   // step_ptr is checked against it on the device
     }
     const size_t moves_bytes =
         mv != nullptr ? (moves_scratch_elems(g->V, n_moves) * sizeof(int32_t) + 255) / 256 * 256
@@ -486,9 +497,10 @@ int evaluate_impl(Graph *g, int32_t n_place, const int32_t *placements, const Mo
 
     const int32_t K = label_mem != nullptr ? n_labels : 0;
     int32_t *fit = gated ? g->bt_fit : nullptr;
-    HIP_TRY(launch_fill_i32(g->err, 4, 0, g->stream));
+    HIP_TRY(clear_errors(g));
     if (fit != nullptr) HIP_TRY(launch_fill_i32(fit, 1, 1, g->stream));
     if (mv != nullptr) {
+        HIP_TRY(launch_check_steps(mv->step_ptr, n_place, n_moves, g->err, g->stream));
         HIP_TRY(launch_moves_to_slices(*g, mv->base, n_place, mv->step_ptr, n_moves, mv->node,
                                        mv->label, S, moves_scratch, lab_w, lab_stride, K,
                                        g->err, fit));
@@ -569,6 +581,9 @@ int evaluate_impl(Graph *g, int32_t n_place, const int32_t *placements, const Mo
                                             ? "a moved node id is outside [0, n_nodes)"
                                             : "a label or a moved node id is out of range");
         if (g->h_err[0] & 2) return fail(PARDNN_E_INVAL, "a capacity is negative");
+        if (g->h_err[0] & kErrSteps)
+            return fail(PARDNN_E_INVAL, "step_ptr must start at 0, never decrease and end at "
+                                        "n_moves");
     }
     return PARDNN_OK;
 }
@@ -1004,7 +1019,7 @@ int pardnn_label_memory(pardnn_graph *h, const int32_t *placement, int32_t n_lab
     if (label_mem == nullptr || (g->V > 0 && placement == nullptr))
         return fail(PARDNN_E_INVAL, "placement and label_mem must be non-null");
     DEVICE_SCOPE(g);
-    HIP_TRY(launch_fill_i32(g->err, 4, 0, g->stream));
+    HIP_TRY(clear_errors(g));
     HIP_TRY(launch_label_memory(*g, placement, n_labels, capacity, label_mem, overflow, g->err));
     int st = read_errors(g);
     if (st != PARDNN_OK) return st;
@@ -1027,7 +1042,7 @@ int pardnn_memory_balance(pardnn_graph *h, int32_t n_place, const int32_t *place
     if (g->V > 0 && (placements == nullptr || node_type == nullptr || ref_target == nullptr))
         return fail(PARDNN_E_INVAL, "placements, node_type and ref_target must be non-null");
     DEVICE_SCOPE(g);
-    HIP_TRY(launch_fill_i32(g->err, 4, 0, g->stream));
+    HIP_TRY(clear_errors(g));
     // the events bracket the sums kernel alone (recorded inside the launch)
     if (g->timing && g->V > 0) {
         g->timed_kernel = "k_mem_balance_sums";
@@ -1081,7 +1096,7 @@ int pardnn_span_work(pardnn_graph *h, const int32_t *label, int32_t K, const int
         HIP_TRY(dalloc(*g, &g->span_cache.ids, g->V));
         HIP_TRY(dalloc(*g, &g->span_cache.changed, 1));
     }
-    HIP_TRY(launch_fill_i32(g->err, 4, 0, g->stream));
+    HIP_TRY(clear_errors(g));
     {
         TimedLaunch t(g, "span_work");
         HIP_TRY(launch_span_work(*g, label, K, cluster, n_clusters, tl, span_lo, span_hi, work,
@@ -1114,7 +1129,7 @@ int pardnn_cluster_criticality(pardnn_graph *h, const int32_t *cluster, int32_t 
     }
     const size_t sort_bytes = (cluster_sort_bytes(V, n_clusters) + 255) / 256 * 256;
     HIP_TRY(grow_aux(g, sort_bytes + cluster_relabel_bytes(V, n_clusters)));
-    HIP_TRY(launch_fill_i32(g->err, 4, 0, g->stream));
+    HIP_TRY(clear_errors(g));
     // The pair sweep packs labels below 2^16. The cluster ids fit when there
     // are few clusters; otherwise labels with the same equality on every edge
     // (levels for lone nodes, L + rank for the others) often do.
@@ -1290,7 +1305,7 @@ int pardnn_slice_graph(pardnn_graph *h, int32_t K, int32_t *cluster, int32_t *cl
     int64_t *ms = reinterpret_cast<int64_t *>(base + paths_bytes);
     int32_t *plen = reinterpret_cast<int32_t *>(ms + K);
     void *peel = base + paths_bytes + small_bytes;
-    HIP_TRY(launch_fill_i32(g->err, 4, 0, g->stream));
+    HIP_TRY(launch_fill_i32(g->err + 1, 1, 0, g->stream));
     if (V == 0) {
         HIP_TRY(launch_fill_i32(cluster_off, (int64_t)K + 1, 0, g->stream));
         HIP_TRY(launch_fill_i32(n_clusters, 1, K, g->stream));
@@ -1307,11 +1322,14 @@ int pardnn_slice_graph(pardnn_graph *h, int32_t K, int32_t *cluster, int32_t *cl
         TimedLaunch t(g, "secondary clusters");
         HIP_TRY(launch_slice_secondaries(*g, K, paths, stride, plen, g->sl_tl, g->sl_bl,
                                          g->sl_alive, cluster, cluster_off, cluster_nodes,
-                                         n_clusters, peel, lds, g->err));
+                                         n_clusters, peel, lds, g->err + 1));
     }
-    st = read_errors(g);
-    if (st != PARDNN_OK) return st;
-    if (g->h_err[0] & 1) return fail(PARDNN_E_DEVICE, "the secondary walk stopped early");
+    // an internal check, never deferred
+    int32_t walk_err = 0;
+    HIP_TRY(hipMemcpyAsync(&walk_err, g->err + 1, sizeof(int32_t), hipMemcpyDeviceToHost,
+                           g->stream));
+    HIP_TRY(hipStreamSynchronize(g->stream));
+    if (walk_err & 1) return fail(PARDNN_E_DEVICE, "the secondary walk stopped early");
     return PARDNN_OK;
 }
 
@@ -1328,7 +1346,7 @@ int pardnn_apply_moves(pardnn_graph *h, int32_t *placement, int32_t n_moves, con
         HIP_TRY(dalloc(*g, &g->move_stamp, g->V));
         HIP_TRY(launch_fill_i32(g->move_stamp, g->V, -1, g->stream));
     }
-    HIP_TRY(launch_fill_i32(g->err, 4, 0, g->stream));
+    HIP_TRY(clear_errors(g));
     HIP_TRY(launch_apply_moves(*g, placement, n_moves, node, label, g->err));
     int st = read_errors(g);
     if (st != PARDNN_OK) return st;
@@ -1337,31 +1355,28 @@ int pardnn_apply_moves(pardnn_graph *h, int32_t *placement, int32_t n_moves, con
 }
 
 int pardnn_build_placements(pardnn_graph *h, const int32_t *base, int32_t n_place,
-                            const int64_t *step_ptr, const int32_t *node, const int32_t *label,
-                            int32_t *placements) {
+                            const int64_t *step_ptr, int64_t n_moves, const int32_t *node,
+                            const int32_t *label, int32_t *placements) {
     CHECK_HANDLE(h);
     Graph *g = reinterpret_cast<Graph *>(h);
     if (n_place < 0) return fail(PARDNN_E_INVAL, "n_place must be >= 0");
     if (n_place == 0) return PARDNN_OK;
     if (step_ptr == nullptr || (g->V > 0 && (base == nullptr || placements == nullptr)))
         return fail(PARDNN_E_INVAL, "base, step_ptr and placements must be non-null");
-    DEVICE_SCOPE(g);
-    int64_t ends[2] = {0, 0};
-    HIP_TRY(hipMemcpyAsync(&ends[0], step_ptr, sizeof(int64_t), hipMemcpyDeviceToHost, g->stream));
-    HIP_TRY(hipMemcpyAsync(&ends[1], step_ptr + n_place, sizeof(int64_t), hipMemcpyDeviceToHost,
-                           g->stream));
-    HIP_TRY(hipStreamSynchronize(g->stream));
-    const int64_t M = ends[1];
-    if (ends[0] != 0 || M < 0 || M >= (int64_t)INT32_MAX)
-        return fail(PARDNN_E_INVAL, "step_ptr must start at 0 and hold fewer than 2^31 moves");
-    if (M > 0 && (node == nullptr || label == nullptr))
+    if (n_moves < 0 || n_moves >= (int64_t)INT32_MAX)
+        return fail(PARDNN_E_INVAL, "n_moves must lie in [0, 2^31)");
+    if (n_moves > 0 && (node == nullptr || label == nullptr))
         return fail(PARDNN_E_INVAL, "node and label must be non-null");
-    HIP_TRY(launch_fill_i32(g->err, 4, 0, g->stream));
-    HIP_TRY(launch_build_placements(*g, base, n_place, step_ptr, M, node, label, placements,
+    DEVICE_SCOPE(g);
+    HIP_TRY(clear_errors(g));
+    HIP_TRY(launch_check_steps(step_ptr, n_place, n_moves, g->err, g->stream));
+    HIP_TRY(launch_build_placements(*g, base, n_place, step_ptr, n_moves, node, label, placements,
                                     g->err));
     int st = read_errors(g);
     if (st != PARDNN_OK) return st;
     if (g->h_err[0] & 1) return fail(PARDNN_E_INVAL, "a moved node id is outside [0, n_nodes)");
+    if (g->h_err[0] & kErrSteps)
+        return fail(PARDNN_E_INVAL, "step_ptr must start at 0, never decrease and end at n_moves");
     return PARDNN_OK;
 }
 
@@ -1379,7 +1394,8 @@ int pardnn_evaluate_batch(pardnn_graph *h, int32_t n_place, const int32_t *place
 }
 
 int pardnn_evaluate_moves(pardnn_graph *h, const int32_t *base, int32_t n_place,
-                          const int64_t *step_ptr, const int32_t *node, const int32_t *label,
+                          const int64_t *step_ptr, int64_t n_moves, const int32_t *node,
+                          const int32_t *label,
                           int32_t n_labels, const int64_t *capacity, int64_t *tl, int64_t *bl,
                           int64_t *makespan, uint8_t *is_critical, int32_t *path,
                           int32_t path_stride, int32_t *path_len, int64_t *label_mem,
@@ -1387,9 +1403,34 @@ int pardnn_evaluate_moves(pardnn_graph *h, const int32_t *base, int32_t n_place,
     CHECK_HANDLE(h);
     Graph *g = reinterpret_cast<Graph *>(h);
     if (n_place > 0 && step_ptr == nullptr) return fail(PARDNN_E_INVAL, "step_ptr must be non-null");
-    MovesIn mv{base, step_ptr, node, label};
+    MovesIn mv{base, step_ptr, n_moves, node, label};
     return evaluate_impl(g, n_place, nullptr, &mv, n_labels, capacity, tl, bl, makespan,
                          is_critical, path, path_stride, path_len, label_mem, overflow);
+}
+
+int pardnn_set_deferred_errors(pardnn_graph *h, int enable) {
+    CHECK_HANDLE(h);
+    Graph *g = reinterpret_cast<Graph *>(h);
+    DEVICE_SCOPE(g);
+    // a fresh start either way: no flags from before the switch
+    HIP_TRY(launch_fill_i32(g->err, 1, 0, g->stream));
+    g->defer_errors = enable != 0;
+    return PARDNN_OK;
+}
+
+int pardnn_take_errors(pardnn_graph *h) {
+    CHECK_HANDLE(h);
+    Graph *g = reinterpret_cast<Graph *>(h);
+    DEVICE_SCOPE(g);
+    int32_t flags = 0;
+    HIP_TRY(hipMemcpyAsync(&flags, g->err, sizeof(int32_t), hipMemcpyDeviceToHost, g->stream));
+    HIP_TRY(hipStreamSynchronize(g->stream));
+    HIP_TRY(launch_fill_i32(g->err, 1, 0, g->stream));
+    if (flags != 0)
+        return fail(PARDNN_E_INVAL, "a call made since the last take found an argument out of "
+                                    "range on the device (error flags " +
+                                        std::to_string(flags) + ")");
+    return PARDNN_OK;
 }
 
 int pardnn_set_timing(pardnn_graph *h, int enable) {

@@ -130,6 +130,7 @@ struct Graph {
 
     // instrumentation: events around the main kernel of a call
     bool timing = false;
+    bool defer_errors = false;   // argument errors found on the device: kept for pardnn_take_errors
     bool timed = false;
     hipEvent_t ev0 = nullptr, ev1 = nullptr;
     const char *timed_kernel = "";
@@ -300,6 +301,12 @@ hipError_t launch_apply_moves(const Graph &g, int32_t *placement, int32_t n, con
 hipError_t launch_build_placements(const Graph &g, const int32_t *base, int32_t P,
                                    const int64_t *step_ptr, int64_t M, const int32_t *node,
                                    const int32_t *label, int32_t *placements, int32_t *err);
+// err bit of a step_ptr that does not start at 0, decreases somewhere or does
+// not end at the number of moves the caller passed
+constexpr int32_t kErrSteps = 8;
+// checks step_ptr[0 .. P] against M moves (sets kErrSteps in *err)
+hipError_t launch_check_steps(const int64_t *step_ptr, int32_t P, int64_t M, int32_t *err,
+                              hipStream_t s);
 // ---- heuristics.hip ----
 // Memory Heuristic II sums, Eq. 6 and reference co-location for P placements
 // [V][P]; err bits: 1 label out of range, 2 bad node kind, 4 bad reference target

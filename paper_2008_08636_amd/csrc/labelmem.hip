@@ -434,7 +434,29 @@ hipError_t launch_apply_moves(const Graph &g, int32_t *placement, int32_t n, con
     return hipGetLastError();
 }
 
-// M = step_ptr[P], the number of moves, read on the host by the caller.
+namespace {
+
+__global__ void k_check_steps(const int64_t *step_ptr, int32_t P, int64_t M, int32_t *err) {
+    for (int64_t p = blockIdx.x * (int64_t)blockDim.x + threadIdx.x; p <= P;
+         p += (int64_t)gridDim.x * blockDim.x) {
+        const int64_t x = step_ptr[p];
+        const bool bad = (p == 0 && x != 0) || (p == P && x != M) || (p < P && step_ptr[p + 1] < x);
+        if (bad) atomicOr(err, kErrSteps);
+    }
+}
+
+}  // namespace
+
+hipError_t launch_check_steps(const int64_t *step_ptr, int32_t P, int64_t M, int32_t *err,
+                              hipStream_t s) {
+    if (P < 0) return hipErrorInvalidValue;
+    k_check_steps<<<grid_for((int64_t)P + 1, kBlock), kBlock, 0, s>>>(step_ptr, P, M, err);
+    return hipGetLastError();
+}
+
+// M: the number of moves (the length of node and label), passed by the
+// caller; the moves of each step are found by binary search in step_ptr, so
+// any step_ptr keeps every access in bounds.
 hipError_t launch_build_placements(const Graph &g, const int32_t *base, int32_t P,
                                    const int64_t *step_ptr, int64_t M, const int32_t *node,
                                    const int32_t *label, int32_t *placements, int32_t *err) {

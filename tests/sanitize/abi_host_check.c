@@ -79,13 +79,13 @@ int main(void)
     EXPECT(pardnn_critical_path(NULL, i32, i64, i64, i64, u8, i32, i32) == PARDNN_E_INVAL);
     EXPECT(pardnn_label_memory(NULL, i32, 1, i64, i64, i64) == PARDNN_E_INVAL);
     EXPECT(pardnn_apply_moves(NULL, i32, 1, i32, i32) == PARDNN_E_INVAL);
-    EXPECT(pardnn_build_placements(NULL, i32, 1, i64, i32, i32, i32) == PARDNN_E_INVAL);
+    EXPECT(pardnn_build_placements(NULL, i32, 1, i64, 1, i32, i32, i32) == PARDNN_E_INVAL);
     EXPECT(pardnn_evaluate_batch(NULL, 1, i32, 1, i64, i64, i64, i64, u8, i32, 1, i32, i64,
                                  i64) == PARDNN_E_INVAL);
     EXPECT(pardnn_evaluate_batch_fixed(NULL, 1, i32, 1, i64, i64, i64, i64, u8, i32, 1, i32,
                                        i64, i64) == PARDNN_E_INVAL);
-    EXPECT(pardnn_evaluate_moves(NULL, i32, 1, i64, i32, i32, 1, i64, i64, i64, i64, u8, i32, 1,
-                                 i32, i64, i64) == PARDNN_E_INVAL);
+    EXPECT(pardnn_evaluate_moves(NULL, i32, 1, i64, 1, i32, i32, 1, i64, i64, i64, i64, u8, i32,
+                                 1, i32, i64, i64) == PARDNN_E_INVAL);
     EXPECT(pardnn_memory_balance(NULL, 1, i32, i32, i32, 1, i64, i64, u8, i64) ==
            PARDNN_E_INVAL);
     EXPECT(pardnn_cluster_criticality(NULL, i32, 1, i64, i32) == PARDNN_E_INVAL);
@@ -96,6 +96,8 @@ int main(void)
     EXPECT(pardnn_tb_levels_batch(NULL, 1, i32, i64, i64, i64) == PARDNN_E_INVAL);
     EXPECT(pardnn_set_timing(NULL, 1) == PARDNN_E_INVAL);
     EXPECT(pardnn_get_timing(NULL, &name, &ms) == PARDNN_E_INVAL);
+    EXPECT(pardnn_set_deferred_errors(NULL, 1) == PARDNN_E_INVAL);
+    EXPECT(pardnn_take_errors(NULL) == PARDNN_E_INVAL);
     EXPECT(strstr(pardnn_last_error(), "null") != NULL);
 
     /* many failing calls: the error text is replaced, never accumulated */

@@ -683,6 +683,67 @@ def test_evaluate_moves_small(P):
     G.close()
 
 
+def test_step_ptr_checks_and_deferred_errors(P):
+    """step_ptr is checked against the number of moves on the device (no host
+    read-back): one that does not start at 0, decreases or does not end at
+    n_moves gives E_INVAL. With deferred errors the calls only enqueue and
+    pardnn_take_errors reports what they found, once; valid calls give the
+    same results in both modes."""
+    say("step_ptr checks and deferred errors")
+    g = cfg(0)
+    sched = W.config4_moves(g, n_place=20, frac=0.05, seed=5)
+    G = P.Graph(g.n_nodes, g.src, g.dst, g.comp, g.edge_cost, g.mem)
+    base, ptr = dev(sched.base, torch.int32), dev(sched.ptr, torch.int64)
+    node, lab = dev(sched.node, torch.int32), dev(sched.label, torch.int32)
+    cap = dev(g.capacity, torch.int64)
+    ref = {k: v.cpu().numpy() for k, v in
+           G.evaluate_moves(base, ptr, node, lab, g.n_labels, cap).items()}
+    check_batch(g, W.materialize_placements(sched).T.copy(), ref, range(20))
+    bads = []
+    b = sched.ptr.copy(); b[-1] -= 1; bads.append(b)          # ends before n_moves
+    b = sched.ptr.copy(); b[0] = 1; bads.append(b)            # does not start at 0
+    b = sched.ptr.copy(); b[5], b[6] = b[6] + 1, b[5]; bads.append(b)   # decreases
+    for b in bads:
+        for call in (lambda: G.evaluate_moves(base, dev(b, torch.int64), node, lab, g.n_labels,
+                                              cap),
+                     lambda: G.build_placements(base, dev(b, torch.int64), node, lab)):
+            with pytest.raises(P.PardnnError) as e:
+                call()
+            assert e.value.status == P.E_INVAL and "step_ptr" in str(e.value)
+    # a shorter n_moves than step_ptr ends at
+    with pytest.raises(P.PardnnError) as e:
+        o, stride = G._outputs(20, g.n_labels, True, True, True)
+        P.pardnn_evaluate_moves(G.handle, base, 20, ptr, node, lab, g.n_labels, cap, o["tl"],
+                                o["bl"], o["makespan"], o["is_critical"], o["path"], stride,
+                                o["path_len"], o["label_mem"], o["overflow"],
+                                n_moves=node.numel() - 1)
+    assert e.value.status == P.E_INVAL
+    # deferred: the bad calls return at once, the take reports them once
+    P.pardnn_set_deferred_errors(G.handle, True)
+    bad_node = sched.node.copy()
+    bad_node[2] = g.n_nodes + 3
+    G.evaluate_moves(base, ptr, dev(bad_node, torch.int32), lab, g.n_labels, cap)
+    G.build_placements(base, dev(bads[2], torch.int64), node, lab)
+    out = G.evaluate_moves(base, ptr, node, lab, g.n_labels, cap)
+    with pytest.raises(P.PardnnError) as e:
+        P.pardnn_take_errors(G.handle)
+    assert e.value.status == P.E_INVAL
+    P.pardnn_take_errors(G.handle)   # cleared
+    got = {k: v.cpu().numpy() for k, v in out.items()}
+    for k in ref:
+        assert (ref[k] == got[k]).all(), k
+    bad_lab = dev(np.full(g.n_nodes, g.n_labels, np.int32), torch.int32)
+    G.label_memory(bad_lab, g.n_labels, cap)
+    with pytest.raises(P.PardnnError) as e:
+        P.pardnn_take_errors(G.handle)
+    assert e.value.status == P.E_INVAL
+    P.pardnn_set_deferred_errors(G.handle, False)
+    with pytest.raises(P.PardnnError) as e:
+        G.label_memory(bad_lab, g.n_labels, cap)
+    assert e.value.status == P.E_INVAL
+    G.close()
+
+
 def test_c4_refinement_loop_full_size(P):
     """The 1000-placement refinement loop on the transformer graph, in the
     launch configuration the benchmark times (pardnn_evaluate_moves); sampled
