@@ -61,6 +61,14 @@ def algorithmic_bytes_tb_single(V: int, E: int) -> int:
     return 48 * E + 64 * V
 
 
+def algorithmic_bytes_secondary(V: int, E: int) -> int:
+    """The secondary walk of graph slicing over the graph left after the
+    primaries (bounded here by the whole graph): per node its priority (8 B)
+    read and its cluster id and list entry written (4 + 4 B); per edge the
+    successor id read (4 B) and the successor's removed flag tested (4 B)."""
+    return 16 * V + 8 * E
+
+
 def algorithmic_bytes_mem_balance(V: int, P: int, K: int, n_ref: int) -> int:
     """The sums kernel of Memory Heuristic II on P placements: the [V][P]
     placement matrix (4 B per entry), the target label of each reference node
@@ -169,7 +177,8 @@ def cpu_baseline_line(r, E: int, what: str):
     }
 
 
-ROWS = ("refinement", "single", "memory_balance", "cluster_criticality", "slicing", "span_work")
+ROWS = ("refinement", "single", "memory_balance", "cluster_criticality", "slicing", "slice_graph",
+        "span_work")
 
 
 def time_calls(P, G, fn, steps: int, warmup: int):
@@ -461,6 +470,35 @@ def bench_row(args, row: str) -> int:
             cpu = {"value": round(reps * Ks / dt, 3), "unit": unit, "cores": 1,
                    "kind": "oracle",
                    "sample": f"{reps} runs of the same {Ks} rounds, {dt:.1f} s on one core of "
+                             f"'{host_cpu_model()}'"}
+    elif row == "slice_graph":
+        Ks = 16
+        i32 = dict(dtype=torch.int32, device="cuda")
+        cluster = torch.empty(V, **i32)
+        off = torch.empty(V + Ks + 1, **i32)
+        nodes = torch.empty(V, **i32)
+        n_cl = torch.empty(1, **i32)
+        ms = torch.empty(Ks, dtype=torch.int64, device="cuda")
+        fn = lambda: P.pardnn_slice_graph(G.handle, Ks, cluster, off, nodes, n_cl, ms)
+        wall, k_ms, kname = time_calls(P, G, fn, args.steps, args.warmup)
+        n_clusters = int(n_cl.item())
+        roof = hbm_roofline(kname, k_ms, algorithmic_bytes_secondary(V, E),
+                            "the timed launches are the secondary clusters (priority sort, "
+                            "then one wave following one dependent step per node); their "
+                            "bound is latency")
+        value, unit = 1e3 / wall, "slicings/s"
+        metric = "graph slicings/sec (Alg. 1 in full: K primaries, then the secondary clusters), 1 MI355X"
+        workload = (f"graph slicing with {Ks} primaries and the secondary walk on stale "
+                    f"priorities ({n_clusters} clusters in all) on the {graph_desc}")
+        if budget > 0:
+            from oracle.slicing import slice_all
+            t0, reps = time.perf_counter(), 0
+            while reps < 1 or time.perf_counter() - t0 < budget:
+                slice_all(V, g.src, g.dst, g.comp, g.edge_cost, Ks)
+                reps += 1
+            dt = time.perf_counter() - t0
+            cpu = {"value": round(reps / dt, 4), "unit": unit, "cores": 1, "kind": "oracle",
+                   "sample": f"{reps} full slicings, {dt:.1f} s on one core of "
                              f"'{host_cpu_model()}'"}
     else:
         raise ValueError(row)

@@ -62,11 +62,13 @@ constexpr int kBinsNone = 0, kBinsLds = 1, kBinsGlobal = 2;
 
 typedef const __attribute__((address_space(4))) PairLevel *ConstPairLevel;
 typedef const __attribute__((address_space(4))) SweepArgs KArgs;
+typedef __attribute__((address_space(3))) char LdsBytes;   // the dynamic LDS, as bytes
 
 // The kernel's argument block (its only argument, at offset 0 of the kernarg
 // segment) through a pointer the compiler cannot see through, so that loads
 // from it stay where they are written: the general level path re-reads its
-// pointers inside its branch instead of keeping them live across the loop.
+// pointers instead of the loop keeping them live. Defined in the kernel's own
+// code only (a called function would read a null segment pointer).
 __device__ __forceinline__ KArgs *kargs_here() {
     KArgs *p = (KArgs *)__builtin_amdgcn_kernarg_segment_ptr();
     asm volatile("" : "+s"(p));
@@ -266,11 +268,16 @@ __device__ __forceinline__ int32_t pipe_start(const Ctx &c) {
 // The general level step, for both waves: the level in chunks of 64 nodes
 // from the workspace, the early folds of a level too wide for the ring, and
 // the next level's edges. Everything it reads from the arguments is read
-// afresh through kargs_here(), so that the pipelined loop around it does not
-// carry its pointers in registers.
+// afresh through `a` (the kernel's argument block: the kernarg segment
+// pointer is defined in the kernel only, so the caller passes it), so that the
+// pipelined loop around it does not carry its pointers in registers. It is a
+// real call, not inlined: the unrolled loop would otherwise hold eight copies
+// of it per chain, and the smaller loop body takes instruction-cache misses
+// off every fast level.
 template <int S, bool FWD, bool NEAR, int BM>
-__device__ __forceinline__ void pair_slow(int32_t slice, int32_t step, char *smem) {
-    KArgs *a = kargs_here();
+__device__ __attribute__((noinline)) void pair_slow(KArgs *a, int32_t slice, int32_t step,
+                                                    LdsBytes *smem_l) {
+    char *smem = (char *)smem_l;
     const PairCtx<S, FWD, BM> c(a, slice, smem);
     using VS = VecS<S>;
     using LS = LabS<S>;
@@ -431,7 +438,7 @@ __device__ __forceinline__ void pair_chain(const SweepArgs &a, int32_t slice, ch
         __syncthreads();
         // a segment's first levels, on the general path
         for (int32_t sx = s0; sx < a0; sx++) {
-            pair_slow<S, FWD, true, BM>(c.p0 / S, sx, reinterpret_cast<char *>(c.win));
+            pair_slow<S, FWD, true, BM>(kargs_here(), c.p0 / S, sx, (LdsBytes *)c.win);
             __syncthreads();
         }
         if (a0 < s1) {
@@ -457,7 +464,7 @@ __device__ __forceinline__ void pair_chain(const SweepArgs &a, int32_t slice, ch
                 if (cnt_fast(b0.cnt))
                     body(sa, b0, b1, st[r], st[(r + 1) % kNS]);
                 else
-                    pair_slow<S, FWD, true, BM>(c.p0 / S, sa, reinterpret_cast<char *>(c.win));
+                    pair_slow<S, FWD, true, BM>(kargs_here(), c.p0 / S, sa, (LdsBytes *)c.win);
                 tail(sa, st[(r + 2) % kNS], st[(r + kLN) % kNS], b2, bl);
                 step++;
             }
@@ -468,7 +475,7 @@ __device__ __forceinline__ void pair_chain(const SweepArgs &a, int32_t slice, ch
         // the last levels (fewer than kNS) on the general path; folding an
         // edge a second time into a maximum changes nothing
         for (; step < s1; step++) {
-            pair_slow<S, FWD, true, BM>(c.p0 / S, step, reinterpret_cast<char *>(c.win));
+            pair_slow<S, FWD, true, BM>(kargs_here(), c.p0 / S, step, (LdsBytes *)c.win);
             __syncthreads();
         }
     } else {
@@ -515,7 +522,7 @@ __device__ __forceinline__ void pair_chain(const SweepArgs &a, int32_t slice, ch
         const int32_t s0 = c.s0, s1 = c.s1;
         const int32_t a0 = pipe_start(c);
         for (int32_t sx = s0; sx < a0; sx++) {
-            pair_slow<S, FWD, false, BM>(c.p0 / S, sx, reinterpret_cast<char *>(c.win));
+            pair_slow<S, FWD, false, BM>(kargs_here(), c.p0 / S, sx, (LdsBytes *)c.win);
             __syncthreads();
         }
         if (a0 < s1) {
@@ -545,7 +552,7 @@ __device__ __forceinline__ void pair_chain(const SweepArgs &a, int32_t slice, ch
                 if (cnt_fast(b0.cnt)) {
                     if (cnt_fast(b1.cnt)) fold_far(sa, B1, b1);
                 } else {
-                    pair_slow<S, FWD, false, BM>(c.p0 / S, sa, reinterpret_cast<char *>(c.win));
+                    pair_slow<S, FWD, false, BM>(kargs_here(), c.p0 / S, sa, (LdsBytes *)c.win);
                 }
                 // far values in flight stay valid across a general-path level:
                 // a far edge either spans more than D + 1 levels or was folded
@@ -558,7 +565,7 @@ __device__ __forceinline__ void pair_chain(const SweepArgs &a, int32_t slice, ch
         };
         while (step + kNS <= s1) unroll_seq(one, std::make_integer_sequence<int, kNS>{});
         for (; step < s1; step++) {
-            pair_slow<S, FWD, false, BM>(c.p0 / S, step, reinterpret_cast<char *>(c.win));
+            pair_slow<S, FWD, false, BM>(kargs_here(), c.p0 / S, step, (LdsBytes *)c.win);
             __syncthreads();
         }
     }
