@@ -648,6 +648,22 @@ def main() -> int:
         lean_ms = (time.perf_counter() - t0) * 1e3 / args.steps
         print(f"[bench] per-placement results only: {lean_ms:.3f} ms/step", file=sys.stderr,
               flush=True)
+    # the same loop without label sums: the labels are then unchecked, and
+    # whether they fit the packed sweep (below 2^16) is decided on the device
+    nolab_ms = None
+    if args.steps > 0:
+        def nolab():
+            P.pardnn_evaluate_moves(G.handle, base, Pn, ptr, node, lab, 0, None, out["tl"],
+                                    out["bl"], out["makespan"], out["crit"], out["path"], L,
+                                    out["path_len"], None, None)
+        nolab()
+        torch.cuda.synchronize()
+        t0 = time.perf_counter()
+        for _ in range(args.steps):
+            nolab()
+        torch.cuda.synchronize()
+        nolab_ms = (time.perf_counter() - t0) * 1e3 / args.steps
+        print(f"[bench] without label sums: {nolab_ms:.3f} ms/step", file=sys.stderr, flush=True)
     P.pardnn_take_errors(G.handle)   # raises if any step found an argument error
     P.pardnn_set_deferred_errors(G.handle, False)
 
@@ -718,6 +734,11 @@ def main() -> int:
                           "evals_per_s": round(Pn / (lean_ms / 1e3), 1),
                           "note": "same loop; tl, bl and critical flags computed but not "
                                   "written out (makespan, path, label sums, overflows kept)"}),
+        "no_label_sums": (None if nolab_ms is None else
+                          {"ms_per_step": round(nolab_ms, 4),
+                           "evals_per_s": round(Pn / (nolab_ms / 1e3), 1),
+                           "note": "same loop without label sums (every other output written); "
+                                   "the packed sweep is chosen on the device"}),
         "structure_ms": round(structure_ms, 2),
         "roofline": roofline,
         "single": single,
