@@ -219,8 +219,11 @@ int pardnn_build_placements(pardnn_graph *g, const int32_t *base,
  * pardnn_tb_levels, pardnn_critical_path and pardnn_label_memory. All arrays
  * are placement-minor.
  *   placements     int32[n_nodes][n_place].
- *   n_labels, capacity  as for pardnn_label_memory (n_labels is ignored when
- *                  label_mem is NULL).
+ *   n_labels, capacity  as for pardnn_label_memory. When label_mem is NULL,
+ *                  labels are not checked and only their equality matters;
+ *                  n_labels in [1, 2^16] is then a hint that they lie in
+ *                  [0, n_labels) (fewer bits to pack: faster when it holds,
+ *                  the same results either way), and other values give none.
  *   tl, bl         int64[n_nodes][n_place] outputs, each or both NULL: the
  *                  levels are still computed (they decide everything else)
  *                  but not written out, for callers that keep only the
@@ -436,7 +439,9 @@ int pardnn_get_timing(pardnn_graph *g, const char **kernel, float *ms);
  * still fail at once. pardnn_take_errors waits for the handle's stream,
  * returns E_INVAL if a call made since the last take found such an error
  * (detail: the flags; results of those calls are unspecified) and clears
- * them; PARDNN_OK otherwise. Default: errors are not deferred.
+ * them; PARDNN_OK otherwise. With errors not deferred (the default) every
+ * call reports its own, and pardnn_take_errors only waits for the stream.
+ * Switching the mode clears the flags.
  */
 int pardnn_set_deferred_errors(pardnn_graph *g, int enable);
 int pardnn_take_errors(pardnn_graph *g);

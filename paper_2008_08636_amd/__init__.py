@@ -444,11 +444,12 @@ class Graph:
                        path=True, labels=True, values=True):
         """All outputs for the successive placements base + moves (see
         pardnn_evaluate_moves); arrays are placement-minor [V][P]. values=False
-        leaves out the per-node tl / bl."""
+        leaves out the per-node tl / bl; labels=False the label sums (n_labels
+        is then a hint of the label range)."""
         P = step_ptr.numel() - 1
         out, stride = self._outputs(P, n_labels, crit, path, labels, values)
         pardnn_evaluate_moves(self._h, base, P, step_ptr, node, label,
-                              n_labels if labels else 0, capacity, out.get("tl"), out.get("bl"),
+                              n_labels, capacity, out.get("tl"), out.get("bl"),
                               out["makespan"], out.get("is_critical"), out.get("path"), stride,
                               out.get("path_len"), out.get("label_mem"), out.get("overflow"))
         return out
@@ -542,7 +543,7 @@ class Graph:
         if labels and n_labels > 0:
             out["label_mem"] = torch.empty((P, n_labels), dtype=torch.int64, device=dev)
             out["overflow"] = torch.empty((P, n_labels), dtype=torch.int64, device=dev)
-        pardnn_evaluate_batch(self._h, P, placements, n_labels if labels else 0, capacity,
+        pardnn_evaluate_batch(self._h, P, placements, n_labels, capacity,
                               out["tl"], out["bl"], out["makespan"], out.get("is_critical"),
                               out.get("path"), stride, out.get("path_len"),
                               out.get("label_mem"), out.get("overflow"))

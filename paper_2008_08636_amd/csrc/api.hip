@@ -466,16 +466,21 @@ int evaluate_impl(Graph *g, int32_t n_place, const int32_t *placements, const Mo
     // [0, n_labels) (they are checked) and values leave room for their bits.
     // The b keys then also carry the successor id: (value << ob) | (2^ob - 1 - id)
     // with 2^ob > V, which needs values below 2^(62 - ob) as well.
-    // Without label sums the labels are unchecked: those below 2^16 still fit,
+    // Without label sums the labels are unchecked: those below 2^16 -- or
+    // below n_labels, when the caller gives it as a hint in [1, 2^16], which
+    // leaves fewer label bits and room for the successor links -- still fit,
     // which the label build finds out on the device (bt_fit); then both sweeps
     // are enqueued and the one that does not apply returns at once, so the
     // call needs no host round trip to choose.
     int32_t lb = 0, ob = 0;
     bool gated = false;
+    const int64_t label_range = label_mem != nullptr ? (int64_t)n_labels
+                                : n_labels >= 1 && (uint32_t)n_labels <= kPackLabels
+                                    ? (int64_t)n_labels
+                                    : (int64_t)kPackLabels;
     if (g->V > 0) {
         int32_t bits = 1;
-        while ((1ll << bits) < (label_mem != nullptr ? (int64_t)n_labels : (int64_t)kPackLabels))
-            bits++;
+        while ((1ll << bits) < label_range) bits++;
         const int32_t obits = succ_bits(g->V);
         const int32_t wide = std::max(bits, obits);
         if (bits <= 16 && wide < 62 && g->weight_bound < (1ll << (62 - wide))) {
@@ -503,10 +508,10 @@ int evaluate_impl(Graph *g, int32_t n_place, const int32_t *placements, const Mo
         HIP_TRY(launch_check_steps(mv->step_ptr, n_place, n_moves, g->err, g->stream));
         HIP_TRY(launch_moves_to_slices(*g, mv->base, n_place, mv->step_ptr, n_moves, mv->node,
                                        mv->label, S, moves_scratch, lab_w, lab_stride, K,
-                                       g->err, fit));
+                                       g->err, fit, 1u << lb));
     } else {
         HIP_TRY(launch_permute_labels_batch(*g, placements, n_place, S, lab_w, lab_stride, K,
-                                            g->err, fit));
+                                            g->err, fit, 1u << lb));
     }
     if (K > 0) {
         HIP_TRY(launch_fill_i64(label_mem, (int64_t)n_place * K, 0, g->stream));
@@ -541,9 +546,9 @@ int evaluate_impl(Graph *g, int32_t n_place, const int32_t *placements, const Mo
         a.pretie_b = g->pretie_b;
     }
     // The successor links ride in the packed b values when those have room
-    // for them (not in a gated call: its unpacked alternative writes nx_w,
-    // and the path walk reads one or the other)
-    a.nxf = path != nullptr && lb > 0 && !gated && lb + ob < 62 &&
+    // for them (a gated call's unpacked alternative writes nx_w instead; the
+    // path walk reads the gate to know which)
+    a.nxf = path != nullptr && lb > 0 && lb + ob < 62 &&
                     g->weight_bound < (1ll << (62 - lb - ob))
                 ? 1
                 : 0;
@@ -1422,6 +1427,10 @@ int pardnn_take_errors(pardnn_graph *h) {
     CHECK_HANDLE(h);
     Graph *g = reinterpret_cast<Graph *>(h);
     DEVICE_SCOPE(g);
+    if (!g->defer_errors) {   // every call has reported its own errors already
+        HIP_TRY(hipStreamSynchronize(g->stream));
+        return PARDNN_OK;
+    }
     int32_t flags = 0;
     HIP_TRY(hipMemcpyAsync(&flags, g->err, sizeof(int32_t), hipMemcpyDeviceToHost, g->stream));
     HIP_TRY(hipStreamSynchronize(g->stream));

@@ -244,7 +244,8 @@ __global__ __launch_bounds__(256) void k_moves_to_slices(int32_t V, int32_t P,
                                                          const int32_t *mv_off,
                                                          const int4 *mv_ent, int32_t *lab_w,
                                                          int64_t lab_stride, int32_t K,
-                                                         int32_t *err, int32_t *fit) {
+                                                         int32_t *err, int32_t *fit,
+                                                         uint32_t fit_limit) {
     constexpr int TV = 64, TP = 64, NW = 256 / kWave, RW = TV / NW;
     __shared__ int32_t tile[TV][TP + 1];
     const int lane = lane_id(), w = wave_id();
@@ -314,7 +315,7 @@ __global__ __launch_bounds__(256) void k_moves_to_slices(int32_t V, int32_t P,
                     x.v[s2] = tile[r][sl * S + s2];
                     if (c0 + sl * S + s2 < P) {
                         if (K > 0 && (x.v[s2] < 0 || x.v[s2] >= K)) atomicOr(err, 1);
-                        if (fit != nullptr && (uint32_t)x.v[s2] >= kPackLabels) *fit = 0;
+                        if (fit != nullptr && (uint32_t)x.v[s2] >= fit_limit) *fit = 0;
                     }
                 }
                 // streamed: the sweep reads these long after, and dirty
@@ -357,7 +358,7 @@ hipError_t launch_moves_to_slices(const Graph &g, const int32_t *base, int32_t P
                                   const int64_t *step_ptr, int64_t M, const int32_t *node,
                                   const int32_t *label, int32_t S, int32_t *scratch,
                                   int32_t *lab_w, int64_t lab_stride, int32_t K, int32_t *err,
-                                  int32_t *fit) {
+                                  int32_t *fit, uint32_t fit_limit) {
     if (g.V == 0 || P == 0) return hipSuccess;
     const int32_t V = g.V;
     const size_t m64 = al64((size_t)M);
@@ -389,13 +390,13 @@ hipError_t launch_moves_to_slices(const Graph &g, const int32_t *base, int32_t P
     const unsigned grid = (unsigned)((V + 63) / 64);
     if (S == 1)
         k_moves_to_slices<1><<<grid, 256, 0, g.stream>>>(V, P, g.order, base, off, ent, lab_w,
-                                                         lab_stride, K, err, fit);
+                                                         lab_stride, K, err, fit, fit_limit);
     else if (S == 2)
         k_moves_to_slices<2><<<grid, 256, 0, g.stream>>>(V, P, g.order, base, off, ent, lab_w,
-                                                         lab_stride, K, err, fit);
+                                                         lab_stride, K, err, fit, fit_limit);
     else if (S == 4)
         k_moves_to_slices<4><<<grid, 256, 0, g.stream>>>(V, P, g.order, base, off, ent, lab_w,
-                                                         lab_stride, K, err, fit);
+                                                         lab_stride, K, err, fit, fit_limit);
     else
         return hipErrorInvalidValue;
     return hipGetLastError();

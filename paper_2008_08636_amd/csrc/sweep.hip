@@ -51,7 +51,8 @@ __global__ __launch_bounds__(256) void k_permute_labels(int32_t V, int32_t P,
                                                         const int32_t *order,
                                                         const int32_t *placements,
                                                         int32_t *lab_w, int64_t lab_stride,
-                                                        int32_t K, int32_t *err, int32_t *fit) {
+                                                        int32_t K, int32_t *err, int32_t *fit,
+                                                        uint32_t fit_limit) {
     constexpr int TV = 64, TP = 64;  // tile: 64 nodes x 64 placements
     __shared__ int32_t tile[TV][TP + 1];
     const int32_t n_slices = (P + S - 1) / S;
@@ -64,7 +65,7 @@ __global__ __launch_bounds__(256) void k_permute_labels(int32_t V, int32_t P,
         if (v < V && p < P) {
             x = placements[(int64_t)order[v] * P + p];
             if (K > 0 && (x < 0 || x >= K)) atomicOr(err, 1);
-            if (fit != nullptr && (uint32_t)x >= kPackLabels) *fit = 0;
+            if (fit != nullptr && (uint32_t)x >= fit_limit) *fit = 0;
         }
         tile[r][tx] = x;
     }
@@ -642,9 +643,11 @@ __device__ void chase_wave(const SweepArgs &a, const uint32_t *cbits, int32_t p,
     const int32_t V = a.V;
     const int32_t slice = p / S, s = p % S;
     const int32_t n_words = (V + 31) / 32;
-    // successor links: nx_w, or the low bits of the packed b values
-    const int32_t *nx = a.nxf ? nullptr : a.nx_w + (int64_t)slice * a.ws_stride;
-    const int64_t *bvals = a.nxf ? a.bll + (int64_t)slice * a.ws_stride : nullptr;
+    // successor links: the low bits of the packed b values, or nx_w (always
+    // where the sweep that ran is the gated call's unpacked alternative)
+    const bool folded = a.nxf && (a.gate == nullptr || *a.gate == a.gate_want);
+    const int32_t *nx = folded ? nullptr : a.nx_w + (int64_t)slice * a.ws_stride;
+    const int64_t *bvals = folded ? a.bll + (int64_t)slice * a.ws_stride : nullptr;
     const long long omax = (1ll << a.ob) - 1;
     const uint32_t *bits = cbits + (int64_t)p * n_words;
     // scratch: pos[0, V) and link[V, 2V) in int32 units, in the placement's
@@ -814,15 +817,15 @@ hipError_t launch_permute_labels(const Graph &g, const int32_t *placement, int32
 
 hipError_t launch_permute_labels_batch(const Graph &g, const int32_t *placements, int32_t P,
                                        int32_t S, int32_t *lab_w, int64_t lab_stride, int32_t K,
-                                       int32_t *err, int32_t *fit) {
+                                       int32_t *err, int32_t *fit, uint32_t fit_limit) {
     if (g.V == 0 || P == 0) return hipSuccess;
     dim3 grid((g.V + 63) / 64, (P + 63) / 64);
     if (S == 1)
         k_permute_labels<1><<<grid, 256, 0, g.stream>>>(g.V, P, g.order, placements, lab_w,
-                                                        lab_stride, K, err, fit);
+                                                        lab_stride, K, err, fit, fit_limit);
     else if (S == kBatchSlots)
         k_permute_labels<kBatchSlots><<<grid, 256, 0, g.stream>>>(g.V, P, g.order, placements,
-                                                                  lab_w, lab_stride, K, err, fit);
+                                                                  lab_w, lab_stride, K, err, fit, fit_limit);
     else
         return hipErrorInvalidValue;
     return hipGetLastError();

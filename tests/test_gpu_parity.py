@@ -741,6 +741,7 @@ def test_step_ptr_checks_and_deferred_errors(P):
     with pytest.raises(P.PardnnError) as e:
         G.label_memory(bad_lab, g.n_labels, cap)
     assert e.value.status == P.E_INVAL
+    P.pardnn_take_errors(G.handle)   # not deferred: the call reported it itself
     G.close()
 
 
@@ -889,20 +890,25 @@ def test_tb_levels_batch_labels_beyond_16_bits(P, i, n_place):
     _tb_batch_case(P, g, pl)
 
 
-def test_evaluate_moves_without_label_sums(P):
+@pytest.mark.parametrize("hint", [0, 2])
+def test_evaluate_moves_without_label_sums(P, hint):
     """The moves entry point without label sums takes the same device-side
-    choice; labels outside 16 bits among the moves take the unpacked sweep."""
+    choice: labels outside 16 bits among the moves take the unpacked sweep,
+    and so do labels past the caller's hint n_labels (hint 2 on this
+    two-label graph: 1 label bit, room for the successor links in the b
+    values; a moved label 5 breaks the hint)."""
     g = cfg(1)
-    say("evaluate_moves without label sums")
+    say(f"evaluate_moves without label sums, hint {hint}")
     sched = W.config4_moves(g, n_place=40)
     G = P.Graph(g.n_nodes, g.src, g.dst, g.comp, g.edge_cost, g.mem)
-    for wide in (False, True):
+    for wide in (0, 1 << 20, 5):
         label = sched.label.copy()
         if wide:
-            label[len(label) // 2] = 1 << 20
+            label[len(label) // 2] = wide
         s2 = W.MoveSchedule(sched.base, sched.ptr, sched.node, label, sched.n_labels)
         out = G.evaluate_moves(dev(s2.base, torch.int32), dev(s2.ptr, torch.int64),
-                               dev(s2.node, torch.int32), dev(label, torch.int32), 0)
+                               dev(s2.node, torch.int32), dev(label, torch.int32), hint,
+                               labels=False)
         torch.cuda.synchronize()
         got = {k: v.cpu().numpy() for k, v in out.items()}
         pl = W.materialize_placements(s2).T.copy()
