@@ -491,6 +491,23 @@ def test_batch_large_weights_successor_links(P, shift):
     G.close()
 
 
+def test_batch_wide_resnet(P):
+    """The batched pair sweep on the largest graph (1.05M nodes, 100,270
+    levels, about 90 levels of 9,500 nodes: the general level path and the
+    early folds of wide levels on every chain; its weights leave no room for
+    the successor links in the b values, so they take their own array),
+    element by element against the oracle."""
+    g = cfg(3)
+    say(f"batch config3 V={g.n_nodes} P=3")
+    rng = np.random.default_rng(33)
+    pl = np.stack([g.placement, rng.integers(0, g.n_labels, g.n_nodes),
+                   np.zeros(g.n_nodes)], axis=1).astype(np.int32)
+    G = P.Graph(g.n_nodes, g.src, g.dst, g.comp, g.edge_cost, g.mem)
+    out = run_batch(P, G, pl, g)
+    check_batch(g, pl, out, range(3))
+    G.close()
+
+
 def test_batch_small_graphs(P):
     say("batch on small random DAGs")
     rng = np.random.default_rng(4242)
