@@ -353,6 +353,7 @@ def bench_row(args, row: str) -> int:
                     f"per placement) on the {graph_desc}, {K} partitions, node kinds from the "
                     f"graph (variables residual, their optimiser updates reference nodes)")
         if budget > 0:
+            print("[bench] timing the oracle ...", file=sys.stderr, flush=True)
             from oracle.memory_balance import memory_balance
             n, dt = 0, 0.0
             while n < Pn and dt < budget:
@@ -384,6 +385,7 @@ def bench_row(args, row: str) -> int:
             workload = (f"criticality and order of {C} clusters (the {n_pri} primaries of "
                         f"slicing, every other node on its own) on the {graph_desc}")
             if budget > 0:
+                print("[bench] timing the oracle ...", file=sys.stderr, flush=True)
                 from oracle.clusters import cluster_criticality
                 t0, reps = time.perf_counter(), 0
                 while reps < 1 or time.perf_counter() - t0 < budget:
@@ -425,6 +427,7 @@ def bench_row(args, row: str) -> int:
             if budget > 0:
                 from oracle.span_work import span_work
                 import oracle
+                print("[bench] timing the oracle ...", file=sys.stderr, flush=True)
                 tl_h = oracle.tb_levels(V, g.src, g.dst, g.comp, g.edge_cost, np.arange(V))[0]
                 lab_h = prim_h
                 span_work(V, g.src, g.dst, g.comp, g.edge_cost, lab_h, Kp, cl_h, C, tl_h,
@@ -433,11 +436,16 @@ def bench_row(args, row: str) -> int:
                 span_work(V, g.src, g.dst, g.comp, g.edge_cost, lab_h, Kp, cl_h, C, tl_h,
                           clusters=[])
                 setup = time.perf_counter() - t0
+                # the per-cluster cost from a sample large enough to stand
+                # above the noise of the setup time; the sample size then
+                # follows from the budget, capped so a wrong estimate cannot
+                # run away
+                probe = min(C, 64)
                 t1 = time.perf_counter()
                 span_work(V, g.src, g.dst, g.comp, g.edge_cost, lab_h, Kp, cl_h, C, tl_h,
-                          clusters=range(0, C, max(1, C // 8))[:8])
-                per = (time.perf_counter() - t1 - setup) / 8
-                n = max(8, min(C, int(max(budget - 2 * setup, 1) / max(per, 1e-6))))
+                          clusters=np.linspace(0, C - 1, probe).astype(np.int64))
+                per = max((time.perf_counter() - t1 - setup) / probe, 1e-4)
+                n = max(8, min(C, 1024, int(max(budget - 2 * setup, 1) / per)))
                 rows = np.linspace(0, C - 1, n).astype(np.int64)
                 t0 = time.perf_counter()
                 span_work(V, g.src, g.dst, g.comp, g.edge_cost, lab_h, Kp, cl_h, C, tl_h,
@@ -461,6 +469,7 @@ def bench_row(args, row: str) -> int:
         metric = "graph slicing rounds/sec (Alg. 1 primaries), 1 MI355X"
         workload = f"{Ks} slicing rounds (Alg. 1 primaries) on the {graph_desc}"
         if budget > 0:
+            print("[bench] timing the oracle ...", file=sys.stderr, flush=True)
             from oracle.slicing import slice_primaries
             t0, reps = time.perf_counter(), 0
             while reps < 1 or time.perf_counter() - t0 < budget:
@@ -491,6 +500,7 @@ def bench_row(args, row: str) -> int:
         workload = (f"graph slicing with {Ks} primaries and the secondary walk on stale "
                     f"priorities ({n_clusters} clusters in all) on the {graph_desc}")
         if budget > 0:
+            print("[bench] timing the oracle ...", file=sys.stderr, flush=True)
             from oracle.slicing import slice_all
             t0, reps = time.perf_counter(), 0
             while reps < 1 or time.perf_counter() - t0 < budget:

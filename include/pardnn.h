@@ -424,7 +424,9 @@ int pardnn_tb_levels_batch(pardnn_graph *g, int32_t n_place,
  * pardnn_tb_levels, pardnn_evaluate_batch / pardnn_tb_levels_batch and
  * pardnn_levelize call. pardnn_get_timing waits for the last recorded pair and
  * returns its elapsed time in milliseconds and the kernel's name (a static
- * string). Errors: E_INVAL if nothing was recorded yet.
+ * string). Errors: E_INVAL if nothing was recorded yet. Independently of
+ * this switch, the same spots push roctx ranges named for those kernels, which
+ * a profiler's marker trace shows.
  */
 int pardnn_set_timing(pardnn_graph *g, int enable);
 int pardnn_get_timing(pardnn_graph *g, const char **kernel, float *ms);
