@@ -336,8 +336,9 @@ def test_span_work_hand_example(P):
 
 
 def test_span_work_small_random(P):
-    """Random DAGs, partial placements and clusters; tl either the graph's top
-    levels or arbitrary values with many duplicates (negative ones included)."""
+    """Random DAGs, partial placements and clusters (in some cases with members
+    already placed); tl either the graph's top levels or arbitrary values with
+    many duplicates (negative ones included)."""
     say("eq2 small random")
     rng = np.random.default_rng(801)
     for t in range(24):
@@ -347,8 +348,11 @@ def test_span_work_small_random(P):
         K = int(rng.integers(1, 9))
         C = int(rng.integers(0, n + 4))
         label = np.where(rng.random(n) < 0.5, rng.integers(0, K, n), -1).astype(np.int32)
-        cluster = (np.where(label < 0, rng.integers(-1, C, n), -1) if C else
-                   np.full(n, -1)).astype(np.int32)
+        if C and t % 4 == 1:    # members already placed: edges inside stay free
+            cluster = rng.integers(-1, C, n).astype(np.int32)
+        else:
+            cluster = (np.where(label < 0, rng.integers(-1, C, n), -1) if C else
+                       np.full(n, -1)).astype(np.int32)
         if t % 3 == 2:
             tl = rng.integers(-5, 12, n).astype(np.int64)
         else:

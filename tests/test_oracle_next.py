@@ -531,6 +531,37 @@ def test_eq2_invariants():
     assert set(r1["choice"].tolist()) <= {0, -1}
 
 
+def test_eq2_comm_ignores_the_clusters_own_partitions():
+    """Members of a cluster may already sit on a partition (a placed cluster
+    re-evaluated). An edge inside the cluster carries no communication, so a
+    cluster's comm row cannot depend on where its own members sit, while its
+    work row grows by exactly their weight where their tl lies in the span."""
+    rng = np.random.default_rng(23)
+    for t in range(12):
+        n = int(rng.integers(10, 70))
+        g = W.random_dag(rng, n, p_edge=0.12, max_weight=9, n_labels=1)
+        K = int(rng.integers(2, 5))
+        tl, _, _ = tb_levels(n, g.src, g.dst, g.comp, g.edge_cost, np.arange(n))
+        C = int(rng.integers(1, 6))
+        cluster = rng.integers(-1, C, n)
+        label = np.where(rng.random(n) < 0.5, rng.integers(0, K, n), -1)
+        r1 = span_work(n, g.src, g.dst, g.comp, g.edge_cost, label, K, cluster, C, tl)
+        for c in range(C):
+            free = np.where(cluster == c, -1, label)
+            r0 = span_work(n, g.src, g.dst, g.comp, g.edge_cost, free, K, cluster, C, tl,
+                           clusters=[c])
+            assert (r1["comm"][c] == r0["comm"][0]).all(), (t, c)
+            assert r1["span_lo"][c] == r0["span_lo"][0] and r1["span_hi"][c] == r0["span_hi"][0]
+            inside = (tl >= r0["span_lo"][0]) & (tl <= r0["span_hi"][0]) & (cluster == c)
+            for k in range(K):
+                extra = int(g.comp[inside & (label == k)].sum())
+                assert r1["work"][c, k] == r0["work"][0, k] + extra, (t, c, k)
+        # with every edge inside one cluster there is no communication at all
+        one = np.zeros(n, np.int64)
+        r2 = span_work(n, g.src, g.dst, g.comp, g.edge_cost, label, K, one, 1, tl)
+        assert (r2["comm"] == 0).all()
+
+
 def test_eq2_rejects_bad_ids():
     with pytest.raises(ValueError):
         span_work(2, [0], [1], [1, 1], [1], [0, 2], 2, [-1, 0], 1, [0, 2])
