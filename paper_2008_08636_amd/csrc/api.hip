@@ -307,6 +307,9 @@ int ensure_pair(Graph *g) {
         if (e == hipSuccess) e = dalloc(*g, &fr[d], E - (size_t)n_near);
         if (e == hipSuccess)
             e = launch_pair_split(*g, fwd, rank, pl[d], nr[d], fr[d]);
+        int32_t *&lsrc = fwd ? g->lsrc_t : g->lsrc_b;
+        if (e == hipSuccess) e = dalloc(*g, &lsrc, (size_t)long_list_elems(g->L));
+        if (e == hipSuccess) e = launch_long_blocks(*g, fwd, pl[d], fr[d], lsrc);
         // edges that wide levels fold early
         if (e == hipSuccess) e = hipStreamSynchronize(g->stream);
         if (e == hipSuccess) e = launch_fill_i32(rank, (int64_t)E + 1, 0, g->stream);
@@ -539,6 +542,8 @@ int evaluate_impl(Graph *g, int32_t n_place, const int32_t *placements, const Mo
         a.nr_b = g->nr_b;
         a.fr_t = g->fr_t;
         a.fr_b = g->fr_b;
+        a.lsrc_t = g->lsrc_t;
+        a.lsrc_b = g->lsrc_b;
         a.preoff_t = g->preoff_t;
         a.preoff_b = g->preoff_b;
         a.pre_t = g->pre_t;
@@ -699,6 +704,8 @@ int pair_single_sweep(Graph *g, int32_t lb, int32_t ob, NodeRec16 *node_rec, int
     a.nr_b = g->nr_b;
     a.fr_t = g->fr_t;
     a.fr_b = g->fr_b;
+    a.lsrc_t = g->lsrc_t;
+    a.lsrc_b = g->lsrc_b;
     a.preoff_t = g->preoff_t;
     a.preoff_b = g->preoff_b;
     a.pre_t = g->pre_t;

@@ -86,6 +86,7 @@ struct Graph {
     PairLevel *pl_t = nullptr, *pl_b = nullptr;   // built on first batched evaluation
     NearRec16 *nr_t = nullptr, *nr_b = nullptr;
     FarRec16 *fr_t = nullptr, *fr_b = nullptr;
+    int32_t *lsrc_t = nullptr, *lsrc_b = nullptr;   // long edges' neighbours per block
     int32_t *preoff_t = nullptr, *preoff_b = nullptr;
     PreRec16 *pre_t = nullptr, *pre_b = nullptr;
     int32_t *pretie_b = nullptr;
@@ -209,6 +210,10 @@ hipError_t launch_pair_flags(const Graph &g, bool fwd, int32_t *flag);
 // near_rank = exclusive scan of flag (E + 1 entries); fills pl, nr, fr
 hipError_t launch_pair_split(const Graph &g, bool fwd, const int32_t *near_rank, PairLevel *pl,
                              NearRec16 *nr, FarRec16 *fr);
+// long edges of the pair sweep: fills lsrc (long_list_elems(L)) and points
+// the far records of long edges at their LDS entries
+hipError_t launch_long_blocks(const Graph &g, bool fwd, PairLevel *pl, FarRec16 *fr,
+                              int32_t *lsrc);
 // flag[e] = 1 for the edges a wide level folds early (neighbour-grouped order)
 hipError_t launch_pre_flags(const Graph &g, bool fwd, int32_t *flag);
 // rank = exclusive scan of those flags; fills preoff [L + 1], pre, pretie

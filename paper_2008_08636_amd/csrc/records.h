@@ -26,9 +26,11 @@ struct alignas(16) EdgeRec16 {
 };
 
 // Batched sweeps: per level and direction, the first node and the first
-// near / far edge record (entries L and L + 1 hold the totals).
+// near / far edge record (entries L and L + 1 hold the totals), and how many
+// of the level's far records read the workspace (kNoRing); those come first
+// among the level's far records.
 struct alignas(16) PairLevel {
-    int32_t node_lo, near_lo, far_lo, pad;
+    int32_t node_lo, near_lo, far_lo, n_gather;
 };
 // The cost word of the batched sweeps' edge records: in the t direction the
 // edge cost; in the b direction the cost with the successor tie-break below
@@ -43,18 +45,37 @@ struct alignas(16) NearRec16 {
     int32_t pad;
     int64_t ck;
 };
-// A longer edge: the neighbour (level-major id), the owner's index inside its
-// level and the neighbour's entry in the LDS ring of recent levels
-// (own | ring << 16; kNoRing: read the workspace; kPreFolded: folded by the
-// general path of the neighbour's level, which is too wide for the ring) and
-// the cost word.
+// A longer edge: the cost word, the owner's index inside its level and where
+// the sweep finds the neighbour's value (own | ring << 16), and the neighbour
+// (level-major id). The cost word comes first: a load of the first twelve
+// bytes (the neighbour unused) keeps it in an aligned register pair. `ring` indexes the LDS entries of the chain: below
+// kLongBase the ring of recent levels, from kLongBase on the bulk buffers of
+// long edges (see kLongBlock); kNoRing: gathered from the workspace level by
+// level; kPreFolded: folded by the general path of the neighbour's level,
+// which is too wide for the ring.
 struct alignas(16) FarRec16 {
-    int32_t nb;
-    uint32_t ol;
     int64_t ck;
+    uint32_t ol;
+    int32_t nb;
 };
 constexpr uint32_t kNoRing = 0xffffu;
 constexpr uint32_t kPreFolded = 0xfffeu;
+// Long edges of the batched sweeps. The steps of a chain fall into blocks of
+// kLongBlock; an edge whose neighbour finished at least kLongLead steps before
+// its owner's block begins is long. Per block, the distinct neighbours of its
+// long edges (at most kLongCap, in level-major order) are listed once; the
+// chain gathers them in 64-lane chunks, one chunk per step, into one of two
+// LDS buffers ahead of the block, so that neighbours shared by nearby levels
+// cost one gather and neighbours on one cache line one line. The list holds
+// kLongCap entries per block (0 past its distinct neighbours) and three
+// blocks of padding past the last.
+constexpr int kLongBlock = 8;
+constexpr int kLongCap = 512;
+constexpr int kLongLead = 12;
+constexpr uint32_t kLongBase = 256;   // LDS ring entries before the bulk buffers
+inline int64_t long_list_elems(int32_t L) {
+    return ((int64_t)(L + kLongBlock - 1) / kLongBlock + 3) * kLongCap;
+}
 // An edge folded early by the general path of its neighbour's (wide) level:
 // the neighbour, the owner's index in its level and the span (own | span << 16)
 // and the cost; grouped by the neighbour's level (pre_off).
@@ -114,6 +135,7 @@ struct SweepArgs {
     const PairLevel *pl_t, *pl_b;         // batched sweeps: near / far split per level
     const NearRec16 *nr_t, *nr_b;
     const FarRec16 *fr_t, *fr_b;
+    const int32_t *lsrc_t, *lsrc_b;       // long edges' neighbours per block (long_list_elems)
     const int32_t *preoff_t, *preoff_b;   // [L + 1] per neighbour level
     const PreRec16 *pre_t, *pre_b;
     const int32_t *pretie_b;

@@ -22,6 +22,13 @@
 // loads all run ahead:
 //   near wave: node constants, labels and span-1 edge records LN levels ahead;
 //   far wave:  edge records D + RF levels ahead, neighbour values D ahead.
+// Long edges (the neighbour finished well before the owner's block of
+// kLongBlock levels begins) read their values from LDS too: per block, the
+// far wave gathers the block's distinct long-edge neighbours, sorted by
+// position, one 64-lane chunk per level, into one of two LDS buffers ahead of
+// the block. Neighbours that several nearby levels share then cost one
+// gather, and neighbours on one cache line one line request: the per-level
+// gathers that remain are the few edges of medium span.
 // The register state of the levels in flight rotates by name through an
 // NS-times unrolled loop, and every global load and store of a fast level is
 // unconditional (clamped addresses; idle lanes store into the slice's
@@ -56,6 +63,17 @@ constexpr int kRS = kD + 1;          // LDS ring slots (levels)
 constexpr int kNB = 8;               // accumulator buffers (levels; >= kD + 2, a power of 2)
 static_assert(kNB >= kD + 2 && (kNB & (kNB - 1)) == 0, "accumulator buffers");
 constexpr int kPBinsCap = 2048;      // labels x slots of the LDS label bins
+// long edges: the ring's LDS entries are followed by two bulk buffers of
+// kLongCap entries; a block is one unrolled group of levels
+static_assert(kLongBlock == kNS, "one long-edge block per unrolled group");
+static_assert(kLongCap == kLongBlock * kLanes, "one 64-lane chunk per level of a block");
+static_assert(kLongBase == (uint32_t)(kRS * kPNodes), "bulk buffers follow the ring");
+static_assert(kLongBase + 2 * kLongCap <= kPreFolded, "ring field range");
+// chunk c of block k is listed at step 8k - 14 + c, gathered at 8k - 11 + c
+// and stored to LDS at 8k - 9 + c; the block is read from step 8k - 1 (the
+// far folds of its first level) to 8k + 6. Its neighbours must be final when
+// gathered: finished by step 8k - 12.
+static_assert(kLongLead >= kLongBlock + 4, "long neighbours final when gathered");
 // label sums of the t sweep: none, in LDS bins (K S <= kPBinsCap), or by
 // global atomics; a template parameter, so that a chain carries one of them
 constexpr int kBinsNone = 0, kBinsLds = 1, kBinsGlobal = 2;
@@ -110,7 +128,8 @@ __device__ __forceinline__ int32_t cnt_w(uint32_t c) { return (int32_t)(c & 255u
 __device__ __forceinline__ int32_t cnt_near(uint32_t c) { return (int32_t)((c >> 8) & 255u); }
 __device__ __forceinline__ int32_t cnt_far(uint32_t c) { return (int32_t)((c >> 16) & 255u); }
 // a level of the fast shape: at most 64 nodes, 64 kNEn span-1 and 64 kNEf
-// longer edges (decided when the window entry is staged)
+// longer edges, of which at most 64 read the workspace (decided when the
+// window entry is staged)
 __device__ __forceinline__ bool cnt_fast(uint32_t c) { return (int32_t)c < 0; }
 
 template <int S>
@@ -128,7 +147,7 @@ struct FarSet {    // wave 1, one level
     int32_t nb[kNEf];
     uint32_t ol[kNEf];
     int64_t c[kNEf];
-    VecS<S> f[kNEf];
+    VecS<S> f;         // the workspace value of task 0 (only task 0 reads one)
     uint32_t wcnt;     // the level's counts (its window entry)
 };
 
@@ -137,6 +156,7 @@ constexpr size_t pair_lds_fixed() {
     return (size_t)kWin * sizeof(WinEnt)        // bounds window
            + (size_t)kNB * kPNodes * S * 8       // acc[kNB]
            + (size_t)kRS * kPNodes * S * 8       // ring
+           + (size_t)2 * kLongCap * S * 8        // long-edge buffers (after the ring)
            + (size_t)2 * kPNodes * S * 4;        // slab[2]
 }
 
@@ -189,8 +209,8 @@ struct PairCtx {
         pls = (ConstPairLevel)(FWD ? a->pl_t : a->pl_b);
         win = reinterpret_cast<WinEnt *>(smem);                       // [kWin]
         acc = reinterpret_cast<long long *>(win + kWin);              // [kNB][64 S]
-        ring = reinterpret_cast<VS *>(acc + kNB * kPNodes * S);       // [kRS][64]
-        slab = reinterpret_cast<LS *>(ring + kRS * kPNodes);           // [2][64]
+        ring = reinterpret_cast<VS *>(acc + kNB * kPNodes * S);       // [kRS][64], [2][kLongCap]
+        slab = reinterpret_cast<LS *>(ring + kLongBase + 2 * kLongCap);   // [2][64]
         bins = reinterpret_cast<long long *>(slab + 2 * kPNodes);     // [K S]
     }
     // the tl + comp or bl of a workspace (or ring) value
@@ -365,7 +385,7 @@ __device__ __forceinline__ void pair_chain(const SweepArgs &a, int32_t slice, ch
             const int32_t w = l1.node_lo - l0.node_lo, nn = l1.near_lo - l0.near_lo,
                           nf = l1.far_lo - l0.far_lo;
             const bool fast = w <= kPNodes && nn <= kNEn * kLanes && nf <= kNEf * kLanes &&
-                              sx >= c.gen_end;
+                              l0.n_gather <= kLanes && sx >= c.gen_end;
             e.cnt = (uint32_t)min(w, 255) | (uint32_t)min(nn, 255) << 8 |
                     (uint32_t)min(nf, 255) << 16 | (fast ? 1u << 31 : 0u);
             c.win[sx & (kWin - 1)] = e;
@@ -494,13 +514,11 @@ __device__ __forceinline__ void pair_chain(const SweepArgs &a, int32_t slice, ch
                 X.c[j] = r.ck;
             }
         };
+        // a fast level's records that read the workspace come first, at
+        // most 64 of them: task 0 of each lane
         auto far_loads = [&](FarSet<S> &X, const WinEnt &b) {
-            const int32_t nt = cnt_far(b.cnt);
-#pragma unroll
-            for (int j = 0; j < kNEf; j++) {
-                const bool far = lane + j * kLanes < nt && (X.ol[j] >> 16) == kNoRing;
-                X.f[j] = at(c.vals, far ? (uint32_t)X.nb[j] : 0u);
-            }
+            const bool far = lane < cnt_far(b.cnt) && (X.ol[0] >> 16) == kNoRing;
+            X.f = at(c.vals, far ? (uint32_t)X.nb[0] : 0u);
         };
         auto fold_far = [&](int32_t step, const FarSet<S> &B1, const WinEnt &b1) {
             const int32_t nt = cnt_far(b1.cnt);
@@ -510,13 +528,47 @@ __device__ __forceinline__ void pair_chain(const SweepArgs &a, int32_t slice, ch
             for (int j = 0; j < kNEf; j++) {
                 if (lane + j * kLanes < nt && (B1.ol[j] >> 16) != kPreFolded) {
                     const uint32_t own = B1.ol[j] & 0xffffu, rg = B1.ol[j] >> 16;
-                    const VS g = rg != kNoRing ? c.ring[rg] : B1.f[j];
+                    const VS g = j == 0 && rg == kNoRing ? B1.f : c.ring[rg];
                     const LS ol = sl[own];
 #pragma unroll
                     for (int s = 0; s < S; s++)
                         lds_max_i64(&ab[own * S + s], c.rkey(g.v[s], ol.v[s], B1.c[j]));
                 }
             }
+        };
+        // long edges, step i (position r = i mod kNS): list chunk (r + 6) mod
+        // 8, gather chunk (r + 3) mod 8 (listed three steps ago), store chunk
+        // (r + 1) mod 8 (gathered two steps ago); lst and lval rotate by name
+        const int32_t *lsrc = FWD ? a.lsrc_t : a.lsrc_b;
+        VS *lbuf = c.ring + kLongBase;
+        // (values as plain elements: whole-record copies would stay in
+        // scratch memory)
+        int32_t lst[4];
+        int64_t lval[4][S];
+        auto long_entry = [&](int32_t k, int ch) {
+            return at(lsrc, (uint32_t)(k * kLongCap + ch * kLanes + lane));
+        };
+        auto long_load = [&](int64_t(&d)[S], int32_t v) {
+            const VS &g = at(c.vals, (uint32_t)v);
+#pragma unroll
+            for (int s = 0; s < S; s++) d[s] = g.v[s];
+        };
+        auto long_put = [&](int32_t k, int ch, const int64_t(&x)[S]) {
+            VS &d = lbuf[(k & 1) * kLongCap + ch * kLanes + lane];
+#pragma unroll
+            for (int s = 0; s < S; s++) d.v[s] = x[s];
+        };
+        auto long_list = [&](int32_t i, auto RC) {
+            constexpr int r = decltype(RC)::value, ch = (r + 6) % kLongBlock;
+            lst[r % 4] = long_entry((i + 14 - ch) / kLongBlock, ch);
+        };
+        auto long_gather = [&](auto RC) {
+            constexpr int r = decltype(RC)::value;
+            long_load(lval[r % 4], lst[(r + 1) % 4]);
+        };
+        auto long_store = [&](int32_t i, auto RC) {
+            constexpr int r = decltype(RC)::value, ch = (r + 1) % kLongBlock;
+            long_put((i + 9 - ch) / kLongBlock, ch, lval[(r + 2) % 4]);
         };
         __syncthreads();   // the window is filled by wave 0
         const int32_t s0 = c.s0, s1 = c.s1;
@@ -526,6 +578,32 @@ __device__ __forceinline__ void pair_chain(const SweepArgs &a, int32_t slice, ch
             __syncthreads();
         }
         if (a0 < s1) {
+            // what the long-edge steps before a0 leave behind (a0 is a
+            // multiple of kNS, every neighbour they read is final): block b0
+            // and the first chunk of block b0 + 1 in LDS, the next two chunks
+            // gathered, the three after them listed
+            const int32_t b0 = a0 / kLongBlock;
+            {
+                int32_t l[kLongBlock + 1];
+#pragma unroll
+                for (int ch = 0; ch < kLongBlock; ch++) l[ch] = long_entry(b0, ch);
+                l[kLongBlock] = long_entry(b0 + 1, 0);
+                lst[2] = long_entry(b0 + 1, 1);
+                lst[3] = long_entry(b0 + 1, 2);
+                __builtin_amdgcn_s_waitcnt(0);
+                int64_t v[kLongBlock + 1][S];
+#pragma unroll
+                for (int ch = 0; ch <= kLongBlock; ch++) long_load(v[ch], l[ch]);
+                long_load(lval[2], lst[2]);
+                long_load(lval[3], lst[3]);
+                __builtin_amdgcn_s_waitcnt(0);
+#pragma unroll
+                for (int ch = 0; ch < kLongBlock; ch++) long_put(b0, ch, v[ch]);
+                long_put(b0 + 1, 0, v[kLongBlock]);
+                lst[1] = long_entry(b0 + 1, 3);
+                lst[2] = long_entry(b0 + 1, 4);
+                lst[3] = long_entry(b0 + 1, 5);
+            }
             st[0].wcnt = c.W(a0).cnt;
 #pragma unroll
             for (int j = 1; j <= kD + kRF; j++) records(st[j], c.W(a0 + j));
@@ -554,10 +632,15 @@ __device__ __forceinline__ void pair_chain(const SweepArgs &a, int32_t slice, ch
                 } else {
                     pair_slow<S, FWD, false, BM>(kargs_here(), c.p0 / S, sa, (LdsBytes *)c.win);
                 }
+                // the long-edge loads before the step's other loads: the waits
+                // they need then fall on loads the steps need anyway
+                long_list(sa, RC);
+                long_gather(RC);
                 // far values in flight stay valid across a general-path level:
                 // a far edge either spans more than D + 1 levels or was folded
                 // early by its wide level
                 far_loads(st[(r + 1 + kD) % kNS], bd);
+                long_store(sa, RC);
                 records(st[(r + 1 + kD + kRF) % kNS], brf);
                 __syncthreads();
                 step++;
@@ -719,12 +802,15 @@ __global__ void k_pair_levels(int32_t L, const int32_t *level_ptr, const int32_t
     for (int32_t k = blockIdx.x * blockDim.x + threadIdx.x; k <= L + 1;
          k += gridDim.x * blockDim.x) {
         const int32_t lo = level_ptr[min(k, L)];
-        const int32_t e = off[lo];
+        const int32_t e = off[lo], e1 = off[level_ptr[min(k + 1, L)]];
         PairLevel x;
         x.node_lo = lo;
         x.near_lo = near_rank[e];
         x.far_lo = e - near_rank[e];
-        x.pad = 0;
+        // every far record, until the long-edge pass has put the ones that
+        // read the workspace first and counted them (64 or fewer far records
+        // are all task 0 in any order)
+        x.n_gather = (e1 - near_rank[e1]) - x.far_lo;
         pl[k] = x;
     }
 }
@@ -764,6 +850,114 @@ __global__ void k_pair_records(int64_t E, int32_t L, bool fwd, int32_t ob, const
             r.ck = ck;
             fr[e - near_rank[e]] = r;
         }
+    }
+}
+
+// Long edges, one workgroup per block of kLongBlock steps: the block's far
+// records whose neighbour finished by step kLongBlock * k - kLongLead (levels
+// of the fast shape only: the others read the workspace), sorted by
+// neighbour; distinct neighbours are listed in that order and the records
+// pointed at their entry in the block's LDS buffer. A block with more than
+// kLongCap distinct neighbours keeps the rest on the per-level gathers.
+// Then each level's far records are reordered so that those still reading
+// the workspace come first, and counted.
+constexpr int kLongSort = 2048;   // >= kLongBlock * kNEf * kLanes
+static_assert(kLongSort >= kLongBlock * kNEf * kLanes, "a block's far records fit the sort");
+
+__device__ __forceinline__ bool fast_shape(const PairLevel &l0, const PairLevel &l1) {
+    return l1.node_lo - l0.node_lo <= kPNodes && l1.near_lo - l0.near_lo <= kNEn * kLanes &&
+           l1.far_lo - l0.far_lo <= kNEf * kLanes;
+}
+
+__device__ void long_assign(int32_t L, bool fwd, const PairLevel *pl, const int32_t *level,
+                            const int32_t *order, FarRec16 *fr, int32_t *lsrc, int32_t k,
+                            int32_t last, int32_t *key, int32_t *idx, int32_t *cnt_p) {
+    int32_t &cnt = *cnt_p;
+    if (threadIdx.x == 0) cnt = 0;
+    __syncthreads();
+    for (int32_t sx = k * kLongBlock; sx < min(L, (k + 1) * kLongBlock); sx++) {
+        const int32_t x = fwd ? sx : L - 1 - sx;
+        const PairLevel l0 = pl[x], l1 = pl[x + 1];
+        if (!fast_shape(l0, l1)) continue;
+        for (int32_t e = l0.far_lo + threadIdx.x; e < l1.far_lo; e += blockDim.x) {
+            const FarRec16 r = fr[e];
+            if ((r.ol >> 16) != kNoRing) continue;
+            const int32_t lv = level[order[r.nb]];
+            if ((fwd ? lv : L - 1 - lv) > last) continue;
+            const int32_t p = atomicAdd(&cnt, 1);
+            key[p] = r.nb;
+            idx[p] = e;
+        }
+    }
+    __syncthreads();
+    const int32_t n = cnt;
+    int32_t m = 1;
+    while (m < n) m <<= 1;
+    for (int32_t i = n + threadIdx.x; i < m; i += blockDim.x) {
+        key[i] = INT32_MAX;
+        idx[i] = -1;
+    }
+    __syncthreads();
+    // bitonic sort by neighbour
+    for (int32_t size = 2; size <= m; size <<= 1)
+        for (int32_t stride = size >> 1; stride > 0; stride >>= 1) {
+            for (int32_t i = threadIdx.x; i < m; i += blockDim.x) {
+                const int32_t j = i ^ stride;
+                if (j > i) {
+                    const int32_t ki = key[i], kj = key[j];
+                    if ((ki > kj) == ((i & size) == 0)) {
+                        key[i] = kj;
+                        key[j] = ki;
+                        const int32_t t = idx[i];
+                        idx[i] = idx[j];
+                        idx[j] = t;
+                    }
+                }
+            }
+            __syncthreads();
+        }
+    if (threadIdx.x == 0) {
+        int32_t slot = -1;
+        for (int32_t i = 0; i < n; i++) {
+            if (i == 0 || key[i] != key[i - 1]) {
+                if (++slot == kLongCap) break;
+                lsrc[(int64_t)k * kLongCap + slot] = key[i];
+            }
+            FarRec16 &r = fr[idx[i]];
+            r.ol = (r.ol & 0xffffu) | ((kLongBase + (uint32_t)((k & 1) * kLongCap + slot)) << 16);
+        }
+    }
+}
+
+__global__ __launch_bounds__(256) void k_long_blocks(int32_t L, bool fwd, PairLevel *pl,
+                                                      const int32_t *level, const int32_t *order,
+                                                      FarRec16 *fr, int32_t *lsrc) {
+    __shared__ int32_t key[kLongSort], idx[kLongSort];
+    __shared__ int32_t cnt;
+    __shared__ int wsum[256 / kLanes + 1];
+    const int32_t k = blockIdx.x;
+    const int32_t sx0 = k * kLongBlock, sx1 = min(L, sx0 + kLongBlock);
+    const int32_t last = sx0 - kLongLead;   // latest neighbour step of a long edge
+    if (last >= 0) long_assign(L, fwd, pl, level, order, fr, lsrc, k, last, key, idx, &cnt);
+    __syncthreads();
+    static_assert(kNEf * kLanes <= 256, "one far record per thread");
+    for (int32_t sx = sx0; sx < sx1; sx++) {
+        const int32_t x = fwd ? sx : L - 1 - sx;
+        const PairLevel l0 = pl[x], l1 = pl[x + 1];
+        if (!fast_shape(l0, l1)) continue;
+        const int32_t nf = l1.far_lo - l0.far_lo;
+        FarRec16 r{};
+        int flag = 0;
+        if ((int32_t)threadIdx.x < nf) {
+            r = fr[l0.far_lo + threadIdx.x];
+            flag = (r.ol >> 16) == kNoRing ? 1 : 0;
+        }
+        int total;
+        const int before = block_excl_scan_i32(flag, wsum, &total);   // every read is done
+        if ((int32_t)threadIdx.x < nf)
+            fr[l0.far_lo + (flag ? before : total + (int32_t)threadIdx.x - before)] = r;
+        if (threadIdx.x == 0) pl[x].n_gather = total;
+        __syncthreads();
     }
 }
 
@@ -830,6 +1024,15 @@ hipError_t launch_pre_split(const Graph &g, bool fwd, const int32_t *rank, int32
     k_pre_records<<<grid, 256, 0, g.stream>>>(
         g.E, fwd, succ_bits(g.V), g.level, g.order, g.level_ptr, fwd ? g.out_src : g.in_dst,
         fwd ? g.out_dst : g.in_src, fwd ? g.out_cost : g.in_cost, rank, pre, pretie);
+    return hipGetLastError();
+}
+
+hipError_t launch_long_blocks(const Graph &g, bool fwd, PairLevel *pl, FarRec16 *fr,
+                              int32_t *lsrc) {
+    hipError_t e = launch_fill_i32(lsrc, long_list_elems(g.L), 0, g.stream);
+    const int32_t n_blk = (g.L + kLongBlock - 1) / kLongBlock;
+    if (e != hipSuccess || n_blk == 0 || g.E == 0) return e;
+    k_long_blocks<<<(unsigned)n_blk, 256, 0, g.stream>>>(g.L, fwd, pl, g.level, g.order, fr, lsrc);
     return hipGetLastError();
 }
 
