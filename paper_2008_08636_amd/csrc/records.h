@@ -38,12 +38,13 @@ struct alignas(16) PairLevel {
 // is (value << ob) plus this word (labels differ) or its low ob bits (same
 // label). It fits whenever the packed keys are used: their condition bounds
 // every cost by 2^(62 - ob).
-// A span-1 edge: owner's and neighbour's index inside their levels
-// (own | nb << 16) and the cost word.
+// A span-1 edge: the cost word and the owner's and neighbour's index inside
+// their levels (own | nb << 16); the pad last, so that a load of the used
+// twelve bytes is one instruction.
 struct alignas(16) NearRec16 {
+    int64_t ck;
     uint32_t ol;
     int32_t pad;
-    int64_t ck;
 };
 // A longer edge: the cost word, the owner's index inside its level and where
 // the sweep finds the neighbour's value (own | ring << 16), and the neighbour

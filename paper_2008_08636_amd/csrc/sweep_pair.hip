@@ -238,7 +238,7 @@ struct PairCtx {
     // accumulators: value, successor, ring entry, label sums, workspace
     __device__ __forceinline__ void finish(int64_t *label_mem, int32_t step, int32_t v, bool act,
                                            bool to_ring, int slot, int64_t comp, int64_t mem,
-                                           const LS &lab) const {
+                                           const LS &lab, bool side = true) const {
         long long *ab = accb(step);
         VS out;
         LS nxv;
@@ -251,10 +251,20 @@ struct PairCtx {
             out.v[s] = EL::make(x, lab.v[s], lb);
             nxv.v[s] = k == 0 ? -1 : (int32_t)(omax - (k & omax));
         }
+        if (act && to_ring) ring[((uint32_t)step % kRS) * kPNodes + slot] = out;
+        const uint32_t sv = act ? (uint32_t)v : (uint32_t)V;   // idle lanes: one padding slot
+        at(vals, sv) = out;
+        if (want_nx) at(nxs, sv) = nxv;
+        if (side) finish_side(label_mem, step, act, slot, mem, lab);
+    }
+    // the parts of finishing a node that nothing reads soon: clearing its
+    // accumulator slot and its label sums
+    __device__ __forceinline__ void finish_side(int64_t *label_mem, int32_t step, bool act, int slot,
+                                                int64_t mem, const LS &lab) const {
+        long long *ab = accb(step);
 #pragma unroll
         for (int s = 0; s < S; s++) ab[slot * S + s] = 0;
         if (act) {
-            if (to_ring) ring[((uint32_t)step % kRS) * kPNodes + slot] = out;
             if constexpr (want_bins) {
 #pragma unroll
                 for (int s = 0; s < S; s++) {
@@ -269,9 +279,6 @@ struct PairCtx {
                 }
             }
         }
-        const uint32_t sv = act ? (uint32_t)v : (uint32_t)V;   // idle lanes: one padding slot
-        at(vals, sv) = out;
-        if (want_nx) at(nxs, sv) = nxv;
     }
 };
 
@@ -426,7 +433,7 @@ __device__ __forceinline__ void pair_chain(const SweepArgs &a, int32_t slice, ch
         auto body = [&](int32_t step, const WinEnt &b0, const WinEnt &b1, NearSet<S> &A,
                         const NearSet<S> &B1) {
             c.finish(a.label_mem, step, b0.nlo + lane, lane < cnt_w(b0.cnt), true, lane, A.comp, A.mem,
-                     A.lab);
+                     A.lab, false);
             // span-1 edges of the next level, from the ring slot just written
             if (cnt_fast(b1.cnt)) {
                 const int32_t nt = cnt_near(b1.cnt);
@@ -445,6 +452,9 @@ __device__ __forceinline__ void pair_chain(const SweepArgs &a, int32_t slice, ch
                     }
                 }
             }
+            // after the folds, so that the LDS (in order) serves the folds'
+            // reads first
+            c.finish_side(a.label_mem, step, lane < cnt_w(b0.cnt), lane, A.mem, A.lab);
         };
         const int32_t s0 = c.s0, s1 = c.s1;
         const int32_t a0 = pipe_start(c);
@@ -480,11 +490,13 @@ __device__ __forceinline__ void pair_chain(const SweepArgs &a, int32_t slice, ch
                 const WinEnt b0 = {st[r].wnlo, 0, 0, st[r].wcnt};
                 const WinEnt b1 = {0, 0, 0, st[(r + 1) % kNS].wcnt};
                 const WinEnt b2 = {0, 0, 0, st[(r + 2) % kNS].wcnt};
-                const WinEnt bl = c.W(sa + kLN);
                 if (cnt_fast(b0.cnt))
                     body(sa, b0, b1, st[r], st[(r + 1) % kNS]);
                 else
                     pair_slow<S, FWD, true, BM>(kargs_here(), c.p0 / S, sa, (LdsBytes *)c.win);
+                // the window entry of the level loaded now: read after the
+                // level's own LDS work, which it would otherwise delay
+                const WinEnt bl = c.W(sa + kLN);
                 tail(sa, st[(r + 2) % kNS], st[(r + kLN) % kNS], b2, bl);
                 step++;
             }
