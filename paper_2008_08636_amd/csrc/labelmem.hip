@@ -264,6 +264,12 @@ __global__ __launch_bounds__(256) void k_moves_to_slices(int32_t V, int32_t P,
 #pragma unroll
     for (int j = 0; j < RW; j++)
         ent[j] = lane < cnt[j] ? mv_ent[lo[j] + lane] : make_int4(-1, -1, 0, 0);
+    // the largest label (as unsigned: a negative one counts as huge) over
+    // this lane's columns, checked against K and fit_limit once at the end
+    // instead of at every store. Columns past the last placement repeat its
+    // labels (every move applies there) and rows past the last node hold 0,
+    // so neither needs a mask.
+    uint32_t umax = 0;
     // fold move x (uniform) into lane's value if it applies at lane's placement
     auto apply = [&](int32_t c0, int32_t st, int32_t m, int32_t lab, int32_t &best,
                      int32_t &val) {
@@ -301,33 +307,40 @@ __global__ __launch_bounds__(256) void k_moves_to_slices(int32_t V, int32_t P,
             }
             tile[w + j * NW][lane] = val;
             carry[j] = __builtin_amdgcn_readlane(val, kWave - 1);
+            umax = max(umax, (uint32_t)val);
         }
         __syncthreads();
         const int32_t sl0 = c0 / S;
         const int n_sl = min(TP / S, n_slices - sl0);
-        for (int i = threadIdx.x; i < n_sl * TV; i += 256) {
-            const int sl = i / TV, r = i % TV;
+        // streamed: the sweep reads these long after, and dirty lines left in
+        // L2 would be written back during the sweep. Two adjacent nodes of
+        // one slice per thread (one 16-byte store for two slots per slice).
+        constexpr int NP = S == 2 ? 2 : 1;
+        using W = typename LabPack<S * NP>::Word;
+        for (int i = threadIdx.x; i < n_sl * (TV / NP); i += 256) {
+            const int sl = i / (TV / NP), r = NP * (i % (TV / NP));
             const int32_t v = v0 + r;
-            if (v < V) {
+            if (v >= V) continue;
+            int32_t *dst = lab_w + (int64_t)(sl0 + sl) * lab_stride + (int64_t)v * S;
+            if (NP == 1 || v + 1 < V) {
+                LabPack<S * NP> x;
+#pragma unroll
+                for (int q = 0; q < S * NP; q++) x.v[q] = tile[r + q / S][sl * S + q % S];
+                __builtin_nontemporal_store(*reinterpret_cast<const W *>(&x),
+                                            reinterpret_cast<W *>(dst));
+            } else {   // the graph's last node alone
                 LabPack<S> x;
 #pragma unroll
-                for (int s2 = 0; s2 < S; s2++) {
-                    x.v[s2] = tile[r][sl * S + s2];
-                    if (c0 + sl * S + s2 < P) {
-                        if (K > 0 && (x.v[s2] < 0 || x.v[s2] >= K)) atomicOr(err, 1);
-                        if (fit != nullptr && (uint32_t)x.v[s2] >= fit_limit) *fit = 0;
-                    }
-                }
-                // streamed: the sweep reads these long after, and dirty
-                // lines left in L2 would be written back during the sweep
-                using W = typename LabPack<S>::Word;
-                __builtin_nontemporal_store(
-                    *reinterpret_cast<const W *>(&x),
-                    reinterpret_cast<W *>(lab_w + (int64_t)(sl0 + sl) * lab_stride + (int64_t)v * S));
+                for (int q = 0; q < S; q++) x.v[q] = tile[r][sl * S + q];
+                using W1 = typename LabPack<S>::Word;
+                __builtin_nontemporal_store(*reinterpret_cast<const W1 *>(&x),
+                                            reinterpret_cast<W1 *>(dst));
             }
         }
         __syncthreads();
     }
+    if (K > 0 && umax >= (uint32_t)K) atomicOr(err, 1);
+    if (fit != nullptr && umax >= fit_limit) *fit = 0;
 }
 
 }  // namespace
