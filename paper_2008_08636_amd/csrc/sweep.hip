@@ -619,6 +619,121 @@ __device__ void emit_rows(const SweepArgs &a, uint8_t *crit, uint32_t *cbits, in
     }
 }
 
+// The same outputs for the batched pair sweep (two slots per slice, packed
+// values), 16 bytes per lane: a thread reads both slots of one node of a
+// slice, and writes two adjacent placements of one output row (and their two
+// flag bytes), so that every request carries twice the bytes of the general
+// version. With an odd number of placements the rows are not 16-byte
+// aligned, and the stores fall back to 8-byte (and single-byte) ones.
+template <int TV, int TP>
+__device__ void emit_rows_pair(const SweepArgs &a, uint8_t *crit, uint32_t *cbits, int32_t bx,
+                               char *smem) {
+    using EL = Elem<true>;
+    using BW = typename std::conditional<TV == 64, unsigned long long, uint32_t>::type;
+    typedef long long v2i64 __attribute__((ext_vector_type(2)));
+    constexpr int S = 2, NT = 256, NW = NT / kWave;
+    constexpr int PER = TV * TP / S / NT;   // 16-byte loads per thread and array
+    constexpr int RPW = TV / NW;            // output rows per wave
+    static_assert(TP == 2 * kWave, "a lane writes two placements of a row");
+    static_assert(TV == 32 || TV == 64, "one or two bit words per placement");
+    long long(*t_tl)[TP + 1] = reinterpret_cast<long long(*)[TP + 1]>(smem);
+    long long(*t_bl)[TP + 1] = reinterpret_cast<long long(*)[TP + 1]>(smem + TV * (TP + 1) * 8);
+    int32_t *s_ord = reinterpret_cast<int32_t *>(smem + 2 * TV * (TP + 1) * 8);
+    long long *s_comp = reinterpret_cast<long long *>(s_ord + TV);
+    BW *s_bits = reinterpret_cast<BW *>(s_comp + TV);   // [TP]
+    const int tid = threadIdx.x, lane = lane_id(), w = wave_id();
+    const int32_t V = a.V, P = a.P;
+    const int32_t v0 = bx * TV;
+    const int32_t n_words = (V + 31) / 32;
+    const int32_t n_slices = (P + S - 1) / S;
+    const int32_t n_chunks = (P + TP - 1) / TP;
+    const bool even = (P & 1) == 0;
+    const int bfo = a.nxf ? a.ob : 0;   // successor links below the label bits
+    if (tid < TV) {
+        const int32_t v = min(v0 + tid, V - 1);
+        s_ord[tid] = a.order[v];
+        s_comp[tid] = a.comp_lm[v];
+    }
+    if (tid < TP) s_bits[tid] = 0;
+    // load j of a chunk: slice (tid + j NT) / TV, node (tid + j NT) % TV
+    v2i64 fv[PER], bv[PER];
+    auto load = [&](int32_t ch) {
+        const int32_t sl0 = ch * (TP / S);
+#pragma unroll
+        for (int j = 0; j < PER; j++) {
+            const int i = tid + j * NT;
+            const int64_t idx = (int64_t)min(sl0 + i / TV, n_slices - 1) * a.ws_stride +
+                                (int64_t)min(v0 + i % TV, V - 1) * S;
+            fv[j] = __builtin_nontemporal_load(reinterpret_cast<const v2i64 *>(a.ftl + idx));
+            bv[j] = __builtin_nontemporal_load(reinterpret_cast<const v2i64 *>(a.bll + idx));
+        }
+    };
+    load(0);
+    for (int32_t ch = 0; ch < n_chunks; ch++) {
+        __syncthreads();   // the tiles are free (and s_ord, s_comp, s_bits are set)
+#pragma unroll
+        for (int j = 0; j < PER; j++) {
+            const int i = tid + j * NT, sl = i / TV, r = i % TV;
+            t_tl[r][sl * S] = EL::val(fv[j].x, a.lb) - s_comp[r];
+            t_tl[r][sl * S + 1] = EL::val(fv[j].y, a.lb) - s_comp[r];
+            t_bl[r][sl * S] = EL::val(bv[j].x, a.lb) >> bfo;
+            t_bl[r][sl * S + 1] = EL::val(bv[j].y, a.lb) >> bfo;
+        }
+        if (ch + 1 < n_chunks) load(ch + 1);
+        const int32_t p = ch * TP + 2 * lane;   // this lane's two placement columns
+        const int64_t m0 = a.makespan[min(p, P - 1)], m1 = a.makespan[min(p + 1, P - 1)];
+        __syncthreads();
+        BW bits0 = 0, bits1 = 0;
+        if (p < P) {
+#pragma unroll
+            for (int k = 0; k < RPW; k++) {
+                const int r = w + k * NW;
+                if (v0 + r >= V) continue;
+                const int64_t o = (int64_t)s_ord[r] * P + p;
+                const long long t0 = t_tl[r][2 * lane], t1 = t_tl[r][2 * lane + 1];
+                const long long b0 = t_bl[r][2 * lane], b1 = t_bl[r][2 * lane + 1];
+                const bool c0 = t0 + b0 == m0, c1 = t1 + b1 == m1;
+                bits0 |= (BW)c0 << r;
+                bits1 |= (BW)c1 << r;
+                if (even && p + 1 < P) {
+                    // written once and streamed past the caches; the flag
+                    // pairs stay ordinary stores so that partial lines merge
+                    if (a.tl_out) __builtin_nontemporal_store(v2i64{t0, t1}, reinterpret_cast<v2i64 *>(a.tl_out + o));
+                    if (a.bl_out) __builtin_nontemporal_store(v2i64{b0, b1}, reinterpret_cast<v2i64 *>(a.bl_out + o));
+                    if (crit)
+                        *reinterpret_cast<uint16_t *>(crit + o) = (uint16_t)((uint16_t)c0 | ((uint16_t)c1 << 8));
+                } else {
+                    if (a.tl_out) __builtin_nontemporal_store(t0, &a.tl_out[o]);
+                    if (a.bl_out) __builtin_nontemporal_store(b0, &a.bl_out[o]);
+                    if (crit) crit[o] = (uint8_t)c0;
+                    if (p + 1 < P) {
+                        if (a.tl_out) __builtin_nontemporal_store(t1, &a.tl_out[o + 1]);
+                        if (a.bl_out) __builtin_nontemporal_store(b1, &a.bl_out[o + 1]);
+                        if (crit) crit[o + 1] = (uint8_t)c1;
+                    }
+                }
+            }
+        }
+        if (cbits != nullptr) {
+            __hip_atomic_fetch_or(&s_bits[2 * lane], bits0, __ATOMIC_RELAXED,
+                                  __HIP_MEMORY_SCOPE_WORKGROUP);
+            __hip_atomic_fetch_or(&s_bits[2 * lane + 1], bits1, __ATOMIC_RELAXED,
+                                  __HIP_MEMORY_SCOPE_WORKGROUP);
+            __syncthreads();
+            if (tid < TP) {
+                const int32_t q = ch * TP + tid;
+                if (q < P) {
+                    const BW x = s_bits[tid];
+                    uint32_t *row = cbits + (int64_t)q * n_words + bx * (TV / 32);
+                    row[0] = (uint32_t)x;
+                    if (TV == 64 && bx * 2 + 1 < n_words) row[1] = (uint32_t)((uint64_t)x >> 32);
+                }
+                s_bits[tid] = 0;
+            }
+        }
+    }
+}
+
 // One wave per placement extracts its canonical critical path. Every path
 // node is critical, so the wave (1) lists the placement's critical nodes in
 // level-major order from the bit words the emit pass wrote, and (2) maps the
@@ -800,8 +915,11 @@ template <int S, bool PACKED>
 __global__ __launch_bounds__(256) void k_emit(SweepArgs a, uint8_t *crit, uint32_t *cbits) {
     __shared__ __align__(16) char smem[emit_lds<kEmitNodes, kEmitCols>()];
     if (a.gate != nullptr && *a.gate != a.gate_want) return;
-    emit_rows<S, PACKED, kEmitNodes, kEmitCols>(a, crit, cbits, xcd_major(blockIdx.x, gridDim.x),
-                                                smem);
+    if constexpr (S == 2 && PACKED)
+        emit_rows_pair<kEmitNodes, kEmitCols>(a, crit, cbits, xcd_major(blockIdx.x, gridDim.x), smem);
+    else
+        emit_rows<S, PACKED, kEmitNodes, kEmitCols>(a, crit, cbits,
+                                                    xcd_major(blockIdx.x, gridDim.x), smem);
 }
 
 constexpr int kSingleThreads = 512;

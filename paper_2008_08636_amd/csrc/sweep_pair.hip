@@ -161,8 +161,10 @@ constexpr size_t pair_lds_fixed() {
 }
 
 // Everything a chain derives from the arguments: the slice's workspace, the
-// LDS layout and the value encoding.
-template <int S, bool FWD, int BM>
+// LDS layout and the value encoding. NXF (b only): the successor links ride
+// in the b values, a property of the launch fixed at compile time so that
+// the b chain carries no arithmetic of the other encoding.
+template <int S, bool FWD, int BM, bool NXF>
 struct PairCtx {
     static constexpr bool want_bins = FWD && BM != kBinsNone;
     static constexpr bool lds_bins = FWD && BM == kBinsLds;
@@ -200,11 +202,11 @@ struct PairCtx {
         p0 = slice * S;
         lb = a->lb;
         ob = FWD ? 0 : a->ob;
-        fo = !FWD && a->nxf ? ob : 0;
+        fo = !FWD && NXF ? ob : 0;
         omax = (1ll << ob) - 1;
         vals = reinterpret_cast<VS *>((FWD ? a->ftl : a->bll) + (int64_t)slice * a->ws_stride);
         labs = reinterpret_cast<const LS *>(a->lab_w + (int64_t)slice * a->lab_stride);
-        want_nx = !FWD && a->nx_w != nullptr && !a->nxf;
+        want_nx = !FWD && !NXF && a->nx_w != nullptr;
         nxs = reinterpret_cast<LS *>(a->nx_w + (want_nx ? (int64_t)slice * a->ws_stride : 0));
         pls = (ConstPairLevel)(FWD ? a->pl_t : a->pl_b);
         win = reinterpret_cast<WinEnt *>(smem);                       // [kWin]
@@ -214,7 +216,12 @@ struct PairCtx {
         bins = reinterpret_cast<long long *>(slab + 2 * kPNodes);     // [K S]
     }
     // the tl + comp or bl of a workspace (or ring) value
-    __device__ __forceinline__ int64_t gval(int64_t g) const { return EL::val(g, lb) >> fo; }
+    __device__ __forceinline__ int64_t gval(int64_t g) const {
+        if constexpr (!FWD && NXF)
+            return EL::val(g, lb) >> ob;
+        else
+            return EL::val(g, lb);
+    }
     __device__ __forceinline__ int64_t cand(int64_t g, int32_t own_lab, int64_t c) const {
         return gval(g) + (EL::lab(g, lb) != own_lab ? c : 0);
     }
@@ -223,7 +230,13 @@ struct PairCtx {
     }
     // the key of an edge record's candidate from its cost word ck (t: ob = 0)
     __device__ __forceinline__ long long rkey(int64_t g, int32_t own_lab, int64_t ck) const {
-        return (gval(g) << ob) + (EL::lab(g, lb) != own_lab ? ck : (ck & omax));
+        const bool cross = EL::lab(g, lb) != own_lab;
+        if constexpr (FWD)
+            return gval(g) + (cross ? ck : 0);
+        else if constexpr (NXF)   // the value's key bits sit above its link bits already
+            return ((g >> lb) & ~omax) + (cross ? ck : (ck & omax));
+        else
+            return ((g >> lb) << ob) + (cross ? ck : (ck & omax));
     }
     __device__ __forceinline__ int32_t level_of(int32_t step) const {   // L: empty level
         if (FWD) return step < L ? step : L;
@@ -241,20 +254,26 @@ struct PairCtx {
                                            const LS &lab, bool side = true) const {
         long long *ab = accb(step);
         VS out;
-        LS nxv;
+        long long kk[S];
 #pragma unroll
         for (int s = 0; s < S; s++) {
             const long long k = ab[slot * S + s];
+            kk[s] = k;
             // b, folded: (comp << ob) + k = ((comp + max) << ob) | successor's tie
             // key, with k = 0 (no successor) leaving the link bits 0
-            const int64_t x = FWD ? k + comp : fo != 0 ? (comp << ob) + k : comp + (k >> ob);
+            const int64_t x = FWD ? k + comp : NXF ? (comp << ob) + k : comp + (k >> ob);
             out.v[s] = EL::make(x, lab.v[s], lb);
-            nxv.v[s] = k == 0 ? -1 : (int32_t)(omax - (k & omax));
         }
         if (act && to_ring) ring[((uint32_t)step % kRS) * kPNodes + slot] = out;
         const uint32_t sv = act ? (uint32_t)v : (uint32_t)V;   // idle lanes: one padding slot
         at(vals, sv) = out;
-        if (want_nx) at(nxs, sv) = nxv;
+        if (want_nx) {
+            LS nxv;
+#pragma unroll
+            for (int s = 0; s < S; s++)
+                nxv.v[s] = kk[s] == 0 ? -1 : (int32_t)(omax - (kk[s] & omax));
+            at(nxs, sv) = nxv;
+        }
         if (side) finish_side(label_mem, step, act, slot, mem, lab);
     }
     // the parts of finishing a node that nothing reads soon: clearing its
@@ -301,11 +320,11 @@ __device__ __forceinline__ int32_t pipe_start(const Ctx &c) {
 // real call, not inlined: the unrolled loop would otherwise hold eight copies
 // of it per chain, and the smaller loop body takes instruction-cache misses
 // off every fast level.
-template <int S, bool FWD, bool NEAR, int BM>
+template <int S, bool FWD, bool NEAR, int BM, bool NXF>
 __device__ __attribute__((noinline)) void pair_slow(KArgs *a, int32_t slice, int32_t step,
                                                     LdsBytes *smem_l) {
     char *smem = (char *)smem_l;
-    const PairCtx<S, FWD, BM> c(a, slice, smem);
+    const PairCtx<S, FWD, BM, NXF> c(a, slice, smem);
     using VS = VecS<S>;
     using LS = LabS<S>;
     __builtin_amdgcn_s_waitcnt(0);
@@ -368,12 +387,12 @@ __device__ __attribute__((noinline)) void pair_slow(KArgs *a, int32_t slice, int
     }
 }
 
-template <int S, bool FWD, bool NEAR, int BM>
+template <int S, bool FWD, bool NEAR, int BM, bool NXF>
 __device__ __forceinline__ void pair_chain(const SweepArgs &a, int32_t slice, char *smem) {
     using EL = Elem<true>;
     using VS = VecS<S>;
     using LS = LabS<S>;
-    const PairCtx<S, FWD, BM> c(&a, slice, smem);
+    const PairCtx<S, FWD, BM, NXF> c(&a, slice, smem);
     const int lane = c.lane;
     const int32_t L = c.L;
     const uint32_t vmax = c.V > 0 ? (uint32_t)(c.V - 1) : 0u;
@@ -468,7 +487,7 @@ __device__ __forceinline__ void pair_chain(const SweepArgs &a, int32_t slice, ch
         __syncthreads();
         // a segment's first levels, on the general path
         for (int32_t sx = s0; sx < a0; sx++) {
-            pair_slow<S, FWD, true, BM>(kargs_here(), c.p0 / S, sx, (LdsBytes *)c.win);
+            pair_slow<S, FWD, true, BM, NXF>(kargs_here(), c.p0 / S, sx, (LdsBytes *)c.win);
             __syncthreads();
         }
         if (a0 < s1) {
@@ -493,7 +512,7 @@ __device__ __forceinline__ void pair_chain(const SweepArgs &a, int32_t slice, ch
                 if (cnt_fast(b0.cnt))
                     body(sa, b0, b1, st[r], st[(r + 1) % kNS]);
                 else
-                    pair_slow<S, FWD, true, BM>(kargs_here(), c.p0 / S, sa, (LdsBytes *)c.win);
+                    pair_slow<S, FWD, true, BM, NXF>(kargs_here(), c.p0 / S, sa, (LdsBytes *)c.win);
                 // the window entry of the level loaded now: read after the
                 // level's own LDS work, which it would otherwise delay
                 const WinEnt bl = c.W(sa + kLN);
@@ -507,7 +526,7 @@ __device__ __forceinline__ void pair_chain(const SweepArgs &a, int32_t slice, ch
         // the last levels (fewer than kNS) on the general path; folding an
         // edge a second time into a maximum changes nothing
         for (; step < s1; step++) {
-            pair_slow<S, FWD, true, BM>(kargs_here(), c.p0 / S, step, (LdsBytes *)c.win);
+            pair_slow<S, FWD, true, BM, NXF>(kargs_here(), c.p0 / S, step, (LdsBytes *)c.win);
             __syncthreads();
         }
     } else {
@@ -586,7 +605,7 @@ __device__ __forceinline__ void pair_chain(const SweepArgs &a, int32_t slice, ch
         const int32_t s0 = c.s0, s1 = c.s1;
         const int32_t a0 = pipe_start(c);
         for (int32_t sx = s0; sx < a0; sx++) {
-            pair_slow<S, FWD, false, BM>(kargs_here(), c.p0 / S, sx, (LdsBytes *)c.win);
+            pair_slow<S, FWD, false, BM, NXF>(kargs_here(), c.p0 / S, sx, (LdsBytes *)c.win);
             __syncthreads();
         }
         if (a0 < s1) {
@@ -642,7 +661,7 @@ __device__ __forceinline__ void pair_chain(const SweepArgs &a, int32_t slice, ch
                 if (cnt_fast(b0.cnt)) {
                     if (cnt_fast(b1.cnt)) fold_far(sa, B1, b1);
                 } else {
-                    pair_slow<S, FWD, false, BM>(kargs_here(), c.p0 / S, sa, (LdsBytes *)c.win);
+                    pair_slow<S, FWD, false, BM, NXF>(kargs_here(), c.p0 / S, sa, (LdsBytes *)c.win);
                 }
                 // the long-edge loads before the step's other loads: the waits
                 // they need then fall on loads the steps need anyway
@@ -660,7 +679,7 @@ __device__ __forceinline__ void pair_chain(const SweepArgs &a, int32_t slice, ch
         };
         while (step + kNS <= s1) unroll_seq(one, std::make_integer_sequence<int, kNS>{});
         for (; step < s1; step++) {
-            pair_slow<S, FWD, false, BM>(kargs_here(), c.p0 / S, step, (LdsBytes *)c.win);
+            pair_slow<S, FWD, false, BM, NXF>(kargs_here(), c.p0 / S, step, (LdsBytes *)c.win);
             __syncthreads();
         }
     }
@@ -701,7 +720,7 @@ __device__ __forceinline__ void pair_chain(const SweepArgs &a, int32_t slice, ch
     (void)vmax;
 }
 
-template <int S, int BM>
+template <int S, int BM, bool NXF>
 __global__ __launch_bounds__(2 * kLanes) void k_sweep_pair(SweepArgs a) {
     extern __shared__ __align__(16) char smem[];
     if (a.gate != nullptr && *a.gate != a.gate_want) return;
@@ -710,14 +729,14 @@ __global__ __launch_bounds__(2 * kLanes) void k_sweep_pair(SweepArgs a) {
     const int32_t slice = fwd ? blockIdx.x - n_slices : blockIdx.x;
     if (wave_id() == 0) {
         if (fwd)
-            pair_chain<S, true, true, BM>(a, slice, smem);
+            pair_chain<S, true, true, BM, false>(a, slice, smem);
         else
-            pair_chain<S, false, true, kBinsNone>(a, slice, smem);
+            pair_chain<S, false, true, kBinsNone, NXF>(a, slice, smem);
     } else {
         if (fwd)
-            pair_chain<S, true, false, BM>(a, slice, smem);
+            pair_chain<S, true, false, BM, false>(a, slice, smem);
         else
-            pair_chain<S, false, false, kBinsNone>(a, slice, smem);
+            pair_chain<S, false, false, kBinsNone, NXF>(a, slice, smem);
     }
 }
 
@@ -1078,12 +1097,24 @@ hipError_t launch_pair(const SweepArgs &a, hipStream_t s) {
     if (a.lb <= 0) return hipErrorInvalidValue;
     const size_t bins = a.K > 0 && a.K * S <= kPBinsCap ? (size_t)a.K * S * 8 : 0;
     const size_t lds = pair_lds_fixed<S>() + bins;
-    if (a.K <= 0)
-        k_sweep_pair<S, kBinsNone><<<2 * n_slices, 2 * kLanes, lds, s>>>(a);
-    else if (bins > 0)
-        k_sweep_pair<S, kBinsLds><<<2 * n_slices, 2 * kLanes, lds, s>>>(a);
-    else
-        k_sweep_pair<S, kBinsGlobal><<<2 * n_slices, 2 * kLanes, lds, s>>>(a);
+    if (a.nxf) {   // links folded into the b values: batches only
+        if constexpr (S == kBatchSlots) {
+            if (a.K <= 0)
+                k_sweep_pair<S, kBinsNone, true><<<2 * n_slices, 2 * kLanes, lds, s>>>(a);
+            else if (bins > 0)
+                k_sweep_pair<S, kBinsLds, true><<<2 * n_slices, 2 * kLanes, lds, s>>>(a);
+            else
+                k_sweep_pair<S, kBinsGlobal, true><<<2 * n_slices, 2 * kLanes, lds, s>>>(a);
+        } else {
+            return hipErrorInvalidValue;
+        }
+    } else if (a.K <= 0) {
+        k_sweep_pair<S, kBinsNone, false><<<2 * n_slices, 2 * kLanes, lds, s>>>(a);
+    } else if (bins > 0) {
+        k_sweep_pair<S, kBinsLds, false><<<2 * n_slices, 2 * kLanes, lds, s>>>(a);
+    } else {
+        k_sweep_pair<S, kBinsGlobal, false><<<2 * n_slices, 2 * kLanes, lds, s>>>(a);
+    }
     return hipGetLastError();
 }
 
