@@ -466,6 +466,70 @@ def test_batch_random_placements(P, i, n_place):
     G.close()
 
 
+def _long_edge_coverage(g):
+    """How a graph exercises the batch sweep's long-edge machinery, from its
+    shape alone (blocks of 8 steps; an edge is long when its neighbour's step
+    is at most 8 k - 12 for the owner's block k; at most 512 neighbours per
+    block get LDS entries; a level of the fast shape -- at most 64 nodes, 128
+    span-1 and 192 longer edges -- with more than 64 longer edges left to
+    gather from the workspace takes the general path). Per direction: blocks
+    past 512 neighbours, fast-shaped levels past 64 gathers, fast levels
+    with some gathers."""
+    src, dst = np.asarray(g.src, np.int64), np.asarray(g.dst, np.int64)
+    lvl = oracle.levelize(g.n_nodes, src, dst)[0].astype(np.int64)
+    L = int(lvl.max() + 1)
+    span, w = lvl[dst] - lvl[src], np.bincount(lvl, minlength=L)
+    out = {}
+    for fwd in (True, False):
+        own, nb = (dst, src) if fwd else (src, dst)
+        step = lvl[own] if fwd else L - 1 - lvl[own]
+        nstep = lvl[nb] if fwd else L - 1 - lvl[nb]
+        nn = np.bincount(step[span == 1], minlength=L)
+        nf = np.bincount(step[span >= 2], minlength=L)
+        shape = ((w if fwd else w[::-1]) <= 64) & (nn <= 128) & (nf <= 192)
+        slot, over = np.zeros(src.shape[0], bool), 0
+        for k in range((L + 7) // 8):
+            m = (step // 8 == k) & shape[step] & (span > 4) & (nstep <= 8 * k - 12)
+            u = np.unique(nb[m])
+            over += len(u) > 512
+            slot |= m & np.isin(nb, u[:512])
+        gathered = np.bincount(step[(span > 4) & ~slot], minlength=L)
+        out["t" if fwd else "b"] = (over, int(((gathered > 64) & shape).sum()),
+                                    int((shape & (gathered > 0) & (gathered <= 64)).sum()))
+    return out
+
+
+def test_batch_long_edge_blocks(P):
+    """A layered DAG whose long edges overflow the per-block LDS lists (more
+    than 512 distinct neighbours in a block of 8 levels), with levels that
+    gather more than 64 values from the workspace (general path) and levels
+    that mix gathered and LDS-served records, in both directions: the batch
+    with and without label sums and the one-placement sweep, against the
+    oracle for every placement."""
+    g = W.long_edge_dag(np.random.default_rng(5))
+    cov = _long_edge_coverage(g)
+    say(f"long-edge blocks V={g.n_nodes} E={g.n_edges} coverage={cov}")
+    for d in ("t", "b"):
+        assert all(x > 0 for x in cov[d]), cov   # every case present
+    rng = np.random.default_rng(6)
+    n_place = 7
+    pl = rng.integers(0, g.n_labels, (g.n_nodes, n_place)).astype(np.int32)
+    pl[:, 0] = g.placement
+    pl[:, -1] = 0
+    G = P.Graph(g.n_nodes, g.src, g.dst, g.comp, g.edge_cost, g.mem)
+    out = run_batch(P, G, pl, g)
+    check_batch(g, pl, out, range(n_place))
+    for p in (1, 4):   # one placement per chain reads the same lists
+        tl, bl, m = G.tb_levels(dev(pl[:, p].copy(), torch.int32))
+        torch.cuda.synchronize()
+        etl, ebl, em = oracle.tb_levels(g.n_nodes, g.src, g.dst, g.comp, g.edge_cost,
+                                        pl[:, p].copy())
+        assert (tl.cpu().numpy() == etl).all() and (bl.cpu().numpy() == ebl).all(), p
+        assert int(m.item()) == em, p
+    G.close()
+    _tb_batch_case(P, g, pl)
+
+
 @pytest.mark.parametrize("shift", [18, 20])
 def test_batch_large_weights_successor_links(P, shift):
     """Weights scaled by 2^shift on config 0 (4 labels: 2 label bits; 2050

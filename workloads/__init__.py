@@ -17,6 +17,7 @@ from .graphs import (  # noqa: F401
     random_dag,
     chain_graph,
     layered_dag,
+    long_edge_dag,
     node_kinds,
     path_clusters,
 )

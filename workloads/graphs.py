@@ -562,6 +562,48 @@ def random_dag(rng: np.random.Generator, n: int, p_edge: float = 0.3,
                       np.full(max(1, n_labels), 150, np.int64), {})
 
 
+def long_edge_dag(rng: np.random.Generator, levels: int = 80, width: int = 40,
+                  n_sources: int = 600, n_long: int = 3, min_long_span: int = 20,
+                  mid_levels=None, n_labels: int = 4) -> SynthGraph:
+    """A layered DAG rich in long edges: a first level of ``n_sources`` nodes,
+    then ``levels`` levels of ``width`` nodes. Every node past the first level
+    has one in-edge from the level before it (which fixes its level) and
+    ``n_long`` in-edges from random nodes at least ``min_long_span`` levels
+    back; a level in ``mid_levels`` (level -> count) instead gives each node
+    that many in-edges of span 5 to 11. Small weights force ties."""
+    if mid_levels is None:
+        mid_levels = {30: 2, 31: 2, 45: 1, 60: 1}
+    ids = [np.arange(n_sources)]
+    nxt = n_sources
+    for _ in range(levels):
+        ids.append(np.arange(nxt, nxt + width))
+        nxt += width
+    n = nxt
+    src, dst = [], []
+    for lv in range(1, levels + 1):
+        for v in ids[lv]:
+            src.append(int(rng.choice(ids[lv - 1]))); dst.append(int(v))
+            if lv in mid_levels:
+                for _ in range(mid_levels[lv]):
+                    span = int(rng.integers(5, 12))
+                    if lv - span >= 0:
+                        src.append(int(rng.choice(ids[lv - span]))); dst.append(int(v))
+            elif lv - min_long_span >= 0:
+                pool = np.concatenate(ids[:lv - min_long_span + 1])
+                for u in rng.choice(pool, n_long, replace=False):
+                    src.append(int(u)); dst.append(int(v))
+    perm = rng.permutation(n)            # ids in no particular order
+    src = perm[np.asarray(src, np.int64)].astype(np.int32)
+    dst = perm[np.asarray(dst, np.int64)].astype(np.int32)
+    ne = src.shape[0]
+    comp = rng.integers(1, 10, n).astype(np.int64)
+    cost = rng.integers(0, 10, ne).astype(np.int64)
+    mem = rng.integers(0, 100, n).astype(np.int64)
+    label = rng.integers(0, n_labels, n).astype(np.int32)
+    return SynthGraph("long_edge_dag", n, src, dst, comp, cost, mem, label, n_labels,
+                      np.full(n_labels, 5_000, np.int64), {})
+
+
 def chain_graph(rng: np.random.Generator, n: int, n_labels: int = 2) -> SynthGraph:
     """The path 0 -> 1 -> ... -> n-1 with random weights and labels."""
     src = np.arange(max(n - 1, 0), dtype=np.int32)
