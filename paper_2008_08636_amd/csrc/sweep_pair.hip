@@ -444,7 +444,6 @@ __device__ __forceinline__ void pair_chain(const SweepArgs &a, int32_t slice, ch
         // after level `step`: labels of step + 2, loads of step + LN, window refill
         auto tail = [&](int32_t step, const NearSet<S> &B2, NearSet<S> &LD, const WinEnt &b2,
                         const WinEnt &bl) {
-            if (lane < cnt_w(b2.cnt)) c.slab[(step & 1) * kPNodes + lane] = B2.lab;
             loads(LD, bl);
             if ((step & (kWin / 2 - 1)) == 0 && step > 0) fill(step + kWin / 2, 1);
             __syncthreads();
@@ -485,6 +484,8 @@ __device__ __forceinline__ void pair_chain(const SweepArgs &a, int32_t slice, ch
             __builtin_amdgcn_s_waitcnt(0);
         }
         __syncthreads();
+        // the window entry of the level each step loads, read one step ahead
+        WinEnt wn[2];
         // a segment's first levels, on the general path
         for (int32_t sx = s0; sx < a0; sx++) {
             pair_slow<S, FWD, true, BM, NXF>(kargs_here(), c.p0 / S, sx, (LdsBytes *)c.win);
@@ -495,6 +496,7 @@ __device__ __forceinline__ void pair_chain(const SweepArgs &a, int32_t slice, ch
             for (int j = 0; j < kLN; j++) loads(st[j], c.W(a0 + j));
             __builtin_amdgcn_s_waitcnt(0);
             if (lane < cnt_w(c.W(a0 + 1).cnt)) c.slab[((a0 + 1) & 1) * kPNodes + lane] = st[1].lab;
+            wn[0] = c.W(a0 + kLN);
         }
         __syncthreads();
         int32_t step = a0;
@@ -509,13 +511,23 @@ __device__ __forceinline__ void pair_chain(const SweepArgs &a, int32_t slice, ch
                 const WinEnt b0 = {st[r].wnlo, 0, 0, st[r].wcnt};
                 const WinEnt b1 = {0, 0, 0, st[(r + 1) % kNS].wcnt};
                 const WinEnt b2 = {0, 0, 0, st[(r + 2) % kNS].wcnt};
+                // off the level's dependent LDS chain: the labels of level
+                // step + 2 (their slot was last read at the step before) and
+                // the window entry the next step's loads need
+                if (lane < cnt_w(b2.cnt)) c.slab[(sa & 1) * kPNodes + lane] = st[(r + 2) % kNS].lab;
+                const WinEnt bl = wn[r & 1];
+                {
+                    // an index the compiler cannot see is zero: the entry
+                    // stays in vector registers and nothing waits for it
+                    // before its first use
+                    int32_t z;
+                    asm volatile("v_mov_b32 %0, 0" : "=v"(z));
+                    wn[(r + 1) & 1] = c.win[((sa + kLN + 1) & (kWin - 1)) + z];
+                }
                 if (cnt_fast(b0.cnt))
                     body(sa, b0, b1, st[r], st[(r + 1) % kNS]);
                 else
                     pair_slow<S, FWD, true, BM, NXF>(kargs_here(), c.p0 / S, sa, (LdsBytes *)c.win);
-                // the window entry of the level loaded now: read after the
-                // level's own LDS work, which it would otherwise delay
-                const WinEnt bl = c.W(sa + kLN);
                 tail(sa, st[(r + 2) % kNS], st[(r + kLN) % kNS], b2, bl);
                 step++;
             }
