@@ -398,12 +398,8 @@ __device__ __forceinline__ void pair_chain(const SweepArgs &a, int32_t slice, ch
     const uint32_t vmax = c.V > 0 ? (uint32_t)(c.V - 1) : 0u;
     const PairLevel *plv = FWD ? a.pl_t : a.pl_b;   // per-lane reads
 
-    // window entries for steps s0 + lane + 64 k, k < n (wave 0, synchronous)
-    auto fill = [&](int32_t s0, int n) {
-        for (int k = 0; k < n; k++) {
-            const int32_t sx = s0 + lane + k * kLanes;
-            const int32_t x = c.level_of(sx);
-            const PairLevel l0 = plv[x], l1 = plv[x + 1];
+    // the window entry of step sx from its level's bounds l0, l1
+    auto fill_entry = [&](int32_t sx, const PairLevel &l0, const PairLevel &l1) {
             WinEnt e;
             e.nlo = l0.node_lo;
             e.nrlo = l0.near_lo;
@@ -415,6 +411,14 @@ __device__ __forceinline__ void pair_chain(const SweepArgs &a, int32_t slice, ch
             e.cnt = (uint32_t)min(w, 255) | (uint32_t)min(nn, 255) << 8 |
                     (uint32_t)min(nf, 255) << 16 | (fast ? 1u << 31 : 0u);
             c.win[sx & (kWin - 1)] = e;
+    };
+    // window entries for steps s0 + lane + 64 k, k < n (wave 0, synchronous:
+    // before the pipelined loop)
+    auto fill = [&](int32_t s0, int n) {
+        for (int k = 0; k < n; k++) {
+            const int32_t sx = s0 + lane + k * kLanes;
+            const int32_t x = c.level_of(sx);
+            fill_entry(sx, plv[x], plv[x + 1]);
         }
     };
 
@@ -442,10 +446,20 @@ __device__ __forceinline__ void pair_chain(const SweepArgs &a, int32_t slice, ch
             X.wcnt = b.cnt;
         };
         // after level `step`: labels of step + 2, loads of step + LN, window refill
+        // the window is refilled 64 entries at a time, 64 steps ahead: the
+        // bounds load at step 64 m and the entries go to LDS at step 64 m + 4,
+        // so the stores wait on loads that are due by then anyway (a
+        // synchronous refill drained every load in flight)
+        PairLevel fl0 = {}, fl1 = {};
         auto tail = [&](int32_t step, const NearSet<S> &B2, NearSet<S> &LD, const WinEnt &b2,
                         const WinEnt &bl) {
             loads(LD, bl);
-            if ((step & (kWin / 2 - 1)) == 0 && step > 0) fill(step + kWin / 2, 1);
+            if ((step & (kWin / 2 - 1)) == 0 && step > 0) {
+                const int32_t x = c.level_of(step + kWin / 2 + lane);
+                fl0 = plv[x];
+                fl1 = plv[x + 1];
+            }
+            if ((step & (kWin / 2 - 1)) == 4 && step > 4) fill_entry(step - 4 + kWin / 2 + lane, fl0, fl1);
             __syncthreads();
         };
         auto body = [&](int32_t step, const WinEnt &b0, const WinEnt &b1, NearSet<S> &A,
@@ -550,6 +564,9 @@ __device__ __forceinline__ void pair_chain(const SweepArgs &a, int32_t slice, ch
             X.wcnt = b.cnt;
 #pragma unroll
             for (int j = 0; j < kNEf; j++) {
+                // tasks past the level's records are never read: load them
+                // only where the level has records for them (uniform)
+                if (j > 0 && nf <= j * kLanes) continue;
                 const uint32_t e = lane + j * kLanes < nf ? (uint32_t)(b.frlo + lane + j * kLanes) : 0u;
                 const FarRec16 r = at(frec, e);
                 X.nb[j] = r.nb;
