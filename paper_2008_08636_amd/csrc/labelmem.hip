@@ -343,6 +343,84 @@ __global__ __launch_bounds__(256) void k_moves_to_slices(int32_t V, int32_t P,
     if (fit != nullptr && umax >= fit_limit) *fit = 0;
 }
 
+// The same labels with one lane per level-major node, for schedules with a
+// few moves per node. The workgroup first stages the move lists of its 256
+// nodes, {step, label} in move order, in LDS (a workgroup whose lists hold
+// more than kLaneMoves entries reads them from global memory instead); then
+// each lane walks the slices in order, keeping its node's current label and
+// next move, takes every move whose step is at most the placement, and writes
+// the slice's S labels with one store. Consecutive lanes hold consecutive
+// nodes, so each wave's store is one contiguous run of 64 x 4S bytes, and the
+// only memory operations in the walk are these stores (the move reads come
+// from LDS), so no wait on the stores is ever needed.
+constexpr int kLaneMoves = 3584;   // LDS entries per workgroup (28 KB)
+constexpr int kLaneMovesPerNode = 11;   // the host takes this kernel up to M <= 11 V
+
+template <int S>
+__global__ __launch_bounds__(256) void k_moves_lanes(int32_t V, int32_t P, const int32_t *order,
+                                                     const int32_t *base, const int32_t *mv_off,
+                                                     const int4 *mv_ent, int32_t *lab_w,
+                                                     int64_t lab_stride, int32_t K, int32_t *err,
+                                                     int32_t *fit, uint32_t fit_limit) {
+    __shared__ int2 mv[kLaneMoves];
+    __shared__ int wsum[256 / kWave + 1];
+    const int32_t v = blockIdx.x * 256 + threadIdx.x;
+    const int32_t o = v < V ? order[v] : -1;
+    const int32_t lo = o >= 0 ? mv_off[o] : 0;
+    const int32_t cnt = o >= 0 ? mv_off[o + 1] - lo : 0;
+    const int32_t lab0 = o >= 0 ? base[o] : 0;
+    int total;
+    const int32_t at = block_excl_scan_i32(cnt, wsum, &total);
+    const bool in_lds = total <= kLaneMoves;   // uniform over the workgroup
+    if (in_lds) {
+        for (int32_t k = 0; k < cnt; k += 4) {   // four loads in flight per lane
+            int4 e[4];
+#pragma unroll
+            for (int j = 0; j < 4; j++)
+                if (k + j < cnt) e[j] = mv_ent[lo + k + j];
+#pragma unroll
+            for (int j = 0; j < 4; j++)
+                if (k + j < cnt) mv[at + k + j] = make_int2(e[j].x, e[j].z);
+        }
+    }
+    __syncthreads();
+    const int32_t n_slices = (P + S - 1) / S;
+    uint32_t umax = 0;
+    // the walk, with move k of the lane's list read by get(k)
+    auto walk = [&](auto get) {
+        constexpr int32_t kNone = INT32_MAX;   // past the last move
+        int32_t cur = lab0, k = 0;
+        int2 nx = cnt > 0 ? get(0) : make_int2(kNone, 0);
+        int32_t *dst = lab_w + (int64_t)min(v, V - 1) * S;
+        for (int32_t sl = 0; sl < n_slices; sl++, dst += lab_stride) {
+            LabPack<S> x;
+#pragma unroll
+            for (int q = 0; q < S; q++) {
+                const int32_t p = sl * S + q;   // past P every move applies
+                while (nx.x <= p) {
+                    cur = nx.y;
+                    k++;
+                    nx = k < cnt ? get(k) : make_int2(kNone, 0);
+                }
+                x.v[q] = cur;
+                umax = max(umax, (uint32_t)cur);
+            }
+            if (v < V)
+                __builtin_nontemporal_store(*reinterpret_cast<const typename LabPack<S>::Word *>(&x),
+                                            reinterpret_cast<typename LabPack<S>::Word *>(dst));
+        }
+    };
+    if (in_lds)
+        walk([&](int32_t k) { return mv[at + k]; });
+    else
+        walk([&](int32_t k) {
+            const int4 e = mv_ent[lo + k];
+            return make_int2(e.x, e.z);
+        });
+    if (K > 0 && umax >= (uint32_t)K) atomicOr(err, 1);
+    if (fit != nullptr && umax >= fit_limit) *fit = 0;
+}
+
 }  // namespace
 
 namespace {
@@ -400,6 +478,21 @@ hipError_t launch_moves_to_slices(const Graph &g, const int32_t *base, int32_t P
         e = hipGetLastError();
     }
     if (e != hipSuccess) return e;
+    if (M <= (int64_t)kLaneMovesPerNode * V) {
+        const unsigned grid = (unsigned)((V + 255) / 256);
+        if (S == 1)
+            k_moves_lanes<1><<<grid, 256, 0, g.stream>>>(V, P, g.order, base, off, ent, lab_w,
+                                                         lab_stride, K, err, fit, fit_limit);
+        else if (S == 2)
+            k_moves_lanes<2><<<grid, 256, 0, g.stream>>>(V, P, g.order, base, off, ent, lab_w,
+                                                         lab_stride, K, err, fit, fit_limit);
+        else if (S == 4)
+            k_moves_lanes<4><<<grid, 256, 0, g.stream>>>(V, P, g.order, base, off, ent, lab_w,
+                                                         lab_stride, K, err, fit, fit_limit);
+        else
+            return hipErrorInvalidValue;
+        return hipGetLastError();
+    }
     const unsigned grid = (unsigned)((V + 63) / 64);
     if (S == 1)
         k_moves_to_slices<1><<<grid, 256, 0, g.stream>>>(V, P, g.order, base, off, ent, lab_w,

@@ -764,6 +764,40 @@ def test_evaluate_moves_small(P):
     G.close()
 
 
+@pytest.mark.parametrize("n_moves,n_place", [(3584, 64), (3585, 63), (6400, 64)])
+def test_evaluate_moves_label_build_forms(P, n_moves, n_place):
+    """The labels built from the moves take one of three forms: one lane per
+    node with the moves of a 256-node workgroup staged in LDS (up to 3,584
+    entries), the same walk reading the moves from global memory (a workgroup
+    with more), and one wave per 64-node tile (more than 11 moves per node on
+    average). Two levels of 256 nodes, every move on a source, so the first
+    workgroup holds all of them: 3,584 moves fit, 3,585 do not, and 6,400 on
+    512 nodes exceed the average. Each equals build + evaluate_batch and the
+    oracle."""
+    say(f"evaluate_moves label build forms: {n_moves} moves, {n_place} placements")
+    rng = np.random.default_rng(4242 + n_moves)
+    g = W.layered_dag(rng, [256, 256], [0, 3], n_labels=4)
+    sources = np.setdiff1d(np.arange(g.n_nodes), g.dst).astype(np.int32)
+    assert sources.shape[0] == 256
+    cuts = np.sort(rng.integers(0, n_moves + 1, n_place - 1))
+    ptr = np.concatenate([[0], cuts, [n_moves]]).astype(np.int64)
+    node = rng.choice(sources, n_moves).astype(np.int32)      # repeats within a step too
+    label = rng.integers(0, g.n_labels, n_moves).astype(np.int32)
+    sched = W.MoveSchedule(g.placement.copy(), ptr, node, label, g.n_labels)
+    G = P.Graph(g.n_nodes, g.src, g.dst, g.comp, g.edge_cost, g.mem)
+    args = (dev(sched.base, torch.int32), dev(ptr, torch.int64), dev(node, torch.int32),
+            dev(label, torch.int32))
+    out = G.evaluate_moves(*args, g.n_labels, dev(g.capacity, torch.int64))
+    torch.cuda.synchronize()
+    got = {k: v.cpu().numpy() for k, v in out.items()}
+    pl = W.materialize_placements(sched).T.copy()
+    check_batch(g, pl, got, sorted({0, 1, n_place // 2, n_place - 2, n_place - 1}))
+    ref = run_batch(P, G, pl, g)
+    for k in ref:
+        assert (ref[k] == got[k]).all(), k
+    G.close()
+
+
 def test_step_ptr_checks_and_deferred_errors(P):
     """step_ptr is checked against the number of moves on the device (no host
     read-back): one that does not start at 0, decreases or does not end at
