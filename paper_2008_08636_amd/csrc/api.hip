@@ -289,7 +289,7 @@ int ensure_pair(Graph *g) {
     if (e == hipSuccess)
         e = dev_malloc((void **)&ws, sizeof(int32_t) * scan_workspace_elems((int32_t)E));
     PairLevel *pl[2] = {nullptr, nullptr};
-    NearRec16 *nr[2] = {nullptr, nullptr};
+    NearRec12 *nr[2] = {nullptr, nullptr};
     FarRec16 *fr[2] = {nullptr, nullptr};
     for (int d = 0; d < 2 && e == hipSuccess; d++) {
         const bool fwd = d == 0;

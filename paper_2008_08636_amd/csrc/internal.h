@@ -17,7 +17,7 @@
 //     comp_lm, mem_lm int64[V]
 //     in_rec, out_rec EdgeRec16[E] and node_rec NodeRec16[V]: the same data
 //       as 16-byte records, so a sweep task loads its edge with one load
-//     pl_t / pl_b PairLevel[L+2], nr_t / nr_b NearRec16[], fr_t / fr_b
+//     pl_t / pl_b PairLevel[L+2], nr_t / nr_b NearRec12[], fr_t / fr_b
 //       FarRec16[]: the edges of each level split into span-1
 //       ("near") and longer ("far") edges for the batched sweeps, per
 //       direction; built on first use
@@ -84,7 +84,7 @@ struct Graph {
     EdgeRec16 *in_rec = nullptr, *out_rec = nullptr;
     NodeRec16 *node_rec = nullptr;
     PairLevel *pl_t = nullptr, *pl_b = nullptr;   // built on first batched evaluation
-    NearRec16 *nr_t = nullptr, *nr_b = nullptr;
+    NearRec12 *nr_t = nullptr, *nr_b = nullptr;
     FarRec16 *fr_t = nullptr, *fr_b = nullptr;
     int32_t *lsrc_t = nullptr, *lsrc_b = nullptr;   // long edges' neighbours per block
     int32_t *preoff_t = nullptr, *preoff_b = nullptr;
@@ -209,7 +209,7 @@ hipError_t launch_finish(const SweepArgs &a, int32_t S, uint8_t *crit, uint32_t 
 hipError_t launch_pair_flags(const Graph &g, bool fwd, int32_t *flag);
 // near_rank = exclusive scan of flag (E + 1 entries); fills pl, nr, fr
 hipError_t launch_pair_split(const Graph &g, bool fwd, const int32_t *near_rank, PairLevel *pl,
-                             NearRec16 *nr, FarRec16 *fr);
+                             NearRec12 *nr, FarRec16 *fr);
 // long edges of the pair sweep: fills lsrc (long_list_elems(L)) and points
 // the far records of long edges at their LDS entries
 hipError_t launch_long_blocks(const Graph &g, bool fwd, PairLevel *pl, FarRec16 *fr,

@@ -38,14 +38,15 @@ struct alignas(16) PairLevel {
 // is (value << ob) plus this word (labels differ) or its low ob bits (same
 // label). It fits whenever the packed keys are used: their condition bounds
 // every cost by 2^(62 - ob).
-// A span-1 edge: the cost word and the owner's and neighbour's index inside
-// their levels (own | nb << 16); the pad last, so that a load of the used
-// twelve bytes is one instruction.
-struct alignas(16) NearRec16 {
-    int64_t ck;
+// A span-1 edge: the cost word (as two 32-bit halves, so that the records
+// pack at a twelve-byte stride and a level's records span fewer cache lines;
+// one load instruction reads a record) and the owner's and neighbour's index
+// inside their levels (own | nb << 16).
+struct NearRec12 {
+    uint32_t ck_lo, ck_hi;
     uint32_t ol;
-    int32_t pad;
 };
+static_assert(sizeof(NearRec12) == 12, "twelve-byte span-1 records");
 // A longer edge: the cost word, the owner's index inside its level and where
 // the sweep finds the neighbour's value (own | ring << 16), and the neighbour
 // (level-major id). The cost word comes first: a load of the first twelve
@@ -134,7 +135,7 @@ struct SweepArgs {
     int32_t *nx_w;          // [slice][V][S] original id of the chosen successor (-1: none), or null
     int64_t ws_stride;      // elements of ftl / bll / nx_w per slice (>= V * S)
     const PairLevel *pl_t, *pl_b;         // batched sweeps: near / far split per level
-    const NearRec16 *nr_t, *nr_b;
+    const NearRec12 *nr_t, *nr_b;
     const FarRec16 *fr_t, *fr_b;
     const int32_t *lsrc_t, *lsrc_b;       // long edges' neighbours per block (long_list_elems)
     const int32_t *preoff_t, *preoff_b;   // [L + 1] per neighbour level

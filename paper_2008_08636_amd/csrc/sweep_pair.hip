@@ -424,7 +424,7 @@ __device__ __forceinline__ void pair_chain(const SweepArgs &a, int32_t slice, ch
 
     if (NEAR) {
         // ================= wave 0: finalise + span-1 edges =================
-        const NearRec16 *nrec = FWD ? a.nr_t : a.nr_b;
+        const NearRec12 *nrec = FWD ? a.nr_t : a.nr_b;
         NearSet<S> st[kNS];
         // unconditional loads (idle lanes read element 0), so that the
         // compiler's in-order wait counts are the same on every path
@@ -433,14 +433,19 @@ __device__ __forceinline__ void pair_chain(const SweepArgs &a, int32_t slice, ch
 #pragma unroll
             for (int j = 0; j < kNEn; j++) {
                 const uint32_t e = lane + j * kLanes < nn ? (uint32_t)(b.nrlo + lane + j * kLanes) : 0u;
-                const NearRec16 r = at(nrec, e);
+                const NearRec12 r = at(nrec, e);
                 X.ol[j] = r.ol;
-                X.c[j] = r.ck;
+                X.c[j] = (int64_t)(((uint64_t)r.ck_hi << 32) | r.ck_lo);
             }
             const uint32_t v = lane < w ? (uint32_t)(b.nlo + lane) : 0u;
-            const NodeRec16 n = at(a.node_rec, v);
-            X.comp = n.comp;
-            X.mem = n.mem;
+            if constexpr (FWD && BM != kBinsNone) {   // the label sums need the memory
+                const NodeRec16 n = at(a.node_rec, v);
+                X.comp = n.comp;
+                X.mem = n.mem;
+            } else {
+                X.comp = at(a.comp_lm, v);
+                X.mem = 0;
+            }
             X.lab = at(c.labs, v);
             X.wnlo = b.nlo;
             X.wcnt = b.cnt;
@@ -878,7 +883,7 @@ __global__ void k_pair_levels(int32_t L, const int32_t *level_ptr, const int32_t
 __global__ void k_pair_records(int64_t E, int32_t L, bool fwd, int32_t ob, const int32_t *level,
                                const int32_t *order, const int32_t *level_ptr, const int32_t *nbr,
                                const int32_t *own, const int64_t *cost, const int32_t *nb_orig,
-                               const int32_t *near_rank, NearRec16 *nr, FarRec16 *fr) {
+                               const int32_t *near_rank, NearRec12 *nr, FarRec16 *fr) {
     const long long omax = (1ll << ob) - 1;
     for (int64_t e = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; e < E;
          e += (int64_t)gridDim.x * blockDim.x) {
@@ -893,10 +898,10 @@ __global__ void k_pair_records(int64_t E, int32_t L, bool fwd, int32_t ob, const
         const int64_t ck = fwd ? cost[e]
                                : (int64_t)(((uint64_t)cost[e] << ob) | (uint64_t)(omax - nb_orig[e]));
         if (span == 1) {
-            NearRec16 r;
+            NearRec12 r;
             r.ol = own_local | ((nb_local & 0xffffu) << 16);
-            r.pad = 0;
-            r.ck = ck;
+            r.ck_lo = (uint32_t)ck;
+            r.ck_hi = (uint32_t)((uint64_t)ck >> 32);
             nr[near_rank[e]] = r;
         } else {
             const int32_t w_nb = level_ptr[lv_nb + 1] - nb_lo;
@@ -1106,7 +1111,7 @@ hipError_t launch_pair_flags(const Graph &g, bool fwd, int32_t *flag) {
 }
 
 hipError_t launch_pair_split(const Graph &g, bool fwd, const int32_t *near_rank, PairLevel *pl,
-                             NearRec16 *nr, FarRec16 *fr) {
+                             NearRec12 *nr, FarRec16 *fr) {
     k_pair_levels<<<(unsigned)((g.L + 2 + 255) / 256), 256, 0, g.stream>>>(
         g.L, g.level_ptr, fwd ? g.in_off : g.out_off, near_rank, pl);
     hipError_t e = hipGetLastError();
