@@ -505,16 +505,22 @@ int evaluate_impl(Graph *g, int32_t n_place, const int32_t *placements, const Mo
 
     const int32_t K = label_mem != nullptr ? n_labels : 0;
     int32_t *fit = gated ? g->bt_fit : nullptr;
+    // The pair sweep with label sums reads 16-bit labels (checked below K <=
+    // 2^16): half the bytes for the label build to write and for the sweep to
+    // read. The per-slice stride, in 16-bit elements, stays within the bytes
+    // of the 32-bit layout.
+    const bool lab16 = K > 0 && lb > 0 && g->V > 0;
+    const int64_t lab_elems = lab16 ? ((int64_t)g->V * S + 127) / 128 * 128 : lab_stride;
     HIP_TRY(clear_errors(g));
     if (fit != nullptr) HIP_TRY(launch_fill_i32(fit, 1, 1, g->stream));
     if (mv != nullptr) {
         HIP_TRY(launch_check_steps(mv->step_ptr, n_place, n_moves, g->err, g->stream));
         HIP_TRY(launch_moves_to_slices(*g, mv->base, n_place, mv->step_ptr, n_moves, mv->node,
-                                       mv->label, S, moves_scratch, lab_w, lab_stride, K,
-                                       g->err, fit, 1u << lb));
+                                       mv->label, S, moves_scratch, lab_w, lab_elems, K,
+                                       g->err, fit, 1u << lb, lab16));
     } else {
-        HIP_TRY(launch_permute_labels_batch(*g, placements, n_place, S, lab_w, lab_stride, K,
-                                            g->err, fit, 1u << lb));
+        HIP_TRY(launch_permute_labels_batch(*g, placements, n_place, S, lab_w, lab_elems, K,
+                                            g->err, fit, 1u << lb, lab16));
     }
     if (K > 0) {
         HIP_TRY(launch_fill_i64(label_mem, (int64_t)n_place * K, 0, g->stream));
@@ -523,7 +529,8 @@ int evaluate_impl(Graph *g, int32_t n_place, const int32_t *placements, const Mo
     a.P = n_place;
     a.K = K;
     a.lab_w = lab_w;
-    a.lab_stride = lab_stride;
+    a.lab_stride = lab_elems;
+    a.lab16 = lab16 ? 1 : 0;
     a.ftl = ftl;
     a.bll = bll;
     a.nx_w = path != nullptr ? nx_w : nullptr;

@@ -38,6 +38,12 @@ struct alignas(4 * S) LabPack {
     static_assert(S == 1 || S == 2 || S == 4, "one, two or four slots per slice");
 };
 
+// two labels as 16-bit halves of one word (the 16-bit label layout; the
+// labels were checked against the full values)
+__device__ __forceinline__ uint32_t pack16x2(int32_t a, int32_t b) {
+    return (uint32_t)(uint16_t)a | ((uint32_t)(uint16_t)b << 16);
+}
+
 inline unsigned grid_for(int64_t n, int block, int cap = 65536) {
     int64_t g = (n + block - 1) / block;
     if (g < 1) g = 1;
@@ -245,7 +251,7 @@ __global__ __launch_bounds__(256) void k_moves_to_slices(int32_t V, int32_t P,
                                                          const int4 *mv_ent, int32_t *lab_w,
                                                          int64_t lab_stride, int32_t K,
                                                          int32_t *err, int32_t *fit,
-                                                         uint32_t fit_limit) {
+                                                         uint32_t fit_limit, int lab16) {
     constexpr int TV = 64, TP = 64, NW = 256 / kWave, RW = TV / NW;
     __shared__ int32_t tile[TV][TP + 1];
     const int lane = lane_id(), w = wave_id();
@@ -321,6 +327,22 @@ __global__ __launch_bounds__(256) void k_moves_to_slices(int32_t V, int32_t P,
             const int sl = i / (TV / NP), r = NP * (i % (TV / NP));
             const int32_t v = v0 + r;
             if (v >= V) continue;
+            if constexpr (S == 2) {
+                if (lab16) {   // 16-bit labels: 8 bytes for two nodes
+                    uint32_t *d16 = reinterpret_cast<uint32_t *>(
+                        reinterpret_cast<uint16_t *>(lab_w) + (int64_t)(sl0 + sl) * lab_stride +
+                        (int64_t)v * 2);
+                    const uint32_t w0 = pack16x2(tile[r][sl * 2], tile[r][sl * 2 + 1]);
+                    if (v + 1 < V) {
+                        typedef uint32_t u2 __attribute__((ext_vector_type(2)));
+                        const u2 x = {w0, pack16x2(tile[r + 1][sl * 2], tile[r + 1][sl * 2 + 1])};
+                        __builtin_nontemporal_store(x, reinterpret_cast<u2 *>(d16));
+                    } else {
+                        __builtin_nontemporal_store(w0, d16);
+                    }
+                    continue;
+                }
+            }
             int32_t *dst = lab_w + (int64_t)(sl0 + sl) * lab_stride + (int64_t)v * S;
             if (NP == 1 || v + 1 < V) {
                 LabPack<S * NP> x;
@@ -361,7 +383,7 @@ __global__ __launch_bounds__(256) void k_moves_lanes(int32_t V, int32_t P, const
                                                      const int32_t *base, const int32_t *mv_off,
                                                      const int4 *mv_ent, int32_t *lab_w,
                                                      int64_t lab_stride, int32_t K, int32_t *err,
-                                                     int32_t *fit, uint32_t fit_limit) {
+                                                     int32_t *fit, uint32_t fit_limit, int lab16) {
     __shared__ int2 mv[kLaneMoves];
     __shared__ int wsum[256 / kWave + 1];
     const int32_t v = blockIdx.x * 256 + threadIdx.x;
@@ -391,8 +413,12 @@ __global__ __launch_bounds__(256) void k_moves_lanes(int32_t V, int32_t P, const
         constexpr int32_t kNone = INT32_MAX;   // past the last move
         int32_t cur = lab0, k = 0;
         int2 nx = cnt > 0 ? get(0) : make_int2(kNone, 0);
+        // 32-bit labels at dst, or (16-bit layout, S = 2) one word per node
         int32_t *dst = lab_w + (int64_t)min(v, V - 1) * S;
-        for (int32_t sl = 0; sl < n_slices; sl++, dst += lab_stride) {
+        uint32_t *d16 = reinterpret_cast<uint32_t *>(reinterpret_cast<uint16_t *>(lab_w) +
+                                                     (int64_t)min(v, V - 1) * 2);
+        const int64_t step16 = lab_stride / 2;   // words per slice (the stride is even)
+        for (int32_t sl = 0; sl < n_slices; sl++, dst += lab_stride, d16 += step16) {
             LabPack<S> x;
 #pragma unroll
             for (int q = 0; q < S; q++) {
@@ -405,9 +431,16 @@ __global__ __launch_bounds__(256) void k_moves_lanes(int32_t V, int32_t P, const
                 x.v[q] = cur;
                 umax = max(umax, (uint32_t)cur);
             }
-            if (v < V)
+            if (v < V) {
+                if constexpr (S == 2) {
+                    if (lab16) {
+                        __builtin_nontemporal_store(pack16x2(x.v[0], x.v[1]), d16);
+                        continue;
+                    }
+                }
                 __builtin_nontemporal_store(*reinterpret_cast<const typename LabPack<S>::Word *>(&x),
                                             reinterpret_cast<typename LabPack<S>::Word *>(dst));
+            }
         }
     };
     if (in_lds)
@@ -449,8 +482,10 @@ hipError_t launch_moves_to_slices(const Graph &g, const int32_t *base, int32_t P
                                   const int64_t *step_ptr, int64_t M, const int32_t *node,
                                   const int32_t *label, int32_t S, int32_t *scratch,
                                   int32_t *lab_w, int64_t lab_stride, int32_t K, int32_t *err,
-                                  int32_t *fit, uint32_t fit_limit) {
+                                  int32_t *fit, uint32_t fit_limit, bool lab16) {
     if (g.V == 0 || P == 0) return hipSuccess;
+    if (lab16 && (S != 2 || lab_stride % 2 != 0)) return hipErrorInvalidValue;
+    const int l16 = lab16 ? 1 : 0;
     const int32_t V = g.V;
     const size_t m64 = al64((size_t)M);
     int32_t *off = scratch;
@@ -482,13 +517,13 @@ hipError_t launch_moves_to_slices(const Graph &g, const int32_t *base, int32_t P
         const unsigned grid = (unsigned)((V + 255) / 256);
         if (S == 1)
             k_moves_lanes<1><<<grid, 256, 0, g.stream>>>(V, P, g.order, base, off, ent, lab_w,
-                                                         lab_stride, K, err, fit, fit_limit);
+                                                         lab_stride, K, err, fit, fit_limit, l16);
         else if (S == 2)
             k_moves_lanes<2><<<grid, 256, 0, g.stream>>>(V, P, g.order, base, off, ent, lab_w,
-                                                         lab_stride, K, err, fit, fit_limit);
+                                                         lab_stride, K, err, fit, fit_limit, l16);
         else if (S == 4)
             k_moves_lanes<4><<<grid, 256, 0, g.stream>>>(V, P, g.order, base, off, ent, lab_w,
-                                                         lab_stride, K, err, fit, fit_limit);
+                                                         lab_stride, K, err, fit, fit_limit, l16);
         else
             return hipErrorInvalidValue;
         return hipGetLastError();
@@ -496,13 +531,13 @@ hipError_t launch_moves_to_slices(const Graph &g, const int32_t *base, int32_t P
     const unsigned grid = (unsigned)((V + 63) / 64);
     if (S == 1)
         k_moves_to_slices<1><<<grid, 256, 0, g.stream>>>(V, P, g.order, base, off, ent, lab_w,
-                                                         lab_stride, K, err, fit, fit_limit);
+                                                         lab_stride, K, err, fit, fit_limit, l16);
     else if (S == 2)
         k_moves_to_slices<2><<<grid, 256, 0, g.stream>>>(V, P, g.order, base, off, ent, lab_w,
-                                                         lab_stride, K, err, fit, fit_limit);
+                                                         lab_stride, K, err, fit, fit_limit, l16);
     else if (S == 4)
         k_moves_to_slices<4><<<grid, 256, 0, g.stream>>>(V, P, g.order, base, off, ent, lab_w,
-                                                         lab_stride, K, err, fit, fit_limit);
+                                                         lab_stride, K, err, fit, fit_limit, l16);
     else
         return hipErrorInvalidValue;
     return hipGetLastError();

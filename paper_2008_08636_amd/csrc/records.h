@@ -161,6 +161,11 @@ struct SweepArgs {
     // (((bl << ob) | (2^ob - 1 - successor id, 0: none)) << lb) | label, which
     // needs values below 2^(62 - ob - lb); 0 = plain packed b values.
     int32_t nxf;
+    // 1: lab_w holds 16-bit labels (unsigned; lab_stride counts 16-bit
+    // elements), so a node's two labels of a slice are one 32-bit word. The
+    // batched pair sweep with label sums takes them (labels checked below K
+    // <= 2^16); every other sweep reads 32-bit labels.
+    int32_t lab16;
 };
 
 }  // namespace pardnn

@@ -52,7 +52,7 @@ __global__ __launch_bounds__(256) void k_permute_labels(int32_t V, int32_t P,
                                                         const int32_t *placements,
                                                         int32_t *lab_w, int64_t lab_stride,
                                                         int32_t K, int32_t *err, int32_t *fit,
-                                                        uint32_t fit_limit) {
+                                                        uint32_t fit_limit, int lab16) {
     constexpr int TV = 64, TP = 64;  // tile: 64 nodes x 64 placements
     __shared__ int32_t tile[TV][TP + 1];
     const int32_t n_slices = (P + S - 1) / S;
@@ -78,9 +78,15 @@ __global__ __launch_bounds__(256) void k_permute_labels(int32_t V, int32_t P,
         const int rem = i % (TV * S);
         const int r = rem / S, s = rem % S;
         const int32_t v = v0 + r;
-        if (v < V)   // streamed past L2, as the sweep reads it much later
-            __builtin_nontemporal_store(tile[r][sl * S + s],
-                                        &lab_w[(int64_t)(sl0 + sl) * lab_stride + (int64_t)v * S + s]);
+        const int64_t o = (int64_t)(sl0 + sl) * lab_stride + (int64_t)v * S + s;
+        if (v >= V) continue;
+        // streamed past L2, as the sweep reads it much later; 16-bit labels
+        // were checked against their full values above
+        if (lab16)
+            __builtin_nontemporal_store((uint16_t)tile[r][sl * S + s],
+                                        reinterpret_cast<uint16_t *>(lab_w) + o);
+        else
+            __builtin_nontemporal_store(tile[r][sl * S + s], &lab_w[o]);
     }
 }
 
@@ -935,15 +941,17 @@ hipError_t launch_permute_labels(const Graph &g, const int32_t *placement, int32
 
 hipError_t launch_permute_labels_batch(const Graph &g, const int32_t *placements, int32_t P,
                                        int32_t S, int32_t *lab_w, int64_t lab_stride, int32_t K,
-                                       int32_t *err, int32_t *fit, uint32_t fit_limit) {
+                                       int32_t *err, int32_t *fit, uint32_t fit_limit,
+                                       bool lab16) {
+    if (lab16 && S != kBatchSlots) return hipErrorInvalidValue;
     if (g.V == 0 || P == 0) return hipSuccess;
     dim3 grid((g.V + 63) / 64, (P + 63) / 64);
     if (S == 1)
         k_permute_labels<1><<<grid, 256, 0, g.stream>>>(g.V, P, g.order, placements, lab_w,
-                                                        lab_stride, K, err, fit, fit_limit);
+                                                        lab_stride, K, err, fit, fit_limit, 0);
     else if (S == kBatchSlots)
-        k_permute_labels<kBatchSlots><<<grid, 256, 0, g.stream>>>(g.V, P, g.order, placements,
-                                                                  lab_w, lab_stride, K, err, fit, fit_limit);
+        k_permute_labels<kBatchSlots><<<grid, 256, 0, g.stream>>>(
+            g.V, P, g.order, placements, lab_w, lab_stride, K, err, fit, fit_limit, lab16 ? 1 : 0);
     else
         return hipErrorInvalidValue;
     return hipGetLastError();

@@ -171,6 +171,10 @@ struct PairCtx {
     using EL = Elem<true>;
     using VS = VecS<S>;
     using LS = LabS<S>;
+    // two 16-bit labels per node (the batch with label sums); a fast level's
+    // load keeps the word as it is (in v[0]) until the labels are used, so
+    // that nothing waits for the load early
+    static constexpr bool L16 = S == 2 && BM != kBinsNone;
     int lane, tid;
     int32_t V, L, P, K, p0;
     int32_t s0, s1, gen_end;   // steps of this chain; general path before gen_end
@@ -178,7 +182,7 @@ struct PairCtx {
     int fo;          // bits of successor link below a workspace value's label (b, folded)
     long long omax;
     VS *vals;
-    const LS *labs;
+    const void *labs;
     LS *nxs;
     bool want_nx;
     ConstPairLevel pls;
@@ -205,7 +209,9 @@ struct PairCtx {
         fo = !FWD && NXF ? ob : 0;
         omax = (1ll << ob) - 1;
         vals = reinterpret_cast<VS *>((FWD ? a->ftl : a->bll) + (int64_t)slice * a->ws_stride);
-        labs = reinterpret_cast<const LS *>(a->lab_w + (int64_t)slice * a->lab_stride);
+        labs = L16 ? (const void *)(reinterpret_cast<const uint16_t *>(a->lab_w) +
+                                    (int64_t)slice * a->lab_stride)
+                   : (const void *)(a->lab_w + (int64_t)slice * a->lab_stride);
         want_nx = !FWD && !NXF && a->nx_w != nullptr;
         nxs = reinterpret_cast<LS *>(a->nx_w + (want_nx ? (int64_t)slice * a->ws_stride : 0));
         pls = (ConstPairLevel)(FWD ? a->pl_t : a->pl_b);
@@ -215,6 +221,29 @@ struct PairCtx {
         slab = reinterpret_cast<LS *>(ring + kLongBase + 2 * kLongCap);   // [2][64]
         bins = reinterpret_cast<long long *>(slab + 2 * kPNodes);     // [K S]
     }
+    // node v's labels as loaded: the 32-bit labels, or (L16) the word of its
+    // two 16-bit labels in v[0]
+    __device__ __forceinline__ LS lab_raw(uint32_t v) const {
+        LS r;
+        if constexpr (L16) {
+            r.v[0] = (int32_t)at(reinterpret_cast<const uint32_t *>(labs), v);
+            r.v[1] = 0;
+        } else {
+            r = at(reinterpret_cast<const LS *>(labs), v);
+        }
+        return r;
+    }
+    __device__ __forceinline__ LS lab_use(const LS &x) const {
+        if constexpr (L16) {
+            LS r;
+            r.v[0] = (int32_t)((uint32_t)x.v[0] & 0xffffu);
+            r.v[1] = (int32_t)((uint32_t)x.v[0] >> 16);
+            return r;
+        } else {
+            return x;
+        }
+    }
+    __device__ __forceinline__ LS lab(uint32_t v) const { return lab_use(lab_raw(v)); }
     // the tl + comp or bl of a workspace (or ring) value
     __device__ __forceinline__ int64_t gval(int64_t g) const {
         if constexpr (!FWD && NXF)
@@ -343,7 +372,7 @@ __device__ __attribute__((noinline)) void pair_slow(KArgs *a, int32_t slice, int
             const int64_t cost = costs[e];
             const int32_t tie = FWD ? 0 : (int32_t)(c.omax - a->out_dst_orig[e]);
             const VS g = c.vals[nb];
-            const LS ol = c.labs[cn0 + own];
+            const LS ol = c.lab(cn0 + own);
 #pragma unroll
             for (int s = 0; s < S; s++)
                 lds_max_i64(&ab[own * S + s], c.akey(c.cand(g.v[s], ol.v[s], cost), tie));
@@ -357,7 +386,7 @@ __device__ __attribute__((noinline)) void pair_slow(KArgs *a, int32_t slice, int
             const int32_t v = cn0 + c.lane;
             const uint32_t vc = min((uint32_t)v, vmax);
             const NodeRec16 nr = at(a->node_rec, vc);
-            c.finish(a->label_mem, step, v, v < cn1, to_ring, c.lane, nr.comp, nr.mem, at(c.labs, vc));
+            c.finish(a->label_mem, step, v, v < cn1, to_ring, c.lane, nr.comp, nr.mem, c.lab(vc));
         }
         __syncthreads();
     }
@@ -372,7 +401,7 @@ __device__ __attribute__((noinline)) void pair_slow(KArgs *a, int32_t slice, int
             const int32_t own = (int32_t)(r.os & 0xffffu), span = (int32_t)(r.os >> 16);
             const int32_t tie = FWD ? 0 : a->pretie_b[e];
             const VS g = c.vals[r.nb];
-            const LS ol = c.labs[c.W(step + span).nlo + own];
+            const LS ol = c.lab(c.W(step + span).nlo + own);
             long long *ab = c.accb(step + span);
 #pragma unroll
             for (int s = 0; s < S; s++)
@@ -446,7 +475,7 @@ __device__ __forceinline__ void pair_chain(const SweepArgs &a, int32_t slice, ch
                 X.comp = at(a.comp_lm, v);
                 X.mem = 0;
             }
-            X.lab = at(c.labs, v);
+            X.lab = c.lab_raw(v);
             X.wnlo = b.nlo;
             X.wcnt = b.cnt;
         };
@@ -470,7 +499,7 @@ __device__ __forceinline__ void pair_chain(const SweepArgs &a, int32_t slice, ch
         auto body = [&](int32_t step, const WinEnt &b0, const WinEnt &b1, NearSet<S> &A,
                         const NearSet<S> &B1) {
             c.finish(a.label_mem, step, b0.nlo + lane, lane < cnt_w(b0.cnt), true, lane, A.comp, A.mem,
-                     A.lab, false);
+                     c.lab_use(A.lab), false);
             // span-1 edges of the next level, from the ring slot just written
             if (cnt_fast(b1.cnt)) {
                 const int32_t nt = cnt_near(b1.cnt);
@@ -491,7 +520,7 @@ __device__ __forceinline__ void pair_chain(const SweepArgs &a, int32_t slice, ch
             }
             // after the folds, so that the LDS (in order) serves the folds'
             // reads first
-            c.finish_side(a.label_mem, step, lane < cnt_w(b0.cnt), lane, A.mem, A.lab);
+            c.finish_side(a.label_mem, step, lane < cnt_w(b0.cnt), lane, A.mem, c.lab_use(A.lab));
         };
         const int32_t s0 = c.s0, s1 = c.s1;
         const int32_t a0 = pipe_start(c);
@@ -514,7 +543,7 @@ __device__ __forceinline__ void pair_chain(const SweepArgs &a, int32_t slice, ch
 #pragma unroll
             for (int j = 0; j < kLN; j++) loads(st[j], c.W(a0 + j));
             __builtin_amdgcn_s_waitcnt(0);
-            if (lane < cnt_w(c.W(a0 + 1).cnt)) c.slab[((a0 + 1) & 1) * kPNodes + lane] = st[1].lab;
+            if (lane < cnt_w(c.W(a0 + 1).cnt)) c.slab[((a0 + 1) & 1) * kPNodes + lane] = c.lab_use(st[1].lab);
             wn[0] = c.W(a0 + kLN);
         }
         __syncthreads();
@@ -533,7 +562,7 @@ __device__ __forceinline__ void pair_chain(const SweepArgs &a, int32_t slice, ch
                 // off the level's dependent LDS chain: the labels of level
                 // step + 2 (their slot was last read at the step before) and
                 // the window entry the next step's loads need
-                if (lane < cnt_w(b2.cnt)) c.slab[(sa & 1) * kPNodes + lane] = st[(r + 2) % kNS].lab;
+                if (lane < cnt_w(b2.cnt)) c.slab[(sa & 1) * kPNodes + lane] = c.lab_use(st[(r + 2) % kNS].lab);
                 const WinEnt bl = wn[r & 1];
                 {
                     // an index the compiler cannot see is zero: the entry
@@ -761,16 +790,18 @@ __global__ __launch_bounds__(2 * kLanes) void k_sweep_pair(SweepArgs a) {
     const int32_t n_slices = (a.P + S - 1) / S;
     const bool fwd = (int32_t)blockIdx.x >= n_slices;
     const int32_t slice = fwd ? blockIdx.x - n_slices : blockIdx.x;
+    // both directions take BM (only the t chain keeps label sums; BM also
+    // says which label layout the launch reads)
     if (wave_id() == 0) {
         if (fwd)
             pair_chain<S, true, true, BM, false>(a, slice, smem);
         else
-            pair_chain<S, false, true, kBinsNone, NXF>(a, slice, smem);
+            pair_chain<S, false, true, BM, NXF>(a, slice, smem);
     } else {
         if (fwd)
             pair_chain<S, true, false, BM, false>(a, slice, smem);
         else
-            pair_chain<S, false, false, kBinsNone, NXF>(a, slice, smem);
+            pair_chain<S, false, false, BM, NXF>(a, slice, smem);
     }
 }
 
@@ -1131,6 +1162,8 @@ hipError_t launch_pair(const SweepArgs &a, hipStream_t s) {
     if (a.lb <= 0) return hipErrorInvalidValue;
     const size_t bins = a.K > 0 && a.K * S <= kPBinsCap ? (size_t)a.K * S * 8 : 0;
     const size_t lds = pair_lds_fixed<S>() + bins;
+    // the batch with label sums reads 16-bit labels, and only it does
+    if ((S == kBatchSlots && a.K > 0) != (a.lab16 != 0)) return hipErrorInvalidValue;
     if (a.nxf) {   // links folded into the b values: batches only
         if constexpr (S == kBatchSlots) {
             if (a.K <= 0)

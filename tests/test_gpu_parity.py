@@ -667,17 +667,20 @@ def test_batch_any_int32_labels(P, seed):
     G.close()
 
 
-@pytest.mark.parametrize("K", [3000, 70000])
+@pytest.mark.parametrize("K", [3000, 65536, 70000])
 def test_batch_many_labels(P, K):
     """Label sums with many labels: 3,000 labels keep packed keys but sum by
-    global atomics (more than the LDS bins hold); 70,000 labels no longer pack
-    into 16 bits, so the batch keeps {value, label} pairs."""
+    global atomics (more than the LDS bins hold); 65,536 labels are the most
+    the 16-bit label layout holds (labels up to 65,535 must come back whole,
+    not as negative 16-bit values); 70,000 labels no longer pack into 16 bits,
+    so the batch keeps {value, label} pairs and 32-bit labels."""
     say(f"batch with K={K} labels")
     rng = np.random.default_rng(K)
     g = W.random_dag(rng, 900, p_edge=0.01, max_weight=9, n_labels=1)
     n_place = 5
     pl = rng.integers(0, K, (g.n_nodes, n_place)).astype(np.int32)
     pl[:, 1] = rng.integers(0, 3, g.n_nodes)      # a few labels in use, many idle
+    pl[:, 2] = K - 1 - rng.integers(0, 3, g.n_nodes)   # the top labels
     cap = rng.integers(0, 2000, K).astype(np.int64)
     G = P.Graph(g.n_nodes, g.src, g.dst, g.comp, g.edge_cost, g.mem)
     out = G.evaluate_batch(dev(pl, torch.int32), K, dev(cap, torch.int64))
@@ -694,6 +697,41 @@ def test_batch_many_labels(P, K):
         assert (out["path"][p, : out["path_len"][p]] == exp["path"]).all(), p
         assert (out["label_mem"][p] == exp["label_mem"]).all(), p
         assert (out["overflow"][p] == exp["overflow"]).all(), p
+
+
+def test_labels_checked_before_16_bit_storage(P):
+    """The batch with label sums stores labels as 16 bits; a label that is
+    out of range only in its upper bits (K + 3 with K = 2^16, which 16 bits
+    would read as 3) is still rejected, by the placements path and by the
+    moves path, and the handle stays usable."""
+    say("labels checked before 16-bit storage")
+    rng = np.random.default_rng(77)
+    g = W.random_dag(rng, 300, p_edge=0.02, max_weight=9, n_labels=1)
+    K = 1 << 16
+    G = P.Graph(g.n_nodes, g.src, g.dst, g.comp, g.edge_cost, g.mem)
+    pl = rng.integers(0, 4, (g.n_nodes, 4)).astype(np.int32)
+    bad = pl.copy()
+    bad[7, 2] = K + 3
+    with pytest.raises(P.PardnnError) as e:
+        G.evaluate_batch(dev(bad, torch.int32), K)
+    assert e.value.status == P.E_INVAL
+    base = pl[:, 0].copy()
+    ptr = np.array([0, 1, 2, 2], np.int64)
+    node = np.array([5, 9], np.int32)
+    with pytest.raises(P.PardnnError) as e:
+        G.evaluate_moves(dev(base, torch.int32), dev(ptr, torch.int64), dev(node, torch.int32),
+                         dev(np.array([1, K + 3], np.int32), torch.int32), K)
+    assert e.value.status == P.E_INVAL
+    # the same calls with the labels in range match the oracle
+    out = G.evaluate_batch(dev(pl, torch.int32), K)
+    torch.cuda.synchronize()
+    got = {k: v.cpu().numpy() for k, v in out.items()}
+    for p in range(4):
+        exp = oracle.evaluate(g.n_nodes, g.src, g.dst, g.comp, g.edge_cost, g.mem,
+                              pl[:, p].copy(), K, None)
+        assert (got["tl"][:, p] == exp["tl"]).all(), p
+        assert (got["label_mem"][p] == exp["label_mem"]).all(), p
+    G.close()
 
 
 def test_evaluate_moves_without_values(P):
