@@ -422,6 +422,13 @@ int evaluate_impl(Graph *g, int32_t n_place, const int32_t *placements, const Mo
     const int64_t lab_stride = ((int64_t)g->V * S + 63) / 64 * 64;
     const size_t per = (size_t)n_slices * (size_t)ws_stride;
     const size_t per_lab = (size_t)n_slices * (size_t)lab_stride;
+    // The pair sweep reads 16-bit labels (a node's two labels of a slice are
+    // one 4-byte word): half the bytes for the label build to write and for
+    // the sweep to read. They have a region of their own, lab_h, so that a
+    // call without label sums can keep 32-bit labels in lab_w for its
+    // unpacked alternative.
+    const int64_t lab_elems16 = ((int64_t)g->V * S + 127) / 128 * 128;
+    const size_t lab_h_bytes = ((size_t)n_slices * (size_t)lab_elems16 * 2 + 255) / 256 * 256;
     // successive placements from moves: the number of moves sizes the scratch
     // that groups them by node
     int64_t n_moves = 0;
@@ -439,11 +446,11 @@ int evaluate_impl(Graph *g, int32_t n_place, const int32_t *placements, const Mo
     // critical bit words for the path walk: [P][ceil(V / 32)]
     const size_t cbits_bytes =
         path != nullptr ? (((size_t)g->V + 31) / 32 * (size_t)n_place * 4 + 255) / 256 * 256 : 0;
-    // ftl, bll: room for 16-byte pairs; lab_w, nx_w: int32; start: [P]; then
-    // the critical bit words and the moves scratch
+    // ftl, bll: room for 16-byte pairs; lab_w, nx_w: int32; start: [P]; the
+    // 16-bit labels; then the critical bit words and the moves scratch
     const size_t need = per * (4 * sizeof(int64_t) + sizeof(int32_t)) +
                         per_lab * sizeof(int32_t) + (size_t)n_place * sizeof(int32_t) + 1024 +
-                        cbits_bytes + moves_bytes;
+                        lab_h_bytes + cbits_bytes + moves_bytes;
     void *ws_base = nullptr;
     if (fixed != nullptr) {
         if (need > fixed_bytes)
@@ -498,6 +505,11 @@ int evaluate_impl(Graph *g, int32_t n_place, const int32_t *placements, const Mo
     int32_t *lab_w = (int32_t *)(bll + 2 * per);
     int32_t *nx_w = lab_w + per_lab;
     int32_t *start = nx_w + per;
+    // after start[P], on a 256-byte boundary
+    const size_t lab_h_off = (per * (4 * sizeof(int64_t) + sizeof(int32_t)) +
+                              per_lab * sizeof(int32_t) + (size_t)n_place * sizeof(int32_t) + 255) /
+                             256 * 256;
+    int32_t *lab_h = reinterpret_cast<int32_t *>((char *)ws_base + lab_h_off);
     uint32_t *cbits = reinterpret_cast<uint32_t *>(
         (char *)ws_base + (need - moves_bytes - cbits_bytes) / 256 * 256);
     int32_t *moves_scratch = reinterpret_cast<int32_t *>(
@@ -505,22 +517,31 @@ int evaluate_impl(Graph *g, int32_t n_place, const int32_t *placements, const Mo
 
     const int32_t K = label_mem != nullptr ? n_labels : 0;
     int32_t *fit = gated ? g->bt_fit : nullptr;
-    // The pair sweep with label sums reads 16-bit labels (checked below K <=
-    // 2^16): half the bytes for the label build to write and for the sweep to
-    // read. The per-slice stride, in 16-bit elements, stays within the bytes
-    // of the 32-bit layout.
-    const bool lab16 = K > 0 && lb > 0 && g->V > 0;
-    const int64_t lab_elems = lab16 ? ((int64_t)g->V * S + 127) / 128 * 128 : lab_stride;
+    // The labels the pair sweep reads are 16-bit: checked at their full width
+    // (against K, or for a call without label sums against 2^lb, which sets
+    // the fit flag) as the workspace is built. A call without label sums then
+    // writes the 32-bit labels for its unpacked alternative only when some
+    // label does not fit: that pass reads the fit flag on the device and
+    // returns at once otherwise.
+    const bool lab16 = lb > 0 && g->V > 0;
+    int32_t *lab_sweep = lab16 ? lab_h : lab_w;
+    const int64_t lab_elems = lab16 ? lab_elems16 : lab_stride;
     HIP_TRY(clear_errors(g));
     if (fit != nullptr) HIP_TRY(launch_fill_i32(fit, 1, 1, g->stream));
     if (mv != nullptr) {
         HIP_TRY(launch_check_steps(mv->step_ptr, n_place, n_moves, g->err, g->stream));
         HIP_TRY(launch_moves_to_slices(*g, mv->base, n_place, mv->step_ptr, n_moves, mv->node,
-                                       mv->label, S, moves_scratch, lab_w, lab_elems, K,
+                                       mv->label, S, moves_scratch, lab_sweep, lab_elems, K,
                                        g->err, fit, 1u << lb, lab16));
+        if (gated)
+            HIP_TRY(launch_moves_write(*g, mv->base, n_place, n_moves, S, moves_scratch, lab_w,
+                                       lab_stride, fit, 0));
     } else {
-        HIP_TRY(launch_permute_labels_batch(*g, placements, n_place, S, lab_w, lab_elems, K,
+        HIP_TRY(launch_permute_labels_batch(*g, placements, n_place, S, lab_sweep, lab_elems, K,
                                             g->err, fit, 1u << lb, lab16));
+        if (gated)
+            HIP_TRY(launch_permute_labels_batch(*g, placements, n_place, S, lab_w, lab_stride, 0,
+                                                nullptr, nullptr, kPackLabels, false, fit, 0));
     }
     if (K > 0) {
         HIP_TRY(launch_fill_i64(label_mem, (int64_t)n_place * K, 0, g->stream));
@@ -528,7 +549,7 @@ int evaluate_impl(Graph *g, int32_t n_place, const int32_t *placements, const Mo
     SweepArgs a = sweep_args(g);
     a.P = n_place;
     a.K = K;
-    a.lab_w = lab_w;
+    a.lab_w = lab_sweep;
     a.lab_stride = lab_elems;
     a.lab16 = lab16 ? 1 : 0;
     a.ftl = ftl;
@@ -569,6 +590,9 @@ int evaluate_impl(Graph *g, int32_t n_place, const int32_t *placements, const Mo
     alt.lb = 0;
     alt.ob = 0;
     alt.nxf = 0;
+    alt.lab_w = lab_w;   // the 32-bit labels of the gated second pass
+    alt.lab_stride = lab_stride;
+    alt.lab16 = 0;
     alt.gate = fit;
     alt.gate_want = 0;
     if (gated) {

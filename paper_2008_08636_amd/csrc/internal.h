@@ -187,14 +187,16 @@ hipError_t launch_level_order(const Graph &g, int32_t bits, void *scratch);
 // ---- sweep.hip ----
 hipError_t launch_permute_labels(const Graph &g, const int32_t *placement, int32_t *lab_lm);
 // K > 0: labels outside [0, K) set bit 0 of err. fit (if given): set to 0
-// when a label lies outside [0, fit_limit). lab16 (S = 2, K <= 2^16): the
-// labels are stored as 16 bits (lab_stride in 16-bit elements); the checks
-// see the full values.
+// when a label lies outside [0, fit_limit). lab16 (S = 2): the labels are
+// stored as 16 bits (lab_stride in 16-bit elements); the checks see the full
+// values. gate (if given): the kernel returns at once unless *gate ==
+// gate_want (read on the device).
 hipError_t launch_permute_labels_batch(const Graph &g, const int32_t *placements, int32_t P,
                                        int32_t S, int32_t *lab_w, int64_t lab_stride,
                                        int32_t K = 0, int32_t *err = nullptr,
                                        int32_t *fit = nullptr, uint32_t fit_limit = kPackLabels,
-                                       bool lab16 = false);
+                                       bool lab16 = false, const int32_t *gate = nullptr,
+                                       int32_t gate_want = 0);
 // flag = 1 if every label lies in [0, limit), else 0 (on the device)
 hipError_t launch_label_fit(const Graph &g, const int32_t *labels, int32_t limit, int32_t *flag);
 hipError_t launch_sweep(const SweepArgs &a, int32_t S, hipStream_t s);
@@ -331,5 +333,11 @@ hipError_t launch_moves_to_slices(const Graph &g, const int32_t *base, int32_t P
                                   int32_t *lab_w, int64_t lab_stride, int32_t K, int32_t *err,
                                   int32_t *fit = nullptr, uint32_t fit_limit = kPackLabels,
                                   bool lab16 = false);
+// The 32-bit labels again from the moves launch_moves_to_slices grouped in
+// the same scratch (no checks), when *gate == gate_want on the device: the
+// unpacked alternative of a call without label sums.
+hipError_t launch_moves_write(const Graph &g, const int32_t *base, int32_t P, int64_t M,
+                              int32_t S, int32_t *scratch, int32_t *lab_w, int64_t lab_stride,
+                              const int32_t *gate, int32_t gate_want);
 
 }  // namespace pardnn

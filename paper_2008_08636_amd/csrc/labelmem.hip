@@ -251,7 +251,9 @@ __global__ __launch_bounds__(256) void k_moves_to_slices(int32_t V, int32_t P,
                                                          const int4 *mv_ent, int32_t *lab_w,
                                                          int64_t lab_stride, int32_t K,
                                                          int32_t *err, int32_t *fit,
-                                                         uint32_t fit_limit, int lab16) {
+                                                         uint32_t fit_limit, int lab16,
+                                                         const int32_t *gate, int32_t gate_want) {
+    if (gate != nullptr && *gate != gate_want) return;   // (uniform)
     constexpr int TV = 64, TP = 64, NW = 256 / kWave, RW = TV / NW;
     __shared__ int32_t tile[TV][TP + 1];
     const int lane = lane_id(), w = wave_id();
@@ -383,7 +385,9 @@ __global__ __launch_bounds__(256) void k_moves_lanes(int32_t V, int32_t P, const
                                                      const int32_t *base, const int32_t *mv_off,
                                                      const int4 *mv_ent, int32_t *lab_w,
                                                      int64_t lab_stride, int32_t K, int32_t *err,
-                                                     int32_t *fit, uint32_t fit_limit, int lab16) {
+                                                     int32_t *fit, uint32_t fit_limit, int lab16,
+                                                     const int32_t *gate, int32_t gate_want) {
+    if (gate != nullptr && *gate != gate_want) return;   // (uniform)
     __shared__ int2 mv[kLaneMoves];
     __shared__ int wsum[256 / kWave + 1];
     const int32_t v = blockIdx.x * 256 + threadIdx.x;
@@ -478,6 +482,71 @@ size_t moves_scratch_elems(int32_t V, int64_t M) {
            al64((mv_sort_temp_bytes(V, M) + 3) / 4);
 }
 
+namespace {
+
+// the grouped moves in the scratch (see moves_scratch_elems)
+struct MovesScratch {
+    int32_t *off;
+    uint32_t *key_in, *key_out;
+    int32_t *idx_in, *idx_out;
+    int4 *ent;
+    void *temp;
+};
+MovesScratch moves_scratch(int32_t V, int64_t M, int32_t *scratch) {
+    const size_t m64 = al64((size_t)M);
+    MovesScratch m;
+    m.off = scratch;
+    m.key_in = reinterpret_cast<uint32_t *>(m.off + al64((size_t)V + 1));
+    m.key_out = m.key_in + m64;
+    m.idx_in = reinterpret_cast<int32_t *>(m.key_out + m64);
+    m.idx_out = m.idx_in + m64;
+    m.ent = reinterpret_cast<int4 *>(m.idx_out + m64);
+    m.temp = reinterpret_cast<int32_t *>(m.ent) + 4 * m64;
+    return m;
+}
+
+// the labels of every slice from the grouped moves: one lane per node for
+// schedules with a few moves per node, else 64 x 64 tiles
+template <int S>
+void moves_writer(const Graph &g, bool lanes, const int32_t *base, int32_t P,
+                  const MovesScratch &m, int32_t *lab_w, int64_t lab_stride, int32_t K,
+                  int32_t *err, int32_t *fit, uint32_t fit_limit, int l16, const int32_t *gate,
+                  int32_t gate_want) {
+    const int32_t V = g.V;
+    if (lanes)
+        k_moves_lanes<S><<<(unsigned)((V + 255) / 256), 256, 0, g.stream>>>(
+            V, P, g.order, base, m.off, m.ent, lab_w, lab_stride, K, err, fit, fit_limit, l16,
+            gate, gate_want);
+    else
+        k_moves_to_slices<S><<<(unsigned)((V + 63) / 64), 256, 0, g.stream>>>(
+            V, P, g.order, base, m.off, m.ent, lab_w, lab_stride, K, err, fit, fit_limit, l16,
+            gate, gate_want);
+}
+
+hipError_t launch_moves_writer(const Graph &g, const int32_t *base, int32_t P, int64_t M,
+                               int32_t S, const MovesScratch &m, int32_t *lab_w,
+                               int64_t lab_stride, int32_t K, int32_t *err, int32_t *fit,
+                               uint32_t fit_limit, bool lab16, const int32_t *gate,
+                               int32_t gate_want) {
+    if (lab16 && (S != 2 || lab_stride % 2 != 0)) return hipErrorInvalidValue;
+    const bool lanes = M <= (int64_t)kLaneMovesPerNode * g.V;
+    const int l16 = lab16 ? 1 : 0;
+    if (S == 1)
+        moves_writer<1>(g, lanes, base, P, m, lab_w, lab_stride, K, err, fit, fit_limit, l16,
+                        gate, gate_want);
+    else if (S == 2)
+        moves_writer<2>(g, lanes, base, P, m, lab_w, lab_stride, K, err, fit, fit_limit, l16,
+                        gate, gate_want);
+    else if (S == 4)
+        moves_writer<4>(g, lanes, base, P, m, lab_w, lab_stride, K, err, fit, fit_limit, l16,
+                        gate, gate_want);
+    else
+        return hipErrorInvalidValue;
+    return hipGetLastError();
+}
+
+}  // namespace
+
 hipError_t launch_moves_to_slices(const Graph &g, const int32_t *base, int32_t P,
                                   const int64_t *step_ptr, int64_t M, const int32_t *node,
                                   const int32_t *label, int32_t S, int32_t *scratch,
@@ -485,62 +554,39 @@ hipError_t launch_moves_to_slices(const Graph &g, const int32_t *base, int32_t P
                                   int32_t *fit, uint32_t fit_limit, bool lab16) {
     if (g.V == 0 || P == 0) return hipSuccess;
     if (lab16 && (S != 2 || lab_stride % 2 != 0)) return hipErrorInvalidValue;
-    const int l16 = lab16 ? 1 : 0;
     const int32_t V = g.V;
-    const size_t m64 = al64((size_t)M);
-    int32_t *off = scratch;
-    uint32_t *key_in = reinterpret_cast<uint32_t *>(off + al64((size_t)V + 1));
-    uint32_t *key_out = key_in + m64;
-    int32_t *idx_in = reinterpret_cast<int32_t *>(key_out + m64);
-    int32_t *idx_out = idx_in + m64;
-    int4 *ent = reinterpret_cast<int4 *>(idx_out + m64);
-    void *temp = reinterpret_cast<int32_t *>(ent) + 4 * m64;
+    const MovesScratch m = moves_scratch(V, M, scratch);
     hipError_t e = hipSuccess;
     if (M > 0) {
-        k_mv_keys<<<grid_for(M, kBlock), kBlock, 0, g.stream>>>(M, node, V, key_in, idx_in, err);
+        k_mv_keys<<<grid_for(M, kBlock), kBlock, 0, g.stream>>>(M, node, V, m.key_in, m.idx_in,
+                                                                 err);
         e = hipGetLastError();
         if (e == hipSuccess)
-            e = sort_pairs_u32(key_in, key_out, idx_in, idx_out, (int32_t)M, 0,
-                               (int)mv_key_bits(V), temp, g.stream);
+            e = sort_pairs_u32(m.key_in, m.key_out, m.idx_in, m.idx_out, (int32_t)M, 0,
+                               (int)mv_key_bits(V), m.temp, g.stream);
     }
     if (e == hipSuccess) {
-        k_mv_off<<<grid_for((int64_t)V + 1, kBlock), kBlock, 0, g.stream>>>(V, M, key_out, off);
+        k_mv_off<<<grid_for((int64_t)V + 1, kBlock), kBlock, 0, g.stream>>>(V, M, m.key_out,
+                                                                            m.off);
         e = hipGetLastError();
     }
     if (e == hipSuccess && M > 0) {
-        k_mv_gather<<<grid_for(M, kBlock), kBlock, 0, g.stream>>>(M, P, step_ptr, key_out,
-                                                                   idx_out, label, V, ent);
+        k_mv_gather<<<grid_for(M, kBlock), kBlock, 0, g.stream>>>(M, P, step_ptr, m.key_out,
+                                                                   m.idx_out, label, V, m.ent);
         e = hipGetLastError();
     }
     if (e != hipSuccess) return e;
-    if (M <= (int64_t)kLaneMovesPerNode * V) {
-        const unsigned grid = (unsigned)((V + 255) / 256);
-        if (S == 1)
-            k_moves_lanes<1><<<grid, 256, 0, g.stream>>>(V, P, g.order, base, off, ent, lab_w,
-                                                         lab_stride, K, err, fit, fit_limit, l16);
-        else if (S == 2)
-            k_moves_lanes<2><<<grid, 256, 0, g.stream>>>(V, P, g.order, base, off, ent, lab_w,
-                                                         lab_stride, K, err, fit, fit_limit, l16);
-        else if (S == 4)
-            k_moves_lanes<4><<<grid, 256, 0, g.stream>>>(V, P, g.order, base, off, ent, lab_w,
-                                                         lab_stride, K, err, fit, fit_limit, l16);
-        else
-            return hipErrorInvalidValue;
-        return hipGetLastError();
-    }
-    const unsigned grid = (unsigned)((V + 63) / 64);
-    if (S == 1)
-        k_moves_to_slices<1><<<grid, 256, 0, g.stream>>>(V, P, g.order, base, off, ent, lab_w,
-                                                         lab_stride, K, err, fit, fit_limit, l16);
-    else if (S == 2)
-        k_moves_to_slices<2><<<grid, 256, 0, g.stream>>>(V, P, g.order, base, off, ent, lab_w,
-                                                         lab_stride, K, err, fit, fit_limit, l16);
-    else if (S == 4)
-        k_moves_to_slices<4><<<grid, 256, 0, g.stream>>>(V, P, g.order, base, off, ent, lab_w,
-                                                         lab_stride, K, err, fit, fit_limit, l16);
-    else
-        return hipErrorInvalidValue;
-    return hipGetLastError();
+    return launch_moves_writer(g, base, P, M, S, m, lab_w, lab_stride, K, err, fit, fit_limit,
+                               lab16, nullptr, 0);
+}
+
+hipError_t launch_moves_write(const Graph &g, const int32_t *base, int32_t P, int64_t M,
+                              int32_t S, int32_t *scratch, int32_t *lab_w, int64_t lab_stride,
+                              const int32_t *gate, int32_t gate_want) {
+    if (g.V == 0 || P == 0) return hipSuccess;
+    return launch_moves_writer(g, base, P, M, S, moves_scratch(g.V, M, scratch), lab_w,
+                               lab_stride, 0, nullptr, nullptr, kPackLabels, false, gate,
+                               gate_want);
 }
 
 hipError_t launch_label_memory(const Graph &g, const int32_t *placement, int32_t K,

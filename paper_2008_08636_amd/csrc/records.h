@@ -163,8 +163,8 @@ struct SweepArgs {
     int32_t nxf;
     // 1: lab_w holds 16-bit labels (unsigned; lab_stride counts 16-bit
     // elements), so a node's two labels of a slice are one 32-bit word. The
-    // batched pair sweep with label sums takes them (labels checked below K
-    // <= 2^16); every other sweep reads 32-bit labels.
+    // batched pair sweep takes them (labels checked below 2^lb <= 2^16 as
+    // they were written); every other sweep reads 32-bit labels.
     int32_t lab16;
 };
 

@@ -52,7 +52,9 @@ __global__ __launch_bounds__(256) void k_permute_labels(int32_t V, int32_t P,
                                                         const int32_t *placements,
                                                         int32_t *lab_w, int64_t lab_stride,
                                                         int32_t K, int32_t *err, int32_t *fit,
-                                                        uint32_t fit_limit, int lab16) {
+                                                        uint32_t fit_limit, int lab16,
+                                                        const int32_t *gate, int32_t gate_want) {
+    if (gate != nullptr && *gate != gate_want) return;   // (uniform)
     constexpr int TV = 64, TP = 64;  // tile: 64 nodes x 64 placements
     __shared__ int32_t tile[TV][TP + 1];
     const int32_t n_slices = (P + S - 1) / S;
@@ -942,16 +944,18 @@ hipError_t launch_permute_labels(const Graph &g, const int32_t *placement, int32
 hipError_t launch_permute_labels_batch(const Graph &g, const int32_t *placements, int32_t P,
                                        int32_t S, int32_t *lab_w, int64_t lab_stride, int32_t K,
                                        int32_t *err, int32_t *fit, uint32_t fit_limit,
-                                       bool lab16) {
+                                       bool lab16, const int32_t *gate, int32_t gate_want) {
     if (lab16 && S != kBatchSlots) return hipErrorInvalidValue;
     if (g.V == 0 || P == 0) return hipSuccess;
     dim3 grid((g.V + 63) / 64, (P + 63) / 64);
     if (S == 1)
         k_permute_labels<1><<<grid, 256, 0, g.stream>>>(g.V, P, g.order, placements, lab_w,
-                                                        lab_stride, K, err, fit, fit_limit, 0);
+                                                        lab_stride, K, err, fit, fit_limit, 0,
+                                                        gate, gate_want);
     else if (S == kBatchSlots)
         k_permute_labels<kBatchSlots><<<grid, 256, 0, g.stream>>>(
-            g.V, P, g.order, placements, lab_w, lab_stride, K, err, fit, fit_limit, lab16 ? 1 : 0);
+            g.V, P, g.order, placements, lab_w, lab_stride, K, err, fit, fit_limit, lab16 ? 1 : 0,
+            gate, gate_want);
     else
         return hipErrorInvalidValue;
     return hipGetLastError();

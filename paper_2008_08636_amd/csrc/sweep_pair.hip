@@ -171,10 +171,10 @@ struct PairCtx {
     using EL = Elem<true>;
     using VS = VecS<S>;
     using LS = LabS<S>;
-    // two 16-bit labels per node (the batch with label sums); a fast level's
-    // load keeps the word as it is (in v[0]) until the labels are used, so
-    // that nothing waits for the load early
-    static constexpr bool L16 = S == 2 && BM != kBinsNone;
+    // two 16-bit labels per node (every batch: S = 2); a fast level's load
+    // keeps the word as it is (in v[0]) until the labels are used, so that
+    // nothing waits for the load early
+    static constexpr bool L16 = S == 2;
     int lane, tid;
     int32_t V, L, P, K, p0;
     int32_t s0, s1, gen_end;   // steps of this chain; general path before gen_end
@@ -790,8 +790,7 @@ __global__ __launch_bounds__(2 * kLanes) void k_sweep_pair(SweepArgs a) {
     const int32_t n_slices = (a.P + S - 1) / S;
     const bool fwd = (int32_t)blockIdx.x >= n_slices;
     const int32_t slice = fwd ? blockIdx.x - n_slices : blockIdx.x;
-    // both directions take BM (only the t chain keeps label sums; BM also
-    // says which label layout the launch reads)
+    // both directions take BM (only the t chain keeps label sums)
     if (wave_id() == 0) {
         if (fwd)
             pair_chain<S, true, true, BM, false>(a, slice, smem);
@@ -1162,8 +1161,8 @@ hipError_t launch_pair(const SweepArgs &a, hipStream_t s) {
     if (a.lb <= 0) return hipErrorInvalidValue;
     const size_t bins = a.K > 0 && a.K * S <= kPBinsCap ? (size_t)a.K * S * 8 : 0;
     const size_t lds = pair_lds_fixed<S>() + bins;
-    // the batch with label sums reads 16-bit labels, and only it does
-    if ((S == kBatchSlots && a.K > 0) != (a.lab16 != 0)) return hipErrorInvalidValue;
+    // the batch reads 16-bit labels, and only it does
+    if ((S == kBatchSlots) != (a.lab16 != 0)) return hipErrorInvalidValue;
     if (a.nxf) {   // links folded into the b values: batches only
         if constexpr (S == kBatchSlots) {
             if (a.K <= 0)
