@@ -255,8 +255,8 @@ int pardnn_evaluate_batch(pardnn_graph *g, int32_t n_place,
  * hipMalloc): the same arguments and results, but its workspace is a fixed
  * array of 128 MiB compiled into the library (one per GPU, held until the
  * process ends) and the call allocates nothing.
- *   Limit: the batch must fit that workspace, about 40 bytes per node and
- *   placement (n_nodes * n_place <= ~3.3M, e.g. 10 placements of a
+ *   Limit: the batch must fit that workspace, about 42 bytes per node and
+ *   placement (n_nodes * n_place <= ~3.2M, e.g. 10 placements of a
  *   300k-node graph); larger batches return E_INVAL with the bytes needed.
  *   The graph must already be levelized (pardnn_levelize); otherwise E_INVAL.
  *   All calls on one GPU share the array: calls that overlap in time on one
