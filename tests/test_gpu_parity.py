@@ -802,19 +802,21 @@ def test_evaluate_moves_small(P):
     G.close()
 
 
-@pytest.mark.parametrize("n_moves,n_place", [(3584, 64), (3585, 63), (6400, 64)])
-def test_evaluate_moves_label_build_forms(P, n_moves, n_place):
+@pytest.mark.parametrize("n_moves,n_place,width", [(3584, 64, 256), (3585, 63, 256),
+                                                   (6400, 64, 256), (6400, 63, 255)])
+def test_evaluate_moves_label_build_forms(P, n_moves, n_place, width):
     """The labels built from the moves take one of three forms: one lane per
     node with the moves of a 256-node workgroup staged in LDS (up to 3,584
     entries), the same walk reading the moves from global memory (a workgroup
     with more), and one wave per 64-node tile (more than 11 moves per node on
     average). Two levels of 256 nodes, every move on a source, so the first
     workgroup holds all of them: 3,584 moves fit, 3,585 do not, and 6,400 on
-    512 nodes exceed the average. Each equals build + evaluate_batch and the
-    oracle."""
-    say(f"evaluate_moves label build forms: {n_moves} moves, {n_place} placements")
+    512 nodes exceed the average (with 511 nodes, the tile form's last node
+    has no neighbour to share its store with). Each equals build +
+    evaluate_batch and the oracle."""
+    say(f"evaluate_moves label build forms: {n_moves} moves, {n_place} placements, {width}")
     rng = np.random.default_rng(4242 + n_moves)
-    g = W.layered_dag(rng, [256, 256], [0, 3], n_labels=4)
+    g = W.layered_dag(rng, [256, width], [0, 3], n_labels=4)
     sources = np.setdiff1d(np.arange(g.n_nodes), g.dst).astype(np.int32)
     assert sources.shape[0] == 256
     cuts = np.sort(rng.integers(0, n_moves + 1, n_place - 1))
